@@ -1,0 +1,283 @@
+#!/usr/bin/env python3
+"""TT-embedding training-step benchmark on one MI355X.
+
+One step is the whole hot path over one batch: prefix-based index grouping,
+fused forward (C = A.B per prefix group, E = C.D per unique row), sum pooling,
+backward (dE segment sums, per-group dD/dC/dA/dB, core-gradient reduction)
+and the in-place SGD update.  Default workload: 8 TT tables of 1e7 rows
+(200 x 200 x 250), D = 128 = 4 x 4 x 8, rank 32, 32,768 bags per table with
+Poisson(20) lengths clipped to [1, 64], Zipf(1.1) row popularity over a seeded
+permutation, upstream gradient N(0, 1), lr 0.01.  Inputs are synthetic and
+already resident in HBM when the timed region starts.
+
+Prints one JSON line (see the keys at the end of main()).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA = 157.3e12  # MI355X dense FP32 matrix FLOP/s
+PEAK_HBM = 8.0e12          # MI355X HBM3E bytes/s
+METRIC = "TT-embedding lookups/s + batch-32768 fwd/bwd latency (ms), % of roofline"
+
+
+class HipEvents:
+    """hipEvent_t handles through the HIP runtime (timed on the library's stream)."""
+
+    def __init__(self):
+        self.hip = C.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.hip.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+
+    def create(self):
+        e = C.c_void_p()
+        assert self.hip.hipEventCreate(C.byref(e)) == 0
+        return e.value
+
+    def record(self, e, stream):
+        assert self.hip.hipEventRecord(e, stream) == 0
+
+    def elapsed_ms(self, a, b):
+        assert self.hip.hipEventSynchronize(b) == 0
+        ms = C.c_float()
+        assert self.hip.hipEventElapsedTime(C.byref(ms), a, b) == 0
+        return float(ms.value)
+
+    def destroy(self, e):
+        self.hip.hipEventDestroy(e)
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2609_03459_amd", "csrc")
+    for name in sorted(os.listdir(d)):
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_work(kernel, case, counts):
+    """(amount, unit, bound) per launch of `kernel` from the workload and its grouping."""
+    T, B, R = case["T"], case["B"], case["R"]
+    d1, d2, d3 = case["d"]
+    D = d1 * d2 * d3
+    U, P, nv = counts["U"], counts["P"], counts["nvalid"]
+    M = int(case["idx"].size)
+    NB = T * B
+    if kernel == "fwd_fused":
+        return P * 2.0 * d1 * d2 * R * R + U * 2.0 * D * R, "flop", "mfma"
+    if kernel == "bwd_fused":
+        return P * 6.0 * d1 * d2 * R * R + U * 4.0 * D * R, "flop", "mfma"
+    if kernel == "pool":
+        return 4.0 * M + 8.0 * (NB + 1) + 4.0 * NB * D + 4.0 * U * D, "byte", "hbm"
+    if kernel == "seg_sum":
+        return 4.0 * NB * D + 4.0 * U * D + 12.0 * nv + 4.0 * (U + 1), "byte", "hbm"
+    if kernel == "ingest":
+        return 8.0 * M + 8.0 * (NB + 1) + 12.0 * M, "byte", "hbm"
+    raise ValueError(kernel)
+
+
+def cpu_baseline(case, target_s):
+    """The oracle (plain fp64 C, one thread) on a bounded sample of the same workload:
+    a seeded subset of bags of every table, forward then backward."""
+    import numpy as np
+
+    import oracle
+
+    oracle.build(force=False)
+    T, B = case["T"], case["B"]
+    off = case["offsets"]
+
+    def sub(nb):
+        rng = np.random.default_rng(99)
+        bags = np.sort(rng.choice(B, size=nb, replace=False))
+        idx_parts, lens, dv = [], [], []
+        for t in range(T):
+            for b in bags:
+                gb = t * B + b
+                lo, hi = (off[gb], off[gb + 1]) if off is not None else (gb, gb + 1)
+                idx_parts.append(case["idx"][lo:hi])
+                lens.append(hi - lo)
+            dv.append(case["dV"][t, bags])
+        o = np.zeros(T * nb + 1, np.int64)
+        o[1:] = np.cumsum(lens)
+        return dict(case, B=nb, idx=np.concatenate(idx_parts), offsets=o, dV=np.stack(dv))
+
+    def run(c):
+        t0 = time.perf_counter()
+        oracle.forward(c)
+        oracle.backward(c)
+        return time.perf_counter() - t0
+
+    probe = sub(8)
+    dt = run(probe)
+    rate = probe["idx"].size / max(dt, 1e-6)
+    nb = int(min(B, max(8, target_s * rate / max(probe["idx"].size / 8.0, 1.0))))
+    s = sub(nb)
+    dt = run(s)
+    lookups = int(s["idx"].size)
+    return dict(value=lookups / dt, unit="lookups/s", cores=1, kind="oracle",
+                sample=f"{nb} seeded bags per table x {T} tables ({lookups} lookups), forward + backward, "
+                       f"fp64 C oracle, 1 thread, {dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=6)
+    ap.add_argument("--config", type=int, default=5, help="workload recipe (5 = training step)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run one torch copy of this many MiB (counter calibration runs)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_03459_amd as P
+    import ttgen
+
+    case = ttgen.make(args.config, with_grad=True)
+    T, n, d, R, B = case["T"], case["n"], case["d"], case["R"], case["B"]
+    D = d[0] * d[1] * d[2]
+    M = int(case["idx"].size)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B)
+    G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
+    idx = torch.from_numpy(case["idx"]).to(dev)
+    off = None if case["offsets"] is None else torch.from_numpy(case["offsets"]).to(dev)
+    dV = torch.from_numpy(case["dV"]).to(dev)
+    out = torch.empty((T, B, D), dtype=torch.float32, device=dev)
+    grads = tuple(torch.empty(s, dtype=torch.float32, device=dev) for s in emb.core_shapes())
+    lr = case["lr"]
+    stream = torch.cuda.current_stream().cuda_stream
+    ev = HipEvents()
+
+    def step():
+        emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=False)
+        emb.backward(*G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
+        emb.sgd(*G, *grads, lr)
+
+    if args.copy_mib:
+        x = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+
+    # warmup; the first steps also time each candidate kernel once
+    kernels = list(P.N.KERNELS)
+    kernel_ms = {}
+    e0, e1 = ev.create(), ev.create()
+    for w in range(max(args.warmup, len(kernels))):
+        k = kernels[w] if w < len(kernels) else None
+        if k:
+            P.N.tt_emb_profile(emb.handle, P.N.KERNELS[k], e0, e1)
+        step()
+        if k:
+            torch.cuda.synchronize()
+            kernel_ms[k] = ev.elapsed_ms(e0, e1)
+            P.N.tt_emb_profile(emb.handle, 0, None, None)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    counts = emb.counts()
+    dominant = max(kernel_ms, key=kernel_ms.get)
+
+    # timed region: K steps; the dominant kernel is bracketed by events in every step
+    K = args.steps
+    evs = [(ev.create(), ev.create()) for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        P.N.tt_emb_profile(emb.handle, P.N.KERNELS[dominant], evs[i][0], evs[i][1])
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    P.N.tt_emb_profile(emb.handle, 0, None, None)
+    ms_per_step = (t1 - t0) * 1e3 / K
+    dom_ms = float(np.mean([ev.elapsed_ms(a, b) for a, b in evs]))
+
+    # phase split (grouping / forward / backward / sgd), as in the paper's breakdown
+    phases = {"group": [], "forward": [], "backward": [], "sgd": []}
+    pe = [ev.create() for _ in range(5)]
+    for _ in range(3):
+        ev.record(pe[0], stream)
+        emb.group(idx, off, num_bags=B)
+        ev.record(pe[1], stream)
+        emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=True)
+        ev.record(pe[2], stream)
+        emb.backward(*G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
+        ev.record(pe[3], stream)
+        emb.sgd(*G, *grads, lr)
+        ev.record(pe[4], stream)
+        torch.cuda.synchronize()
+        for j, name in enumerate(phases):
+            phases[name].append(ev.elapsed_ms(pe[j], pe[j + 1]))
+    phases_ms = {k: round(float(np.median(v)), 4) for k, v in phases.items()}
+
+    work, unit, bound = algorithmic_work(dominant, case, counts)
+    if unit == "flop":
+        achieved = work / (dom_ms * 1e-3) / 1e12
+        roof = dict(bound=bound, achieved=round(achieved, 3), peak=PEAK_FP32_MFMA / 1e12, unit="TFLOP/s",
+                    frac=round(achieved / (PEAK_FP32_MFMA / 1e12), 4))
+    else:
+        achieved = work / (dom_ms * 1e-3) / 1e9
+        roof = dict(bound=bound, achieved=round(achieved, 1), peak=PEAK_HBM / 1e9, unit="GB/s",
+                    frac=round(achieved / (PEAK_HBM / 1e9), 4))
+    roof["traffic"] = None
+    tpath = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tpath):
+        tr = json.load(open(tpath))
+        if tr.get("kernel") == dominant and tr.get("source") == source_digest():
+            roof["traffic"] = tr.get("bytes_per_launch")
+    roof["kernel"] = dominant
+    roof["kernel_ms"] = round(dom_ms, 4)
+
+    lookups = M
+    res = {
+        "metric": METRIC,
+        "value": lookups / (ms_per_step * 1e-3),
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "row_factors": list(n),
+                   "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
+                   "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu"},
+        "roofline": roof,
+        "phases_ms": phases_ms,
+        "kernel_ms_warmup": {k: round(v, 4) for k, v in kernel_ms.items()},
+        "grouping": {"unique_rows": counts["U"], "prefix_groups": counts["P"], "slices": counts["nslices"]},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * tt_emb.h - C ABI of the MI355X (gfx950) Tensor-Train embedding gather.
+ *
+ * The operator follows FlowTT (ICCAD'26).  A table of N rows and D = d1*d2*d3
+ * columns is stored as three TT cores (rank profile 1, R, R, 1).  Row g is
+ * split by the mixed-radix conversion of Eq. 2 (Section 3.3) into digits
+ * (i1, i2, i3), with the first factor the most significant digit, and
+ * rebuilt by the chained contraction of Section 3.2 (Fig. 3):
+ *     C = A . B    with A = G1[i1] (d1 x R) and B = G2[i2] (R x d2 R),
+ *     E = C . D    with C viewed as (d1 d2) x R and D = G3[i3] (R x d3),
+ * and rows are sum-pooled per bag into V.  The backward pass (Section 3.2,
+ * Eq. 1) produces dense gradients of all three cores.  Indices are grouped by
+ * their (i1, i2) prefix as in Section 3.3 (sort, exact unique, mixed-radix
+ * digits, run-length encoding of prefixes) so that C is built once per
+ * prefix group and reused for every row of the group.
+ *
+ * Layouts (float32, row-major, all tables of one call contiguous):
+ *     G1 [T][n1][d1][R]
+ *     G2 [T][n2][R][d2][R]
+ *     G3 [T][n3][R][d3]
+ *     out, grad_out [T][B][D], element (t, b, j1*d2*d3 + j2*d3 + j3)
+ *     indices int64 [num_indices]: the row ids of all tables, table-major
+ *     offsets int64 [T*B + 1]: bag t*B+b of table t covers
+ *         indices[offsets[t*B+b] .. offsets[t*B+b+1]); offsets[0] = 0 and
+ *         offsets[T*B] = num_indices.  NULL offsets means one index per bag
+ *         (num_indices = T*B).
+ *
+ * Ownership.  The caller owns every device buffer (cores, indices, offsets,
+ * outputs, gradients, workspace).  The handle holds host-side metadata only;
+ * creating it touches no device.  tt_emb_group, tt_emb_forward,
+ * tt_emb_backward and tt_emb_sgd enqueue kernels on `stream` (a hipStream_t;
+ * NULL = the default stream) and return without synchronising; they allocate
+ * and free nothing.  One handle and one workspace serve one stream at a time.
+ * Device pointers to float data must be 16-byte aligned, to int64 data
+ * 8-byte aligned, and the workspace 256-byte aligned.
+ *
+ * Errors.  Host-checkable faults (NULL pointers, bad sizes or factors,
+ * workspace too small, misalignment) return a status and launch nothing.  A
+ * failing HIP call returns TT_EMB_EHIP.  Faults only the device can see (an
+ * index outside [0, N), offsets that are not monotone within
+ * [0, num_indices]) set a sticky error word in the workspace; the offending
+ * occurrence contributes nothing, and tt_emb_check_errors reports
+ * TT_EMB_ERANGE.  The word is cleared when a grouping starts (tt_emb_group,
+ * or forward/backward with reuse_grouping = 0) and stays set through calls
+ * that reuse that grouping.  No C++ exception crosses this interface.
+ */
+#ifndef TT_EMB_H
+#define TT_EMB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tt_emb_s* tt_emb_handle;
+
+typedef enum {
+  TT_EMB_OK = 0,
+  TT_EMB_EINVAL = 1,      /* bad argument: NULL pointer, size, factor, alignment, small workspace */
+  TT_EMB_ENOMEM = 2,      /* host allocation of the handle failed */
+  TT_EMB_EHIP = 3,        /* a HIP runtime call or kernel launch failed */
+  TT_EMB_ERANGE = 4,      /* device saw an index outside [0, N) or malformed offsets */
+  TT_EMB_EUNSUPPORTED = 5 /* shape beyond this library's limits (see tt_emb_create) */
+} tt_emb_status;
+
+/* Shape of the tables served by one handle.  Every table of a call has the
+ * same TT shape (tables are batched into one launch, one table per key
+ * range; Section 4.1 evaluates many equally-shaped tables). */
+typedef struct {
+  int32_t num_tables;      /* T >= 1 */
+  int64_t num_rows;        /* N, 1 <= N <= n1*n2*n3 */
+  int32_t row_factors[3];  /* (n1, n2, n3) >= 1; n1 is the most significant digit (Eq. 2) */
+  int32_t dim_factors[3];  /* (d1, d2, d3) >= 1; j1 is the most significant output digit */
+  int32_t rank;            /* R = r1 = r2 >= 1 (r0 = r3 = 1) */
+  int64_t max_indices;     /* largest num_indices of any call (all tables together) */
+  int64_t max_bags;        /* largest num_bags (bags per table) of any call */
+} tt_emb_desc;
+
+/* Validate `desc` and create a handle (host memory only).
+ * Limits: T * n1*n2*n3 < 2^32 - 1; T * n1 * n2 < 2^28; max_indices < 2^31;
+ * T * max_bags < 2^31; R <= 64; d1*d2*R <= 8192; D <= 4096.
+ * Returns TT_EMB_EINVAL for non-positive sizes or N > n1*n2*n3,
+ * TT_EMB_EUNSUPPORTED beyond the limits, TT_EMB_ENOMEM on allocation failure. */
+tt_emb_status tt_emb_create(const tt_emb_desc* desc, tt_emb_handle* out);
+
+/* Release a handle.  NULL is accepted. */
+tt_emb_status tt_emb_destroy(tt_emb_handle h);
+
+/* Bytes of device workspace needed for calls up to desc.max_indices and
+ * desc.max_bags.  The same workspace carries the index grouping from a
+ * forward call to the following backward call. */
+tt_emb_status tt_emb_workspace_size(tt_emb_handle h, size_t* bytes);
+
+/* Prefix-based index grouping alone (Section 3.3, Fig. 4): sort the indices
+ * of each table, keep exact uniques, take their mixed-radix digits and
+ * run-length encode the (i1, i2) prefixes into prefix groups, then order the
+ * groups for the fused kernels.  The result stays in `workspace`.  Offsets
+ * as described above (NULL = one index per bag). */
+tt_emb_status tt_emb_group(tt_emb_handle h, const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                           int64_t num_bags, void* workspace, size_t ws_bytes, void* stream);
+
+/* Forward pass (Section 3.2): out[t][b] = sum over the occurrences o of bag
+ * t*B+b of E_{indices[o]}, computed as C = A.B once per prefix group (kept
+ * on chip) and E = C.D once per unique row, then sum pooling (an empty bag
+ * gives zeros).  `out` is overwritten.  reuse_grouping = 1 skips the
+ * grouping step and uses the one already in `workspace` (which must come
+ * from a call with the same indices, offsets and sizes on this handle);
+ * reuse_grouping = 0 groups first. */
+tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                             const int64_t* indices, int64_t num_indices, const int64_t* offsets, int64_t num_bags,
+                             float* out, int reuse_grouping, void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward pass (Section 3.2, Eq. 1) of L = sum <grad_out, out> into dense
+ * core gradients dG1, dG2, dG3 (same shapes as the cores, OVERWRITTEN; rows
+ * no index touches are zero).  Per unique row, dE is the sum of grad_out
+ * over its occurrences; per row dD = C^T dE and dC = dE D^T; per prefix
+ * group the dC are summed first and dA = (sum dC) B^T, dB = A^T (sum dC).
+ * Per-core gradients are reduced by segments, not by per-row global atomics.
+ * reuse_grouping as for tt_emb_forward. */
+tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                              const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                              int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
+                              int reuse_grouping, void* workspace, size_t ws_bytes, void* stream);
+
+/* Plain SGD step in place on all three cores: G_k -= lr * dG_k (no
+ * momentum, no weight decay).  Enqueued on `stream` after the gradients. */
+tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
+                         const float* dG3, float lr, void* stream);
+
+/* Synchronise `stream`, read and clear the sticky device error word of
+ * `workspace`.  Returns TT_EMB_OK, TT_EMB_ERANGE or TT_EMB_EHIP. */
+tt_emb_status tt_emb_check_errors(tt_emb_handle h, void* workspace, void* stream);
+
+/* Copy the grouping held in `workspace` to host arrays (synchronises
+ * `stream`; for tests).  Any output pointer may be NULL.  Sizes: uniq_keys,
+ * uniq_digits: U and 3*U; inv: num_indices of the grouped call (-1 for an
+ * invalid index); occ_start: U+1; occ_pos: nvalid; pg_start: P+1; pg_keys: P.
+ * A unique key is t*(n1*n2*n3) + row; a prefix-group key is t*(n1*n2) +
+ * i1*n2 + i2.  counts receives (U, P, nvalid, number of work slices). */
+tt_emb_status tt_emb_debug_grouping(tt_emb_handle h, void* workspace, int64_t* uniq_keys, int32_t* uniq_digits,
+                                    int32_t* inv, int32_t* occ_start, int32_t* occ_pos, int32_t* pg_start,
+                                    int64_t* pg_keys, int64_t* counts, void* stream);
+
+/* Kernels that tt_emb_profile can bracket with events. */
+typedef enum {
+  TT_EMB_K_NONE = 0,
+  TT_EMB_K_INGEST = 1,    /* grouping: keys, positions and bag ids of the occurrences */
+  TT_EMB_K_FWD_FUSED = 2, /* forward: C = A.B per prefix group, E = C.D per unique row */
+  TT_EMB_K_POOL = 3,      /* forward: sum pooling of E rows into the bags */
+  TT_EMB_K_SEG_SUM = 4,   /* backward: dE per unique row, summed over its occurrences */
+  TT_EMB_K_BWD_FUSED = 5  /* backward: per prefix group dD, dC, sum dC, dA, dB */
+} tt_emb_kernel;
+
+/* Benchmark instrumentation.  While set, every launch of `kernel`
+ * (tt_emb_kernel) made through this handle is bracketed by hipEventRecord of
+ * ev_begin (a hipEvent_t) before it and ev_end after it, on the stream of the
+ * call.  kernel = TT_EMB_K_NONE or NULL events switch it off.  The events
+ * stay owned by the caller. */
+tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* ev_end);
+
+/* Static text for a status code. */
+const char* tt_emb_status_string(tt_emb_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TT_EMB_H */

@@ -1,0 +1,257 @@
+// Backward pass of the TT-embedding gather (FlowTT Section 3.2, Eq. 1) and SGD.
+//   dE segment sums : dE_u = sum of grad_out rows over the occurrences of u,
+//                     walked in sorted order in fixed chunks; rows that cross a
+//                     chunk boundary are finished from per-chunk partials
+//                     (deterministic, no atomics)
+//   per group       : C recomputed, dD_u = C^T dE_u and dC_u = dE_u D_u^T per row,
+//                     sum dC over the group first, then dA = (sum dC) B^T and
+//                     dB = A^T (sum dC)
+#include "common.h"
+
+namespace ttemb {
+
+ShapeArgs shape_args(const Shape& s);
+int persistent_grid();
+
+// ---------------------------------------------------------------------------
+// dE segment sums over the sorted occurrences
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void seg_flush(int cur, int i0, int i1, int c, const int32_t* __restrict__ occ_start,
+                                          int D, int j0, const float* acc, float* __restrict__ dE,
+                                          float* __restrict__ part) {
+  const int lo = occ_start[cur], hi = occ_start[cur + 1];
+  float* dst;
+  if (lo >= i0 && hi <= i1)
+    dst = dE + (int64_t)cur * D;
+  else if (lo < i0)
+    dst = part + ((int64_t)c * 2 + 0) * D;
+  else
+    dst = part + ((int64_t)c * 2 + 1) * D;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int j = j0 + k * 64 + lane_id();
+    if (j < D) dst[j] = acc[k];
+  }
+}
+
+// One wave per chunk of SEG_CHUNK sorted occurrences; lanes hold 4 columns
+// each (column blocks of 256); occurrence indices are fetched 64 at a time.
+__global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+                                               const uint32_t* __restrict__ sorted_pos,
+                                               const int32_t* __restrict__ bag_of,
+                                               const int32_t* __restrict__ occ_start,
+                                               const int32_t* __restrict__ ctr, int D, float* __restrict__ dE,
+                                               float* __restrict__ part) {
+  const int nvalid = ctr[C_NVALID];
+  const int c = blockIdx.x;
+  const int i0 = c * SEG_CHUNK;
+  if (i0 >= nvalid) return;
+  const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
+  const int lane = lane_id();
+  for (int j0 = 0; j0 < D; j0 += 256) {
+    int cur = sorted_uid[i0];
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int base = i0; base < i1; base += 64) {
+      const int i = base + lane;
+      const int my_u = i < i1 ? sorted_uid[i] : -1;
+      const int my_b = i < i1 ? bag_of[sorted_pos[i]] : 0;
+      const int cnt = i1 - base < 64 ? i1 - base : 64;
+      for (int k = 0; k < cnt; ++k) {
+        const int u = __shfl(my_u, k, 64);
+        const int b = __shfl(my_b, k, 64);
+        if (u != cur) {
+          seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
+          cur = u;
+          acc[0] = acc[1] = acc[2] = acc[3] = 0.f;
+        }
+        const float* row = dV + (int64_t)b * D + j0 + lane;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (j0 + q * 64 + lane < D) acc[q] += row[q * 64];
+      }
+    }
+    seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
+  }
+}
+
+// rows whose occurrences span several chunks: first chunk's tail partial plus
+// the head partials of every following chunk, in chunk order
+__global__ void __launch_bounds__(64) k_seg_fix(const int32_t* __restrict__ occ_start, const int32_t* __restrict__ ctr,
+                                                int D, const float* __restrict__ part, float* __restrict__ dE) {
+  const int U = ctr[C_U];
+  for (int u = blockIdx.x; u < U; u += gridDim.x) {
+    const int lo = occ_start[u], hi = occ_start[u + 1];
+    const int c0 = lo / SEG_CHUNK, c1 = (hi - 1) / SEG_CHUNK;
+    if (c0 == c1) continue;
+    for (int j = lane_id(); j < D; j += 64) {
+      float acc = part[((int64_t)c0 * 2 + 1) * D + j];
+      for (int c = c0 + 1; c <= c1; ++c) acc += part[((int64_t)c * 2 + 0) * D + j];
+      dE[(int64_t)u * D + j] = acc;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// generic per-slice backward (any shape; plain VALU; core gradients through
+// global atomics)
+// ---------------------------------------------------------------------------
+constexpr int BWD_THREADS = 256;
+constexpr int BWD_CHUNK = 4;
+
+__global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const float* __restrict__ G1,
+                                                             const float* __restrict__ G2,
+                                                             const float* __restrict__ G3,
+                                                             const int4* __restrict__ slices,
+                                                             const uint32_t* __restrict__ uniq_key,
+                                                             int32_t* __restrict__ ctr, const float* __restrict__ dE,
+                                                             float* __restrict__ dG1, float* __restrict__ dG2,
+                                                             float* __restrict__ dG3) {
+  extern __shared__ float lds[];
+  const int d2R = s.d2 * s.R;
+  const int nC = s.d1 * d2R;
+  float* C = lds;           // nC
+  float* dCs = lds + nC;    // nC: sum of dC over the slice's rows
+  float* dEu = dCs + nC;    // D
+  __shared__ int s_chunk;
+  const int nsl = ctr[C_NSLICES];
+  const int nchunks = (nsl + BWD_CHUNK - 1) / BWD_CHUNK;
+  int victim = 0;
+  int cur_pg = -1;
+  const int rows12 = s.d1 * s.d2;
+  while (true) {
+    int c = claim_chunk(ctr + C_BWD_CTR, nchunks, &victim, &s_chunk);
+    if (c < 0) break;
+    const int s0 = c * BWD_CHUNK;
+    const int s1 = s0 + BWD_CHUNK < nsl ? s0 + BWD_CHUNK : nsl;
+    for (int si = s0; si < s1; ++si) {
+      const int4 sl = slices[si];
+      const int p = sl.x, rb = sl.y, re = sl.z;
+      const uint32_t key = (uint32_t)sl.w;
+      const int t = key / s.n12, q = key % s.n12;
+      const int i1 = q / s.n2, i2 = q % s.n2;
+      const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+      const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
+      __syncthreads();
+      if (p != cur_pg) {
+        for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
+          const int j1 = o / d2R, cc = o % d2R;
+          float acc = 0.f;
+          for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
+          C[o] = acc;
+        }
+        cur_pg = p;
+      }
+      for (int o = threadIdx.x; o < nC; o += BWD_THREADS) dCs[o] = 0.f;
+      __syncthreads();
+      for (int u = rb; u < re; ++u) {
+        const int i3 = decode_key(uniq_key[u], s.Npad, s.n2, s.n3).i3;
+        const float* Dm = G3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3;
+        for (int j = threadIdx.x; j < s.D; j += BWD_THREADS) dEu[j] = dE[(int64_t)u * s.D + j];
+        __syncthreads();
+        // dD_u = C^T dE_u  (R x d3)
+        float* g3 = dG3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3;
+        for (int o = threadIdx.x; o < s.R * s.d3; o += BWD_THREADS) {
+          const int b = o / s.d3, j3 = o % s.d3;
+          float acc = 0.f;
+          for (int r = 0; r < rows12; ++r) acc = fmaf(C[r * s.R + b], dEu[r * s.d3 + j3], acc);
+          unsafeAtomicAdd(&g3[o], acc);
+        }
+        // dC_u = dE_u D_u^T, summed over the slice
+        for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
+          const int r = o / s.R, b = o % s.R;
+          float acc = 0.f;
+          for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(dEu[r * s.d3 + j3], Dm[b * s.d3 + j3], acc);
+          dCs[o] += acc;
+        }
+        __syncthreads();
+      }
+      // dA = (sum dC) B^T  (d1 x R), dB = A^T (sum dC)  (R x d2R)
+      float* g1 = dG1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+      for (int o = threadIdx.x; o < s.d1 * s.R; o += BWD_THREADS) {
+        const int j1 = o / s.R, a = o % s.R;
+        float acc = 0.f;
+        for (int cc = 0; cc < d2R; ++cc) acc = fmaf(dCs[j1 * d2R + cc], Bm[a * d2R + cc], acc);
+        unsafeAtomicAdd(&g1[o], acc);
+      }
+      float* g2 = dG2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
+      for (int o = threadIdx.x; o < s.R * d2R; o += BWD_THREADS) {
+        const int a = o / d2R, cc = o % d2R;
+        float acc = 0.f;
+        for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(A[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
+        unsafeAtomicAdd(&g2[o], acc);
+      }
+    }
+  }
+}
+
+hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                           const int64_t* offsets, int64_t M, int64_t B, const float* dV, float* dG1, float* dG2,
+                           float* dG3, const Prof& prof, hipStream_t st) {
+  (void)offsets;
+  (void)B;
+  const int64_t n1s = (int64_t)s.T * s.n1 * s.d1 * s.R;
+  const int64_t n2s = (int64_t)s.T * s.n2 * s.R * s.d2 * s.R;
+  const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
+  hipError_t e;
+  if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
+  if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
+  if ((e = fill_f32(dG3, n3s, 0.f, st)) != hipSuccess) return e;
+  if (M <= 0) return hipSuccess;
+  float* dE = w.E;
+  const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
+  prof_begin(prof, K_SEG_SUM, st);
+  hipLaunchKernelGGL(k_seg_dE, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
+                     (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+                     (const int32_t*)w.ctr, s.D, dE, w.seg_part);
+  prof_end(prof, K_SEG_SUM, st);
+  hipLaunchKernelGGL(k_seg_fix, dim3(2048), dim3(64), 0, st, (const int32_t*)w.occ_start, (const int32_t*)w.ctr, s.D,
+                     (const float*)w.seg_part, dE);
+  const int grid = persistent_grid() * 2;
+  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid, 0u, st)) != hipSuccess) return e;
+  const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D);
+  if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
+      hipSuccess)
+    return e;
+  prof_begin(prof, K_BWD_FUSED, st);
+  hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
+                     (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3);
+  prof_end(prof, K_BWD_FUSED, st);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// SGD: G -= lr * dG on the three cores
+// ---------------------------------------------------------------------------
+__global__ void k_sgd(float* __restrict__ G, const float* __restrict__ dG, int64_t n, float lr) {
+  int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n4 = n / 4;
+  float4* G4 = reinterpret_cast<float4*>(G);
+  const float4* d4 = reinterpret_cast<const float4*>(dG);
+  for (int64_t k = i; k < n4; k += stride) {
+    float4 g = G4[k], d = d4[k];
+    g.x = fmaf(-lr, d.x, g.x);
+    g.y = fmaf(-lr, d.y, g.y);
+    g.z = fmaf(-lr, d.z, g.z);
+    g.w = fmaf(-lr, d.w, g.w);
+    G4[k] = g;
+  }
+  for (int64_t k = n4 * 4 + i; k < n; k += stride) G[k] = fmaf(-lr, dG[k], G[k]);
+}
+
+hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
+                      const float* dG3, float lr, hipStream_t st) {
+  const int64_t n[3] = {(int64_t)s.T * s.n1 * s.d1 * s.R, (int64_t)s.T * s.n2 * s.R * s.d2 * s.R,
+                        (int64_t)s.T * s.n3 * s.R * s.d3};
+  float* G[3] = {G1, G2, G3};
+  const float* d[3] = {dG1, dG2, dG3};
+  for (int k = 0; k < 3; ++k) {
+    int64_t blocks = (n[k] / 4 + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 2048) blocks = 2048;
+    hipLaunchKernelGGL(k_sgd, dim3((unsigned)blocks), dim3(256), 0, st, G[k], d[k], n[k], lr);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ttemb

@@ -1,0 +1,216 @@
+// Internal declarations shared by the HIP translation units of libttemb.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ttemb {
+
+// ---------------------------------------------------------------------------
+// Shape and derived constants of one handle.
+// ---------------------------------------------------------------------------
+struct Shape {
+  int T;
+  int64_t N;
+  int n1, n2, n3;
+  int d1, d2, d3;
+  int R;
+  int D;           // d1*d2*d3
+  uint32_t Npad;   // n1*n2*n3: key of (t, g) is t*Npad + g
+  uint32_t kinv;   // T*Npad: key given to an invalid occurrence (sorts last)
+  int key_bits;    // significant bits of kinv
+  int n12;         // n1*n2 prefixes per table
+  int64_t ndense;  // T*n1*n2 prefix slots
+};
+
+// Counter slots at the head of the workspace (int32).
+enum : int {
+  C_U = 0,        // unique (table, row) pairs
+  C_P = 1,        // prefix groups
+  C_NVALID = 2,   // valid occurrences
+  C_NSLICES = 3,  // work slices of the fused kernels
+  C_ERR = 4,      // sticky error bits
+  C_NSEG = 5,     // occurrence chunks of the dE segment sums
+  C_FWD_CTR = 64, // per-workgroup claim counters of the forward scheduler
+  C_BWD_CTR = 64 + 4096,
+  C_TOTAL = 64 + 2 * 4096,
+};
+enum : int { ERR_INDEX = 1, ERR_OFFSETS = 2 };
+
+// Fixed tiling constants.
+constexpr int SORT_THREADS = 256;
+constexpr int SORT_ITEMS = 16;
+constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;  // keys per radix tile
+constexpr int RADIX_BITS = 8;
+constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int SCAN_THREADS = 256;
+constexpr int SCAN_ITEMS = 16;
+constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+constexpr int SLICE_ROWS = 32;   // unique rows per work slice
+constexpr int SEG_CHUNK = 256;   // sorted occurrences per dE chunk
+constexpr int MAX_PERSIST_WG = 4096;
+
+// Device pointers carved out of the caller's workspace.
+struct Work {
+  int32_t* ctr;           // [C_TOTAL]
+  uint32_t* keys[2];      // radix ping-pong keys [M]
+  uint32_t* vals[2];      // radix ping-pong positions [M]
+  uint32_t* rcounts;      // [RADIX * ntiles]
+  uint32_t* rtotals;      // [npasses * RADIX]
+  uint64_t* flags;        // [M] packed (row head, group head) then their inclusive scan
+  uint64_t* tsum64;       // scan tile sums [ntiles_scan]
+  uint32_t* tsum32;       // scan tile sums for 32-bit scans
+  int32_t* bag_of;        // [M] global bag of each occurrence
+  int32_t* inv;           // [M] unique id of each occurrence (-1 invalid)
+  int32_t* sorted_uid;    // [M] unique id of each sorted occurrence
+  uint32_t* uniq_key;     // [M] key of each unique row
+  int32_t* occ_start;     // [M+1] first sorted position of each unique row
+  int32_t* pg_start;      // [M+1] first unique row of each prefix group
+  uint32_t* pg_key;       // [M] t*n1*n2 + i1*n2 + i2 of each group
+  uint32_t* dense_cnt;    // [ndense] slices per prefix slot, (t, i2, i1) order
+  uint32_t* dense_base;   // [ndense] exclusive scan of dense_cnt
+  int32_t* dense_pg;      // [ndense] group id per slot
+  int4* slices;           // [M] (group, row_begin, row_end, key)
+  float* E;               // [M][D] rows of the forward, dE rows in the backward
+  float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
+  uint32_t* sorted_keys;  // = keys[x] after the sort
+  uint32_t* sorted_pos;   // = vals[x] after the sort
+  int64_t M;              // capacity in occurrences
+  int64_t B;              // capacity in bags per table
+};
+
+// Event bracketing of one kernel for benchmarks (ids of tt_emb_kernel).
+struct Prof {
+  int kernel;
+  hipEvent_t begin, end;
+};
+enum : int { K_INGEST = 1, K_FWD_FUSED = 2, K_POOL = 3, K_SEG_SUM = 4, K_BWD_FUSED = 5 };
+inline void prof_begin(const Prof& p, int k, hipStream_t st) {
+  if (p.kernel == k && p.begin) (void)hipEventRecord(p.begin, st);
+}
+inline void prof_end(const Prof& p, int k, hipStream_t st) {
+  if (p.kernel == k && p.end) (void)hipEventRecord(p.end, st);
+}
+
+// Workspace layout for given capacities (bytes) and carving.
+size_t workspace_bytes(const Shape& s, int64_t M, int64_t B);
+void carve(const Shape& s, int64_t M, int64_t B, void* base, Work* w);
+
+// Launchers (each returns hipGetLastError() of its launches).
+hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64_t M, const int64_t* offsets,
+                        int64_t B, const Prof& prof, hipStream_t st);
+hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                          const int64_t* offsets, int64_t M, int64_t B, float* out, const Prof& prof,
+                          hipStream_t st);
+hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                           const int64_t* offsets, int64_t M, int64_t B, const float* dV, float* dG1, float* dG2,
+                           float* dG3, const Prof& prof, hipStream_t st);
+hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
+                      const float* dG3, float lr, hipStream_t st);
+
+// Small generic kernels shared across units (defined in group.hip).
+hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
+hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t st);
+hipError_t scan_u32_exclusive(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* tsum, int32_t* total_out,
+                              hipStream_t st);
+int persistent_grid();
+
+// ---------------------------------------------------------------------------
+// Device helpers.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    T u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// Exclusive scan over a block of NT threads; smem holds NT/64 values.
+template <typename T, int NT>
+__device__ __forceinline__ T block_excl_scan(T v, T* smem, T* total) {
+  constexpr int NW = NT / 64;
+  T inc = wave_incl_scan(v);
+  const int w = threadIdx.x >> 6;
+  if (lane_id() == 63) smem[w] = inc;
+  __syncthreads();
+  T base = 0, tot = 0;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    T x = smem[k];
+    if (k < w) base += x;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+}  // namespace ttemb
+
+namespace ttemb {
+
+// Persistent-thread scheduler with chunked work stealing (FlowTT Section 3.4):
+// the chunk list is split evenly over the resident workgroups; workgroup w
+// first claims chunks of its own share through its counter ctrs[w], then
+// steals the remaining chunks of the other shares, visiting victims w+1,
+// w+2, ... in turn.  Returns the next chunk or -1 once every share is
+// exhausted.  Called by all threads of the block; one thread claims.
+__device__ __forceinline__ int claim_chunk(int32_t* ctrs, int nchunks, int* victim_state, int* s_chunk) {
+  const int W = gridDim.x, w = blockIdx.x;
+  if (threadIdx.x == 0) {
+    int c = -1;
+    int k = *victim_state;
+    while (k < W) {
+      int v = w + k;
+      if (v >= W) v -= W;
+      int lo = (int)(((int64_t)nchunks * v) / W), hi = (int)(((int64_t)nchunks * (v + 1)) / W);
+      int got = atomicAdd(&ctrs[v], 1);
+      if (lo + got < hi) {
+        c = lo + got;
+        break;
+      }
+      ++k;
+    }
+    *victim_state = k;
+    *s_chunk = c;
+  }
+  __syncthreads();
+  int c = *s_chunk;
+  __syncthreads();
+  return c;
+}
+
+struct ShapeArgs {  // shape constants passed by value to kernels
+  int T, n1, n2, n3, d1, d2, d3, R, D, n12;
+  uint32_t Npad;
+};
+
+}  // namespace ttemb
+
+namespace ttemb {
+
+// Digits of a sorted key t*Npad + g (Eq. 2: i1 = g / (n2 n3), i2 = (g / n3) mod n2,
+// i3 = g mod n3); every kernel decodes keys through this one function.
+struct Digits {
+  int t, i1, i2, i3;
+};
+__device__ __forceinline__ Digits decode_key(uint32_t key, uint32_t Npad, int n2, int n3) {
+  Digits d;
+  d.t = (int)(key / Npad);
+  const uint32_t g = key - (uint32_t)d.t * Npad;
+  const uint32_t q = g / (uint32_t)n3;
+  d.i3 = (int)(g - q * (uint32_t)n3);
+  d.i1 = (int)(q / (uint32_t)n2);
+  d.i2 = (int)(q - (uint32_t)d.i1 * (uint32_t)n2);
+  return d;
+}
+
+hipError_t launch_debug_digits(const Shape& s, const Work& w, int32_t* out, int U, int which, hipStream_t st);
+
+}  // namespace ttemb

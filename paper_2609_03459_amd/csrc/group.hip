@@ -1,0 +1,486 @@
+// Prefix-based index grouping (FlowTT Section 3.3, Fig. 4) on gfx950:
+//   ingest   -> one 32-bit key per occurrence, t*Npad + g (invalid rows get Npad*T)
+//   sort     -> LSD radix sort of (key, position), 8-bit digits, stable
+//   unique   -> row heads and prefix-group heads, one inclusive scan of packed flags
+//   RLE      -> unique rows, inverse map, occurrence ranges, prefix groups
+//   order    -> prefix groups re-ordered (table, i2, i1) through a dense scan over
+//               the prefix space, cut into work slices of at most SLICE_ROWS rows
+// All kernels are plain HIP for wave64; no library sort or scan is used.
+#include "common.h"
+
+namespace ttemb {
+
+// ---------------------------------------------------------------------------
+// fills
+// ---------------------------------------------------------------------------
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (; i < n; i += stride) p[i] = v;
+}
+
+hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t fill_f32(float* p, int64_t n, float v, hipStream_t st) {
+  union {
+    float f;
+    uint32_t u;
+  } c;
+  c.f = v;
+  return fill_u32(reinterpret_cast<uint32_t*>(p), n, c.u, st);
+}
+
+// ---------------------------------------------------------------------------
+// ingest: keys, positions and bag ids, one tile of SORT_TILE occurrences per block
+// ---------------------------------------------------------------------------
+constexpr int INGEST_WIN = SORT_TILE + 1;
+
+__device__ __forceinline__ int64_t upper_bound_global(const int64_t* a, int64_t lo, int64_t hi, int64_t x) {
+  // first index in [lo, hi) with a[i] > x (hi if none)
+  while (lo < hi) {
+    int64_t mid = lo + ((hi - lo) >> 1);
+    if (a[mid] <= x)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+__global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restrict__ idx, int64_t M,
+                                                         const int64_t* __restrict__ offsets, int64_t B, int T,
+                                                         int64_t N, uint32_t Npad, uint32_t kinv,
+                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                                         int32_t* __restrict__ bag_of, int32_t* __restrict__ ctr) {
+  __shared__ int64_t win[INGEST_WIN];
+  __shared__ int64_t s_first, s_last;
+  const int64_t NB = (int64_t)T * B;
+  const int64_t o0 = (int64_t)blockIdx.x * SORT_TILE;
+  const int64_t o1 = (o0 + SORT_TILE < M ? o0 + SORT_TILE : M);
+  int64_t bfirst = 0, nwin = 0;
+  if (offsets) {
+    if (threadIdx.x == 0) {
+      int64_t f = upper_bound_global(offsets, 0, NB + 1, o0) - 1;
+      int64_t l = upper_bound_global(offsets, 0, NB + 1, o1 - 1) - 1;
+      f = f < 0 ? 0 : (f > NB - 1 ? NB - 1 : f);
+      l = l < f ? f : (l > NB - 1 ? NB - 1 : l);
+      s_first = f;
+      s_last = l;
+    }
+    __syncthreads();
+    bfirst = s_first;
+    nwin = s_last - s_first + 2;  // offsets[bfirst .. blast+1]
+    if (nwin <= INGEST_WIN)
+      for (int k = threadIdx.x; k < nwin; k += SORT_THREADS) win[k] = offsets[bfirst + k];
+    __syncthreads();
+  }
+  int err = 0;
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
+    if (o >= o1) break;
+    int64_t b;
+    if (!offsets) {
+      b = o;
+    } else if (nwin <= INGEST_WIN) {
+      int64_t lo = 0, hi = nwin;
+      while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if (win[mid] <= o)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      b = bfirst + lo - 1;
+    } else {
+      b = upper_bound_global(offsets, bfirst, bfirst + nwin, o) - 1;
+    }
+    b = b < 0 ? 0 : (b > NB - 1 ? NB - 1 : b);
+    int64_t g = idx[o];
+    uint32_t t = (uint32_t)(b / B);
+    uint32_t key;
+    if (g >= 0 && g < N) {
+      key = t * Npad + (uint32_t)g;
+    } else {
+      key = kinv;
+      err = 1;
+    }
+    keys[o] = key;
+    vals[o] = (uint32_t)o;
+    bag_of[o] = (int32_t)b;
+  }
+  if (err) atomicOr(&ctr[C_ERR], ERR_INDEX);
+}
+
+__global__ void k_check_offsets(const int64_t* __restrict__ offsets, int64_t NB, int64_t M, int32_t* ctr) {
+  int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int bad = 0;
+  for (; b < NB; b += stride) {
+    int64_t lo = offsets[b], hi = offsets[b + 1];
+    if (lo < 0 || hi < lo || hi > M) bad = 1;
+    if (b == 0 && lo != 0) bad = 1;
+    if (b == NB - 1 && hi != M) bad = 1;
+  }
+  if (bad) atomicOr(&ctr[C_ERR], ERR_OFFSETS);
+}
+
+// ---------------------------------------------------------------------------
+// LSD radix sort of (key, position), 8-bit digits, stable
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __restrict__ keys, int n, int shift,
+                                                             uint32_t* __restrict__ counts, int ntiles,
+                                                             uint32_t* __restrict__ totals) {
+  __shared__ uint32_t h[4][RADIX];  // one histogram per wave
+  const int w = threadIdx.x >> 6;
+  for (int k = threadIdx.x; k < 4 * RADIX; k += SORT_THREADS) (&h[0][0])[k] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * SORT_TILE;
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    int i = base + j * SORT_THREADS + threadIdx.x;
+    if (i < n) atomicAdd(&h[w][(keys[i] >> shift) & (RADIX - 1)], 1u);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) {
+    uint32_t c = h[0][d] + h[1][d] + h[2][d] + h[3][d];
+    counts[d * ntiles + blockIdx.x] = c;
+    if (c) atomicAdd(&totals[d], c);
+  }
+}
+
+// one block per digit: exclusive offsets of every tile for that digit
+__global__ void __launch_bounds__(256) k_radix_scan(uint32_t* __restrict__ counts, int ntiles,
+                                                    const uint32_t* __restrict__ totals) {
+  __shared__ uint32_t smem[4];
+  __shared__ uint32_t s_base;
+  const int d = blockIdx.x;
+  if (threadIdx.x < 64) {
+    uint32_t s = 0;
+    for (int k = threadIdx.x; k < d; k += 64) s += totals[k];
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (threadIdx.x == 0) s_base = s;
+  }
+  __syncthreads();
+  uint32_t running = s_base;
+  uint32_t* row = counts + (int64_t)d * ntiles;
+  for (int start = 0; start < ntiles; start += 256 * 4) {
+    uint32_t v[4];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      int i = start + threadIdx.x * 4 + k;
+      v[k] = i < ntiles ? row[i] : 0u;
+      sum += v[k];
+    }
+    uint32_t tot;
+    uint32_t ex = block_excl_scan<uint32_t, 256>(sum, smem, &tot);
+    uint32_t acc = running + ex;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      int i = start + threadIdx.x * 4 + k;
+      if (i < ntiles) row[i] = acc;
+      acc += v[k];
+    }
+    running += tot;
+  }
+}
+
+// Stable scatter.  Wave w of the block owns keys [tile + w*1024, +1024); item j
+// of lane l is element w*1024 + j*64 + l, so (w, j, l) order is input order.
+__global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
+                                                                const uint32_t* __restrict__ vin,
+                                                                uint32_t* __restrict__ kout,
+                                                                uint32_t* __restrict__ vout, int n, int shift,
+                                                                const uint32_t* __restrict__ offs, int ntiles) {
+  __shared__ uint32_t wh[4][RADIX];   // running per-wave digit counts
+  __shared__ uint32_t gbase[4][RADIX];  // global base per (wave, digit)
+  const int w = threadIdx.x >> 6;
+  const int lane = lane_id();
+  for (int k = threadIdx.x; k < 4 * RADIX; k += SORT_THREADS) (&wh[0][0])[k] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * SORT_TILE + w * (SORT_ITEMS * 64);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint32_t key[SORT_ITEMS], val[SORT_ITEMS], rk[SORT_ITEMS];
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    int i = base + j * 64 + lane;
+    bool ok = i < n;
+    key[j] = ok ? kin[i] : 0u;
+    val[j] = ok ? vin[i] : 0u;
+    uint32_t dg = (key[j] >> shift) & (RADIX - 1);
+    uint64_t peers = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < RADIX_BITS; ++b) {
+      uint64_t m = __ballot((dg >> b) & 1);
+      peers &= ((dg >> b) & 1) ? m : ~m;
+    }
+    uint32_t before = __popcll(peers & lt);
+    uint32_t cnt = __popcll(peers);
+    uint32_t prev = ok ? wh[w][dg] : 0u;
+    rk[j] = prev + before;
+    if (ok && before == 0) wh[w][dg] = prev + cnt;
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) {
+    uint32_t g = offs[d * ntiles + blockIdx.x];
+    uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
+    gbase[0][d] = g;
+    gbase[1][d] = g + c0;
+    gbase[2][d] = g + c0 + c1;
+    gbase[3][d] = g + c0 + c1 + c2;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    int i = base + j * 64 + lane;
+    if (i < n) {
+      uint32_t dg = (key[j] >> shift) & (RADIX - 1);
+      uint32_t pos = gbase[w][dg] + rk[j];
+      kout[pos] = key[j];
+      vout[pos] = val[j];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// generic scans (tile reduce -> single-block scan of tile sums -> tile scan)
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(const T* __restrict__ in, int64_t n,
+                                                              T* __restrict__ tsum) {
+  __shared__ T smem[SCAN_THREADS / 64];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+  T s = 0;
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    int64_t i = base + j * SCAN_THREADS + threadIdx.x;
+    if (i < n) s += in[i];
+  }
+  T tot;
+  block_excl_scan<T, SCAN_THREADS>(s, smem, &tot);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = tot;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* __restrict__ tsum, int ntiles, int32_t* total_out) {
+  __shared__ T smem[SCAN_THREADS / 64];
+  T running = 0;
+  for (int start = 0; start < ntiles; start += SCAN_THREADS) {
+    int i = start + threadIdx.x;
+    T v = i < ntiles ? tsum[i] : (T)0;
+    T tot;
+    T ex = block_excl_scan<T, SCAN_THREADS>(v, smem, &tot);
+    if (i < ntiles) tsum[i] = running + ex;
+    running += tot;
+  }
+  if (total_out && threadIdx.x == 0) *total_out = (int32_t)running;
+}
+
+// each thread scans SCAN_ITEMS consecutive elements
+template <typename T, bool INCLUSIVE>
+__global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(const T* __restrict__ in, T* __restrict__ out, int64_t n,
+                                                            const T* __restrict__ tsum) {
+  __shared__ T smem[SCAN_THREADS / 64];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + (int64_t)threadIdx.x * SCAN_ITEMS;
+  T v[SCAN_ITEMS];
+  T s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    int64_t i = base + k;
+    v[k] = i < n ? in[i] : (T)0;
+    s += v[k];
+  }
+  T tot;
+  T acc = block_excl_scan<T, SCAN_THREADS>(s, smem, &tot) + tsum[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    int64_t i = base + k;
+    if (INCLUSIVE) acc += v[k];
+    if (i < n) out[i] = acc;
+    if (!INCLUSIVE) acc += v[k];
+  }
+}
+
+template <typename T, bool INCLUSIVE>
+static hipError_t scan_generic(const T* in, T* out, int64_t n, T* tsum, int32_t* total_out, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  int ntiles = (int)((n + SCAN_TILE - 1) / SCAN_TILE);
+  hipLaunchKernelGGL(k_scan_reduce<T>, dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, n, tsum);
+  hipLaunchKernelGGL(k_scan_top<T>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, ntiles, total_out);
+  hipLaunchKernelGGL((k_scan_down<T, INCLUSIVE>), dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, out, n,
+                     (const T*)tsum);
+  return hipGetLastError();
+}
+
+hipError_t scan_u32_exclusive(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* tsum, int32_t* total_out,
+                              hipStream_t st) {
+  return scan_generic<uint32_t, false>(in, out, n, tsum, total_out, st);
+}
+
+// ---------------------------------------------------------------------------
+// unique rows and prefix groups
+// ---------------------------------------------------------------------------
+__global__ void k_flags(const uint32_t* __restrict__ sk, int n, uint32_t kinv, uint32_t n3,
+                        uint64_t* __restrict__ flags, int32_t* __restrict__ ctr) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  uint32_t k = sk[i];
+  uint64_t f = 0;
+  if (k < kinv) {
+    uint32_t kp = i > 0 ? sk[i - 1] : 0xffffffffu;
+    bool head = (i == 0) || kp != k;
+    bool pgh = head && ((i == 0) || (kp / n3) != (k / n3));
+    f = (uint64_t)head | ((uint64_t)pgh << 32);
+    if (i == n - 1 || sk[i + 1] >= kinv) ctr[C_NVALID] = i + 1;
+  }
+  flags[i] = f;
+}
+
+__global__ void k_group_write(const uint32_t* __restrict__ sk, const uint32_t* __restrict__ sp,
+                              const uint64_t* __restrict__ incl, int n, uint32_t kinv, uint32_t n3,
+                              int32_t* __restrict__ inv, int32_t* __restrict__ sorted_uid,
+                              uint32_t* __restrict__ uniq_key, int32_t* __restrict__ occ_start,
+                              int32_t* __restrict__ pg_start, uint32_t* __restrict__ pg_key,
+                              int32_t* __restrict__ ctr) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  uint32_t k = sk[i];
+  uint32_t pos = sp[i];
+  if (k >= kinv) {
+    inv[pos] = -1;
+    return;
+  }
+  uint64_t s = incl[i];
+  int uid = (int)(s & 0xffffffffu) - 1;
+  int pg = (int)(s >> 32) - 1;
+  uint32_t kp = i > 0 ? sk[i - 1] : 0xffffffffu;
+  bool head = (i == 0) || kp != k;
+  bool pgh = head && ((i == 0) || (kp / n3) != (k / n3));
+  inv[pos] = uid;
+  sorted_uid[i] = uid;
+  if (head) {
+    uniq_key[uid] = k;
+    occ_start[uid] = i;
+  }
+  if (pgh) {
+    pg_start[pg] = uid;
+    pg_key[pg] = k / n3;
+  }
+  if (i == n - 1 || sk[i + 1] >= kinv) {
+    ctr[C_U] = uid + 1;
+    ctr[C_P] = pg + 1;
+    occ_start[uid + 1] = i + 1;
+    pg_start[pg + 1] = uid + 1;
+  }
+}
+
+// prefix slots in (table, i2, i1) order: slices per group
+__global__ void k_dense_set(const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key,
+                            const int32_t* __restrict__ ctr, int n1, int n2, uint32_t* __restrict__ dense_cnt,
+                            int32_t* __restrict__ dense_pg) {
+  const int P = ctr[C_P];
+  const int n12 = n1 * n2;
+  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < P; p += gridDim.x * blockDim.x) {
+    uint32_t key = pg_key[p];
+    uint32_t t = key / n12, q = key % n12;
+    uint32_t i1 = q / n2, i2 = q % n2;
+    int64_t slot = ((int64_t)t * n2 + i2) * n1 + i1;
+    int rows = pg_start[p + 1] - pg_start[p];
+    dense_cnt[slot] = (uint32_t)((rows + SLICE_ROWS - 1) / SLICE_ROWS);
+    dense_pg[slot] = p;
+  }
+}
+
+__global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint32_t* __restrict__ dense_base,
+                              const int32_t* __restrict__ dense_pg, int64_t ndense,
+                              const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key,
+                              int4* __restrict__ slices) {
+  for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < ndense;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t c = dense_cnt[s];
+    if (!c) continue;
+    int p = dense_pg[s];
+    uint32_t b = dense_base[s];
+    int r0 = pg_start[p], r1 = pg_start[p + 1];
+    for (uint32_t k = 0; k < c; ++k) {
+      int rb = r0 + (int)k * SLICE_ROWS;
+      int re = rb + SLICE_ROWS < r1 ? rb + SLICE_ROWS : r1;
+      slices[b + k] = make_int4(p, rb, re, (int)pg_key[p]);
+    }
+  }
+}
+
+__global__ void k_group_init(int32_t* ctr, int32_t* occ_start, int32_t* pg_start, uint32_t* rtotals,
+                             int nrtotals) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < C_TOTAL) ctr[i] = 0;  // counters and the error word start each grouping at zero
+  if (i < nrtotals) rtotals[i] = 0;
+  if (i == 0) {
+    occ_start[0] = 0;
+    pg_start[0] = 0;
+  }
+}
+
+static int grid_for(int64_t n, int per_block, int cap) {
+  int64_t g = (n + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (int)g;
+}
+
+hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64_t M, const int64_t* offsets,
+                        int64_t B, const Prof& prof, hipStream_t st) {
+  const int npasses = (s.key_bits + RADIX_BITS - 1) / RADIX_BITS;
+  const int nrt = npasses * RADIX;
+  {
+    int total = C_TOTAL > nrt ? C_TOTAL : nrt;
+    hipLaunchKernelGGL(k_group_init, dim3((total + 255) / 256), dim3(256), 0, st, w.ctr, w.occ_start, w.pg_start,
+                       w.rtotals, nrt);
+  }
+  hipError_t e = fill_u32(w.dense_cnt, s.ndense, 0u, st);
+  if (e != hipSuccess) return e;
+  const int64_t NB = (int64_t)s.T * B;
+  if (offsets && NB > 0)
+    hipLaunchKernelGGL(k_check_offsets, dim3(grid_for(NB, 256, 1024)), dim3(256), 0, st, offsets, NB, M, w.ctr);
+  if (M <= 0) return hipGetLastError();
+  const int n = (int)M;
+  const int ntiles = (n + SORT_TILE - 1) / SORT_TILE;
+  prof_begin(prof, K_INGEST, st);
+  hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, B, s.T, s.N, s.Npad, s.kinv,
+                     w.keys[0], w.vals[0], w.bag_of, w.ctr);
+  prof_end(prof, K_INGEST, st);
+  int cur = 0;
+  for (int p = 0; p < npasses; ++p) {
+    const int shift = p * RADIX_BITS;
+    uint32_t* tot = w.rtotals + p * RADIX;
+    hipLaunchKernelGGL(k_radix_hist, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift, w.rcounts,
+                       ntiles, tot);
+    hipLaunchKernelGGL(k_radix_scan, dim3(RADIX), dim3(256), 0, st, w.rcounts, ntiles, (const uint32_t*)tot);
+    hipLaunchKernelGGL(k_radix_scatter, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
+                       w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles);
+    cur ^= 1;
+  }
+  const uint32_t* sk = w.keys[cur];
+  const uint32_t* sp = w.vals[cur];
+  hipLaunchKernelGGL(k_flags, dim3((n + 255) / 256), dim3(256), 0, st, sk, n, s.kinv, (uint32_t)s.n3, w.flags,
+                     w.ctr);
+  e = scan_generic<uint64_t, true>(w.flags, w.flags, M, w.tsum64, nullptr, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_group_write, dim3((n + 255) / 256), dim3(256), 0, st, sk, sp, (const uint64_t*)w.flags, n,
+                     s.kinv, (uint32_t)s.n3, w.inv, w.sorted_uid, w.uniq_key, w.occ_start, w.pg_start, w.pg_key,
+                     w.ctr);
+  hipLaunchKernelGGL(k_dense_set, dim3(grid_for(M, 256, 2048)), dim3(256), 0, st, (const int32_t*)w.pg_start,
+                     (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, w.dense_cnt, w.dense_pg);
+  e = scan_generic<uint32_t, false>(w.dense_cnt, w.dense_base, s.ndense, w.tsum32, w.ctr + C_NSLICES, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
+                     (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
+                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, w.slices);
+  return hipGetLastError();
+}
+
+}  // namespace ttemb

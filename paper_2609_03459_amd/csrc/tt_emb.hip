@@ -1,0 +1,353 @@
+// C ABI of libttemb: argument checks, workspace layout and launch order.
+// The operator and its conventions are described in include/tt_emb.h.
+#include "../../include/tt_emb.h"
+
+#include <new>
+#include <stdint.h>
+#include <string.h>
+
+#include "common.h"
+
+using namespace ttemb;
+
+struct tt_emb_s {
+  Shape s;
+  tt_emb_desc desc;
+  // the grouping last written into a workspace, for reuse_grouping = 1
+  bool g_valid;
+  const void* g_ws;
+  const int64_t* g_idx;
+  const int64_t* g_off;
+  int64_t g_M, g_B;
+  Prof prof;  // benchmark event bracketing
+};
+
+namespace ttemb {
+
+static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static int sort_passes(const Shape& s) { return (s.key_bits + RADIX_BITS - 1) / RADIX_BITS; }
+
+// Walks the workspace regions in a fixed order; with base == nullptr it only
+// measures.
+static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) {
+  (void)B;
+  const int64_t m = M > 0 ? M : 1;
+  const int64_t sort_tiles = (m + SORT_TILE - 1) / SORT_TILE;
+  const int64_t scan_tiles = (m + SCAN_TILE - 1) / SCAN_TILE;
+  const int64_t dscan_tiles = (s.ndense + SCAN_TILE - 1) / SCAN_TILE;
+  const int64_t nseg = (m + SEG_CHUNK - 1) / SEG_CHUNK;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* p = base ? base + off : nullptr;
+    off = align_up(off + bytes);
+    return p;
+  };
+  Work tmp;
+  Work* W = w ? w : &tmp;
+  W->ctr = (int32_t*)take(sizeof(int32_t) * C_TOTAL);
+  W->keys[0] = (uint32_t*)take(4 * m);
+  W->keys[1] = (uint32_t*)take(4 * m);
+  W->vals[0] = (uint32_t*)take(4 * m);
+  W->vals[1] = (uint32_t*)take(4 * m);
+  W->rcounts = (uint32_t*)take(4 * RADIX * sort_tiles);
+  W->rtotals = (uint32_t*)take(4 * RADIX * 4);
+  W->flags = (uint64_t*)take(8 * m);
+  W->tsum64 = (uint64_t*)take(8 * scan_tiles);
+  W->tsum32 = (uint32_t*)take(4 * (dscan_tiles > scan_tiles ? dscan_tiles : scan_tiles));
+  W->bag_of = (int32_t*)take(4 * m);
+  W->inv = (int32_t*)take(4 * m);
+  W->sorted_uid = (int32_t*)take(4 * m);
+  W->uniq_key = (uint32_t*)take(4 * m);
+  W->occ_start = (int32_t*)take(4 * (m + 1));
+  W->pg_start = (int32_t*)take(4 * (m + 1));
+  W->pg_key = (uint32_t*)take(4 * m);
+  W->dense_cnt = (uint32_t*)take(4 * s.ndense);
+  W->dense_base = (uint32_t*)take(4 * s.ndense);
+  W->dense_pg = (int32_t*)take(4 * s.ndense);
+  W->slices = (int4*)take(16 * m);
+  W->E = (float*)take(4 * (size_t)m * s.D);
+  W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
+  const int par = sort_passes(s) & 1;
+  W->sorted_keys = W->keys[par];
+  W->sorted_pos = W->vals[par];
+  W->M = M;
+  W->B = B;
+  return off;
+}
+
+size_t workspace_bytes(const Shape& s, int64_t M, int64_t B) { return layout(s, M, B, nullptr, nullptr); }
+
+void carve(const Shape& s, int64_t M, int64_t B, void* base, Work* w) { layout(s, M, B, (char*)base, w); }
+
+__global__ void k_debug_digits(const uint32_t* __restrict__ uniq_key, int U, uint32_t Npad, int n2, int n3,
+                               int which, int32_t* __restrict__ out) {
+  int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= U) return;
+  Digits d = decode_key(uniq_key[u], Npad, n2, n3);
+  out[u] = which == 0 ? d.i1 : (which == 1 ? d.i2 : d.i3);
+}
+
+// digit `which` (0: i1, 1: i2, 2: i3) of every unique row into out[U]
+hipError_t launch_debug_digits(const Shape& s, const Work& w, int32_t* out, int U, int which, hipStream_t st) {
+  if (U <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_debug_digits, dim3((U + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.uniq_key, U, s.Npad,
+                     s.n2, s.n3, which, out);
+  return hipGetLastError();
+}
+
+}  // namespace ttemb
+
+static bool al(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+static int bit_length(uint64_t x) {
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+extern "C" {
+
+const char* tt_emb_status_string(tt_emb_status s) {
+  switch (s) {
+    case TT_EMB_OK: return "ok";
+    case TT_EMB_EINVAL: return "invalid argument";
+    case TT_EMB_ENOMEM: return "out of host memory";
+    case TT_EMB_EHIP: return "HIP runtime error";
+    case TT_EMB_ERANGE: return "index or offsets out of range";
+    case TT_EMB_EUNSUPPORTED: return "shape not supported";
+  }
+  return "unknown status";
+}
+
+tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
+  if (!d || !out) return TT_EMB_EINVAL;
+  *out = nullptr;
+  if (d->num_tables < 1 || d->num_rows < 1 || d->rank < 1 || d->max_indices < 0 || d->max_bags < 0)
+    return TT_EMB_EINVAL;
+  for (int k = 0; k < 3; ++k)
+    if (d->row_factors[k] < 1 || d->dim_factors[k] < 1) return TT_EMB_EINVAL;
+  const uint64_t npad = (uint64_t)d->row_factors[0] * d->row_factors[1] * d->row_factors[2];
+  if ((uint64_t)d->num_rows > npad) return TT_EMB_EINVAL;
+  const uint64_t T = (uint64_t)d->num_tables;
+  const uint64_t D = (uint64_t)d->dim_factors[0] * d->dim_factors[1] * d->dim_factors[2];
+  if (T * npad >= 0xffffffffull) return TT_EMB_EUNSUPPORTED;
+  if (T * d->row_factors[0] * d->row_factors[1] >= (1ull << 28)) return TT_EMB_EUNSUPPORTED;
+  if ((uint64_t)d->max_indices >= (1ull << 31)) return TT_EMB_EUNSUPPORTED;
+  if (T * (uint64_t)d->max_bags >= (1ull << 31)) return TT_EMB_EUNSUPPORTED;
+  if (d->rank > 64 || (uint64_t)d->dim_factors[0] * d->dim_factors[1] * d->rank > 8192 || D > 4096)
+    return TT_EMB_EUNSUPPORTED;
+  tt_emb_s* h = new (std::nothrow) tt_emb_s();
+  if (!h) return TT_EMB_ENOMEM;
+  h->desc = *d;
+  Shape& s = h->s;
+  s.T = d->num_tables;
+  s.N = d->num_rows;
+  s.n1 = d->row_factors[0];
+  s.n2 = d->row_factors[1];
+  s.n3 = d->row_factors[2];
+  s.d1 = d->dim_factors[0];
+  s.d2 = d->dim_factors[1];
+  s.d3 = d->dim_factors[2];
+  s.R = d->rank;
+  s.D = (int)D;
+  s.Npad = (uint32_t)npad;
+  s.kinv = (uint32_t)(T * npad);
+  s.key_bits = bit_length(s.kinv);
+  s.n12 = s.n1 * s.n2;
+  s.ndense = (int64_t)T * s.n1 * s.n2;
+  h->g_valid = false;
+  h->prof.kernel = 0;
+  h->prof.begin = nullptr;
+  h->prof.end = nullptr;
+  *out = h;
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* ev_end) {
+  if (!h || kernel < TT_EMB_K_NONE || kernel > TT_EMB_K_BWD_FUSED) return TT_EMB_EINVAL;
+  const bool off = kernel == TT_EMB_K_NONE || !ev_begin || !ev_end;
+  h->prof.kernel = off ? 0 : kernel;
+  h->prof.begin = off ? nullptr : (hipEvent_t)ev_begin;
+  h->prof.end = off ? nullptr : (hipEvent_t)ev_end;
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_destroy(tt_emb_handle h) {
+  delete h;
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_workspace_size(tt_emb_handle h, size_t* bytes) {
+  if (!h || !bytes) return TT_EMB_EINVAL;
+  *bytes = workspace_bytes(h->s, h->desc.max_indices, h->desc.max_bags);
+  return TT_EMB_OK;
+}
+
+static tt_emb_status check_batch(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets, int64_t B,
+                                 const void* ws, size_t ws_bytes) {
+  if (!h || !ws) return TT_EMB_EINVAL;
+  if (M < 0 || B < 0 || M > h->desc.max_indices || B > h->desc.max_bags) return TT_EMB_EINVAL;
+  if (M > 0 && !idx) return TT_EMB_EINVAL;
+  if (!offsets && M != (int64_t)h->s.T * B) return TT_EMB_EINVAL;
+  if (offsets && B == 0 && M != 0) return TT_EMB_EINVAL;
+  if (!al(idx, 8) || !al(offsets, 8) || !al(ws, 256)) return TT_EMB_EINVAL;
+  if (ws_bytes < workspace_bytes(h->s, h->desc.max_indices, h->desc.max_bags)) return TT_EMB_EINVAL;
+  return TT_EMB_OK;
+}
+
+static tt_emb_status hip_status(hipError_t e) { return e == hipSuccess ? TT_EMB_OK : TT_EMB_EHIP; }
+
+static tt_emb_status do_group(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets, int64_t B,
+                              void* ws, hipStream_t st) {
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, ws, &w);
+  h->g_valid = false;
+  hipError_t e = launch_group(h->s, w, idx, M, offsets, B, h->prof, st);
+  if (e != hipSuccess) return TT_EMB_EHIP;
+  h->g_valid = true;
+  h->g_ws = ws;
+  h->g_idx = idx;
+  h->g_off = offsets;
+  h->g_M = M;
+  h->g_B = B;
+  return TT_EMB_OK;
+}
+
+static bool grouping_matches(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets, int64_t B,
+                             const void* ws) {
+  return h->g_valid && h->g_ws == ws && h->g_idx == idx && h->g_off == offsets && h->g_M == M && h->g_B == B;
+}
+
+tt_emb_status tt_emb_group(tt_emb_handle h, const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                           int64_t num_bags, void* workspace, size_t ws_bytes, void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  return do_group(h, indices, num_indices, offsets, num_bags, workspace, (hipStream_t)stream);
+}
+
+tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                             const int64_t* indices, int64_t num_indices, const int64_t* offsets, int64_t num_bags,
+                             float* out, int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  if (!G1 || !G2 || !G3 || (!out && num_bags > 0)) return TT_EMB_EINVAL;
+  if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(out, 16)) return TT_EMB_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (reuse_grouping) {
+    if (!grouping_matches(h, indices, num_indices, offsets, num_bags, workspace)) return TT_EMB_EINVAL;
+  } else {
+    st = do_group(h, indices, num_indices, offsets, num_bags, workspace, s);
+    if (st != TT_EMB_OK) return st;
+  }
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  return hip_status(launch_forward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, out, h->prof, s));
+}
+
+tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                              const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                              int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
+                              int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  if (!G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
+  if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(grad_out, 16) || !al(dG1, 16) || !al(dG2, 16) ||
+      !al(dG3, 16))
+    return TT_EMB_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (reuse_grouping) {
+    if (!grouping_matches(h, indices, num_indices, offsets, num_bags, workspace)) return TT_EMB_EINVAL;
+  } else {
+    st = do_group(h, indices, num_indices, offsets, num_bags, workspace, s);
+    if (st != TT_EMB_OK) return st;
+  }
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  return hip_status(
+      launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, dG1, dG2, dG3, h->prof, s));
+}
+
+tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
+                         const float* dG3, float lr, void* stream) {
+  if (!h || !G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3) return TT_EMB_EINVAL;
+  if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(dG1, 16) || !al(dG2, 16) || !al(dG3, 16))
+    return TT_EMB_EINVAL;
+  return hip_status(launch_sgd(h->s, G1, G2, G3, dG1, dG2, dG3, lr, (hipStream_t)stream));
+}
+
+tt_emb_status tt_emb_check_errors(tt_emb_handle h, void* workspace, void* stream) {
+  if (!h || !workspace) return TT_EMB_EINVAL;
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return TT_EMB_EHIP;
+  int32_t err = 0;
+  if (hipMemcpy(&err, w.ctr + C_ERR, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess) return TT_EMB_EHIP;
+  if (err) {
+    int32_t zero = 0;
+    if (hipMemcpy(w.ctr + C_ERR, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return TT_EMB_EHIP;
+    return TT_EMB_ERANGE;
+  }
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_debug_grouping(tt_emb_handle h, void* workspace, int64_t* uniq_keys, int32_t* uniq_digits,
+                                    int32_t* inv, int32_t* occ_start, int32_t* occ_pos, int32_t* pg_start,
+                                    int64_t* pg_keys, int64_t* counts, void* stream) {
+  if (!h || !workspace) return TT_EMB_EINVAL;
+  if (!h->g_valid || h->g_ws != workspace) return TT_EMB_EINVAL;
+  hipStream_t st = (hipStream_t)stream;
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  if (hipStreamSynchronize(st) != hipSuccess) return TT_EMB_EHIP;
+  int32_t c[8];
+  if (hipMemcpy(c, w.ctr, sizeof(c), hipMemcpyDeviceToHost) != hipSuccess) return TT_EMB_EHIP;
+  const int U = c[C_U], P = c[C_P], nv = c[C_NVALID];
+  if (counts) {
+    counts[0] = U;
+    counts[1] = P;
+    counts[2] = nv;
+    counts[3] = c[C_NSLICES];
+  }
+  const int64_t M = h->g_M;
+  bool ok = true;
+  if (uniq_keys && U > 0) {
+    uint32_t* tmp = new (std::nothrow) uint32_t[U];
+    if (!tmp) return TT_EMB_ENOMEM;
+    ok &= hipMemcpy(tmp, w.uniq_key, 4 * (size_t)U, hipMemcpyDeviceToHost) == hipSuccess;
+    for (int i = 0; i < U; ++i) uniq_keys[i] = tmp[i];
+    delete[] tmp;
+  }
+  if (uniq_digits && U > 0) {
+    // decoded on the device by the kernels' own key decoder, one digit at a time,
+    // into the radix buffer that the sort no longer needs
+    int32_t* scratch = reinterpret_cast<int32_t*>(w.sorted_keys == w.keys[0] ? w.keys[1] : w.keys[0]);
+    int32_t* tmp = new (std::nothrow) int32_t[U];
+    if (!tmp) return TT_EMB_ENOMEM;
+    for (int k = 0; k < 3 && ok; ++k) {
+      ok &= launch_debug_digits(h->s, w, scratch, U, k, st) == hipSuccess;
+      ok &= hipStreamSynchronize(st) == hipSuccess;
+      ok &= hipMemcpy(tmp, scratch, 4 * (size_t)U, hipMemcpyDeviceToHost) == hipSuccess;
+      for (int i = 0; i < U; ++i) uniq_digits[3 * i + k] = tmp[i];
+    }
+    delete[] tmp;
+  }
+  if (inv && M > 0) ok &= hipMemcpy(inv, w.inv, 4 * (size_t)M, hipMemcpyDeviceToHost) == hipSuccess;
+  if (occ_start) ok &= hipMemcpy(occ_start, w.occ_start, 4 * (size_t)(U + 1), hipMemcpyDeviceToHost) == hipSuccess;
+  if (occ_pos && nv > 0)
+    ok &= hipMemcpy(occ_pos, w.sorted_pos, 4 * (size_t)nv, hipMemcpyDeviceToHost) == hipSuccess;
+  if (pg_start) ok &= hipMemcpy(pg_start, w.pg_start, 4 * (size_t)(P + 1), hipMemcpyDeviceToHost) == hipSuccess;
+  if (pg_keys && P > 0) {
+    uint32_t* tmp = new (std::nothrow) uint32_t[P];
+    if (!tmp) return TT_EMB_ENOMEM;
+    ok &= hipMemcpy(tmp, w.pg_key, 4 * (size_t)P, hipMemcpyDeviceToHost) == hipSuccess;
+    for (int i = 0; i < P; ++i) pg_keys[i] = tmp[i];
+    delete[] tmp;
+  }
+  return ok ? TT_EMB_OK : TT_EMB_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,91 @@
+"""The C-ABI library loads on the CPU and exports every symbol the header declares;
+host-side argument checks reject bad calls before anything is launched."""
+import ctypes as C
+
+import pytest
+
+
+@pytest.fixture(scope="module")
+def N():
+    from paper_2609_03459_amd import _native
+
+    return _native
+
+
+def _desc(N, T=2, n=(3, 4, 5), d=(2, 2, 2), R=4, M=100, B=10, rows=None):
+    x = N.tt_emb_desc()
+    x.num_tables = T
+    x.num_rows = rows if rows is not None else n[0] * n[1] * n[2]
+    for k in range(3):
+        x.row_factors[k] = n[k]
+        x.dim_factors[k] = d[k]
+    x.rank = R
+    x.max_indices = M
+    x.max_bags = B
+    return x
+
+
+def test_every_header_symbol_is_exported(N):
+    names = N.header_symbols()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(N.lib, name), name
+
+
+def test_create_destroy_and_workspace(N):
+    h = N.tt_emb_create(_desc(N))
+    ws = N.tt_emb_workspace_size(h)
+    assert ws > 0 and ws % 256 == 0
+    h2 = N.tt_emb_create(_desc(N, M=1000))
+    assert N.tt_emb_workspace_size(h2) > ws
+    N.tt_emb_destroy(h)
+    N.tt_emb_destroy(h2)
+    assert N.lib.tt_emb_destroy(None) == N.TT_EMB_OK
+    assert N.status_string(N.TT_EMB_ERANGE).startswith("index")
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=0), 1), (dict(R=0), 1), (dict(n=(3, 0, 5)), 1), (dict(d=(1, -1, 1)), 1),
+    (dict(rows=61), 1), (dict(M=-1), 1),
+    (dict(R=65), 5), (dict(T=100, n=(1000, 1000, 100)), 5), (dict(d=(64, 64, 2)), 5),
+])
+def test_create_rejects_bad_shapes(N, kw, code):
+    h = C.c_void_p()
+    assert N.lib.tt_emb_create(C.byref(_desc(N, **kw)), C.byref(h)) == code
+    assert not h.value
+    assert N.lib.tt_emb_create(None, C.byref(h)) == N.TT_EMB_EINVAL
+
+
+def test_calls_reject_bad_arguments_without_launching(N):
+    h = N.tt_emb_create(_desc(N, T=2, M=100, B=10))
+    ws_bytes = N.tt_emb_workspace_size(h)
+    fake = 1 << 20  # aligned non-null addresses; nothing may be dereferenced
+    off = fake
+    E = N.TT_EMB_EINVAL
+    f = N.lib.tt_emb_forward
+    # null handle, null workspace, small workspace
+    assert f(None, fake, fake, fake, fake, 20, None, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake, 20, None, 10, fake, 0, None, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake, 20, None, 10, fake, 0, fake, ws_bytes - 1, None) == E
+    # NULL offsets require num_indices == T*B
+    assert f(h, fake, fake, fake, fake, 19, None, 10, fake, 0, fake, ws_bytes, None) == E
+    # beyond capacities
+    assert f(h, fake, fake, fake, fake, 101, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake, 20, off, 11, fake, 0, fake, ws_bytes, None) == E
+    # indices without bags
+    assert f(h, fake, fake, fake, fake, 5, off, 0, fake, 0, fake, ws_bytes, None) == E
+    # null cores / output, misaligned pointers
+    assert f(h, None, fake, fake, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake, 20, off, 10, None, 0, fake, ws_bytes, None) == E
+    assert f(h, fake + 4, fake, fake, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake + 4, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, fake, fake, fake, fake, 20, off, 10, fake, 0, fake + 64, ws_bytes, None) == E
+    # reuse of a grouping that was never made
+    assert f(h, fake, fake, fake, fake, 20, off, 10, fake, 1, fake, ws_bytes, None) == E
+    b = N.lib.tt_emb_backward
+    assert b(h, fake, fake, fake, fake, 20, off, 10, fake, None, fake, fake, 0, fake, ws_bytes, None) == E
+    assert b(h, fake, fake, fake, fake, 20, off, 10, fake, fake, fake, fake, 1, fake, ws_bytes, None) == E
+    assert N.lib.tt_emb_sgd(h, fake, fake, None, fake, fake, fake, C.c_float(0.1), None) == E
+    assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
+    assert N.lib.tt_emb_debug_grouping(h, fake, None, None, None, None, None, None, None, None, None) == E
+    N.tt_emb_destroy(h)

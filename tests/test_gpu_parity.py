@@ -1,0 +1,286 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer grouping outputs must match bit for bit; float outputs within the
+scaled-error bound of tests/_util.py.  Small cases compare every element;
+full-size workloads compare seeded samples the oracle computes one by one.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import ttgen
+from tests._util import TOL, abs_case, assert_close
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_03459_amd as P
+
+    return P
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _dev(case):
+    G = [torch.from_numpy(np.ascontiguousarray(case[k])).cuda() for k in ("G1", "G2", "G3")]
+    idx = torch.from_numpy(np.ascontiguousarray(case["idx"], dtype=np.int64)).cuda()
+    off = None if case["offsets"] is None else torch.from_numpy(np.ascontiguousarray(case["offsets"])).cuda()
+    return G, idx, off
+
+
+def _make(lib, case):
+    M = int(case["idx"].size)
+    return lib.TTEmbedding(case["T"], case["N"], case["n"], case["d"], case["R"], max_indices=max(M, 1),
+                           max_bags=max(int(case["B"]), 1))
+
+
+def gpu_forward(lib, case):
+    emb = _make(lib, case)
+    G, idx, off = _dev(case)
+    out = emb.forward(*G, idx, off, num_bags=case["B"])
+    torch.cuda.synchronize()
+    D = int(np.prod(case["d"]))
+    return out.cpu().numpy().reshape(case["T"] * case["B"], D), emb, G, idx, off
+
+
+def check_forward(lib, orc, case, bags=None, name=""):
+    _say(f"[fwd] {name} T={case['T']} n={case['n']} d={case['d']} R={case['R']} B={case['B']} "
+         f"M={case['idx'].size}")
+    V, emb, *_ = gpu_forward(lib, case)
+    assert emb.check_errors() == 0
+    ref, inv = orc.forward(case, bags=bags)
+    mag, _ = orc.forward(abs_case(case), bags=bags)
+    got = V if bags is None else V[bags]
+    return assert_close(f"forward {name}", got, ref, mag)
+
+
+TINY = [
+    dict(T=1, n=(3, 4, 5), d=(2, 3, 2), R=3, B=7, max_len=5),
+    dict(T=2, n=(2, 3, 7), d=(1, 2, 4), R=5, B=40, max_len=6),
+    dict(T=3, n=(1, 5, 2), d=(3, 1, 1), R=1, B=9, max_len=4),
+    dict(T=2, n=(7, 1, 3), d=(2, 2, 2), R=4, B=33, max_len=5),
+    dict(T=1, n=(50, 40, 30), d=(4, 4, 8), R=32, B=300, max_len=20, zipf=1.1),
+    dict(T=2, n=(20, 30, 40), d=(4, 4, 8), R=64, B=100, max_len=32, zipf=1.2),
+    dict(T=1, n=(100, 100, 100), d=(2, 2, 4), R=8, B=1000, single=True),
+    dict(T=2, n=(9, 11, 13), d=(3, 5, 7), R=17, B=50, max_len=9),
+    dict(T=4, n=(200, 200, 250), d=(4, 4, 4), R=16, B=512, single=True, zipf=1.05),
+]
+
+
+@pytest.mark.parametrize("k", range(len(TINY)))
+def test_forward_small(lib, orc, k):
+    c = dict(TINY[k])
+    case = ttgen.tiny(1000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    check_forward(lib, orc, case, name=f"tiny{k}")
+
+
+@pytest.mark.parametrize("k", [0, 1, 4, 5, 7])
+def test_grouping_bit_exact(lib, orc, k):
+    c = dict(TINY[k])
+    case = ttgen.tiny(2000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    _say(f"[group] tiny{k}")
+    emb = _make(lib, case)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    got = emb.debug_grouping(case["idx"].size)
+    ref = orc.grouping(case)
+    n = case["n"]
+    npad = n[0] * n[1] * n[2]
+    assert got["U"] == ref["U"] and got["P"] == ref["P"] and got["nvalid"] == ref["nvalid"]
+    assert np.array_equal(got["uniq_keys"], ref["uniq_t"] * npad + ref["uniq_g"])
+    assert np.array_equal(got["digits"], orc.digits(ref["uniq_g"], n).astype(np.int32))
+    assert np.array_equal(got["inv"], ref["inv"])
+    assert np.array_equal(got["occ_start"], ref["occ_start"])
+    assert np.array_equal(got["occ_pos"], ref["occ_pos"])
+    assert np.array_equal(got["pg_start"], ref["pg_start"])
+    assert np.array_equal(got["pg_keys"], ref["pg_t"] * (n[0] * n[1]) + ref["pg_q"])
+
+
+def _rank2_cores(n, d, R):
+    n1, n2, n3 = n
+    d1, d2, d3 = d
+    D = d1 * d2 * d3
+    G1 = np.zeros((1, n1, d1, R), np.float32)
+    G2 = np.zeros((1, n2, R, d2, R), np.float32)
+    G3 = np.zeros((1, n3, R, d3), np.float32)
+    G1[0, :, :, 0] = (np.arange(n1)[:, None] * n2 * n3 * D + np.arange(d1)[None, :] * d2 * d3)
+    G1[0, :, :, 1] = 1
+    G2[0, :, 0, :, 0] = 1
+    G2[0, :, 1, :, 0] = np.arange(n2)[:, None] * n3 * D + np.arange(d2)[None, :] * d3
+    G2[0, :, 1, :, 1] = 1
+    G3[0, :, 0, :] = 1
+    G3[0, :, 1, :] = np.arange(n3)[:, None] * D + np.arange(d3)[None, :]
+    return G1, G2, G3
+
+
+def test_rank2_closed_form_bit_exact_config1_shape(lib):
+    # E[g][j] = g*D + j exactly in fp32 while N*D < 2^24 (1e6 rows, D = 16)
+    case = ttgen.make(1)
+    case["G1"], case["G2"], case["G3"] = _rank2_cores(case["n"], case["d"], case["R"])
+    _say("[fwd] rank-2 closed form, 1e6 x 16, R=8")
+    V, emb, *_ = gpu_forward(lib, case)
+    D = 16
+    ref = case["idx"][:, None].astype(np.float64) * D + np.arange(D)[None, :]
+    assert np.array_equal(V.astype(np.float64), ref)
+
+
+def test_full_config1(lib, orc):
+    check_forward(lib, orc, ttgen.make(1), name="config1 full")
+
+
+def test_full_config2(lib, orc):
+    check_forward(lib, orc, ttgen.make(2), name="config2 full")
+
+
+def test_config3_small_batch(lib, orc):
+    check_forward(lib, orc, ttgen.make(3, bags=256), name="config3 B=256")
+
+
+def test_config4_small_batch(lib, orc):
+    check_forward(lib, orc, ttgen.make(4, bags=128), name="config4 B=128")
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_full_size_sampled_bags(lib, orc, cfg):
+    case = ttgen.make(cfg)
+    bags = ttgen.sample_bags(cfg, case["T"], case["B"], 96)
+    check_forward(lib, orc, case, bags=bags, name=f"config{cfg} full, 96 sampled bags")
+
+
+def test_forward_deterministic(lib):
+    case = ttgen.make(3, bags=512)
+    _say("[fwd] determinism config3 B=512")
+    V1, *_ = gpu_forward(lib, case)
+    V2, *_ = gpu_forward(lib, case)
+    assert np.array_equal(V1, V2)
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+def _edge(kind):
+    case = ttgen.tiny(77, 2, (6, 5, 100), (2, 2, 2), 4, B=40, max_len=8, zipf=1.1)
+    idx = case["idx"].copy()
+    rng = np.random.default_rng(5)
+    n3 = 100
+    if kind == "all_equal":
+        idx[:] = 1234
+    elif kind == "one_prefix":
+        idx = 7 * n3 + rng.integers(0, n3, idx.size)  # one (i1, i2) group, up to 100 rows: several slices
+    elif kind == "distinct_prefixes":
+        q = rng.permutation(30)[: min(30, idx.size)]
+        idx = (np.resize(q, idx.size) * n3 + rng.integers(0, n3, idx.size)).astype(np.int64)
+    case["idx"] = idx.astype(np.int64)
+    return case
+
+
+@pytest.mark.parametrize("kind", ["all_equal", "one_prefix", "distinct_prefixes"])
+def test_edge_index_patterns(lib, orc, kind):
+    check_forward(lib, orc, _edge(kind), name=kind)
+
+
+def test_edge_empty_and_single_bag(lib, orc):
+    case = ttgen.tiny(8, 2, (3, 4, 5), (2, 2, 2), 3, B=6, max_len=0)  # every bag empty, no indices
+    assert case["idx"].size == 0
+    _say("[fwd] all bags empty")
+    V, *_ = gpu_forward(lib, case)
+    assert np.array_equal(V, np.zeros_like(V))
+    check_forward(lib, orc, ttgen.tiny(9, 3, (3, 4, 5), (2, 2, 2), 3, B=1, max_len=7, empty_bags=False),
+                  name="B=1")
+
+
+def test_invalid_indices_flagged_and_skipped(lib, orc):
+    case = ttgen.tiny(10, 2, (4, 5, 6), (2, 2, 2), 3, B=30, max_len=6, N=100)
+    idx = case["idx"].copy()
+    idx[::5] = 100  # == N: first invalid row
+    idx[1::7] = -2
+    case["idx"] = idx
+    _say("[fwd] invalid indices")
+    V, emb, *_ = gpu_forward(lib, case)
+    assert emb.check_errors() == 4  # TT_EMB_ERANGE
+    assert emb.check_errors() == 0  # cleared
+    ref, ninv = orc.forward(case)
+    assert ninv > 0
+    mag, _ = orc.forward(abs_case(case))
+    assert_close("forward with invalid", V, ref, mag)
+
+
+# ---------------------------------------------------------------------------
+# backward and SGD
+# ---------------------------------------------------------------------------
+def gpu_train(lib, case):
+    V, emb, G, idx, off = gpu_forward(lib, case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    grads = emb.backward(*G, idx, off, dV, num_bags=case["B"], reuse_grouping=True)
+    torch.cuda.synchronize()
+    return emb, G, grads, dV
+
+
+def check_backward(lib, orc, case, name="", want=None):
+    _say(f"[bwd] {name} T={case['T']} n={case['n']} d={case['d']} R={case['R']} B={case['B']} "
+         f"M={case['idx'].size}")
+    emb, G, grads, dV = gpu_train(lib, case)
+    ref = orc.backward(case, want=want)[:3]
+    mag = orc.backward(abs_case(case), want=want)[:3]
+    for k in range(3):
+        got = grads[k].cpu().numpy()
+        if want is None:
+            assert_close(f"dG{k + 1} {name}", got, ref[k], mag[k])
+        else:
+            sel = np.flatnonzero(want[k])
+            T = case["T"]
+            g = got.reshape(T * got.shape[1], -1)[sel]
+            r = ref[k].reshape(T * ref[k].shape[1], -1)[sel]
+            m = mag[k].reshape(T * mag[k].shape[1], -1)[sel]
+            assert_close(f"dG{k + 1} {name} (sampled slices)", g, r, m)
+    return emb, G, grads, ref, mag
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4, 5, 7])
+def test_backward_small(lib, orc, k):
+    c = dict(TINY[k])
+    case = ttgen.tiny(3000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    check_backward(lib, orc, case, name=f"tiny{k}")
+
+
+def test_backward_config5_small_batch(lib, orc):
+    check_backward(lib, orc, ttgen.make(5, bags=64), name="config5 B=64")
+
+
+def test_backward_config5_full_sampled_slices(lib, orc):
+    case = ttgen.make(5)
+    T, n = case["T"], case["n"]
+    rng = np.random.default_rng(17)
+    want = []
+    for k in range(3):
+        m = np.zeros(T * n[k], np.uint8)
+        for t in (0, T - 1):
+            m[t * n[k] + rng.integers(0, n[k])] = 1
+        want.append(m)
+    check_backward(lib, orc, case, name="config5 full", want=want)
+
+
+def test_sgd_step(lib, orc):
+    case = ttgen.make(5, bags=32)
+    _say("[sgd] config5 B=32")
+    emb, G, grads, dV = gpu_train(lib, case)
+    lr = case["lr"]
+    emb.sgd(*G, *grads, lr)
+    torch.cuda.synchronize()
+    ref = orc.backward(case)[:3]
+    mag = orc.backward(abs_case(case))[:3]
+    for k, name in enumerate(("G1", "G2", "G3")):
+        new = G[k].cpu().numpy().astype(np.float64)
+        exp = orc.sgd(case[name], ref[k], lr)
+        # gradient error scaled by lr plus one fp32 rounding of the updated value
+        bound = TOL * lr * mag[k] + 2.0 ** -23 * np.abs(exp)
+        assert np.all(np.abs(new - exp) <= bound + 1e-30), name
