@@ -74,20 +74,23 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
   }
 }
 
-// rows whose occurrences span several chunks: first chunk's tail partial plus
-// the head partials of every following chunk, in chunk order
-__global__ void __launch_bounds__(64) k_seg_fix(const int32_t* __restrict__ occ_start, const int32_t* __restrict__ ctr,
+// Rows whose occurrences span several chunks: chunk c0 + 1, where c0 holds the
+// row's first occurrence, finishes the row from c0's tail partial and the head
+// partials of every following chunk, in chunk order.  One wave per chunk.
+__global__ void __launch_bounds__(64) k_seg_fix(const int32_t* __restrict__ sorted_uid,
+                                                const int32_t* __restrict__ occ_start, const int32_t* __restrict__ ctr,
                                                 int D, const float* __restrict__ part, float* __restrict__ dE) {
-  const int U = ctr[C_U];
-  for (int u = blockIdx.x; u < U; u += gridDim.x) {
-    const int lo = occ_start[u], hi = occ_start[u + 1];
-    const int c0 = lo / SEG_CHUNK, c1 = (hi - 1) / SEG_CHUNK;
-    if (c0 == c1) continue;
-    for (int j = lane_id(); j < D; j += 64) {
-      float acc = part[((int64_t)c0 * 2 + 1) * D + j];
-      for (int c = c0 + 1; c <= c1; ++c) acc += part[((int64_t)c * 2 + 0) * D + j];
-      dE[(int64_t)u * D + j] = acc;
-    }
+  const int nvalid = ctr[C_NVALID];
+  const int c = blockIdx.x;
+  if (c == 0 || c * SEG_CHUNK >= nvalid) return;
+  const int u = sorted_uid[c * SEG_CHUNK];
+  const int lo = occ_start[u], hi = occ_start[u + 1];
+  const int c0 = lo / SEG_CHUNK, c1 = (hi - 1) / SEG_CHUNK;
+  if (c0 != c - 1) return;
+  for (int j = lane_id(); j < D; j += 64) {
+    float acc = part[((int64_t)c0 * 2 + 1) * D + j];
+    for (int k = c0 + 1; k <= c1; ++k) acc += part[((int64_t)k * 2 + 0) * D + j];
+    dE[(int64_t)u * D + j] = acc;
   }
 }
 
@@ -119,7 +122,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
   int cur_pg = -1;
   const int rows12 = s.d1 * s.d2;
   while (true) {
-    int c = claim_chunk(ctr + C_BWD_CTR, nchunks, &victim, &s_chunk);
+    int c = claim_chunk(ctr + C_BWD_CTR, ctr + C_BWD_STEAL, nchunks, &victim, &s_chunk);
     if (c < 0) break;
     const int s0 = c * BWD_CHUNK;
     const int s1 = s0 + BWD_CHUNK < nsl ? s0 + BWD_CHUNK : nsl;
@@ -204,10 +207,11 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   prof_end(prof, K_SEG_SUM, st);
-  hipLaunchKernelGGL(k_seg_fix, dim3(2048), dim3(64), 0, st, (const int32_t*)w.occ_start, (const int32_t*)w.ctr, s.D,
-                     (const float*)w.seg_part, dE);
+  hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(64), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
+                     (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid, 0u, st)) != hipSuccess) return e;
+  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_STEAL), 1, 0u, st)) != hipSuccess) return e;
   const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D);
   if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
       hipSuccess)

@@ -31,6 +31,8 @@ enum : int {
   C_NSLICES = 3,  // work slices of the fused kernels
   C_ERR = 4,      // sticky error bits
   C_NSEG = 5,     // occurrence chunks of the dE segment sums
+  C_FWD_STEAL = 6,  // chunks claimed so far by the schedulers
+  C_BWD_STEAL = 7,
   C_FWD_CTR = 64, // per-workgroup claim counters of the forward scheduler
   C_BWD_CTR = 64 + 4096,
   C_TOTAL = 64 + 2 * 4096,
@@ -155,30 +157,75 @@ __device__ __forceinline__ T block_excl_scan(T v, T* smem, T* total) {
 
 namespace ttemb {
 
-// Persistent-thread scheduler with chunked work stealing (FlowTT Section 3.4):
-// the chunk list is split evenly over the resident workgroups; workgroup w
-// first claims chunks of its own share through its counter ctrs[w], then
-// steals the remaining chunks of the other shares, visiting victims w+1,
-// w+2, ... in turn.  Returns the next chunk or -1 once every share is
-// exhausted.  Called by all threads of the block; one thread claims.
-__device__ __forceinline__ int claim_chunk(int32_t* ctrs, int nchunks, int* victim_state, int* s_chunk) {
-  const int W = gridDim.x, w = blockIdx.x;
-  if (threadIdx.x == 0) {
+// Persistent-thread scheduler with chunked work stealing (FlowTT Section 3.4).
+// The chunk list is split evenly over the workers; worker w first claims the
+// chunks of its own share through its counter ctrs[w] (consecutive chunks, so
+// B = G2[i2] and C stay on chip).  Then it steals: one wave reads the
+// counters of 64 victims at a time (w+1, w+2, ... cyclically) with plain
+// loads, and claims with an atomic only from victims that still show work.
+// `cursor` remembers how far the scan got, so exhausted victims are never
+// revisited.  *claimed counts claimed chunks; once it reaches the total,
+// every idle worker exits at once.  A claim takes at most W/64 rounds.
+__device__ __forceinline__ int share_lo(int nchunks, int W, int v) { return (int)(((int64_t)nchunks * v) / W); }
+
+__device__ __forceinline__ int claim_chunk_wave(int32_t* ctrs, int32_t* claimed, int nchunks, int W, int me,
+                                                int* cursor) {
+  const int lane = lane_id();
+  if (*cursor == 0) {
     int c = -1;
-    int k = *victim_state;
-    while (k < W) {
-      int v = w + k;
-      if (v >= W) v -= W;
-      int lo = (int)(((int64_t)nchunks * v) / W), hi = (int)(((int64_t)nchunks * (v + 1)) / W);
-      int got = atomicAdd(&ctrs[v], 1);
-      if (lo + got < hi) {
-        c = lo + got;
-        break;
+    if (lane == 0) {
+      const int got = atomicAdd(&ctrs[me], 1);
+      if (share_lo(nchunks, W, me) + got < share_lo(nchunks, W, me + 1)) {
+        c = share_lo(nchunks, W, me) + got;
+        atomicAdd(claimed, 1);
       }
-      ++k;
     }
-    *victim_state = k;
-    *s_chunk = c;
+    c = __shfl(c, 0, 64);
+    if (c >= 0) return c;
+    *cursor = 1;
+  }
+  while (*cursor < W) {
+    if (__hip_atomic_load(claimed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nchunks) {
+      *cursor = W;
+      break;
+    }
+    const int k = *cursor + lane;
+    int v = me + k;
+    if (v >= W) v -= W;
+    bool has = false;
+    if (k < W) {
+      const int used = __hip_atomic_load(&ctrs[v], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      has = share_lo(nchunks, W, v) + used < share_lo(nchunks, W, v + 1);
+    }
+    uint64_t m = __ballot(has);
+    while (m) {
+      const int f = __ffsll((unsigned long long)m) - 1;
+      const int vf = __shfl(v, f, 64);
+      int c = -1;
+      if (lane == 0) {
+        const int got = atomicAdd(&ctrs[vf], 1);
+        if (share_lo(nchunks, W, vf) + got < share_lo(nchunks, W, vf + 1)) {
+          c = share_lo(nchunks, W, vf) + got;
+          atomicAdd(claimed, 1);
+        }
+      }
+      c = __shfl(c, 0, 64);
+      if (c >= 0) {
+        *cursor += f;  // this victim may hold more
+        return c;
+      }
+      m &= m - 1;
+    }
+    *cursor += 64;
+  }
+  return -1;
+}
+
+// Block-level worker: wave 0 claims for the block.
+__device__ __forceinline__ int claim_chunk(int32_t* ctrs, int32_t* claimed, int nchunks, int* cursor, int* s_chunk) {
+  if (threadIdx.x < 64) {
+    const int c = claim_chunk_wave(ctrs, claimed, nchunks, gridDim.x, blockIdx.x, cursor);
+    if (threadIdx.x == 0) *s_chunk = c;
   }
   __syncthreads();
   int c = *s_chunk;
@@ -212,5 +259,20 @@ __device__ __forceinline__ Digits decode_key(uint32_t key, uint32_t Npad, int n2
 }
 
 hipError_t launch_debug_digits(const Shape& s, const Work& w, int32_t* out, int U, int which, hipStream_t st);
+
+}  // namespace ttemb
+
+namespace ttemb {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Orders this wave's LDS writes before its later LDS reads of other lanes'
+// data (a wave's LDS requests complete in order; this keeps the compiler
+// from reordering across the exchange and waits for outstanding writes).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 }  // namespace ttemb
