@@ -11,7 +11,9 @@
 namespace ttemb {
 
 ShapeArgs shape_args(const Shape& s);
-int persistent_grid();
+bool bwd_r32_supported(const Shape& s);
+hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                          float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // dE segment sums over the sorted occurrences
@@ -196,9 +198,12 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int64_t n2s = (int64_t)s.T * s.n2 * s.R * s.d2 * s.R;
   const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
   hipError_t e;
-  if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
-  if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
-  if ((e = fill_f32(dG3, n3s, 0.f, st)) != hipSuccess) return e;
+  const bool fast = bwd_r32_supported(s);
+  if (!fast || M <= 0) {
+    if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
+    if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
+    if ((e = fill_f32(dG3, n3s, 0.f, st)) != hipSuccess) return e;
+  }
   if (M <= 0) return hipSuccess;
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
@@ -209,6 +214,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   prof_end(prof, K_SEG_SUM, st);
   hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(64), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
+  if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, prof, st);
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid, 0u, st)) != hipSuccess) return e;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_STEAL), 1, 0u, st)) != hipSuccess) return e;

@@ -1,0 +1,284 @@
+// Backward pass for d = (4, 4, 8), R = 32 (D = 128) on MFMA (FlowTT Section 3.2, Eq. 1).
+//
+// Work is split by table t and by half h of the rank index b of the last
+// core (b = 16 h + b'), so each (t, h) owner does its half of every product
+// exactly once and keeps its half of dG3[t] (n3 x 16 x 8 floats) in LDS:
+//   C_h   = A . B_h                 (4 x 64 per group; B_h = G2[i2][:, :, 16h:16h+16])
+//   dD_h  = C_h^T . dE_u            -> LDS accumulator of dG3[t][i3][16h + b'][j3]
+//   dC_h  = dE_u . D_{u,h}^T, summed over the group's rows into dC_h
+//   dB_h += A^T . dC_h              (32 x 64, summed over the chunk's groups)
+//   dA_h  = dC_h . B_h^T            (4 x 32, half of the sum over (j2, b))
+// A chunk is up to 32 slices of one (t, i2) run, processed four at a time
+// ("quads") so stage 1 and dA use 16-row MFMA tiles.  dB_h of a chunk and
+// dA_h of a slice go to scratch; three small kernels finish dG1, dG2 and dG3
+// by fixed-order segment sums.  Workgroup blockIdx % (2T) owns (t, h), so
+// with T = 8 every table lives on one XCD (blockIdx % 8).
+#include "common.h"
+
+namespace ttemb {
+
+ShapeArgs shape_args(const Shape& s);
+
+constexpr int BW_WAVES = 8;
+constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
+
+__global__ void __launch_bounds__(64 * BW_WAVES, 1)
+    k_bwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
+              const float* __restrict__ dE, const int4* __restrict__ slices, const int4* __restrict__ chunks,
+              const uint32_t* __restrict__ run_base, const uint32_t* __restrict__ uniq_key, int32_t* __restrict__ ctr,
+              float* __restrict__ dApart, float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap,
+              int nch_cap) {
+  extern __shared__ float lds[];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int acc_n = s.n3 * 128;
+  float* g3acc = lds;  // [n3][16][8]
+  float* scr = lds + acc_n + wave * BW_SCR;
+  const int nq = 2 * s.T;
+  const int q = blockIdx.x % nq;
+  const int t = q % s.T, h = q / s.T;
+  const int per_q = gridDim.x / nq;
+  const int me = (blockIdx.x / nq) * BW_WAVES + wave;
+  const int nworkers = per_q * BW_WAVES;
+  int32_t* qctr = ctr + C_BWD_CTR + q * nworkers;
+  int32_t* qclaimed = ctr + C_BWD_CTR + gridDim.x * BW_WAVES + q;
+
+  for (int i = threadIdx.x; i < acc_n; i += blockDim.x) g3acc[i] = 0.f;
+  __syncthreads();
+
+  const int c_lo = (int)run_base[t * s.n2], c_hi = (int)run_base[(t + 1) * s.n2];
+  const int nch = c_hi - c_lo;
+  const int l15 = lane & 15, l4 = lane >> 4;
+  int cursor = 0;
+  int cur_run = -1;
+  float Bop[32];   // stage-1 B operand  B_h[a = 4s + l4][16 nt + l15]       (s, nt) -> 4 s + nt
+  while (true) {
+    const int c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
+    if (c < 0) break;
+    const int4 ch = chunks[c_lo + c];
+    const int f = ch.x, ns = ch.y, run = ch.z;
+    if (run != cur_run) {
+      const float* Bg = G2 + (int64_t)run * 4096;
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) Bop[4 * s4 + nt] = Bg[((4 * s4 + l4) * 4 + nt) * 32 + 16 * h + l15];
+      cur_run = run;
+    }
+    f32x4 dB[8];  // (mt, nt) -> 4 mt + nt
+#pragma unroll
+    for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int qd = 0; qd < ns; qd += 4) {
+      const int nqs = ns - qd < 4 ? ns - qd : 4;
+      int4 sd = make_int4(0, 0, 0, 0);
+      if (lane < nqs) sd = slices[f + qd + lane];
+      // i1 of each slice of the quad (lane j holds slice j)
+      int my_i1 = 0;
+      if (lane < nqs) my_i1 = (int)(((uint32_t)sd.w % (uint32_t)s.n12) / (uint32_t)s.n2);
+      // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
+      const int aj = l15 >> 2;
+      const int aj_i1 = __shfl(my_i1, aj, 64);
+      const bool aj_ok = aj < nqs;
+      const float* Ag = G1 + ((int64_t)(t * s.n1 + aj_i1) * 4 + (lane & 3)) * 32;
+      float Aop[8];
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = aj_ok ? Ag[4 * s4 + l4] : 0.f;
+      f32x4 Cs[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+          Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[s4], Bop[4 * s4 + nt], Cs[nt], 0, 0, 0);
+      // lane holds C_h[slice l4][j1 r][j2 nt][b' l15]; scratch layout [slice][j1][j2][b']
+      wave_lds_sync();
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) scr[((l4 * 4 + r) * 4 + nt) * 16 + l15] = Cs[nt][r];
+      wave_lds_sync();
+
+      for (int j = 0; j < nqs; ++j) {
+        const int rb = __shfl(sd.y, j, 64), re = __shfl(sd.z, j, 64);
+        const int i1 = __shfl(my_i1, j, 64);
+        const int nr = re - rb;
+        // dD A operand: C_h^T[b' = l15][(j1 j2) = 4 s + l4] = C_h[j][s][l4][l15]
+        float CT[4];
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[((j * 4 + s4) * 4 + l4) * 16 + l15];
+        const uint32_t ukey = lane < nr ? uniq_key[rb + lane] : 0u;
+        f32x4 dC = {0.f, 0.f, 0.f, 0.f};
+        const int rowsel = l15 >> 3;
+        for (int r0 = 0; r0 < nr; r0 += 2) {
+          const bool has1 = r0 + 1 < nr;
+          const int mine = r0 + (rowsel && has1 ? 1 : 0);
+          const bool live = !rowsel || has1;
+          const int i3m = decode_key((uint32_t)__shfl((int)ukey, mine, 64), s.Npad, s.n2, s.n3).i3;
+          const float* Em = dE + (int64_t)(rb + mine) * 128;
+          float EB[4];
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) EB[s4] = live ? Em[(4 * s4 + l4) * 8 + (lane & 7)] : 0.f;
+          f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], EB[s4], dd, 0, 0, 0);
+          // dd: lane holds dD_h[b' = 4 l4 + r][row rowsel][j3 = lane & 7]
+          if (live) {
+            float* gp = g3acc + i3m * 128 + (4 * l4) * 8 + (lane & 7);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) atomicAdd(gp + r * 8, dd[r]);
+          }
+          // dC_h += dE_u . D_{u,h}^T for each row of the pair (a missing second row adds zeros)
+          const int u1 = has1 ? r0 + 1 : r0;
+          const int i3a = decode_key((uint32_t)__shfl((int)ukey, r0, 64), s.Npad, s.n2, s.n3).i3;
+          const int i3b = decode_key((uint32_t)__shfl((int)ukey, u1, 64), s.Npad, s.n2, s.n3).i3;
+          const float* Ea = dE + (int64_t)(rb + r0) * 128 + l15 * 8 + l4;
+          const float* Eb = dE + (int64_t)(rb + u1) * 128 + l15 * 8 + l4;
+          const float* Da = G3 + ((int64_t)(t * s.n3 + i3a) * 32 + 16 * h + l15) * 8 + l4;
+          const float* Db = G3 + ((int64_t)(t * s.n3 + i3b) * 32 + 16 * h + l15) * 8 + l4;
+          const float ea0 = Ea[0], ea1 = Ea[4], da0 = Da[0], da1 = Da[4];
+          const float eb0 = has1 ? Eb[0] : 0.f, eb1 = has1 ? Eb[4] : 0.f, db0 = Db[0], db1 = Db[4];
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ea0, da0, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ea1, da1, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(eb0, db0, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(eb1, db1, dC, 0, 0, 0);
+        }
+        // dC: lane holds dC_h[j1 = l4][j2 = r][b' = l15]
+        // dB_h += A^T . dC_h  (M = a, N = (j2, b'), K = j1)
+        const float* Aj = G1 + ((int64_t)(t * s.n1 + i1) * 4 + l4) * 32 + l15;
+        const float AT0 = Aj[0], AT1 = Aj[16];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          dB[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT0, dC[nt], dB[nt], 0, 0, 0);
+          dB[4 + nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT1, dC[nt], dB[4 + nt], 0, 0, 0);
+        }
+        // keep dC_h of slice j for the quad's dA: slot j, layout [j1][j2][b']
+        wave_lds_sync();
+#pragma unroll
+        for (int r = 0; r < 4; ++r) scr[((j * 4 + l4) * 4 + r) * 16 + l15] = dC[r];
+      }
+      wave_lds_sync();
+      // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32); B operand
+      // B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15] read from G2 (L1/L2)
+      const int ms = l15 >> 2, mj1 = lane & 3;
+      const bool m_ok = ms < nqs;
+      const float* Bg = G2 + (int64_t)run * 4096 + 16 * h;
+      f32x4 dA[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int s2 = 0; s2 < 16; ++s2) {
+        const int k = 4 * s2 + l4;
+        const float av = m_ok ? scr[((ms * 4 + mj1) * 4 + (k >> 4)) * 16 + (k & 15)] : 0.f;
+        const float b0 = Bg[(l15 * 4 + (k >> 4)) * 32 + (k & 15)];
+        const float b1 = Bg[((16 + l15) * 4 + (k >> 4)) * 32 + (k & 15)];
+        dA[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b0, dA[0], 0, 0, 0);
+        dA[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b1, dA[1], 0, 0, 0);
+      }
+      // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]
+      if (l4 < nqs) {
+        float* dst = dApart + ((int64_t)h * nsl_cap + (f + qd + l4)) * 128 + l15;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          dst[r * 32] = dA[0][r];
+          dst[r * 32 + 16] = dA[1][r];
+        }
+      }
+      wave_lds_sync();
+    }
+    // dB_h partial of this chunk: lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
+    float* dst = dBpart + ((int64_t)h * nch_cap + (c_lo + c)) * 2048;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
+  }
+  __syncthreads();
+  float* gdst = g3part + (int64_t)blockIdx.x * acc_n;
+  for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
+}
+
+// dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2)
+__global__ void __launch_bounds__(128) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
+                                                   const uint32_t* __restrict__ dense_base,
+                                                   const float* __restrict__ dApart, int nsl_cap,
+                                                   float* __restrict__ dG1) {
+  const int ti1 = blockIdx.x;  // t * n1 + i1
+  const int t = ti1 / s.n1, i1 = ti1 % s.n1;
+  const int e = threadIdx.x;
+  float acc = 0.f;
+  for (int i2 = 0; i2 < s.n2; ++i2) {
+    const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
+    const uint32_t cnt = dense_cnt[slot];
+    if (!cnt) continue;
+    const uint32_t b = dense_base[slot];
+    for (uint32_t k = 0; k < cnt; ++k) {
+      acc += dApart[((int64_t)0 * nsl_cap + b + k) * 128 + e];
+      acc += dApart[((int64_t)1 * nsl_cap + b + k) * 128 + e];
+    }
+  }
+  dG1[(int64_t)ti1 * 128 + e] = acc;
+}
+
+// dG2[t][i2][a][j2][16 h + b'] = sum of the chunk partials of run (t, i2), half h
+__global__ void __launch_bounds__(256) k_reduce_g2(const uint32_t* __restrict__ run_base,
+                                                   const float* __restrict__ dBpart, int nch_cap,
+                                                   float* __restrict__ dG2) {
+  const int run = blockIdx.x >> 1, h = blockIdx.x & 1;
+  const int c0 = (int)run_base[run], c1 = (int)run_base[run + 1];
+  for (int e = threadIdx.x; e < 2048; e += 256) {
+    float acc = 0.f;
+    for (int c = c0; c < c1; ++c) acc += dBpart[((int64_t)h * nch_cap + c) * 2048 + e];
+    const int a = e >> 6, j2 = (e >> 4) & 3, bp = e & 15;
+    dG2[(int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp] = acc;
+  }
+}
+
+// dG3[t][i3][16 h + b'][j3] = sum over the workgroups that owned (t, h)
+__global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __restrict__ g3part, int nwg,
+                                                   float* __restrict__ dG3) {
+  const int nq = 2 * s.T;
+  const int q = blockIdx.y;
+  const int t = q % s.T, h = q / s.T;
+  const int acc_n = s.n3 * 128;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= acc_n) return;
+  float acc = 0.f;
+  for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
+  const int i3 = e >> 7, bp = (e >> 3) & 15, j3 = e & 7;
+  dG3[(((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3] = acc;
+}
+
+bool bwd_r32_supported(const Shape& s) {
+  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64;
+}
+
+hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                          float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st) {
+  const int nq = 2 * s.T;
+  int per_q = persistent_grid() / nq;
+  if (per_q < 1) per_q = 1;
+  const int grid = nq * per_q;
+  if (grid > MAX_BWD_WG || grid * BW_WAVES + nq > MAX_PERSIST_WG) return hipErrorInvalidValue;
+  hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid * BW_WAVES + nq, 0u, st);
+  if (e != hipSuccess) return e;
+  const size_t lds = sizeof(float) * ((size_t)s.n3 * 128 + BW_WAVES * BW_SCR);
+  e = hipFuncSetAttribute((const void*)k_bwd_r32, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  prof_begin(prof, K_BWD_FUSED, st);
+  hipLaunchKernelGGL(k_bwd_r32, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
+                     (const float*)w.E, (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                     (const uint32_t*)w.uniq_key, w.ctr, w.dApart, w.dBpart, w.g3part, (int)w.nsl_max,
+                     (int)w.nch_max);
+  prof_end(prof, K_BWD_FUSED, st);
+  hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(128), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
+                     (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1);
+  hipLaunchKernelGGL(k_reduce_g2, dim3(s.T * s.n2 * 2), dim3(256), 0, st, (const uint32_t*)w.run_nch,
+                     (const float*)w.dBpart, (int)w.nch_max, dG2);
+  hipLaunchKernelGGL(k_reduce_g3, dim3((s.n3 * 128 + 255) / 256, nq), dim3(256), 0, st, shape_args(s),
+                     (const float*)w.g3part, grid, dG3);
+  return hipGetLastError();
+}
+
+}  // namespace ttemb

@@ -33,8 +33,10 @@ enum : int {
   C_NSEG = 5,     // occurrence chunks of the dE segment sums
   C_FWD_STEAL = 6,  // chunks claimed so far by the schedulers
   C_BWD_STEAL = 7,
-  C_FWD_CTR = 64, // per-workgroup claim counters of the forward scheduler
-  C_BWD_CTR = 64 + 4096,
+  C_NCHUNKS = 8,    // chunks of the specialised kernels
+  C_BWD_CLAIMED = 16,  // [16] claimed chunks per backward queue
+  C_FWD_CTR = 64, // per-worker claim counters of the forward scheduler
+  C_BWD_CTR = 64 + 4096,  // per-worker counters of the backward, then claimed counts
   C_TOTAL = 64 + 2 * 4096,
 };
 enum : int { ERR_INDEX = 1, ERR_OFFSETS = 2 };
@@ -49,8 +51,10 @@ constexpr int SCAN_THREADS = 256;
 constexpr int SCAN_ITEMS = 16;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
 constexpr int SLICE_ROWS = 32;   // unique rows per work slice
+constexpr int CHUNK_SLICES = 32; // slices per chunk of the specialised kernels (one (t, i2) run)
 constexpr int SEG_CHUNK = 256;   // sorted occurrences per dE chunk
 constexpr int MAX_PERSIST_WG = 4096;
+constexpr int MAX_BWD_WG = 1024;
 
 // Device pointers carved out of the caller's workspace.
 struct Work {
@@ -72,7 +76,13 @@ struct Work {
   uint32_t* dense_cnt;    // [ndense] slices per prefix slot, (t, i2, i1) order
   uint32_t* dense_base;   // [ndense] exclusive scan of dense_cnt
   int32_t* dense_pg;      // [ndense] group id per slot
-  int4* slices;           // [M] (group, row_begin, row_end, key)
+  int4* slices;           // [nsl_max] (group, row_begin, row_end, key)
+  uint32_t* run_nch;      // [T*n2 + 1] chunks per (t, i2) run, then their exclusive scan
+  int4* chunks;           // [nch_max] (first slice, slice count, run, 0)
+  float* dApart;          // [2][nsl_max][d1*R] backward: dA of each slice, per rank half
+  float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
+  float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
+  int64_t nsl_max, nch_max;
   float* E;               // [M][D] rows of the forward, dE rows in the backward
   float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
   uint32_t* sorted_keys;  // = keys[x] after the sort

@@ -414,6 +414,35 @@ __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint
   }
 }
 
+// chunks of the specialised kernels: up to CHUNK_SLICES consecutive slices of
+// one (t, i2) run; run r covers slices [dense_base[r*n1], dense_base[(r+1)*n1])
+__global__ void k_run_counts(const uint32_t* __restrict__ dense_base, const int32_t* __restrict__ ctr, int nruns,
+                             int n1, uint32_t* __restrict__ run_nch) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r > nruns) return;
+  if (r == nruns) {  // the scan turns this slot into the total
+    run_nch[r] = 0;
+    return;
+  }
+  const uint32_t b0 = dense_base[(int64_t)r * n1];
+  const uint32_t b1 = r + 1 < nruns ? dense_base[(int64_t)(r + 1) * n1] : (uint32_t)ctr[C_NSLICES];
+  run_nch[r] = (b1 - b0 + CHUNK_SLICES - 1) / CHUNK_SLICES;
+}
+
+__global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uint32_t* __restrict__ run_base,
+                              const int32_t* __restrict__ ctr, int nruns, int n1, int4* __restrict__ chunks) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= nruns) return;
+  const uint32_t b0 = dense_base[(int64_t)r * n1];
+  const uint32_t b1 = r + 1 < nruns ? dense_base[(int64_t)(r + 1) * n1] : (uint32_t)ctr[C_NSLICES];
+  const uint32_t c0 = run_base[r];
+  for (uint32_t k = 0; b0 + k * CHUNK_SLICES < b1; ++k) {
+    const uint32_t f = b0 + k * CHUNK_SLICES;
+    const uint32_t n = b1 - f < (uint32_t)CHUNK_SLICES ? b1 - f : (uint32_t)CHUNK_SLICES;
+    chunks[c0 + k] = make_int4((int)f, (int)n, r, 0);
+  }
+}
+
 __global__ void k_group_init(int32_t* ctr, int32_t* occ_start, int32_t* pg_start, uint32_t* rtotals,
                              int nrtotals) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -480,6 +509,14 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
                      (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
                      s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, w.slices);
+  const int nruns = s.T * s.n2;
+  hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
+                     (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
+  // exclusive scan in place; the tile sums buffer of the dense scan is free again
+  e = scan_generic<uint32_t, false>(w.run_nch, w.run_nch, nruns + 1, w.tsum32, w.ctr + C_NCHUNKS, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_make_chunks, dim3((nruns + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
+                     (const uint32_t*)w.run_nch, (const int32_t*)w.ctr, nruns, s.n1, w.chunks);
   return hipGetLastError();
 }
 

@@ -65,9 +65,23 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->dense_cnt = (uint32_t*)take(4 * s.ndense);
   W->dense_base = (uint32_t*)take(4 * s.ndense);
   W->dense_pg = (int32_t*)take(4 * s.ndense);
-  W->slices = (int4*)take(16 * m);
+  // slices: at most one per valid occurrence and ceil(n3 / SLICE_ROWS) per prefix
+  const int64_t per_prefix = (s.n3 + SLICE_ROWS - 1) / SLICE_ROWS;
+  int64_t nsl_max = s.ndense * per_prefix;
+  if (nsl_max > m) nsl_max = m;
+  int64_t nch_max = nsl_max / CHUNK_SLICES + (int64_t)s.T * s.n2 + 1;
+  if (nch_max > nsl_max) nch_max = nsl_max;
+  W->nsl_max = nsl_max;
+  W->nch_max = nch_max;
+  W->slices = (int4*)take(16 * nsl_max);
+  W->run_nch = (uint32_t*)take(4 * ((int64_t)s.T * s.n2 + 1));
+  W->chunks = (int4*)take(16 * nch_max);
   W->E = (float*)take(4 * (size_t)m * s.D);
   W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
+  const bool bwd_r32 = s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256;
+  W->dApart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nsl_max * s.d1 * s.R : 0);
+  W->dBpart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2) : 0);
+  W->g3part = (float*)take(bwd_r32 ? 4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2) : 0);
   const int par = sort_passes(s) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];
