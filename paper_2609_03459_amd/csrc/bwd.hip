@@ -11,7 +11,7 @@
 namespace ttemb {
 
 ShapeArgs shape_args(const Shape& s);
-bool bwd_r32_supported(const Shape& s);
+bool bwd_r32_supported(const Shape& s, int64_t max_indices);
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st);
 
@@ -37,7 +37,8 @@ __device__ __forceinline__ void seg_flush(int cur, int i0, int i1, int c, const 
 }
 
 // One wave per chunk of SEG_CHUNK sorted occurrences; lanes hold 4 columns
-// each (column blocks of 256); occurrence indices are fetched 64 at a time.
+// each (column blocks of 256); occurrence indices are fetched 64 at a time and
+// the grad_out rows of 8 occurrences are loaded before they are summed.
 __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                const uint32_t* __restrict__ sorted_pos,
                                                const int32_t* __restrict__ bag_of,
@@ -51,6 +52,9 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
   const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
   for (int j0 = 0; j0 < D; j0 += 256) {
+    bool colok[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) colok[q] = j0 + q * 64 + lane < D;
     int cur = sorted_uid[i0];
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int base = i0; base < i1; base += 64) {
@@ -58,18 +62,30 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
       const int my_u = i < i1 ? sorted_uid[i] : -1;
       const int my_b = i < i1 ? bag_of[sorted_pos[i]] : 0;
       const int cnt = i1 - base < 64 ? i1 - base : 64;
-      for (int k = 0; k < cnt; ++k) {
-        const int u = __shfl(my_u, k, 64);
-        const int b = __shfl(my_b, k, 64);
-        if (u != cur) {
-          seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
-          cur = u;
-          acc[0] = acc[1] = acc[2] = acc[3] = 0.f;
-        }
-        const float* row = dV + (int64_t)b * D + j0 + lane;
+      for (int k0 = 0; k0 < cnt; k0 += 8) {
+        float v[8][4];
+        int uk[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (j0 + q * 64 + lane < D) acc[q] += row[q * 64];
+        for (int kk = 0; kk < 8; ++kk) {
+          const int k = k0 + kk < cnt ? k0 + kk : k0;
+          const int b = __shfl(my_b, k, 64);
+          uk[kk] = __shfl(my_u, k, 64);
+          const float* row = dV + (int64_t)b * D + j0 + lane;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[kk][q] = colok[q] ? row[q * 64] : 0.f;
+        }
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+          if (k0 + kk < cnt) {
+            if (uk[kk] != cur) {
+              seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
+              cur = uk[kk];
+              acc[0] = acc[1] = acc[2] = acc[3] = 0.f;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) acc[q] += v[kk][q];
+          }
+        }
       }
     }
     seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
@@ -78,10 +94,14 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
 
 // Rows whose occurrences span several chunks: chunk c0 + 1, where c0 holds the
 // row's first occurrence, finishes the row from c0's tail partial and the head
-// partials of every following chunk, in chunk order.  One wave per chunk.
-__global__ void __launch_bounds__(64) k_seg_fix(const int32_t* __restrict__ sorted_uid,
-                                                const int32_t* __restrict__ occ_start, const int32_t* __restrict__ ctr,
-                                                int D, const float* __restrict__ part, float* __restrict__ dE) {
+// partials of every following chunk.  Four waves split the chunk range; each
+// sums its part with 8 independent accumulators; the parts are combined in a
+// fixed order.
+__global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sorted_uid,
+                                                 const int32_t* __restrict__ occ_start,
+                                                 const int32_t* __restrict__ ctr, int D,
+                                                 const float* __restrict__ part, float* __restrict__ dE) {
+  __shared__ float red[4][256];
   const int nvalid = ctr[C_NVALID];
   const int c = blockIdx.x;
   if (c == 0 || c * SEG_CHUNK >= nvalid) return;
@@ -89,10 +109,37 @@ __global__ void __launch_bounds__(64) k_seg_fix(const int32_t* __restrict__ sort
   const int lo = occ_start[u], hi = occ_start[u + 1];
   const int c0 = lo / SEG_CHUNK, c1 = (hi - 1) / SEG_CHUNK;
   if (c0 != c - 1) return;
-  for (int j = lane_id(); j < D; j += 64) {
-    float acc = part[((int64_t)c0 * 2 + 1) * D + j];
-    for (int k = c0 + 1; k <= c1; ++k) acc += part[((int64_t)k * 2 + 0) * D + j];
-    dE[(int64_t)u * D + j] = acc;
+  const int w = threadIdx.x >> 6, lane = lane_id();
+  const int n = c1 - c0;  // head partials of chunks c0+1 .. c1
+  const int k_lo = c0 + 1 + (int)(((int64_t)n * w) / 4), k_hi = c0 + 1 + (int)(((int64_t)n * (w + 1)) / 4);
+  for (int j0 = 0; j0 < D; j0 += 256) {
+    for (int jj = 0; jj < 4; ++jj) {
+      const int j = j0 + jj * 64 + lane;
+      float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (j < D) {
+        int k = k_lo;
+        for (; k + 8 <= k_hi; k += 8)
+#pragma unroll
+          for (int kk = 0; kk < 8; ++kk) a[kk] += part[((int64_t)(k + kk) * 2 + 0) * D + j];
+        for (; k < k_hi; ++k) a[0] += part[((int64_t)k * 2 + 0) * D + j];
+      }
+      red[w][jj * 64 + lane] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+    }
+    __syncthreads();
+    if (w == 0) {
+      for (int jj = 0; jj < 4; ++jj) {
+        const int j = j0 + jj * 64 + lane;
+        if (j < D) {
+          float acc = part[((int64_t)c0 * 2 + 1) * D + j];
+          acc += red[0][jj * 64 + lane];
+          acc += red[1][jj * 64 + lane];
+          acc += red[2][jj * 64 + lane];
+          acc += red[3][jj * 64 + lane];
+          dE[(int64_t)u * D + j] = acc;
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -198,7 +245,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int64_t n2s = (int64_t)s.T * s.n2 * s.R * s.d2 * s.R;
   const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
   hipError_t e;
-  const bool fast = bwd_r32_supported(s);
+  const bool fast = bwd_r32_supported(s, w.M);
   if (!fast || M <= 0) {
     if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
     if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
@@ -212,7 +259,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   prof_end(prof, K_SEG_SUM, st);
-  hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(64), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
+  hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, prof, st);
   const int grid = persistent_grid() * 2;

@@ -24,10 +24,10 @@ constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
 
 __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     k_bwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
-              const float* __restrict__ dE, const int4* __restrict__ slices, const int4* __restrict__ chunks,
-              const uint32_t* __restrict__ run_base, const uint32_t* __restrict__ uniq_key, int32_t* __restrict__ ctr,
-              float* __restrict__ dApart, float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap,
-              int nch_cap) {
+              const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
+              const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
+              const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ dApart,
+              float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -49,20 +49,29 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const int c_lo = (int)run_base[t * s.n2], c_hi = (int)run_base[(t + 1) * s.n2];
   const int nch = c_hi - c_lo;
   const int l15 = lane & 15, l4 = lane >> 4;
+  const int rowsel = l15 >> 3;
+  // per-lane float offsets (all operands are addressed as uniform base + 32-bit lane offset)
+  const uint32_t o_eb = (uint32_t)(l4 * 8 + (lane & 7));             // dD B operand in a dE row
+  const uint32_t o_e4 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));          // dC A operand (4 consecutive j3)
+  const uint32_t o_d4 = (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));  // dC B operand in a G3 slice
+  const int prow = l4 >> 1;                                          // row of the pair this lane feeds to dC
+  const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
+  const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
   int cursor = 0;
   int cur_run = -1;
-  float Bop[32];   // stage-1 B operand  B_h[a = 4s + l4][16 nt + l15]       (s, nt) -> 4 s + nt
+  float Bop[32];  // stage-1 B operand  B_h[a = 4s + l4][16 nt + l15]       (s, nt) -> 4 s + nt
   while (true) {
     const int c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
     if (c < 0) break;
     const int4 ch = chunks[c_lo + c];
-    const int f = ch.x, ns = ch.y, run = ch.z;
+    const int f = __builtin_amdgcn_readfirstlane(ch.x), ns = __builtin_amdgcn_readfirstlane(ch.y);
+    const int run = __builtin_amdgcn_readfirstlane(ch.z);
+    const float* Bg = G2 + (uint32_t)run * 4096u + 16 * h;
     if (run != cur_run) {
-      const float* Bg = G2 + (int64_t)run * 4096;
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) Bop[4 * s4 + nt] = Bg[((4 * s4 + l4) * 4 + nt) * 32 + 16 * h + l15];
+        for (int nt = 0; nt < 4; ++nt) Bop[4 * s4 + nt] = Bg[((4 * s4 + l4) * 4 + nt) * 32 + l15];
       cur_run = run;
     }
     f32x4 dB[8];  // (mt, nt) -> 4 mt + nt
@@ -71,19 +80,20 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 
     for (int qd = 0; qd < ns; qd += 4) {
       const int nqs = ns - qd < 4 ? ns - qd : 4;
-      int4 sd = make_int4(0, 0, 0, 0);
-      if (lane < nqs) sd = slices[f + qd + lane];
-      // i1 of each slice of the quad (lane j holds slice j)
-      int my_i1 = 0;
-      if (lane < nqs) my_i1 = (int)(((uint32_t)sd.w % (uint32_t)s.n12) / (uint32_t)s.n2);
+      const int sl = f + qd + (lane < nqs ? lane : 0);
+      const int4 sd = slices[sl];
+      const int my_i1 = slice_i1[sl];  // lane j holds slice j of the quad
       // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
       const int aj = l15 >> 2;
       const int aj_i1 = __shfl(my_i1, aj, 64);
       const bool aj_ok = aj < nqs;
-      const float* Ag = G1 + ((int64_t)(t * s.n1 + aj_i1) * 4 + (lane & 3)) * 32;
+      const float* Ag = G1t + (uint32_t)aj_i1 * 128u + (uint32_t)((lane & 3) * 32 + l4);
       float Aop[8];
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = aj_ok ? Ag[4 * s4 + l4] : 0.f;
+      for (int s4 = 0; s4 < 8; ++s4) {
+        const float v = Ag[4 * s4];
+        Aop[s4] = aj_ok ? v : 0.f;
+      }
       f32x4 Cs[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -101,52 +111,54 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       wave_lds_sync();
 
       for (int j = 0; j < nqs; ++j) {
-        const int rb = __shfl(sd.y, j, 64), re = __shfl(sd.z, j, 64);
-        const int i1 = __shfl(my_i1, j, 64);
+        const int rb = __builtin_amdgcn_readlane(sd.y, j), re = __builtin_amdgcn_readlane(sd.z, j);
+        const int i1 = __builtin_amdgcn_readlane(my_i1, j);
         const int nr = re - rb;
         // dD A operand: C_h^T[b' = l15][(j1 j2) = 4 s + l4] = C_h[j][s][l4][l15]
         float CT[4];
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[((j * 4 + s4) * 4 + l4) * 16 + l15];
-        const uint32_t ukey = lane < nr ? uniq_key[rb + lane] : 0u;
+        const int i3v = uniq_i3[rb + (lane < nr ? lane : 0)];  // lane k: i3 of row k of the slice
+        const float* Es = dE + (uint32_t)rb * 128u;
         f32x4 dC = {0.f, 0.f, 0.f, 0.f};
-        const int rowsel = l15 >> 3;
         for (int r0 = 0; r0 < nr; r0 += 2) {
           const bool has1 = r0 + 1 < nr;
-          const int mine = r0 + (rowsel && has1 ? 1 : 0);
+          const int u1 = has1 ? r0 + 1 : r0;
           const bool live = !rowsel || has1;
-          const int i3m = decode_key((uint32_t)__shfl((int)ukey, mine, 64), s.Npad, s.n2, s.n3).i3;
-          const float* Em = dE + (int64_t)(rb + mine) * 128;
+          const float* Ea = Es + (uint32_t)r0 * 128u;
+          const float* Eb = Es + (uint32_t)u1 * 128u;
+          const int i3a = __builtin_amdgcn_readlane(i3v, r0), i3b = __builtin_amdgcn_readlane(i3v, u1);
+          // dD B operand: lanes 0-7 of each 16 take row r0, lanes 8-15 row r0 + 1
+          const float* Em = rowsel ? Eb : Ea;
           float EB[4];
 #pragma unroll
-          for (int s4 = 0; s4 < 4; ++s4) EB[s4] = live ? Em[(4 * s4 + l4) * 8 + (lane & 7)] : 0.f;
+          for (int s4 = 0; s4 < 4; ++s4) {
+            const float v = Em[o_eb + 32 * s4];
+            EB[s4] = live ? v : 0.f;
+          }
+          // dC operands: K index (row, j3) with row = l4 >> 1, j3 = 4 (l4 & 1) + k, so each lane
+          // reads four consecutive floats of its dE row and of its G3 slice
+          const float4 e4 = *(const float4*)((prow ? Eb : Ea) + o_e4);
+          const float4 d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
+          const bool ez = prow && !has1;
+          const int i3m = rowsel && has1 ? i3b : i3a;
           f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], EB[s4], dd, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.x, d4.x, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.y, d4.y, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.z, d4.z, dC, 0, 0, 0);
+          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.w, d4.w, dC, 0, 0, 0);
           // dd: lane holds dD_h[b' = 4 l4 + r][row rowsel][j3 = lane & 7]
           if (live) {
-            float* gp = g3acc + i3m * 128 + (4 * l4) * 8 + (lane & 7);
+            float* gp = g3acc + (uint32_t)i3m * 128u + (uint32_t)(32 * l4 + (lane & 7));
 #pragma unroll
             for (int r = 0; r < 4; ++r) atomicAdd(gp + r * 8, dd[r]);
           }
-          // dC_h += dE_u . D_{u,h}^T for each row of the pair (a missing second row adds zeros)
-          const int u1 = has1 ? r0 + 1 : r0;
-          const int i3a = decode_key((uint32_t)__shfl((int)ukey, r0, 64), s.Npad, s.n2, s.n3).i3;
-          const int i3b = decode_key((uint32_t)__shfl((int)ukey, u1, 64), s.Npad, s.n2, s.n3).i3;
-          const float* Ea = dE + (int64_t)(rb + r0) * 128 + l15 * 8 + l4;
-          const float* Eb = dE + (int64_t)(rb + u1) * 128 + l15 * 8 + l4;
-          const float* Da = G3 + ((int64_t)(t * s.n3 + i3a) * 32 + 16 * h + l15) * 8 + l4;
-          const float* Db = G3 + ((int64_t)(t * s.n3 + i3b) * 32 + 16 * h + l15) * 8 + l4;
-          const float ea0 = Ea[0], ea1 = Ea[4], da0 = Da[0], da1 = Da[4];
-          const float eb0 = has1 ? Eb[0] : 0.f, eb1 = has1 ? Eb[4] : 0.f, db0 = Db[0], db1 = Db[4];
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ea0, da0, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ea1, da1, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(eb0, db0, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(eb1, db1, dC, 0, 0, 0);
         }
         // dC: lane holds dC_h[j1 = l4][j2 = r][b' = l15]
         // dB_h += A^T . dC_h  (M = a, N = (j2, b'), K = j1)
-        const float* Aj = G1 + ((int64_t)(t * s.n1 + i1) * 4 + l4) * 32 + l15;
+        const float* Aj = G1t + (uint32_t)i1 * 128u + (uint32_t)(l4 * 32 + l15);
         const float AT0 = Aj[0], AT1 = Aj[16];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
@@ -163,12 +175,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       // B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15] read from G2 (L1/L2)
       const int ms = l15 >> 2, mj1 = lane & 3;
       const bool m_ok = ms < nqs;
-      const float* Bg = G2 + (int64_t)run * 4096 + 16 * h;
       f32x4 dA[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
       for (int s2 = 0; s2 < 16; ++s2) {
         const int k = 4 * s2 + l4;
-        const float av = m_ok ? scr[((ms * 4 + mj1) * 4 + (k >> 4)) * 16 + (k & 15)] : 0.f;
+        const float v = scr[((ms * 4 + mj1) * 4 + (k >> 4)) * 16 + (k & 15)];
+        const float av = m_ok ? v : 0.f;
         const float b0 = Bg[(l15 * 4 + (k >> 4)) * 32 + (k & 15)];
         const float b1 = Bg[((16 + l15) * 4 + (k >> 4)) * 32 + (k & 15)];
         dA[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b0, dA[0], 0, 0, 0);
@@ -176,7 +188,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       }
       // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]
       if (l4 < nqs) {
-        float* dst = dApart + ((int64_t)h * nsl_cap + (f + qd + l4)) * 128 + l15;
+        float* dst = dApart + ((size_t)h * nsl_cap + (f + qd + l4)) * 128 + l15;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           dst[r * 32] = dA[0][r];
@@ -186,7 +198,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       wave_lds_sync();
     }
     // dB_h partial of this chunk: lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
-    float* dst = dBpart + ((int64_t)h * nch_cap + (c_lo + c)) * 2048;
+    float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c)) * 2048;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
@@ -195,30 +207,35 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
   }
   __syncthreads();
-  float* gdst = g3part + (int64_t)blockIdx.x * acc_n;
+  float* gdst = g3part + (size_t)blockIdx.x * acc_n;
   for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
 }
 
-// dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2)
-__global__ void __launch_bounds__(128) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
+// dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2).
+// Four groups of 128 threads take i2 = g, g + 4, ...; their sums are combined
+// in a fixed order.
+__global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                    const uint32_t* __restrict__ dense_base,
                                                    const float* __restrict__ dApart, int nsl_cap,
                                                    float* __restrict__ dG1) {
+  __shared__ float red[4][128];
   const int ti1 = blockIdx.x;  // t * n1 + i1
   const int t = ti1 / s.n1, i1 = ti1 % s.n1;
-  const int e = threadIdx.x;
-  float acc = 0.f;
-  for (int i2 = 0; i2 < s.n2; ++i2) {
+  const int g = threadIdx.x >> 7, e = threadIdx.x & 127;
+  float a0 = 0.f, a1 = 0.f;
+  for (int i2 = g; i2 < s.n2; i2 += 4) {
     const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
     const uint32_t cnt = dense_cnt[slot];
     if (!cnt) continue;
     const uint32_t b = dense_base[slot];
     for (uint32_t k = 0; k < cnt; ++k) {
-      acc += dApart[((int64_t)0 * nsl_cap + b + k) * 128 + e];
-      acc += dApart[((int64_t)1 * nsl_cap + b + k) * 128 + e];
+      a0 += dApart[((int64_t)0 * nsl_cap + b + k) * 128 + e];
+      a1 += dApart[((int64_t)1 * nsl_cap + b + k) * 128 + e];
     }
   }
-  dG1[(int64_t)ti1 * 128 + e] = acc;
+  red[g][e] = a0 + a1;
+  __syncthreads();
+  if (g == 0) dG1[(int64_t)ti1 * 128 + e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
 }
 
 // dG2[t][i2][a][j2][16 h + b'] = sum of the chunk partials of run (t, i2), half h
@@ -250,8 +267,10 @@ __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __r
   dG3[(((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3] = acc;
 }
 
-bool bwd_r32_supported(const Shape& s) {
-  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64;
+bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
+  // 32-bit float offsets into dE (rows x 128) and G3 must fit
+  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64 &&
+         max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
 }
 
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
@@ -268,11 +287,11 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   if (e != hipSuccess) return e;
   prof_begin(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_bwd_r32, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
-                     (const float*)w.E, (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                     (const uint32_t*)w.uniq_key, w.ctr, w.dApart, w.dBpart, w.g3part, (int)w.nsl_max,
-                     (int)w.nch_max);
+                     (const float*)w.E, (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
+                     (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.g3part,
+                     (int)w.nsl_max, (int)w.nch_max);
   prof_end(prof, K_BWD_FUSED, st);
-  hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(128), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
+  hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(512), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
                      (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1);
   hipLaunchKernelGGL(k_reduce_g2, dim3(s.T * s.n2 * 2), dim3(256), 0, st, (const uint32_t*)w.run_nch,
                      (const float*)w.dBpart, (int)w.nch_max, dG2);

@@ -70,6 +70,7 @@ struct Work {
   int32_t* inv;           // [M] unique id of each occurrence (-1 invalid)
   int32_t* sorted_uid;    // [M] unique id of each sorted occurrence
   uint32_t* uniq_key;     // [M] key of each unique row
+  int32_t* uniq_i3;       // [M] last digit i3 of each unique row
   int32_t* occ_start;     // [M+1] first sorted position of each unique row
   int32_t* pg_start;      // [M+1] first unique row of each prefix group
   uint32_t* pg_key;       // [M] t*n1*n2 + i1*n2 + i2 of each group
@@ -77,6 +78,7 @@ struct Work {
   uint32_t* dense_base;   // [ndense] exclusive scan of dense_cnt
   int32_t* dense_pg;      // [ndense] group id per slot
   int4* slices;           // [nsl_max] (group, row_begin, row_end, key)
+  int32_t* slice_i1;      // [nsl_max] first digit i1 of each slice's group
   uint32_t* run_nch;      // [T*n2 + 1] chunks per (t, i2) run, then their exclusive scan
   int4* chunks;           // [nch_max] (first slice, slice count, run, 0)
   float* dApart;          // [2][nsl_max][d1*R] backward: dA of each slice, per rank half

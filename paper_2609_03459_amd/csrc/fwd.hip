@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 3) k_fwd_r32(ShapeArgs s, cons
       const int t = key / s.n12, q = key % s.n12;
       const int i2 = q % s.n2;
       const int ti2 = t * s.n2 + i2;
-      const uint32_t keyc = keyn;
+      const int i3c = decode_key(keyn, s.Npad, s.n2, s.n3).i3;  // i3 of row rb + lane
       const bool need_c = p != cur_pg;
       if (ti2 != cur_ti2) {
         const float* Bg = G2 + (int64_t)ti2 * 4096;
@@ -201,8 +201,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 3) k_fwd_r32(ShapeArgs s, cons
       auto load_pair = [&](int r0, float* Dv) {
         const bool has1 = r0 + 1 < nr;
         const int rr = sel ? (has1 ? r0 + 1 : r0) : r0;
-        const uint32_t k = (uint32_t)__shfl((int)keyc, rr, 64);
-        const int i3 = decode_key(k, s.Npad, s.n2, s.n3).i3;
+        const int i3 = __shfl(i3c, rr, 64);
         const float* Dg = G3t + i3 * 256;
         const bool live = !sel || has1;
 #pragma unroll

@@ -341,9 +341,10 @@ __global__ void k_flags(const uint32_t* __restrict__ sk, int n, uint32_t kinv, u
 }
 
 __global__ void k_group_write(const uint32_t* __restrict__ sk, const uint32_t* __restrict__ sp,
-                              const uint64_t* __restrict__ incl, int n, uint32_t kinv, uint32_t n3,
+                              const uint64_t* __restrict__ incl, int n, uint32_t kinv, uint32_t n3, uint32_t Npad,
                               int32_t* __restrict__ inv, int32_t* __restrict__ sorted_uid,
-                              uint32_t* __restrict__ uniq_key, int32_t* __restrict__ occ_start,
+                              uint32_t* __restrict__ uniq_key, int32_t* __restrict__ uniq_i3,
+                              int32_t* __restrict__ occ_start,
                               int32_t* __restrict__ pg_start, uint32_t* __restrict__ pg_key,
                               int32_t* __restrict__ ctr) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -364,6 +365,7 @@ __global__ void k_group_write(const uint32_t* __restrict__ sk, const uint32_t* _
   sorted_uid[i] = uid;
   if (head) {
     uniq_key[uid] = k;
+    uniq_i3[uid] = (int)((k % Npad) % n3);
     occ_start[uid] = i;
   }
   if (pgh) {
@@ -397,8 +399,8 @@ __global__ void k_dense_set(const int32_t* __restrict__ pg_start, const uint32_t
 
 __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint32_t* __restrict__ dense_base,
                               const int32_t* __restrict__ dense_pg, int64_t ndense,
-                              const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key,
-                              int4* __restrict__ slices) {
+                              const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key, int n1,
+                              int4* __restrict__ slices, int32_t* __restrict__ slice_i1) {
   for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < ndense;
        s += (int64_t)gridDim.x * blockDim.x) {
     uint32_t c = dense_cnt[s];
@@ -410,6 +412,7 @@ __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint
       int rb = r0 + (int)k * SLICE_ROWS;
       int re = rb + SLICE_ROWS < r1 ? rb + SLICE_ROWS : r1;
       slices[b + k] = make_int4(p, rb, re, (int)pg_key[p]);
+      slice_i1[b + k] = (int)(s % n1);  // slot = (t * n2 + i2) * n1 + i1
     }
   }
 }
@@ -500,15 +503,15 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   e = scan_generic<uint64_t, true>(w.flags, w.flags, M, w.tsum64, nullptr, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_group_write, dim3((n + 255) / 256), dim3(256), 0, st, sk, sp, (const uint64_t*)w.flags, n,
-                     s.kinv, (uint32_t)s.n3, w.inv, w.sorted_uid, w.uniq_key, w.occ_start, w.pg_start, w.pg_key,
-                     w.ctr);
+                     s.kinv, (uint32_t)s.n3, s.Npad, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
+                     w.pg_start, w.pg_key, w.ctr);
   hipLaunchKernelGGL(k_dense_set, dim3(grid_for(M, 256, 2048)), dim3(256), 0, st, (const int32_t*)w.pg_start,
                      (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, w.dense_cnt, w.dense_pg);
   e = scan_generic<uint32_t, false>(w.dense_cnt, w.dense_base, s.ndense, w.tsum32, w.ctr + C_NSLICES, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
                      (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
-                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, w.slices);
+                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, w.slices, w.slice_i1);
   const int nruns = s.T * s.n2;
   hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
                      (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
