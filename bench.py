@@ -90,6 +90,53 @@ def algorithmic_work(kernel, case, counts):
     raise ValueError(kernel)
 
 
+KERNEL_SYMBOL = {"fwd_fused": "k_fwd_r32", "bwd_fused": "k_bwd_r32", "pool": "k_pool", "seg_sum": "k_seg_dE",
+                 "ingest": "k_ingest"}
+
+
+def write_traffic(pmc_dir, copy_mib=1024, kernel="bwd_fused"):
+    """HBM bytes per launch of `kernel` from rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch).
+
+    Each counter is scaled by the factor that makes it read the true size on the
+    calibration copy (one elementwise kernel that reads and writes copy_mib MiB).
+    """
+    import csv
+    import glob
+
+    import numpy as np
+
+    sym = KERNEL_SYMBOL[kernel]
+    vals = {"FETCH_SIZE": {"k": [], "copy": []}, "WRITE_SIZE": {"k": [], "copy": []}}
+    for f in sorted(glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)):
+        for r in csv.DictReader(open(f)):
+            c = r["Counter_Name"]
+            if c not in vals:
+                continue
+            name = r["Kernel_Name"]
+            if f"::{sym}(" in name or f"::{sym}<" in name:
+                vals[c]["k"].append(float(r["Counter_Value"]))
+            elif "elementwise" in name:
+                vals[c]["copy"].append(float(r["Counter_Value"]))
+    true_kib = copy_mib * 1024.0
+    out = {"kernel": kernel, "symbol": sym, "source": source_digest(), "copy_mib": copy_mib}
+    total = 0.0
+    for c, v in vals.items():
+        if not v["k"] or not v["copy"]:
+            raise SystemExit(f"{pmc_dir}: no {c} rows for {sym} and the calibration copy")
+        raw = float(np.mean(v["k"]))
+        scale = true_kib / max(v["copy"])
+        out[c] = {"raw_kib_per_dispatch": round(raw, 1), "dispatches": len(v["k"]),
+                  "copy_raw_kib": round(max(v["copy"]), 1), "scale": round(scale, 4),
+                  "bytes_per_launch": round(raw * scale * 1024.0)}
+        total += raw * scale * 1024.0
+    out["bytes_per_launch"] = round(total)
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
 def cpu_baseline(case, target_s):
     """The oracle (plain fp64 C, one thread) on a bounded sample of the same workload:
     a seeded subset of bags of every table, forward then backward."""
@@ -143,8 +190,14 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
-                    help="also run one torch copy of this many MiB (counter calibration runs)")
+                    help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
+    ap.add_argument("--write-traffic", metavar="DIR", default=None,
+                    help="CPU only: turn the FETCH_SIZE / WRITE_SIZE counter CSVs under DIR (one rocprofv3 --pmc "
+                         "pass each, of a run with --copy-mib) into profiles/traffic.json, then exit")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.write_traffic)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(the sharding design is described in DESIGN.md)", file=sys.stderr)
@@ -179,10 +232,12 @@ def main():
         emb.sgd(*G, *grads, lr)
 
     if args.copy_mib:
-        x = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev)
+        # reads and writes exactly copy_mib MiB each: the calibration of the byte counters
+        x = torch.ones(args.copy_mib << 18, dtype=torch.float32, device=dev)
         y = torch.empty_like(x)
-        y.copy_(x)
+        torch.mul(x, 2.0, out=y)
         torch.cuda.synchronize()
+        del x, y
 
     # warmup; the first steps also time each candidate kernel once
     kernels = list(P.N.KERNELS)
