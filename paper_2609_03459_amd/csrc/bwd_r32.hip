@@ -22,6 +22,38 @@ ShapeArgs shape_args(const Shape& s);
 constexpr int BW_WAVES = 8;
 constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
 
+// The LDS dG3 accumulator stores rank row b' of a table row i3 at slot
+// p(b') = 4 (b' >> 2) + ((b' + (b' >> 2)) & 3).  A dD tile puts b' = 4 l4 + r in
+// register r of lane group l4, so in step r the four lane groups of one row add
+// to four different 8-bank groups: each 32-lane add is free of bank conflicts.
+__device__ __forceinline__ int g3_unslot(int p) {
+  const int g = p >> 2;
+  return 4 * g + (((p & 3) - g) & 3);
+}
+
+// Per-wave scratch holds a [slice][j1][(j2, b')] stack (4 x 4 x 64 floats): first
+// C_h, then dC_h.  The 64-float rows are XOR-swizzled by (8 slice + 10 j1) mod 64
+// so that all four access patterns (C and dC writes, C^T and dA operand reads)
+// put at most two of the 64 lanes on one bank.
+__device__ __forceinline__ uint32_t scr_at(int sl, int j1, int j2b) {
+  return (uint32_t)(sl * 256 + j1 * 64 + (j2b ^ ((8 * sl + 10 * j1) & 63)));
+}
+
+template <typename T>
+__device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
+  return j == 0 ? a : (j == 1 ? b : (j == 2 ? c : d));
+}
+
+// operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs with itself)
+struct BwPair {
+  float eb[4];  // dD B operand: dE[row][(4 s + l4) * 8 + j3], row r0 in lanes 0-7 of each 16, r0 + 1 in 8-15
+  float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
+  float4 d4;    // dC B operand: G3[i3 of that row][16 h + l15][4 (l4 & 1) + k]
+  int i3m;      // i3 of this lane's dD column
+  bool live;    // this lane's dD column is a real row
+  bool ez;      // this lane's dC K slots belong to a missing second row (add zeros)
+};
+
 __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     k_bwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
               const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
@@ -32,7 +64,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const int acc_n = s.n3 * 128;
-  float* g3acc = lds;  // [n3][16][8]
+  float* g3acc = lds;  // [n3][slot p(b')][8]
   float* scr = lds + acc_n + wave * BW_SCR;
   const int nq = 2 * s.T;
   const int q = blockIdx.x % nq;
@@ -49,162 +81,250 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const int c_lo = (int)run_base[t * s.n2], c_hi = (int)run_base[(t + 1) * s.n2];
   const int nch = c_hi - c_lo;
   const int l15 = lane & 15, l4 = lane >> 4;
-  const int rowsel = l15 >> 3;
-  // per-lane float offsets (all operands are addressed as uniform base + 32-bit lane offset)
-  const uint32_t o_eb = (uint32_t)(l4 * 8 + (lane & 7));             // dD B operand in a dE row
-  const uint32_t o_e4 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));          // dC A operand (4 consecutive j3)
-  const uint32_t o_d4 = (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));  // dC B operand in a G3 slice
-  const int prow = l4 >> 1;                                          // row of the pair this lane feeds to dC
+  const bool rowsel = (l15 >> 3) != 0;  // dD column of row r0 + 1
+  const bool prow = (l4 >> 1) != 0;     // dC K slots of row r0 + 1
+  // per-lane float offsets; every operand is a uniform base plus one of these
+  const uint32_t o_eb0 = (uint32_t)(l4 * 8 + (lane & 7));
+  const uint32_t o_eb1 = o_eb0 + (rowsel ? 128u : 0u);
+  const uint32_t o_e40 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));
+  const uint32_t o_e41 = o_e40 + (prow ? 128u : 0u);
+  const uint32_t o_d4 = (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));
+  // dD LDS adds: register r of lane group l4 goes to slot p(4 l4 + r)
+  uint32_t o_g3[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) o_g3[r] = (uint32_t)((4 * l4 + ((r + l4) & 3)) * 8 + (lane & 7));
   const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
   const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
+
   int cursor = 0;
   int cur_run = -1;
-  float Bop[32];  // stage-1 B operand  B_h[a = 4s + l4][16 nt + l15]       (s, nt) -> 4 s + nt
-  while (true) {
-    const int c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
-    if (c < 0) break;
+  float Bop[32];   // stage-1 B operand B_h[a = 4 s + l4][16 nt + l15], (s, nt) -> 4 s + nt
+  float BTop[32];  // dA B operand B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15], (s2, nt2) -> 2 s2 + nt2
+  f32x4 dB[8];     // (mt, nt) -> 4 mt + nt
+
+  // quad slice descriptors (wave-uniform)
+  // quad descriptors, lane j < 4 holding slice j: first row, row count, i1
+  int q_rb = 0, q_nr = 0, q_i1 = 0;
+  // i3 of the quad's rows: slice j row k in lane 32 (j & 1) + k of i3A (j < 2) or i3B (j >= 2)
+  int i3A = 0, i3B = 0;
+  // row pairs of the quad, flattened: slice j owns pairs [cp_j, cp_{j+1}), cp_0 = 0
+  int cp1 = 0, cp2 = 0, cp3 = 0, np = 0;
+  auto pair_load = [&](BwPair& X, int P) {
+    const int pj = (P >= cp1) + (P >= cp2) + (P >= cp3);
+    const int pr = 2 * (P - (pj == 0 ? 0 : (pj == 1 ? cp1 : (pj == 2 ? cp2 : cp3))));
+    const int rb = __builtin_amdgcn_readlane(q_rb, pj), nr = __builtin_amdgcn_readlane(q_nr, pj);
+    const bool has1 = pr + 1 < nr;
+    const int i3v = pj < 2 ? i3A : i3B;
+    const int li = (pj & 1) * 32 + pr;
+    const int i3a = __builtin_amdgcn_readlane(i3v, li);
+    const int i3b = __builtin_amdgcn_readlane(i3v, has1 ? li + 1 : li);
+    const float* Es = dE + (uint32_t)(rb + pr) * 128u;
+    const uint32_t ob = has1 ? o_eb1 : o_eb0;
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = Es[ob + 32u * s4];
+    X.e4 = *(const float4*)(Es + (has1 ? o_e41 : o_e40));
+    X.d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
+    X.i3m = rowsel ? i3b : i3a;
+    X.live = has1 || !rowsel;
+    X.ez = prow && !has1;
+  };
+
+  int c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
+  int f = 0, ns = 0, run = -1, qd = 0;
+  if (c >= 0) {
     const int4 ch = chunks[c_lo + c];
-    const int f = __builtin_amdgcn_readfirstlane(ch.x), ns = __builtin_amdgcn_readfirstlane(ch.y);
-    const int run = __builtin_amdgcn_readfirstlane(ch.z);
+    f = __builtin_amdgcn_readfirstlane(ch.x);
+    ns = __builtin_amdgcn_readfirstlane(ch.y);
+    run = __builtin_amdgcn_readfirstlane(ch.z);
+  }
+  while (c >= 0) {
     const float* Bg = G2 + (uint32_t)run * 4096u + 16 * h;
     if (run != cur_run) {
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) Bop[4 * s4 + nt] = Bg[((4 * s4 + l4) * 4 + nt) * 32 + l15];
+#pragma unroll
+      for (int s2 = 0; s2 < 16; ++s2) {
+        const int k = 4 * s2 + l4;
+        BTop[2 * s2 + 0] = Bg[(l15 * 4 + (k >> 4)) * 32 + (k & 15)];
+        BTop[2 * s2 + 1] = Bg[((16 + l15) * 4 + (k >> 4)) * 32 + (k & 15)];
+      }
       cur_run = run;
     }
-    f32x4 dB[8];  // (mt, nt) -> 4 mt + nt
+    if (qd == 0) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int qd = 0; qd < ns; qd += 4) {
-      const int nqs = ns - qd < 4 ? ns - qd : 4;
-      const int sl = f + qd + (lane < nqs ? lane : 0);
+      for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const int nqs = ns - qd < 4 ? ns - qd : 4;
+    const int sb = f + qd;
+    {
+      // lane j < nqs holds slice sb + j; the other lanes repeat slice sb with no rows
+      const int sl = sb + (lane < nqs ? lane : 0);
       const int4 sd = slices[sl];
-      const int my_i1 = slice_i1[sl];  // lane j holds slice j of the quad
-      // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
-      const int aj = l15 >> 2;
-      const int aj_i1 = __shfl(my_i1, aj, 64);
-      const bool aj_ok = aj < nqs;
-      const float* Ag = G1t + (uint32_t)aj_i1 * 128u + (uint32_t)((lane & 3) * 32 + l4);
-      float Aop[8];
+      q_rb = sd.y;
+      q_nr = lane < nqs ? sd.z - sd.y : 0;
+      q_i1 = slice_i1[sl];
+    }
+    {
+      // lane 32 h2 + k of i3A / i3B: row k of slice h2 / 2 + h2 (row clamped into the slice)
+      const int ja = lane >> 5, k = lane & 31;
+      const int rba = __builtin_amdgcn_readlane(q_rb, 0), rbb = __builtin_amdgcn_readlane(q_rb, 1);
+      const int rbc = __builtin_amdgcn_readlane(q_rb, 2), rbd = __builtin_amdgcn_readlane(q_rb, 3);
+      const int nra = __builtin_amdgcn_readlane(q_nr, 0), nrb = __builtin_amdgcn_readlane(q_nr, 1);
+      const int nrc = __builtin_amdgcn_readlane(q_nr, 2), nrd = __builtin_amdgcn_readlane(q_nr, 3);
+      const int rA = ja ? rbb : rba, nA = ja ? nrb : nra;
+      const int rB = ja ? rbd : rbc, nB = ja ? nrd : nrc;
+      i3A = uniq_i3[rA + (k < nA ? k : 0)];
+      i3B = uniq_i3[rB + (k < nB ? k : 0)];
+      cp1 = (nra + 1) >> 1;
+      cp2 = cp1 + ((nrb + 1) >> 1);
+      cp3 = cp2 + ((nrc + 1) >> 1);
+      np = cp3 + ((nrd + 1) >> 1);
+    }
+    // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
+    const int aj = l15 >> 2;
+    const float* Ag = G1t + (uint32_t)slice_i1[sb + (aj < nqs ? aj : 0)] * 128u + (uint32_t)((lane & 3) * 32 + l4);
+    float Aop[8];
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4) {
-        const float v = Ag[4 * s4];
-        Aop[s4] = aj_ok ? v : 0.f;
-      }
+    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
+    BwPair XA, XB;
+    pair_load(XA, 0);  // first row pair, in flight during stage 1
+    const bool aj_ok = aj < nqs;
+    // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
+    {
       f32x4 Cs[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4)
+      for (int s4 = 0; s4 < 8; ++s4) {
+        const float a = aj_ok ? Aop[s4] : 0.f;
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-          Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[s4], Bop[4 * s4 + nt], Cs[nt], 0, 0, 0);
+        for (int nt = 0; nt < 4; ++nt) Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bop[4 * s4 + nt], Cs[nt], 0, 0, 0);
+      }
       // lane holds C_h[slice l4][j1 r][j2 nt][b' l15]; scratch layout [slice][j1][j2][b']
-      wave_lds_sync();
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) scr[((l4 * 4 + r) * 4 + nt) * 16 + l15] = Cs[nt][r];
+        for (int r = 0; r < 4; ++r) scr[scr_at(l4, r, nt * 16 + l15)] = Cs[nt][r];
       wave_lds_sync();
-
-      for (int j = 0; j < nqs; ++j) {
-        const int rb = __builtin_amdgcn_readlane(sd.y, j), re = __builtin_amdgcn_readlane(sd.z, j);
-        const int i1 = __builtin_amdgcn_readlane(my_i1, j);
-        const int nr = re - rb;
-        // dD A operand: C_h^T[b' = l15][(j1 j2) = 4 s + l4] = C_h[j][s][l4][l15]
-        float CT[4];
+    }
+    // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4] and the dB A operand rows
+    float CT[4], AT0, AT1;
+    auto slice_begin = [&](int j) {
 #pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[((j * 4 + s4) * 4 + l4) * 16 + l15];
-        const int i3v = uniq_i3[rb + (lane < nr ? lane : 0)];  // lane k: i3 of row k of the slice
-        const float* Es = dE + (uint32_t)rb * 128u;
-        f32x4 dC = {0.f, 0.f, 0.f, 0.f};
-        for (int r0 = 0; r0 < nr; r0 += 2) {
-          const bool has1 = r0 + 1 < nr;
-          const int u1 = has1 ? r0 + 1 : r0;
-          const bool live = !rowsel || has1;
-          const float* Ea = Es + (uint32_t)r0 * 128u;
-          const float* Eb = Es + (uint32_t)u1 * 128u;
-          const int i3a = __builtin_amdgcn_readlane(i3v, r0), i3b = __builtin_amdgcn_readlane(i3v, u1);
-          // dD B operand: lanes 0-7 of each 16 take row r0, lanes 8-15 row r0 + 1
-          const float* Em = rowsel ? Eb : Ea;
-          float EB[4];
+      for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[scr_at(j, s4, l4 * 16 + l15)];
+      const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(q_i1, j) * 128u + (uint32_t)(l4 * 32 + l15);
+      AT0 = Aj[0];
+      AT1 = Aj[16];
+    };
+    slice_begin(0);
+    f32x4 dC = {0.f, 0.f, 0.f, 0.f};
+    auto pair_compute = [&](const BwPair& X) {
+      f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int s4 = 0; s4 < 4; ++s4) {
-            const float v = Em[o_eb + 32 * s4];
-            EB[s4] = live ? v : 0.f;
-          }
-          // dC operands: K index (row, j3) with row = l4 >> 1, j3 = 4 (l4 & 1) + k, so each lane
-          // reads four consecutive floats of its dE row and of its G3 slice
-          const float4 e4 = *(const float4*)((prow ? Eb : Ea) + o_e4);
-          const float4 d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
-          const bool ez = prow && !has1;
-          const int i3m = rowsel && has1 ? i3b : i3a;
-          f32x4 dd = {0.f, 0.f, 0.f, 0.f};
+      for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], X.eb[s4], dd, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.x, X.d4.x, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.y, X.d4.y, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.z, X.d4.z, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.w, X.d4.w, dC, 0, 0, 0);
+      // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7].  The two rows'
+      // lanes add in separate instructions: a 64-lane LDS atomic always has a
+      // 2-way bank conflict, which costs far more than two conflict-free halves.
+      float* gp = g3acc + (uint32_t)X.i3m * 128u;
+      if (!rowsel) {
 #pragma unroll
-          for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], EB[s4], dd, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.x, d4.x, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.y, d4.y, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.z, d4.z, dC, 0, 0, 0);
-          dC = __builtin_amdgcn_mfma_f32_16x16x4f32(ez ? 0.f : e4.w, d4.w, dC, 0, 0, 0);
-          // dd: lane holds dD_h[b' = 4 l4 + r][row rowsel][j3 = lane & 7]
-          if (live) {
-            float* gp = g3acc + (uint32_t)i3m * 128u + (uint32_t)(32 * l4 + (lane & 7));
+        for (int r = 0; r < 4; ++r) atomicAdd(gp + o_g3[r], dd[r]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (X.live && rowsel) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) atomicAdd(gp + r * 8, dd[r]);
-          }
-        }
-        // dC: lane holds dC_h[j1 = l4][j2 = r][b' = l15]
-        // dB_h += A^T . dC_h  (M = a, N = (j2, b'), K = j1)
-        const float* Aj = G1t + (uint32_t)i1 * 128u + (uint32_t)(l4 * 32 + l15);
-        const float AT0 = Aj[0], AT1 = Aj[16];
+        for (int r = 3; r >= 0; --r) atomicAdd(gp + o_g3[r], dd[r]);
+      }
+    };
+    // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
+    auto slice_end = [&](int j) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          dB[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT0, dC[nt], dB[nt], 0, 0, 0);
-          dB[4 + nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT1, dC[nt], dB[4 + nt], 0, 0, 0);
-        }
-        // keep dC_h of slice j for the quad's dA: slot j, layout [j1][j2][b']
-        wave_lds_sync();
-#pragma unroll
-        for (int r = 0; r < 4; ++r) scr[((j * 4 + l4) * 4 + r) * 16 + l15] = dC[r];
+      for (int nt = 0; nt < 4; ++nt) {
+        dB[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT0, dC[nt], dB[nt], 0, 0, 0);
+        dB[4 + nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT1, dC[nt], dB[4 + nt], 0, 0, 0);
       }
       wave_lds_sync();
-      // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32); B operand
-      // B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15] read from G2 (L1/L2)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) scr[scr_at(j, l4, r * 16 + l15)] = dC[r];
+      dC = f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    // row pairs of the quad in order, two per iteration; the operands of the
+    // next pair are always in flight while one is computed (indices clamped, so
+    // every load is unconditional and in bounds)
+    int cj = 0;
+    for (int P = 0; P < np; P += 2) {
+      pair_load(XB, P + 1 < np ? P + 1 : np - 1);
+      {
+        const int j = (P >= cp1) + (P >= cp2) + (P >= cp3);
+        if (j != cj) {
+          slice_end(cj);
+          slice_begin(j);
+          cj = j;
+        }
+        pair_compute(XA);
+      }
+      pair_load(XA, P + 2 < np ? P + 2 : np - 1);
+      if (P + 1 < np) {
+        const int j = (P + 1 >= cp1) + (P + 1 >= cp2) + (P + 1 >= cp3);
+        if (j != cj) {
+          slice_end(cj);
+          slice_begin(j);
+          cj = j;
+        }
+        pair_compute(XB);
+      }
+    }
+    slice_end(cj);
+    wave_lds_sync();
+    // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32)
+    {
       const int ms = l15 >> 2, mj1 = lane & 3;
       const bool m_ok = ms < nqs;
-      f32x4 dA[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+      f32x4 dA0 = {0.f, 0.f, 0.f, 0.f}, dA1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s2 = 0; s2 < 16; ++s2) {
         const int k = 4 * s2 + l4;
-        const float v = scr[((ms * 4 + mj1) * 4 + (k >> 4)) * 16 + (k & 15)];
+        const float v = scr[scr_at(ms, mj1, k)];
         const float av = m_ok ? v : 0.f;
-        const float b0 = Bg[(l15 * 4 + (k >> 4)) * 32 + (k & 15)];
-        const float b1 = Bg[((16 + l15) * 4 + (k >> 4)) * 32 + (k & 15)];
-        dA[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b0, dA[0], 0, 0, 0);
-        dA[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b1, dA[1], 0, 0, 0);
+        dA0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[2 * s2 + 0], dA0, 0, 0, 0);
+        dA1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[2 * s2 + 1], dA1, 0, 0, 0);
       }
       // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]
       if (l4 < nqs) {
-        float* dst = dApart + ((size_t)h * nsl_cap + (f + qd + l4)) * 128 + l15;
+        float* dst = dApart + ((size_t)h * nsl_cap + (sb + l4)) * 128 + l15;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          dst[r * 32] = dA[0][r];
-          dst[r * 32 + 16] = dA[1][r];
+          dst[r * 32] = dA0[r];
+          dst[r * 32 + 16] = dA1[r];
         }
       }
-      wave_lds_sync();
     }
-    // dB_h partial of this chunk: lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
-    float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c)) * 2048;
+    wave_lds_sync();
+    qd += 4;
+    if (qd >= ns) {
+      // end of the chunk: dB_h partial, lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
+      float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c)) * 2048;
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+        for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
+          for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
+      c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
+      qd = 0;
+      if (c >= 0) {
+        const int4 ch = chunks[c_lo + c];
+        f = __builtin_amdgcn_readfirstlane(ch.x);
+        ns = __builtin_amdgcn_readfirstlane(ch.y);
+        run = __builtin_amdgcn_readfirstlane(ch.z);
+      }
+    }
   }
   __syncthreads();
   float* gdst = g3part + (size_t)blockIdx.x * acc_n;
@@ -263,7 +383,7 @@ __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __r
   if (e >= acc_n) return;
   float acc = 0.f;
   for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
-  const int i3 = e >> 7, bp = (e >> 3) & 15, j3 = e & 7;
+  const int i3 = e >> 7, bp = g3_unslot((e >> 3) & 15), j3 = e & 7;
   dG3[(((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3] = acc;
 }
 
