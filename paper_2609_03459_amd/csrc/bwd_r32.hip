@@ -24,8 +24,8 @@ constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
 
 // The LDS dG3 accumulator stores rank row b' of a table row i3 at slot
 // p(b') = 4 (b' >> 2) + ((b' + (b' >> 2)) & 3).  A dD tile puts b' = 4 l4 + r in
-// register r of lane group l4, so in step r the four lane groups of one row add
-// to four different 8-bank groups: each 32-lane add is free of bank conflicts.
+// register r of lane group l4, so in step r the four lane groups of one row
+// touch four different 8-bank groups.
 __device__ __forceinline__ int g3_unslot(int p) {
   const int g = p >> 2;
   return 4 * g + (((p & 3) - g) & 3);
@@ -37,6 +37,34 @@ __device__ __forceinline__ int g3_unslot(int p) {
 // put at most two of the 64 lanes on one bank.
 __device__ __forceinline__ uint32_t scr_at(int sl, int j1, int j2b) {
   return (uint32_t)(sl * 256 + j1 * 64 + (j2b ^ ((8 * sl + 10 * j1) & 63)));
+}
+
+// p[o[r]] += v[r] for r < 4 on LDS floats shared by the workgroup's waves.  A
+// float ds_add is slow on this LDS, integer compare-and-swap is not: read, add,
+// swap, and retry only the lanes whose word changed in between (lock-free; a
+// failed swap means another wave's add landed, so the loop always progresses).
+__device__ __forceinline__ void lds_add4(float* p, const uint32_t o[4], f32x4 v) {
+  uint32_t* u = reinterpret_cast<uint32_t*>(p);
+  uint32_t seen[4], got[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) seen[r] = __hip_atomic_load(u + o[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    got[r] = seen[r];
+    __hip_atomic_compare_exchange_strong(u + o[r], &got[r], __float_as_uint(__uint_as_float(seen[r]) + v[r]),
+                                         __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    uint32_t cur = got[r];
+    bool done = cur == seen[r];
+    while (!done) {
+      uint32_t expect = cur;
+      done = __hip_atomic_compare_exchange_strong(u + o[r], &expect, __float_as_uint(__uint_as_float(cur) + v[r]),
+                                                  __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      cur = expect;
+    }
+  }
 }
 
 template <typename T>
@@ -228,19 +256,8 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.y, X.d4.y, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.z, X.d4.z, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.w, X.d4.w, dC, 0, 0, 0);
-      // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7].  The two rows'
-      // lanes add in separate instructions: a 64-lane LDS atomic always has a
-      // 2-way bank conflict, which costs far more than two conflict-free halves.
-      float* gp = g3acc + (uint32_t)X.i3m * 128u;
-      if (!rowsel) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) atomicAdd(gp + o_g3[r], dd[r]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (X.live && rowsel) {
-#pragma unroll
-        for (int r = 3; r >= 0; --r) atomicAdd(gp + o_g3[r], dd[r]);
-      }
+      // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7]
+      if (X.live) lds_add4(g3acc + (uint32_t)X.i3m * 128u, o_g3, dd);
     };
     // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
     auto slice_end = [&](int j) {
