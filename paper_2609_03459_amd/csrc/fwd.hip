@@ -85,143 +85,188 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
 
 
 // ---------------------------------------------------------------------------
-// MFMA forward for d = (4, 4, 8), R = 32 (D = 128).  Every wave is an
-// independent worker over chunks of FWD_CHUNK slices:
-//   * B = G2[t][i2] (32 x 128) stays in 64 VGPRs while consecutive slices share
-//     (t, i2) (lane l holds columns l and l + 64 of every row k);
-//   * stage 1, C = A.B (4 x 128), per prefix group with v_mfma_f32_4x4x1f32
-//     (16 blocks of 4x4; block = 4 columns, rows = j1), 64 instructions;
-//   * C goes through a per-wave LDS tile (padded) into the A operand of
-//     stage 2, C' = (j1 j2) x b = 16 x 32;
-//   * stage 2, E_u = C'.D_u for two rows at a time with v_mfma_f32_16x16x4f32
-//     (N = 2 rows x 8 columns), 8 instructions per pair.
+// MFMA forward for d = (4, 4, 8), R = 32 (D = 128).  Persistent waves claim
+// chunks (up to 32 slices of one (t, i2) run, so B = G2[t][i2] stays in VGPRs)
+// and work through them four slices ("a quad") at a time:
+//   * stage 1: Cstack (16 x 128) = Astack (16 x 32) . B (32 x 128) with
+//     v_mfma_f32_16x16x4f32, rows (slice, j1), columns (j2, b); 64 instructions;
+//   * Cstack goes through a per-wave XOR-swizzled LDS tile into the B operand of
+//     stage 2, C'^T (b x jj) of one slice;
+//   * stage 2 per row pair: E^T (rows x j3, jj) = D^T . C'^T, 8 instructions;
+//     each lane ends up with four consecutive floats of one E row (one 16-byte
+//     store).
+// The next row pair's G3 operands are in flight while a pair is computed.
 // ---------------------------------------------------------------------------
 constexpr int F32_WAVES = 4;
-constexpr int F32_CSTRIDE = 33;              // padded b stride of the C tile
-constexpr int F32_CTILE = 4 * 4 * F32_CSTRIDE;  // floats per wave
+constexpr int F32_SCR = 2048;  // per-wave LDS floats: [slice 4][j1 4][j2 4][b 32]
 
-__device__ __forceinline__ void f32_load_A(const float* G1, int t, int i1, int n1, int lane, float* A) {
-  const float4* Ag = reinterpret_cast<const float4*>(G1 + (int64_t)(t * n1 + i1) * 128 + (lane & 3) * 32);
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    float4 v = Ag[m];
-    A[4 * m + 0] = v.x;
-    A[4 * m + 1] = v.y;
-    A[4 * m + 2] = v.z;
-    A[4 * m + 3] = v.w;
-  }
+// XOR swizzle of the b index: both the stage-1 writes and the stage-2 operand
+// reads put at most two lanes on one bank
+__device__ __forceinline__ uint32_t fscr_at(int sl, int j1, int j2, int b) {
+  return (uint32_t)(sl * 512 + j1 * 128 + j2 * 32 + (b ^ ((8 * sl + 4 * j1 + 16 * j2) & 31)));
 }
 
-__global__ void __launch_bounds__(64 * F32_WAVES, 3) k_fwd_r32(ShapeArgs s, const float* __restrict__ G1,
-                                                           const float* __restrict__ G2,
-                                                           const float* __restrict__ G3,
-                                                           const int4* __restrict__ slices,
-                                                           const uint32_t* __restrict__ uniq_key,
-                                                           int32_t* __restrict__ ctr, float* __restrict__ E) {
-  __shared__ float ctile[F32_WAVES][F32_CTILE];
+__global__ void __launch_bounds__(64 * F32_WAVES, 2)
+    k_fwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
+              const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
+              const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
+              const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ E) {
+  __shared__ float scr_all[F32_WAVES * F32_SCR];
   const int lane = lane_id();
-  const int wv = threadIdx.x >> 6;
-  float* Ct = ctile[wv];
-  const int me = blockIdx.x * F32_WAVES + wv;
+  const int wave = threadIdx.x >> 6;
+  float* scr = scr_all + wave * F32_SCR;
+  const int me = blockIdx.x * F32_WAVES + wave;
   const int nworkers = gridDim.x * F32_WAVES;
-  const int nsl = ctr[C_NSLICES];
-  const int nchunks = (nsl + FWD_CHUNK - 1) / FWD_CHUNK;
-  int victim = 0;
-  int cur_ti2 = -1, cur_pg = -1;
-  float Bl[32], Bh[32];  // B[k][lane], B[k][lane + 64]
-  float Cop[8];          // stage-2 A operand: C'[lane % 16][4 s + lane / 16]
-  const int jr = (lane & 15) >> 2, j2r = lane & 3, kq = lane >> 4;  // C' read coordinates
-  const int sel = (lane & 15) >> 3, j3 = lane & 7;                    // stage-2 B operand / output column
-  while (true) {
-    const int c = claim_chunk_wave(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nchunks, nworkers, me, &victim);
-    if (c < 0) break;
-    const int s0 = c * FWD_CHUNK;
-    const int ns = (s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl) - s0;
-    // the chunk's slice descriptors, one per lane
-    int4 myd = make_int4(0, 0, 0, 0);
-    if (lane < ns) myd = slices[s0 + lane];
-    // prefetch of slice 0: A and the uniq keys of its rows (lane r holds row rb + r)
-    float An[32];
-    uint32_t keyn = 0;
-    {
-      const int p = __shfl(myd.x, 0, 64), rb = __shfl(myd.y, 0, 64), re = __shfl(myd.z, 0, 64);
-      const uint32_t key = (uint32_t)__shfl(myd.w, 0, 64);
-      const int t = key / s.n12, q = key % s.n12;
-      if (p != cur_pg) f32_load_A(G1, t, q / s.n2, s.n1, lane, An);
-      if (lane < re - rb) keyn = uniq_key[rb + lane];
+  const int nch = (int)run_base[s.T * s.n2];
+  const int l15 = lane & 15, l4 = lane >> 4;
+  const int orow = l4 >> 1;  // E row of the pair this lane's output belongs to
+  // stage-2 A operand: lane m = l15 = (row sel, j3), K index b = 4 s + l4
+  const int asel = l15 >> 3;
+  const uint32_t o_d = (uint32_t)(l4 * 8 + (l15 & 7));
+  const uint32_t o_e = (uint32_t)(l15 * 8 + 4 * (l4 & 1));  // E store offset inside a row
+
+  int cursor = 0;
+  int cur_run = -1;
+  float Bop[64];  // B[a = 4 s + l4][16 nt + l15], (s, nt) -> 8 s + nt
+  int q_rb = 0, q_nr = 0, i3A = 0, i3B = 0;
+  int cp1 = 0, cp2 = 0, cp3 = 0, np = 0;
+  int tcur = 0;
+  const float* G3t = G3;
+
+  struct FPair {
+    float d[8];
+    int eoff;   // float offset of this lane's E store
+    bool live;  // this lane's output row exists
+  };
+  auto pair_load = [&](FPair& X, int P) {
+    const int pj = (P >= cp1) + (P >= cp2) + (P >= cp3);
+    const int pr = 2 * (P - (pj == 0 ? 0 : (pj == 1 ? cp1 : (pj == 2 ? cp2 : cp3))));
+    const int rb = __builtin_amdgcn_readlane(q_rb, pj), nr = __builtin_amdgcn_readlane(q_nr, pj);
+    const bool has1 = pr + 1 < nr;
+    const int i3v = pj < 2 ? i3A : i3B;
+    const int li = (pj & 1) * 32 + pr;
+    const int i3a = __builtin_amdgcn_readlane(i3v, li);
+    const int i3b = __builtin_amdgcn_readlane(i3v, has1 ? li + 1 : li);
+    const float* Dg = G3t + (uint32_t)(asel ? i3b : i3a) * 256u + o_d;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) X.d[k] = Dg[32 * k];
+    X.eoff = (rb + pr + orow) * 128 + (int)o_e;
+    X.live = has1 || orow == 0;
+  };
+
+  int c = claim_chunk_wave(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nch, nworkers, me, &cursor);
+  int f = 0, ns = 0, run = -1, qd = 0;
+  if (c >= 0) {
+    const int4 ch = chunks[c];
+    f = __builtin_amdgcn_readfirstlane(ch.x);
+    ns = __builtin_amdgcn_readfirstlane(ch.y);
+    run = __builtin_amdgcn_readfirstlane(ch.z);
+  }
+  while (c >= 0) {
+    if (run != cur_run) {
+      const float* Bg = G2 + (uint32_t)run * 4096u + (uint32_t)(l4 * 128 + l15);
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4)
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) Bop[8 * s4 + nt] = Bg[s4 * 512 + 16 * nt];
+      cur_run = run;
+      tcur = run / s.n2;
+      G3t = G3 + (uint32_t)(tcur * s.n3) * 256u;
     }
-    for (int j = 0; j < ns; ++j) {
-      const int p = __shfl(myd.x, j, 64), rb = __shfl(myd.y, j, 64), re = __shfl(myd.z, j, 64);
-      const uint32_t key = (uint32_t)__shfl(myd.w, j, 64);
-      const int t = key / s.n12, q = key % s.n12;
-      const int i2 = q % s.n2;
-      const int ti2 = t * s.n2 + i2;
-      const int i3c = decode_key(keyn, s.Npad, s.n2, s.n3).i3;  // i3 of row rb + lane
-      const bool need_c = p != cur_pg;
-      if (ti2 != cur_ti2) {
-        const float* Bg = G2 + (int64_t)ti2 * 4096;
+    const int nqs = ns - qd < 4 ? ns - qd : 4;
+    const int sb = f + qd;
+    {
+      const int sl = sb + (lane < nqs ? lane : 0);
+      const int4 sd = slices[sl];
+      q_rb = sd.y;
+      q_nr = lane < nqs ? sd.z - sd.y : 0;
+    }
+    {
+      const int ja = lane >> 5, k = lane & 31;
+      const int rba = __builtin_amdgcn_readlane(q_rb, 0), rbb = __builtin_amdgcn_readlane(q_rb, 1);
+      const int rbc = __builtin_amdgcn_readlane(q_rb, 2), rbd = __builtin_amdgcn_readlane(q_rb, 3);
+      const int nra = __builtin_amdgcn_readlane(q_nr, 0), nrb = __builtin_amdgcn_readlane(q_nr, 1);
+      const int nrc = __builtin_amdgcn_readlane(q_nr, 2), nrd = __builtin_amdgcn_readlane(q_nr, 3);
+      const int rA = ja ? rbb : rba, nA = ja ? nrb : nra;
+      const int rB = ja ? rbd : rbc, nB = ja ? nrd : nrc;
+      i3A = uniq_i3[rA + (k < nA ? k : 0)];
+      i3B = uniq_i3[rB + (k < nB ? k : 0)];
+      cp1 = (nra + 1) >> 1;
+      cp2 = cp1 + ((nrb + 1) >> 1);
+      cp3 = cp2 + ((nrc + 1) >> 1);
+      np = cp3 + ((nrd + 1) >> 1);
+    }
+    // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
+    const int aj = l15 >> 2;
+    const float* Ag = G1 + (uint32_t)(tcur * s.n1 + slice_i1[sb + (aj < nqs ? aj : 0)]) * 128u +
+                      (uint32_t)((lane & 3) * 32 + l4);
+    float Aop[8];
 #pragma unroll
-        for (int k = 0; k < 32; ++k) {
-          Bl[k] = Bg[k * 128 + lane];
-          Bh[k] = Bg[k * 128 + 64 + lane];
+    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
+    FPair XA, XB;
+    pair_load(XA, 0);
+    // stage 1 (rows of slices beyond nqs are computed from a repeated slice and never read)
+    {
+      f32x4 Cs[8];
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4)
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt)
+          Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[s4], Bop[8 * s4 + nt], Cs[nt], 0, 0, 0);
+      // lane holds C[slice l4][j1 r][j2 = nt >> 1][b = 16 (nt & 1) + l15]
+#pragma unroll
+      for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) scr[fscr_at(l4, r, nt >> 1, 16 * (nt & 1) + l15)] = Cs[nt][r];
+      wave_lds_sync();
+    }
+    // stage-2 B operand of slice j: C'^T[b = 4 s + l4][jj = l15]
+    float CT[8];
+    auto slice_begin = [&](int j) {
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr[fscr_at(j, l15 >> 2, l15 & 3, 4 * s4 + l4)];
+    };
+    slice_begin(0);
+    auto pair_compute = [&](const FPair& X) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[s4], CT[s4], acc, 0, 0, 0);
+      // lane holds E[row orow][jj = l15][j3 = 4 (l4 & 1) + r]
+      if (X.live) *reinterpret_cast<float4*>(E + (uint32_t)X.eoff) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    };
+    int cj = 0;
+    for (int P = 0; P < np; P += 2) {
+      pair_load(XB, P + 1 < np ? P + 1 : np - 1);
+      {
+        const int j = (P >= cp1) + (P >= cp2) + (P >= cp3);
+        if (j != cj) {
+          slice_begin(j);
+          cj = j;
         }
-        cur_ti2 = ti2;
+        pair_compute(XA);
       }
-      if (need_c) {
-        f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int k = 0; k < 32; ++k) {
-          c0 = __builtin_amdgcn_mfma_f32_4x4x1f32(An[k], Bl[k], c0, 0, 0, 0);
-          c1 = __builtin_amdgcn_mfma_f32_4x4x1f32(An[k], Bh[k], c1, 0, 0, 0);
+      pair_load(XA, P + 2 < np ? P + 2 : np - 1);
+      if (P + 1 < np) {
+        const int j = (P + 1 >= cp1) + (P + 1 >= cp2) + (P + 1 >= cp3);
+        if (j != cj) {
+          slice_begin(j);
+          cj = j;
         }
-        // lane holds C[j1 = r][col = lane + 64 h], col = j2 * 32 + b
-        wave_lds_sync();
-        const int b = lane & 31, j2lo = lane >> 5;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          Ct[r * (4 * F32_CSTRIDE) + j2lo * F32_CSTRIDE + b] = c0[r];
-          Ct[r * (4 * F32_CSTRIDE) + (j2lo + 2) * F32_CSTRIDE + b] = c1[r];
-        }
-        wave_lds_sync();
-#pragma unroll
-        for (int q4 = 0; q4 < 8; ++q4) Cop[q4] = Ct[jr * (4 * F32_CSTRIDE) + j2r * F32_CSTRIDE + 4 * q4 + kq];
-        cur_pg = p;
+        pair_compute(XB);
       }
-      // prefetch slice j + 1 (its A once this one's stage 1 is done, and its row keys)
-      if (j + 1 < ns) {
-        const int pn = __shfl(myd.x, j + 1, 64), rbn = __shfl(myd.y, j + 1, 64), ren = __shfl(myd.z, j + 1, 64);
-        const uint32_t kn = (uint32_t)__shfl(myd.w, j + 1, 64);
-        const int tn = kn / s.n12, qn = kn % s.n12;
-        if (pn != p) f32_load_A(G1, tn, qn / s.n2, s.n1, lane, An);
-        keyn = lane < ren - rbn ? uniq_key[rbn + lane] : 0u;
-      }
-      // rows in pairs; G3 operands of the next pair are loaded before this pair's MFMAs
-      const int nr = re - rb;
-      const float* G3t = G3 + (int64_t)t * s.n3 * 256;
-      auto load_pair = [&](int r0, float* Dv) {
-        const bool has1 = r0 + 1 < nr;
-        const int rr = sel ? (has1 ? r0 + 1 : r0) : r0;
-        const int i3 = __shfl(i3c, rr, 64);
-        const float* Dg = G3t + i3 * 256;
-        const bool live = !sel || has1;
-#pragma unroll
-        for (int q4 = 0; q4 < 8; ++q4) Dv[q4] = live ? Dg[(4 * q4 + kq) * 8 + j3] : 0.f;
-      };
-      float Dc[8], Dn[8];
-      load_pair(0, Dc);
-      for (int r0 = 0; r0 < nr; r0 += 2) {
-        if (r0 + 2 < nr) load_pair(r0 + 2, Dn);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int q4 = 0; q4 < 8; ++q4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Cop[q4], Dc[q4], acc, 0, 0, 0);
-        const bool has1 = r0 + 1 < nr;
-        if (!sel || has1) {
-          float* Eo = E + (int64_t)(rb + r0 + sel) * 128 + (4 * kq) * 8 + j3;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) Eo[r * 8] = acc[r];
-        }
-#pragma unroll
-        for (int q4 = 0; q4 < 8; ++q4) Dc[q4] = Dn[q4];
+    }
+    wave_lds_sync();
+    qd += 4;
+    if (qd >= ns) {
+      c = claim_chunk_wave(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nch, nworkers, me, &cursor);
+      qd = 0;
+      if (c >= 0) {
+        const int4 ch = chunks[c];
+        f = __builtin_amdgcn_readfirstlane(ch.x);
+        ns = __builtin_amdgcn_readfirstlane(ch.y);
+        run = __builtin_amdgcn_readfirstlane(ch.z);
       }
     }
   }
@@ -337,6 +382,13 @@ hipError_t launch_pool(const Shape& s, const float* E, const int32_t* inv, const
   return hipGetLastError();
 }
 
+bool fwd_r32_supported(const Shape& s, int64_t max_indices) {
+  // 32-bit float offsets into E (rows x 128), G1 and G3; workers fit the counter area
+  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
+         (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) &&
+         persistent_grid() * 2 * F32_WAVES <= MAX_PERSIST_WG;
+}
+
 hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           const int64_t* offsets, int64_t M, int64_t B, float* out, const Prof& prof,
                           hipStream_t st) {
@@ -346,11 +398,12 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
     if (e != hipSuccess) return e;
     e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_FWD_STEAL), 1, 0u, st);
     if (e != hipSuccess) return e;
-    if (s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32) {
-      const int blocks = (persistent_grid() * 12) / F32_WAVES;
+    if (fwd_r32_supported(s, M)) {
+      const int blocks = persistent_grid() * 2;  // two workgroups of four waves per CU
       prof_begin(prof, K_FWD_FUSED, st);
       hipLaunchKernelGGL(k_fwd_r32, dim3(blocks), dim3(64 * F32_WAVES), 0, st, shape_args(s), G1, G2, G3,
-                         (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E);
+                         (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
+                         (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.E);
       prof_end(prof, K_FWD_FUSED, st);
       e = hipGetLastError();
       if (e != hipSuccess) return e;
