@@ -92,6 +92,65 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
   }
 }
 
+// D = 128: a lane owns two columns (one 8-byte load per occurrence), the bag
+// index of each occurrence is read into a scalar register so every dV row is a
+// uniform base, and 16 rows are in flight before they are summed in order.
+__global__ void __launch_bounds__(64) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+                                                  const uint32_t* __restrict__ sorted_pos,
+                                                  const int32_t* __restrict__ bag_of,
+                                                  const int32_t* __restrict__ occ_start,
+                                                  const int32_t* __restrict__ ctr, float* __restrict__ dE,
+                                                  float* __restrict__ part) {
+  const int nvalid = ctr[C_NVALID];
+  const int c = blockIdx.x;
+  const int i0 = c * SEG_CHUNK;
+  if (i0 >= nvalid) return;
+  const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
+  const int lane = lane_id();
+  auto flush = [&](int u, float2 acc) {
+    const int lo = occ_start[u], hi = occ_start[u + 1];
+    float* dst;
+    if (lo >= i0 && hi <= i1)
+      dst = dE + (size_t)u * 128;
+    else if (lo < i0)
+      dst = part + ((size_t)c * 2 + 0) * 128;
+    else
+      dst = part + ((size_t)c * 2 + 1) * 128;
+    reinterpret_cast<float2*>(dst)[lane] = acc;
+  };
+  int cur = sorted_uid[i0];
+  float2 acc = make_float2(0.f, 0.f);
+  for (int base = i0; base < i1; base += 64) {
+    const int i = base + lane;
+    const int my_u = i < i1 ? sorted_uid[i] : -1;
+    const int my_b = i < i1 ? bag_of[sorted_pos[i]] : 0;
+    const int cnt = i1 - base < 64 ? i1 - base : 64;
+    for (int k0 = 0; k0 < cnt; k0 += 16) {
+      float2 v[16];
+#pragma unroll
+      for (int kk = 0; kk < 16; ++kk) {
+        const int k = k0 + kk < cnt ? k0 + kk : k0;  // clamped: every load is unconditional
+        const int b = __builtin_amdgcn_readlane(my_b, k);
+        v[kk] = reinterpret_cast<const float2*>(dV + (size_t)b * 128)[lane];
+      }
+#pragma unroll
+      for (int kk = 0; kk < 16; ++kk) {
+        if (k0 + kk < cnt) {
+          const int u = __builtin_amdgcn_readlane(my_u, k0 + kk);
+          if (u != cur) {
+            flush(cur, acc);
+            cur = u;
+            acc = make_float2(0.f, 0.f);
+          }
+          acc.x += v[kk].x;
+          acc.y += v[kk].y;
+        }
+      }
+    }
+  }
+  flush(cur, acc);
+}
+
 // Rows whose occurrences span several chunks: chunk c0 + 1, where c0 holds the
 // row's first occurrence, finishes the row from c0's tail partial and the head
 // partials of every following chunk.  Four waves split the chunk range; each
@@ -255,9 +314,14 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
   prof_begin(prof, K_SEG_SUM, st);
-  hipLaunchKernelGGL(k_seg_dE, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
-                     (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
-                     (const int32_t*)w.ctr, s.D, dE, w.seg_part);
+  if (s.D == 128)
+    hipLaunchKernelGGL(k_seg_dE128, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
+                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+                       (const int32_t*)w.ctr, dE, w.seg_part);
+  else
+    hipLaunchKernelGGL(k_seg_dE, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
+                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+                       (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   prof_end(prof, K_SEG_SUM, st);
   hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);

@@ -90,7 +90,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
               float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap) {
   extern __shared__ float lds[];
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int acc_n = s.n3 * 128;
   float* g3acc = lds;  // [n3][slot p(b')][8]
   float* scr = lds + acc_n + wave * BW_SCR;

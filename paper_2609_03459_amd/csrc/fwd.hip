@@ -113,7 +113,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 2)
               const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ E) {
   __shared__ float scr_all[F32_WAVES * F32_SCR];
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* scr = scr_all + wave * F32_SCR;
   const int me = blockIdx.x * F32_WAVES + wave;
   const int nworkers = gridDim.x * F32_WAVES;
@@ -315,6 +315,61 @@ __global__ void __launch_bounds__(256) k_pool4(const float4* __restrict__ E, con
   }
 }
 
+// D = 128: two bags per wave, 32 lanes and one float4 column each.  Each half
+// reads up to 32 of its bag's row indices in one load; 16 rows per half are in
+// flight before they are summed in occurrence order.
+__global__ void __launch_bounds__(256) k_pool128(const float4* __restrict__ E, const int32_t* __restrict__ inv,
+                                                 const int64_t* __restrict__ offsets, int64_t M, int64_t NB,
+                                                 float4* __restrict__ out) {
+  const int lane = lane_id();
+  const int half = lane >> 5, sub = lane & 31;
+  const int64_t gb = ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)) * 2 + half;
+  const bool bag_ok = gb < NB;
+  int64_t lo = 0, hi = 0;
+  if (bag_ok) {
+    if (offsets) {
+      lo = offsets[gb];
+      hi = offsets[gb + 1];
+      lo = lo < 0 ? 0 : (lo > M ? M : lo);
+      hi = hi < lo ? lo : (hi > M ? M : hi);
+    } else {
+      lo = gb;
+      hi = gb + 1;
+    }
+  }
+  const int cnt = (int)(hi - lo);
+  const int c0 = __builtin_amdgcn_readlane(cnt, 0), c1 = __builtin_amdgcn_readlane(cnt, 32);
+  const int cmax = c0 > c1 ? c0 : c1;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int base = 0; base < cmax; base += 32) {
+    const int my_u = base + sub < cnt ? inv[lo + base + sub] : -1;
+    const int nb = cmax - base < 32 ? cmax - base : 32;
+    for (int k0 = 0; k0 < nb; k0 += 16) {
+      float4 v[16];
+#pragma unroll
+      for (int kk = 0; kk < 16; ++kk) {
+        const int k = k0 + kk;
+        const int uA = __builtin_amdgcn_readlane(my_u, k & 31), uB = __builtin_amdgcn_readlane(my_u, 32 + (k & 31));
+        const int u = half ? uB : uA;
+        if (base + k < cnt) v[kk] = E[(size_t)(u < 0 ? 0 : u) * 32 + sub];  // invalid rows: row 0, skipped
+      }
+#pragma unroll
+      for (int kk = 0; kk < 16; ++kk) {
+        const int k = k0 + kk;
+        const int uA = __builtin_amdgcn_readlane(my_u, k & 31), uB = __builtin_amdgcn_readlane(my_u, 32 + (k & 31));
+        const int u = half ? uB : uA;
+        if (base + k < cnt && u >= 0) {
+          acc.x += v[kk].x;
+          acc.y += v[kk].y;
+          acc.z += v[kk].z;
+          acc.w += v[kk].w;
+        }
+      }
+    }
+  }
+  if (bag_ok) out[gb * 32 + sub] = acc;
+}
+
 __global__ void __launch_bounds__(256) k_pool1(const float* __restrict__ E, const int32_t* __restrict__ inv,
                                                const int64_t* __restrict__ offsets, int64_t M, int64_t NB, int D,
                                                float* __restrict__ out) {
@@ -358,7 +413,10 @@ hipError_t launch_pool(const Shape& s, const float* E, const int32_t* inv, const
   const int64_t NB = (int64_t)s.T * B;
   if (NB <= 0) return hipSuccess;
   prof_begin(prof, K_POOL, st);
-  if (s.D % 4 == 0) {
+  if (s.D == 128) {
+    hipLaunchKernelGGL(k_pool128, dim3((unsigned)((NB + 7) / 8)), dim3(256), 0, st,
+                       reinterpret_cast<const float4*>(E), inv, offsets, M, NB, reinterpret_cast<float4*>(out));
+  } else if (s.D % 4 == 0) {
     const int D4 = s.D / 4;
     int lpb = 1;
     while (lpb < D4 && lpb < 64) lpb <<= 1;
