@@ -349,28 +349,58 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 }
 
 // dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2).
-// Four groups of 128 threads take i2 = g, g + 4, ...; their sums are combined
-// in a fixed order.
+// The block first lists the slices of (t, i1) in i2 order (up to 512 prefixes
+// per round), then four groups of 128 threads take list entries g, g + 4, ...
+// with eight loads in flight per thread; the group sums are combined in a
+// fixed order.
+constexpr int G1_LIST = 4096;  // 512 prefixes x at most 8 slices each (n3 <= 256)
+
 __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                    const uint32_t* __restrict__ dense_base,
                                                    const float* __restrict__ dApart, int nsl_cap,
                                                    float* __restrict__ dG1) {
+  __shared__ int list[G1_LIST];
+  __shared__ uint32_t wsum[8];
   __shared__ float red[4][128];
   const int ti1 = blockIdx.x;  // t * n1 + i1
   const int t = ti1 / s.n1, i1 = ti1 % s.n1;
   const int g = threadIdx.x >> 7, e = threadIdx.x & 127;
-  float a0 = 0.f, a1 = 0.f;
-  for (int i2 = g; i2 < s.n2; i2 += 4) {
-    const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
-    const uint32_t cnt = dense_cnt[slot];
-    if (!cnt) continue;
-    const uint32_t b = dense_base[slot];
-    for (uint32_t k = 0; k < cnt; ++k) {
-      a0 += dApart[((int64_t)0 * nsl_cap + b + k) * 128 + e];
-      a1 += dApart[((int64_t)1 * nsl_cap + b + k) * 128 + e];
+  const float* P0 = dApart + e;
+  const float* P1 = dApart + (size_t)nsl_cap * 128 + e;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int i2b = 0; i2b < s.n2; i2b += 512) {
+    const int i2 = i2b + (int)threadIdx.x;
+    uint32_t cnt = 0, base = 0;
+    if (i2 < s.n2) {
+      const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
+      cnt = dense_cnt[slot];
+      base = dense_base[slot];
     }
+    uint32_t total;
+    const uint32_t pos = block_excl_scan<uint32_t, 512>(cnt, wsum, &total);
+    for (uint32_t k = 0; k < cnt && pos + k < (uint32_t)G1_LIST; ++k) list[pos + k] = (int)(base + k);
+    __syncthreads();
+    int j = g;
+    for (; j + 12 < (int)total; j += 16) {
+      const size_t l0 = (size_t)list[j] * 128, l1 = (size_t)list[j + 4] * 128;
+      const size_t l2 = (size_t)list[j + 8] * 128, l3 = (size_t)list[j + 12] * 128;
+      a[0] += P0[l0];
+      a[1] += P1[l0];
+      a[2] += P0[l1];
+      a[3] += P1[l1];
+      a[4] += P0[l2];
+      a[5] += P1[l2];
+      a[6] += P0[l3];
+      a[7] += P1[l3];
+    }
+    for (; j < (int)total; j += 4) {
+      const size_t l0 = (size_t)list[j] * 128;
+      a[0] += P0[l0];
+      a[1] += P1[l0];
+    }
+    __syncthreads();
   }
-  red[g][e] = a0 + a1;
+  red[g][e] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   __syncthreads();
   if (g == 0) dG1[(int64_t)ti1 * 128 + e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
 }
@@ -381,11 +411,18 @@ __global__ void __launch_bounds__(256) k_reduce_g2(const uint32_t* __restrict__ 
                                                    float* __restrict__ dG2) {
   const int run = blockIdx.x >> 1, h = blockIdx.x & 1;
   const int c0 = (int)run_base[run], c1 = (int)run_base[run + 1];
-  for (int e = threadIdx.x; e < 2048; e += 256) {
-    float acc = 0.f;
-    for (int c = c0; c < c1; ++c) acc += dBpart[((int64_t)h * nch_cap + c) * 2048 + e];
+  // thread k owns elements k + 256 m (m < 8): eight independent loads per chunk
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int c = c0; c < c1; ++c) {
+    const float* src = dBpart + ((size_t)h * nch_cap + c) * 2048 + threadIdx.x;
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc[m] += src[256 * m];
+  }
+#pragma unroll
+  for (int m = 0; m < 8; ++m) {
+    const int e = (int)threadIdx.x + 256 * m;
     const int a = e >> 6, j2 = (e >> 4) & 3, bp = e & 15;
-    dG2[(int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp] = acc;
+    dG2[(int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp] = acc[m];
   }
 }
 
