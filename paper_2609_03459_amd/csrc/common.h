@@ -45,8 +45,10 @@ enum : int { ERR_INDEX = 1, ERR_OFFSETS = 2 };
 constexpr int SORT_THREADS = 256;
 constexpr int SORT_ITEMS = 16;
 constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;  // keys per radix tile
-constexpr int RADIX_BITS = 8;
-constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int RADIX_MAX_BITS = 11;               // widest radix digit
+constexpr int RADIX_MAX = 1 << RADIX_MAX_BITS;
+// LSD radix passes for keys of key_bits bits: equal-width digits of at most RADIX_MAX_BITS
+inline int sort_passes(int key_bits) { return (key_bits + RADIX_MAX_BITS - 1) / RADIX_MAX_BITS; }
 constexpr int SCAN_THREADS = 256;
 constexpr int SCAN_ITEMS = 16;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
@@ -61,8 +63,8 @@ struct Work {
   int32_t* ctr;           // [C_TOTAL]
   uint32_t* keys[2];      // radix ping-pong keys [M]
   uint32_t* vals[2];      // radix ping-pong positions [M]
-  uint32_t* rcounts;      // [RADIX * ntiles]
-  uint32_t* rtotals;      // [npasses * RADIX]
+  uint32_t* rcounts;      // [RADIX_MAX * ntiles]
+  uint32_t* rtotals;      // [npasses * RADIX_MAX]
   uint64_t* flags;        // [M] packed (row head, group head) then their inclusive scan
   uint64_t* tsum64;       // scan tile sums [ntiles_scan]
   uint32_t* tsum32;       // scan tile sums for 32-bit scans

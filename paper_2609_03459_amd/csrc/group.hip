@@ -131,22 +131,24 @@ __global__ void k_check_offsets(const int64_t* __restrict__ offsets, int64_t NB,
 }
 
 // ---------------------------------------------------------------------------
-// LSD radix sort of (key, position), 8-bit digits, stable
+// LSD radix sort of (key, position), stable, BITS-bit digits (8..11)
 // ---------------------------------------------------------------------------
+template <int BITS>
 __global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __restrict__ keys, int n, int shift,
                                                              uint32_t* __restrict__ counts, int ntiles,
                                                              uint32_t* __restrict__ totals) {
-  __shared__ uint32_t h[4][RADIX];  // one histogram per wave
+  constexpr int NB = 1 << BITS;
+  __shared__ uint32_t h[4][NB];  // one histogram per wave
   const int w = threadIdx.x >> 6;
-  for (int k = threadIdx.x; k < 4 * RADIX; k += SORT_THREADS) (&h[0][0])[k] = 0;
+  for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&h[0][0])[k] = 0;
   __syncthreads();
   const int base = blockIdx.x * SORT_TILE;
   for (int j = 0; j < SORT_ITEMS; ++j) {
     int i = base + j * SORT_THREADS + threadIdx.x;
-    if (i < n) atomicAdd(&h[w][(keys[i] >> shift) & (RADIX - 1)], 1u);
+    if (i < n) atomicAdd(&h[w][(keys[i] >> shift) & (NB - 1)], 1u);
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) {
+  for (int d = threadIdx.x; d < NB; d += SORT_THREADS) {
     uint32_t c = h[0][d] + h[1][d] + h[2][d] + h[3][d];
     counts[d * ntiles + blockIdx.x] = c;
     if (c) atomicAdd(&totals[d], c);
@@ -192,16 +194,18 @@ __global__ void __launch_bounds__(256) k_radix_scan(uint32_t* __restrict__ count
 
 // Stable scatter.  Wave w of the block owns keys [tile + w*1024, +1024); item j
 // of lane l is element w*1024 + j*64 + l, so (w, j, l) order is input order.
+template <int BITS>
 __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
                                                                 const uint32_t* __restrict__ vin,
                                                                 uint32_t* __restrict__ kout,
                                                                 uint32_t* __restrict__ vout, int n, int shift,
                                                                 const uint32_t* __restrict__ offs, int ntiles) {
-  __shared__ uint32_t wh[4][RADIX];   // running per-wave digit counts
-  __shared__ uint32_t gbase[4][RADIX];  // global base per (wave, digit)
+  constexpr int NB = 1 << BITS;
+  __shared__ uint32_t wh[4][NB];     // running per-wave digit counts
+  __shared__ uint32_t gbase[4][NB];  // global base per (wave, digit)
   const int w = threadIdx.x >> 6;
   const int lane = lane_id();
-  for (int k = threadIdx.x; k < 4 * RADIX; k += SORT_THREADS) (&wh[0][0])[k] = 0;
+  for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&wh[0][0])[k] = 0;
   __syncthreads();
   const int base = blockIdx.x * SORT_TILE + w * (SORT_ITEMS * 64);
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -212,10 +216,10 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
     bool ok = i < n;
     key[j] = ok ? kin[i] : 0u;
     val[j] = ok ? vin[i] : 0u;
-    uint32_t dg = (key[j] >> shift) & (RADIX - 1);
+    uint32_t dg = (key[j] >> shift) & (NB - 1);
     uint64_t peers = __ballot(ok);
 #pragma unroll
-    for (int b = 0; b < RADIX_BITS; ++b) {
+    for (int b = 0; b < BITS; ++b) {
       uint64_t m = __ballot((dg >> b) & 1);
       peers &= ((dg >> b) & 1) ? m : ~m;
     }
@@ -226,7 +230,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
     if (ok && before == 0) wh[w][dg] = prev + cnt;
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < RADIX; d += SORT_THREADS) {
+  for (int d = threadIdx.x; d < NB; d += SORT_THREADS) {
     uint32_t g = offs[d * ntiles + blockIdx.x];
     uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
     gbase[0][d] = g;
@@ -239,7 +243,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
   for (int j = 0; j < SORT_ITEMS; ++j) {
     int i = base + j * 64 + lane;
     if (i < n) {
-      uint32_t dg = (key[j] >> shift) & (RADIX - 1);
+      uint32_t dg = (key[j] >> shift) & (NB - 1);
       uint32_t pos = gbase[w][dg] + rk[j];
       kout[pos] = key[j];
       vout[pos] = val[j];
@@ -464,10 +468,25 @@ static int grid_for(int64_t n, int per_block, int cap) {
   return (int)g;
 }
 
+template <int BITS>
+static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntiles, uint32_t* tot, hipStream_t st) {
+  hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift, w.rcounts,
+                     ntiles, tot);
+  hipLaunchKernelGGL(k_radix_scan, dim3(1 << BITS), dim3(256), 0, st, w.rcounts, ntiles, (const uint32_t*)tot);
+  hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
+                     w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles);
+  return hipGetLastError();
+}
+
 hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64_t M, const int64_t* offsets,
                         int64_t B, const Prof& prof, hipStream_t st) {
-  const int npasses = (s.key_bits + RADIX_BITS - 1) / RADIX_BITS;
-  const int nrt = npasses * RADIX;
+  // passes of equal width, at most RADIX_MAX_BITS bits each
+  const int npasses = sort_passes(s.key_bits);
+  // digit width actually used: 8..11 bits; pass p sorts bits [p dbits, p dbits + bits)
+  const int dbits = npasses ? (s.key_bits + npasses - 1) / npasses : 8;
+  const int bits = dbits < 8 ? 8 : dbits;
+  const int radix = 1 << bits;
+  const int nrt = npasses * radix;
   {
     int total = C_TOTAL > nrt ? C_TOTAL : nrt;
     hipLaunchKernelGGL(k_group_init, dim3((total + 255) / 256), dim3(256), 0, st, w.ctr, w.occ_start, w.pg_start,
@@ -487,13 +506,15 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   prof_end(prof, K_INGEST, st);
   int cur = 0;
   for (int p = 0; p < npasses; ++p) {
-    const int shift = p * RADIX_BITS;
-    uint32_t* tot = w.rtotals + p * RADIX;
-    hipLaunchKernelGGL(k_radix_hist, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift, w.rcounts,
-                       ntiles, tot);
-    hipLaunchKernelGGL(k_radix_scan, dim3(RADIX), dim3(256), 0, st, w.rcounts, ntiles, (const uint32_t*)tot);
-    hipLaunchKernelGGL(k_radix_scatter, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
-                       w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles);
+    const int shift = p * dbits;
+    uint32_t* tot = w.rtotals + p * radix;
+    switch (bits) {
+      case 8: e = radix_pass<8>(w, cur, n, shift, ntiles, tot, st); break;
+      case 9: e = radix_pass<9>(w, cur, n, shift, ntiles, tot, st); break;
+      case 10: e = radix_pass<10>(w, cur, n, shift, ntiles, tot, st); break;
+      default: e = radix_pass<11>(w, cur, n, shift, ntiles, tot, st); break;
+    }
+    if (e != hipSuccess) return e;
     cur ^= 1;
   }
   const uint32_t* sk = w.keys[cur];

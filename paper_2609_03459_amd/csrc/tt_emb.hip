@@ -26,7 +26,6 @@ namespace ttemb {
 
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static int sort_passes(const Shape& s) { return (s.key_bits + RADIX_BITS - 1) / RADIX_BITS; }
 
 // Walks the workspace regions in a fixed order; with base == nullptr it only
 // measures.
@@ -50,8 +49,8 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->keys[1] = (uint32_t*)take(4 * m);
   W->vals[0] = (uint32_t*)take(4 * m);
   W->vals[1] = (uint32_t*)take(4 * m);
-  W->rcounts = (uint32_t*)take(4 * RADIX * sort_tiles);
-  W->rtotals = (uint32_t*)take(4 * RADIX * 4);
+  W->rcounts = (uint32_t*)take(4 * (size_t)RADIX_MAX * sort_tiles);
+  W->rtotals = (uint32_t*)take(4 * (size_t)RADIX_MAX * 4);  // at most 3 passes of up to 11 bits
   W->flags = (uint64_t*)take(8 * m);
   W->tsum64 = (uint64_t*)take(8 * scan_tiles);
   W->tsum32 = (uint32_t*)take(4 * (dscan_tiles > scan_tiles ? dscan_tiles : scan_tiles));
@@ -85,7 +84,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->dApart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nsl_max * s.d1 * s.R : 0);
   W->dBpart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2) : 0);
   W->g3part = (float*)take(bwd_r32 ? 4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2) : 0);
-  const int par = sort_passes(s) & 1;
+  const int par = sort_passes(s.key_bits) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];
   W->M = M;
