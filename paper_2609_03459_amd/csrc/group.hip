@@ -135,40 +135,34 @@ __global__ void k_check_offsets(const int64_t* __restrict__ offsets, int64_t NB,
 // ---------------------------------------------------------------------------
 template <int BITS>
 __global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __restrict__ keys, int n, int shift,
-                                                             uint32_t* __restrict__ counts, int ntiles,
-                                                             uint32_t* __restrict__ totals) {
+                                                             uint32_t* __restrict__ counts, int ntiles) {
   constexpr int NB = 1 << BITS;
   __shared__ uint32_t h[4][NB];  // one histogram per wave
   const int w = threadIdx.x >> 6;
   for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&h[0][0])[k] = 0;
   __syncthreads();
   const int base = blockIdx.x * SORT_TILE;
+  uint32_t k[SORT_ITEMS];
+#pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
-    int i = base + j * SORT_THREADS + threadIdx.x;
-    if (i < n) atomicAdd(&h[w][(keys[i] >> shift) & (NB - 1)], 1u);
+    const int i = base + j * SORT_THREADS + threadIdx.x;
+    k[j] = i < n ? keys[i] : 0u;
   }
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j)
+    if (base + j * SORT_THREADS + (int)threadIdx.x < n) atomicAdd(&h[w][(k[j] >> shift) & (NB - 1)], 1u);
   __syncthreads();
-  for (int d = threadIdx.x; d < NB; d += SORT_THREADS) {
-    uint32_t c = h[0][d] + h[1][d] + h[2][d] + h[3][d];
-    counts[d * ntiles + blockIdx.x] = c;
-    if (c) atomicAdd(&totals[d], c);
-  }
+  for (int d = threadIdx.x; d < NB; d += SORT_THREADS)
+    counts[d * ntiles + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
 }
 
-// one block per digit: exclusive offsets of every tile for that digit
+// one block per digit: exclusive offsets of every tile within that digit, and
+// the digit's total (the digit bases are formed by the scatter blocks)
 __global__ void __launch_bounds__(256) k_radix_scan(uint32_t* __restrict__ counts, int ntiles,
-                                                    const uint32_t* __restrict__ totals) {
+                                                    uint32_t* __restrict__ totals) {
   __shared__ uint32_t smem[4];
-  __shared__ uint32_t s_base;
   const int d = blockIdx.x;
-  if (threadIdx.x < 64) {
-    uint32_t s = 0;
-    for (int k = threadIdx.x; k < d; k += 64) s += totals[k];
-    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
-    if (threadIdx.x == 0) s_base = s;
-  }
-  __syncthreads();
-  uint32_t running = s_base;
+  uint32_t running = 0;
   uint32_t* row = counts + (int64_t)d * ntiles;
   for (int start = 0; start < ntiles; start += 256 * 4) {
     uint32_t v[4];
@@ -190,64 +184,121 @@ __global__ void __launch_bounds__(256) k_radix_scan(uint32_t* __restrict__ count
     }
     running += tot;
   }
+  if (threadIdx.x == 0) totals[d] = running;
 }
 
 // Stable scatter.  Wave w of the block owns keys [tile + w*1024, +1024); item j
 // of lane l is element w*1024 + j*64 + l, so (w, j, l) order is input order.
+// Ranks come from per-wave ballots; the tile is first placed in LDS in digit
+// order, then written out so that consecutive threads of one digit write
+// consecutive addresses.
 template <int BITS>
 __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
                                                                 const uint32_t* __restrict__ vin,
                                                                 uint32_t* __restrict__ kout,
                                                                 uint32_t* __restrict__ vout, int n, int shift,
-                                                                const uint32_t* __restrict__ offs, int ntiles) {
+                                                                const uint32_t* __restrict__ offs, int ntiles,
+                                                                const uint32_t* __restrict__ totals) {
   constexpr int NB = 1 << BITS;
-  __shared__ uint32_t wh[4][NB];     // running per-wave digit counts
-  __shared__ uint32_t gbase[4][NB];  // global base per (wave, digit)
+  __shared__ uint32_t wh[4][NB];  // per-wave digit counts, then the wave's local base per digit
+  __shared__ uint32_t lbase[NB];  // tile-local start of each digit
+  __shared__ uint32_t dbase[NB];  // global start of each digit
+  __shared__ uint32_t sk[SORT_TILE], sv[SORT_TILE];
+  __shared__ uint32_t scan_tmp[SORT_THREADS / 64];
   const int w = threadIdx.x >> 6;
   const int lane = lane_id();
   for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&wh[0][0])[k] = 0;
   __syncthreads();
-  const int base = blockIdx.x * SORT_TILE + w * (SORT_ITEMS * 64);
+  const int tile0 = blockIdx.x * SORT_TILE;
+  const int base = tile0 + w * (SORT_ITEMS * 64);
+  const int nt = n - tile0 < SORT_TILE ? n - tile0 : SORT_TILE;  // keys in this tile
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   uint32_t key[SORT_ITEMS], val[SORT_ITEMS], rk[SORT_ITEMS];
 #pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
-    int i = base + j * 64 + lane;
-    bool ok = i < n;
+    const int i = base + j * 64 + lane;
+    const bool ok = i < n;
     key[j] = ok ? kin[i] : 0u;
     val[j] = ok ? vin[i] : 0u;
-    uint32_t dg = (key[j] >> shift) & (NB - 1);
+  }
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    const int i = base + j * 64 + lane;
+    const bool ok = i < n;
+    const uint32_t dg = (key[j] >> shift) & (NB - 1);
     uint64_t peers = __ballot(ok);
 #pragma unroll
     for (int b = 0; b < BITS; ++b) {
-      uint64_t m = __ballot((dg >> b) & 1);
+      const uint64_t m = __ballot((dg >> b) & 1);
       peers &= ((dg >> b) & 1) ? m : ~m;
     }
-    uint32_t before = __popcll(peers & lt);
-    uint32_t cnt = __popcll(peers);
-    uint32_t prev = ok ? wh[w][dg] : 0u;
+    const uint32_t before = __popcll(peers & lt);
+    const uint32_t cnt = __popcll(peers);
+    const uint32_t prev = ok ? wh[w][dg] : 0u;
     rk[j] = prev + before;
     if (ok && before == 0) wh[w][dg] = prev + cnt;
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < NB; d += SORT_THREADS) {
-    uint32_t g = offs[d * ntiles + blockIdx.x];
-    uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
-    gbase[0][d] = g;
-    gbase[1][d] = g + c0;
-    gbase[2][d] = g + c0 + c1;
-    gbase[3][d] = g + c0 + c1 + c2;
+  // tile-local digit starts (exclusive scan over digits of the per-digit totals)
+  constexpr int DPT = (NB + SORT_THREADS - 1) / SORT_THREADS;  // digits per thread
+  uint32_t tot[DPT], my = 0;
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) {
+    const int d = threadIdx.x * DPT + q;
+    tot[q] = d < NB ? wh[0][d] + wh[1][d] + wh[2][d] + wh[3][d] : 0u;
+    my += tot[q];
+  }
+  uint32_t all;
+  uint32_t run = block_excl_scan<uint32_t, SORT_THREADS>(my, scan_tmp, &all);
+  {
+    // digit bases: exclusive scan of the digit totals of the whole pass
+    uint32_t gt[DPT], gmy = 0;
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int d = threadIdx.x * DPT + q;
+      gt[q] = d < NB ? totals[d] : 0u;
+      gmy += gt[q];
+    }
+    uint32_t gall;
+    uint32_t grun = block_excl_scan<uint32_t, SORT_THREADS>(gmy, scan_tmp, &gall);
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int d = threadIdx.x * DPT + q;
+      if (d < NB) dbase[d] = grun;
+      grun += gt[q];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) {
+    const int d = threadIdx.x * DPT + q;
+    if (d < NB) {
+      lbase[d] = run;
+      const uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
+      wh[0][d] = run;
+      wh[1][d] = run + c0;
+      wh[2][d] = run + c0 + c1;
+      wh[3][d] = run + c0 + c1 + c2;
+    }
+    run += tot[q];
   }
   __syncthreads();
 #pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
-    int i = base + j * 64 + lane;
+    const int i = base + j * 64 + lane;
     if (i < n) {
-      uint32_t dg = (key[j] >> shift) & (NB - 1);
-      uint32_t pos = gbase[w][dg] + rk[j];
-      kout[pos] = key[j];
-      vout[pos] = val[j];
+      const uint32_t dg = (key[j] >> shift) & (NB - 1);
+      const uint32_t p = wh[w][dg] + rk[j];
+      sk[p] = key[j];
+      sv[p] = val[j];
     }
+  }
+  __syncthreads();
+  for (int p = threadIdx.x; p < nt; p += SORT_THREADS) {
+    const uint32_t k = sk[p];
+    const uint32_t dg = (k >> shift) & (NB - 1);
+    const uint32_t pos = dbase[dg] + offs[dg * ntiles + blockIdx.x] + ((uint32_t)p - lbase[dg]);
+    kout[pos] = k;
+    vout[pos] = sv[p];
   }
 }
 
@@ -471,10 +522,11 @@ static int grid_for(int64_t n, int per_block, int cap) {
 template <int BITS>
 static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntiles, uint32_t* tot, hipStream_t st) {
   hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift, w.rcounts,
-                     ntiles, tot);
-  hipLaunchKernelGGL(k_radix_scan, dim3(1 << BITS), dim3(256), 0, st, w.rcounts, ntiles, (const uint32_t*)tot);
+                     ntiles);
+  hipLaunchKernelGGL(k_radix_scan, dim3(1 << BITS), dim3(256), 0, st, w.rcounts, ntiles, tot);
   hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
-                     w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles);
+                     w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles,
+                     (const uint32_t*)tot);
   return hipGetLastError();
 }
 
