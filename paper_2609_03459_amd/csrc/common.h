@@ -64,6 +64,7 @@ struct Work {
   uint32_t* keys[2];      // radix ping-pong keys [M]
   uint32_t* vals[2];      // radix ping-pong positions [M]
   uint32_t* rcounts;      // [RADIX_MAX * ntiles]
+  int32_t* tile_bag;      // [ntiles + 1] bag holding the first occurrence of each sort tile
   uint32_t* rtotals;      // [npasses * RADIX_MAX]
   uint64_t* flags;        // [M] packed (row head, group head) then their inclusive scan
   uint64_t* tsum64;       // scan tile sums [ntiles_scan]

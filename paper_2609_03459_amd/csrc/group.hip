@@ -53,29 +53,37 @@ __device__ __forceinline__ int64_t upper_bound_global(const int64_t* a, int64_t 
   return lo;
 }
 
+// tile_bag[k] = the bag whose occurrence range holds occurrence k * SORT_TILE
+// (entries stay 0 where invalid offsets leave a tile start uncovered)
+__global__ void k_tile_bags(const int64_t* __restrict__ offsets, int64_t NB, int64_t M,
+                            int32_t* __restrict__ tile_bag) {
+  const int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (b >= NB) return;
+  int64_t lo = offsets[b], hi = offsets[b + 1];
+  lo = lo < 0 ? 0 : (lo > M ? M : lo);
+  hi = hi < lo ? lo : (hi > M ? M : hi);
+  for (int64_t k = (lo + SORT_TILE - 1) / SORT_TILE; k * SORT_TILE < hi; ++k) tile_bag[k] = (int32_t)b;
+}
+
 __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restrict__ idx, int64_t M,
-                                                         const int64_t* __restrict__ offsets, int64_t B, int T,
+                                                         const int64_t* __restrict__ offsets,
+                                                         const int32_t* __restrict__ tile_bag, int64_t B, int T,
                                                          int64_t N, uint32_t Npad, uint32_t kinv,
                                                          uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
                                                          int32_t* __restrict__ bag_of, int32_t* __restrict__ ctr) {
   __shared__ int64_t win[INGEST_WIN];
-  __shared__ int64_t s_first, s_last;
   const int64_t NB = (int64_t)T * B;
   const int64_t o0 = (int64_t)blockIdx.x * SORT_TILE;
   const int64_t o1 = (o0 + SORT_TILE < M ? o0 + SORT_TILE : M);
   int64_t bfirst = 0, nwin = 0;
   if (offsets) {
-    if (threadIdx.x == 0) {
-      int64_t f = upper_bound_global(offsets, 0, NB + 1, o0) - 1;
-      int64_t l = upper_bound_global(offsets, 0, NB + 1, o1 - 1) - 1;
-      f = f < 0 ? 0 : (f > NB - 1 ? NB - 1 : f);
-      l = l < f ? f : (l > NB - 1 ? NB - 1 : l);
-      s_first = f;
-      s_last = l;
-    }
-    __syncthreads();
-    bfirst = s_first;
-    nwin = s_last - s_first + 2;  // offsets[bfirst .. blast+1]
+    // bags of this tile: from the bag holding o0 to the one holding the next tile's first occurrence
+    int64_t f = tile_bag[blockIdx.x];
+    int64_t l = o1 < M ? (int64_t)tile_bag[blockIdx.x + 1] : NB - 1;
+    f = f < 0 ? 0 : (f > NB - 1 ? NB - 1 : f);
+    l = l < f ? f : (l > NB - 1 ? NB - 1 : l);
+    bfirst = f;
+    nwin = l - f + 2;  // offsets[bfirst .. l + 1]
     if (nwin <= INGEST_WIN)
       for (int k = threadIdx.x; k < nwin; k += SORT_THREADS) win[k] = offsets[bfirst + k];
     __syncthreads();
@@ -88,9 +96,9 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     if (!offsets) {
       b = o;
     } else if (nwin <= INGEST_WIN) {
-      int64_t lo = 0, hi = nwin;
+      int lo = 0, hi = (int)nwin;
       while (lo < hi) {
-        int64_t mid = (lo + hi) >> 1;
+        const int mid = (lo + hi) >> 1;
         if (win[mid] <= o)
           lo = mid + 1;
         else
@@ -98,11 +106,11 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
       }
       b = bfirst + lo - 1;
     } else {
-      b = upper_bound_global(offsets, bfirst, bfirst + nwin, o) - 1;
+      b = upper_bound_global(offsets, 0, NB + 1, o) - 1;
     }
     b = b < 0 ? 0 : (b > NB - 1 ? NB - 1 : b);
-    int64_t g = idx[o];
-    uint32_t t = (uint32_t)(b / B);
+    const int64_t g = idx[o];
+    const uint32_t t = (uint32_t)b / (uint32_t)B;
     uint32_t key;
     if (g >= 0 && g < N) {
       key = t * Npad + (uint32_t)g;
@@ -553,8 +561,14 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   const int n = (int)M;
   const int ntiles = (n + SORT_TILE - 1) / SORT_TILE;
   prof_begin(prof, K_INGEST, st);
-  hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, B, s.T, s.N, s.Npad, s.kinv,
-                     w.keys[0], w.vals[0], w.bag_of, w.ctr);
+  if (offsets && NB > 0) {
+    e = fill_u32(reinterpret_cast<uint32_t*>(w.tile_bag), ntiles + 1, 0u, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_tile_bags, dim3((unsigned)((NB + 255) / 256)), dim3(256), 0, st, offsets, NB, M,
+                       w.tile_bag);
+  }
+  hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, (const int32_t*)w.tile_bag,
+                     B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr);
   prof_end(prof, K_INGEST, st);
   int cur = 0;
   for (int p = 0; p < npasses; ++p) {

@@ -50,6 +50,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->vals[0] = (uint32_t*)take(4 * m);
   W->vals[1] = (uint32_t*)take(4 * m);
   W->rcounts = (uint32_t*)take(4 * (size_t)RADIX_MAX * sort_tiles);
+  W->tile_bag = (int32_t*)take(4 * (size_t)(sort_tiles + 1));
   W->rtotals = (uint32_t*)take(4 * (size_t)RADIX_MAX * 4);  // at most 3 passes of up to 11 bits
   W->flags = (uint64_t*)take(8 * m);
   W->tsum64 = (uint64_t*)take(8 * scan_tiles);
