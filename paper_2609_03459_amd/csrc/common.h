@@ -66,7 +66,6 @@ struct Work {
   uint32_t* rcounts;      // [RADIX_MAX * ntiles]
   int32_t* tile_bag;      // [ntiles + 1] bag holding the first occurrence of each sort tile
   uint32_t* rtotals;      // [npasses * RADIX_MAX]
-  uint64_t* flags;        // [M] packed (row head, group head) then their inclusive scan
   uint64_t* tsum64;       // scan tile sums [ntiles_scan]
   uint32_t* tsum32;       // scan tile sums for 32-bit scans
   int32_t* bag_of;        // [M] global bag of each occurrence

@@ -1,7 +1,7 @@
 // Prefix-based index grouping (FlowTT Section 3.3, Fig. 4) on gfx950:
 //   ingest   -> one 32-bit key per occurrence, t*Npad + g (invalid rows get Npad*T)
 //   sort     -> LSD radix sort of (key, position), 8-bit digits, stable
-//   unique   -> row heads and prefix-group heads, one inclusive scan of packed flags
+//   unique   -> row heads and prefix-group heads, counted per tile and scanned
 //   RLE      -> unique rows, inverse map, occurrence ranges, prefix groups
 //   order    -> prefix groups re-ordered (table, i2, i1) through a dense scan over
 //               the prefix space, cut into work slices of at most SLICE_ROWS rows
@@ -387,59 +387,122 @@ hipError_t scan_u32_exclusive(const uint32_t* in, uint32_t* out, int64_t n, uint
 // ---------------------------------------------------------------------------
 // unique rows and prefix groups
 // ---------------------------------------------------------------------------
-__global__ void k_flags(const uint32_t* __restrict__ sk, int n, uint32_t kinv, uint32_t n3,
-                        uint64_t* __restrict__ flags, int32_t* __restrict__ ctr) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  uint32_t k = sk[i];
-  uint64_t f = 0;
-  if (k < kinv) {
-    uint32_t kp = i > 0 ? sk[i - 1] : 0xffffffffu;
-    bool head = (i == 0) || kp != k;
-    bool pgh = head && ((i == 0) || (kp / n3) != (k / n3));
-    f = (uint64_t)head | ((uint64_t)pgh << 32);
-    if (i == n - 1 || sk[i + 1] >= kinv) ctr[C_NVALID] = i + 1;
+// Unique rows and prefix groups in two passes over the sorted keys.  An
+// occurrence starts a row when its key differs from the previous one, and a
+// prefix group when, in addition, key / n3 (table and prefix) differs.  Counts
+// are packed (rows | groups << 32).
+__global__ void __launch_bounds__(SCAN_THREADS) k_group_reduce(const uint32_t* __restrict__ sk, int n, uint32_t kinv,
+                                                               uint32_t n3, uint64_t* __restrict__ tsum,
+                                                               int32_t* __restrict__ ctr) {
+  __shared__ uint64_t smem[SCAN_THREADS / 64];
+  const int base = blockIdx.x * SCAN_TILE;
+  uint64_t c = 0;
+#pragma unroll 4
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    const int i = base + j * SCAN_THREADS + (int)threadIdx.x;
+    if (i < n) {
+      const uint32_t k = sk[i];
+      if (k < kinv) {
+        const uint32_t kp = i > 0 ? sk[i - 1] : 0u;
+        const bool head = i == 0 || kp != k;
+        const bool pgh = head && (i == 0 || kp / n3 != k / n3);
+        c += (uint64_t)head | ((uint64_t)pgh << 32);
+        if (i == n - 1 || sk[i + 1] >= kinv) ctr[C_NVALID] = i + 1;
+      }
+    }
   }
-  flags[i] = f;
+  uint64_t tot;
+  block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot);
+  if (threadIdx.x == 0) tsum[blockIdx.x] = tot;
 }
 
-__global__ void k_group_write(const uint32_t* __restrict__ sk, const uint32_t* __restrict__ sp,
-                              const uint64_t* __restrict__ incl, int n, uint32_t kinv, uint32_t n3, uint32_t Npad,
-                              int32_t* __restrict__ inv, int32_t* __restrict__ sorted_uid,
-                              uint32_t* __restrict__ uniq_key, int32_t* __restrict__ uniq_i3,
-                              int32_t* __restrict__ occ_start,
-                              int32_t* __restrict__ pg_start, uint32_t* __restrict__ pg_key,
-                              int32_t* __restrict__ ctr) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  uint32_t k = sk[i];
-  uint32_t pos = sp[i];
-  if (k >= kinv) {
-    inv[pos] = -1;
-    return;
+// The tile's keys and positions go through LDS so that each thread scans
+// SCAN_ITEMS consecutive occurrences while global reads and writes stay
+// coalesced; writes the inverse map, row id per sorted occurrence, unique keys,
+// i3 per row, occurrence starts, prefix-group starts and keys.
+__device__ __forceinline__ int pad32(int x) { return x + (x >> 5); }
+
+__global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __restrict__ sk,
+                                                             const uint32_t* __restrict__ sp, int n, uint32_t kinv,
+                                                             uint32_t n3, uint32_t Npad,
+                                                             const uint64_t* __restrict__ tsum,
+                                                             int32_t* __restrict__ inv, int32_t* __restrict__ sorted_uid,
+                                                             uint32_t* __restrict__ uniq_key,
+                                                             int32_t* __restrict__ uniq_i3,
+                                                             int32_t* __restrict__ occ_start,
+                                                             int32_t* __restrict__ pg_start,
+                                                             uint32_t* __restrict__ pg_key, int32_t* __restrict__ ctr) {
+  // LDS index x is stored at x + x / 32 so that the per-thread runs of
+  // SCAN_ITEMS consecutive entries do not all fall on two banks
+  __shared__ uint32_t lk[SCAN_TILE + 2 + SCAN_TILE / 32];  // lk[e + 1] = key of tile element e, lk[0] = key before
+  __shared__ int32_t lu[SCAN_TILE + SCAN_TILE / 32];        // row id of each element (-1: invalid)
+  __shared__ int32_t lg[SCAN_TILE + SCAN_TILE / 32];        // (group id << 1) | group starts here; -1: invalid
+  __shared__ uint64_t smem[SCAN_THREADS / 64];
+  const int base = blockIdx.x * SCAN_TILE;
+#pragma unroll 4
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    const int e = j * SCAN_THREADS + (int)threadIdx.x;
+    lk[pad32(e + 1)] = base + e < n ? sk[base + e] : kinv;
   }
-  uint64_t s = incl[i];
-  int uid = (int)(s & 0xffffffffu) - 1;
-  int pg = (int)(s >> 32) - 1;
-  uint32_t kp = i > 0 ? sk[i - 1] : 0xffffffffu;
-  bool head = (i == 0) || kp != k;
-  bool pgh = head && ((i == 0) || (kp / n3) != (k / n3));
-  inv[pos] = uid;
-  sorted_uid[i] = uid;
-  if (head) {
-    uniq_key[uid] = k;
-    uniq_i3[uid] = (int)((k % Npad) % n3);
-    occ_start[uid] = i;
+  if (threadIdx.x == 0) lk[0] = base > 0 ? sk[base - 1] : 0u;
+  __syncthreads();
+  // run ids: each thread scans SCAN_ITEMS consecutive elements
+  const int e0 = (int)threadIdx.x * SCAN_ITEMS;
+  uint32_t hb = 0, pb = 0;  // head / group-head bits of the thread's elements
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int i = base + e0 + k;
+    const uint32_t key = lk[pad32(e0 + k + 1)], kp = lk[pad32(e0 + k)];
+    if (i < n && key < kinv) {
+      const bool head = i == 0 || kp != key;
+      const bool pgh = head && (i == 0 || kp / n3 != key / n3);
+      hb |= (uint32_t)head << k;
+      pb |= (uint32_t)pgh << k;
+    }
   }
-  if (pgh) {
-    pg_start[pg] = uid;
-    pg_key[pg] = k / n3;
+  uint64_t tot;
+  const uint64_t c = (uint64_t)__popc(hb) | ((uint64_t)__popc(pb) << 32);
+  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + tsum[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int i = base + e0 + k;
+    const uint32_t key = lk[pad32(e0 + k + 1)];
+    acc += (uint64_t)((hb >> k) & 1) | ((uint64_t)((pb >> k) & 1) << 32);
+    const bool valid = i < n && key < kinv;
+    lu[pad32(e0 + k)] = valid ? (int)(acc & 0xffffffffu) - 1 : -1;
+    lg[pad32(e0 + k)] = valid ? (((int)(acc >> 32) - 1) << 1) | (int)((pb >> k) & 1) : -1;
   }
-  if (i == n - 1 || sk[i + 1] >= kinv) {
-    ctr[C_U] = uid + 1;
-    ctr[C_P] = pg + 1;
-    occ_start[uid + 1] = i + 1;
-    pg_start[pg + 1] = uid + 1;
+  __syncthreads();
+  // all global writes in striped order (consecutive lanes, consecutive elements)
+#pragma unroll 4
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    const int e = j * SCAN_THREADS + (int)threadIdx.x;
+    const int i = base + e;
+    if (i >= n) continue;
+    const int32_t uid = lu[pad32(e)];
+    inv[sp[i]] = uid;
+    if (uid < 0) continue;
+    sorted_uid[i] = uid;
+    const uint32_t key = lk[pad32(e + 1)], kp = lk[pad32(e)];
+    if (i == 0 || kp != key) {
+      uniq_key[uid] = key;
+      uniq_i3[uid] = (int)((key % Npad) % n3);
+      occ_start[uid] = i;
+    }
+    const int32_t gv = lg[pad32(e)];
+    const int32_t pg = gv >> 1;
+    if (gv & 1) {
+      pg_start[pg] = uid;
+      pg_key[pg] = key / n3;
+    }
+    const uint32_t knext = e + 1 < SCAN_TILE ? lk[pad32(e + 2)] : (i + 1 < n ? sk[i + 1] : kinv);
+    if (i == n - 1 || knext >= kinv) {
+      // the last valid occurrence: totals and end sentinels
+      ctr[C_U] = uid + 1;
+      ctr[C_P] = pg + 1;
+      occ_start[uid + 1] = i + 1;
+      pg_start[pg + 1] = uid + 1;
+    }
   }
 }
 
@@ -585,13 +648,15 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   }
   const uint32_t* sk = w.keys[cur];
   const uint32_t* sp = w.vals[cur];
-  hipLaunchKernelGGL(k_flags, dim3((n + 255) / 256), dim3(256), 0, st, sk, n, s.kinv, (uint32_t)s.n3, w.flags,
-                     w.ctr);
-  e = scan_generic<uint64_t, true>(w.flags, w.flags, M, w.tsum64, nullptr, st);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_group_write, dim3((n + 255) / 256), dim3(256), 0, st, sk, sp, (const uint64_t*)w.flags, n,
-                     s.kinv, (uint32_t)s.n3, s.Npad, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
-                     w.pg_start, w.pg_key, w.ctr);
+  {
+    const int gt = (n + SCAN_TILE - 1) / SCAN_TILE;
+    hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, w.tsum64,
+                       w.ctr);
+    hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
+    hipLaunchKernelGGL(k_group_down, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
+                       (const uint64_t*)w.tsum64, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
+                       w.pg_start, w.pg_key, w.ctr);
+  }
   hipLaunchKernelGGL(k_dense_set, dim3(grid_for(M, 256, 2048)), dim3(256), 0, st, (const int32_t*)w.pg_start,
                      (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, w.dense_cnt, w.dense_pg);
   e = scan_generic<uint32_t, false>(w.dense_cnt, w.dense_base, s.ndense, w.tsum32, w.ctr + C_NSLICES, st);

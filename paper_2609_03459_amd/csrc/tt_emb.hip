@@ -52,7 +52,6 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->rcounts = (uint32_t*)take(4 * (size_t)RADIX_MAX * sort_tiles);
   W->tile_bag = (int32_t*)take(4 * (size_t)(sort_tiles + 1));
   W->rtotals = (uint32_t*)take(4 * (size_t)RADIX_MAX * 4);  // at most 3 passes of up to 11 bits
-  W->flags = (uint64_t*)take(8 * m);
   W->tsum64 = (uint64_t*)take(8 * scan_tiles);
   W->tsum32 = (uint32_t*)take(4 * (dscan_tiles > scan_tiles ? dscan_tiles : scan_tiles));
   W->bag_of = (int32_t*)take(4 * m);
