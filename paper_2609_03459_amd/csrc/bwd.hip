@@ -230,7 +230,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
   int cur_pg = -1;
   const int rows12 = s.d1 * s.d2;
   while (true) {
-    int c = claim_chunk(ctr + C_BWD_CTR, ctr + C_BWD_STEAL, nchunks, &victim, &s_chunk);
+    int c = claim_block(ctr + C_BWD_CTR, nchunks, SCHED_NQ, blockIdx.x % SCHED_NQ, &victim, &s_chunk);
     if (c < 0) break;
     const int s0 = c * BWD_CHUNK;
     const int s1 = s0 + BWD_CHUNK < nsl ? s0 + BWD_CHUNK : nsl;
@@ -327,8 +327,8 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, prof, st);
   const int grid = persistent_grid() * 2;
-  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid, 0u, st)) != hipSuccess) return e;
-  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_STEAL), 1, 0u, st)) != hipSuccess) return e;
+  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
+    return e;
   const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D);
   if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
       hipSuccess)

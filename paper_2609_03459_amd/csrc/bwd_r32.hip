@@ -97,11 +97,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const int nq = 2 * s.T;
   const int q = blockIdx.x % nq;
   const int t = q % s.T, h = q / s.T;
-  const int per_q = gridDim.x / nq;
-  const int me = (blockIdx.x / nq) * BW_WAVES + wave;
-  const int nworkers = per_q * BW_WAVES;
-  int32_t* qctr = ctr + C_BWD_CTR + q * nworkers;
-  int32_t* qclaimed = ctr + C_BWD_CTR + gridDim.x * BW_WAVES + q;
+  int32_t* qctr = ctr + C_BWD_CTR + q * SCHED_STRIDE;  // the owner's queue: all of table t's chunks
 
   for (int i = threadIdx.x; i < acc_n; i += blockDim.x) g3acc[i] = 0.f;
   __syncthreads();
@@ -157,7 +153,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     X.ez = prow && !has1;
   };
 
-  int c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
+  int c = claim_queues(qctr, nch, 1, 0, &cursor);
   int f = 0, ns = 0, run = -1, qd = 0;
   if (c >= 0) {
     const int4 ch = chunks[c_lo + c];
@@ -333,7 +329,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
-      c = claim_chunk_wave(qctr, qclaimed, nch, nworkers, me, &cursor);
+      c = claim_queues(qctr, nch, 1, 0, &cursor);
       qd = 0;
       if (c >= 0) {
         const int4 ch = chunks[c_lo + c];
@@ -453,8 +449,8 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   int per_q = persistent_grid() / nq;
   if (per_q < 1) per_q = 1;
   const int grid = nq * per_q;
-  if (grid > MAX_BWD_WG || grid * BW_WAVES + nq > MAX_PERSIST_WG) return hipErrorInvalidValue;
-  hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), grid * BW_WAVES + nq, 0u, st);
+  if (grid > MAX_BWD_WG || nq * SCHED_STRIDE > C_TOTAL - C_BWD_CTR) return hipErrorInvalidValue;
+  hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), nq * SCHED_STRIDE, 0u, st);
   if (e != hipSuccess) return e;
   const size_t lds = sizeof(float) * ((size_t)s.n3 * 128 + BW_WAVES * BW_SCR);
   e = hipFuncSetAttribute((const void*)k_bwd_r32, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -31,12 +31,9 @@ enum : int {
   C_NSLICES = 3,  // work slices of the fused kernels
   C_ERR = 4,      // sticky error bits
   C_NSEG = 5,     // occurrence chunks of the dE segment sums
-  C_FWD_STEAL = 6,  // chunks claimed so far by the schedulers
-  C_BWD_STEAL = 7,
   C_NCHUNKS = 8,    // chunks of the specialised kernels
-  C_BWD_CLAIMED = 16,  // [16] claimed chunks per backward queue
-  C_FWD_CTR = 64, // per-worker claim counters of the forward scheduler
-  C_BWD_CTR = 64 + 4096,  // per-worker counters of the backward, then claimed counts
+  C_FWD_CTR = 64,         // queue counters of the forward scheduler (stride SCHED_STRIDE)
+  C_BWD_CTR = 64 + 4096,  // queue counters of the backward scheduler (stride SCHED_STRIDE)
   C_TOTAL = 64 + 2 * 4096,
 };
 enum : int { ERR_INDEX = 1, ERR_OFFSETS = 2 };
@@ -55,7 +52,6 @@ constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
 constexpr int SLICE_ROWS = 32;   // unique rows per work slice
 constexpr int CHUNK_SLICES = 32; // slices per chunk of the specialised kernels (one (t, i2) run)
 constexpr int SEG_CHUNK = 256;   // sorted occurrences per dE chunk
-constexpr int MAX_PERSIST_WG = 4096;
 constexpr int MAX_BWD_WG = 1024;
 
 // Device pointers carved out of the caller's workspace.
@@ -172,73 +168,41 @@ __device__ __forceinline__ T block_excl_scan(T v, T* smem, T* total) {
 namespace ttemb {
 
 // Persistent-thread scheduler with chunked work stealing (FlowTT Section 3.4).
-// The chunk list is split evenly over the workers; worker w first claims the
-// chunks of its own share through its counter ctrs[w] (consecutive chunks, so
-// B = G2[i2] and C stay on chip).  Then it steals: one wave reads the
-// counters of 64 victims at a time (w+1, w+2, ... cyclically) with plain
-// loads, and claims with an atomic only from victims that still show work.
-// `cursor` remembers how far the scan got, so exhausted victims are never
-// revisited.  *claimed counts claimed chunks; once it reaches the total,
-// every idle worker exits at once.  A claim takes at most W/64 rounds.
+// The chunk list is cut into nq contiguous queues; queue v holds chunks
+// [share_lo(v), share_lo(v + 1)) and has one claim counter on a 128-byte line
+// of its own.  A worker claims the next chunk of its home queue with a single
+// atomic (consecutive chunks, so neighbouring groups stay in the home XCD's L2);
+// once the home queue is empty it steals from the following queues in turn.  An
+// empty queue is never visited again, so a worker makes at most nq failed
+// claims before it exits.  The forward uses one queue per XCD (workgroup
+// blockIdx % 8 runs on XCD blockIdx % 8); the specialised backward gives every
+// (table, rank half) owner one queue, since its LDS accumulator is its own.
+constexpr int SCHED_NQ = 8;       // queues of the forward scheduler: one per XCD
+constexpr int SCHED_STRIDE = 32;  // ints between queue counters (128 bytes)
+
 __device__ __forceinline__ int share_lo(int nchunks, int W, int v) { return (int)(((int64_t)nchunks * v) / W); }
 
-__device__ __forceinline__ int claim_chunk_wave(int32_t* ctrs, int32_t* claimed, int nchunks, int W, int me,
-                                                int* cursor) {
-  const int lane = lane_id();
-  if (*cursor == 0) {
+__device__ __forceinline__ int claim_queues(int32_t* q, int nchunks, int nq, int home, int* cursor) {
+  while (*cursor < nq) {
+    int v = home + *cursor;
+    if (v >= nq) v -= nq;
+    const int lo = share_lo(nchunks, nq, v), hi = share_lo(nchunks, nq, v + 1);
     int c = -1;
-    if (lane == 0) {
-      const int got = atomicAdd(&ctrs[me], 1);
-      if (share_lo(nchunks, W, me) + got < share_lo(nchunks, W, me + 1)) {
-        c = share_lo(nchunks, W, me) + got;
-        atomicAdd(claimed, 1);
-      }
+    if (lane_id() == 0) {
+      const int got = atomicAdd(&q[v * SCHED_STRIDE], 1);
+      if (lo + got < hi) c = lo + got;
     }
-    c = __shfl(c, 0, 64);
+    c = __builtin_amdgcn_readfirstlane(c);
     if (c >= 0) return c;
-    *cursor = 1;
-  }
-  while (*cursor < W) {
-    if (__hip_atomic_load(claimed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nchunks) {
-      *cursor = W;
-      break;
-    }
-    const int k = *cursor + lane;
-    int v = me + k;
-    if (v >= W) v -= W;
-    bool has = false;
-    if (k < W) {
-      const int used = __hip_atomic_load(&ctrs[v], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      has = share_lo(nchunks, W, v) + used < share_lo(nchunks, W, v + 1);
-    }
-    uint64_t m = __ballot(has);
-    while (m) {
-      const int f = __ffsll((unsigned long long)m) - 1;
-      const int vf = __shfl(v, f, 64);
-      int c = -1;
-      if (lane == 0) {
-        const int got = atomicAdd(&ctrs[vf], 1);
-        if (share_lo(nchunks, W, vf) + got < share_lo(nchunks, W, vf + 1)) {
-          c = share_lo(nchunks, W, vf) + got;
-          atomicAdd(claimed, 1);
-        }
-      }
-      c = __shfl(c, 0, 64);
-      if (c >= 0) {
-        *cursor += f;  // this victim may hold more
-        return c;
-      }
-      m &= m - 1;
-    }
-    *cursor += 64;
+    ++*cursor;
   }
   return -1;
 }
 
 // Block-level worker: wave 0 claims for the block.
-__device__ __forceinline__ int claim_chunk(int32_t* ctrs, int32_t* claimed, int nchunks, int* cursor, int* s_chunk) {
+__device__ __forceinline__ int claim_block(int32_t* q, int nchunks, int nq, int home, int* cursor, int* s_chunk) {
   if (threadIdx.x < 64) {
-    const int c = claim_chunk_wave(ctrs, claimed, nchunks, gridDim.x, blockIdx.x, cursor);
+    const int c = claim_queues(q, nchunks, nq, home, cursor);
     if (threadIdx.x == 0) *s_chunk = c;
   }
   __syncthreads();

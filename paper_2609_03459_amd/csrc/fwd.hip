@@ -43,7 +43,7 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
   int victim = 0;
   int cur_pg = -1;
   while (true) {
-    int c = claim_chunk(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nchunks, &victim, &s_chunk);
+    int c = claim_block(ctr + C_FWD_CTR, nchunks, SCHED_NQ, blockIdx.x % SCHED_NQ, &victim, &s_chunk);
     if (c < 0) break;
     const int s0 = c * FWD_CHUNK;
     const int s1 = s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl;
@@ -98,7 +98,8 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
 // The next row pair's G3 operands are in flight while a pair is computed.
 // ---------------------------------------------------------------------------
 constexpr int F32_WAVES = 4;
-constexpr int F32_SCR = 2048;  // per-wave LDS floats: [slice 4][j1 4][j2 4][b 32]
+constexpr int F32_WG_PER_CU = 2;  // two workgroups (8 waves, 64 KB LDS) per CU
+constexpr int F32_SCR = 2048;     // per-wave LDS floats: [slice 4][j1 4][j2 4][b 32]
 
 // XOR swizzle of the b index: both the stage-1 writes and the stage-2 operand
 // reads put at most two lanes on one bank
@@ -106,7 +107,7 @@ __device__ __forceinline__ uint32_t fscr_at(int sl, int j1, int j2, int b) {
   return (uint32_t)(sl * 512 + j1 * 128 + j2 * 32 + (b ^ ((8 * sl + 4 * j1 + 16 * j2) & 31)));
 }
 
-__global__ void __launch_bounds__(64 * F32_WAVES, 2)
+__global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     k_fwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
               const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
               const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
@@ -115,8 +116,6 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 2)
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* scr = scr_all + wave * F32_SCR;
-  const int me = blockIdx.x * F32_WAVES + wave;
-  const int nworkers = gridDim.x * F32_WAVES;
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
   const int orow = l4 >> 1;  // E row of the pair this lane's output belongs to
@@ -154,7 +153,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 2)
     X.live = has1 || orow == 0;
   };
 
-  int c = claim_chunk_wave(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nch, nworkers, me, &cursor);
+  int c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
   int f = 0, ns = 0, run = -1, qd = 0;
   if (c >= 0) {
     const int4 ch = chunks[c];
@@ -260,7 +259,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, 2)
     wave_lds_sync();
     qd += 4;
     if (qd >= ns) {
-      c = claim_chunk_wave(ctr + C_FWD_CTR, ctr + C_FWD_STEAL, nch, nworkers, me, &cursor);
+      c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
       qd = 0;
       if (c >= 0) {
         const int4 ch = chunks[c];
@@ -441,10 +440,9 @@ hipError_t launch_pool(const Shape& s, const float* E, const int32_t* inv, const
 }
 
 bool fwd_r32_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit float offsets into E (rows x 128), G1 and G3; workers fit the counter area
+  // 32-bit float offsets into E (rows x 128), G1 and G3
   return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
-         (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) &&
-         persistent_grid() * 2 * F32_WAVES <= MAX_PERSIST_WG;
+         (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31);
 }
 
 hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
@@ -452,12 +450,10 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
                           hipStream_t st) {
   if (M > 0) {
     const int grid = persistent_grid() * 2;
-    hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_FWD_CTR), MAX_PERSIST_WG, 0u, st);
-    if (e != hipSuccess) return e;
-    e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_FWD_STEAL), 1, 0u, st);
+    hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_FWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st);
     if (e != hipSuccess) return e;
     if (fwd_r32_supported(s, M)) {
-      const int blocks = persistent_grid() * 2;  // two workgroups of four waves per CU
+      const int blocks = persistent_grid() * F32_WG_PER_CU;
       prof_begin(prof, K_FWD_FUSED, st);
       hipLaunchKernelGGL(k_fwd_r32, dim3(blocks), dim3(64 * F32_WAVES), 0, st, shape_args(s), G1, G2, G3,
                          (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
