@@ -126,17 +126,30 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   float BTop[32];  // dA B operand B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15], (s2, nt2) -> 2 s2 + nt2
   f32x4 dB[8];     // (mt, nt) -> 4 mt + nt
 
-  // quad slice descriptors (wave-uniform)
-  // quad descriptors, lane j < 4 holding slice j: first row, row count, i1
-  int q_rb = 0, q_nr = 0, q_i1 = 0;
-  // i3 of the quad's rows: slice j row k in lane 32 (j & 1) + k of i3A (j < 2) or i3B (j >= 2)
-  int i3A = 0, i3B = 0;
+  // slice descriptors of the current chunk, lane j holding slice f + j (j < ns;
+  // other lanes have no rows): first row, row count, i1
+  int c_rb = 0, c_nr = 0, c_i1 = 0;
+  int qd = 0;  // first slice of the current quad within the chunk
+  // i3 of the quad's rows: slice j row k in lane 32 (j & 1) + k of i3A (j < 2) or i3B (j >= 2);
+  // n3A / n3B hold the same for the next quad of the chunk (loaded one quad ahead)
+  int i3A = 0, i3B = 0, n3A = 0, n3B = 0;
+  auto load_i3 = [&](int qd0, int& A, int& Bv) {
+    const int ja = lane >> 5, k = lane & 31;
+    const int r0 = __builtin_amdgcn_readlane(c_rb, qd0), r1 = __builtin_amdgcn_readlane(c_rb, qd0 + 1);
+    const int r2 = __builtin_amdgcn_readlane(c_rb, qd0 + 2), r3 = __builtin_amdgcn_readlane(c_rb, qd0 + 3);
+    const int n0 = __builtin_amdgcn_readlane(c_nr, qd0), n1 = __builtin_amdgcn_readlane(c_nr, qd0 + 1);
+    const int n2 = __builtin_amdgcn_readlane(c_nr, qd0 + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd0 + 3);
+    const int rA = ja ? r1 : r0, nA = ja ? n1 : n0;
+    const int rB = ja ? r3 : r2, nB = ja ? n3 : n2;
+    A = uniq_i3[rA + (k < nA ? k : 0)];
+    Bv = uniq_i3[rB + (k < nB ? k : 0)];
+  };
   // row pairs of the quad, flattened: slice j owns pairs [cp_j, cp_{j+1}), cp_0 = 0
   int cp1 = 0, cp2 = 0, cp3 = 0, np = 0;
   auto pair_load = [&](BwPair& X, int P) {
     const int pj = (P >= cp1) + (P >= cp2) + (P >= cp3);
     const int pr = 2 * (P - (pj == 0 ? 0 : (pj == 1 ? cp1 : (pj == 2 ? cp2 : cp3))));
-    const int rb = __builtin_amdgcn_readlane(q_rb, pj), nr = __builtin_amdgcn_readlane(q_nr, pj);
+    const int rb = __builtin_amdgcn_readlane(c_rb, qd + pj), nr = __builtin_amdgcn_readlane(c_nr, qd + pj);
     const bool has1 = pr + 1 < nr;
     const int i3v = pj < 2 ? i3A : i3B;
     const int li = (pj & 1) * 32 + pr;
@@ -153,14 +166,26 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     X.ez = prow && !has1;
   };
 
-  int c = claim_queues(qctr, nch, 1, 0, &cursor);
-  int f = 0, ns = 0, run = -1, qd = 0;
-  if (c >= 0) {
-    const int4 ch = chunks[c_lo + c];
-    f = __builtin_amdgcn_readfirstlane(ch.x);
-    ns = __builtin_amdgcn_readfirstlane(ch.y);
-    run = __builtin_amdgcn_readfirstlane(ch.z);
-  }
+  int f = 0, ns = 0, run = -1;
+  // claim a chunk; load its slice descriptors and the i3 words of its first quad
+  auto next_chunk = [&]() {
+    const int cc = claim_queues(qctr, nch, 1, 0, &cursor);
+    if (cc >= 0) {
+      const int4 ch = chunks[c_lo + cc];
+      f = __builtin_amdgcn_readfirstlane(ch.x);
+      ns = __builtin_amdgcn_readfirstlane(ch.y);
+      run = __builtin_amdgcn_readfirstlane(ch.z);
+      const int sl = f + (lane < ns ? lane : 0);
+      const int4 sd = slices[sl];
+      c_rb = sd.y;
+      c_nr = lane < ns ? sd.z - sd.y : 0;
+      c_i1 = slice_i1[sl];
+      load_i3(0, n3A, n3B);
+    }
+    qd = 0;
+    return cc;
+  };
+  int c = next_chunk();
   while (c >= 0) {
     const float* Bg = G2 + (uint32_t)run * 4096u + 16 * h;
     if (run != cur_run) {
@@ -182,25 +207,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     const int nqs = ns - qd < 4 ? ns - qd : 4;
     const int sb = f + qd;
+    i3A = n3A;
+    i3B = n3B;
+    if (qd + 4 < ns) load_i3(qd + 4, n3A, n3B);  // next quad of this chunk, one quad ahead
     {
-      // lane j < nqs holds slice sb + j; the other lanes repeat slice sb with no rows
-      const int sl = sb + (lane < nqs ? lane : 0);
-      const int4 sd = slices[sl];
-      q_rb = sd.y;
-      q_nr = lane < nqs ? sd.z - sd.y : 0;
-      q_i1 = slice_i1[sl];
-    }
-    {
-      // lane 32 h2 + k of i3A / i3B: row k of slice h2 / 2 + h2 (row clamped into the slice)
-      const int ja = lane >> 5, k = lane & 31;
-      const int rba = __builtin_amdgcn_readlane(q_rb, 0), rbb = __builtin_amdgcn_readlane(q_rb, 1);
-      const int rbc = __builtin_amdgcn_readlane(q_rb, 2), rbd = __builtin_amdgcn_readlane(q_rb, 3);
-      const int nra = __builtin_amdgcn_readlane(q_nr, 0), nrb = __builtin_amdgcn_readlane(q_nr, 1);
-      const int nrc = __builtin_amdgcn_readlane(q_nr, 2), nrd = __builtin_amdgcn_readlane(q_nr, 3);
-      const int rA = ja ? rbb : rba, nA = ja ? nrb : nra;
-      const int rB = ja ? rbd : rbc, nB = ja ? nrd : nrc;
-      i3A = uniq_i3[rA + (k < nA ? k : 0)];
-      i3B = uniq_i3[rB + (k < nB ? k : 0)];
+      const int nra = __builtin_amdgcn_readlane(c_nr, qd), nrb = __builtin_amdgcn_readlane(c_nr, qd + 1);
+      const int nrc = __builtin_amdgcn_readlane(c_nr, qd + 2), nrd = __builtin_amdgcn_readlane(c_nr, qd + 3);
       cp1 = (nra + 1) >> 1;
       cp2 = cp1 + ((nrb + 1) >> 1);
       cp3 = cp2 + ((nrc + 1) >> 1);
@@ -208,12 +220,16 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
     const int aj = l15 >> 2;
-    const float* Ag = G1t + (uint32_t)slice_i1[sb + (aj < nqs ? aj : 0)] * 128u + (uint32_t)((lane & 3) * 32 + l4);
+    const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
+    const int i1c = __builtin_amdgcn_readlane(c_i1, qd + 2), i1d = __builtin_amdgcn_readlane(c_i1, qd + 3);
+    const float* Ag = G1t + (uint32_t)sel4(aj < nqs ? aj : 0, i1a, i1b, i1c, i1d) * 128u +
+                      (uint32_t)((lane & 3) * 32 + l4);
     float Aop[8];
 #pragma unroll
     for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
-    BwPair XA, XB;
-    pair_load(XA, 0);  // first row pair, in flight during stage 1
+    BwPair XA, XB, XC;
+    pair_load(XA, 0);  // first two row pairs, in flight during stage 1
+    pair_load(XB, np > 1 ? 1 : 0);
     const bool aj_ok = aj < nqs;
     // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
     {
@@ -238,7 +254,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     auto slice_begin = [&](int j) {
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[scr_at(j, s4, l4 * 16 + l15)];
-      const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(q_i1, j) * 128u + (uint32_t)(l4 * 32 + l15);
+      const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(c_i1, qd + j) * 128u + (uint32_t)(l4 * 32 + l15);
       AT0 = Aj[0];
       AT1 = Aj[16];
     };
@@ -267,31 +283,26 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       for (int r = 0; r < 4; ++r) scr[scr_at(j, l4, r * 16 + l15)] = dC[r];
       dC = f32x4{0.f, 0.f, 0.f, 0.f};
     };
-    // row pairs of the quad in order, two per iteration; the operands of the
-    // next pair are always in flight while one is computed (indices clamped, so
-    // every load is unconditional and in bounds)
+    // row pairs of the quad in order, three per iteration over three operand
+    // sets: the operands of the next two pairs are always in flight while one is
+    // computed (indices clamped, so every load is unconditional and in bounds)
     int cj = 0;
-    for (int P = 0; P < np; P += 2) {
-      pair_load(XB, P + 1 < np ? P + 1 : np - 1);
-      {
-        const int j = (P >= cp1) + (P >= cp2) + (P >= cp3);
-        if (j != cj) {
-          slice_end(cj);
-          slice_begin(j);
-          cj = j;
-        }
-        pair_compute(XA);
+    auto step = [&](const BwPair& X, int Pc) {
+      const int j = (Pc >= cp1) + (Pc >= cp2) + (Pc >= cp3);
+      if (j != cj) {
+        slice_end(cj);
+        slice_begin(j);
+        cj = j;
       }
-      pair_load(XA, P + 2 < np ? P + 2 : np - 1);
-      if (P + 1 < np) {
-        const int j = (P + 1 >= cp1) + (P + 1 >= cp2) + (P + 1 >= cp3);
-        if (j != cj) {
-          slice_end(cj);
-          slice_begin(j);
-          cj = j;
-        }
-        pair_compute(XB);
-      }
+      pair_compute(X);
+    };
+    for (int P = 0; P < np; P += 3) {
+      pair_load(XC, P + 2 < np ? P + 2 : np - 1);
+      step(XA, P);
+      pair_load(XA, P + 3 < np ? P + 3 : np - 1);
+      if (P + 1 < np) step(XB, P + 1);
+      pair_load(XB, P + 4 < np ? P + 4 : np - 1);
+      if (P + 2 < np) step(XC, P + 2);
     }
     slice_end(cj);
     wave_lds_sync();
@@ -329,14 +340,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
-      c = claim_queues(qctr, nch, 1, 0, &cursor);
-      qd = 0;
-      if (c >= 0) {
-        const int4 ch = chunks[c_lo + c];
-        f = __builtin_amdgcn_readfirstlane(ch.x);
-        ns = __builtin_amdgcn_readfirstlane(ch.y);
-        run = __builtin_amdgcn_readfirstlane(ch.z);
-      }
+      c = next_chunk();
     }
   }
   __syncthreads();
