@@ -105,6 +105,50 @@ def test_grouping_bit_exact(lib, orc, k):
     assert np.array_equal(got["pg_keys"], ref["pg_t"] * (n[0] * n[1]) + ref["pg_q"])
 
 
+# key widths that select each radix digit width: 19 bits (two 10-bit passes),
+# 22 bits (two 11-bit passes), 31 and 32 bits (three 11-bit passes)
+WIDE_KEYS = [
+    dict(T=1, n=(64, 64, 64)),
+    dict(T=1, n=(128, 128, 128)),
+    dict(T=3, n=(1000, 1000, 700)),
+    dict(T=2, n=(1024, 1024, 1024)),
+]
+
+
+@pytest.mark.parametrize("k", range(len(WIDE_KEYS)))
+def test_grouping_and_forward_wide_keys(lib, orc, k):
+    c = WIDE_KEYS[k]
+    case = ttgen.tiny(2500 + k, c["T"], c["n"], (1, 2, 2), 2, B=300, max_len=6, zipf=1.1)
+    _say(f"[group wide] T={c['T']} n={c['n']} M={case['idx'].size}")
+    emb = _make(lib, case)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    got = emb.debug_grouping(case["idx"].size)
+    ref = orc.grouping(case)
+    n = case["n"]
+    npad = n[0] * n[1] * n[2]
+    assert got["U"] == ref["U"] and got["P"] == ref["P"] and got["nvalid"] == ref["nvalid"]
+    assert np.array_equal(got["uniq_keys"], ref["uniq_t"] * npad + ref["uniq_g"])
+    assert np.array_equal(got["inv"], ref["inv"])
+    assert np.array_equal(got["occ_pos"], ref["occ_pos"])
+    assert np.array_equal(got["pg_start"], ref["pg_start"])
+    assert np.array_equal(got["pg_keys"], ref["pg_t"] * (n[0] * n[1]) + ref["pg_q"])
+    check_forward(lib, orc, case, name=f"wide{k}")
+
+
+def test_many_short_bags(lib, orc):
+    # 20,000 bags of at most one index: a tile of 4096 occurrences spans more
+    # bags than the ingest window holds, so bag ids come from the global search
+    case = ttgen.tiny(2600, 1, (10, 10, 10), (2, 2, 2), 2, B=20000, max_len=1)
+    check_forward(lib, orc, case, name="short bags")
+    emb = _make(lib, case)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    got = emb.debug_grouping(case["idx"].size)
+    ref = orc.grouping(case)
+    assert np.array_equal(got["inv"], ref["inv"]) and np.array_equal(got["occ_pos"], ref["occ_pos"])
+
+
 def _rank2_cores(n, d, R):
     n1, n2, n3 = n
     d1, d2, d3 = d
