@@ -22,13 +22,45 @@ ShapeArgs shape_args(const Shape& s);
 constexpr int BW_WAVES = 8;
 constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
 
-// The LDS dG3 accumulator stores rank row b' of a table row i3 at slot
-// p(b') = 4 (b' >> 2) + ((b' + (b' >> 2)) & 3).  A dD tile puts b' = 4 l4 + r in
-// register r of lane group l4, so in step r the four lane groups of one row
-// touch four different 8-bank groups.
-__device__ __forceinline__ int g3_unslot(int p) {
-  const int g = p >> 2;
-  return 4 * g + (((p & 3) - g) & 3);
+// The LDS dG3 accumulator holds, per table row i3, 128 floats ordered
+// [j3][16 slots]: rank row b' = 4 g + r of column j3 sits at slot
+// 4 ((g + (j3 >> 1)) & 3) + r.  A dD tile gives lane (j3, g) the four
+// consecutive slots of its column, and the rotation by j3 >> 1 spreads the
+// lanes of one 16-byte access over all banks.
+__device__ __forceinline__ uint32_t g3_slot_base(int j3, int g) {
+  return (uint32_t)(j3 * 16 + 4 * ((g + (j3 >> 1)) & 3));
+}
+__device__ __forceinline__ int g3_unslot(int j3, int p) {  // slot p of column j3 -> b'
+  return 4 * (((p >> 2) - (j3 >> 1)) & 3) + (p & 3);
+}
+
+// p[0..3] += v on LDS floats shared by the workgroup's waves.  A float ds_add is
+// slow on this LDS, integer compare-and-swap is not: read both 64-bit words,
+// add, swap, and retry only a word that changed in between (lock-free: a failed
+// swap means another wave's add landed, so the loop always progresses).
+__device__ __forceinline__ uint64_t add2(uint64_t w, float a, float b) {
+  const float lo = __uint_as_float((uint32_t)w) + a, hi = __uint_as_float((uint32_t)(w >> 32)) + b;
+  return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
+}
+__device__ __forceinline__ void lds_add4(float* p, f32x4 v) {
+  uint64_t* u = reinterpret_cast<uint64_t*>(p);
+  const uint64_t s0 = __hip_atomic_load(u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  const uint64_t s1 = __hip_atomic_load(u + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  uint64_t g0 = s0, g1 = s1;
+  bool d0 = __hip_atomic_compare_exchange_strong(u, &g0, add2(s0, v[0], v[1]), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+  bool d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, add2(s1, v[2], v[3]), __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  while (!d0) {
+    const uint64_t cur = g0;
+    d0 = __hip_atomic_compare_exchange_strong(u, &g0, add2(cur, v[0], v[1]), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  while (!d1) {
+    const uint64_t cur = g1;
+    d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, add2(cur, v[2], v[3]), __ATOMIC_RELAXED,
+                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
 }
 
 // Per-wave scratch holds a [slice][j1][(j2, b')] stack (4 x 4 x 64 floats): first
@@ -39,34 +71,6 @@ __device__ __forceinline__ uint32_t scr_at(int sl, int j1, int j2b) {
   return (uint32_t)(sl * 256 + j1 * 64 + (j2b ^ ((8 * sl + 10 * j1) & 63)));
 }
 
-// p[o[r]] += v[r] for r < 4 on LDS floats shared by the workgroup's waves.  A
-// float ds_add is slow on this LDS, integer compare-and-swap is not: read, add,
-// swap, and retry only the lanes whose word changed in between (lock-free; a
-// failed swap means another wave's add landed, so the loop always progresses).
-__device__ __forceinline__ void lds_add4(float* p, const uint32_t o[4], f32x4 v) {
-  uint32_t* u = reinterpret_cast<uint32_t*>(p);
-  uint32_t seen[4], got[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) seen[r] = __hip_atomic_load(u + o[r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    got[r] = seen[r];
-    __hip_atomic_compare_exchange_strong(u + o[r], &got[r], __float_as_uint(__uint_as_float(seen[r]) + v[r]),
-                                         __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    uint32_t cur = got[r];
-    bool done = cur == seen[r];
-    while (!done) {
-      uint32_t expect = cur;
-      done = __hip_atomic_compare_exchange_strong(u + o[r], &expect, __float_as_uint(__uint_as_float(cur) + v[r]),
-                                                  __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      cur = expect;
-    }
-  }
-}
-
 template <typename T>
 __device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
   return j == 0 ? a : (j == 1 ? b : (j == 2 ? c : d));
@@ -75,11 +79,11 @@ __device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
 // operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs with itself)
 struct BwPair {
   float eb[4];  // dD B operand: dE[row][(4 s + l4) * 8 + j3], row r0 in lanes 0-7 of each 16, r0 + 1 in 8-15
+                // (a lone last row pairs with the all-zero row zrow)
   float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
   float4 d4;    // dC B operand: G3[i3 of that row][16 h + l15][4 (l4 & 1) + k]
   int i3m;      // i3 of this lane's dD column
   bool live;    // this lane's dD column is a real row
-  bool ez;      // this lane's dC K slots belong to a missing second row (add zeros)
 };
 
 __global__ void __launch_bounds__(64 * BW_WAVES, 1)
@@ -87,12 +91,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
               const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
               const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
               const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ dApart,
-              float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap) {
+              float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap, int zrow) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int acc_n = s.n3 * 128;
-  float* g3acc = lds;  // [n3][slot p(b')][8]
+  float* g3acc = lds;  // [n3][j3][16 slots]
   float* scr = lds + acc_n + wave * BW_SCR;
   const int nq = 2 * s.T;
   const int q = blockIdx.x % nq;
@@ -108,15 +112,10 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const bool rowsel = (l15 >> 3) != 0;  // dD column of row r0 + 1
   const bool prow = (l4 >> 1) != 0;     // dC K slots of row r0 + 1
   // per-lane float offsets; every operand is a uniform base plus one of these
-  const uint32_t o_eb0 = (uint32_t)(l4 * 8 + (lane & 7));
-  const uint32_t o_eb1 = o_eb0 + (rowsel ? 128u : 0u);
-  const uint32_t o_e40 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));
-  const uint32_t o_e41 = o_e40 + (prow ? 128u : 0u);
+  const uint32_t o_eb = (uint32_t)(l4 * 8 + (lane & 7));
+  const uint32_t o_e4 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));
   const uint32_t o_d4 = (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));
-  // dD LDS adds: register r of lane group l4 goes to slot p(4 l4 + r)
-  uint32_t o_g3[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) o_g3[r] = (uint32_t)((4 * l4 + ((r + l4) & 3)) * 8 + (lane & 7));
+  const uint32_t o_g3 = g3_slot_base(lane & 7, l4);  // this lane's four dD values in an accumulator row
   const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
   const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
 
@@ -155,15 +154,17 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     const int li = (pj & 1) * 32 + pr;
     const int i3a = __builtin_amdgcn_readlane(i3v, li);
     const int i3b = __builtin_amdgcn_readlane(i3v, has1 ? li + 1 : li);
-    const float* Es = dE + (uint32_t)(rb + pr) * 128u;
-    const uint32_t ob = has1 ? o_eb1 : o_eb0;
+    // rows r0 and r1 (r1 = the zero row for a lone last row), both scalar
+    const int ra = rb + pr, r1 = has1 ? ra + 1 : zrow;
+    const float* Es = dE + (uint32_t)ra * 128u;
+    const uint32_t dl = (uint32_t)(r1 - ra) * 128u;  // second row, relative to the first
+    const uint32_t ob = o_eb + (rowsel ? dl : 0u);
 #pragma unroll
     for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = Es[ob + 32u * s4];
-    X.e4 = *(const float4*)(Es + (has1 ? o_e41 : o_e40));
+    X.e4 = *(const float4*)(Es + o_e4 + (prow ? dl : 0u));
     X.d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
     X.i3m = rowsel ? i3b : i3a;
     X.live = has1 || !rowsel;
-    X.ez = prow && !has1;
   };
 
   int f = 0, ns = 0, run = -1;
@@ -264,12 +265,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], X.eb[s4], dd, 0, 0, 0);
-      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.x, X.d4.x, dC, 0, 0, 0);
-      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.y, X.d4.y, dC, 0, 0, 0);
-      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.z, X.d4.z, dC, 0, 0, 0);
-      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.ez ? 0.f : X.e4.w, X.d4.w, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.x, X.d4.x, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.y, X.d4.y, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.z, X.d4.z, dC, 0, 0, 0);
+      dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.w, X.d4.w, dC, 0, 0, 0);
       // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7]
-      if (X.live) lds_add4(g3acc + (uint32_t)X.i3m * 128u, o_g3, dd);
+      if (X.live) lds_add4(g3acc + (uint32_t)X.i3m * 128u + o_g3, dd);
     };
     // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
     auto slice_end = [&](int j) {
@@ -437,7 +438,7 @@ __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __r
   if (e >= acc_n) return;
   float acc = 0.f;
   for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
-  const int i3 = e >> 7, bp = g3_unslot((e >> 3) & 15), j3 = e & 7;
+  const int i3 = e >> 7, j3 = (e >> 4) & 7, bp = g3_unslot(j3, e & 15);
   dG3[(((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3] = acc;
 }
 
@@ -456,6 +457,9 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   if (grid > MAX_BWD_WG || nq * SCHED_STRIDE > C_TOTAL - C_BWD_CTR) return hipErrorInvalidValue;
   hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), nq * SCHED_STRIDE, 0u, st);
   if (e != hipSuccess) return e;
+  // the zero dE row that a lone last row of a slice is paired with
+  e = fill_u32(reinterpret_cast<uint32_t*>(w.E + (size_t)w.zrow * 128), 128, 0u, st);
+  if (e != hipSuccess) return e;
   const size_t lds = sizeof(float) * ((size_t)s.n3 * 128 + BW_WAVES * BW_SCR);
   e = hipFuncSetAttribute((const void*)k_bwd_r32, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -463,7 +467,7 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   hipLaunchKernelGGL(k_bwd_r32, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
                      (const float*)w.E, (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
                      (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.g3part,
-                     (int)w.nsl_max, (int)w.nch_max);
+                     (int)w.nsl_max, (int)w.nch_max, (int)w.zrow);
   prof_end(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(512), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
                      (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1);

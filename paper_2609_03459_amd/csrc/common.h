@@ -83,7 +83,8 @@ struct Work {
   float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
   int64_t nsl_max, nch_max;
-  float* E;               // [M][D] rows of the forward, dE rows in the backward
+  float* E;               // [M + 1][D]: E rows (forward), dE rows (backward); row M is the zero row
+  int64_t zrow;           // index of the zero row (max_indices)
   float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
   uint32_t* sorted_keys;  // = keys[x] after the sort
   uint32_t* sorted_pos;   // = vals[x] after the sort
