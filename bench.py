@@ -188,6 +188,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=6)
     ap.add_argument("--config", type=int, default=5, help="workload recipe (5 = training step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--reuse", choices=["prefix", "unique", "none"], default="prefix",
+                    help="reuse level (ablation of Section 4.5): prefix groups (default), exact dedup only, none")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
@@ -215,7 +217,7 @@ def main():
     M = int(case["idx"].size)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B)
+    emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B, reuse=args.reuse)
     G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
     idx = torch.from_numpy(case["idx"]).to(dev)
     off = None if case["offsets"] is None else torch.from_numpy(case["offsets"]).to(dev)
@@ -323,7 +325,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "row_factors": list(n),
                    "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
-                   "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu"},
+                   "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu",
+                   "reuse": args.reuse},
         "roofline": roof,
         "phases_ms": phases_ms,
         "kernel_ms_warmup": {k: round(v, 4) for k, v in kernel_ms.items()},

@@ -88,9 +88,22 @@ tt_emb_status tt_emb_create(const tt_emb_desc* desc, tt_emb_handle* out);
 /* Release a handle.  NULL is accepted. */
 tt_emb_status tt_emb_destroy(tt_emb_handle h);
 
+/* Reuse levels of the gather, for the reuse ablation of Section 4.5:
+ *   TT_EMB_REUSE_PREFIX  (default) exact dedup and prefix groups: C = A.B once
+ *                        per prefix group (Section 3.3);
+ *   TT_EMB_REUSE_UNIQUE  exact dedup only: C recomputed for every unique row;
+ *   TT_EMB_REUSE_NONE    no dedup: every occurrence is its own row and
+ *                        recomputes C.
+ * All three compute the same function.  Set the level before
+ * tt_emb_workspace_size (the workspace grows for the two ablation levels) and
+ * before the first call that uses a workspace.  Host only; returns
+ * TT_EMB_EINVAL for an unknown level. */
+typedef enum { TT_EMB_REUSE_PREFIX = 0, TT_EMB_REUSE_UNIQUE = 1, TT_EMB_REUSE_NONE = 2 } tt_emb_reuse;
+tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
+
 /* Bytes of device workspace needed for calls up to desc.max_indices and
- * desc.max_bags.  The same workspace carries the index grouping from a
- * forward call to the following backward call. */
+ * desc.max_bags at the handle's reuse level.  The same workspace carries the
+ * index grouping from a forward call to the following backward call. */
 tt_emb_status tt_emb_workspace_size(tt_emb_handle h, size_t* bytes);
 
 /* Prefix-based index grouping alone (Section 3.3, Fig. 4): sort the indices

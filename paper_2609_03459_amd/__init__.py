@@ -31,7 +31,7 @@ class TTEmbedding:
     """
 
     def __init__(self, num_tables, num_rows, row_factors, dim_factors, rank, max_indices, max_bags,
-                 device="cuda"):
+                 device="cuda", reuse="prefix"):
         d = N.tt_emb_desc()
         d.num_tables = int(num_tables)
         d.num_rows = int(num_rows)
@@ -47,6 +47,9 @@ class TTEmbedding:
         self.d = tuple(int(x) for x in dim_factors)
         self.D = self.d[0] * self.d[1] * self.d[2]
         self.handle = N.tt_emb_create(d)
+        # reuse level (Section 4.5 ablation): "prefix" (default), "unique" or "none"
+        N.tt_emb_set_reuse(self.handle, N.REUSE[reuse])
+        self.reuse = reuse
         self.ws_bytes = N.tt_emb_workspace_size(self.handle)
         # 256-byte aligned workspace carved from one torch allocation
         raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)

@@ -350,11 +350,11 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 }
 
 // dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2).
-// The block first lists the slices of (t, i1) in i2 order (up to 512 prefixes
-// per round), then four groups of 128 threads take list entries g, g + 4, ...
-// with eight loads in flight per thread; the group sums are combined in a
-// fixed order.
-constexpr int G1_LIST = 4096;  // 512 prefixes x at most 8 slices each (n3 <= 256)
+// The block lists the slices of (t, i1) in i2 order (512 prefixes per round,
+// the list G1_LIST entries at a time), and four groups of 128 threads take
+// list entries g, g + 4, ... with eight loads in flight per thread; the group
+// sums are combined in a fixed order.
+constexpr int G1_LIST = 4096;
 
 __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                    const uint32_t* __restrict__ dense_base,
@@ -379,27 +379,33 @@ __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* 
     }
     uint32_t total;
     const uint32_t pos = block_excl_scan<uint32_t, 512>(cnt, wsum, &total);
-    for (uint32_t k = 0; k < cnt && pos + k < (uint32_t)G1_LIST; ++k) list[pos + k] = (int)(base + k);
-    __syncthreads();
-    int j = g;
-    for (; j + 12 < (int)total; j += 16) {
-      const size_t l0 = (size_t)list[j] * 128, l1 = (size_t)list[j + 4] * 128;
-      const size_t l2 = (size_t)list[j + 8] * 128, l3 = (size_t)list[j + 12] * 128;
-      a[0] += P0[l0];
-      a[1] += P1[l0];
-      a[2] += P0[l1];
-      a[3] += P1[l1];
-      a[4] += P0[l2];
-      a[5] += P1[l2];
-      a[6] += P0[l3];
-      a[7] += P1[l3];
+    // the round's slice list, G1_LIST entries at a time
+    for (uint32_t w0 = 0; w0 < total; w0 += G1_LIST) {
+      const uint32_t k0 = w0 > pos ? w0 - pos : 0u, k1e = w0 + G1_LIST - pos;
+      const uint32_t k1 = pos >= w0 + G1_LIST ? 0u : (cnt < k1e ? cnt : k1e);
+      for (uint32_t k = k0; k < k1; ++k) list[pos + k - w0] = (int)(base + k);
+      __syncthreads();
+      const int wn = (int)(total - w0 < (uint32_t)G1_LIST ? total - w0 : (uint32_t)G1_LIST);
+      int j = g;
+      for (; j + 12 < wn; j += 16) {
+        const size_t l0 = (size_t)list[j] * 128, l1 = (size_t)list[j + 4] * 128;
+        const size_t l2 = (size_t)list[j + 8] * 128, l3 = (size_t)list[j + 12] * 128;
+        a[0] += P0[l0];
+        a[1] += P1[l0];
+        a[2] += P0[l1];
+        a[3] += P1[l1];
+        a[4] += P0[l2];
+        a[5] += P1[l2];
+        a[6] += P0[l3];
+        a[7] += P1[l3];
+      }
+      for (; j < wn; j += 4) {
+        const size_t l0 = (size_t)list[j] * 128;
+        a[0] += P0[l0];
+        a[1] += P1[l0];
+      }
+      __syncthreads();
     }
-    for (; j < (int)total; j += 4) {
-      const size_t l0 = (size_t)list[j] * 128;
-      a[0] += P0[l0];
-      a[1] += P1[l0];
-    }
-    __syncthreads();
   }
   red[g][e] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   __syncthreads();

@@ -21,6 +21,8 @@ struct Shape {
   int key_bits;    // significant bits of kinv
   int n12;         // n1*n2 prefixes per table
   int64_t ndense;  // T*n1*n2 prefix slots
+  int slice_rows;  // rows per work slice: SLICE_ROWS, or 1 when prefix reuse is off (ablation)
+  int dedup;       // 1: exact dedup of rows; 0: every occurrence is its own row (ablation)
 };
 
 // Counter slots at the head of the workspace (int32).

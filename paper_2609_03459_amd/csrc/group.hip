@@ -392,7 +392,7 @@ hipError_t scan_u32_exclusive(const uint32_t* in, uint32_t* out, int64_t n, uint
 // prefix group when, in addition, key / n3 (table and prefix) differs.  Counts
 // are packed (rows | groups << 32).
 __global__ void __launch_bounds__(SCAN_THREADS) k_group_reduce(const uint32_t* __restrict__ sk, int n, uint32_t kinv,
-                                                               uint32_t n3, uint64_t* __restrict__ tsum,
+                                                               uint32_t n3, int dedup, uint64_t* __restrict__ tsum,
                                                                int32_t* __restrict__ ctr) {
   __shared__ uint64_t smem[SCAN_THREADS / 64];
   const int base = blockIdx.x * SCAN_TILE;
@@ -404,7 +404,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_reduce(const uint32_t* _
       const uint32_t k = sk[i];
       if (k < kinv) {
         const uint32_t kp = i > 0 ? sk[i - 1] : 0u;
-        const bool head = i == 0 || kp != k;
+        const bool head = i == 0 || kp != k || !dedup;
         const bool pgh = head && (i == 0 || kp / n3 != k / n3);
         c += (uint64_t)head | ((uint64_t)pgh << 32);
         if (i == n - 1 || sk[i + 1] >= kinv) ctr[C_NVALID] = i + 1;
@@ -424,7 +424,7 @@ __device__ __forceinline__ int pad32(int x) { return x + (x >> 5); }
 
 __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __restrict__ sk,
                                                              const uint32_t* __restrict__ sp, int n, uint32_t kinv,
-                                                             uint32_t n3, uint32_t Npad,
+                                                             uint32_t n3, uint32_t Npad, int dedup,
                                                              const uint64_t* __restrict__ tsum,
                                                              int32_t* __restrict__ inv, int32_t* __restrict__ sorted_uid,
                                                              uint32_t* __restrict__ uniq_key,
@@ -454,7 +454,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
     const int i = base + e0 + k;
     const uint32_t key = lk[pad32(e0 + k + 1)], kp = lk[pad32(e0 + k)];
     if (i < n && key < kinv) {
-      const bool head = i == 0 || kp != key;
+      const bool head = i == 0 || kp != key || !dedup;
       const bool pgh = head && (i == 0 || kp / n3 != key / n3);
       hb |= (uint32_t)head << k;
       pb |= (uint32_t)pgh << k;
@@ -484,7 +484,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
     if (uid < 0) continue;
     sorted_uid[i] = uid;
     const uint32_t key = lk[pad32(e + 1)], kp = lk[pad32(e)];
-    if (i == 0 || kp != key) {
+    if (i == 0 || kp != key || !dedup) {
       uniq_key[uid] = key;
       uniq_i3[uid] = (int)((key % Npad) % n3);
       occ_start[uid] = i;
@@ -508,8 +508,8 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
 
 // prefix slots in (table, i2, i1) order: slices per group
 __global__ void k_dense_set(const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key,
-                            const int32_t* __restrict__ ctr, int n1, int n2, uint32_t* __restrict__ dense_cnt,
-                            int32_t* __restrict__ dense_pg) {
+                            const int32_t* __restrict__ ctr, int n1, int n2, int slice_rows,
+                            uint32_t* __restrict__ dense_cnt, int32_t* __restrict__ dense_pg) {
   const int P = ctr[C_P];
   const int n12 = n1 * n2;
   for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < P; p += gridDim.x * blockDim.x) {
@@ -518,7 +518,7 @@ __global__ void k_dense_set(const int32_t* __restrict__ pg_start, const uint32_t
     uint32_t i1 = q / n2, i2 = q % n2;
     int64_t slot = ((int64_t)t * n2 + i2) * n1 + i1;
     int rows = pg_start[p + 1] - pg_start[p];
-    dense_cnt[slot] = (uint32_t)((rows + SLICE_ROWS - 1) / SLICE_ROWS);
+    dense_cnt[slot] = (uint32_t)((rows + slice_rows - 1) / slice_rows);
     dense_pg[slot] = p;
   }
 }
@@ -526,7 +526,7 @@ __global__ void k_dense_set(const int32_t* __restrict__ pg_start, const uint32_t
 __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint32_t* __restrict__ dense_base,
                               const int32_t* __restrict__ dense_pg, int64_t ndense,
                               const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key, int n1,
-                              int4* __restrict__ slices, int32_t* __restrict__ slice_i1) {
+                              int slice_rows, int4* __restrict__ slices, int32_t* __restrict__ slice_i1) {
   for (int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; s < ndense;
        s += (int64_t)gridDim.x * blockDim.x) {
     uint32_t c = dense_cnt[s];
@@ -535,8 +535,8 @@ __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint
     uint32_t b = dense_base[s];
     int r0 = pg_start[p], r1 = pg_start[p + 1];
     for (uint32_t k = 0; k < c; ++k) {
-      int rb = r0 + (int)k * SLICE_ROWS;
-      int re = rb + SLICE_ROWS < r1 ? rb + SLICE_ROWS : r1;
+      int rb = r0 + (int)k * slice_rows;
+      int re = rb + slice_rows < r1 ? rb + slice_rows : r1;
       slices[b + k] = make_int4(p, rb, re, (int)pg_key[p]);
       slice_i1[b + k] = (int)(s % n1);  // slot = (t * n2 + i2) * n1 + i1
     }
@@ -650,20 +650,22 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   const uint32_t* sp = w.vals[cur];
   {
     const int gt = (n + SCAN_TILE - 1) / SCAN_TILE;
-    hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, w.tsum64,
-                       w.ctr);
+    hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, s.dedup,
+                       w.tsum64, w.ctr);
     hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
     hipLaunchKernelGGL(k_group_down, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
-                       (const uint64_t*)w.tsum64, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
+                       s.dedup, (const uint64_t*)w.tsum64, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
                        w.pg_start, w.pg_key, w.ctr);
   }
   hipLaunchKernelGGL(k_dense_set, dim3(grid_for(M, 256, 2048)), dim3(256), 0, st, (const int32_t*)w.pg_start,
-                     (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, w.dense_cnt, w.dense_pg);
+                     (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, s.slice_rows, w.dense_cnt,
+                     w.dense_pg);
   e = scan_generic<uint32_t, false>(w.dense_cnt, w.dense_base, s.ndense, w.tsum32, w.ctr + C_NSLICES, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
                      (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
-                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, w.slices, w.slice_i1);
+                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, s.slice_rows, w.slices,
+                     w.slice_i1);
   const int nruns = s.T * s.n2;
   hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
                      (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);

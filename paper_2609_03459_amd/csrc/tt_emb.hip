@@ -66,7 +66,8 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->dense_base = (uint32_t*)take(4 * s.ndense);
   W->dense_pg = (int32_t*)take(4 * s.ndense);
   // slices: at most one per valid occurrence and ceil(n3 / SLICE_ROWS) per prefix
-  const int64_t per_prefix = (s.n3 + SLICE_ROWS - 1) / SLICE_ROWS;
+  // (without dedup a prefix can hold any number of rows: bounded by m alone)
+  const int64_t per_prefix = s.dedup ? (s.n3 + s.slice_rows - 1) / s.slice_rows : m;
   int64_t nsl_max = s.ndense * per_prefix;
   if (nsl_max > m) nsl_max = m;
   int64_t nch_max = nsl_max / CHUNK_SLICES + (int64_t)s.T * s.n2 + 1;
@@ -176,6 +177,8 @@ tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
   s.key_bits = bit_length(s.kinv);
   s.n12 = s.n1 * s.n2;
   s.ndense = (int64_t)T * s.n1 * s.n2;
+  s.slice_rows = SLICE_ROWS;
+  s.dedup = 1;
   h->g_valid = false;
   h->prof.kernel = 0;
   h->prof.begin = nullptr;
@@ -195,6 +198,14 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
 
 tt_emb_status tt_emb_destroy(tt_emb_handle h) {
   delete h;
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level) {
+  if (!h || level < TT_EMB_REUSE_PREFIX || level > TT_EMB_REUSE_NONE) return TT_EMB_EINVAL;
+  h->s.slice_rows = level == TT_EMB_REUSE_PREFIX ? SLICE_ROWS : 1;
+  h->s.dedup = level == TT_EMB_REUSE_NONE ? 0 : 1;
+  h->g_valid = false;  // a grouping made at another level must not be reused
   return TT_EMB_OK;
 }
 

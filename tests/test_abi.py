@@ -89,3 +89,20 @@ def test_calls_reject_bad_arguments_without_launching(N):
     assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
     assert N.lib.tt_emb_debug_grouping(h, fake, None, None, None, None, None, None, None, None, None) == E
     N.tt_emb_destroy(h)
+
+
+def test_reuse_levels_and_workspace(N):
+    h = N.tt_emb_create(_desc(N, T=2, M=1000, B=100))
+    base = N.tt_emb_workspace_size(h)
+    assert N.lib.tt_emb_set_reuse(h, 3) == N.TT_EMB_EINVAL
+    assert N.lib.tt_emb_set_reuse(h, -1) == N.TT_EMB_EINVAL
+    assert N.lib.tt_emb_set_reuse(None, 0) == N.TT_EMB_EINVAL
+    sizes = {}
+    for name, level in N.REUSE.items():
+        N.tt_emb_set_reuse(h, level)
+        sizes[name] = N.tt_emb_workspace_size(h)
+    assert sizes["prefix"] == base
+    # one slice per row (and per occurrence without dedup) needs more room
+    assert sizes["unique"] >= base and sizes["none"] >= sizes["unique"]
+    N.tt_emb_destroy(h)
+

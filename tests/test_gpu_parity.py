@@ -149,6 +149,34 @@ def test_many_short_bags(lib, orc):
     assert np.array_equal(got["inv"], ref["inv"]) and np.array_equal(got["occ_pos"], ref["occ_pos"])
 
 
+@pytest.mark.parametrize("reuse", ["unique", "none"])
+@pytest.mark.parametrize("k", [4, 5, 7])
+def test_reuse_levels_same_results(lib, orc, reuse, k):
+    # Section 4.5 ablation levels compute the same function: forward and backward
+    # against the oracle with exact dedup only, and with no dedup at all
+    c = dict(TINY[k])
+    case = ttgen.tiny(4000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    _say(f"[reuse {reuse}] tiny{k}")
+    M = int(case["idx"].size)
+    emb = lib.TTEmbedding(case["T"], case["N"], case["n"], case["d"], case["R"], max_indices=max(M, 1),
+                          max_bags=max(int(case["B"]), 1), reuse=reuse)
+    G, idx, off = _dev(case)
+    D = int(np.prod(case["d"]))
+    out = emb.forward(*G, idx, off, num_bags=case["B"])
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    ref, _ = orc.forward(case)
+    mag, _ = orc.forward(abs_case(case))
+    assert_close(f"forward {reuse}", out.cpu().numpy().reshape(-1, D), ref, mag)
+    dV = torch.from_numpy(case["dV"]).cuda()
+    grads = emb.backward(*G, idx, off, dV, num_bags=case["B"])
+    torch.cuda.synchronize()
+    refg = orc.backward(case)
+    magg = orc.backward(abs_case(case))
+    for k2, name in enumerate(("dG1", "dG2", "dG3")):
+        assert_close(f"{name} {reuse}", grads[k2].cpu().numpy().ravel(), refg[k2].ravel(), magg[k2].ravel())
+
+
 def _rank2_cores(n, d, R):
     n1, n2, n3 = n
     d1, d2, d3 = d
