@@ -543,6 +543,34 @@ __global__ void k_make_slices(const uint32_t* __restrict__ dense_cnt, const uint
   }
 }
 
+// One-row slices (reuse ablation levels): one thread per slice, so a hot prefix
+// with many occurrences is not written out by a single thread. The slice's slot
+// is found by binary search over the exclusive scan of the slice counts.
+__global__ void k_make_slices_rows(const uint32_t* __restrict__ dense_base,
+                                   const int32_t* __restrict__ dense_pg, int64_t ndense,
+                                   const int32_t* __restrict__ pg_start, const uint32_t* __restrict__ pg_key,
+                                   int n1, const int32_t* __restrict__ ctr, int4* __restrict__ slices,
+                                   int32_t* __restrict__ slice_i1) {
+  const int nsl = ctr[C_NSLICES];
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < nsl; x += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo = 0, hi = ndense;  // first slot with base > x, minus one
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (dense_base[mid] <= (uint32_t)x)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    // An empty slot shares its base with the slot after it, so the last slot whose
+    // base does not exceed x is never empty (x < nsl rules out an empty final slot).
+    const int64_t slot = lo - 1;
+    const int p = dense_pg[slot];
+    const int rb = pg_start[p] + (int)((uint32_t)x - dense_base[slot]);
+    slices[x] = make_int4(p, rb, rb + 1, (int)pg_key[p]);
+    slice_i1[x] = (int)(slot % n1);
+  }
+}
+
 // chunks of the specialised kernels: up to CHUNK_SLICES consecutive slices of
 // one (t, i2) run; run r covers slices [dense_base[r*n1], dense_base[(r+1)*n1])
 __global__ void k_run_counts(const uint32_t* __restrict__ dense_base, const int32_t* __restrict__ ctr, int nruns,
@@ -662,10 +690,16 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
                      w.dense_pg);
   e = scan_generic<uint32_t, false>(w.dense_cnt, w.dense_base, s.ndense, w.tsum32, w.ctr + C_NSLICES, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
-                     (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
-                     s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, s.slice_rows, w.slices,
-                     w.slice_i1);
+  if (s.slice_rows == 1)
+    hipLaunchKernelGGL(k_make_slices_rows, dim3(grid_for(M, 256, 8192)), dim3(256), 0, st,
+                       (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
+                       s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, (const int32_t*)w.ctr,
+                       w.slices, w.slice_i1);
+  else
+    hipLaunchKernelGGL(k_make_slices, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
+                       (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const int32_t*)w.dense_pg,
+                       s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, s.slice_rows,
+                       w.slices, w.slice_i1);
   const int nruns = s.T * s.n2;
   hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
                      (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
