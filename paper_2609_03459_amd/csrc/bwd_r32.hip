@@ -42,24 +42,21 @@ __device__ __forceinline__ uint64_t add2(uint64_t w, float a, float b) {
   const float lo = __uint_as_float((uint32_t)w) + a, hi = __uint_as_float((uint32_t)(w >> 32)) + b;
   return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
 }
+__device__ __forceinline__ bool lds_cas2(uint64_t* u, uint64_t& seen, float a, float b) {
+  return __hip_atomic_compare_exchange_strong(u, &seen, add2(seen, a, b), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_WORKGROUP);
+}
 __device__ __forceinline__ void lds_add4(float* p, f32x4 v) {
   uint64_t* u = reinterpret_cast<uint64_t*>(p);
-  const uint64_t s0 = __hip_atomic_load(u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  const uint64_t s1 = __hip_atomic_load(u + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  uint64_t g0 = s0, g1 = s1;
-  bool d0 = __hip_atomic_compare_exchange_strong(u, &g0, add2(s0, v[0], v[1]), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-  bool d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, add2(s1, v[2], v[3]), __ATOMIC_RELAXED,
-                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  while (!d0) {
-    const uint64_t cur = g0;
-    d0 = __hip_atomic_compare_exchange_strong(u, &g0, add2(cur, v[0], v[1]), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_WORKGROUP);
-  }
-  while (!d1) {
-    const uint64_t cur = g1;
-    d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, add2(cur, v[2], v[3]), __ATOMIC_RELAXED,
-                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  // both words in one 16-byte read: a stale or torn word only fails its swap, which
+  // then retries with the value the swap returned
+  const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(u);
+  uint64_t g0 = w.x, g1 = w.y;
+  bool d0 = lds_cas2(u, g0, v[0], v[1]);
+  bool d1 = lds_cas2(u + 1, g1, v[2], v[3]);
+  while (!(d0 && d1)) {
+    if (!d0) d0 = lds_cas2(u, g0, v[0], v[1]);
+    if (!d1) d1 = lds_cas2(u + 1, g1, v[2], v[3]);
   }
 }
 
@@ -83,6 +80,7 @@ struct BwPair {
   float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
   float4 d4;    // dC B operand: G3[i3 of that row][16 h + l15][4 (l4 & 1) + k]
   int i3m;      // i3 of this lane's dD column
+  int j;        // the pair's slice within the quad (wave-uniform)
   bool live;    // this lane's dD column is a real row
 };
 
@@ -129,33 +127,36 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   // other lanes have no rows): first row, row count, i1
   int c_rb = 0, c_nr = 0, c_i1 = 0;
   int qd = 0;  // first slice of the current quad within the chunk
-  // i3 of the quad's rows: slice j row k in lane 32 (j & 1) + k of i3A (j < 2) or i3B (j >= 2);
-  // n3A / n3B hold the same for the next quad of the chunk (loaded one quad ahead)
-  int i3A = 0, i3B = 0, n3A = 0, n3B = 0;
-  auto load_i3 = [&](int qd0, int& A, int& Bv) {
-    const int ja = lane >> 5, k = lane & 31;
-    const int r0 = __builtin_amdgcn_readlane(c_rb, qd0), r1 = __builtin_amdgcn_readlane(c_rb, qd0 + 1);
-    const int r2 = __builtin_amdgcn_readlane(c_rb, qd0 + 2), r3 = __builtin_amdgcn_readlane(c_rb, qd0 + 3);
+  // Row-pair descriptors of a quad, lane P holding pair P (P < np; slice j owns
+  // (nr_j + 1) / 2 consecutive pairs): the pair's first row, and packed, i3 of its
+  // two rows (8 bits each, n3 <= 256), its slice j and whether the second row is
+  // real.  Built one quad ahead (e_*) so the i3 loads are in flight meanwhile.
+  int d_ra = 0, d_pk = 0, np = 0;
+  int e_ra = 0, e_ia = 0, e_ib = 0, e_jh = 0, e_np = 0;
+  auto build_desc = [&](int qd0) {
     const int n0 = __builtin_amdgcn_readlane(c_nr, qd0), n1 = __builtin_amdgcn_readlane(c_nr, qd0 + 1);
     const int n2 = __builtin_amdgcn_readlane(c_nr, qd0 + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd0 + 3);
-    const int rA = ja ? r1 : r0, nA = ja ? n1 : n0;
-    const int rB = ja ? r3 : r2, nB = ja ? n3 : n2;
-    A = uniq_i3[rA + (k < nA ? k : 0)];
-    Bv = uniq_i3[rB + (k < nB ? k : 0)];
+    const int b0 = __builtin_amdgcn_readlane(c_rb, qd0), b1 = __builtin_amdgcn_readlane(c_rb, qd0 + 1);
+    const int b2 = __builtin_amdgcn_readlane(c_rb, qd0 + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd0 + 3);
+    const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
+    e_np = q3 + ((n3 + 1) >> 1);
+    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
+    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
+    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    const bool ok = lane < e_np;
+    const bool has1 = ok && pr + 1 < nr;
+    e_ra = ok ? rb + pr : b0;  // lanes past the quad's pairs keep a valid row
+    e_ia = uniq_i3[e_ra];
+    e_ib = uniq_i3[has1 ? e_ra + 1 : e_ra];
+    e_jh = (j << 16) | (has1 ? 1 << 18 : 0);
   };
-  // row pairs of the quad, flattened: slice j owns pairs [cp_j, cp_{j+1}), cp_0 = 0
-  int cp1 = 0, cp2 = 0, cp3 = 0, np = 0;
   auto pair_load = [&](BwPair& X, int P) {
-    const int pj = (P >= cp1) + (P >= cp2) + (P >= cp3);
-    const int pr = 2 * (P - (pj == 0 ? 0 : (pj == 1 ? cp1 : (pj == 2 ? cp2 : cp3))));
-    const int rb = __builtin_amdgcn_readlane(c_rb, qd + pj), nr = __builtin_amdgcn_readlane(c_nr, qd + pj);
-    const bool has1 = pr + 1 < nr;
-    const int i3v = pj < 2 ? i3A : i3B;
-    const int li = (pj & 1) * 32 + pr;
-    const int i3a = __builtin_amdgcn_readlane(i3v, li);
-    const int i3b = __builtin_amdgcn_readlane(i3v, has1 ? li + 1 : li);
-    // rows r0 and r1 (r1 = the zero row for a lone last row), both scalar
-    const int ra = rb + pr, r1 = has1 ? ra + 1 : zrow;
+    const int ra = __builtin_amdgcn_readlane(d_ra, P), pk = __builtin_amdgcn_readlane(d_pk, P);
+    const int i3a = pk & 255, i3b = (pk >> 8) & 255;
+    const bool has1 = (pk >> 18) & 1;
+    X.j = (pk >> 16) & 3;
+    // rows ra and r1 (r1 = the zero row for a lone last row), both scalar
+    const int r1 = has1 ? ra + 1 : zrow;
     const float* Es = dE + (uint32_t)ra * 128u;
     const uint32_t dl = (uint32_t)(r1 - ra) * 128u;  // second row, relative to the first
     const uint32_t ob = o_eb + (rowsel ? dl : 0u);
@@ -181,7 +182,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       c_rb = sd.y;
       c_nr = lane < ns ? sd.z - sd.y : 0;
       c_i1 = slice_i1[sl];
-      load_i3(0, n3A, n3B);
+      build_desc(0);
     }
     qd = 0;
     return cc;
@@ -208,17 +209,10 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     const int nqs = ns - qd < 4 ? ns - qd : 4;
     const int sb = f + qd;
-    i3A = n3A;
-    i3B = n3B;
-    if (qd + 4 < ns) load_i3(qd + 4, n3A, n3B);  // next quad of this chunk, one quad ahead
-    {
-      const int nra = __builtin_amdgcn_readlane(c_nr, qd), nrb = __builtin_amdgcn_readlane(c_nr, qd + 1);
-      const int nrc = __builtin_amdgcn_readlane(c_nr, qd + 2), nrd = __builtin_amdgcn_readlane(c_nr, qd + 3);
-      cp1 = (nra + 1) >> 1;
-      cp2 = cp1 + ((nrb + 1) >> 1);
-      cp3 = cp2 + ((nrc + 1) >> 1);
-      np = cp3 + ((nrd + 1) >> 1);
-    }
+    d_ra = e_ra;
+    d_pk = e_ia | (e_ib << 8) | e_jh;
+    np = e_np;
+    if (qd + 4 < ns) build_desc(qd + 4);  // next quad of this chunk, one quad ahead
     // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
     const int aj = l15 >> 2;
     const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
@@ -288,22 +282,21 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     // sets: the operands of the next two pairs are always in flight while one is
     // computed (indices clamped, so every load is unconditional and in bounds)
     int cj = 0;
-    auto step = [&](const BwPair& X, int Pc) {
-      const int j = (Pc >= cp1) + (Pc >= cp2) + (Pc >= cp3);
-      if (j != cj) {
+    auto step = [&](const BwPair& X) {
+      if (X.j != cj) {
         slice_end(cj);
-        slice_begin(j);
-        cj = j;
+        slice_begin(X.j);
+        cj = X.j;
       }
       pair_compute(X);
     };
     for (int P = 0; P < np; P += 3) {
       pair_load(XC, P + 2 < np ? P + 2 : np - 1);
-      step(XA, P);
+      step(XA);
       pair_load(XA, P + 3 < np ? P + 3 : np - 1);
-      if (P + 1 < np) step(XB, P + 1);
+      if (P + 1 < np) step(XB);
       pair_load(XB, P + 4 < np ? P + 4 : np - 1);
-      if (P + 2 < np) step(XC, P + 2);
+      if (P + 2 < np) step(XC);
     }
     slice_end(cj);
     wave_lds_sync();
