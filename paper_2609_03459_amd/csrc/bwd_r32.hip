@@ -187,10 +187,33 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     qd = 0;
     return cc;
   };
+  // The next quad's operands are loaded before the current quad's dA product, so
+  // that product and its stores cover their latency: its row-pair descriptors,
+  // its stage-1 A operand (clamped rows, zeroed at use for missing slices) and
+  // its first two row pairs.  At a chunk end the next chunk is claimed first.
+  float Aop[8];
+  BwPair XA, XB, XC;
+  auto prefetch_quad = [&]() {
+    d_ra = e_ra;
+    d_pk = e_ia | (e_ib << 8) | e_jh;
+    np = e_np;
+    if (qd + 4 < ns) build_desc(qd + 4);  // the quad after it, one quad ahead
+    const int nq4 = ns - qd < 4 ? ns - qd : 4;
+    const int aj = l15 >> 2;
+    const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
+    const int i1c = __builtin_amdgcn_readlane(c_i1, qd + 2), i1d = __builtin_amdgcn_readlane(c_i1, qd + 3);
+    const float* Ag = G1t + (uint32_t)sel4(aj < nq4 ? aj : 0, i1a, i1b, i1c, i1d) * 128u +
+                      (uint32_t)((lane & 3) * 32 + l4);
+#pragma unroll
+    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
+    pair_load(XA, 0);
+    pair_load(XB, np > 1 ? 1 : 0);
+  };
   int c = next_chunk();
+  if (c >= 0) prefetch_quad();
   while (c >= 0) {
-    const float* Bg = G2 + (uint32_t)run * 4096u + 16 * h;
     if (run != cur_run) {
+      const float* Bg = G2 + (uint32_t)run * 4096u + 16 * h;
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4)
 #pragma unroll
@@ -209,25 +232,10 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     const int nqs = ns - qd < 4 ? ns - qd : 4;
     const int sb = f + qd;
-    d_ra = e_ra;
-    d_pk = e_ia | (e_ib << 8) | e_jh;
-    np = e_np;
-    if (qd + 4 < ns) build_desc(qd + 4);  // next quad of this chunk, one quad ahead
-    // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
-    const int aj = l15 >> 2;
-    const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
-    const int i1c = __builtin_amdgcn_readlane(c_i1, qd + 2), i1d = __builtin_amdgcn_readlane(c_i1, qd + 3);
-    const float* Ag = G1t + (uint32_t)sel4(aj < nqs ? aj : 0, i1a, i1b, i1c, i1d) * 128u +
-                      (uint32_t)((lane & 3) * 32 + l4);
-    float Aop[8];
-#pragma unroll
-    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
-    BwPair XA, XB, XC;
-    pair_load(XA, 0);  // first two row pairs, in flight during stage 1
-    pair_load(XB, np > 1 ? 1 : 0);
-    const bool aj_ok = aj < nqs;
-    // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64)
+    // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64),
+    // Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
     {
+      const bool aj_ok = (l15 >> 2) < nqs;
       f32x4 Cs[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -300,6 +308,16 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     slice_end(cj);
     wave_lds_sync();
+    // the next quad: the rest of this chunk, or the first quad of the next chunk
+    const int c_done = c;
+    const bool chunk_end = qd + 4 >= ns;
+    if (!chunk_end) {
+      qd += 4;
+      prefetch_quad();
+    } else {
+      c = next_chunk();
+      if (c >= 0) prefetch_quad();
+    }
     // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32)
     {
       const int ms = l15 >> 2, mj1 = lane & 3;
@@ -324,17 +342,15 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       }
     }
     wave_lds_sync();
-    qd += 4;
-    if (qd >= ns) {
-      // end of the chunk: dB_h partial, lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
-      float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c)) * 2048;
+    if (chunk_end) {
+      // dB_h partial of the finished chunk, lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
+      float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c_done)) * 2048;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
-      c = next_chunk();
     }
   }
   __syncthreads();
