@@ -46,14 +46,16 @@ __device__ __forceinline__ bool lds_cas2(uint64_t* u, uint64_t& seen, float a, f
   return __hip_atomic_compare_exchange_strong(u, &seen, add2(seen, a, b), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-__device__ __forceinline__ void lds_add4(float* p, f32x4 v) {
+// p[0..3] += v, given w: both words as read earlier (one 16-byte read) and n: the
+// words with v added.  A stale or torn word only fails its swap, which then retries
+// with the value the swap returned.
+__device__ __forceinline__ void lds_add4(float* p, const ulonglong2& w, uint64_t n0, uint64_t n1, f32x4 v) {
   uint64_t* u = reinterpret_cast<uint64_t*>(p);
-  // both words in one 16-byte read: a stale or torn word only fails its swap, which
-  // then retries with the value the swap returned
-  const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(u);
   uint64_t g0 = w.x, g1 = w.y;
-  bool d0 = lds_cas2(u, g0, v[0], v[1]);
-  bool d1 = lds_cas2(u + 1, g1, v[2], v[3]);
+  bool d0 = __hip_atomic_compare_exchange_strong(u, &g0, n0, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+  bool d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, n1, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
   while (!(d0 && d1)) {
     if (!d0) d0 = lds_cas2(u, g0, v[0], v[1]);
     if (!d1) d1 = lds_cas2(u + 1, g1, v[2], v[3]);
@@ -79,9 +81,10 @@ struct BwPair {
                 // (a lone last row pairs with the all-zero row zrow)
   float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
   float4 d4;    // dC B operand: G3[i3 of that row][16 h + l15][4 (l4 & 1) + k]
-  int i3m;      // i3 of this lane's dD column
+  int i3m;      // accumulator row of this lane's dD column: i3 of its row, or for the
+                // zero row's column (exact zeros) a neighbouring i3, so that its no-op
+                // swap never targets the same words as a live lane of the pair
   int j;        // the pair's slice within the quad (wave-uniform)
-  bool live;    // this lane's dD column is a real row
 };
 
 __global__ void __launch_bounds__(64 * BW_WAVES, 1)
@@ -164,8 +167,8 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = Es[ob + 32u * s4];
     X.e4 = *(const float4*)(Es + o_e4 + (prow ? dl : 0u));
     X.d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
-    X.i3m = rowsel ? i3b : i3a;
-    X.live = has1 || !rowsel;
+    const int i3z = i3a > 0 ? i3a - 1 : (s.n3 > 1 ? 1 : 0);
+    X.i3m = rowsel ? (has1 ? i3b : i3z) : i3a;
   };
 
   int f = 0, ns = 0, run = -1;
@@ -264,6 +267,10 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     slice_begin(0);
     f32x4 dC = {0.f, 0.f, 0.f, 0.f};
     auto pair_compute = [&](const BwPair& X) {
+      // this lane's accumulator words, read before the products so the read's
+      // latency overlaps them
+      float* ap = g3acc + (uint32_t)X.i3m * 128u + o_g3;
+      const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(ap);
       f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], X.eb[s4], dd, 0, 0, 0);
@@ -272,7 +279,9 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.z, X.d4.z, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.w, X.d4.w, dC, 0, 0, 0);
       // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7]
-      if (X.live) lds_add4(g3acc + (uint32_t)X.i3m * 128u + o_g3, dd);
+      // every lane swaps (the zero row's column adds exact zeros), so the add is
+      // straight-line code and the read stays ahead of the products
+      lds_add4(ap, w, add2(w.x, dd[0], dd[1]), add2(w.y, dd[2], dd[3]), dd);
     };
     // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
     auto slice_end = [&](int j) {
