@@ -75,10 +75,10 @@ __device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
   return j == 0 ? a : (j == 1 ? b : (j == 2 ? c : d));
 }
 
-// operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs with itself)
+// operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs
+// with a row of zeros, which its buffer loads return past the end of the pair)
 struct BwPair {
   float eb[4];  // dD B operand: dE[row][(4 s + l4) * 8 + j3], row r0 in lanes 0-7 of each 16, r0 + 1 in 8-15
-                // (a lone last row pairs with the all-zero row zrow)
   float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
   float4 d4;    // dC B operand: G3[i3 of that row][16 h + l15][4 (l4 & 1) + k]
   int i3m;      // accumulator row of this lane's dD column: i3 of its row, or for the
@@ -92,7 +92,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
               const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
               const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
               const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ dApart,
-              float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap, int zrow) {
+              float* __restrict__ dBpart, float* __restrict__ g3part, int nsl_cap, int nch_cap) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -113,12 +113,15 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const bool rowsel = (l15 >> 3) != 0;  // dD column of row r0 + 1
   const bool prow = (l4 >> 1) != 0;     // dC K slots of row r0 + 1
   // per-lane float offsets; every operand is a uniform base plus one of these
-  const uint32_t o_eb = (uint32_t)(l4 * 8 + (lane & 7));
-  const uint32_t o_e4 = (uint32_t)(l15 * 8 + 4 * (l4 & 1));
-  const uint32_t o_d4 = (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));
+  // byte offsets of this lane's operand words: in a pair's two dE rows (the second
+  // row 512 bytes on) and in a G3[t] row
+  const uint32_t vo_eb = 4u * (uint32_t)(l4 * 8 + (lane & 7) + (rowsel ? 128 : 0));
+  const uint32_t vo_e4 = 4u * (uint32_t)(l15 * 8 + 4 * (l4 & 1) + (prow ? 128 : 0));
+  const uint32_t vo_d4 = 4u * (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));
   const uint32_t o_g3 = g3_slot_base(lane & 7, l4);  // this lane's four dD values in an accumulator row
   const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
   const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
+  const buf_t g3buf = make_buf(G3t, (uint32_t)s.n3 * 1024u);
 
   int cursor = 0;
   int cur_run = -1;
@@ -158,15 +161,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     const int i3a = pk & 255, i3b = (pk >> 8) & 255;
     const bool has1 = (pk >> 18) & 1;
     X.j = (pk >> 16) & 3;
-    // rows ra and r1 (r1 = the zero row for a lone last row), both scalar
-    const int r1 = has1 ? ra + 1 : zrow;
-    const float* Es = dE + (uint32_t)ra * 128u;
-    const uint32_t dl = (uint32_t)(r1 - ra) * 128u;  // second row, relative to the first
-    const uint32_t ob = o_eb + (rowsel ? dl : 0u);
+    // rows ra and ra + 1 through one descriptor that ends after the rows that exist
+    const buf_t eb = make_buf(dE + (size_t)(uint32_t)ra * 128, has1 ? 1024u : 512u);
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = Es[ob + 32u * s4];
-    X.e4 = *(const float4*)(Es + o_e4 + (prow ? dl : 0u));
-    X.d4 = *(const float4*)(G3t + (uint32_t)(prow ? i3b : i3a) * 256u + o_d4);
+    for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = buf_f32(eb, vo_eb, 128u * s4);
+    X.e4 = buf_f32x4(eb, vo_e4);
+    X.d4 = buf_f32x4(g3buf, vo_d4 + (uint32_t)(prow ? i3b : i3a) * 1024u);
     const int i3z = i3a > 0 ? i3a - 1 : (s.n3 > 1 ? 1 : 0);
     X.i3m = rowsel ? (has1 ? i3b : i3z) : i3a;
   };
@@ -481,9 +481,6 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   if (grid > MAX_BWD_WG || nq * SCHED_STRIDE > C_TOTAL - C_BWD_CTR) return hipErrorInvalidValue;
   hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), nq * SCHED_STRIDE, 0u, st);
   if (e != hipSuccess) return e;
-  // the zero dE row that a lone last row of a slice is paired with
-  e = fill_u32(reinterpret_cast<uint32_t*>(w.E + (size_t)w.zrow * 128), 128, 0u, st);
-  if (e != hipSuccess) return e;
   const size_t lds = sizeof(float) * ((size_t)s.n3 * 128 + BW_WAVES * BW_SCR);
   e = hipFuncSetAttribute((const void*)k_bwd_r32, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -491,7 +488,7 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   hipLaunchKernelGGL(k_bwd_r32, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
                      (const float*)w.E, (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
                      (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.g3part,
-                     (int)w.nsl_max, (int)w.nch_max, (int)w.zrow);
+                     (int)w.nsl_max, (int)w.nch_max);
   prof_end(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(512), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
                      (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1);

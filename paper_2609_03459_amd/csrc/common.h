@@ -85,8 +85,7 @@ struct Work {
   float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
   int64_t nsl_max, nch_max;
-  float* E;               // [M + 1][D]: E rows (forward), dE rows (backward); row M is the zero row
-  int64_t zrow;           // index of the zero row (max_indices)
+  float* E;               // [M][D]: E rows (forward), dE rows (backward)
   float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
   uint32_t* sorted_keys;  // = keys[x] after the sort
   uint32_t* sorted_pos;   // = vals[x] after the sort
@@ -250,6 +249,20 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // Orders this wave's LDS writes before its later LDS reads of other lanes'
 // data (a wave's LDS requests complete in order; this keeps the compiler
 // from reordering across the exchange and waits for outstanding writes).
+// Raw buffer loads through a gfx9 buffer descriptor (stride 0, dword data):
+// the address is base + offset (+ a wave-uniform offset), and a load at or past
+// num_bytes returns zero instead of touching memory.
+typedef __amdgpu_buffer_rsrc_t buf_t;
+__device__ __forceinline__ buf_t make_buf(const void* base, uint32_t num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)num_bytes, 0x00020000);
+}
+__device__ __forceinline__ float buf_f32(buf_t r, uint32_t off, uint32_t soff = 0) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0));
+}
+__device__ __forceinline__ float4 buf_f32x4(buf_t r, uint32_t off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();

@@ -78,8 +78,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->slice_i1 = (int32_t*)take(4 * nsl_max);
   W->run_nch = (uint32_t*)take(4 * ((int64_t)s.T * s.n2 + 1));
   W->chunks = (int4*)take(16 * nch_max);
-  W->E = (float*)take(4 * (size_t)(m + 1) * s.D);  // one spare row: the backward's zero row
-  W->zrow = m;
+  W->E = (float*)take(4 * (size_t)m * s.D);
   W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
   const bool bwd_r32 = s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64 &&
                        m * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
