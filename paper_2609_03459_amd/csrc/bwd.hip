@@ -11,7 +11,6 @@
 namespace ttemb {
 
 ShapeArgs shape_args(const Shape& s);
-bool bwd_r32_supported(const Shape& s, int64_t max_indices);
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st);
 

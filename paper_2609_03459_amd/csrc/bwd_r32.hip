@@ -20,7 +20,13 @@ namespace ttemb {
 ShapeArgs shape_args(const Shape& s);
 
 constexpr int BW_WAVES = 8;
-constexpr int BW_SCR = 1024;  // per-wave scratch floats: 4 slices x 16 x 16
+// Per-wave scratch: the quad's [slice][j1][(j2, b')] stack (16 rows of 64 floats),
+// first C_h, then dC_h, with rows SCR_PITCH floats apart.  The 4-float pad makes
+// every access a per-lane constant base plus an immediate offset and keeps the
+// C writes, C^T reads and dA operand reads at the two-lanes-per-bank minimum
+// (the dC writes, four per slice, take four lanes per bank).
+constexpr int SCR_PITCH = 68;
+constexpr int BW_SCR = 16 * SCR_PITCH;
 
 // The LDS dG3 accumulator holds, per table row i3, 128 floats ordered
 // [j3][16 slots]: rank row b' = 4 g + r of column j3 sits at slot
@@ -60,14 +66,6 @@ __device__ __forceinline__ void lds_add4(float* p, const ulonglong2& w, uint64_t
     if (!d0) d0 = lds_cas2(u, g0, v[0], v[1]);
     if (!d1) d1 = lds_cas2(u + 1, g1, v[2], v[3]);
   }
-}
-
-// Per-wave scratch holds a [slice][j1][(j2, b')] stack (4 x 4 x 64 floats): first
-// C_h, then dC_h.  The 64-float rows are XOR-swizzled by (8 slice + 10 j1) mod 64
-// so that all four access patterns (C and dC writes, C^T and dA operand reads)
-// put at most two of the 64 lanes on one bank.
-__device__ __forceinline__ uint32_t scr_at(int sl, int j1, int j2b) {
-  return (uint32_t)(sl * 256 + j1 * 64 + (j2b ^ ((8 * sl + 10 * j1) & 63)));
 }
 
 template <typename T>
@@ -121,12 +119,17 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   const uint32_t o_g3 = g3_slot_base(lane & 7, l4);  // this lane's four dD values in an accumulator row
   const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
   const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
+  // this lane's scratch bases: C write (row 4 l4 + r, column 16 nt + l15), dC write
+  // (row 4 j + l4, column 16 r + l15) and dA operand read (row l15, columns 16 l4 + s)
+  float* scr_c = scr + 4 * SCR_PITCH * l4 + l15;
+  float* scr_d = scr + SCR_PITCH * l4 + l15;
+  const float* scr_a = scr + SCR_PITCH * l15 + 16 * l4;
   const buf_t g3buf = make_buf(G3t, (uint32_t)s.n3 * 1024u);
 
   int cursor = 0;
   int cur_run = -1;
   float Bop[32];   // stage-1 B operand B_h[a = 4 s + l4][16 nt + l15], (s, nt) -> 4 s + nt
-  float BTop[32];  // dA B operand B_h^T[(j2, b') = 4 s2 + l4][a = 16 nt2 + l15], (s2, nt2) -> 2 s2 + nt2
+  float BTop[32];  // dA B operand B_h^T[(j2 = l4, b' = s)][a = 16 nt2 + l15], (s, nt2) -> 16 nt2 + s
   f32x4 dB[8];     // (mt, nt) -> 4 mt + nt
 
   // slice descriptors of the current chunk, lane j holding slice f + j (j < ns;
@@ -222,11 +225,15 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) Bop[4 * s4 + nt] = Bg[((4 * s4 + l4) * 4 + nt) * 32 + l15];
 #pragma unroll
-      for (int s2 = 0; s2 < 16; ++s2) {
-        const int k = 4 * s2 + l4;
-        BTop[2 * s2 + 0] = Bg[(l15 * 4 + (k >> 4)) * 32 + (k & 15)];
-        BTop[2 * s2 + 1] = Bg[((16 + l15) * 4 + (k >> 4)) * 32 + (k & 15)];
-      }
+      for (int nt2 = 0; nt2 < 2; ++nt2)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {  // B_h[a][j2 = l4][b' = 4 q .. 4 q + 3]: 16 contiguous bytes
+          const float4 v = *(const float4*)(Bg + ((16 * nt2 + l15) * 4 + l4) * 32 + 4 * q);
+          BTop[16 * nt2 + 4 * q + 0] = v.x;
+          BTop[16 * nt2 + 4 * q + 1] = v.y;
+          BTop[16 * nt2 + 4 * q + 2] = v.z;
+          BTop[16 * nt2 + 4 * q + 3] = v.w;
+        }
       cur_run = run;
     }
     if (qd == 0) {
@@ -248,18 +255,18 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bop[4 * s4 + nt], Cs[nt], 0, 0, 0);
       }
-      // lane holds C_h[slice l4][j1 r][j2 nt][b' l15]; scratch layout [slice][j1][j2][b']
+      // lane holds C_h[slice l4][j1 r][j2 nt][b' l15]: row 4 l4 + r, column 16 nt + l15
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) scr[scr_at(l4, r, nt * 16 + l15)] = Cs[nt][r];
+        for (int r = 0; r < 4; ++r) scr_c[SCR_PITCH * r + 16 * nt] = Cs[nt][r];
       wave_lds_sync();
     }
     // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4] and the dB A operand rows
     float CT[4], AT0, AT1;
     auto slice_begin = [&](int j) {
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[scr_at(j, s4, l4 * 16 + l15)];
+      for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[4 * SCR_PITCH * j + SCR_PITCH * s4 + lane];  // row 4 j + s4
       const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(c_i1, qd + j) * 128u + (uint32_t)(l4 * 32 + l15);
       AT0 = Aj[0];
       AT1 = Aj[16];
@@ -292,7 +299,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       }
       wave_lds_sync();
 #pragma unroll
-      for (int r = 0; r < 4; ++r) scr[scr_at(j, l4, r * 16 + l15)] = dC[r];
+      for (int r = 0; r < 4; ++r) scr_d[4 * SCR_PITCH * j + 16 * r] = dC[r];  // row 4 j + l4, column 16 r + l15
       dC = f32x4{0.f, 0.f, 0.f, 0.f};
     };
     // row pairs of the quad in order, three per iteration over three operand
@@ -327,18 +334,21 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       c = next_chunk();
       if (c >= 0) prefetch_quad();
     }
-    // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32)
+    // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32), the contraction over
+    // (j2, b') taken as (j2 = l4, b' = s) in step s, so that each lane reads 16
+    // contiguous floats of its stack row l15
     {
-      const int ms = l15 >> 2, mj1 = lane & 3;
-      const bool m_ok = ms < nqs;
+      const bool m_ok = (l15 >> 2) < nqs;
       f32x4 dA0 = {0.f, 0.f, 0.f, 0.f}, dA1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s2 = 0; s2 < 16; ++s2) {
-        const int k = 4 * s2 + l4;
-        const float v = scr[scr_at(ms, mj1, k)];
-        const float av = m_ok ? v : 0.f;
-        dA0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[2 * s2 + 0], dA0, 0, 0, 0);
-        dA1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[2 * s2 + 1], dA1, 0, 0, 0);
+      for (int q = 0; q < 4; ++q) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(scr_a + 4 * q);
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const float av = m_ok ? v[c4] : 0.f;
+          dA0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[4 * q + c4], dA0, 0, 0, 0);
+          dA1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[16 + 4 * q + c4], dA1, 0, 0, 0);
+        }
       }
       // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]
       if (l4 < nqs) {
@@ -468,7 +478,8 @@ __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __r
 
 bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
   // 32-bit float offsets into dE (rows x 128) and G3 must fit
-  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64 &&
+  // LDS: the n3 x 128 accumulator plus 8 x 16 x SCR_PITCH scratch floats fit 160 KB for n3 <= 252
+  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 252 && s.T <= 64 &&
          max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
 }
 

@@ -121,6 +121,8 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                            float* dG3, const Prof& prof, hipStream_t st);
 hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                       const float* dG3, float lr, hipStream_t st);
+// Whether the MFMA backward (and its partial-sum workspace) serves this shape.
+bool bwd_r32_supported(const Shape& s, int64_t max_indices);
 
 // Small generic kernels shared across units (defined in group.hip).
 hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);

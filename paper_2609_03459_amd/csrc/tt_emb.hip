@@ -80,8 +80,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->chunks = (int4*)take(16 * nch_max);
   W->E = (float*)take(4 * (size_t)m * s.D);
   W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
-  const bool bwd_r32 = s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 256 && s.T <= 64 &&
-                       m * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
+  const bool bwd_r32 = bwd_r32_supported(s, m);
   W->dApart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nsl_max * s.d1 * s.R : 0);
   W->dBpart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2) : 0);
   W->g3part = (float*)take(bwd_r32 ? 4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2) : 0);
