@@ -40,32 +40,20 @@ __device__ __forceinline__ int g3_unslot(int j3, int p) {  // slot p of column j
   return 4 * (((p >> 2) - (j3 >> 1)) & 3) + (p & 3);
 }
 
-// p[0..3] += v on LDS floats shared by the workgroup's waves.  A float ds_add is
-// slow on this LDS, integer compare-and-swap is not: read both 64-bit words,
-// add, swap, and retry only a word that changed in between (lock-free: a failed
-// swap means another wave's add landed, so the loop always progresses).
+// Adds to LDS floats shared by the workgroup's waves.  A float ds_add is slow on
+// this LDS, integer compare-and-swap is not: read two floats as a 64-bit word,
+// add, swap, and retry from the returned word if it changed in between
+// (lock-free: a failed swap means another wave's add landed).
 __device__ __forceinline__ uint64_t add2(uint64_t w, float a, float b) {
   const float lo = __uint_as_float((uint32_t)w) + a, hi = __uint_as_float((uint32_t)(w >> 32)) + b;
   return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
 }
-__device__ __forceinline__ bool lds_cas2(uint64_t* u, uint64_t& seen, float a, float b) {
-  return __hip_atomic_compare_exchange_strong(u, &seen, add2(seen, a, b), __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                              __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-// p[0..3] += v, given w: both words as read earlier (one 16-byte read) and n: the
-// words with v added.  A stale or torn word only fails its swap, which then retries
-// with the value the swap returned.
-__device__ __forceinline__ void lds_add4(float* p, const ulonglong2& w, uint64_t n0, uint64_t n1, f32x4 v) {
-  uint64_t* u = reinterpret_cast<uint64_t*>(p);
-  uint64_t g0 = w.x, g1 = w.y;
-  bool d0 = __hip_atomic_compare_exchange_strong(u, &g0, n0, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-  bool d1 = __hip_atomic_compare_exchange_strong(u + 1, &g1, n1, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-  while (!(d0 && d1)) {
-    if (!d0) d0 = lds_cas2(u, g0, v[0], v[1]);
-    if (!d1) d1 = lds_cas2(u + 1, g1, v[2], v[3]);
-  }
+// Compare-and-swap returning the old word only (equal to cmp exactly when the swap
+// took place), so that checking the result can wait until it is needed.
+__device__ __forceinline__ uint64_t lds_cas_old(uint64_t* u, uint64_t cmp, uint64_t val) {
+  __hip_atomic_compare_exchange_strong(u, &cmp, val, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+  return cmp;
 }
 
 template <typename T>
@@ -193,6 +181,29 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     qd = 0;
     return cc;
   };
+  // The LDS accumulate of the last row pair: its two swaps (expected words pa_e,
+  // returned old words pa_o, added values pa_v).  A swap took place when the old
+  // word equals the expected one; otherwise it is retried from the returned word.
+  // Checking at the next pair lets the round trip overlap that pair's products,
+  // and a retry before the next pair's swaps keeps every add.
+  uint64_t* pa_u = reinterpret_cast<uint64_t*>(g3acc);
+  uint64_t pa_e0 = 0, pa_e1 = 0, pa_o0 = 0, pa_o1 = 0;
+  f32x4 pa_v = {0.f, 0.f, 0.f, 0.f};
+  auto acc_finish = [&]() {
+    bool d0 = pa_o0 == pa_e0, d1 = pa_o1 == pa_e1;
+    while (!(d0 && d1)) {
+      if (!d0) {
+        pa_e0 = pa_o0;
+        pa_o0 = lds_cas_old(pa_u, pa_e0, add2(pa_e0, pa_v[0], pa_v[1]));
+        d0 = pa_o0 == pa_e0;
+      }
+      if (!d1) {
+        pa_e1 = pa_o1;
+        pa_o1 = lds_cas_old(pa_u + 1, pa_e1, add2(pa_e1, pa_v[2], pa_v[3]));
+        d1 = pa_o1 == pa_e1;
+      }
+    }
+  };
   // The next quad's operands are loaded before the current quad's dA product, so
   // that product and its stores cover their latency: its row-pair descriptors,
   // its stage-1 A operand (clamped rows, zeroed at use for missing slices) and
@@ -287,8 +298,15 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.w, X.d4.w, dC, 0, 0, 0);
       // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7]
       // every lane swaps (the zero row's column adds exact zeros), so the add is
-      // straight-line code and the read stays ahead of the products
-      lds_add4(ap, w, add2(w.x, dd[0], dd[1]), add2(w.y, dd[2], dd[3]), dd);
+      // straight-line code and the read stays ahead of the products; the previous
+      // pair's swaps are checked first, this pair's at the next pair
+      acc_finish();
+      pa_u = reinterpret_cast<uint64_t*>(ap);
+      pa_e0 = w.x;
+      pa_e1 = w.y;
+      pa_v = dd;
+      pa_o0 = lds_cas_old(pa_u, w.x, add2(w.x, dd[0], dd[1]));
+      pa_o1 = lds_cas_old(pa_u + 1, w.y, add2(w.y, dd[2], dd[3]));
     };
     // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
     auto slice_end = [&](int j) {
@@ -372,6 +390,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
           for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
     }
   }
+  acc_finish();
   __syncthreads();
   float* gdst = g3part + (size_t)blockIdx.x * acc_n;
   for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
