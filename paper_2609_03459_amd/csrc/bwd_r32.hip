@@ -345,13 +345,13 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     // the next quad: the rest of this chunk, or the first quad of the next chunk
     const int c_done = c;
     const bool chunk_end = qd + 4 >= ns;
-    if (!chunk_end) {
-      qd += 4;
-      prefetch_quad();
-    } else {
+    if (chunk_end)
       c = next_chunk();
-      if (c >= 0) prefetch_quad();
-    }
+    else
+      qd += 4;
+    // one call site, so the loads land in the registers the next quad reads (two
+    // inlined copies would need register copies, and so waits, where they merge)
+    if (c >= 0) prefetch_quad();
     // dA_h (16 x 32) = dCstack_h (16 x 64) . B_h^T (64 x 32), the contraction over
     // (j2, b') taken as (j2 = l4, b' = s) in step s, so that each lane reads 16
     // contiguous floats of its stack row l15
