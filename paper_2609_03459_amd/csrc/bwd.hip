@@ -17,17 +17,30 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
 // ---------------------------------------------------------------------------
 // dE segment sums over the sorted occurrences
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void seg_flush(int cur, int i0, int i1, int c, const int32_t* __restrict__ occ_start,
-                                          int D, int j0, const float* acc, float* __restrict__ dE,
+// Where chunk c's sum for row cur goes.  A row's occurrences are contiguous, so
+// only the chunk's first row can have begun before it (head partial) and only its
+// last row can go on after it (tail partial); k_seg_fix finishes those rows.
+struct SegEnds {
+  int u_first, u_last;
+  bool head_open, tail_open;
+};
+__device__ __forceinline__ SegEnds seg_ends(const int32_t* __restrict__ sorted_uid, int i0, int i1, int nvalid) {
+  SegEnds e;
+  e.u_first = sorted_uid[i0];
+  e.u_last = sorted_uid[i1 - 1];
+  e.head_open = i0 > 0 && sorted_uid[i0 - 1] == e.u_first;
+  e.tail_open = i1 < nvalid && sorted_uid[i1] == e.u_last;
+  return e;
+}
+__device__ __forceinline__ float* seg_dst(const SegEnds& e, int cur, int c, int D, float* __restrict__ dE,
                                           float* __restrict__ part) {
-  const int lo = occ_start[cur], hi = occ_start[cur + 1];
-  float* dst;
-  if (lo >= i0 && hi <= i1)
-    dst = dE + (int64_t)cur * D;
-  else if (lo < i0)
-    dst = part + ((int64_t)c * 2 + 0) * D;
-  else
-    dst = part + ((int64_t)c * 2 + 1) * D;
+  if (e.head_open && cur == e.u_first) return part + ((int64_t)c * 2 + 0) * D;
+  if (e.tail_open && cur == e.u_last) return part + ((int64_t)c * 2 + 1) * D;
+  return dE + (int64_t)cur * D;
+}
+__device__ __forceinline__ void seg_flush(const SegEnds& e, int cur, int c, int D, int j0, const float* acc,
+                                          float* __restrict__ dE, float* __restrict__ part) {
+  float* dst = seg_dst(e, cur, c, D, dE, part);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int j = j0 + k * 64 + lane_id();
@@ -38,18 +51,22 @@ __device__ __forceinline__ void seg_flush(int cur, int i0, int i1, int c, const 
 // One wave per chunk of SEG_CHUNK sorted occurrences; lanes hold 4 columns
 // each (column blocks of 256); occurrence indices are fetched 64 at a time and
 // the grad_out rows of 8 occurrences are loaded before they are summed.
-__global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+// Four waves per workgroup (one-wave workgroups would cap the waves a CU holds),
+// each wave one chunk.
+constexpr int SEG_WAVES = 4;
+
+__global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                const uint32_t* __restrict__ sorted_pos,
                                                const int32_t* __restrict__ bag_of,
-                                               const int32_t* __restrict__ occ_start,
                                                const int32_t* __restrict__ ctr, int D, float* __restrict__ dE,
                                                float* __restrict__ part) {
   const int nvalid = ctr[C_NVALID];
-  const int c = blockIdx.x;
+  const int c = blockIdx.x * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
   if (i0 >= nvalid) return;
   const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
+  const SegEnds ends = seg_ends(sorted_uid, i0, i1, nvalid);
   for (int j0 = 0; j0 < D; j0 += 256) {
     bool colok[4];
 #pragma unroll
@@ -77,7 +94,7 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
         for (int kk = 0; kk < 8; ++kk) {
           if (k0 + kk < cnt) {
             if (uk[kk] != cur) {
-              seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
+              seg_flush(ends, cur, c, D, j0, acc, dE, part);
               cur = uk[kk];
               acc[0] = acc[1] = acc[2] = acc[3] = 0.f;
             }
@@ -87,37 +104,29 @@ __global__ void __launch_bounds__(64) k_seg_dE(const float* __restrict__ dV, con
         }
       }
     }
-    seg_flush(cur, i0, i1, c, occ_start, D, j0, acc, dE, part);
+    seg_flush(ends, cur, c, D, j0, acc, dE, part);
   }
 }
 
 // D = 128: a lane owns two columns (one 8-byte load per occurrence), the bag
 // index of each occurrence is read into a scalar register so every dV row is a
 // uniform base, and 16 rows are in flight before they are summed in order.
-__global__ void __launch_bounds__(64) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+__global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                   const uint32_t* __restrict__ sorted_pos,
                                                   const int32_t* __restrict__ bag_of,
-                                                  const int32_t* __restrict__ occ_start,
                                                   const int32_t* __restrict__ ctr, float* __restrict__ dE,
                                                   float* __restrict__ part) {
   const int nvalid = ctr[C_NVALID];
-  const int c = blockIdx.x;
+  const int c = blockIdx.x * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
   if (i0 >= nvalid) return;
   const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
+  const SegEnds ends = seg_ends(sorted_uid, i0, i1, nvalid);
   auto flush = [&](int u, float2 acc) {
-    const int lo = occ_start[u], hi = occ_start[u + 1];
-    float* dst;
-    if (lo >= i0 && hi <= i1)
-      dst = dE + (size_t)u * 128;
-    else if (lo < i0)
-      dst = part + ((size_t)c * 2 + 0) * 128;
-    else
-      dst = part + ((size_t)c * 2 + 1) * 128;
-    reinterpret_cast<float2*>(dst)[lane] = acc;
+    reinterpret_cast<float2*>(seg_dst(ends, u, c, 128, dE, part))[lane] = acc;
   };
-  int cur = sorted_uid[i0];
+  int cur = ends.u_first;
   float2 acc = make_float2(0.f, 0.f);
   for (int base = i0; base < i1; base += 64) {
     const int i = base + lane;
@@ -314,12 +323,12 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
   prof_begin(prof, K_SEG_SUM, st);
   if (s.D == 128)
-    hipLaunchKernelGGL(k_seg_dE128, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
-                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+    hipLaunchKernelGGL(k_seg_dE128, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
+                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
                        (const int32_t*)w.ctr, dE, w.seg_part);
   else
-    hipLaunchKernelGGL(k_seg_dE, dim3(nseg), dim3(64), 0, st, dV, (const int32_t*)w.sorted_uid,
-                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+    hipLaunchKernelGGL(k_seg_dE, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
+                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
                        (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   prof_end(prof, K_SEG_SUM, st);
   hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
