@@ -56,10 +56,6 @@ __device__ __forceinline__ uint64_t lds_cas_old(uint64_t* u, uint64_t cmp, uint6
   return cmp;
 }
 
-template <typename T>
-__device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
-  return j == 0 ? a : (j == 1 ? b : (j == 2 ? c : d));
-}
 
 // operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs
 // with a row of zeros, which its buffer loads return past the end of the pair)

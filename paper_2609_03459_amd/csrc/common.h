@@ -247,10 +247,17 @@ hipError_t launch_debug_digits(const Shape& s, const Work& w, int32_t* out, int 
 namespace ttemb {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Orders this wave's LDS writes before its later LDS reads of other lanes'
 // data (a wave's LDS requests complete in order; this keeps the compiler
 // from reordering across the exchange and waits for outstanding writes).
+// one of four wave-uniform values by a per-lane index
+template <typename T>
+__device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
+  return j == 0 ? a : (j == 1 ? b : (j == 2 ? c : d));
+}
+
 // Raw buffer loads through a gfx9 buffer descriptor (stride 0, dword data):
 // the address is base + offset (+ a wave-uniform offset), and a load at or past
 // num_bytes returns zero instead of touching memory.

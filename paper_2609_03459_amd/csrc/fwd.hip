@@ -121,45 +121,104 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   const int orow = l4 >> 1;  // E row of the pair this lane's output belongs to
   // stage-2 A operand: lane m = l15 = (row sel, j3), K index b = 4 s + l4
   const int asel = l15 >> 3;
-  const uint32_t o_d = (uint32_t)(l4 * 8 + (l15 & 7));
-  const uint32_t o_e = (uint32_t)(l15 * 8 + 4 * (l4 & 1));  // E store offset inside a row
+  // byte offsets: this lane's stage-2 A word in a G3 row (b = l4, j3 = l15 & 7; + 128 bytes
+  // per K step) and its E store (row orow of the pair, four floats)
+  const uint32_t vo_d = 4u * (uint32_t)(l4 * 8 + (l15 & 7));
+  const uint32_t vo_e = 4u * (uint32_t)(orow * 128 + l15 * 8 + 4 * (l4 & 1));
 
   int cursor = 0;
   int cur_run = -1;
   float Bop[64];  // B[a = 4 s + l4][16 nt + l15], (s, nt) -> 8 s + nt
-  int q_rb = 0, q_nr = 0, i3A = 0, i3B = 0;
-  int cp1 = 0, cp2 = 0, cp3 = 0, np = 0;
-  int tcur = 0;
-  const float* G3t = G3;
+
+  // slice descriptors of the current chunk, lane j holding slice f + j (j < ns;
+  // other lanes have no rows): first row, row count, i1
+  int c_rb = 0, c_nr = 0, c_i1 = 0;
+  int f = 0, ns = 0, run = -1, t = 0, qd = 0;
+  int c = -1;
+  auto next_chunk = [&]() {
+    c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
+    qd = 0;
+    if (c >= 0) {
+      const int4 ch = chunks[c];
+      f = __builtin_amdgcn_readfirstlane(ch.x);
+      ns = __builtin_amdgcn_readfirstlane(ch.y);
+      run = __builtin_amdgcn_readfirstlane(ch.z);
+      t = run / s.n2;
+      const int sl = f + (lane < ns ? lane : 0);
+      const int4 sd = slices[sl];
+      c_rb = sd.y;
+      c_nr = lane < ns ? sd.z - sd.y : 0;
+      c_i1 = slice_i1[sl];
+    }
+  };
+
+  // Row-pair descriptors, lane P holding pair P of a quad (slice j owns
+  // (nr_j + 1) / 2 consecutive pairs): first row | j << 28 | (second row real) << 30,
+  // and i3 of both rows.  Built for the next quad while the current one runs (e_*),
+  // then made current (d_*).
+  int d_ra = 0, d_ia = 0, d_ib = 0, np = 0;
+  int e_ra = 0, e_ia = 0, e_ib = 0, e_np = 0;
+  auto build_desc = [&]() {
+    const int n0 = __builtin_amdgcn_readlane(c_nr, qd), n1 = __builtin_amdgcn_readlane(c_nr, qd + 1);
+    const int n2 = __builtin_amdgcn_readlane(c_nr, qd + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd + 3);
+    const int b0 = __builtin_amdgcn_readlane(c_rb, qd), b1 = __builtin_amdgcn_readlane(c_rb, qd + 1);
+    const int b2 = __builtin_amdgcn_readlane(c_rb, qd + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd + 3);
+    const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
+    e_np = q3 + ((n3 + 1) >> 1);
+    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
+    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
+    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    const bool ok = lane < e_np;
+    const bool has1 = ok && pr + 1 < nr;
+    const int ra = ok ? rb + pr : b0;  // lanes past the quad's pairs keep a valid row
+    e_ia = uniq_i3[ra];
+    e_ib = uniq_i3[has1 ? ra + 1 : ra];
+    e_ra = ra | (j << 28) | (has1 ? 1 << 30 : 0);
+  };
+  // stage-1 A operand of the quad at qd: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
+  // (missing slices repeat the first; their rows are never read)
+  float Aop[8];
+  auto load_A = [&]() {
+    const int nq4 = ns - qd < 4 ? ns - qd : 4;
+    const int aj = l15 >> 2;
+    const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
+    const int i1c = __builtin_amdgcn_readlane(c_i1, qd + 2), i1d = __builtin_amdgcn_readlane(c_i1, qd + 3);
+    const float* Ag = G1 + (uint32_t)(t * s.n1 + sel4(aj < nq4 ? aj : 0, i1a, i1b, i1c, i1d)) * 128u +
+                      (uint32_t)((lane & 3) * 32 + l4);
+#pragma unroll
+    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
+  };
 
   struct FPair {
     float d[8];
-    int eoff;   // float offset of this lane's E store
-    bool live;  // this lane's output row exists
+    int ra;     // first row of the pair (wave-uniform)
+    int j;      // slice within the quad (wave-uniform)
+    bool has1;  // the second row is real (wave-uniform)
   };
+  buf_t g3buf = make_buf(G3, 0);  // G3[t] of the current quad
   auto pair_load = [&](FPair& X, int P) {
-    const int pj = (P >= cp1) + (P >= cp2) + (P >= cp3);
-    const int pr = 2 * (P - (pj == 0 ? 0 : (pj == 1 ? cp1 : (pj == 2 ? cp2 : cp3))));
-    const int rb = __builtin_amdgcn_readlane(q_rb, pj), nr = __builtin_amdgcn_readlane(q_nr, pj);
-    const bool has1 = pr + 1 < nr;
-    const int i3v = pj < 2 ? i3A : i3B;
-    const int li = (pj & 1) * 32 + pr;
-    const int i3a = __builtin_amdgcn_readlane(i3v, li);
-    const int i3b = __builtin_amdgcn_readlane(i3v, has1 ? li + 1 : li);
-    const float* Dg = G3t + (uint32_t)(asel ? i3b : i3a) * 256u + o_d;
+    const int rw = __builtin_amdgcn_readlane(d_ra, P);
+    const int ia = __builtin_amdgcn_readlane(d_ia, P), ib = __builtin_amdgcn_readlane(d_ib, P);
+    X.ra = rw & 0x0FFFFFFF;
+    X.j = (rw >> 28) & 3;
+    X.has1 = (rw >> 30) & 1;
+    const uint32_t o = vo_d + (uint32_t)(asel ? ib : ia) * 1024u;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) X.d[k] = Dg[32 * k];
-    X.eoff = (rb + pr + orow) * 128 + (int)o_e;
-    X.live = has1 || orow == 0;
+    for (int k = 0; k < 8; ++k) X.d[k] = buf_f32(g3buf, o, 128u * k);
   };
 
-  int c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
-  int f = 0, ns = 0, run = -1, qd = 0;
+  FPair XA, XB;
+  next_chunk();
   if (c >= 0) {
-    const int4 ch = chunks[c];
-    f = __builtin_amdgcn_readfirstlane(ch.x);
-    ns = __builtin_amdgcn_readfirstlane(ch.y);
-    run = __builtin_amdgcn_readfirstlane(ch.z);
+    build_desc();
+    load_A();
+    d_ra = e_ra;
+    d_ia = e_ia;
+    d_ib = e_ib;
+    np = e_np;
+    g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+    pair_load(XA, 0);
+    pair_load(XB, np > 1 ? 1 : 0);
   }
   while (c >= 0) {
     if (run != cur_run) {
@@ -169,42 +228,8 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
 #pragma unroll
         for (int nt = 0; nt < 8; ++nt) Bop[8 * s4 + nt] = Bg[s4 * 512 + 16 * nt];
       cur_run = run;
-      tcur = run / s.n2;
-      G3t = G3 + (uint32_t)(tcur * s.n3) * 256u;
     }
-    const int nqs = ns - qd < 4 ? ns - qd : 4;
-    const int sb = f + qd;
-    {
-      const int sl = sb + (lane < nqs ? lane : 0);
-      const int4 sd = slices[sl];
-      q_rb = sd.y;
-      q_nr = lane < nqs ? sd.z - sd.y : 0;
-    }
-    {
-      const int ja = lane >> 5, k = lane & 31;
-      const int rba = __builtin_amdgcn_readlane(q_rb, 0), rbb = __builtin_amdgcn_readlane(q_rb, 1);
-      const int rbc = __builtin_amdgcn_readlane(q_rb, 2), rbd = __builtin_amdgcn_readlane(q_rb, 3);
-      const int nra = __builtin_amdgcn_readlane(q_nr, 0), nrb = __builtin_amdgcn_readlane(q_nr, 1);
-      const int nrc = __builtin_amdgcn_readlane(q_nr, 2), nrd = __builtin_amdgcn_readlane(q_nr, 3);
-      const int rA = ja ? rbb : rba, nA = ja ? nrb : nra;
-      const int rB = ja ? rbd : rbc, nB = ja ? nrd : nrc;
-      i3A = uniq_i3[rA + (k < nA ? k : 0)];
-      i3B = uniq_i3[rB + (k < nB ? k : 0)];
-      cp1 = (nra + 1) >> 1;
-      cp2 = cp1 + ((nrb + 1) >> 1);
-      cp3 = cp2 + ((nrc + 1) >> 1);
-      np = cp3 + ((nrd + 1) >> 1);
-    }
-    // stage-1 A operand: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
-    const int aj = l15 >> 2;
-    const float* Ag = G1 + (uint32_t)(tcur * s.n1 + slice_i1[sb + (aj < nqs ? aj : 0)]) * 128u +
-                      (uint32_t)((lane & 3) * 32 + l4);
-    float Aop[8];
-#pragma unroll
-    for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
-    FPair XA, XB;
-    pair_load(XA, 0);
-    // stage 1 (rows of slices beyond nqs are computed from a repeated slice and never read)
+    // stage 1 (rows of slices beyond the chunk's end come from a repeated slice and are never read)
     {
       f32x4 Cs[8];
 #pragma unroll
@@ -221,6 +246,16 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
         for (int r = 0; r < 4; ++r) scr[fscr_at(l4, r, nt >> 1, 16 * (nt & 1) + l15)] = Cs[nt][r];
       wave_lds_sync();
     }
+    // the next quad (the rest of this chunk, or a new chunk claimed now): its
+    // descriptors and stage-1 A operand load while this quad's rows are computed
+    if (qd + 4 >= ns)
+      next_chunk();
+    else
+      qd += 4;
+    if (c >= 0) {
+      build_desc();
+      load_A();
+    }
     // stage-2 B operand of slice j: C'^T[b = 4 s + l4][jj = l15]
     float CT[8];
     auto slice_begin = [&](int j) {
@@ -228,45 +263,40 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr[fscr_at(j, l15 >> 2, l15 & 3, 4 * s4 + l4)];
     };
     slice_begin(0);
+    // E rows of a pair through a descriptor that ends after the pair's real rows, so
+    // the missing second row of a lone last row is not written
     auto pair_compute = [&](const FPair& X) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[s4], CT[s4], acc, 0, 0, 0);
       // lane holds E[row orow][jj = l15][j3 = 4 (l4 & 1) + r]
-      if (X.live) *reinterpret_cast<float4*>(E + (uint32_t)X.eoff) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * 128, X.has1 ? 1024u : 512u);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
     };
     int cj = 0;
+    auto step = [&](const FPair& X) {
+      if (X.j != cj) {
+        slice_begin(X.j);
+        cj = X.j;
+      }
+      pair_compute(X);
+    };
     for (int P = 0; P < np; P += 2) {
       pair_load(XB, P + 1 < np ? P + 1 : np - 1);
-      {
-        const int j = (P >= cp1) + (P >= cp2) + (P >= cp3);
-        if (j != cj) {
-          slice_begin(j);
-          cj = j;
-        }
-        pair_compute(XA);
-      }
+      step(XA);
       pair_load(XA, P + 2 < np ? P + 2 : np - 1);
-      if (P + 1 < np) {
-        const int j = (P + 1 >= cp1) + (P + 1 >= cp2) + (P + 1 >= cp3);
-        if (j != cj) {
-          slice_begin(j);
-          cj = j;
-        }
-        pair_compute(XB);
-      }
+      if (P + 1 < np) step(XB);
     }
     wave_lds_sync();
-    qd += 4;
-    if (qd >= ns) {
-      c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
-      qd = 0;
-      if (c >= 0) {
-        const int4 ch = chunks[c];
-        f = __builtin_amdgcn_readfirstlane(ch.x);
-        ns = __builtin_amdgcn_readfirstlane(ch.y);
-        run = __builtin_amdgcn_readfirstlane(ch.z);
-      }
+    // the next quad becomes current; its first two row pairs load during its stage 1
+    if (c >= 0) {
+      d_ra = e_ra;
+      d_ia = e_ia;
+      d_ib = e_ib;
+      np = e_np;
+      g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+      pair_load(XA, 0);
+      pair_load(XB, np > 1 ? 1 : 0);
     }
   }
 }
