@@ -139,7 +139,9 @@ def write_traffic(pmc_dir, copy_mib=1024, kernel="bwd_fused"):
 
 def cpu_baseline(case, target_s):
     """The oracle (plain fp64 C, one thread) on a bounded sample of the same workload:
-    a seeded subset of bags of every table, forward then backward."""
+    a seeded subset of bags of every table, forward then backward.  Returns the
+    one-thread figure and the same sample with the tables (independent) run on a
+    thread pool, one single-table oracle call per table."""
     import numpy as np
 
     import oracle
@@ -169,6 +171,13 @@ def cpu_baseline(case, target_s):
         oracle.backward(c)
         return time.perf_counter() - t0
 
+    def table(c, t):  # table t of a sample as a one-table case
+        nb = c["B"]
+        o = c["offsets"]
+        lo, hi = o[t * nb], o[(t + 1) * nb]
+        return dict(c, T=1, G1=c["G1"][t:t + 1], G2=c["G2"][t:t + 1], G3=c["G3"][t:t + 1],
+                    idx=c["idx"][lo:hi], offsets=o[t * nb:(t + 1) * nb + 1] - lo, dV=c["dV"][t:t + 1])
+
     probe = sub(8)
     dt = run(probe)
     rate = probe["idx"].size / max(dt, 1e-6)
@@ -176,16 +185,27 @@ def cpu_baseline(case, target_s):
     s = sub(nb)
     dt = run(s)
     lookups = int(s["idx"].size)
-    return dict(value=lookups / dt, unit="lookups/s", cores=1, kind="oracle",
-                sample=f"{nb} seeded bags per table x {T} tables ({lookups} lookups), forward + backward, "
-                       f"fp64 C oracle, 1 thread, {dt:.1f} s")
+    one = dict(value=lookups / dt, unit="lookups/s", cores=1, kind="oracle",
+               sample=f"{nb} seeded bags per table x {T} tables ({lookups} lookups), forward + backward, "
+                      f"fp64 C oracle, 1 thread, {dt:.1f} s")
+    from concurrent.futures import ThreadPoolExecutor
+    nthr = max(1, min(T, os.cpu_count() or 1, 16))
+    parts = [table(s, t) for t in range(T)]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(nthr) as ex:
+        list(ex.map(run, parts))
+    dtm = time.perf_counter() - t0
+    many = dict(value=lookups / dtm, unit="lookups/s", cores=nthr, kind="oracle",
+                sample=f"the same sample, {T} tables on {nthr} threads (one single-table oracle call each), "
+                       f"{dtm:.1f} s")
+    return one, many
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=6)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=5, help="workload recipe (5 = training step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--reuse", choices=["prefix", "unique", "none"], default="prefix",
@@ -259,19 +279,38 @@ def main():
     counts = emb.counts()
     dominant = max(kernel_ms, key=kernel_ms.get)
 
-    # timed region: K steps; the dominant kernel is bracketed by events in every step
+    # timed region: K steps; the dominant kernel is bracketed by events in every
+    # step, and every step by events on the stream (for the per-step median)
     K = args.steps
     evs = [(ev.create(), ev.create()) for _ in range(K)]
+    sev = [ev.create() for _ in range(K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
+        ev.record(sev[i], stream)
         P.N.tt_emb_profile(emb.handle, P.N.KERNELS[dominant], evs[i][0], evs[i][1])
         step()
+    ev.record(sev[K], stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     P.N.tt_emb_profile(emb.handle, 0, None, None)
     ms_per_step = (t1 - t0) * 1e3 / K
     dom_ms = float(np.mean([ev.elapsed_ms(a, b) for a, b in evs]))
+    step_med = float(np.median([ev.elapsed_ms(sev[i], sev[i + 1]) for i in range(K)]))
+
+    # measured copy bandwidth: one elementwise kernel reading and writing 1 GiB each
+    x = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    cps = []
+    ce0, ce1 = ev.create(), ev.create()
+    for _ in range(4):
+        ev.record(ce0, stream)
+        torch.mul(x, 2.0, out=y)
+        ev.record(ce1, stream)
+        torch.cuda.synchronize()
+        cps.append(ev.elapsed_ms(ce0, ce1))
+    copy_gbps = 2.0 * x.numel() * 4 / (float(np.median(cps[1:])) * 1e-3) / 1e9
+    del x, y
 
     # phase split (grouping / forward / backward / sgd), as in the paper's breakdown
     phases = {"group": [], "forward": [], "backward": [], "sgd": []}
@@ -328,12 +367,14 @@ def main():
                    "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu",
                    "reuse": args.reuse},
         "roofline": roof,
+        "step_ms_median": round(step_med, 4),
+        "copy_gbps_measured": round(copy_gbps, 1),
         "phases_ms": phases_ms,
         "kernel_ms_warmup": {k: round(v, 4) for k, v in kernel_ms.items()},
         "grouping": {"unique_rows": counts["U"], "prefix_groups": counts["P"], "slices": counts["nslices"]},
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+        res["cpu_baseline"], res["cpu_baseline_threads"] = cpu_baseline(case, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 

@@ -28,9 +28,9 @@
  * Ownership.  The caller owns every device buffer (cores, indices, offsets,
  * outputs, gradients, workspace).  The handle holds host-side metadata only;
  * creating it touches no device.  tt_emb_group, tt_emb_forward,
- * tt_emb_backward and tt_emb_sgd enqueue kernels on `stream` (a hipStream_t;
- * NULL = the default stream) and return without synchronising; they allocate
- * and free nothing.  One handle and one workspace serve one stream at a time.
+ * tt_emb_backward, tt_emb_backward_sgd and tt_emb_sgd enqueue kernels on
+ * `stream` (a hipStream_t; NULL = the default stream) and return without
+ * synchronising; they allocate and free nothing.  One handle and one workspace serve one stream at a time.
  * Device pointers to float data must be 16-byte aligned, to int64 data
  * 8-byte aligned, and the workspace 256-byte aligned.
  *
@@ -141,6 +141,24 @@ tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2,
  * momentum, no weight decay).  Enqueued on `stream` after the gradients. */
 tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                          const float* dG3, float lr, void* stream);
+
+/* Backward pass and plain SGD in one call: the weight update fused into the
+ * backward (an optimisation Section 3.2 describes and leaves out of its
+ * final text: each core slice's gradient is aggregated once and applied
+ * directly, with no separate optimizer pass).  Leaves every core at
+ * G_k - lr * dG_k, with dG_k exactly the gradient tt_emb_backward would
+ * return for the same arguments, and writes no gradient arrays.  The update
+ * happens after the whole reduction (the kernels that read the cores have
+ * finished; rows no index touches are unchanged).  G1..G3 are read and then
+ * updated in place; indices, offsets, grad_out, reuse_grouping, workspace
+ * and errors as for tt_emb_backward.  On the shapes the MFMA kernels serve
+ * the update is applied inside the final gradient reductions; otherwise the
+ * gradients go to a core-sized region of the workspace first (included in
+ * tt_emb_workspace_size for those shapes). */
+tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const int64_t* indices,
+                                  int64_t num_indices, const int64_t* offsets, int64_t num_bags,
+                                  const float* grad_out, float lr, int reuse_grouping, void* workspace,
+                                  size_t ws_bytes, void* stream);
 
 /* Synchronise `stream`, read and clear the sticky device error word of
  * `workspace`.  Returns TT_EMB_OK, TT_EMB_ERANGE or TT_EMB_EHIP. */

@@ -12,7 +12,7 @@ import torch
 
 from . import _native as N
 
-__all__ = ["TTEmbedding", "N"]
+__all__ = ["TTEmbedding", "TTEmbeddingBag", "tt_embedding_bag", "N"]
 
 
 def _ptr(t):
@@ -102,6 +102,12 @@ class TTEmbedding:
     def sgd(self, G1, G2, G3, dG1, dG2, dG3, lr):
         N.tt_emb_sgd(self.handle, _ptr(G1), _ptr(G2), _ptr(G3), _ptr(dG1), _ptr(dG2), _ptr(dG3), lr, _stream())
 
+    def backward_sgd(self, G1, G2, G3, idx, offsets, grad_out, lr, num_bags=None, reuse_grouping=True):
+        """Backward pass with the SGD step fused in: G_k -= lr * dG_k in place, no gradient arrays."""
+        nb = self._nb(idx, offsets, num_bags)
+        N.tt_emb_backward_sgd(self.handle, _ptr(G1), _ptr(G2), _ptr(G3), _ptr(idx), idx.numel(), _ptr(offsets), nb,
+                              _ptr(grad_out), lr, reuse_grouping, _ptr(self.workspace), self.ws_bytes, _stream())
+
     def check_errors(self) -> int:
         return N.tt_emb_check_errors(self.handle, _ptr(self.workspace), _stream())
 
@@ -137,3 +143,64 @@ class TTEmbedding:
         del C
         return dict(uniq_keys=uk[:U], digits=dg[:U], inv=inv[:num_indices], occ_start=os_, occ_pos=op[:nv],
                     pg_start=ps, pg_keys=pk[:P], U=U, P=P, nvalid=nv, nslices=ns)
+
+
+class _TTEmbeddingBagFn(torch.autograd.Function):
+    """Autograd node of the pooled TT gather: forward groups the indices and runs the
+    fused forward; backward reuses that grouping (regrouping if another call on the
+    same handle replaced it) and returns the three dense core gradients."""
+
+    @staticmethod
+    def forward(ctx, G1, G2, G3, emb, idx, offsets, num_bags):
+        out = emb.forward(G1, G2, G3, idx, offsets, num_bags=num_bags)
+        ctx.emb, ctx.idx, ctx.offsets, ctx.num_bags = emb, idx, offsets, num_bags
+        ctx.save_for_backward(G1, G2, G3)
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        G1, G2, G3 = ctx.saved_tensors
+        emb = ctx.emb
+        g = grad_out.contiguous().to(torch.float32)
+        try:
+            grads = emb.backward(G1, G2, G3, ctx.idx, ctx.offsets, g, num_bags=ctx.num_bags, reuse_grouping=True)
+        except N.TTEmbError as e:
+            if e.code != N.TT_EMB_EINVAL:
+                raise
+            grads = emb.backward(G1, G2, G3, ctx.idx, ctx.offsets, g, num_bags=ctx.num_bags, reuse_grouping=False)
+        return grads[0], grads[1], grads[2], None, None, None, None
+
+
+def tt_embedding_bag(G1, G2, G3, emb, idx, offsets=None, num_bags=None):
+    """Differentiable pooled lookup: out [T][B][D], gradients flow to G1, G2, G3."""
+    return _TTEmbeddingBagFn.apply(G1, G2, G3, emb, idx, offsets, emb._nb(idx, offsets, num_bags))
+
+
+class TTEmbeddingBag(torch.nn.Module):
+    """T sum-pooled embedding tables of one TT shape, the cores as parameters.
+
+    forward(idx, offsets) returns [T][B][D]; loss.backward() fills G1/G2/G3.grad.
+    step_fused(idx, offsets, grad_out, lr) is the training step without autograd:
+    backward and SGD in one library call (no gradient tensors).
+    """
+
+    def __init__(self, num_tables, num_rows, row_factors, dim_factors, rank, max_indices, max_bags, init_std=0.05,
+                 reuse="prefix", device="cuda", generator=None):
+        super().__init__()
+        self.emb = TTEmbedding(num_tables, num_rows, row_factors, dim_factors, rank, max_indices, max_bags,
+                               device=device, reuse=reuse)
+        s1, s2, s3 = self.emb.core_shapes()
+
+        def init(shape):
+            return torch.nn.Parameter(
+                (torch.randn(shape, generator=generator, dtype=torch.float32) * init_std).to(device))
+
+        self.G1, self.G2, self.G3 = init(s1), init(s2), init(s3)
+
+    def forward(self, idx, offsets=None, num_bags=None):
+        return tt_embedding_bag(self.G1, self.G2, self.G3, self.emb, idx, offsets, num_bags)
+
+    @torch.no_grad()
+    def step_fused(self, idx, offsets, grad_out, lr, num_bags=None, reuse_grouping=True):
+        self.emb.backward_sgd(self.G1.data, self.G2.data, self.G3.data, idx, offsets, grad_out.contiguous(), lr,
+                              num_bags=num_bags, reuse_grouping=reuse_grouping)

@@ -47,6 +47,8 @@ _SIG = {
     "tt_emb_backward": ([_P, _P, _P, _P, _P, _I64, _P, _I64, _P, _P, _P, _P, C.c_int, _P, C.c_size_t, _P],
                         C.c_int),
     "tt_emb_sgd": ([_P, _P, _P, _P, _P, _P, _P, C.c_float, _P], C.c_int),
+    "tt_emb_backward_sgd": ([_P, _P, _P, _P, _P, _I64, _P, _I64, _P, C.c_float, C.c_int, _P, C.c_size_t, _P],
+                            C.c_int),
     "tt_emb_check_errors": ([_P, _P, _P], C.c_int),
     "tt_emb_debug_grouping": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "tt_emb_status_string": ([C.c_int], C.c_char_p),
@@ -112,6 +114,11 @@ def tt_emb_backward(h, g1, g2, g3, idx, m, off, nb, dv, dg1, dg2, dg3, reuse, ws
 
 def tt_emb_sgd(h, g1, g2, g3, dg1, dg2, dg3, lr, stream) -> None:
     check("tt_emb_sgd", lib.tt_emb_sgd(h, g1, g2, g3, dg1, dg2, dg3, float(lr), stream))
+
+
+def tt_emb_backward_sgd(h, g1, g2, g3, idx, m, off, nb, dv, lr, reuse, ws, wsb, stream) -> None:
+    check("tt_emb_backward_sgd",
+          lib.tt_emb_backward_sgd(h, g1, g2, g3, idx, m, off, nb, dv, float(lr), int(reuse), ws, wsb, stream))
 
 
 def tt_emb_check_errors(h, ws, stream) -> int:

@@ -12,7 +12,8 @@ namespace ttemb {
 
 ShapeArgs shape_args(const Shape& s);
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
-                          float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st);
+                          float* dG1, float* dG2, float* dG3, float lr, bool update, const Prof& prof,
+                          hipStream_t st);
 
 // ---------------------------------------------------------------------------
 // dE segment sums over the sorted occurrences
@@ -305,7 +306,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
 
 hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                            const int64_t* offsets, int64_t M, int64_t B, const float* dV, float* dG1, float* dG2,
-                           float* dG3, const Prof& prof, hipStream_t st) {
+                           float* dG3, float lr, bool update, const Prof& prof, hipStream_t st) {
   (void)offsets;
   (void)B;
   const int64_t n1s = (int64_t)s.T * s.n1 * s.d1 * s.R;
@@ -313,6 +314,21 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
   hipError_t e;
   const bool fast = bwd_r32_supported(s, w.M);
+  // fused update: the MFMA path applies it in its reductions (dG1..dG3 are the
+  // cores); the generic path sums into the workspace's gradient scratch and then
+  // runs the update
+  float* G1u = dG1;
+  float* G2u = dG2;
+  float* G3u = dG3;
+  if (update) {
+    if (M <= 0) return hipSuccess;  // zero gradients: the update leaves the cores as they are
+    if (!fast) {
+      if (!w.gscratch) return hipErrorInvalidValue;
+      dG1 = w.gscratch;
+      dG2 = dG1 + n1s;
+      dG3 = dG2 + n2s;
+    }
+  }
   if (!fast || M <= 0) {
     if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
     if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
@@ -333,7 +349,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   prof_end(prof, K_SEG_SUM, st);
   hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
-  if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, prof, st);
+  if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, lr, update, prof, st);
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
     return e;
@@ -345,7 +361,9 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
                      (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3);
   prof_end(prof, K_BWD_FUSED, st);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);
+  return hipSuccess;
 }
 
 // ---------------------------------------------------------------------------

@@ -392,6 +392,13 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
 }
 
+// Each reduction writes its sum into `out` (the gradient), or with lr given,
+// subtracts lr times the sum from `out` (the core itself: the update of the fused
+// backward-and-SGD call).  Every element of its core is visited exactly once.
+__device__ __forceinline__ void put_grad(float* out, int64_t i, float acc, float lr, bool update) {
+  out[i] = update ? out[i] - lr * acc : acc;
+}
+
 // dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2).
 // The block lists the slices of (t, i1) in i2 order (512 prefixes per round,
 // the list G1_LIST entries at a time), and four groups of 128 threads take
@@ -402,7 +409,7 @@ constexpr int G1_LIST = 4096;
 __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                    const uint32_t* __restrict__ dense_base,
                                                    const float* __restrict__ dApart, int nsl_cap,
-                                                   float* __restrict__ dG1) {
+                                                   float* __restrict__ dG1, float lr, bool update) {
   __shared__ int list[G1_LIST];
   __shared__ uint32_t wsum[8];
   __shared__ float red[4][128];
@@ -452,13 +459,13 @@ __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* 
   }
   red[g][e] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   __syncthreads();
-  if (g == 0) dG1[(int64_t)ti1 * 128 + e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+  if (g == 0) put_grad(dG1, (int64_t)ti1 * 128 + e, ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e], lr, update);
 }
 
 // dG2[t][i2][a][j2][16 h + b'] = sum of the chunk partials of run (t, i2), half h
 __global__ void __launch_bounds__(256) k_reduce_g2(const uint32_t* __restrict__ run_base,
                                                    const float* __restrict__ dBpart, int nch_cap,
-                                                   float* __restrict__ dG2) {
+                                                   float* __restrict__ dG2, float lr, bool update) {
   const int run = blockIdx.x >> 1, h = blockIdx.x & 1;
   const int c0 = (int)run_base[run], c1 = (int)run_base[run + 1];
   // thread k owns elements k + 256 m (m < 8): eight independent loads per chunk
@@ -472,13 +479,13 @@ __global__ void __launch_bounds__(256) k_reduce_g2(const uint32_t* __restrict__ 
   for (int m = 0; m < 8; ++m) {
     const int e = (int)threadIdx.x + 256 * m;
     const int a = e >> 6, j2 = (e >> 4) & 3, bp = e & 15;
-    dG2[(int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp] = acc[m];
+    put_grad(dG2, (int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp, acc[m], lr, update);
   }
 }
 
 // dG3[t][i3][16 h + b'][j3] = sum over the workgroups that owned (t, h)
 __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __restrict__ g3part, int nwg,
-                                                   float* __restrict__ dG3) {
+                                                   float* __restrict__ dG3, float lr, bool update) {
   const int nq = 2 * s.T;
   const int q = blockIdx.y;
   const int t = q % s.T, h = q / s.T;
@@ -488,7 +495,7 @@ __global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __r
   float acc = 0.f;
   for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
   const int i3 = e >> 7, j3 = (e >> 4) & 7, bp = g3_unslot(j3, e & 15);
-  dG3[(((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3] = acc;
+  put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3, acc, lr, update);
 }
 
 bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
@@ -498,8 +505,10 @@ bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
          max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
 }
 
+// With update set, dG1..dG3 are the cores themselves and receive G -= lr * dG.
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
-                          float* dG1, float* dG2, float* dG3, const Prof& prof, hipStream_t st) {
+                          float* dG1, float* dG2, float* dG3, float lr, bool update, const Prof& prof,
+                          hipStream_t st) {
   const int nq = 2 * s.T;
   int per_q = persistent_grid() / nq;
   if (per_q < 1) per_q = 1;
@@ -517,11 +526,11 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
                      (int)w.nsl_max, (int)w.nch_max);
   prof_end(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(512), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
-                     (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1);
+                     (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1, lr, update);
   hipLaunchKernelGGL(k_reduce_g2, dim3(s.T * s.n2 * 2), dim3(256), 0, st, (const uint32_t*)w.run_nch,
-                     (const float*)w.dBpart, (int)w.nch_max, dG2);
+                     (const float*)w.dBpart, (int)w.nch_max, dG2, lr, update);
   hipLaunchKernelGGL(k_reduce_g3, dim3((s.n3 * 128 + 255) / 256, nq), dim3(256), 0, st, shape_args(s),
-                     (const float*)w.g3part, grid, dG3);
+                     (const float*)w.g3part, grid, dG3, lr, update);
   return hipGetLastError();
 }
 

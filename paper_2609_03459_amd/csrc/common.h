@@ -84,6 +84,7 @@ struct Work {
   float* dApart;          // [2][nsl_max][d1*R] backward: dA of each slice, per rank half
   float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
+  float* gscratch;        // gradients of the fused backward-and-SGD call on the generic path (core-sized), else null
   int64_t nsl_max, nch_max;
   float* E;               // [M][D]: E rows (forward), dE rows (backward)
   float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
@@ -116,9 +117,10 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
 hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           const int64_t* offsets, int64_t M, int64_t B, float* out, const Prof& prof,
                           hipStream_t st);
+// With update set, dG1..dG3 are the cores and receive G -= lr * dG (no gradient arrays written).
 hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                            const int64_t* offsets, int64_t M, int64_t B, const float* dV, float* dG1, float* dG2,
-                           float* dG3, const Prof& prof, hipStream_t st);
+                           float* dG3, float lr, bool update, const Prof& prof, hipStream_t st);
 hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                       const float* dG3, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.

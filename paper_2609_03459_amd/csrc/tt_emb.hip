@@ -84,6 +84,10 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->dApart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nsl_max * s.d1 * s.R : 0);
   W->dBpart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2) : 0);
   W->g3part = (float*)take(bwd_r32 ? 4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2) : 0);
+  const size_t ncore = (size_t)s.T * ((size_t)s.n1 * s.d1 * s.R + (size_t)s.n2 * s.R * s.d2 * s.R +
+                                      (size_t)s.n3 * s.R * s.d3);
+  W->gscratch = (float*)take(bwd_r32 ? 0 : 4 * ncore);
+  if (bwd_r32) W->gscratch = nullptr;
   const int par = sort_passes(s.key_bits) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];
@@ -294,7 +298,29 @@ tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2,
   Work w;
   carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
   return hip_status(
-      launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, dG1, dG2, dG3, h->prof, s));
+      launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, dG1, dG2, dG3, 0.f, false,
+                      h->prof, s));
+}
+
+tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const int64_t* indices,
+                                  int64_t num_indices, const int64_t* offsets, int64_t num_bags,
+                                  const float* grad_out, float lr, int reuse_grouping, void* workspace,
+                                  size_t ws_bytes, void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  if (!G1 || !G2 || !G3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
+  if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(grad_out, 16)) return TT_EMB_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if (reuse_grouping) {
+    if (!grouping_matches(h, indices, num_indices, offsets, num_bags, workspace)) return TT_EMB_EINVAL;
+  } else {
+    st = do_group(h, indices, num_indices, offsets, num_bags, workspace, s);
+    if (st != TT_EMB_OK) return st;
+  }
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  return hip_status(launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, G1, G2, G3, lr,
+                                    true, h->prof, s));
 }
 
 tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,

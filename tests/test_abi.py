@@ -86,6 +86,13 @@ def test_calls_reject_bad_arguments_without_launching(N):
     assert b(h, fake, fake, fake, fake, 20, off, 10, fake, None, fake, fake, 0, fake, ws_bytes, None) == E
     assert b(h, fake, fake, fake, fake, 20, off, 10, fake, fake, fake, fake, 1, fake, ws_bytes, None) == E
     assert N.lib.tt_emb_sgd(h, fake, fake, None, fake, fake, fake, C.c_float(0.1), None) == E
+    bs = N.lib.tt_emb_backward_sgd
+    lr = C.c_float(0.1)
+    assert bs(h, None, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes, None) == E  # null core
+    assert bs(h, fake, fake, fake + 4, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes, None) == E  # misaligned
+    assert bs(h, fake, fake, fake, fake, 20, off, 10, None, lr, 0, fake, ws_bytes, None) == E  # null grad_out
+    assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 1, fake, ws_bytes, None) == E  # no grouping yet
+    assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes - 1, None) == E
     assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
     assert N.lib.tt_emb_debug_grouping(h, fake, None, None, None, None, None, None, None, None, None) == E
     N.tt_emb_destroy(h)

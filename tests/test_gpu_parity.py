@@ -356,3 +356,84 @@ def test_sgd_step(lib, orc):
         # gradient error scaled by lr plus one fp32 rounding of the updated value
         bound = TOL * lr * mag[k] + 2.0 ** -23 * np.abs(exp)
         assert np.all(np.abs(new - exp) <= bound + 1e-30), name
+
+
+def _check_sgd(orc, case, G, lr, name):
+    ref = orc.backward(case)[:3]
+    mag = orc.backward(abs_case(case))[:3]
+    for k, cname in enumerate(("G1", "G2", "G3")):
+        new = G[k].cpu().numpy().astype(np.float64)
+        exp = orc.sgd(case[cname], ref[k], lr)
+        # gradient error scaled by lr plus one fp32 rounding of the updated value
+        bound = TOL * lr * mag[k] + 2.0 ** -23 * np.abs(exp)
+        assert np.all(np.abs(new - exp) <= bound + 1e-30), f"{cname} {name}"
+
+
+@pytest.mark.parametrize("reuse", [True, False])
+@pytest.mark.parametrize("k", [0, 4, 5, 7])
+def test_backward_sgd_fused(lib, orc, k, reuse):
+    # one call for backward + SGD leaves the cores where backward then sgd would
+    # (the MFMA shapes update inside the reductions, the others via workspace gradients)
+    c = dict(TINY[k])
+    case = ttgen.tiny(5000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    _say(f"[bwd+sgd] tiny{k} reuse_grouping={reuse}")
+    emb = _make(lib, case)
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    lr = 0.01
+    if reuse:
+        emb.group(idx, off, num_bags=case["B"])
+    emb.backward_sgd(*G, idx, off, dV, lr, num_bags=case["B"], reuse_grouping=reuse)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    _check_sgd(orc, case, G, lr, f"tiny{k}")
+
+
+def test_backward_sgd_fused_config5(lib, orc):
+    case = ttgen.make(5, bags=32)
+    _say("[bwd+sgd] config5 B=32")
+    emb = _make(lib, case)
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.backward_sgd(*G, idx, off, dV, case["lr"], num_bags=case["B"], reuse_grouping=False)
+    torch.cuda.synchronize()
+    _check_sgd(orc, case, G, case["lr"], "config5 B=32")
+
+
+def test_autograd_module(lib, orc):
+    # torch autograd through the library: forward output and .grad of the three
+    # core parameters against the oracle, for L = sum <dV, out>
+    case = ttgen.tiny(6001, 2, (20, 30, 40), (4, 4, 8), 32, B=60, max_len=12, zipf=1.1)
+    _say("[autograd] T=2 n=(20,30,40) d=(4,4,8) R=32")
+    M = int(case["idx"].size)
+    mod = lib.TTEmbeddingBag(case["T"], case["N"], case["n"], case["d"], case["R"], max_indices=M,
+                             max_bags=case["B"])
+    with torch.no_grad():
+        for name in ("G1", "G2", "G3"):
+            getattr(mod, name).copy_(torch.from_numpy(case[name]))
+    _, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    out = mod(idx, off)
+    # another lookup on the same handle in between: backward must regroup its own indices
+    other = torch.randint(0, case["N"], (idx.numel(),), device=idx.device)
+    mod.emb.group(other, off, num_bags=case["B"])
+    (out * dV).sum().backward()
+    torch.cuda.synchronize()
+    D = int(np.prod(case["d"]))
+    ref_v, _ = orc.forward(case)
+    mag_v, _ = orc.forward(abs_case(case))
+    assert_close("autograd out", out.detach().cpu().numpy().reshape(-1, D), ref_v, mag_v)
+    ref = orc.backward(case)[:3]
+    mag = orc.backward(abs_case(case))[:3]
+    for k, name in enumerate(("G1", "G2", "G3")):
+        assert_close(f"autograd {name}.grad", getattr(mod, name).grad.cpu().numpy(), ref[k], mag[k])
+    # the fused training step on the module matches backward + sgd
+    mod2 = lib.TTEmbeddingBag(case["T"], case["N"], case["n"], case["d"], case["R"], max_indices=M,
+                              max_bags=case["B"])
+    with torch.no_grad():
+        for name in ("G1", "G2", "G3"):
+            getattr(mod2, name).copy_(torch.from_numpy(case[name]))
+    mod2(idx, off)
+    mod2.step_fused(idx, off, dV, 0.01)
+    torch.cuda.synchronize()
+    _check_sgd(orc, case, [mod2.G1.data, mod2.G2.data, mod2.G3.data], 0.01, "module step_fused")
