@@ -210,6 +210,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--reuse", choices=["prefix", "unique", "none"], default="prefix",
                     help="reuse level (ablation of Section 4.5): prefix groups (default), exact dedup only, none")
+    ap.add_argument("--sched", choices=["steal", "static", "steal_ckpt"], default="steal",
+                    help="work distribution (ablation of Section 4.4): stealing (default), static shares, "
+                         "stealing with checkpointed intermediates")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
@@ -237,7 +240,7 @@ def main():
     M = int(case["idx"].size)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B, reuse=args.reuse)
+    emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B, reuse=args.reuse, sched=args.sched)
     G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
     idx = torch.from_numpy(case["idx"]).to(dev)
     off = None if case["offsets"] is None else torch.from_numpy(case["offsets"]).to(dev)
@@ -365,7 +368,7 @@ def main():
         "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "row_factors": list(n),
                    "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
                    "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu",
-                   "reuse": args.reuse},
+                   "reuse": args.reuse, "sched": args.sched},
         "roofline": roof,
         "step_ms_median": round(step_med, 4),
         "copy_gbps_measured": round(copy_gbps, 1),

@@ -101,6 +101,29 @@ tt_emb_status tt_emb_destroy(tt_emb_handle h);
 typedef enum { TT_EMB_REUSE_PREFIX = 0, TT_EMB_REUSE_UNIQUE = 1, TT_EMB_REUSE_NONE = 2 } tt_emb_reuse;
 tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
 
+/* Work distribution of the fused kernels, for the scheduling ablation of
+ * Section 4.4:
+ *   TT_EMB_SCHED_STEAL       (default) persistent workers take chunks of
+ *                            prefix groups from shared queues and steal from
+ *                            other queues when theirs runs dry (Section 3.4);
+ *   TT_EMB_SCHED_STATIC      each worker takes a fixed contiguous share of
+ *                            the chunks (equal counts, no work moves);
+ *   TT_EMB_SCHED_STEAL_CKPT  stealing plus inter-worker reuse of the
+ *                            intermediate C (Section 3.5): a worker that
+ *                            builds C for a prefix group publishes it in a
+ *                            small table in the workspace (a few KB per
+ *                            resident worker, L2-resident), and a worker that
+ *                            meets the same group later reloads it instead of
+ *                            recomputing it, whenever the entry still holds
+ *                            that group.
+ * The checkpoint applies to the kernels that keep one C per worker (every
+ * shape except d = (4,4,8), R = 32); the MFMA kernels for that shape build C
+ * for four slices per matrix-core tile and treat STEAL_CKPT as STEAL.  All
+ * modes compute the same function.  Host only; may be changed between calls;
+ * returns TT_EMB_EINVAL for an unknown mode. */
+typedef enum { TT_EMB_SCHED_STEAL = 0, TT_EMB_SCHED_STATIC = 1, TT_EMB_SCHED_STEAL_CKPT = 2 } tt_emb_sched;
+tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode);
+
 /* Bytes of device workspace needed for calls up to desc.max_indices and
  * desc.max_bags at the handle's reuse level.  The same workspace carries the
  * index grouping from a forward call to the following backward call. */

@@ -31,7 +31,7 @@ class TTEmbedding:
     """
 
     def __init__(self, num_tables, num_rows, row_factors, dim_factors, rank, max_indices, max_bags,
-                 device="cuda", reuse="prefix"):
+                 device="cuda", reuse="prefix", sched="steal"):
         d = N.tt_emb_desc()
         d.num_tables = int(num_tables)
         d.num_rows = int(num_rows)
@@ -50,6 +50,8 @@ class TTEmbedding:
         # reuse level (Section 4.5 ablation): "prefix" (default), "unique" or "none"
         N.tt_emb_set_reuse(self.handle, N.REUSE[reuse])
         self.reuse = reuse
+        # work distribution (Section 4.4 ablation): "steal" (default), "static" or "steal_ckpt"
+        self.set_schedule(sched)
         self.ws_bytes = N.tt_emb_workspace_size(self.handle)
         # 256-byte aligned workspace carved from one torch allocation
         raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
@@ -57,6 +59,10 @@ class TTEmbedding:
         self._raw = raw
         self.workspace = raw[shift:shift + self.ws_bytes]
         self.device = device
+
+    def set_schedule(self, sched):
+        N.tt_emb_set_schedule(self.handle, N.SCHED[sched])
+        self.sched = sched
 
     def __del__(self):
         h = getattr(self, "handle", None)

@@ -16,6 +16,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "tt_emb.h")
 
 TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED = range(6)
 REUSE = {"prefix": 0, "unique": 1, "none": 2}
+SCHED = {"steal": 0, "static": 1, "steal_ckpt": 2}
 KERNELS = {"ingest": 1, "fwd_fused": 2, "pool": 3, "seg_sum": 4, "bwd_fused": 5}
 
 
@@ -54,6 +55,7 @@ _SIG = {
     "tt_emb_status_string": ([C.c_int], C.c_char_p),
     "tt_emb_profile": ([_P, C.c_int, _P, _P], C.c_int),
     "tt_emb_set_reuse": ([_P, C.c_int], C.c_int),
+    "tt_emb_set_schedule": ([_P, C.c_int], C.c_int),
 }
 for _name, (_args, _res) in _SIG.items():
     _f = getattr(lib, _name)
@@ -127,6 +129,10 @@ def tt_emb_check_errors(h, ws, stream) -> int:
 
 def tt_emb_set_reuse(h, level: int) -> None:
     check("tt_emb_set_reuse", lib.tt_emb_set_reuse(h, int(level)))
+
+
+def tt_emb_set_schedule(h, mode: int) -> None:
+    check("tt_emb_set_schedule", lib.tt_emb_set_schedule(h, int(mode)))
 
 
 def tt_emb_profile(h, kernel: int, ev_begin, ev_end) -> None:

@@ -225,21 +225,23 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
                                                              const uint32_t* __restrict__ uniq_key,
                                                              int32_t* __restrict__ ctr, const float* __restrict__ dE,
                                                              float* __restrict__ dG1, float* __restrict__ dG2,
-                                                             float* __restrict__ dG3) {
+                                                             float* __restrict__ dG3, float* __restrict__ ckpt,
+                                                             int32_t* __restrict__ ckpt_tag) {
   extern __shared__ float lds[];
   const int d2R = s.d2 * s.R;
   const int nC = s.d1 * d2R;
   float* C = lds;           // nC
   float* dCs = lds + nC;    // nC: sum of dC over the slice's rows
   float* dEu = dCs + nC;    // D
-  __shared__ int s_chunk;
+  __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
   const int nchunks = (nsl + BWD_CHUNK - 1) / BWD_CHUNK;
   int victim = 0;
+  int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
   int cur_pg = -1;
   const int rows12 = s.d1 * s.d2;
   while (true) {
-    int c = claim_block(ctr + C_BWD_CTR, nchunks, SCHED_NQ, blockIdx.x % SCHED_NQ, &victim, &s_chunk);
+    int c = claim_block_sched(s.sched, ctr + C_BWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk, &next);
     if (c < 0) break;
     const int s0 = c * BWD_CHUNK;
     const int s1 = s0 + BWD_CHUNK < nsl ? s0 + BWD_CHUNK : nsl;
@@ -253,11 +255,19 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
       const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
       __syncthreads();
       if (p != cur_pg) {
-        for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
-          const int j1 = o / d2R, cc = o % d2R;
-          float acc = 0.f;
-          for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
-          C[o] = acc;
+        // C recomputed, or with the checkpoint reloaded / published as in the forward
+        const bool ck = s.sched == SCHED_STEAL_CKPT;
+        if (!(ck && ckpt_load(ckpt, ckpt_tag, p, C, nC, &s_flag))) {
+          for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
+            const int j1 = o / d2R, cc = o % d2R;
+            float acc = 0.f;
+            for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
+            C[o] = acc;
+          }
+          if (ck && s1 < nsl && slices[s1].x == p) {
+            __syncthreads();
+            ckpt_store(ckpt, ckpt_tag, p, C, nC, &s_flag);
+          }
         }
         cur_pg = p;
       }
@@ -357,9 +367,15 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
       hipSuccess)
     return e;
+  if (s.sched == SCHED_STEAL_CKPT) {  // the forward's checkpoints may hold other cores' C
+    if (!w.ckpt_tag) return hipErrorInvalidValue;
+    if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ckpt_tag), CKPT_SLOTS, (uint32_t)CKPT_EMPTY, st)) != hipSuccess)
+      return e;
+  }
   prof_begin(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
-                     (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3);
+                     (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3,
+                     w.ckpt, w.ckpt_tag);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);

@@ -23,6 +23,7 @@ struct Shape {
   int64_t ndense;  // T*n1*n2 prefix slots
   int slice_rows;  // rows per work slice: SLICE_ROWS, or 1 when prefix reuse is off (ablation)
   int dedup;       // 1: exact dedup of rows; 0: every occurrence is its own row (ablation)
+  int sched;       // work distribution: SCHED_STEAL, SCHED_STATIC or SCHED_STEAL_CKPT (ablation)
 };
 
 // Counter slots at the head of the workspace (int32).
@@ -85,6 +86,8 @@ struct Work {
   float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
   float* gscratch;        // gradients of the fused backward-and-SGD call on the generic path (core-sized), else null
+  float* ckpt;            // [CKPT_SLOTS][d1*d2*R] checkpointed C of the generic kernels (null for the MFMA shape)
+  int32_t* ckpt_tag;      // [CKPT_SLOTS] prefix group held by each entry, -1 = none
   int64_t nsl_max, nch_max;
   float* E;               // [M][D]: E rows (forward), dE rows (backward)
   float* seg_part;        // [nseg][2][D] partial dE of rows that cross a chunk
@@ -125,6 +128,8 @@ hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const flo
                       const float* dG3, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.
 bool bwd_r32_supported(const Shape& s, int64_t max_indices);
+// Whether the MFMA forward serves this shape.
+bool fwd_r32_supported(const Shape& s, int64_t max_indices);
 
 // Small generic kernels shared across units (defined in group.hip).
 hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);
@@ -217,10 +222,83 @@ __device__ __forceinline__ int claim_block(int32_t* q, int nchunks, int nq, int 
   return c;
 }
 
+// Work distribution modes (values of the C-ABI's tt_emb_sched).
+enum : int { SCHED_STEAL = 0, SCHED_STATIC = 1, SCHED_STEAL_CKPT = 2 };
+// Checkpoint table of the generic fused kernels: CKPT_SLOTS entries of one C
+// (d1 d2 R floats) each, tagged with the prefix group they hold.
+constexpr int CKPT_SLOTS = 1024;
+
+// The next chunk of a block-level worker: its fixed contiguous share in order
+// (SCHED_STATIC; *next starts at the share's first chunk), or from the shared
+// queues with stealing.  `sched` is a kernel argument, so every thread of the
+// block takes the same branch.
+__device__ __forceinline__ int claim_block_sched(int sched, int32_t* q, int nchunks, int home, int* cursor,
+                                                 int* s_chunk, int* next) {
+  if (sched == SCHED_STATIC) {
+    const int hi = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x + 1);
+    return *next < hi ? (*next)++ : -1;
+  }
+  return claim_block(q, nchunks, SCHED_NQ, home, cursor, s_chunk);
+}
+
+// Checkpointed intermediates of the generic kernels (Section 3.5).  The entry of
+// prefix group p is slot p mod CKPT_SLOTS; its tag holds p when complete, CKPT_BUSY
+// while a block writes it and CKPT_EMPTY after the per-launch reset.  A writer
+// first swaps the tag to CKPT_BUSY (so writers of one slot exclude each other) and
+// publishes p after the data; a reader accepts the data only if the tag read p
+// both before and after its copy.
+constexpr int32_t CKPT_BUSY = -1, CKPT_EMPTY = -2;
+
+// Block-wide: copies p's checkpoint into C (nC floats, LDS) and returns true, or
+// returns false (C unspecified) when the entry does not hold p.
+__device__ __forceinline__ bool ckpt_load(const float* ckpt, int32_t* tag, int p, float* C, int nC, int* s_flag) {
+  const int slot = p % CKPT_SLOTS;
+  if (threadIdx.x == 0)
+    *s_flag = __hip_atomic_load(tag + slot, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == p;
+  __syncthreads();
+  const bool hit = *s_flag;
+  __syncthreads();
+  if (!hit) return false;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  const float* src = ckpt + (size_t)slot * nC;
+  for (int o = threadIdx.x; o < nC; o += blockDim.x) C[o] = __builtin_nontemporal_load(src + o);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *s_flag = __hip_atomic_load(tag + slot, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == p;
+  __syncthreads();
+  const bool still = *s_flag;
+  __syncthreads();
+  return still;
+}
+
+// Block-wide: publishes C (nC floats, LDS) as p's checkpoint unless another block
+// is writing that slot.
+__device__ __forceinline__ void ckpt_store(float* ckpt, int32_t* tag, int p, const float* C, int nC, int* s_flag) {
+  const int slot = p % CKPT_SLOTS;
+  if (threadIdx.x == 0) {
+    int32_t seen = __hip_atomic_load(tag + slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *s_flag = seen != CKPT_BUSY &&
+              __hip_atomic_compare_exchange_strong(tag + slot, &seen, CKPT_BUSY, __ATOMIC_ACQ_REL,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  const bool mine = *s_flag;
+  __syncthreads();
+  if (!mine) return;
+  float* dst = ckpt + (size_t)slot * nC;
+  for (int o = threadIdx.x; o < nC; o += blockDim.x) dst[o] = C[o];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(tag + slot, p, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 struct ShapeArgs {  // shape constants passed by value to kernels
   int T, n1, n2, n3, d1, d2, d3, R, D, n12;
   uint32_t Npad;
+  int sched;
 };
+
 
 }  // namespace ttemb
 

@@ -20,6 +20,7 @@ ShapeArgs shape_args(const Shape& s) {
   a.D = s.D;
   a.n12 = s.n12;
   a.Npad = s.Npad;
+  a.sched = s.sched;
   return a;
 }
 
@@ -32,18 +33,20 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
                                                              const float* __restrict__ G3,
                                                              const int4* __restrict__ slices,
                                                              const uint32_t* __restrict__ uniq_key,
-                                                             int32_t* __restrict__ ctr, float* __restrict__ E) {
+                                                             int32_t* __restrict__ ctr, float* __restrict__ E,
+                                                             float* __restrict__ ckpt, int32_t* __restrict__ ckpt_tag) {
   extern __shared__ float lds[];
   float* C = lds;  // d1 * d2 * R
-  __shared__ int s_chunk;
+  __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
   const int nchunks = (nsl + FWD_CHUNK - 1) / FWD_CHUNK;
   const int d2R = s.d2 * s.R;
   const int nC = s.d1 * d2R;
   int victim = 0;
+  int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
   int cur_pg = -1;
   while (true) {
-    int c = claim_block(ctr + C_FWD_CTR, nchunks, SCHED_NQ, blockIdx.x % SCHED_NQ, &victim, &s_chunk);
+    int c = claim_block_sched(s.sched, ctr + C_FWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk, &next);
     if (c < 0) break;
     const int s0 = c * FWD_CHUNK;
     const int s1 = s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl;
@@ -54,15 +57,24 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
       const int t = key / s.n12, q = key % s.n12;
       const int i1 = q / s.n2, i2 = q % s.n2;
       if (p != cur_pg) {
-        // intermediate C = A.B, kept in LDS while rows of this group follow
+        // intermediate C = A.B, kept in LDS while rows of this group follow; with
+        // the checkpoint, reloaded if another block published it, and published if
+        // the group goes on past this chunk (where a stealing block may meet it)
         __syncthreads();
-        const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
-        const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
-        for (int o = threadIdx.x; o < nC; o += FWD_THREADS) {
-          const int j1 = o / d2R, cc = o % d2R;
-          float acc = 0.f;
-          for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
-          C[o] = acc;
+        const bool ck = s.sched == SCHED_STEAL_CKPT;
+        if (!(ck && ckpt_load(ckpt, ckpt_tag, p, C, nC, &s_flag))) {
+          const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+          const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
+          for (int o = threadIdx.x; o < nC; o += FWD_THREADS) {
+            const int j1 = o / d2R, cc = o % d2R;
+            float acc = 0.f;
+            for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
+            C[o] = acc;
+          }
+          if (ck && s1 < nsl && slices[s1].x == p) {
+            __syncthreads();
+            ckpt_store(ckpt, ckpt_tag, p, C, nC, &s_flag);
+          }
         }
         __syncthreads();
         cur_pg = p;
@@ -135,8 +147,15 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   int c_rb = 0, c_nr = 0, c_i1 = 0;
   int f = 0, ns = 0, run = -1, t = 0, qd = 0;
   int c = -1;
+  // SCHED_STATIC: this wave's fixed share of the chunks, in order
+  const int wid = blockIdx.x * F32_WAVES + wave, nw = gridDim.x * F32_WAVES;
+  int st_next = share_lo(nch, nw, wid);
+  const int st_hi = share_lo(nch, nw, wid + 1);
   auto next_chunk = [&]() {
-    c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
+    if (s.sched == SCHED_STATIC)
+      c = st_next < st_hi ? st_next++ : -1;
+    else
+      c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
     qd = 0;
     if (c >= 0) {
       const int4 ch = chunks[c];
@@ -496,9 +515,14 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
     const size_t lds = sizeof(float) * (size_t)s.d1 * s.d2 * s.R;
     e = hipFuncSetAttribute((const void*)k_fwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
+    if (s.sched == SCHED_STEAL_CKPT) {  // checkpoints of earlier calls may hold other cores' C
+      if (!w.ckpt_tag) return hipErrorInvalidValue;
+      e = fill_u32(reinterpret_cast<uint32_t*>(w.ckpt_tag), CKPT_SLOTS, (uint32_t)CKPT_EMPTY, st);
+      if (e != hipSuccess) return e;
+    }
     prof_begin(prof, K_FWD_FUSED, st);
     hipLaunchKernelGGL(k_fwd_generic, dim3(grid), dim3(FWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
-                       (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E);
+                       (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag);
     prof_end(prof, K_FWD_FUSED, st);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

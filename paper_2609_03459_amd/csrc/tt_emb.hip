@@ -88,6 +88,14 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
                                       (size_t)s.n3 * s.R * s.d3);
   W->gscratch = (float*)take(bwd_r32 ? 0 : 4 * ncore);
   if (bwd_r32) W->gscratch = nullptr;
+  const bool generic = !bwd_r32 || !fwd_r32_supported(s, m);
+  const size_t nC = (size_t)s.d1 * s.d2 * s.R;
+  W->ckpt = (float*)take(generic ? 4 * CKPT_SLOTS * nC : 0);
+  W->ckpt_tag = (int32_t*)take(generic ? 4 * CKPT_SLOTS : 0);
+  if (!generic) {
+    W->ckpt = nullptr;
+    W->ckpt_tag = nullptr;
+  }
   const int par = sort_passes(s.key_bits) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];
@@ -181,6 +189,7 @@ tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
   s.ndense = (int64_t)T * s.n1 * s.n2;
   s.slice_rows = SLICE_ROWS;
   s.dedup = 1;
+  s.sched = SCHED_STEAL;
   h->g_valid = false;
   h->prof.kernel = 0;
   h->prof.begin = nullptr;
@@ -208,6 +217,12 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level) {
   h->s.slice_rows = level == TT_EMB_REUSE_PREFIX ? SLICE_ROWS : 1;
   h->s.dedup = level == TT_EMB_REUSE_NONE ? 0 : 1;
   h->g_valid = false;  // a grouping made at another level must not be reused
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode) {
+  if (!h || mode < TT_EMB_SCHED_STEAL || mode > TT_EMB_SCHED_STEAL_CKPT) return TT_EMB_EINVAL;
+  h->s.sched = mode;
   return TT_EMB_OK;
 }
 

@@ -94,6 +94,9 @@ def test_calls_reject_bad_arguments_without_launching(N):
     assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 1, fake, ws_bytes, None) == E  # no grouping yet
     assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes - 1, None) == E
     assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
+    assert N.lib.tt_emb_set_schedule(h, 3) == E and N.lib.tt_emb_set_schedule(h, -1) == E
+    assert N.lib.tt_emb_set_schedule(None, 0) == E
+    assert N.lib.tt_emb_set_schedule(h, 2) == N.TT_EMB_OK and N.lib.tt_emb_set_schedule(h, 0) == N.TT_EMB_OK
     assert N.lib.tt_emb_debug_grouping(h, fake, None, None, None, None, None, None, None, None, None) == E
     N.tt_emb_destroy(h)
 

@@ -437,3 +437,43 @@ def test_autograd_module(lib, orc):
     mod2.step_fused(idx, off, dV, 0.01)
     torch.cuda.synchronize()
     _check_sgd(orc, case, [mod2.G1.data, mod2.G2.data, mod2.G3.data], 0.01, "module step_fused")
+
+
+def _run_mode(lib, case, **kw):
+    M = int(case["idx"].size)
+    emb = lib.TTEmbedding(case["T"], case["N"], case["n"], case["d"], case["R"], max_indices=max(M, 1),
+                          max_bags=max(int(case["B"]), 1), **kw)
+    G, idx, off = _dev(case)
+    out = emb.forward(*G, idx, off, num_bags=case["B"])
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    grads = emb.backward(*G, idx, off, dV, num_bags=case["B"], reuse_grouping=True)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    D = int(np.prod(case["d"]))
+    return out.cpu().numpy().reshape(-1, D), [g.cpu().numpy() for g in grads], emb
+
+
+@pytest.mark.parametrize("which", ["hot_r64", "mfma"])
+def test_schedules_same_results(lib, orc, which):
+    # Section 4.4 ablation modes compute the same function: static shares, stealing,
+    # and stealing with the checkpointed intermediate (hot prefix groups spanning
+    # several chunks on the generic kernels)
+    if which == "hot_r64":
+        case = ttgen.make(4, bags=256, with_grad=True)
+    else:
+        c = dict(TINY[4])
+        case = ttgen.tiny(7004, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    ref_v, _ = orc.forward(case)
+    mag_v, _ = orc.forward(abs_case(case))
+    ref = orc.backward(case)[:3]
+    mag = orc.backward(abs_case(case))[:3]
+    for sched in ("steal", "static", "steal_ckpt"):
+        _say(f"[sched] {which} {sched}")
+        V, grads, emb = _run_mode(lib, case, sched=sched)
+        assert_close(f"forward {which} {sched}", V, ref_v, mag_v)
+        for k in range(3):
+            assert_close(f"dG{k + 1} {which} {sched}", grads[k], ref[k], mag[k])
+        if which == "hot_r64" and sched == "steal_ckpt":
+            # the workload must exercise the checkpoint: some prefix group spans chunks
+            g = emb.debug_grouping(int(case["idx"].size))
+            assert np.max(np.diff(g["pg_start"])) > 8 * 32
