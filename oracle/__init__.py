@@ -33,6 +33,11 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+class _ShapeN(C.Structure):
+    _fields_ = [("T", C.c_int), ("N", C.c_int64), ("L", C.c_int), ("n", C.c_int32 * 8), ("d", C.c_int32 * 8),
+                ("R", C.c_int), ("B", C.c_int64)]
+
+
 class _Shape(C.Structure):
     _fields_ = [("T", C.c_int), ("N", C.c_int64), ("n", C.c_int32 * 3), ("d", C.c_int32 * 3), ("R", C.c_int),
                 ("B", C.c_int64)]
@@ -53,6 +58,10 @@ def _load():
         lib.orc_forward.restype = C.c_int64
         lib.orc_backward.argtypes = [C.POINTER(_Shape), P, P, P, P, C.c_int64, P, P, P, P, P, P, P, P]
         lib.orc_backward.restype = C.c_int64
+        lib.orc_forward_n.argtypes = [C.POINTER(_ShapeN), P, P, C.c_int64, P, P]
+        lib.orc_forward_n.restype = C.c_int64
+        lib.orc_backward_n.argtypes = [C.POINTER(_ShapeN), P, P, C.c_int64, P, P, P]
+        lib.orc_backward_n.restype = C.c_int64
         lib.orc_sgd.argtypes = [P, P, C.c_int64, C.c_double, P]
         lib.orc_sgd.restype = None
         lib.orc_grouping.argtypes = [C.POINTER(_Shape), P, C.c_int64, P, P, P, P, P, P, P, P, P, P]
@@ -174,3 +183,47 @@ def grouping(case) -> dict:
 
 
 __all__ = ["build", "digits", "row", "forward", "backward", "sgd", "grouping"]
+
+
+def _shape_n(case) -> _ShapeN:
+    s = _ShapeN()
+    s.T, s.N, s.L, s.R, s.B = int(case["T"]), int(case["N"]), int(case["L"]), int(case["R"]), int(case["B"])
+    if not 2 <= s.L <= 8:
+        raise ValueError("2 <= L <= 8 cores")
+    for k in range(s.L):
+        s.n[k] = int(case["n"][k])
+        s.d[k] = int(case["d"][k])
+    return s
+
+
+def _ptr_array(arrays):
+    a = (C.c_void_p * len(arrays))(*[x.ctypes.data for x in arrays])
+    return a
+
+
+def forward_n(case):
+    """Sum-pooled gather with L = len(case["n"]) cores: each row is the chain of its
+    L core slices (Eq. 2 digits, Section 3.2 contraction extended to L cores).
+    Returns (V [T*B][D], invalid_count)."""
+    s = _shape_n(case)
+    cores = [_f32(G) for G in case["cores"]]
+    idx = _i64(case["idx"])
+    off = _i64(case["offsets"])
+    V = np.zeros((int(case["T"]) * int(case["B"]), int(np.prod(case["d"]))), dtype=np.float64)
+    inv = _load().orc_forward_n(C.byref(s), C.cast(_ptr_array(cores), C.c_void_p), _ptr(idx), idx.size, _ptr(off),
+                                _ptr(V))
+    return V, int(inv)
+
+
+def backward_n(case, dV=None):
+    """Core gradients with L cores of L = sum <dV, V>: the chain rule through the chain
+    of slices, per occurrence (for L = 3 exactly Eq. 1).  Returns ([dG_k], invalid)."""
+    s = _shape_n(case)
+    cores = [_f32(G) for G in case["cores"]]
+    dV = _f32(case["dV"] if dV is None else dV)
+    idx = _i64(case["idx"])
+    off = _i64(case["offsets"])
+    dG = [np.zeros(G.shape, dtype=np.float64) for G in cores]
+    inv = _load().orc_backward_n(C.byref(s), C.cast(_ptr_array(cores), C.c_void_p), _ptr(idx), idx.size, _ptr(off),
+                                 _ptr(dV), C.cast(_ptr_array(dG), C.c_void_p))
+    return dG, int(inv)

@@ -233,6 +233,183 @@ int64_t orc_backward(const shape_t* s, const float* G1, const float* G2, const f
   return invalid;
 }
 
+/* ---------------------------------------------------------------------------
+ * L cores (L >= 2): the same operator with the row split into L mixed-radix
+ * digits (Eq. 2 is stated for any number of factors) and the row rebuilt by
+ * the chain of the L core slices; the prefix of Section 3.3 becomes the first
+ * L-1 digits (deeper decompositions are the paper's stated future work).
+ *
+ * Core k (k = 0..L-1) is [T][n_k][r_k][d_k][r_{k+1}] with r_0 = r_L = 1 and
+ * the other ranks R; its slice S_k = core k [t][i_k] is r_k x (d_k r_{k+1}).
+ * The chain: X_0 = S_0 (d_0 x R); X_k = X_{k-1} . S_k with X_{k-1} viewed as
+ * m_{k-1} x r_k (m_k = d_0 ... d_k rows), giving m_{k-1} x (d_k r_{k+1}), i.e.
+ * m_k x r_{k+1}; X_{L-1} is the row E (D x 1), output digit j_0 most
+ * significant.  For L = 3 this is C = A.B (X_1) and E = C.D (X_2).
+ * Pinned (CPU tests): equal to the three-core functions above at L = 3; the
+ * additive rank-2 train whose row g is g*D + j exactly, for L = 2, 4, 5; an
+ * identity middle core that turns L = 4 into L = 3; a float64 torch brute
+ * force with autograd gradients; and <dG_k, G_k> = <dV, V> for every k.
+ * ------------------------------------------------------------------------- */
+#define ORC_MAXL 8
+
+typedef struct {
+  int T;
+  int64_t N;
+  int L;
+  int32_t n[ORC_MAXL];
+  int32_t d[ORC_MAXL];
+  int R;
+  int64_t B;
+} shape_n_t;
+
+static int rank_n(const shape_n_t* s, int k) { return (k == 0 || k == s->L) ? 1 : s->R; }
+
+static void mixed_radix_n(const shape_n_t* s, int64_t g, int64_t* dig) {
+  for (int k = 0; k < s->L; ++k) {
+    int64_t prod = 1;
+    for (int j = k + 1; j < s->L; ++j) prod *= s->n[j];
+    dig[k] = (g / prod) % s->n[k];
+  }
+}
+
+static int64_t slice_len_n(const shape_n_t* s, int k) {
+  return (int64_t)rank_n(s, k) * s->d[k] * rank_n(s, k + 1);
+}
+
+static const float* slice_n(const shape_n_t* s, const float* G, int k, int64_t t, int64_t i) {
+  return G + (t * s->n[k] + i) * slice_len_n(s, k);
+}
+
+/* X[k] for k = 0..L-1 of one row; X[k] holds m_k * r_{k+1} doubles. */
+static void chain_n(const shape_n_t* s, const float* const* G, int64_t t, const int64_t* dig, double** X) {
+  const float* S0 = slice_n(s, G[0], 0, t, dig[0]);
+  for (int64_t e = 0; e < slice_len_n(s, 0); ++e) X[0][e] = (double)S0[e];
+  int64_t m = s->d[0];
+  for (int k = 1; k < s->L; ++k) {
+    const float* S = slice_n(s, G[k], k, t, dig[k]);
+    int rk = rank_n(s, k);
+    int64_t cols = (int64_t)s->d[k] * rank_n(s, k + 1);
+    for (int64_t r = 0; r < m; ++r)
+      for (int64_t c = 0; c < cols; ++c) {
+        double acc = 0.0;
+        for (int a = 0; a < rk; ++a) acc += X[k - 1][r * rk + a] * (double)S[a * cols + c];
+        X[k][r * cols + c] = acc;
+      }
+    m *= s->d[k];
+  }
+}
+
+static double** alloc_chain_n(const shape_n_t* s) {
+  double** X = (double**)malloc(sizeof(double*) * s->L);
+  int64_t m = 1;
+  for (int k = 0; k < s->L; ++k) {
+    m *= s->d[k];
+    X[k] = (double*)malloc(sizeof(double) * m * rank_n(s, k + 1));
+  }
+  return X;
+}
+
+static void free_chain_n(const shape_n_t* s, double** X) {
+  for (int k = 0; k < s->L; ++k) free(X[k]);
+  free(X);
+}
+
+static int64_t dimD_n(const shape_n_t* s) {
+  int64_t D = 1;
+  for (int k = 0; k < s->L; ++k) D *= s->d[k];
+  return D;
+}
+
+/* Forward with L cores: V [T*B][D] (sum pooling, empty bag = 0).  Returns the
+ * number of invalid indices met. */
+int64_t orc_forward_n(const shape_n_t* s, const float* const* G, const int64_t* idx, int64_t M,
+                      const int64_t* offsets, double* V) {
+  int64_t D = dimD_n(s), nb = (int64_t)s->T * s->B;
+  double** X = alloc_chain_n(s);
+  int64_t dig[ORC_MAXL];
+  int64_t invalid = 0;
+  (void)M;
+  for (int64_t gb = 0; gb < nb; ++gb) {
+    int64_t t = gb / s->B;
+    int64_t lo = offsets ? offsets[gb] : gb, hi = offsets ? offsets[gb + 1] : gb + 1;
+    double* out = V + gb * D;
+    for (int64_t j = 0; j < D; ++j) out[j] = 0.0;
+    for (int64_t o = lo; o < hi; ++o) {
+      int64_t g = idx[o];
+      if (g < 0 || g >= s->N) {
+        ++invalid;
+        continue;
+      }
+      mixed_radix_n(s, g, dig);
+      chain_n(s, G, t, dig, X);
+      for (int64_t j = 0; j < D; ++j) out[j] += X[s->L - 1][j];
+    }
+  }
+  free_chain_n(s, X);
+  return invalid;
+}
+
+/* Backward with L cores of L = sum <dV, V> into dense core gradients dG[k]
+ * (doubles, shaped like core k, overwritten).  Per occurrence, with
+ * dX_{L-1} = dV[bag] (the chain rule through the chain above):
+ *   for k = L-1 .. 1:  dS_k += X_{k-1}^T dX_k     (dX_k viewed as m_{k-1} x d_k r_{k+1})
+ *                      dX_{k-1} = dX_k S_k^T      (m_{k-1} x r_k)
+ *   dS_0 += dX_0.
+ * For L = 3: dG3 += C^T dE, dC = dE D^T, dG2 += A^T dC, dG1 += dC B^T (Eq. 1). */
+int64_t orc_backward_n(const shape_n_t* s, const float* const* G, const int64_t* idx, int64_t M,
+                       const int64_t* offsets, const float* dV, double* const* dG) {
+  int64_t D = dimD_n(s);
+  for (int k = 0; k < s->L; ++k) memset(dG[k], 0, sizeof(double) * s->T * s->n[k] * slice_len_n(s, k));
+  int64_t* bag = (int64_t*)malloc(sizeof(int64_t) * (M > 0 ? M : 1));
+  if (!offsets) {
+    for (int64_t o = 0; o < M; ++o) bag[o] = o;
+  } else {
+    for (int64_t gb = 0; gb < (int64_t)s->T * s->B; ++gb)
+      for (int64_t o = offsets[gb]; o < offsets[gb + 1]; ++o) bag[o] = gb;
+  }
+  double** X = alloc_chain_n(s);
+  double** dX = alloc_chain_n(s);
+  int64_t dig[ORC_MAXL];
+  int64_t invalid = 0;
+  for (int64_t o = 0; o < M; ++o) {
+    int64_t g = idx[o];
+    if (g < 0 || g >= s->N) {
+      ++invalid;
+      continue;
+    }
+    int64_t gb = bag[o], t = gb / s->B;
+    mixed_radix_n(s, g, dig);
+    chain_n(s, G, t, dig, X);
+    for (int64_t j = 0; j < D; ++j) dX[s->L - 1][j] = (double)dV[gb * D + j];
+    int64_t m = D / s->d[s->L - 1];  /* m_{L-2} */
+    for (int k = s->L - 1; k >= 1; --k) {
+      const float* S = slice_n(s, G[k], k, t, dig[k]);
+      int rk = rank_n(s, k);
+      int64_t cols = (int64_t)s->d[k] * rank_n(s, k + 1);
+      double* dS = dG[k] + (t * s->n[k] + dig[k]) * slice_len_n(s, k);
+      for (int a = 0; a < rk; ++a)
+        for (int64_t c = 0; c < cols; ++c) {
+          double acc = 0.0;
+          for (int64_t r = 0; r < m; ++r) acc += X[k - 1][r * rk + a] * dX[k][r * cols + c];
+          dS[a * cols + c] += acc;
+        }
+      for (int64_t r = 0; r < m; ++r)
+        for (int a = 0; a < rk; ++a) {
+          double acc = 0.0;
+          for (int64_t c = 0; c < cols; ++c) acc += dX[k][r * cols + c] * (double)S[a * cols + c];
+          dX[k - 1][r * rk + a] = acc;
+        }
+      m /= s->d[k - 1];
+    }
+    double* dS0 = dG[0] + (t * s->n[0] + dig[0]) * slice_len_n(s, 0);
+    for (int64_t e = 0; e < slice_len_n(s, 0); ++e) dS0[e] += dX[0][e];
+  }
+  free_chain_n(s, X);
+  free_chain_n(s, dX);
+  free(bag);
+  return invalid;
+}
+
 /* Plain SGD step: out = G - lr * dG (no momentum, no weight decay). */
 void orc_sgd(const float* G, const double* dG, int64_t count, double lr, double* out) {
   for (int64_t i = 0; i < count; ++i) out[i] = (double)G[i] - lr * dG[i];

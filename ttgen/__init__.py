@@ -230,3 +230,43 @@ def math_check_zipf_mass(alpha: float, n: int) -> float:
 __all__ = ["BASE_SEED", "CONFIGS", "make", "tiny", "zipf_bounded", "draw_cores", "bag_lengths",
            "sample_bags", "math_check_zipf_mass"]
 _ = math
+
+
+def core_shapes_n(T: int, n, d, R: int):
+    """Shapes of the L cores of a TT table: core k is [T][n_k][r_k][d_k][r_{k+1}]
+    with r_0 = r_L = 1 (the unit ranks dropped from the shape) and the others R."""
+    L = len(n)
+    shapes = []
+    for k in range(L):
+        s = [T, int(n[k])]
+        if k > 0:
+            s.append(R)
+        s.append(int(d[k]))
+        if k < L - 1:
+            s.append(R)
+        shapes.append(tuple(s))
+    return shapes
+
+
+def tiny_n(seed: int, T: int, n, d, R: int, B: int, max_len: int = 4, sigma: float = 0.5,
+           zipf: float | None = None, grad: bool = True) -> dict:
+    """A small random case with L = len(n) cores (random data only)."""
+    rng = np.random.default_rng([int(seed), 778])
+    n = tuple(int(x) for x in n)
+    d = tuple(int(x) for x in d)
+    N = int(np.prod(n))
+    cores = [(rng.standard_normal(s) * sigma).astype(np.float32) for s in core_shapes_n(T, n, d, R)]
+    lens = rng.integers(0, max_len + 1, size=T * B).astype(np.int64)
+    m = int(lens.sum())
+    if zipf is not None and N > 1:
+        idx = (zipf_bounded(rng, zipf, N, m) - 1).astype(np.int64)
+    else:
+        idx = rng.integers(0, N, size=m, dtype=np.int64)
+    offsets = np.zeros(T * B + 1, dtype=np.int64)
+    np.cumsum(lens, out=offsets[1:])
+    out = dict(workload="tiny_n", T=T, N=N, L=len(n), n=n, d=d, R=R, B=B, cores=cores, idx=idx, offsets=offsets,
+               seed=seed)
+    if grad:
+        out["dV"] = rng.standard_normal((T, B, int(np.prod(d)))).astype(np.float32)
+        out["lr"] = 0.01
+    return out
