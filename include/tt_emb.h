@@ -183,6 +183,79 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
                                   const float* grad_out, float lr, int reuse_grouping, void* workspace,
                                   size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Tables with L TT cores, 2 <= L <= TT_EMB_MAX_CORES.  Eq. 2 splits row g into
+ * L mixed-radix digits (i_0, ..., i_{L-1}), i_0 most significant, and the row
+ * is the chain of the L core slices: X_0 = S_0, X_k = X_{k-1} . S_k with
+ * X_{k-1} viewed as (d_0 ... d_{k-1}) x R, so E = X_{L-1} with output digit
+ * j_0 most significant.  The paper names L > 3 as future work; the prefix of
+ * Section 3.3 becomes the first L-1 digits.
+ *
+ * Core k is [T][n_k][r_k][d_k][r_{k+1}] (float32, row-major) with
+ * r_0 = r_L = 1 and every other rank R: for L = 3 exactly G1, G2, G3 above.
+ * cores and grads are HOST arrays of L device pointers.
+ *
+ * How the library computes it: for L >= 4 a merged first core
+ * [T][n_0...n_{L-3}][d_0...d_{L-3}][R] (the contraction of cores 0..L-3 at
+ * every combination of their digits) is built in the workspace at the start
+ * of each forward and backward call, and the three-core operator runs on it
+ * and cores L-2, L-1: C = (merged slice) . S_{L-2} once per prefix group of
+ * the first L-1 digits, E = C . S_{L-1} per unique row.  The backward carries
+ * the merged core's gradient back through the chain into cores 0..L-3.  For
+ * L = 2 the middle core of the three-core operator is the identity.  Grouping,
+ * reuse levels, schedules, errors and tt_emb_debug_grouping work as above on
+ * the three-factor view (n_0...n_{L-3}, n_{L-2}, n_{L-1}) for L >= 4 and
+ * (n_0, 1, n_1) for L = 2: its digits and prefix keys are those of the view.
+ * ---------------------------------------------------------------------- */
+#define TT_EMB_MAX_CORES 8
+
+typedef struct {
+  int32_t num_tables;                       /* T >= 1 */
+  int64_t num_rows;                         /* N, 1 <= N <= n_0 ... n_{L-1} */
+  int32_t num_cores;                        /* L, 2 <= L <= TT_EMB_MAX_CORES */
+  int32_t row_factors[TT_EMB_MAX_CORES];    /* n_0 .. n_{L-1} >= 1 (entries from L on are ignored) */
+  int32_t dim_factors[TT_EMB_MAX_CORES];    /* d_0 .. d_{L-1} >= 1 */
+  int32_t rank;                             /* R >= 1 */
+  int64_t max_indices;
+  int64_t max_bags;
+} tt_emb_desc_n;
+
+/* Validate `desc` and create a handle for L cores (host memory only).  The
+ * limits of tt_emb_create apply to the three-factor view; in addition
+ * n_0 ... n_{L-1} < 2^32, the merged row product n_0 ... n_{L-3} < 2^28, and
+ * for L >= 4 the chain's on-chip buffers,
+ *   R * (d_0 + d_0 d_1 + ... + d_0 ... d_{L-4} + 2 d_0 ... d_{L-3}) floats,
+ * fit in 64 KiB.  A handle made here with L = 3 is the same as one from
+ * tt_emb_create.  Returns TT_EMB_EINVAL for a bad L, non-positive sizes or
+ * N > n_0 ... n_{L-1}, TT_EMB_EUNSUPPORTED beyond the limits.  The three-core
+ * calls (tt_emb_forward, tt_emb_backward, tt_emb_backward_sgd, tt_emb_sgd)
+ * return TT_EMB_EINVAL on a handle with L != 3; the calls below accept any
+ * handle. */
+tt_emb_status tt_emb_create_n(const tt_emb_desc_n* desc, tt_emb_handle* out);
+
+/* Forward pass with L cores (Section 3.2 with the chain above): out[t][b] is
+ * the sum of the rows of bag t*B+b.  Arguments as for tt_emb_forward; the
+ * workspace also holds the merged core (L >= 4; counted by
+ * tt_emb_workspace_size).  TT_EMB_EINVAL if cores or any cores[k] is NULL or
+ * misaligned. */
+tt_emb_status tt_emb_forward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
+                               int64_t num_indices, const int64_t* offsets, int64_t num_bags, float* out,
+                               int reuse_grouping, void* workspace, size_t ws_bytes, void* stream);
+
+/* Backward pass with L cores (Eq. 1 through every product of the chain):
+ * grads[k] receives the dense gradient of core k (OVERWRITTEN; rows no index
+ * touches are zero).  Gradients of cores 0..L-3 (L >= 4) are summed with
+ * atomics over the merged rows that share a slice.  Arguments as for
+ * tt_emb_backward. */
+tt_emb_status tt_emb_backward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
+                                int64_t num_indices, const int64_t* offsets, int64_t num_bags,
+                                const float* grad_out, float* const* grads, int reuse_grouping, void* workspace,
+                                size_t ws_bytes, void* stream);
+
+/* Plain SGD on the L cores in place: cores[k] -= lr * grads[k]. */
+tt_emb_status tt_emb_sgd_n(tt_emb_handle h, float* const* cores, const float* const* grads, float lr,
+                           void* stream);
+
 /* Synchronise `stream`, read and clear the sticky device error word of
  * `workspace`.  Returns TT_EMB_OK, TT_EMB_ERANGE or TT_EMB_EHIP. */
 tt_emb_status tt_emb_check_errors(tt_emb_handle h, void* workspace, void* stream);
@@ -204,7 +277,9 @@ typedef enum {
   TT_EMB_K_FWD_FUSED = 2, /* forward: C = A.B per prefix group, E = C.D per unique row */
   TT_EMB_K_POOL = 3,      /* forward: sum pooling of E rows into the bags */
   TT_EMB_K_SEG_SUM = 4,   /* backward: dE per unique row, summed over its occurrences */
-  TT_EMB_K_BWD_FUSED = 5  /* backward: per prefix group dD, dC, sum dC, dA, dB */
+  TT_EMB_K_BWD_FUSED = 5, /* backward: per prefix group dD, dC, sum dC, dA, dB */
+  TT_EMB_K_MERGE = 6,     /* L >= 4: merged first core from cores 0..L-3 */
+  TT_EMB_K_SPLIT = 7      /* L >= 4 backward: gradients of cores 0..L-3 from the merged core's */
 } tt_emb_kernel;
 
 /* Benchmark instrumentation.  While set, every launch of `kernel`

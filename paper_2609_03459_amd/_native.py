@@ -17,7 +17,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "tt_emb.h")
 TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED = range(6)
 REUSE = {"prefix": 0, "unique": 1, "none": 2}
 SCHED = {"steal": 0, "static": 1, "steal_ckpt": 2}
-KERNELS = {"ingest": 1, "fwd_fused": 2, "pool": 3, "seg_sum": 4, "bwd_fused": 5}
+KERNELS = {"ingest": 1, "fwd_fused": 2, "pool": 3, "seg_sum": 4, "bwd_fused": 5, "merge": 6, "split": 7}
 
 
 class tt_emb_desc(C.Structure):
@@ -26,6 +26,22 @@ class tt_emb_desc(C.Structure):
         ("num_rows", C.c_int64),
         ("row_factors", C.c_int32 * 3),
         ("dim_factors", C.c_int32 * 3),
+        ("rank", C.c_int32),
+        ("max_indices", C.c_int64),
+        ("max_bags", C.c_int64),
+    ]
+
+
+MAX_CORES = 8
+
+
+class tt_emb_desc_n(C.Structure):
+    _fields_ = [
+        ("num_tables", C.c_int32),
+        ("num_rows", C.c_int64),
+        ("num_cores", C.c_int32),
+        ("row_factors", C.c_int32 * MAX_CORES),
+        ("dim_factors", C.c_int32 * MAX_CORES),
         ("rank", C.c_int32),
         ("max_indices", C.c_int64),
         ("max_bags", C.c_int64),
@@ -56,6 +72,10 @@ _SIG = {
     "tt_emb_profile": ([_P, C.c_int, _P, _P], C.c_int),
     "tt_emb_set_reuse": ([_P, C.c_int], C.c_int),
     "tt_emb_set_schedule": ([_P, C.c_int], C.c_int),
+    "tt_emb_create_n": ([C.POINTER(tt_emb_desc_n), C.POINTER(_P)], C.c_int),
+    "tt_emb_forward_n": ([_P, _P, _P, _I64, _P, _I64, _P, C.c_int, _P, C.c_size_t, _P], C.c_int),
+    "tt_emb_backward_n": ([_P, _P, _P, _I64, _P, _I64, _P, _P, C.c_int, _P, C.c_size_t, _P], C.c_int),
+    "tt_emb_sgd_n": ([_P, _P, _P, C.c_float, _P], C.c_int),
 }
 for _name, (_args, _res) in _SIG.items():
     _f = getattr(lib, _name)
@@ -89,6 +109,33 @@ def tt_emb_create(desc: tt_emb_desc) -> int:
     h = _P()
     check("tt_emb_create", lib.tt_emb_create(C.byref(desc), C.byref(h)))
     return h.value
+
+
+def tt_emb_create_n(desc: tt_emb_desc_n) -> int:
+    h = _P()
+    check("tt_emb_create_n", lib.tt_emb_create_n(C.byref(desc), C.byref(h)))
+    return h.value
+
+
+def ptr_array(ptrs):
+    """Host array of device pointers (cores / grads of the L-core calls)."""
+    arr = (_P * len(ptrs))(*ptrs)
+    return arr
+
+
+def tt_emb_forward_n(h, cores, idx, m, off, nb, out, reuse, ws, ws_bytes, stream) -> None:
+    check("tt_emb_forward_n",
+          lib.tt_emb_forward_n(h, ptr_array(cores), idx, m, off, nb, out, int(reuse), ws, ws_bytes, stream))
+
+
+def tt_emb_backward_n(h, cores, idx, m, off, nb, dv, grads, reuse, ws, ws_bytes, stream) -> None:
+    check("tt_emb_backward_n",
+          lib.tt_emb_backward_n(h, ptr_array(cores), idx, m, off, nb, dv, ptr_array(grads), int(reuse), ws,
+                                ws_bytes, stream))
+
+
+def tt_emb_sgd_n(h, cores, grads, lr, stream) -> None:
+    check("tt_emb_sgd_n", lib.tt_emb_sgd_n(h, ptr_array(cores), ptr_array(grads), float(lr), stream))
 
 
 def tt_emb_destroy(h: int) -> None:

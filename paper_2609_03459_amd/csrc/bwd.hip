@@ -409,11 +409,17 @@ hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const flo
   float* G[3] = {G1, G2, G3};
   const float* d[3] = {dG1, dG2, dG3};
   for (int k = 0; k < 3; ++k) {
-    int64_t blocks = (n[k] / 4 + 255) / 256;
-    if (blocks < 1) blocks = 1;
-    if (blocks > 2048) blocks = 2048;
-    hipLaunchKernelGGL(k_sgd, dim3((unsigned)blocks), dim3(256), 0, st, G[k], d[k], n[k], lr);
+    hipError_t e = launch_sgd1(G[k], d[k], n[k], lr, st);
+    if (e != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st) {
+  int64_t blocks = (n / 4 + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(k_sgd, dim3((unsigned)blocks), dim3(256), 0, st, G, dG, n, lr);
   return hipGetLastError();
 }
 

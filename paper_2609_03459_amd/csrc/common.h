@@ -6,6 +6,8 @@
 
 namespace ttemb {
 
+constexpr int MAX_CORES = 8;  // largest number of TT cores of a handle
+
 // ---------------------------------------------------------------------------
 // Shape and derived constants of one handle.
 // ---------------------------------------------------------------------------
@@ -24,6 +26,15 @@ struct Shape {
   int slice_rows;  // rows per work slice: SLICE_ROWS, or 1 when prefix reuse is off (ablation)
   int dedup;       // 1: exact dedup of rows; 0: every occurrence is its own row (ablation)
   int sched;       // work distribution: SCHED_STEAL, SCHED_STATIC or SCHED_STEAL_CKPT (ablation)
+  // Number of TT cores and their factors.  The fields above are the three-factor
+  // view that the grouping and the fused kernels work on: for L = 3 the cores
+  // themselves; for L >= 4 (n1, d1) = products of the factors of cores 0..L-3,
+  // whose contraction is the merged first core of the view, and (n2, d2),
+  // (n3, d3) those of cores L-2 and L-1; for L = 2 (n1, d1) = core 0, a middle
+  // identity core with n2 = d2 = 1 and (n3, d3) = core 1.
+  int L;
+  int nk[MAX_CORES];
+  int dk[MAX_CORES];
 };
 
 // Counter slots at the head of the workspace (int32).
@@ -86,6 +97,9 @@ struct Work {
   float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
   float* gscratch;        // gradients of the fused backward-and-SGD call on the generic path (core-sized), else null
+  float* g1m;             // L >= 4: merged first core [T][n1][d1][R] of the view; L = 2: identity middle core
+                          // [T][1][R][1][R]; null for L = 3
+  float* dg1m;            // gradient of g1m (same size; for L = 2 computed and discarded)
   float* ckpt;            // [CKPT_SLOTS][d1*d2*R] checkpointed C of the generic kernels (null for the MFMA shape)
   int32_t* ckpt_tag;      // [CKPT_SLOTS] prefix group held by each entry, -1 = none
   int64_t nsl_max, nch_max;
@@ -102,7 +116,7 @@ struct Prof {
   int kernel;
   hipEvent_t begin, end;
 };
-enum : int { K_INGEST = 1, K_FWD_FUSED = 2, K_POOL = 3, K_SEG_SUM = 4, K_BWD_FUSED = 5 };
+enum : int { K_INGEST = 1, K_FWD_FUSED = 2, K_POOL = 3, K_SEG_SUM = 4, K_BWD_FUSED = 5, K_MERGE = 6, K_SPLIT = 7 };
 inline void prof_begin(const Prof& p, int k, hipStream_t st) {
   if (p.kernel == k && p.begin) (void)hipEventRecord(p.begin, st);
 }
@@ -126,6 +140,20 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                            float* dG3, float lr, bool update, const Prof& prof, hipStream_t st);
 hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                       const float* dG3, float lr, hipStream_t st);
+// L-core handles (cores.hip).  cores[k] / grads[k] are the device arrays of core k.
+// Merged first core of the view from cores 0..L-3 (L >= 4), into w.g1m.
+hipError_t launch_merge(const Shape& s, const Work& w, const float* const* cores, const Prof& prof, hipStream_t st);
+// Gradients of cores 0..L-3 from the merged core's gradient w.dg1m (L >= 4); zeroes them first.
+hipError_t launch_split(const Shape& s, const Work& w, const float* const* cores, float* const* grads,
+                        const Prof& prof, hipStream_t st);
+// Identity middle core of an L = 2 handle, into w.g1m.
+hipError_t launch_identity(const Shape& s, const Work& w, hipStream_t st);
+// Element count of core k.
+int64_t core_elems(const Shape& s, int k);
+// LDS floats of the merge and split kernels (0 when L < 4).
+int64_t chain_lds_floats(const Shape& s);
+// G -= lr * dG on n floats.
+hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.
 bool bwd_r32_supported(const Shape& s, int64_t max_indices);
 // Whether the MFMA forward serves this shape.

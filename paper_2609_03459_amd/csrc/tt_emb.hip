@@ -88,6 +88,14 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
                                       (size_t)s.n3 * s.R * s.d3);
   W->gscratch = (float*)take(bwd_r32 ? 0 : 4 * ncore);
   if (bwd_r32) W->gscratch = nullptr;
+  // merged first core (L >= 4) or identity middle core (L = 2), and its gradient
+  const size_t nmerged = s.L >= 4 ? (size_t)s.T * s.n1 * s.d1 * s.R : (s.L == 2 ? (size_t)s.T * s.R * s.R : 0);
+  W->g1m = (float*)take(4 * nmerged);
+  W->dg1m = (float*)take(4 * nmerged);
+  if (!nmerged) {
+    W->g1m = nullptr;
+    W->dg1m = nullptr;
+  }
   const bool generic = !bwd_r32 || !fwd_r32_supported(s, m);
   const size_t nC = (size_t)s.d1 * s.d2 * s.R;
   W->ckpt = (float*)take(generic ? 4 * CKPT_SLOTS * nC : 0);
@@ -151,13 +159,10 @@ const char* tt_emb_status_string(tt_emb_status s) {
   return "unknown status";
 }
 
-tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
-  if (!d || !out) return TT_EMB_EINVAL;
-  *out = nullptr;
-  if (d->num_tables < 1 || d->num_rows < 1 || d->rank < 1 || d->max_indices < 0 || d->max_bags < 0)
-    return TT_EMB_EINVAL;
-  for (int k = 0; k < 3; ++k)
-    if (d->row_factors[k] < 1 || d->dim_factors[k] < 1) return TT_EMB_EINVAL;
+// Validate the three-factor view `d` of a shape with L cores of factors nk, dk
+// and create its handle.
+static tt_emb_status create_view(const tt_emb_desc* d, int L, const int32_t* nk, const int32_t* dk,
+                                 tt_emb_handle* out) {
   const uint64_t npad = (uint64_t)d->row_factors[0] * d->row_factors[1] * d->row_factors[2];
   if ((uint64_t)d->num_rows > npad) return TT_EMB_EINVAL;
   const uint64_t T = (uint64_t)d->num_tables;
@@ -190,6 +195,15 @@ tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
   s.slice_rows = SLICE_ROWS;
   s.dedup = 1;
   s.sched = SCHED_STEAL;
+  s.L = L;
+  for (int k = 0; k < MAX_CORES; ++k) {
+    s.nk[k] = k < L ? nk[k] : 1;
+    s.dk[k] = k < L ? dk[k] : 1;
+  }
+  if (chain_lds_floats(s) * 4 > 65536) {
+    delete h;
+    return TT_EMB_EUNSUPPORTED;
+  }
   h->g_valid = false;
   h->prof.kernel = 0;
   h->prof.begin = nullptr;
@@ -198,8 +212,63 @@ tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
   return TT_EMB_OK;
 }
 
+tt_emb_status tt_emb_create(const tt_emb_desc* d, tt_emb_handle* out) {
+  if (!d || !out) return TT_EMB_EINVAL;
+  *out = nullptr;
+  if (d->num_tables < 1 || d->num_rows < 1 || d->rank < 1 || d->max_indices < 0 || d->max_bags < 0)
+    return TT_EMB_EINVAL;
+  for (int k = 0; k < 3; ++k)
+    if (d->row_factors[k] < 1 || d->dim_factors[k] < 1) return TT_EMB_EINVAL;
+  return create_view(d, 3, d->row_factors, d->dim_factors, out);
+}
+
+tt_emb_status tt_emb_create_n(const tt_emb_desc_n* d, tt_emb_handle* out) {
+  if (!d || !out) return TT_EMB_EINVAL;
+  *out = nullptr;
+  const int L = d->num_cores;
+  if (L < 2 || L > TT_EMB_MAX_CORES || d->num_tables < 1 || d->num_rows < 1 || d->rank < 1 ||
+      d->max_indices < 0 || d->max_bags < 0)
+    return TT_EMB_EINVAL;
+  uint64_t npad = 1, dprod = 1;
+  for (int k = 0; k < L; ++k) {
+    if (d->row_factors[k] < 1 || d->dim_factors[k] < 1) return TT_EMB_EINVAL;
+    npad *= (uint64_t)d->row_factors[k];
+    dprod *= (uint64_t)d->dim_factors[k];
+    if (npad >= (1ull << 32) || dprod > 4096) return TT_EMB_EUNSUPPORTED;
+  }
+  if ((uint64_t)d->num_rows > npad) return TT_EMB_EINVAL;
+  tt_emb_desc v;
+  v.num_tables = d->num_tables;
+  v.num_rows = d->num_rows;
+  v.rank = d->rank;
+  v.max_indices = d->max_indices;
+  v.max_bags = d->max_bags;
+  if (L == 2) {
+    v.row_factors[0] = d->row_factors[0];
+    v.row_factors[1] = 1;
+    v.row_factors[2] = d->row_factors[1];
+    v.dim_factors[0] = d->dim_factors[0];
+    v.dim_factors[1] = 1;
+    v.dim_factors[2] = d->dim_factors[1];
+  } else {
+    int64_t n1 = 1, d1 = 1;
+    for (int k = 0; k + 2 < L; ++k) {
+      n1 *= d->row_factors[k];
+      d1 *= d->dim_factors[k];
+    }
+    if (n1 >= (1 << 28)) return TT_EMB_EUNSUPPORTED;
+    v.row_factors[0] = (int32_t)n1;
+    v.row_factors[1] = d->row_factors[L - 2];
+    v.row_factors[2] = d->row_factors[L - 1];
+    v.dim_factors[0] = (int32_t)d1;
+    v.dim_factors[1] = d->dim_factors[L - 2];
+    v.dim_factors[2] = d->dim_factors[L - 1];
+  }
+  return create_view(&v, L, d->row_factors, d->dim_factors, out);
+}
+
 tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* ev_end) {
-  if (!h || kernel < TT_EMB_K_NONE || kernel > TT_EMB_K_BWD_FUSED) return TT_EMB_EINVAL;
+  if (!h || kernel < TT_EMB_K_NONE || kernel > TT_EMB_K_SPLIT) return TT_EMB_EINVAL;
   const bool off = kernel == TT_EMB_K_NONE || !ev_begin || !ev_end;
   h->prof.kernel = off ? 0 : kernel;
   h->prof.begin = off ? nullptr : (hipEvent_t)ev_begin;
@@ -277,6 +346,7 @@ tt_emb_status tt_emb_group(tt_emb_handle h, const int64_t* indices, int64_t num_
 tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
                              const int64_t* indices, int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                              float* out, int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
+  if (h && h->s.L != 3) return TT_EMB_EINVAL;
   tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || (!out && num_bags > 0)) return TT_EMB_EINVAL;
@@ -297,6 +367,7 @@ tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2,
                               const int64_t* indices, int64_t num_indices, const int64_t* offsets,
                               int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
                               int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
+  if (h && h->s.L != 3) return TT_EMB_EINVAL;
   tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
@@ -321,6 +392,7 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
                                   int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                                   const float* grad_out, float lr, int reuse_grouping, void* workspace,
                                   size_t ws_bytes, void* stream) {
+  if (h && h->s.L != 3) return TT_EMB_EINVAL;
   tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
@@ -340,10 +412,96 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
 
 tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                          const float* dG3, float lr, void* stream) {
-  if (!h || !G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3) return TT_EMB_EINVAL;
+  if (!h || h->s.L != 3 || !G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3) return TT_EMB_EINVAL;
   if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(dG1, 16) || !al(dG2, 16) || !al(dG3, 16))
     return TT_EMB_EINVAL;
   return hip_status(launch_sgd(h->s, G1, G2, G3, dG1, dG2, dG3, lr, (hipStream_t)stream));
+}
+
+static bool cores_ok(tt_emb_handle h, const float* const* p) {
+  if (!p) return false;
+  for (int k = 0; k < h->s.L; ++k)
+    if (!p[k] || !al(p[k], 16)) return false;
+  return true;
+}
+
+static tt_emb_status group_or_reuse(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets,
+                                    int64_t B, void* ws, int reuse_grouping, hipStream_t s) {
+  if (reuse_grouping) return grouping_matches(h, idx, M, offsets, B, ws) ? TT_EMB_OK : TT_EMB_EINVAL;
+  return do_group(h, idx, M, offsets, B, ws, s);
+}
+
+tt_emb_status tt_emb_forward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
+                               int64_t num_indices, const int64_t* offsets, int64_t num_bags, float* out,
+                               int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  if (!cores_ok(h, cores) || (!out && num_bags > 0) || !al(out, 16)) return TT_EMB_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = group_or_reuse(h, indices, num_indices, offsets, num_bags, workspace, reuse_grouping, s)) != TT_EMB_OK)
+    return st;
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  const int L = h->s.L;
+  const float *G1 = cores[0], *G2 = cores[1], *G3 = cores[L - 1];
+  hipError_t e = hipSuccess;
+  if (L == 2) {
+    e = launch_identity(h->s, w, s);
+    G2 = w.g1m;
+  } else if (L >= 4) {
+    e = launch_merge(h->s, w, cores, h->prof, s);
+    G1 = w.g1m;
+    G2 = cores[L - 2];
+  }
+  if (e != hipSuccess) return TT_EMB_EHIP;
+  return hip_status(launch_forward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, out, h->prof, s));
+}
+
+tt_emb_status tt_emb_backward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
+                                int64_t num_indices, const int64_t* offsets, int64_t num_bags, const float* grad_out,
+                                float* const* grads, int reuse_grouping, void* workspace, size_t ws_bytes,
+                                void* stream) {
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  if (st != TT_EMB_OK) return st;
+  if (!cores_ok(h, cores) || !cores_ok(h, (const float* const*)grads) || (!grad_out && num_bags > 0) ||
+      !al(grad_out, 16))
+    return TT_EMB_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = group_or_reuse(h, indices, num_indices, offsets, num_bags, workspace, reuse_grouping, s)) != TT_EMB_OK)
+    return st;
+  Work w;
+  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  const int L = h->s.L;
+  const float *G1 = cores[0], *G2 = cores[1], *G3 = cores[L - 1];
+  float *dG1 = grads[0], *dG2 = grads[1], *dG3 = grads[L - 1];
+  hipError_t e = hipSuccess;
+  if (L == 2) {
+    e = launch_identity(h->s, w, s);
+    G2 = w.g1m;
+    dG2 = w.dg1m;
+  } else if (L >= 4) {
+    e = launch_merge(h->s, w, cores, h->prof, s);
+    G1 = w.g1m;
+    G2 = cores[L - 2];
+    dG1 = w.dg1m;
+    dG2 = grads[L - 2];
+  }
+  if (e != hipSuccess) return TT_EMB_EHIP;
+  e = launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, dG1, dG2, dG3, 0.f, false,
+                      h->prof, s);
+  if (e != hipSuccess) return TT_EMB_EHIP;
+  if (L >= 4) return hip_status(launch_split(h->s, w, cores, grads, h->prof, s));
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_sgd_n(tt_emb_handle h, float* const* cores, const float* const* grads, float lr,
+                           void* stream) {
+  if (!h || !cores_ok(h, (const float* const*)cores) || !cores_ok(h, grads)) return TT_EMB_EINVAL;
+  for (int k = 0; k < h->s.L; ++k) {
+    hipError_t e = launch_sgd1(cores[k], grads[k], core_elems(h->s, k), lr, (hipStream_t)stream);
+    if (e != hipSuccess) return TT_EMB_EHIP;
+  }
+  return TT_EMB_OK;
 }
 
 tt_emb_status tt_emb_check_errors(tt_emb_handle h, void* workspace, void* stream) {

@@ -116,3 +116,78 @@ def test_reuse_levels_and_workspace(N):
     assert sizes["unique"] >= base and sizes["none"] >= sizes["unique"]
     N.tt_emb_destroy(h)
 
+
+
+def _desc_n(N, L=4, T=2, n=(3, 4, 5, 2), d=(2, 2, 2, 1), R=4, M=100, B=10, rows=None):
+    x = N.tt_emb_desc_n()
+    x.num_tables = T
+    x.num_cores = L
+    x.num_rows = rows if rows is not None else int(__import__("numpy").prod(n[:L]))
+    for k in range(min(len(n), N.MAX_CORES)):
+        x.row_factors[k] = n[k]
+        x.dim_factors[k] = d[k]
+    x.rank = R
+    x.max_indices = M
+    x.max_bags = B
+    return x
+
+
+def test_create_n_shapes_and_workspace(N):
+    # L = 3 through create_n is the three-core handle
+    h3 = N.tt_emb_create(_desc(N))
+    h3n = N.tt_emb_create_n(_desc_n(N, L=3, n=(3, 4, 5), d=(2, 2, 2)))
+    assert N.tt_emb_workspace_size(h3) == N.tt_emb_workspace_size(h3n)
+    # L = 4 and L = 2 need room for the merged / identity core and its gradient
+    h4 = N.tt_emb_create_n(_desc_n(N))
+    h2 = N.tt_emb_create_n(_desc_n(N, L=2, n=(12, 10), d=(4, 2)))
+    assert N.tt_emb_workspace_size(h4) > 0 and N.tt_emb_workspace_size(h2) > 0
+    h8 = N.tt_emb_create_n(_desc_n(N, L=8, n=(2,) * 8, d=(1, 2, 1, 2, 1, 2, 1, 2)))
+    for h in (h3, h3n, h4, h2, h8):
+        N.tt_emb_destroy(h)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=1), 1), (dict(L=9), 1), (dict(L=0), 1), (dict(T=0), 1), (dict(R=0), 1),
+    (dict(n=(3, 0, 5, 2)), 1), (dict(d=(1, 1, -1, 1)), 1), (dict(rows=121), 1),
+    (dict(n=(1000, 1000, 1000, 10)), 5), (dict(d=(16, 16, 16, 2)), 5), (dict(R=65), 5),
+    # chain buffers beyond 64 KiB: R * (d0 + d0 d1 + 2 d0 d1 d2) floats
+    (dict(L=5, n=(2, 2, 2, 2, 2), d=(8, 8, 2, 1, 1), R=64), 5),
+])
+def test_create_n_rejects_bad_shapes(N, kw, code):
+    h = C.c_void_p()
+    assert N.lib.tt_emb_create_n(C.byref(_desc_n(N, **kw)), C.byref(h)) == code
+    assert not h.value
+    assert N.lib.tt_emb_create_n(None, C.byref(h)) == N.TT_EMB_EINVAL
+
+
+def test_calls_n_reject_bad_arguments_without_launching(N):
+    h = N.tt_emb_create_n(_desc_n(N, T=2, M=100, B=10))
+    ws_bytes = N.tt_emb_workspace_size(h)
+    fake = 1 << 20
+    off = fake
+    E = N.TT_EMB_EINVAL
+    cores = N.ptr_array([fake] * 4)
+    short = N.ptr_array([fake, fake, None, fake])
+    mis = N.ptr_array([fake, fake, fake + 4, fake])
+    f = N.lib.tt_emb_forward_n
+    assert f(h, None, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, short, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, mis, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert f(h, cores, fake, 20, off, 10, None, 0, fake, ws_bytes, None) == E
+    assert f(h, cores, fake, 20, off, 10, fake, 0, fake, ws_bytes - 1, None) == E
+    assert f(h, cores, fake, 20, off, 10, fake, 1, fake, ws_bytes, None) == E  # no grouping yet
+    b = N.lib.tt_emb_backward_n
+    assert b(h, cores, fake, 20, off, 10, fake, None, 0, fake, ws_bytes, None) == E
+    assert b(h, cores, fake, 20, off, 10, fake, short, 0, fake, ws_bytes, None) == E
+    assert b(h, cores, fake, 20, off, 10, None, cores, 0, fake, ws_bytes, None) == E
+    assert N.lib.tt_emb_sgd_n(h, cores, mis, C.c_float(0.1), None) == E
+    assert N.lib.tt_emb_sgd_n(None, cores, cores, C.c_float(0.1), None) == E
+    # the three-core calls refuse a handle with four cores
+    lr = C.c_float(0.1)
+    assert N.lib.tt_emb_forward(h, fake, fake, fake, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
+    assert N.lib.tt_emb_backward(h, fake, fake, fake, fake, 20, off, 10, fake, fake, fake, fake, 0, fake,
+                                 ws_bytes, None) == E
+    assert N.lib.tt_emb_backward_sgd(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes,
+                                     None) == E
+    assert N.lib.tt_emb_sgd(h, fake, fake, fake, fake, fake, fake, lr, None) == E
+    N.tt_emb_destroy(h)
