@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA = 157.3e12  # MI355X dense FP32 matrix FLOP/s
 PEAK_HBM = 8.0e12          # MI355X HBM3E bytes/s
+PEAK_FP32_VALU = 157.3e12  # MI355X FP32 vector FLOP/s
 METRIC = "TT-embedding lookups/s + batch-32768 fwd/bwd latency (ms), % of roofline"
 
 
@@ -69,10 +70,39 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+# Factorisations of the 10^7-row, D = 128 tables over L cores (--cores); for
+# L >= 4 the first L-2 cores merge into a first core of (4, ...) columns, so the
+# fused kernels see the same (4, 4, 8), R = 32 shape as with three cores.
+CORE_SPLITS = {
+    2: ((4000, 2500), (16, 8)),
+    3: ((200, 200, 250), (4, 4, 8)),
+    4: ((20, 10, 200, 250), (2, 2, 4, 8)),
+    5: ((10, 20, 10, 20, 250), (2, 2, 1, 4, 8)),
+}
+
+
+def view_dims(n, d):
+    """Three-factor view (rows, columns) that the grouping and fused kernels use."""
+    L = len(n)
+    if L == 2:
+        return (n[0], 1, n[1]), (d[0], 1, d[1])
+    p = lambda xs: int(__import__("numpy").prod(xs))
+    return (p(n[:L - 2]), n[L - 2], n[L - 1]), (p(d[:L - 2]), d[L - 2], d[L - 1])
+
+
+def chain_flops(n, d, R):
+    """Flops of one merged-core row (L >= 4): the products S_0 . S_1 ... S_{L-3}."""
+    m, f = d[0], 0.0
+    for k in range(1, len(n) - 2):
+        f += 2.0 * m * R * d[k] * R
+        m *= d[k]
+    return f
+
+
 def algorithmic_work(kernel, case, counts):
     """(amount, unit, bound) per launch of `kernel` from the workload and its grouping."""
     T, B, R = case["T"], case["B"], case["R"]
-    d1, d2, d3 = case["d"]
+    _, (d1, d2, d3) = view_dims(case["n"], case["d"])
     D = d1 * d2 * d3
     U, P, nv = counts["U"], counts["P"], counts["nvalid"]
     M = int(case["idx"].size)
@@ -87,6 +117,11 @@ def algorithmic_work(kernel, case, counts):
         return 4.0 * NB * D + 4.0 * U * D + 12.0 * nv + 4.0 * (U + 1), "byte", "hbm"
     if kernel == "ingest":
         return 8.0 * M + 8.0 * (NB + 1) + 12.0 * M, "byte", "hbm"
+    (n1, _, _), _ = view_dims(case["n"], case["d"])
+    if kernel == "merge":
+        return T * n1 * chain_flops(case["n"], case["d"], R), "flop", "alu"
+    if kernel == "split":  # two products per chain step, on every merged row
+        return T * n1 * 2.0 * chain_flops(case["n"], case["d"], R), "flop", "alu"
     raise ValueError(kernel)
 
 
@@ -167,16 +202,24 @@ def cpu_baseline(case, target_s):
 
     def run(c):
         t0 = time.perf_counter()
-        oracle.forward(c)
-        oracle.backward(c)
+        if "cores" in c:
+            oracle.forward_n(c)
+            oracle.backward_n(c)
+        else:
+            oracle.forward(c)
+            oracle.backward(c)
         return time.perf_counter() - t0
 
     def table(c, t):  # table t of a sample as a one-table case
         nb = c["B"]
         o = c["offsets"]
         lo, hi = o[t * nb], o[(t + 1) * nb]
-        return dict(c, T=1, G1=c["G1"][t:t + 1], G2=c["G2"][t:t + 1], G3=c["G3"][t:t + 1],
-                    idx=c["idx"][lo:hi], offsets=o[t * nb:(t + 1) * nb + 1] - lo, dV=c["dV"][t:t + 1])
+        one = dict(c, T=1, idx=c["idx"][lo:hi], offsets=o[t * nb:(t + 1) * nb + 1] - lo, dV=c["dV"][t:t + 1])
+        if "cores" in c:
+            one["cores"] = [G[t:t + 1] for G in c["cores"]]
+        else:
+            one.update(G1=c["G1"][t:t + 1], G2=c["G2"][t:t + 1], G3=c["G3"][t:t + 1])
+        return one
 
     probe = sub(8)
     dt = run(probe)
@@ -213,6 +256,11 @@ def main():
     ap.add_argument("--sched", choices=["steal", "static", "steal_ckpt"], default="steal",
                     help="work distribution (ablation of Section 4.4): stealing (default), static shares, "
                          "stealing with checkpointed intermediates")
+    ap.add_argument("--cores", type=int, choices=sorted(CORE_SPLITS), default=3,
+                    help="number of TT cores: the same tables factorised over L cores (L > 3: future work in "
+                         "the paper)")
+    ap.add_argument("--row-factors", default=None, help="comma-separated row factors (overrides --cores)")
+    ap.add_argument("--dim-factors", default=None, help="comma-separated column factors (with --row-factors)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
@@ -235,13 +283,33 @@ def main():
     import ttgen
 
     case = ttgen.make(args.config, with_grad=True)
+    if args.row_factors or args.cores != 3:
+        if args.row_factors:
+            nL = tuple(int(x) for x in args.row_factors.split(","))
+            dL = tuple(int(x) for x in args.dim_factors.split(","))
+        else:
+            nL, dL = CORE_SPLITS[args.cores]
+        if int(np.prod(nL)) < case["N"] or int(np.prod(dL)) != int(np.prod(case["d"])):
+            sys.exit(f"factors {nL} x {dL} do not hold {case['N']} rows of {int(np.prod(case['d']))} columns")
+        rng = np.random.default_rng([int(case["seed"]), 4242])
+        # random cores of the same spread as the three-core recipe's, per core
+        sig = float(np.std(case["G2"]))
+        case = dict(case, n=nL, d=dL, L=len(nL), workload=case["workload"] + f"_{len(nL)}cores",
+                    cores=[(rng.standard_normal(sh) * sig).astype(np.float32)
+                           for sh in ttgen.core_shapes_n(case["T"], nL, dL, case["R"])])
+        for k in ("G1", "G2", "G3"):
+            case.pop(k)
     T, n, d, R, B = case["T"], case["n"], case["d"], case["R"], case["B"]
-    D = d[0] * d[1] * d[2]
+    L = len(n)
+    D = int(np.prod(d))
     M = int(case["idx"].size)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     emb = P.TTEmbedding(T, case["N"], n, d, R, max_indices=M, max_bags=B, reuse=args.reuse, sched=args.sched)
-    G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
+    if "cores" in case:
+        G = [torch.from_numpy(x).to(dev) for x in case["cores"]]
+    else:
+        G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
     idx = torch.from_numpy(case["idx"]).to(dev)
     off = None if case["offsets"] is None else torch.from_numpy(case["offsets"]).to(dev)
     dV = torch.from_numpy(case["dV"]).to(dev)
@@ -251,10 +319,29 @@ def main():
     stream = torch.cuda.current_stream().cuda_stream
     ev = HipEvents()
 
+    if "cores" in case:
+        def fwd(reuse):
+            emb.forward_n(G, idx, off, num_bags=B, out=out, reuse_grouping=reuse)
+
+        def bwd():
+            emb.backward_n(G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
+
+        def sgd():
+            emb.sgd_n(G, grads, lr)
+    else:
+        def fwd(reuse):
+            emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=reuse)
+
+        def bwd():
+            emb.backward(*G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
+
+        def sgd():
+            emb.sgd(*G, *grads, lr)
+
     def step():
-        emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=False)
-        emb.backward(*G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
-        emb.sgd(*G, *grads, lr)
+        fwd(False)
+        bwd()
+        sgd()
 
     if args.copy_mib:
         # reads and writes exactly copy_mib MiB each: the calibration of the byte counters
@@ -265,7 +352,7 @@ def main():
         del x, y
 
     # warmup; the first steps also time each candidate kernel once
-    kernels = list(P.N.KERNELS)
+    kernels = [k for k in P.N.KERNELS if L >= 4 or k not in ("merge", "split")]
     kernel_ms = {}
     e0, e1 = ev.create(), ev.create()
     for w in range(max(args.warmup, len(kernels))):
@@ -322,11 +409,11 @@ def main():
         ev.record(pe[0], stream)
         emb.group(idx, off, num_bags=B)
         ev.record(pe[1], stream)
-        emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=True)
+        fwd(True)
         ev.record(pe[2], stream)
-        emb.backward(*G, idx, off, dV, num_bags=B, grads=grads, reuse_grouping=True)
+        bwd()
         ev.record(pe[3], stream)
-        emb.sgd(*G, *grads, lr)
+        sgd()
         ev.record(pe[4], stream)
         torch.cuda.synchronize()
         for j, name in enumerate(phases):
@@ -334,7 +421,11 @@ def main():
     phases_ms = {k: round(float(np.median(v)), 4) for k, v in phases.items()}
 
     work, unit, bound = algorithmic_work(dominant, case, counts)
-    if unit == "flop":
+    if unit == "flop" and bound == "alu":
+        achieved = work / (dom_ms * 1e-3) / 1e12
+        roof = dict(bound=bound, achieved=round(achieved, 3), peak=PEAK_FP32_VALU / 1e12, unit="TFLOP/s",
+                    frac=round(achieved / (PEAK_FP32_VALU / 1e12), 4))
+    elif unit == "flop":
         achieved = work / (dom_ms * 1e-3) / 1e12
         roof = dict(bound=bound, achieved=round(achieved, 3), peak=PEAK_FP32_MFMA / 1e12, unit="TFLOP/s",
                     frac=round(achieved / (PEAK_FP32_MFMA / 1e12), 4))
@@ -365,7 +456,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "row_factors": list(n),
+        "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "cores": L,
+                   "row_factors": list(n),
                    "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
                    "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu",
                    "reuse": args.reuse, "sched": args.sched},
