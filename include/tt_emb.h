@@ -198,11 +198,14 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
  * How the library computes it: for L >= 4 a merged first core
  * [T][n_0...n_{L-3}][d_0...d_{L-3}][R] (the contraction of cores 0..L-3 at
  * every combination of their digits) is built in the workspace at the start
- * of each forward and backward call, and the three-core operator runs on it
- * and cores L-2, L-1: C = (merged slice) . S_{L-2} once per prefix group of
- * the first L-1 digits, E = C . S_{L-1} per unique row.  The backward carries
- * the merged core's gradient back through the chain into cores 0..L-3.  For
- * L = 2 the middle core of the three-core operator is the identity.  Grouping,
+ * of each forward and backward call, one level of the chain at a time (each
+ * partial product S_0 ... S_k built once per distinct prefix of k+1 digits),
+ * and the three-core operator runs on it and cores L-2, L-1:
+ * C = (merged slice) . S_{L-2} once per prefix group of the first L-1 digits,
+ * E = C . S_{L-1} per unique row.  The backward carries the merged core's
+ * gradient back through the chain one level at a time, with plain sums (no
+ * atomics), into cores 0..L-3.  For L = 2 the middle core of the three-core
+ * operator is the identity.  Grouping,
  * reuse levels, schedules, errors and tt_emb_debug_grouping work as above on
  * the three-factor view (n_0...n_{L-3}, n_{L-2}, n_{L-1}) for L >= 4 and
  * (n_0, 1, n_1) for L = 2: its digits and prefix keys are those of the view.
@@ -222,10 +225,8 @@ typedef struct {
 
 /* Validate `desc` and create a handle for L cores (host memory only).  The
  * limits of tt_emb_create apply to the three-factor view; in addition
- * n_0 ... n_{L-1} < 2^32, the merged row product n_0 ... n_{L-3} < 2^28, and
- * for L >= 4 the chain's on-chip buffers,
- *   R * (d_0 + d_0 d_1 + ... + d_0 ... d_{L-4} + 2 d_0 ... d_{L-3}) floats,
- * fit in 64 KiB.  A handle made here with L = 3 is the same as one from
+ * n_0 ... n_{L-1} < 2^32 and the merged row product n_0 ... n_{L-3} < 2^28.
+ * A handle made here with L = 3 is the same as one from
  * tt_emb_create.  Returns TT_EMB_EINVAL for a bad L, non-positive sizes or
  * N > n_0 ... n_{L-1}, TT_EMB_EUNSUPPORTED beyond the limits.  The three-core
  * calls (tt_emb_forward, tt_emb_backward, tt_emb_backward_sgd, tt_emb_sgd)
@@ -244,9 +245,7 @@ tt_emb_status tt_emb_forward_n(tt_emb_handle h, const float* const* cores, const
 
 /* Backward pass with L cores (Eq. 1 through every product of the chain):
  * grads[k] receives the dense gradient of core k (OVERWRITTEN; rows no index
- * touches are zero).  Gradients of cores 0..L-3 (L >= 4) are summed with
- * atomics over the merged rows that share a slice.  Arguments as for
- * tt_emb_backward. */
+ * touches are zero).  Arguments as for tt_emb_backward. */
 tt_emb_status tt_emb_backward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
                                 int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                                 const float* grad_out, float* const* grads, int reuse_grouping, void* workspace,

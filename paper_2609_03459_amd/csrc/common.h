@@ -100,6 +100,8 @@ struct Work {
   float* g1m;             // L >= 4: merged first core [T][n1][d1][R] of the view; L = 2: identity middle core
                           // [T][1][R][1][R]; null for L = 3
   float* dg1m;            // gradient of g1m (same size; for L = 2 computed and discarded)
+  float* xlev;            // L >= 5: partial products of the merged cores' inner levels, chain_level_floats(s)
+  float* dxlev;           // L >= 5: their gradients (same size)
   float* ckpt;            // [CKPT_SLOTS][d1*d2*R] checkpointed C of the generic kernels (null for the MFMA shape)
   int32_t* ckpt_tag;      // [CKPT_SLOTS] prefix group held by each entry, -1 = none
   int64_t nsl_max, nch_max;
@@ -141,17 +143,18 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
 hipError_t launch_sgd(const Shape& s, float* G1, float* G2, float* G3, const float* dG1, const float* dG2,
                       const float* dG3, float lr, hipStream_t st);
 // L-core handles (cores.hip).  cores[k] / grads[k] are the device arrays of core k.
-// Merged first core of the view from cores 0..L-3 (L >= 4), into w.g1m.
+// Merged first core of the view from cores 0..L-3 (L >= 4), level by level, into w.g1m.
 hipError_t launch_merge(const Shape& s, const Work& w, const float* const* cores, const Prof& prof, hipStream_t st);
-// Gradients of cores 0..L-3 from the merged core's gradient w.dg1m (L >= 4); zeroes them first.
+// Gradients of cores 0..L-3 from the merged core's gradient w.dg1m (L >= 4), level by level
+// (reads the levels launch_merge left in w; overwrites the gradients).
 hipError_t launch_split(const Shape& s, const Work& w, const float* const* cores, float* const* grads,
                         const Prof& prof, hipStream_t st);
 // Identity middle core of an L = 2 handle, into w.g1m.
 hipError_t launch_identity(const Shape& s, const Work& w, hipStream_t st);
 // Element count of core k.
 int64_t core_elems(const Shape& s, int k);
-// LDS floats of the merge and split kernels (0 when L < 4).
-int64_t chain_lds_floats(const Shape& s);
+// Floats of the inner partial-product levels of the merged cores (0 when L < 5).
+int64_t chain_level_floats(const Shape& s);
 // G -= lr * dG on n floats.
 hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.

@@ -6,50 +6,49 @@
 // The grouping and the fused kernels work on a three-factor view of the shape.
 // For L >= 4 the first L-2 cores are contracted into a merged first core
 //     G1m[t][i1'] = S_0 . S_1 . ... . S_{L-3}   (d1' x R, d1' = d_0 ... d_{L-3})
-// for every i1' = (i_0, ..., i_{L-3}) of every table (k_merge).  Cores L-2 and
-// L-1 are the view's second and third cores, so per prefix group the fused
-// forward builds C = G1m[i1'] . S_{L-2} once and E = C . S_{L-1} per row, as
-// for three cores: the prefix is the first L-1 digits, and the product of the
-// first L-2 digits is built once per distinct value rather than once per group.
-// The backward of the view yields dG1m; k_split carries it back through the
-// chain (Eq. 1 applied to each product in turn) into the gradients of cores
-// 0..L-3.  For L = 2 the view's middle core is the identity.
+// for every i1' = (i_0, ..., i_{L-3}) of every table.  Cores L-2 and L-1 are
+// the view's second and third cores, so per prefix group the fused forward
+// builds C = G1m[i1'] . S_{L-2} once and E = C . S_{L-1} per row, as for three
+// cores: the prefix is the first L-1 digits, and the product of the first L-2
+// digits is built once per distinct value rather than once per group.  The
+// backward of the view yields dG1m, which goes back through the chain (Eq. 1
+// applied to each product in turn) into the gradients of cores 0..L-3.  For
+// L = 2 the view's middle core is the identity.
 #include "common.h"
 
 namespace ttemb {
 
-constexpr int CH_THREADS = 128;
+constexpr int LV_THREADS = 256;
 
-struct ChainArgs {
-  int T, K, R;        // K = L - 2 merged cores
-  int n1v, d1v;       // their row and column products
-  int n[MAX_CORES];   // row factors of the merged cores
-  int d[MAX_CORES];   // column factors
-  int rstride[MAX_CORES];  // digit k of i1' is (i1' / rstride[k]) mod n[k]
+// Per table, level k (k = 0..K-1, K = L-2 merged cores) holds the partial
+// product X_k(q) = S_0[i_0] . ... . S_k[i_k] of every prefix q = (i_0, ..., i_k)
+// of the merged digits: P_{k+1} = n_0 ... n_k rows of m_k x R floats,
+// m_k = d_0 ... d_k.  Level 0 is core 0 itself and level K-1 is the merged core.
+// Each level is built once from its parent level (prefix reuse down the chain),
+// and the gradient goes back one level at a time:
+//   dS_k[c]      = sum over parents p of X_{k-1}(p)^T . dX_k(p n_k + c)
+//   dX_{k-1}(p)  = sum over children c of dX_k(p n_k + c) . S_k[c]^T
+// with dX_{K-1} the merged core's gradient and dS_0 = dX_0.
+struct LevelArgs {
+  int T, R;
+  int nk;         // children per parent: n_k
+  int64_t P;      // parents per table: P_k = n_0 ... n_{k-1}
+  int mprev;      // rows of a parent product: m_{k-1}
+  int cols;       // d_k R
 };
 
-struct CorePtrs {
-  const float* p[MAX_CORES];
-};
-struct GradPtrs {
-  float* p[MAX_CORES];
-};
-
-static ChainArgs chain_args(const Shape& s) {
-  ChainArgs a;
+static LevelArgs level_args(const Shape& s, int k) {
+  LevelArgs a;
   a.T = s.T;
-  a.K = s.L - 2;
   a.R = s.R;
-  a.n1v = s.n1;
-  a.d1v = s.d1;
-  int stride = 1;
-  for (int k = MAX_CORES - 1; k >= 0; --k) {
-    const bool in = k < a.K;
-    a.n[k] = in ? s.nk[k] : 1;
-    a.d[k] = in ? s.dk[k] : 1;
-    a.rstride[k] = in ? stride : 1;
-    if (in) stride *= s.nk[k];
+  a.nk = s.nk[k];
+  a.P = 1;
+  a.mprev = 1;
+  for (int j = 0; j < k; ++j) {
+    a.P *= s.nk[j];
+    a.mprev *= s.dk[j];
   }
+  a.cols = s.dk[k] * s.R;
   return a;
 }
 
@@ -58,123 +57,117 @@ int64_t core_elems(const Shape& s, int k) {
   return (int64_t)s.T * s.nk[k] * rl * s.dk[k] * rr;
 }
 
-// LDS of the split kernel (the larger of the two): X_0 .. X_{K-2} plus two dX
-// buffers of d1' x R; the merge kernel needs two buffers of d1' x R.
-int64_t chain_lds_floats(const Shape& s) {
-  if (s.L < 4) return 0;
-  int64_t m = 1, xs = 0;
-  for (int k = 0; k + 1 < s.L - 2; ++k) {
-    m *= s.dk[k];
-    xs += m * s.R;
+// Floats of the inner levels 1..K-2 (one region for the products, one for
+// their gradients); level k starts at level_offset(s, k).
+static int64_t level_offset(const Shape& s, int k) {
+  int64_t off = 0, P = s.nk[0], m = s.dk[0];
+  for (int j = 1; j < k; ++j) {
+    P *= s.nk[j];
+    m *= s.dk[j];
+    off += (int64_t)s.T * P * m * s.R;
   }
-  return xs + 2 * (int64_t)s.d1 * s.R;
+  return off;
 }
 
-// Slice S_k of table t at digit i: r_k x (d_k r_{k+1}) floats; r_0 = 1, else R.
-__device__ __forceinline__ const float* chain_slice(const ChainArgs& a, const float* G, int k, int t, int i) {
-  const int64_t len = (int64_t)(k == 0 ? 1 : a.R) * a.d[k] * a.R;
-  return G + ((int64_t)t * a.n[k] + i) * len;
-}
+int64_t chain_level_floats(const Shape& s) { return s.L >= 5 ? level_offset(s, s.L - 3) : 0; }
 
-// out (m x cols) = X (m x R) . S (R x cols), X in LDS, S in global memory.
-__device__ __forceinline__ void chain_mul(const float* X, const float* __restrict__ S, float* out, int m, int R,
-                                          int cols) {
-  for (int o = threadIdx.x; o < m * cols; o += CH_THREADS) {
-    const int r = o / cols, c = o - r * cols;
-    float acc = 0.f;
-    for (int b = 0; b < R; ++b) acc = fmaf(X[r * R + b], S[b * cols + c], acc);
-    out[o] = acc;
-  }
-}
-
-// One block per (table, i1'): G1m[t][i1'] = S_0 . ... . S_{K-1}.
-__global__ void __launch_bounds__(CH_THREADS) k_merge(ChainArgs a, CorePtrs G, float* __restrict__ G1m) {
+// X_k(t, p n_k + c) = X_{k-1}(t, p) . S_k(t, c).  Block (t, c, chunk) takes
+// child c and a chunk of pc consecutive parents: their rows X_{k-1} and the
+// slice S_k(t, c) (padded rows) are staged in LDS, and each thread forms
+// output columns of the chunk's products.
+__global__ void __launch_bounds__(LV_THREADS) k_merge_level(LevelArgs a, int pc, int stage_s,
+                                                            const float* __restrict__ Xprev,
+                                                            const float* __restrict__ Sk, float* __restrict__ Xk) {
   extern __shared__ float lds[];
-  const int row = blockIdx.x;
-  const int t = row / a.n1v, i1 = row - t * a.n1v;
-  float* X = lds;
-  float* Y = lds + a.d1v * a.R;
-  const float* S0 = chain_slice(a, G.p[0], 0, t, (i1 / a.rstride[0]) % a.n[0]);
-  int m = a.d[0];
-  for (int o = threadIdx.x; o < m * a.R; o += CH_THREADS) X[o] = S0[o];
-  for (int k = 1; k < a.K; ++k) {
-    __syncthreads();
-    const float* S = chain_slice(a, G.p[k], k, t, (i1 / a.rstride[k]) % a.n[k]);
-    float* out = k == a.K - 1 ? G1m + (int64_t)row * a.d1v * a.R : Y;
-    chain_mul(X, S, out, m, a.R, a.d[k] * a.R);
-    float* tmp = X;
-    X = Y;
-    Y = tmp;
-    m *= a.d[k];
-  }
-}
-
-// One block per (table, i1'): the gradient dX_{K-1} = dG1m[t][i1'] goes back
-// through the chain; per product X_k = X_{k-1} . S_k,
-//     dS_k += X_{k-1}^T . dX_k   and   dX_{k-1} = dX_k . S_k^T
-// (dX_k viewed as m_{k-1} x (d_k R)), and finally dS_0 += dX_0.  Core
-// gradients of slices shared by several i1' meet in global atomics.  A row with
-// an all-zero gradient (no index reached it) adds nothing and is skipped.
-__global__ void __launch_bounds__(CH_THREADS) k_split(ChainArgs a, CorePtrs G, GradPtrs dG,
-                                                      const float* __restrict__ dG1m) {
-  extern __shared__ float lds[];
-  const int row = blockIdx.x;
-  const int t = row / a.n1v, i1 = row - t * a.n1v;
-  const int nd = a.d1v * a.R;
-  float* dX = lds;
-  float* dY = lds + nd;
-  float* Xs = lds + 2 * nd;  // X_0, X_1, ... X_{K-2}, packed
-  const float* g = dG1m + (int64_t)row * nd;
-  int nz = 0;
-  for (int o = threadIdx.x; o < nd; o += CH_THREADS) {
-    const float v = g[o];
-    dX[o] = v;
-    nz |= v != 0.f;
-  }
-  if (!__syncthreads_or(nz)) return;
-  // X_0 .. X_{K-2}
-  const float* S0 = chain_slice(a, G.p[0], 0, t, (i1 / a.rstride[0]) % a.n[0]);
-  int m = a.d[0];
-  for (int o = threadIdx.x; o < m * a.R; o += CH_THREADS) Xs[o] = S0[o];
-  float* Xk = Xs;
-  for (int k = 1; k + 1 < a.K; ++k) {
-    __syncthreads();
-    const float* S = chain_slice(a, G.p[k], k, t, (i1 / a.rstride[k]) % a.n[k]);
-    chain_mul(Xk, S, Xk + m * a.R, m, a.R, a.d[k] * a.R);
-    Xk += m * a.R;
-    m *= a.d[k];
-  }
-  // Xk = X_{K-2} (m = m_{K-2} rows)
-  for (int k = a.K - 1; k >= 1; --k) {
-    __syncthreads();
-    const int cols = a.d[k] * a.R;
-    const int ik = (i1 / a.rstride[k]) % a.n[k];
-    const float* S = chain_slice(a, G.p[k], k, t, ik);
-    float* gk = dG.p[k] + ((int64_t)t * a.n[k] + ik) * a.R * cols;
-    for (int o = threadIdx.x; o < a.R * cols; o += CH_THREADS) {
-      const int b = o / cols, c = o - b * cols;
-      float acc = 0.f;
-      for (int r = 0; r < m; ++r) acc = fmaf(Xk[r * a.R + b], dX[r * cols + c], acc);
-      unsafeAtomicAdd(&gk[o], acc);
+  const int64_t nchunk = (a.P + pc - 1) / pc;
+  const int64_t tc = blockIdx.x / nchunk;  // t * n_k + c
+  const int64_t p0 = (blockIdx.x - tc * nchunk) * pc;
+  const int64_t t = tc / a.nk;
+  const int ch = (int)(tc - t * a.nk);
+  const int np = (int)(a.P - p0 < pc ? a.P - p0 : pc);
+  const int xl = a.mprev * a.R, ol = a.mprev * a.cols;
+  const int spitch = a.cols + 1;
+  float* Xs = lds;
+  float* Ss = lds + pc * xl;
+  const float* Xg = Xprev + (t * a.P + p0) * xl;
+  for (int e = threadIdx.x; e < np * xl; e += LV_THREADS) Xs[e] = Xg[e];
+  const float* S = Sk + tc * a.R * a.cols;
+  if (stage_s)
+    for (int e = threadIdx.x; e < a.R * a.cols; e += LV_THREADS) {
+      const int b = e / a.cols, col = e - b * a.cols;
+      Ss[b * spitch + col] = S[e];
     }
-    for (int o = threadIdx.x; o < m * a.R; o += CH_THREADS) {
-      const int r = o / a.R, b = o - r * a.R;
-      float acc = 0.f;
-      for (int c = 0; c < cols; ++c) acc = fmaf(dX[r * cols + c], S[b * cols + c], acc);
-      dY[o] = acc;
-    }
-    float* tmp = dX;
-    dX = dY;
-    dY = tmp;
-    if (k > 1) {
-      m /= a.d[k - 1];
-      Xk -= m * a.R;
-    }
-  }
   __syncthreads();
-  const int i0 = (i1 / a.rstride[0]) % a.n[0];
-  float* g0 = dG.p[0] + ((int64_t)t * a.n[0] + i0) * a.d[0] * a.R;
-  for (int o = threadIdx.x; o < a.d[0] * a.R; o += CH_THREADS) unsafeAtomicAdd(&g0[o], dX[o]);
+  const float* Sb = stage_s ? Ss : S;
+  const int sp = stage_s ? spitch : a.cols;
+  for (int o = threadIdx.x; o < np * ol; o += LV_THREADS) {
+    const int pr = o / a.cols, col = o - pr * a.cols;  // pr = pp * mprev + r
+    const int pp = pr / a.mprev, r = pr - pp * a.mprev;
+    const float* x = Xs + pr * a.R;
+    float acc = 0.f;
+    for (int b = 0; b < a.R; ++b) acc = fmaf(x[b], Sb[b * sp + col], acc);
+    Xk[((t * a.P + p0 + pp) * a.nk + ch) * ol + r * a.cols + col] = acc;
+  }
+}
+
+// One backward level k of the merged chain.  Block (t, c, chunk) takes child c of
+// core k and a chunk of pc consecutive parents p; with X = X_{k-1}(t, p) and
+// dX = dX_k(t, p n_k + c) staged in LDS it adds
+//     X^T . dX              into dS_k(t, c)        (summed over the chunk first)
+//     dX . S_k(t, c)^T      into dX_{k-1}(t, p)    (one partial per child)
+// with atomics into zeroed outputs; zero partials are not added.
+__global__ void __launch_bounds__(LV_THREADS) k_split_level(LevelArgs a, int pc, int stage_s,
+                                                            const float* __restrict__ Xprev,
+                                                            const float* __restrict__ dXk,
+                                                            const float* __restrict__ Sk, float* __restrict__ dSk,
+                                                            float* __restrict__ dXprev) {
+  extern __shared__ float lds[];
+  const int64_t nchunk = (a.P + pc - 1) / pc;
+  const int64_t tc = blockIdx.x / nchunk;  // t * n_k + c
+  const int64_t p0 = (blockIdx.x - tc * nchunk) * pc;
+  const int64_t t = tc / a.nk;
+  const int ch = (int)(tc - t * a.nk);
+  const int np = (int)(a.P - p0 < pc ? a.P - p0 : pc);
+  const int xl = a.mprev * a.R, dl = a.mprev * a.cols;
+  const int spitch = a.cols + 1;
+  float* Xs = lds;
+  float* dXs = Xs + pc * xl;
+  float* Ss = dXs + pc * dl;
+  const float* S = Sk + tc * a.R * a.cols;
+  const float* Xg = Xprev + (t * a.P + p0) * xl;  // consecutive parents are contiguous
+  for (int e = threadIdx.x; e < np * xl; e += LV_THREADS) Xs[e] = Xg[e];
+  for (int e = threadIdx.x; e < np * dl; e += LV_THREADS) {
+    const int pp = e / dl, w = e - pp * dl;
+    dXs[e] = dXk[((t * a.P + p0 + pp) * a.nk + ch) * dl + w];
+  }
+  if (stage_s)
+    for (int e = threadIdx.x; e < a.R * a.cols; e += LV_THREADS) {
+      const int b = e / a.cols, col = e - b * a.cols;
+      Ss[b * spitch + col] = S[e];
+    }
+  __syncthreads();
+  const int rows = np * a.mprev;
+  float* gS = dSk + tc * a.R * a.cols;
+  for (int o = threadIdx.x; o < a.R * a.cols; o += LV_THREADS) {
+    const int b = o / a.cols, col = o - b * a.cols;
+    float acc = 0.f;
+    for (int r = 0; r < rows; ++r) acc = fmaf(Xs[r * a.R + b], dXs[r * a.cols + col], acc);
+    if (acc != 0.f) unsafeAtomicAdd(&gS[o], acc);
+  }
+  float* gX = dXprev + (t * a.P + p0) * xl;
+  for (int o = threadIdx.x; o < rows * a.R; o += LV_THREADS) {
+    const int r = o / a.R, b = o - r * a.R;
+    const float* d = dXs + r * a.cols;
+    float acc = 0.f;
+    if (stage_s) {
+      const float* sr = Ss + b * spitch;
+      for (int col = 0; col < a.cols; ++col) acc = fmaf(d[col], sr[col], acc);
+    } else {
+      const float* sr = S + b * a.cols;
+      for (int col = 0; col < a.cols; ++col) acc = fmaf(d[col], sr[col], acc);
+    }
+    if (acc != 0.f) unsafeAtomicAdd(&gX[o], acc);
+  }
 }
 
 __global__ void k_identity(float* __restrict__ G, int T, int R) {
@@ -185,41 +178,66 @@ __global__ void k_identity(float* __restrict__ G, int T, int R) {
   }
 }
 
-static CorePtrs core_ptrs(const float* const* cores, int K) {
-  CorePtrs c;
-  for (int k = 0; k < MAX_CORES; ++k) c.p[k] = k < K ? cores[k] : nullptr;
-  return c;
+// Product level k (1..K-1): the merged core for k = K-1, else an inner level.
+static float* level_x(const Shape& s, const Work& w, int k) {
+  return k == s.L - 3 ? w.g1m : w.xlev + level_offset(s, k);
 }
 
 hipError_t launch_merge(const Shape& s, const Work& w, const float* const* cores, const Prof& prof, hipStream_t st) {
-  if (s.L < 4 || !w.g1m) return hipErrorInvalidValue;
-  const ChainArgs a = chain_args(s);
-  const size_t lds = sizeof(float) * 2 * (size_t)s.d1 * s.R;
-  hipError_t e = hipFuncSetAttribute((const void*)k_merge, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
+  if (s.L < 4 || !w.g1m || (s.L >= 5 && !w.xlev)) return hipErrorInvalidValue;
   prof_begin(prof, K_MERGE, st);
-  hipLaunchKernelGGL(k_merge, dim3((unsigned)((int64_t)s.T * s.n1)), dim3(CH_THREADS), lds, st, a,
-                     core_ptrs(cores, a.K), w.g1m);
+  for (int k = 1; k <= s.L - 3; ++k) {
+    const LevelArgs a = level_args(s, k);
+    const float* Xprev = k == 1 ? cores[0] : level_x(s, w, k - 1);
+    // S_k(t, c) staged (padded rows) when it fits in 32 KB; parents per block:
+    // 16, fewer if their rows and the staged slice exceed 48 KB of LDS
+    const int stage_s = (int64_t)a.R * (a.cols + 1) <= 8192;
+    const int64_t sl = stage_s ? (int64_t)a.R * (a.cols + 1) : 0, xl = (int64_t)a.mprev * a.R;
+    int64_t pc = (12288 - sl) / xl;
+    if (pc > 16) pc = 16;
+    if (pc < 1) pc = 1;
+    if (pc > a.P) pc = a.P;
+    const size_t lds = sizeof(float) * (size_t)(pc * xl + sl);
+    hipError_t e = hipFuncSetAttribute((const void*)k_merge_level, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
+    if (e != hipSuccess) return e;
+    const int64_t blocks = (int64_t)a.T * a.nk * ((a.P + pc - 1) / pc);
+    hipLaunchKernelGGL(k_merge_level, dim3((unsigned)blocks), dim3(LV_THREADS), lds, st, a, (int)pc, stage_s,
+                       Xprev, cores[k], level_x(s, w, k));
+  }
   prof_end(prof, K_MERGE, st);
   return hipGetLastError();
 }
 
 hipError_t launch_split(const Shape& s, const Work& w, const float* const* cores, float* const* grads,
                         const Prof& prof, hipStream_t st) {
-  if (s.L < 4 || !w.dg1m) return hipErrorInvalidValue;
-  const ChainArgs a = chain_args(s);
+  if (s.L < 4 || !w.g1m || !w.dg1m || (s.L >= 5 && (!w.xlev || !w.dxlev))) return hipErrorInvalidValue;
   hipError_t e;
-  for (int k = 0; k < a.K; ++k)
+  for (int k = 0; k <= s.L - 3; ++k)
     if ((e = fill_f32(grads[k], core_elems(s, k), 0.f, st)) != hipSuccess) return e;
-  const size_t lds = sizeof(float) * (size_t)chain_lds_floats(s);
-  if ((e = hipFuncSetAttribute((const void*)k_split, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
-      hipSuccess)
-    return e;
-  GradPtrs g;
-  for (int k = 0; k < MAX_CORES; ++k) g.p[k] = k < a.K ? grads[k] : nullptr;
+  const int64_t nlev = chain_level_floats(s);
+  if (nlev && (e = fill_f32(w.dxlev, nlev, 0.f, st)) != hipSuccess) return e;
   prof_begin(prof, K_SPLIT, st);
-  hipLaunchKernelGGL(k_split, dim3((unsigned)((int64_t)s.T * s.n1)), dim3(CH_THREADS), lds, st, a,
-                     core_ptrs(cores, a.K), g, (const float*)w.dg1m);
+  for (int k = s.L - 3; k >= 1; --k) {
+    const LevelArgs a = level_args(s, k);
+    const float* Xprev = k == 1 ? cores[0] : level_x(s, w, k - 1);
+    const float* dXk = k == s.L - 3 ? w.dg1m : w.dxlev + level_offset(s, k);
+    float* dXprev = k == 1 ? grads[0] : w.dxlev + level_offset(s, k - 1);
+    // parents per block: their X and dX rows within 32 KB of LDS; S_k(t, c)
+    // (padded rows) staged too when it fits in 16 KB more
+    const int64_t per = (int64_t)a.mprev * (a.R + a.cols);
+    int64_t pc = 8192 / per;
+    if (pc < 1) pc = 1;
+    if (pc > a.P) pc = a.P;
+    const int stage_s = (int64_t)a.R * (a.cols + 1) <= 4096;
+    const size_t lds = sizeof(float) * (size_t)(pc * per + (stage_s ? a.R * (a.cols + 1) : 0));
+    if ((e = hipFuncSetAttribute((const void*)k_split_level, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)lds)) != hipSuccess)
+      return e;
+    const int64_t blocks = (int64_t)a.T * a.nk * ((a.P + pc - 1) / pc);
+    hipLaunchKernelGGL(k_split_level, dim3((unsigned)blocks), dim3(LV_THREADS), lds, st, a, (int)pc, stage_s, Xprev,
+                       dXk, (const float*)cores[k], grads[k], dXprev);
+  }
   prof_end(prof, K_SPLIT, st);
   return hipGetLastError();
 }

@@ -96,6 +96,13 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
     W->g1m = nullptr;
     W->dg1m = nullptr;
   }
+  const size_t nlev = (size_t)chain_level_floats(s);
+  W->xlev = (float*)take(4 * nlev);
+  W->dxlev = (float*)take(4 * nlev);
+  if (!nlev) {
+    W->xlev = nullptr;
+    W->dxlev = nullptr;
+  }
   const bool generic = !bwd_r32 || !fwd_r32_supported(s, m);
   const size_t nC = (size_t)s.d1 * s.d2 * s.R;
   W->ckpt = (float*)take(generic ? 4 * CKPT_SLOTS * nC : 0);
@@ -199,10 +206,6 @@ static tt_emb_status create_view(const tt_emb_desc* d, int L, const int32_t* nk,
   for (int k = 0; k < MAX_CORES; ++k) {
     s.nk[k] = k < L ? nk[k] : 1;
     s.dk[k] = k < L ? dk[k] : 1;
-  }
-  if (chain_lds_floats(s) * 4 > 65536) {
-    delete h;
-    return TT_EMB_EUNSUPPORTED;
   }
   h->g_valid = false;
   h->prof.kernel = 0;

@@ -142,7 +142,10 @@ def test_create_n_shapes_and_workspace(N):
     h2 = N.tt_emb_create_n(_desc_n(N, L=2, n=(12, 10), d=(4, 2)))
     assert N.tt_emb_workspace_size(h4) > 0 and N.tt_emb_workspace_size(h2) > 0
     h8 = N.tt_emb_create_n(_desc_n(N, L=8, n=(2,) * 8, d=(1, 2, 1, 2, 1, 2, 1, 2)))
-    for h in (h3, h3n, h4, h2, h8):
+    # wide merged cores are served too (their chain runs level by level in the workspace)
+    h5 = N.tt_emb_create_n(_desc_n(N, L=5, n=(2, 2, 2, 2, 2), d=(8, 8, 2, 1, 1), R=64))
+    assert N.tt_emb_workspace_size(h5) > N.tt_emb_workspace_size(h8)
+    for h in (h3, h3n, h4, h2, h8, h5):
         N.tt_emb_destroy(h)
 
 
@@ -150,8 +153,8 @@ def test_create_n_shapes_and_workspace(N):
     (dict(L=1), 1), (dict(L=9), 1), (dict(L=0), 1), (dict(T=0), 1), (dict(R=0), 1),
     (dict(n=(3, 0, 5, 2)), 1), (dict(d=(1, 1, -1, 1)), 1), (dict(rows=121), 1),
     (dict(n=(1000, 1000, 1000, 10)), 5), (dict(d=(16, 16, 16, 2)), 5), (dict(R=65), 5),
-    # chain buffers beyond 64 KiB: R * (d0 + d0 d1 + 2 d0 d1 d2) floats
-    (dict(L=5, n=(2, 2, 2, 2, 2), d=(8, 8, 2, 1, 1), R=64), 5),
+    # merged row product n0 n1 of 2^28 or more
+    (dict(T=1, n=(1 << 14, 1 << 14, 2, 2), d=(1, 1, 2, 2)), 5),
 ])
 def test_create_n_rejects_bad_shapes(N, kw, code):
     h = C.c_void_p()

@@ -80,6 +80,9 @@ CASES = [
     dict(T=2, n=(2, 3, 4, 5, 6), d=(1, 2, 2, 2, 2), R=8, B=60, max_len=8),
     dict(T=1, n=(2, 2, 3, 2, 3, 4), d=(2, 1, 2, 1, 2, 2), R=4, B=30, max_len=6),
     dict(T=2, n=(2,) * 8, d=(1, 2, 1, 2, 1, 2, 1, 2), R=3, B=25, max_len=5),
+    dict(T=2, n=(2, 2, 2, 3, 4), d=(4, 4, 2, 1, 1), R=16, B=40, max_len=6),  # wide merged core: d1' = 32
+    dict(T=2, n=(5, 4, 3, 2, 2), d=(1, 2, 1, 2, 2), R=2, B=40, max_len=6),  # 20 parents: several per-level chunks
+    dict(T=1, n=(2, 2, 2, 2, 2), d=(4, 4, 2, 1, 1), R=64, B=20, max_len=4),  # R = 64: split chunks of 2 parents
 ]
 
 
