@@ -116,9 +116,10 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
  *                            meets the same group later reloads it instead of
  *                            recomputing it, whenever the entry still holds
  *                            that group.
- * The checkpoint applies to the kernels that keep one C per worker (every
- * shape except d = (4,4,8), R = 32); the MFMA kernels for that shape build C
- * for four slices per matrix-core tile and treat STEAL_CKPT as STEAL.  All
+ * The checkpoint applies to the kernels that keep one C per worker (the
+ * generic kernels); the MFMA kernels (forward for d = (4,4,8) with R = 32 or
+ * 64, backward for d = (4,4,8) with R = 32) build C for four slices per
+ * matrix-core tile and treat STEAL_CKPT as STEAL.  All
  * modes compute the same function.  Host only; may be changed between calls;
  * returns TT_EMB_EINVAL for an unknown mode. */
 typedef enum { TT_EMB_SCHED_STEAL = 0, TT_EMB_SCHED_STATIC = 1, TT_EMB_SCHED_STEAL_CKPT = 2 } tt_emb_sched;

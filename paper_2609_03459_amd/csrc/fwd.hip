@@ -320,6 +320,231 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   }
 }
 
+// ---------------------------------------------------------------------------
+// MFMA forward for d = (4, 4, 8), R = 64 (D = 128).  The chunk, quad and row-pair
+// structure of the R = 32 kernel; B = G2[t][i2] (64 x 256 floats) no longer fits in
+// registers and streams from L2, two column tiles at a time:
+//   * stage 1: Cstack (16 x 256) = Astack (16 x 64) . B (64 x 256), 256 MFMAs per
+//     quad, with the contraction index a = 16 (lane >> 4) + s, so a lane's sixteen A
+//     values are four 16-byte loads;
+//   * Cstack goes to a per-wave LDS tile with rows (slice, j1, j2) of 68 floats, the
+//     four slices 1,104 floats apart (the writes of a tile take 64 distinct banks);
+//   * stage 2 per row pair: E^T = D^T . C'^T, 16 MFMAs, with b = 16 (lane >> 4) + s,
+//     so a lane's sixteen C'^T values are four 16-byte LDS reads.
+// ---------------------------------------------------------------------------
+constexpr int F64_WAVES = 4;
+constexpr int F64_WG_PER_CU = 2;
+constexpr int F64_PITCH = 68;
+constexpr int F64_SLICE = 16 * F64_PITCH + 16;
+constexpr int F64_SCR = 4 * F64_SLICE;
+
+__global__ void __launch_bounds__(64 * F64_WAVES, F64_WG_PER_CU)
+    k_fwd_r64(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
+              const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
+              const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
+              const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ E) {
+  __shared__ float scr_all[F64_WAVES * F64_SCR];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float* scr = scr_all + wave * F64_SCR;
+  const int nch = (int)run_base[s.T * s.n2];
+  const int l15 = lane & 15, l4 = lane >> 4;
+  const int orow = l4 >> 1;
+  const int asel = l15 >> 3;
+  // byte offsets: stage-2 A word D^T[(sel, j3 = l15 & 7)][b = 16 l4 + s] in a G3 row
+  // (+ 32 bytes per s), the E store (as for R = 32), and the stage-1 B word
+  // B[a = 16 l4 + s][16 nt + l15] in G2[t][i2] (+ 1,024 bytes per s, + 64 per nt)
+  const uint32_t vo_d = 4u * (uint32_t)(l4 * 128 + (l15 & 7));
+  const uint32_t vo_e = 4u * (uint32_t)(orow * 128 + l15 * 8 + 4 * (l4 & 1));
+  const uint32_t vo_b = 4u * (uint32_t)(l4 * 4096 + l15);
+  // stage-1 output word (slice l4, j1 r, j2, b) and stage-2 operand read (slice j, jj = l15, b = 16 l4 + 4 q)
+  const int wr_base = l4 * F64_SLICE + l15;
+  const int rd_base = l15 * F64_PITCH + 16 * l4;
+
+  int cursor = 0;
+  int c_rb = 0, c_nr = 0, c_i1 = 0;
+  int f = 0, ns = 0, run = -1, t = 0, qd = 0;
+  int c = -1;
+  const int wid = blockIdx.x * F64_WAVES + wave, nw = gridDim.x * F64_WAVES;
+  int st_next = share_lo(nch, nw, wid);
+  const int st_hi = share_lo(nch, nw, wid + 1);
+  auto next_chunk = [&]() {
+    if (s.sched == SCHED_STATIC)
+      c = st_next < st_hi ? st_next++ : -1;
+    else
+      c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
+    qd = 0;
+    if (c >= 0) {
+      const int4 ch = chunks[c];
+      f = __builtin_amdgcn_readfirstlane(ch.x);
+      ns = __builtin_amdgcn_readfirstlane(ch.y);
+      run = __builtin_amdgcn_readfirstlane(ch.z);
+      t = run / s.n2;
+      const int sl = f + (lane < ns ? lane : 0);
+      const int4 sd = slices[sl];
+      c_rb = sd.y;
+      c_nr = lane < ns ? sd.z - sd.y : 0;
+      c_i1 = slice_i1[sl];
+    }
+  };
+
+  int d_ra = 0, d_ia = 0, d_ib = 0, np = 0;
+  int e_ra = 0, e_ia = 0, e_ib = 0, e_np = 0;
+  auto build_desc = [&]() {
+    const int n0 = __builtin_amdgcn_readlane(c_nr, qd), n1 = __builtin_amdgcn_readlane(c_nr, qd + 1);
+    const int n2 = __builtin_amdgcn_readlane(c_nr, qd + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd + 3);
+    const int b0 = __builtin_amdgcn_readlane(c_rb, qd), b1 = __builtin_amdgcn_readlane(c_rb, qd + 1);
+    const int b2 = __builtin_amdgcn_readlane(c_rb, qd + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd + 3);
+    const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
+    e_np = q3 + ((n3 + 1) >> 1);
+    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
+    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
+    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    const bool ok = lane < e_np;
+    const bool has1 = ok && pr + 1 < nr;
+    const int ra = ok ? rb + pr : b0;
+    e_ia = uniq_i3[ra];
+    e_ib = uniq_i3[has1 ? ra + 1 : ra];
+    e_ra = ra | (j << 28) | (has1 ? 1 << 30 : 0);
+  };
+  // stage-1 A operand of the quad at qd: Astack[(slice aj, j1 = lane & 3)][a = 16 l4 + s]
+  float4 A4[4];
+  auto load_A = [&]() {
+    const int nq4 = ns - qd < 4 ? ns - qd : 4;
+    const int aj = l15 >> 2;
+    const int i1a = __builtin_amdgcn_readlane(c_i1, qd), i1b = __builtin_amdgcn_readlane(c_i1, qd + 1);
+    const int i1c = __builtin_amdgcn_readlane(c_i1, qd + 2), i1d = __builtin_amdgcn_readlane(c_i1, qd + 3);
+    const float4* Ag = reinterpret_cast<const float4*>(
+        G1 + (uint32_t)(t * s.n1 + sel4(aj < nq4 ? aj : 0, i1a, i1b, i1c, i1d)) * 256u +
+        (uint32_t)((lane & 3) * 64 + 16 * l4));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) A4[q] = Ag[q];
+  };
+
+  struct FPair {
+    float d[16];
+    int ra;
+    int j;
+    bool has1;
+  };
+  buf_t g3buf = make_buf(G3, 0);
+  auto pair_load = [&](FPair& X, int P) {
+    const int rw = __builtin_amdgcn_readlane(d_ra, P);
+    const int ia = __builtin_amdgcn_readlane(d_ia, P), ib = __builtin_amdgcn_readlane(d_ib, P);
+    X.ra = rw & 0x0FFFFFFF;
+    X.j = (rw >> 28) & 3;
+    X.has1 = (rw >> 30) & 1;
+    const uint32_t o = vo_d + (uint32_t)(asel ? ib : ia) * 2048u;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) X.d[k] = buf_f32(g3buf, o + 32u * k);
+  };
+
+  FPair XA, XB;
+  next_chunk();
+  if (c >= 0) {
+    build_desc();
+    load_A();
+    d_ra = e_ra;
+    d_ia = e_ia;
+    d_ib = e_ib;
+    np = e_np;
+    g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 512u, (uint32_t)s.n3 * 2048u);
+    pair_load(XA, 0);
+    pair_load(XB, np > 1 ? 1 : 0);
+  }
+  while (c >= 0) {
+    // stage 1, two column tiles at a time (rows of slices beyond the chunk's end
+    // come from a repeated slice and are never read)
+    {
+      const buf_t bbuf = make_buf(G2 + (uint32_t)run * 16384u, 65536u);
+      float Aop[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        Aop[4 * q + 0] = A4[q].x;
+        Aop[4 * q + 1] = A4[q].y;
+        Aop[4 * q + 2] = A4[q].z;
+        Aop[4 * q + 3] = A4[q].w;
+      }
+#pragma unroll
+      for (int p2 = 0; p2 < 8; ++p2) {
+        float b0[16], b1[16];
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          b0[k] = buf_f32(bbuf, vo_b + 128u * p2, 1024u * k);
+          b1[k] = buf_f32(bbuf, vo_b + 128u * p2 + 64u, 1024u * k);
+        }
+        f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[k], b0[k], c0, 0, 0, 0);
+          c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[k], b1[k], c1, 0, 0, 0);
+        }
+        // lane holds C[slice l4][j1 r][j2 = nt >> 2][b = 16 (nt & 3) + l15], nt = 2 p2 (+1)
+        const int nt0 = 2 * p2, nt1 = 2 * p2 + 1;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          scr[wr_base + (4 * r + (nt0 >> 2)) * F64_PITCH + 16 * (nt0 & 3)] = c0[r];
+          scr[wr_base + (4 * r + (nt1 >> 2)) * F64_PITCH + 16 * (nt1 & 3)] = c1[r];
+        }
+      }
+      wave_lds_sync();
+    }
+    if (qd + 4 >= ns)
+      next_chunk();
+    else
+      qd += 4;
+    if (c >= 0) {
+      build_desc();
+      load_A();
+    }
+    // stage-2 B operand of slice j: C'^T[b = 16 l4 + s][jj = l15]
+    float CT[16];
+    auto slice_begin = [&](int j) {
+      const float4* rp = reinterpret_cast<const float4*>(scr + j * F64_SLICE + rd_base);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = rp[q];
+        CT[4 * q + 0] = v.x;
+        CT[4 * q + 1] = v.y;
+        CT[4 * q + 2] = v.z;
+        CT[4 * q + 3] = v.w;
+      }
+    };
+    slice_begin(0);
+    auto pair_compute = [&](const FPair& X) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < 16; ++k) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[k], CT[k], acc, 0, 0, 0);
+      const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * 128, X.has1 ? 1024u : 512u);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
+    };
+    int cj = 0;
+    auto step = [&](const FPair& X) {
+      if (X.j != cj) {
+        slice_begin(X.j);
+        cj = X.j;
+      }
+      pair_compute(X);
+    };
+    for (int P = 0; P < np; P += 2) {
+      pair_load(XB, P + 1 < np ? P + 1 : np - 1);
+      step(XA);
+      pair_load(XA, P + 2 < np ? P + 2 : np - 1);
+      if (P + 1 < np) step(XB);
+    }
+    wave_lds_sync();
+    if (c >= 0) {
+      d_ra = e_ra;
+      d_ia = e_ia;
+      d_ib = e_ib;
+      np = e_np;
+      g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 512u, (uint32_t)s.n3 * 2048u);
+      pair_load(XA, 0);
+      pair_load(XB, np > 1 ? 1 : 0);
+    }
+  }
+}
+
 // Sum pooling: LPB lanes per bag, float4 columns, occurrences in position order.
 template <int LPB>
 __global__ void __launch_bounds__(256) k_pool4(const float4* __restrict__ E, const int32_t* __restrict__ inv,
@@ -488,6 +713,13 @@ hipError_t launch_pool(const Shape& s, const float* E, const int32_t* inv, const
   return hipGetLastError();
 }
 
+bool fwd_r64_supported(const Shape& s, int64_t max_indices) {
+  // 32-bit offsets into E (rows x 128), G1, G2 and G3
+  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 64 && max_indices * 128 < (int64_t(1) << 31) &&
+         (int64_t)s.T * s.n1 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n2 * 16384 < (int64_t(1) << 31) &&
+         (int64_t)s.T * s.n3 * 512 < (int64_t(1) << 31);
+}
+
 bool fwd_r32_supported(const Shape& s, int64_t max_indices) {
   // 32-bit float offsets into E (rows x 128), G1 and G3
   return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
@@ -505,6 +737,17 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
       const int blocks = persistent_grid() * F32_WG_PER_CU;
       prof_begin(prof, K_FWD_FUSED, st);
       hipLaunchKernelGGL(k_fwd_r32, dim3(blocks), dim3(64 * F32_WAVES), 0, st, shape_args(s), G1, G2, G3,
+                         (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
+                         (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.E);
+      prof_end(prof, K_FWD_FUSED, st);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      return launch_pool(s, w.E, w.inv, offsets, M, B, out, prof, st);
+    }
+    if (fwd_r64_supported(s, M)) {
+      const int blocks = persistent_grid() * F64_WG_PER_CU;
+      prof_begin(prof, K_FWD_FUSED, st);
+      hipLaunchKernelGGL(k_fwd_r64, dim3(blocks), dim3(64 * F64_WAVES), 0, st, shape_args(s), G1, G2, G3,
                          (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
                          (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.E);
       prof_end(prof, K_FWD_FUSED, st);
