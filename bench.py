@@ -261,6 +261,9 @@ def main():
                          "the paper)")
     ap.add_argument("--row-factors", default=None, help="comma-separated row factors (overrides --cores)")
     ap.add_argument("--dim-factors", default=None, help="comma-separated column factors (with --row-factors)")
+    ap.add_argument("--unfused-sgd", action="store_true",
+                    help="backward into gradient arrays, then a separate SGD call (default with three cores: "
+                         "the fused backward-and-SGD call)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
@@ -328,7 +331,7 @@ def main():
 
         def sgd():
             emb.sgd_n(G, grads, lr)
-    else:
+    elif args.unfused_sgd:
         def fwd(reuse):
             emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=reuse)
 
@@ -337,6 +340,17 @@ def main():
 
         def sgd():
             emb.sgd(*G, *grads, lr)
+    else:
+        # the library's training step: backward with the SGD update applied in its
+        # final gradient reductions (no gradient arrays, no separate update pass)
+        def fwd(reuse):
+            emb.forward(*G, idx, off, num_bags=B, out=out, reuse_grouping=reuse)
+
+        def bwd():
+            emb.backward_sgd(*G, idx, off, dV, lr, num_bags=B, reuse_grouping=True)
+
+        def sgd():
+            pass
 
     def step():
         fwd(False)
@@ -459,7 +473,9 @@ def main():
         "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "cores": L,
                    "row_factors": list(n),
                    "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
-                   "step": "group+forward+pool+backward+sgd", "parallelism": "single-gpu",
+                   "step": "group+forward+pool+backward+sgd" + (
+                       " (sgd fused into the backward's reductions)" if L == 3 and not args.unfused_sgd else ""),
+                   "parallelism": "single-gpu",
                    "reuse": args.reuse, "sched": args.sched},
         "roofline": roof,
         "step_ms_median": round(step_med, 4),

@@ -405,24 +405,32 @@ __device__ __forceinline__ void put_grad(float* out, int64_t i, float acc, float
 
 // dG1[t][i1] = sum over i2 of the dA halves of the slices of prefix (i1, i2).
 // The block lists the slices of (t, i1) in i2 order (512 prefixes per round,
-// the list G1_LIST entries at a time), and four groups of 128 threads take
-// list entries g, g + 4, ... with eight loads in flight per thread; the group
+// the list G1_LIST entries at a time), and its eight waves take list entries
+// g, g + 8, ... (two columns per lane, eight 8-byte loads in flight); the wave
 // sums are combined in a fixed order.
 constexpr int G1_LIST = 4096;
 
-__global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
-                                                   const uint32_t* __restrict__ dense_base,
-                                                   const float* __restrict__ dApart, int nsl_cap,
-                                                   float* __restrict__ dG1, float lr, bool update) {
+constexpr int RED_THREADS = 512;
+
+__device__ __forceinline__ void reduce_g1(int ti1, ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
+                                          const uint32_t* __restrict__ dense_base,
+                                          const float* __restrict__ dApart, int nsl_cap, float* __restrict__ dG1,
+                                          float lr, bool update) {
   __shared__ int list[G1_LIST];
   __shared__ uint32_t wsum[8];
-  __shared__ float red[4][128];
-  const int ti1 = blockIdx.x;  // t * n1 + i1
+  __shared__ float2 red[8][64];
+  // ti1 = t * n1 + i1
   const int t = ti1 / s.n1, i1 = ti1 % s.n1;
-  const int g = threadIdx.x >> 7, e = threadIdx.x & 127;
-  const float* P0 = dApart + e;
-  const float* P1 = dApart + (size_t)nsl_cap * 128 + e;
-  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int g = threadIdx.x >> 6, e = threadIdx.x & 63;  // eight waves, two columns per lane
+  const float2* P0 = reinterpret_cast<const float2*>(dApart) + e;
+  const float2* P1 = reinterpret_cast<const float2*>(dApart + (size_t)nsl_cap * 128) + e;
+  float2 a[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) a[k] = make_float2(0.f, 0.f);
+  auto add = [](float2& x, const float2 y) {
+    x.x += y.x;
+    x.y += y.y;
+  };
   for (int i2b = 0; i2b < s.n2; i2b += 512) {
     const int i2 = i2b + (int)threadIdx.x;
     uint32_t cnt = 0, base = 0;
@@ -433,7 +441,7 @@ __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* 
     }
     uint32_t total;
     const uint32_t pos = block_excl_scan<uint32_t, 512>(cnt, wsum, &total);
-    // the round's slice list, G1_LIST entries at a time
+    // the round's slice list, G1_LIST entries at a time; wave g takes entries g, g + 8, ...
     for (uint32_t w0 = 0; w0 < total; w0 += G1_LIST) {
       const uint32_t k0 = w0 > pos ? w0 - pos : 0u, k1e = w0 + G1_LIST - pos;
       const uint32_t k1 = pos >= w0 + G1_LIST ? 0u : (cnt < k1e ? cnt : k1e);
@@ -441,65 +449,98 @@ __global__ void __launch_bounds__(512) k_reduce_g1(ShapeArgs s, const uint32_t* 
       __syncthreads();
       const int wn = (int)(total - w0 < (uint32_t)G1_LIST ? total - w0 : (uint32_t)G1_LIST);
       int j = g;
-      for (; j + 12 < wn; j += 16) {
-        const size_t l0 = (size_t)list[j] * 128, l1 = (size_t)list[j + 4] * 128;
-        const size_t l2 = (size_t)list[j + 8] * 128, l3 = (size_t)list[j + 12] * 128;
-        a[0] += P0[l0];
-        a[1] += P1[l0];
-        a[2] += P0[l1];
-        a[3] += P1[l1];
-        a[4] += P0[l2];
-        a[5] += P1[l2];
-        a[6] += P0[l3];
-        a[7] += P1[l3];
+      for (; j + 24 < wn; j += 32) {
+        const size_t l0 = (size_t)list[j] * 64, l1 = (size_t)list[j + 8] * 64;
+        const size_t l2 = (size_t)list[j + 16] * 64, l3 = (size_t)list[j + 24] * 64;
+        add(a[0], P0[l0]);
+        add(a[1], P1[l0]);
+        add(a[2], P0[l1]);
+        add(a[3], P1[l1]);
+        add(a[4], P0[l2]);
+        add(a[5], P1[l2]);
+        add(a[6], P0[l3]);
+        add(a[7], P1[l3]);
       }
-      for (; j < wn; j += 4) {
-        const size_t l0 = (size_t)list[j] * 128;
-        a[0] += P0[l0];
-        a[1] += P1[l0];
+      for (; j < wn; j += 8) {
+        const size_t l0 = (size_t)list[j] * 64;
+        add(a[0], P0[l0]);
+        add(a[1], P1[l0]);
       }
       __syncthreads();
     }
   }
-  red[g][e] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  float2 r;
+  r.x = ((a[0].x + a[1].x) + (a[2].x + a[3].x)) + ((a[4].x + a[5].x) + (a[6].x + a[7].x));
+  r.y = ((a[0].y + a[1].y) + (a[2].y + a[3].y)) + ((a[4].y + a[5].y) + (a[6].y + a[7].y));
+  red[g][e] = r;
   __syncthreads();
-  if (g == 0) put_grad(dG1, (int64_t)ti1 * 128 + e, ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e], lr, update);
+  if (g == 0) {
+    float2 v = red[0][e];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) add(v, red[k][e]);
+    put_grad(dG1, (int64_t)ti1 * 128 + 2 * e, v.x, lr, update);
+    put_grad(dG1, (int64_t)ti1 * 128 + 2 * e + 1, v.y, lr, update);
+  }
 }
 
 // dG2[t][i2][a][j2][16 h + b'] = sum of the chunk partials of run (t, i2), half h
-__global__ void __launch_bounds__(256) k_reduce_g2(const uint32_t* __restrict__ run_base,
-                                                   const float* __restrict__ dBpart, int nch_cap,
-                                                   float* __restrict__ dG2, float lr, bool update) {
-  const int run = blockIdx.x >> 1, h = blockIdx.x & 1;
+// (rh = 2 run + h)
+__device__ __forceinline__ void reduce_g2(int rh, const uint32_t* __restrict__ run_base,
+                                          const float* __restrict__ dBpart, int nch_cap, float* __restrict__ dG2,
+                                          float lr, bool update) {
+  const int run = rh >> 1, h = rh & 1;
   const int c0 = (int)run_base[run], c1 = (int)run_base[run + 1];
-  // thread k owns elements k + 256 m (m < 8): eight independent loads per chunk
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  // thread k owns elements k + 512 m (m < 4): four independent loads per chunk
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int c = c0; c < c1; ++c) {
     const float* src = dBpart + ((size_t)h * nch_cap + c) * 2048 + threadIdx.x;
 #pragma unroll
-    for (int m = 0; m < 8; ++m) acc[m] += src[256 * m];
+    for (int m = 0; m < 4; ++m) acc[m] += src[RED_THREADS * m];
   }
 #pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const int e = (int)threadIdx.x + 256 * m;
+  for (int m = 0; m < 4; ++m) {
+    const int e = (int)threadIdx.x + RED_THREADS * m;
     const int a = e >> 6, j2 = (e >> 4) & 3, bp = e & 15;
     put_grad(dG2, (int64_t)run * 4096 + (a * 4 + j2) * 32 + 16 * h + bp, acc[m], lr, update);
   }
 }
 
-// dG3[t][i3][16 h + b'][j3] = sum over the workgroups that owned (t, h)
-__global__ void __launch_bounds__(256) k_reduce_g3(ShapeArgs s, const float* __restrict__ g3part, int nwg,
-                                                   float* __restrict__ dG3, float lr, bool update) {
+// dG3[t][i3][16 h + b'][j3] = sum over the workgroups that owned (t, h); block xb of
+// owner q covers accumulator elements [512 xb, 512 xb + 512)
+__device__ __forceinline__ void reduce_g3(int q, int xb, ShapeArgs s, const float* __restrict__ g3part, int nwg,
+                                          float* __restrict__ dG3, float lr, bool update) {
   const int nq = 2 * s.T;
-  const int q = blockIdx.y;
   const int t = q % s.T, h = q / s.T;
   const int acc_n = s.n3 * 128;
-  const int e = blockIdx.x * 256 + threadIdx.x;
+  const int e = xb * RED_THREADS + threadIdx.x;
   if (e >= acc_n) return;
   float acc = 0.f;
   for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
   const int i3 = e >> 7, j3 = (e >> 4) & 7, bp = g3_unslot(j3, e & 15);
   put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3, acc, lr, update);
+}
+
+// The three reductions in one launch, so they overlap: blocks [0, T n1) reduce dG1
+// (the longest, first), the next 2 T n2 blocks dG2, the rest dG3.
+__global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
+                                                              const uint32_t* __restrict__ dense_base,
+                                                              const float* __restrict__ dApart, int nsl_cap,
+                                                              const uint32_t* __restrict__ run_base,
+                                                              const float* __restrict__ dBpart, int nch_cap,
+                                                              const float* __restrict__ g3part, int nwg,
+                                                              float* __restrict__ dG1, float* __restrict__ dG2,
+                                                              float* __restrict__ dG3, float lr, bool update) {
+  const int b = blockIdx.x;
+  const int n1b = s.T * s.n1, n2b = 2 * s.T * s.n2;
+  if (b < n1b) {
+    reduce_g1(b, s, dense_cnt, dense_base, dApart, nsl_cap, dG1, lr, update);
+  } else if (b < n1b + n2b) {
+    reduce_g2(b - n1b, run_base, dBpart, nch_cap, dG2, lr, update);
+  } else {
+    const int per_q = (s.n3 * 128 + RED_THREADS - 1) / RED_THREADS;
+    const int r = b - n1b - n2b;
+    reduce_g3(r / per_q, r % per_q, s, g3part, nwg, dG3, lr, update);
+  }
 }
 
 bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
@@ -529,12 +570,11 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
                      (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.g3part,
                      (int)w.nsl_max, (int)w.nch_max);
   prof_end(prof, K_BWD_FUSED, st);
-  hipLaunchKernelGGL(k_reduce_g1, dim3(s.T * s.n1), dim3(512), 0, st, shape_args(s), (const uint32_t*)w.dense_cnt,
-                     (const uint32_t*)w.dense_base, (const float*)w.dApart, (int)w.nsl_max, dG1, lr, update);
-  hipLaunchKernelGGL(k_reduce_g2, dim3(s.T * s.n2 * 2), dim3(256), 0, st, (const uint32_t*)w.run_nch,
-                     (const float*)w.dBpart, (int)w.nch_max, dG2, lr, update);
-  hipLaunchKernelGGL(k_reduce_g3, dim3((s.n3 * 128 + 255) / 256, nq), dim3(256), 0, st, shape_args(s),
-                     (const float*)w.g3part, grid, dG3, lr, update);
+  const int red_blocks = s.T * s.n1 + 2 * s.T * s.n2 + nq * ((s.n3 * 128 + RED_THREADS - 1) / RED_THREADS);
+  hipLaunchKernelGGL(k_reduce_grads, dim3(red_blocks), dim3(RED_THREADS), 0, st, shape_args(s),
+                     (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const float*)w.dApart,
+                     (int)w.nsl_max, (const uint32_t*)w.run_nch, (const float*)w.dBpart, (int)w.nch_max,
+                     (const float*)w.g3part, grid, dG1, dG2, dG3, lr, update);
   return hipGetLastError();
 }
 
