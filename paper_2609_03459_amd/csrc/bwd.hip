@@ -212,47 +212,61 @@ __global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sor
 }
 
 // ---------------------------------------------------------------------------
-// generic per-slice backward (any shape; plain VALU; core gradients through
-// global atomics)
+// generic backward (any shape; plain VALU).  A block claims a chunk: up to 32
+// consecutive slices of one (t, i2) run, so every slice of it has the same
+// B = G2[t][i2].  Per slice: C (recomputed, or reloaded from the checkpoint),
+// dD per row into dG3, the dC of its rows summed, dA into dG1; dB = A^T (sum dC)
+// is summed over the chunk in LDS and added to dG2 once per chunk (per slice
+// when R * d2 * R is too large for LDS).  Core gradients meet in global atomics.
 // ---------------------------------------------------------------------------
 constexpr int BWD_THREADS = 256;
-constexpr int BWD_CHUNK = 4;
+constexpr int BWD_DB_LDS = 16384;  // largest R * d2 * R summed over a chunk in LDS
 
 __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const float* __restrict__ G1,
                                                              const float* __restrict__ G2,
                                                              const float* __restrict__ G3,
                                                              const int4* __restrict__ slices,
+                                                             const int4* __restrict__ chunks,
+                                                             const uint32_t* __restrict__ run_base,
                                                              const uint32_t* __restrict__ uniq_key,
                                                              int32_t* __restrict__ ctr, const float* __restrict__ dE,
                                                              float* __restrict__ dG1, float* __restrict__ dG2,
                                                              float* __restrict__ dG3, float* __restrict__ ckpt,
-                                                             int32_t* __restrict__ ckpt_tag) {
+                                                             int32_t* __restrict__ ckpt_tag, int db_lds) {
   extern __shared__ float lds[];
   const int d2R = s.d2 * s.R;
   const int nC = s.d1 * d2R;
+  const int nB = s.R * d2R;
   float* C = lds;           // nC
   float* dCs = lds + nC;    // nC: sum of dC over the slice's rows
   float* dEu = dCs + nC;    // D
+  float* dBs = dEu + s.D;   // nB when db_lds: dB summed over the chunk
   __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
-  const int nchunks = (nsl + BWD_CHUNK - 1) / BWD_CHUNK;
+  const int nchunks = (int)run_base[s.T * s.n2];
   int victim = 0;
   int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
   int cur_pg = -1;
   const int rows12 = s.d1 * s.d2;
   while (true) {
-    int c = claim_block_sched(s.sched, ctr + C_BWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk, &next);
+    const int c = claim_block_sched(s.sched, ctr + C_BWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk,
+                                    &next);
     if (c < 0) break;
-    const int s0 = c * BWD_CHUNK;
-    const int s1 = s0 + BWD_CHUNK < nsl ? s0 + BWD_CHUNK : nsl;
+    const int4 ch = chunks[c];
+    const int s0 = ch.x, s1 = ch.x + ch.y;
+    const int run = ch.z;  // t * n2 + i2
+    const int t = run / s.n2;
+    const float* Bm = G2 + (int64_t)run * nB;
+    float* g2 = dG2 + (int64_t)run * nB;
+    if (db_lds) {
+      __syncthreads();  // the previous chunk's flush has read dBs
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) dBs[o] = 0.f;
+    }
     for (int si = s0; si < s1; ++si) {
       const int4 sl = slices[si];
       const int p = sl.x, rb = sl.y, re = sl.z;
-      const uint32_t key = (uint32_t)sl.w;
-      const int t = key / s.n12, q = key % s.n12;
-      const int i1 = q / s.n2, i2 = q % s.n2;
+      const int i1 = (int)(((uint32_t)sl.w % (uint32_t)s.n12) / (uint32_t)s.n2);
       const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
-      const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
       __syncthreads();
       if (p != cur_pg) {
         // C recomputed, or with the checkpoint reloaded / published as in the forward
@@ -264,7 +278,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
             for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
             C[o] = acc;
           }
-          if (ck && s1 < nsl && slices[s1].x == p) {
+          if (ck && s1 < nsl && slices[s1].x == p) {  // the group goes on past this chunk
             __syncthreads();
             ckpt_store(ckpt, ckpt_tag, p, C, nC, &s_flag);
           }
@@ -303,14 +317,18 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
         for (int cc = 0; cc < d2R; ++cc) acc = fmaf(dCs[j1 * d2R + cc], Bm[a * d2R + cc], acc);
         unsafeAtomicAdd(&g1[o], acc);
       }
-      float* g2 = dG2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
-      for (int o = threadIdx.x; o < s.R * d2R; o += BWD_THREADS) {
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
         const int a = o / d2R, cc = o % d2R;
         float acc = 0.f;
         for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(A[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
-        unsafeAtomicAdd(&g2[o], acc);
+        if (db_lds)
+          dBs[o] += acc;  // each thread owns its elements across the chunk's slices
+        else
+          unsafeAtomicAdd(&g2[o], acc);
       }
     }
+    if (db_lds)
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) unsafeAtomicAdd(&g2[o], dBs[o]);
   }
 }
 
@@ -363,7 +381,9 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
     return e;
-  const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D);
+  const int nB = s.R * s.d2 * s.R;
+  const int db_lds = nB <= BWD_DB_LDS;
+  const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D + (db_lds ? nB : 0));
   if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
       hipSuccess)
     return e;
@@ -374,8 +394,9 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   }
   prof_begin(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
-                     (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3,
-                     w.ckpt, w.ckpt_tag);
+                     (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                     (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
+                     db_lds);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);
