@@ -60,10 +60,23 @@ class HipEvents:
         self.hip.hipEventDestroy(e)
 
 
-def source_digest() -> str:
+# Source files that define each benchmarked kernel and its launch (the counters
+# of a kernel stay valid while these files are unchanged).
+KERNEL_SOURCES = {
+    "bwd_fused": ["bwd_r32.hip", "common.h"],
+    "fwd_fused": ["fwd.hip", "common.h"],
+    "pool": ["fwd.hip", "common.h"],
+    "seg_sum": ["bwd.hip", "common.h"],
+    "ingest": ["group.hip", "common.h"],
+    "merge": ["cores.hip", "common.h"],
+    "split": ["cores.hip", "common.h"],
+}
+
+
+def source_digest(kernel: str) -> str:
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2609_03459_amd", "csrc")
-    for name in sorted(os.listdir(d)):
+    for name in KERNEL_SOURCES[kernel]:
         with open(os.path.join(d, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
@@ -153,7 +166,7 @@ def write_traffic(pmc_dir, copy_mib=1024, kernel="bwd_fused"):
             elif "elementwise" in name:
                 vals[c]["copy"].append(float(r["Counter_Value"]))
     true_kib = copy_mib * 1024.0
-    out = {"kernel": kernel, "symbol": sym, "source": source_digest(), "copy_mib": copy_mib}
+    out = {"kernel": kernel, "symbol": sym, "source": source_digest(kernel), "copy_mib": copy_mib}
     total = 0.0
     for c, v in vals.items():
         if not v["k"] or not v["copy"]:
@@ -451,7 +464,7 @@ def main():
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
     if os.path.exists(tpath):
         tr = json.load(open(tpath))
-        if tr.get("kernel") == dominant and tr.get("source") == source_digest():
+        if tr.get("kernel") == dominant and tr.get("source") == source_digest(dominant):
             roof["traffic"] = tr.get("bytes_per_launch")
     roof["kernel"] = dominant
     roof["kernel_ms"] = round(dom_ms, 4)
