@@ -234,3 +234,36 @@ def test_autograd_module_n(lib, orc):
         # the difference of two nearby floats adds |G| * 2^-24 / lr of rounding
         slack = np.abs(before[k].cpu().numpy()) * 2.0 ** -23 / lr
         assert_close(f"step dG{k + 1}", got, dref[k], dmag[k] + slack / TOL)
+
+
+def _random_shape(rng):
+    L = int(rng.integers(2, 8))
+    while True:
+        n = tuple(int(x) for x in rng.integers(1, 6, size=L))
+        d = tuple(int(x) for x in rng.integers(1, 4, size=L))
+        if np.prod(n) >= 2 and np.prod(d) <= 64:
+            break
+    R = int(rng.choice([1, 2, 3, 5, 8, 16]))
+    T = int(rng.integers(1, 4))
+    B = int(rng.integers(1, 40))
+    return T, n, d, R, B
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes_n(lib, orc, seed):
+    # seeded random L, factors (including 1), ranks and bag mixes; every third case
+    # regroups in the backward instead of reusing the forward's grouping
+    rng = np.random.default_rng([7700, seed])
+    T, n, d, R, B = _random_shape(rng)
+    case = ttgen.tiny_n(7700 + seed, T, n, d, R, B, max_len=int(rng.integers(0, 9)),
+                        zipf=1.2 if seed % 2 else None)
+    _say(f"[cores random {seed}] L={len(n)} T={T} n={n} d={d} R={R} B={B} M={case['idx'].size}")
+    emb = _make(lib, case)
+    cores, idx, off = _dev(case)
+    out = emb.forward_n(cores, idx, off, num_bags=B)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    grads = emb.backward_n(cores, idx, off, dV, num_bags=B, reuse_grouping=seed % 3 != 0)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    D = int(np.prod(d))
+    _check(orc, case, out.cpu().numpy().reshape(-1, D), [g.cpu().numpy() for g in grads], f"random {seed}")
