@@ -214,13 +214,52 @@ __global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sor
 // ---------------------------------------------------------------------------
 // generic backward (any shape; plain VALU).  A block claims a chunk: up to 32
 // consecutive slices of one (t, i2) run, so every slice of it has the same
-// B = G2[t][i2].  Per slice: C (recomputed, or reloaded from the checkpoint),
-// dD per row into dG3, the dC of its rows summed, dA into dG1; dB = A^T (sum dC)
-// is summed over the chunk in LDS and added to dG2 once per chunk (per slice
-// when R * d2 * R is too large for LDS).  Core gradients meet in global atomics.
+// B = G2[t][i2], which is staged in LDS once per chunk (rows padded by one float,
+// so reads across a's take distinct banks) when it fits.  Per slice: A staged; C
+// recomputed (or reloaded from the checkpoint); the slice's rows in batches whose
+// dE rows are staged together: dD per row into dG3, the rows' dC summed; then dA
+// into dG1 and dB = A^T (sum dC) summed over the chunk in LDS (added to dG2 once
+// per chunk) when it fits, else added per slice.  Core gradients meet in global
+// atomics.
 // ---------------------------------------------------------------------------
-constexpr int BWD_THREADS = 256;
-constexpr int BWD_DB_LDS = 16384;  // largest R * d2 * R summed over a chunk in LDS
+constexpr int BWD_THREADS = 1024;  // sixteen waves: with a block per CU, four per SIMD hide latency
+constexpr int BWD_LDS_FLOATS = 40448;  // dynamic LDS budget (158 KB of the 160 KB)
+constexpr int BWD_DE_FLOATS = 4096;    // dE rows staged per batch
+
+// sum over k < n of x[k * xs] * y[k * ys], four independent partial sums
+__device__ __forceinline__ float dot_strided(const float* x, int xs, const float* y, int ys, int n) {
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int k = 0;
+  for (; k + 4 <= n; k += 4) {
+    a0 = fmaf(x[k * xs], y[k * ys], a0);
+    a1 = fmaf(x[(k + 1) * xs], y[(k + 1) * ys], a1);
+    a2 = fmaf(x[(k + 2) * xs], y[(k + 2) * ys], a2);
+    a3 = fmaf(x[(k + 3) * xs], y[(k + 3) * ys], a3);
+  }
+  for (; k < n; ++k) a0 = fmaf(x[k * xs], y[k * ys], a0);
+  return (a0 + a1) + (a2 + a3);
+}
+
+struct GenericBwdPlan {
+  int stage_b;  // B in LDS
+  int db_lds;   // dB summed over the chunk in LDS
+  int rows;     // dE rows per batch
+  size_t lds_floats;
+};
+
+static GenericBwdPlan generic_bwd_plan(const Shape& s) {
+  GenericBwdPlan pl;
+  const size_t nC = (size_t)s.d1 * s.d2 * s.R, nB = (size_t)s.R * s.d2 * s.R;
+  const size_t bs = (size_t)s.R * (s.d2 * s.R + 1);
+  int rows = BWD_DE_FLOATS / s.D;
+  rows = rows < 1 ? 1 : (rows > SLICE_ROWS ? SLICE_ROWS : rows);
+  pl.rows = rows;
+  const size_t base = 2 * nC + (size_t)s.d1 * s.R + (size_t)rows * s.D;
+  pl.stage_b = base + bs <= (size_t)BWD_LDS_FLOATS;
+  pl.db_lds = base + (pl.stage_b ? bs : 0) + nB <= (size_t)BWD_LDS_FLOATS;
+  pl.lds_floats = base + (pl.stage_b ? bs : 0) + (pl.db_lds ? nB : 0);
+  return pl;
+}
 
 __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const float* __restrict__ G1,
                                                              const float* __restrict__ G2,
@@ -232,15 +271,19 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
                                                              int32_t* __restrict__ ctr, const float* __restrict__ dE,
                                                              float* __restrict__ dG1, float* __restrict__ dG2,
                                                              float* __restrict__ dG3, float* __restrict__ ckpt,
-                                                             int32_t* __restrict__ ckpt_tag, int db_lds) {
+                                                             int32_t* __restrict__ ckpt_tag, int stage_b, int db_lds,
+                                                             int rows_per_batch) {
   extern __shared__ float lds[];
   const int d2R = s.d2 * s.R;
   const int nC = s.d1 * d2R;
   const int nB = s.R * d2R;
-  float* C = lds;           // nC
-  float* dCs = lds + nC;    // nC: sum of dC over the slice's rows
-  float* dEu = dCs + nC;    // D
-  float* dBs = dEu + s.D;   // nB when db_lds: dB summed over the chunk
+  const int bp = stage_b ? d2R + 1 : d2R;  // row pitch of B as read below
+  float* C = lds;                          // nC
+  float* dCs = C + nC;                     // nC: sum of dC over the slice's rows
+  float* As = dCs + nC;                    // d1 * R
+  float* dEb = As + s.d1 * s.R;            // rows_per_batch * D
+  float* Bs = dEb + rows_per_batch * s.D;  // R * (d2R + 1) when stage_b
+  float* dBs = Bs + (stage_b ? s.R * bp : 0);  // nB when db_lds
   __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
   const int nchunks = (int)run_base[s.T * s.n2];
@@ -256,27 +299,33 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
     const int s0 = ch.x, s1 = ch.x + ch.y;
     const int run = ch.z;  // t * n2 + i2
     const int t = run / s.n2;
-    const float* Bm = G2 + (int64_t)run * nB;
+    const float* Bg = G2 + (int64_t)run * nB;
     float* g2 = dG2 + (int64_t)run * nB;
-    if (db_lds) {
-      __syncthreads();  // the previous chunk's flush has read dBs
+    __syncthreads();  // the previous chunk is done with Bs and dBs
+    if (stage_b)
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
+        const int a = o / d2R, cc = o - a * d2R;
+        Bs[a * bp + cc] = Bg[o];
+      }
+    const float* Bm = stage_b ? Bs : Bg;
+    if (db_lds)
       for (int o = threadIdx.x; o < nB; o += BWD_THREADS) dBs[o] = 0.f;
-    }
     for (int si = s0; si < s1; ++si) {
       const int4 sl = slices[si];
       const int p = sl.x, rb = sl.y, re = sl.z;
       const int i1 = (int)(((uint32_t)sl.w % (uint32_t)s.n12) / (uint32_t)s.n2);
-      const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+      const float* Ag = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+      __syncthreads();  // the previous slice is done with As, C and dCs
+      for (int o = threadIdx.x; o < s.d1 * s.R; o += BWD_THREADS) As[o] = Ag[o];
+      for (int o = threadIdx.x; o < nC; o += BWD_THREADS) dCs[o] = 0.f;
       __syncthreads();
       if (p != cur_pg) {
         // C recomputed, or with the checkpoint reloaded / published as in the forward
         const bool ck = s.sched == SCHED_STEAL_CKPT;
         if (!(ck && ckpt_load(ckpt, ckpt_tag, p, C, nC, &s_flag))) {
           for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
-            const int j1 = o / d2R, cc = o % d2R;
-            float acc = 0.f;
-            for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
-            C[o] = acc;
+            const int j1 = o / d2R, cc = o - j1 * d2R;
+            C[o] = dot_strided(As + j1 * s.R, 1, Bm + cc, bp, s.R);
           }
           if (ck && s1 < nsl && slices[s1].x == p) {  // the group goes on past this chunk
             __syncthreads();
@@ -284,27 +333,30 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
           }
         }
         cur_pg = p;
-      }
-      for (int o = threadIdx.x; o < nC; o += BWD_THREADS) dCs[o] = 0.f;
-      __syncthreads();
-      for (int u = rb; u < re; ++u) {
-        const int i3 = decode_key(uniq_key[u], s.Npad, s.n2, s.n3).i3;
-        const float* Dm = G3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3;
-        for (int j = threadIdx.x; j < s.D; j += BWD_THREADS) dEu[j] = dE[(int64_t)u * s.D + j];
         __syncthreads();
-        // dD_u = C^T dE_u  (R x d3)
-        float* g3 = dG3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3;
-        for (int o = threadIdx.x; o < s.R * s.d3; o += BWD_THREADS) {
-          const int b = o / s.d3, j3 = o % s.d3;
-          float acc = 0.f;
-          for (int r = 0; r < rows12; ++r) acc = fmaf(C[r * s.R + b], dEu[r * s.d3 + j3], acc);
-          unsafeAtomicAdd(&g3[o], acc);
+      }
+      for (int u0 = rb; u0 < re; u0 += rows_per_batch) {
+        const int nr = re - u0 < rows_per_batch ? re - u0 : rows_per_batch;
+        for (int o = threadIdx.x; o < nr * s.D; o += BWD_THREADS) dEb[o] = dE[(int64_t)u0 * s.D + o];
+        __syncthreads();
+        // dD_u = C^T dE_u  (R x d3) per row
+        for (int o = threadIdx.x; o < nr * s.R * s.d3; o += BWD_THREADS) {
+          const int rr = o / (s.R * s.d3), e = o - rr * (s.R * s.d3);
+          const int b = e / s.d3, j3 = e - b * s.d3;
+          const float acc = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
+          const int i3 = decode_key(uniq_key[u0 + rr], s.Npad, s.n2, s.n3).i3;
+          unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3 + j3], acc);
         }
-        // dC_u = dE_u D_u^T, summed over the slice
+        // dC = sum over the batch's rows of dE_u D_u^T
         for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
-          const int r = o / s.R, b = o % s.R;
+          const int r = o / s.R, b = o - r * s.R;
           float acc = 0.f;
-          for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(dEu[r * s.d3 + j3], Dm[b * s.d3 + j3], acc);
+          for (int rr = 0; rr < nr; ++rr) {
+            const int i3 = decode_key(uniq_key[u0 + rr], s.Npad, s.n2, s.n3).i3;
+            const float* Dm = G3 + ((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3;
+            const float* de = dEb + rr * s.D + r * s.d3;
+            for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(de[j3], Dm[j3], acc);
+          }
           dCs[o] += acc;
         }
         __syncthreads();
@@ -312,15 +364,13 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
       // dA = (sum dC) B^T  (d1 x R), dB = A^T (sum dC)  (R x d2R)
       float* g1 = dG1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
       for (int o = threadIdx.x; o < s.d1 * s.R; o += BWD_THREADS) {
-        const int j1 = o / s.R, a = o % s.R;
-        float acc = 0.f;
-        for (int cc = 0; cc < d2R; ++cc) acc = fmaf(dCs[j1 * d2R + cc], Bm[a * d2R + cc], acc);
-        unsafeAtomicAdd(&g1[o], acc);
+        const int j1 = o / s.R, a = o - j1 * s.R;
+        unsafeAtomicAdd(&g1[o], dot_strided(dCs + j1 * d2R, 1, Bm + a * bp, 1, d2R));
       }
       for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
-        const int a = o / d2R, cc = o % d2R;
+        const int a = o / d2R, cc = o - a * d2R;
         float acc = 0.f;
-        for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(A[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
+        for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(As[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
         if (db_lds)
           dBs[o] += acc;  // each thread owns its elements across the chunk's slices
         else
@@ -381,9 +431,8 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
     return e;
-  const int nB = s.R * s.d2 * s.R;
-  const int db_lds = nB <= BWD_DB_LDS;
-  const size_t lds = sizeof(float) * (2 * (size_t)s.d1 * s.d2 * s.R + s.D + (db_lds ? nB : 0));
+  const GenericBwdPlan pl = generic_bwd_plan(s);
+  const size_t lds = sizeof(float) * pl.lds_floats;
   if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
       hipSuccess)
     return e;
@@ -396,7 +445,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
                      (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
                      (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
-                     db_lds);
+                     pl.stage_b, pl.db_lds, pl.rows);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);
