@@ -222,7 +222,6 @@ __global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sor
 // per chunk) when it fits, else added per slice.  Core gradients meet in global
 // atomics.
 // ---------------------------------------------------------------------------
-constexpr int BWD_THREADS = 1024;  // sixteen waves: with a block per CU, four per SIMD hide latency
 constexpr int BWD_LDS_FLOATS = 40448;  // dynamic LDS budget (158 KB of the 160 KB)
 constexpr int BWD_DE_FLOATS = 4096;    // dE rows staged per batch
 
@@ -261,6 +260,9 @@ static GenericBwdPlan generic_bwd_plan(const Shape& s) {
   return pl;
 }
 
+// BWD_THREADS = 1024 (sixteen waves: at a block per CU, four per SIMD hide latency)
+// for large products, 256 for small ones (where a block's barriers dominate)
+template <int BWD_THREADS>
 __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const float* __restrict__ G1,
                                                              const float* __restrict__ G2,
                                                              const float* __restrict__ G3,
@@ -433,19 +435,25 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
     return e;
   const GenericBwdPlan pl = generic_bwd_plan(s);
   const size_t lds = sizeof(float) * pl.lds_floats;
-  if ((e = hipFuncSetAttribute((const void*)k_bwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) !=
-      hipSuccess)
-    return e;
+  const bool wide = (int64_t)s.d1 * s.d2 * s.R >= 1024 || s.D >= 128;
+  const void* kfn = wide ? (const void*)k_bwd_generic<1024> : (const void*)k_bwd_generic<256>;
+  if ((e = hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess) return e;
   if (s.sched == SCHED_STEAL_CKPT) {  // the forward's checkpoints may hold other cores' C
     if (!w.ckpt_tag) return hipErrorInvalidValue;
     if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ckpt_tag), CKPT_SLOTS, (uint32_t)CKPT_EMPTY, st)) != hipSuccess)
       return e;
   }
   prof_begin(prof, K_BWD_FUSED, st);
-  hipLaunchKernelGGL(k_bwd_generic, dim3(grid), dim3(BWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
-                     (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                     (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
-                     pl.stage_b, pl.db_lds, pl.rows);
+  if (wide)
+    hipLaunchKernelGGL(k_bwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
+                       (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                       (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
+                       pl.stage_b, pl.db_lds, pl.rows);
+  else
+    hipLaunchKernelGGL(k_bwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
+                       (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                       (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
+                       pl.stage_b, pl.db_lds, pl.rows);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);

@@ -24,29 +24,57 @@ ShapeArgs shape_args(const Shape& s) {
   return a;
 }
 
-constexpr int FWD_THREADS = 256;
-constexpr int FWD_CHUNK = 8;  // slices per scheduler chunk
+constexpr int FWD_LDS_FLOATS = 40448;    // dynamic LDS budget (158 KB of the 160 KB)
+constexpr int FWD_CHUNK = 8;             // slices per claim
 
-// Generic fused forward for any shape within the library limits (plain VALU).
+// sum over k < n of x[k * xs] * y[k * ys], four independent partial sums
+__device__ __forceinline__ float fdot_strided(const float* x, int xs, const float* y, int ys, int n) {
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int k = 0;
+  for (; k + 4 <= n; k += 4) {
+    a0 = fmaf(x[k * xs], y[k * ys], a0);
+    a1 = fmaf(x[(k + 1) * xs], y[(k + 1) * ys], a1);
+    a2 = fmaf(x[(k + 2) * xs], y[(k + 2) * ys], a2);
+    a3 = fmaf(x[(k + 3) * xs], y[(k + 3) * ys], a3);
+  }
+  for (; k < n; ++k) a0 = fmaf(x[k * xs], y[k * ys], a0);
+  return (a0 + a1) + (a2 + a3);
+}
+
+// Generic fused forward for any shape within the library limits (plain VALU).  A
+// block claims FWD_CHUNK consecutive slices; B = G2[t][i2] of their (t, i2) run is
+// staged in LDS (rows padded by one float) when it fits, again whenever the run
+// changes; per slice A is staged, C = A.B is built once per prefix group and
+// E = C.D per row.
+// FWD_THREADS = 1024 (sixteen waves: latency hiding at one block per CU) for large
+// products, 256 for small ones (where a block's barriers dominate)
+template <int FWD_THREADS>
 __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const float* __restrict__ G1,
                                                              const float* __restrict__ G2,
                                                              const float* __restrict__ G3,
                                                              const int4* __restrict__ slices,
                                                              const uint32_t* __restrict__ uniq_key,
                                                              int32_t* __restrict__ ctr, float* __restrict__ E,
-                                                             float* __restrict__ ckpt, int32_t* __restrict__ ckpt_tag) {
+                                                             float* __restrict__ ckpt, int32_t* __restrict__ ckpt_tag,
+                                                             int stage_b) {
   extern __shared__ float lds[];
-  float* C = lds;  // d1 * d2 * R
+  const int d2R = s.d2 * s.R;
+  const int nC = s.d1 * d2R;
+  const int nB = s.R * d2R;
+  const int bp = stage_b ? d2R + 1 : d2R;
+  float* C = lds;            // nC = d1 * d2 * R
+  float* As = C + nC;        // d1 * R
+  float* Bs = As + s.d1 * s.R;  // R * (d2R + 1) when stage_b
   __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
   const int nchunks = (nsl + FWD_CHUNK - 1) / FWD_CHUNK;
-  const int d2R = s.d2 * s.R;
-  const int nC = s.d1 * d2R;
   int victim = 0;
   int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
-  int cur_pg = -1;
+  int cur_pg = -1, cur_run = -1;
+  const float* Bm = G2;
   while (true) {
-    int c = claim_block_sched(s.sched, ctr + C_FWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk, &next);
+    const int c = claim_block_sched(s.sched, ctr + C_FWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk,
+                                    &next);
     if (c < 0) break;
     const int s0 = c * FWD_CHUNK;
     const int s1 = s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl;
@@ -54,24 +82,33 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
       const int4 sl = slices[si];
       const int p = sl.x, rb = sl.y, re = sl.z;
       const uint32_t key = (uint32_t)sl.w;
-      const int t = key / s.n12, q = key % s.n12;
-      const int i1 = q / s.n2, i2 = q % s.n2;
+      const int t = (int)(key / (uint32_t)s.n12), q = (int)(key % (uint32_t)s.n12);
+      const int i1 = q / s.n2, run = t * s.n2 + q % s.n2;
       if (p != cur_pg) {
         // intermediate C = A.B, kept in LDS while rows of this group follow; with
         // the checkpoint, reloaded if another block published it, and published if
-        // the group goes on past this chunk (where a stealing block may meet it)
-        __syncthreads();
+        // the group goes on past this claim (where a stealing block may meet it)
+        __syncthreads();  // the previous slice's rows are done with C
         const bool ck = s.sched == SCHED_STEAL_CKPT;
         if (!(ck && ckpt_load(ckpt, ckpt_tag, p, C, nC, &s_flag))) {
-          const float* A = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
-          const float* Bm = G2 + (int64_t)(t * s.n2 + i2) * s.R * d2R;
-          for (int o = threadIdx.x; o < nC; o += FWD_THREADS) {
-            const int j1 = o / d2R, cc = o % d2R;
-            float acc = 0.f;
-            for (int a = 0; a < s.R; ++a) acc = fmaf(A[j1 * s.R + a], Bm[a * d2R + cc], acc);
-            C[o] = acc;
+          const float* Bg = G2 + (int64_t)run * nB;
+          if (run != cur_run) {
+            if (stage_b)
+              for (int o = threadIdx.x; o < nB; o += FWD_THREADS) {
+                const int a = o / d2R, cc = o - a * d2R;
+                Bs[a * bp + cc] = Bg[o];
+              }
+            Bm = stage_b ? Bs : Bg;
+            cur_run = run;
           }
-          if (ck && s1 < nsl && slices[s1].x == p) {
+          const float* Ag = G1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+          for (int o = threadIdx.x; o < s.d1 * s.R; o += FWD_THREADS) As[o] = Ag[o];
+          __syncthreads();
+          for (int o = threadIdx.x; o < nC; o += FWD_THREADS) {
+            const int j1 = o / d2R, cc = o - j1 * d2R;
+            C[o] = fdot_strided(As + j1 * s.R, 1, Bm + cc, bp, s.R);
+          }
+          if (ck && s1 < nsl && slices[s1].x == p) {  // the group goes on past this claim
             __syncthreads();
             ckpt_store(ckpt, ckpt_tag, p, C, nC, &s_flag);
           }
@@ -82,19 +119,16 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
       // embedding rows E_u = C . D_u, C viewed as (d1 d2) x R
       const int total = (re - rb) * s.D;
       for (int o = threadIdx.x; o < total; o += FWD_THREADS) {
-        const int r = o / s.D, j = o % s.D;
+        const int r = o / s.D, j = o - r * s.D;
         const int u = rb + r;
         const int i3 = decode_key(uniq_key[u], s.Npad, s.n2, s.n3).i3;
-        const int jr = j / s.d3, j3 = j % s.d3;
-        const float* Dm = G3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3;
-        float acc = 0.f;
-        for (int b = 0; b < s.R; ++b) acc = fmaf(C[jr * s.R + b], Dm[b * s.d3 + j3], acc);
-        E[(int64_t)u * s.D + j] = acc;
+        const int jr = j / s.d3, j3 = j - jr * s.d3;
+        const float* Dm = G3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3 + j3;
+        E[(int64_t)u * s.D + j] = fdot_strided(C + jr * s.R, 1, Dm, s.d3, s.R);
       }
     }
   }
 }
-
 
 // ---------------------------------------------------------------------------
 // MFMA forward for d = (4, 4, 8), R = 32 (D = 128).  Persistent waves claim
@@ -755,8 +789,13 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
       if (e != hipSuccess) return e;
       return launch_pool(s, w.E, w.inv, offsets, M, B, out, prof, st);
     }
-    const size_t lds = sizeof(float) * (size_t)s.d1 * s.d2 * s.R;
-    e = hipFuncSetAttribute((const void*)k_fwd_generic, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const size_t nC = (size_t)s.d1 * s.d2 * s.R, nA = (size_t)s.d1 * s.R;
+    const size_t bs = (size_t)s.R * (s.d2 * s.R + 1);
+    const int stage_b = nC + nA + bs <= (size_t)FWD_LDS_FLOATS;
+    const size_t lds = sizeof(float) * (nC + nA + (stage_b ? bs : 0));
+    const bool wide = nC >= 1024 || s.D >= 128;
+    const void* kfn = wide ? (const void*)k_fwd_generic<1024> : (const void*)k_fwd_generic<256>;
+    e = hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     if (s.sched == SCHED_STEAL_CKPT) {  // checkpoints of earlier calls may hold other cores' C
       if (!w.ckpt_tag) return hipErrorInvalidValue;
@@ -764,8 +803,14 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
       if (e != hipSuccess) return e;
     }
     prof_begin(prof, K_FWD_FUSED, st);
-    hipLaunchKernelGGL(k_fwd_generic, dim3(grid), dim3(FWD_THREADS), lds, st, shape_args(s), G1, G2, G3,
-                       (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag);
+    if (wide)
+      hipLaunchKernelGGL(k_fwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
+                         (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag,
+                         stage_b);
+    else
+      hipLaunchKernelGGL(k_fwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
+                         (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag,
+                         stage_b);
     prof_end(prof, K_FWD_FUSED, st);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
