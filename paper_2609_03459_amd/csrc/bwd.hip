@@ -269,7 +269,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
                                                              const int4* __restrict__ slices,
                                                              const int4* __restrict__ chunks,
                                                              const uint32_t* __restrict__ run_base,
-                                                             const uint32_t* __restrict__ uniq_key,
+                                                             const int32_t* __restrict__ uniq_i3,
                                                              int32_t* __restrict__ ctr, const float* __restrict__ dE,
                                                              float* __restrict__ dG1, float* __restrict__ dG2,
                                                              float* __restrict__ dG3, float* __restrict__ ckpt,
@@ -346,7 +346,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
           const int rr = o / (s.R * s.d3), e = o - rr * (s.R * s.d3);
           const int b = e / s.d3, j3 = e - b * s.d3;
           const float acc = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
-          const int i3 = decode_key(uniq_key[u0 + rr], s.Npad, s.n2, s.n3).i3;
+          const int i3 = uniq_i3[u0 + rr];
           unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3 + j3], acc);
         }
         // dC = sum over the batch's rows of dE_u D_u^T
@@ -354,7 +354,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
           const int r = o / s.R, b = o - r * s.R;
           float acc = 0.f;
           for (int rr = 0; rr < nr; ++rr) {
-            const int i3 = decode_key(uniq_key[u0 + rr], s.Npad, s.n2, s.n3).i3;
+            const int i3 = uniq_i3[u0 + rr];
             const float* Dm = G3 + ((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3;
             const float* de = dEb + rr * s.D + r * s.d3;
             for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(de[j3], Dm[j3], acc);
@@ -447,12 +447,12 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   if (wide)
     hipLaunchKernelGGL(k_bwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
                        (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                       (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
+                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
                        pl.stage_b, pl.db_lds, pl.rows);
   else
     hipLaunchKernelGGL(k_bwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
                        (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                       (const uint32_t*)w.uniq_key, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
+                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
                        pl.stage_b, pl.db_lds, pl.rows);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -53,7 +53,7 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
                                                              const float* __restrict__ G2,
                                                              const float* __restrict__ G3,
                                                              const int4* __restrict__ slices,
-                                                             const uint32_t* __restrict__ uniq_key,
+                                                             const int32_t* __restrict__ uniq_i3,
                                                              int32_t* __restrict__ ctr, float* __restrict__ E,
                                                              float* __restrict__ ckpt, int32_t* __restrict__ ckpt_tag,
                                                              int stage_b) {
@@ -121,7 +121,7 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
       for (int o = threadIdx.x; o < total; o += FWD_THREADS) {
         const int r = o / s.D, j = o - r * s.D;
         const int u = rb + r;
-        const int i3 = decode_key(uniq_key[u], s.Npad, s.n2, s.n3).i3;
+        const int i3 = uniq_i3[u];
         const int jr = j / s.d3, j3 = j - jr * s.d3;
         const float* Dm = G3 + (int64_t)(t * s.n3 + i3) * s.R * s.d3 + j3;
         E[(int64_t)u * s.D + j] = fdot_strided(C + jr * s.R, 1, Dm, s.d3, s.R);
@@ -805,11 +805,11 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
     prof_begin(prof, K_FWD_FUSED, st);
     if (wide)
       hipLaunchKernelGGL(k_fwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
-                         (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag,
+                         (const int4*)w.slices, (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag,
                          stage_b);
     else
       hipLaunchKernelGGL(k_fwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
-                         (const int4*)w.slices, (const uint32_t*)w.uniq_key, w.ctr, w.E, w.ckpt, w.ckpt_tag,
+                         (const int4*)w.slices, (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag,
                          stage_b);
     prof_end(prof, K_FWD_FUSED, st);
     e = hipGetLastError();
