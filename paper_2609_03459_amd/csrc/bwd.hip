@@ -293,6 +293,8 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
   int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
   int cur_pg = -1;
   const int rows12 = s.d1 * s.d2;
+  // lanes per dC output: 4, 2 or 1, so that the phase keeps the block's threads busy
+  const int g_dc = nC * 4 <= BWD_THREADS ? 4 : (nC * 2 <= BWD_THREADS ? 2 : 1);
   while (true) {
     const int c = claim_block_sched(s.sched, ctr + C_BWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk,
                                     &next);
@@ -349,25 +351,42 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
           const int i3 = uniq_i3[u0 + rr];
           unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3 + j3], acc);
         }
-        // dC = sum over the batch's rows of dE_u D_u^T
-        for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
+        // dC = sum over the batch's rows of dE_u D_u^T; with fewer outputs than threads,
+        // g consecutive lanes share an output (each every g-th row), combined by shuffles
+        for (int base = 0; base < g_dc * nC; base += BWD_THREADS) {
+          const int og = base + (int)threadIdx.x;
+          const bool ok = og < g_dc * nC;
+          const int o = ok ? og / g_dc : 0, part = og - (og / g_dc) * g_dc;
           const int r = o / s.R, b = o - r * s.R;
           float acc = 0.f;
-          for (int rr = 0; rr < nr; ++rr) {
-            const int i3 = uniq_i3[u0 + rr];
-            const float* Dm = G3 + ((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3;
-            const float* de = dEb + rr * s.D + r * s.d3;
-            for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(de[j3], Dm[j3], acc);
-          }
-          dCs[o] += acc;
+          if (ok)
+            for (int rr = part; rr < nr; rr += g_dc) {
+              const int i3 = uniq_i3[u0 + rr];
+              const float* Dm = G3 + ((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3;
+              const float* de = dEb + rr * s.D + r * s.d3;
+              for (int j3 = 0; j3 < s.d3; ++j3) acc = fmaf(de[j3], Dm[j3], acc);
+            }
+          if (g_dc >= 2) acc += __shfl_xor(acc, 1, 64);
+          if (g_dc >= 4) acc += __shfl_xor(acc, 2, 64);
+          if (ok && part == 0) dCs[o] += acc;
         }
         __syncthreads();
       }
       // dA = (sum dC) B^T  (d1 x R), dB = A^T (sum dC)  (R x d2R)
+      // dA: four consecutive lanes per output, each over every fourth term, combined by
+      // shuffles within the wave (the loop runs whole block strides so every lane takes
+      // part in the shuffles)
       float* g1 = dG1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
-      for (int o = threadIdx.x; o < s.d1 * s.R; o += BWD_THREADS) {
+      for (int base = 0; base < 4 * s.d1 * s.R; base += BWD_THREADS) {
+        const int o4 = base + (int)threadIdx.x;
+        const bool ok = o4 < 4 * s.d1 * s.R;
+        const int o = ok ? o4 >> 2 : 0, part = o4 & 3;
         const int j1 = o / s.R, a = o - j1 * s.R;
-        unsafeAtomicAdd(&g1[o], dot_strided(dCs + j1 * d2R, 1, Bm + a * bp, 1, d2R));
+        const int nterm = d2R > part ? (d2R - part + 3) >> 2 : 0;
+        float v = ok ? dot_strided(dCs + j1 * d2R + part, 4, Bm + a * bp + part, 4, nterm) : 0.f;
+        v += __shfl_xor(v, 1, 64);
+        v += __shfl_xor(v, 2, 64);
+        if (ok && part == 0) unsafeAtomicAdd(&g1[o], v);
       }
       for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
         const int a = o / d2R, cc = o - a * d2R;
