@@ -225,6 +225,26 @@ __global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sor
 constexpr int BWD_LDS_FLOATS = 40448;  // dynamic LDS budget (158 KB of the 160 KB)
 constexpr int BWD_DE_FLOATS = 4096;    // dE rows staged per batch
 
+// o = q * div + r along o = o0, o0 + step, ...: the quotient and remainder kept by
+// increments (one division at the start, none per step)
+struct StepQR {
+  int q, r, dq, dr, div;
+  __device__ __forceinline__ StepQR(int o0, int step, int d) : div(d) {
+    q = o0 / d;
+    r = o0 - q * d;
+    dq = step / d;
+    dr = step - dq * d;
+  }
+  __device__ __forceinline__ void next() {
+    q += dq;
+    r += dr;
+    if (r >= div) {
+      r -= div;
+      ++q;
+    }
+  }
+};
+
 // sum over k < n of x[k * xs] * y[k * ys], four independent partial sums
 __device__ __forceinline__ float dot_strided(const float* x, int xs, const float* y, int ys, int n) {
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
@@ -295,6 +315,10 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
   const int rows12 = s.d1 * s.d2;
   // lanes per dC output: 4, 2 or 1, so that the phase keeps the block's threads busy
   const int g_dc = nC * 4 <= BWD_THREADS ? 4 : (nC * 2 <= BWD_THREADS ? 2 : 1);
+  const int g_dc_shift = g_dc == 4 ? 2 : (g_dc == 2 ? 1 : 0);
+  // dD tasks: each of the R d3 elements taken by g_dd threads (over every g_dd-th row)
+  const int RD = s.R * s.d3;
+  const int g_dd = RD >= BWD_THREADS ? 1 : (BWD_THREADS / RD < SLICE_ROWS ? BWD_THREADS / RD : SLICE_ROWS);
   while (true) {
     const int c = claim_block_sched(s.sched, ctr + C_BWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk,
                                     &next);
@@ -306,11 +330,10 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
     const float* Bg = G2 + (int64_t)run * nB;
     float* g2 = dG2 + (int64_t)run * nB;
     __syncthreads();  // the previous chunk is done with Bs and dBs
-    if (stage_b)
-      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
-        const int a = o / d2R, cc = o - a * d2R;
-        Bs[a * bp + cc] = Bg[o];
-      }
+    if (stage_b) {
+      StepQR ix(threadIdx.x, BWD_THREADS, d2R);
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS, ix.next()) Bs[ix.q * bp + ix.r] = Bg[o];
+    }
     const float* Bm = stage_b ? Bs : Bg;
     if (db_lds)
       for (int o = threadIdx.x; o < nB; o += BWD_THREADS) dBs[o] = 0.f;
@@ -327,10 +350,9 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
         // C recomputed, or with the checkpoint reloaded / published as in the forward
         const bool ck = s.sched == SCHED_STEAL_CKPT;
         if (!(ck && ckpt_load(ckpt, ckpt_tag, p, C, nC, &s_flag))) {
-          for (int o = threadIdx.x; o < nC; o += BWD_THREADS) {
-            const int j1 = o / d2R, cc = o - j1 * d2R;
-            C[o] = dot_strided(As + j1 * s.R, 1, Bm + cc, bp, s.R);
-          }
+          StepQR ix(threadIdx.x, BWD_THREADS, d2R);  // (j1, column)
+          for (int o = threadIdx.x; o < nC; o += BWD_THREADS, ix.next())
+            C[o] = dot_strided(As + ix.q * s.R, 1, Bm + ix.r, bp, s.R);
           if (ck && s1 < nsl && slices[s1].x == p) {  // the group goes on past this chunk
             __syncthreads();
             ckpt_store(ckpt, ckpt_tag, p, C, nC, &s_flag);
@@ -343,21 +365,24 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
         const int nr = re - u0 < rows_per_batch ? re - u0 : rows_per_batch;
         for (int o = threadIdx.x; o < nr * s.D; o += BWD_THREADS) dEb[o] = dE[(int64_t)u0 * s.D + o];
         __syncthreads();
-        // dD_u = C^T dE_u  (R x d3) per row
-        for (int o = threadIdx.x; o < nr * s.R * s.d3; o += BWD_THREADS) {
-          const int rr = o / (s.R * s.d3), e = o - rr * (s.R * s.d3);
+        // dD_u = C^T dE_u  (R x d3) per row: task (part, e) takes element e = (b, j3) of
+        // rows part, part + g_dd, ... of the batch
+        for (int tk = threadIdx.x; tk < g_dd * RD; tk += BWD_THREADS) {
+          const int part = tk / RD, e = tk - part * RD;
           const int b = e / s.d3, j3 = e - b * s.d3;
-          const float acc = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
-          const int i3 = uniq_i3[u0 + rr];
-          unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + i3) * s.R + b) * s.d3 + j3], acc);
+          for (int rr = part; rr < nr; rr += g_dd) {
+            const float acc = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
+            unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + uniq_i3[u0 + rr]) * s.R + b) * s.d3 + j3], acc);
+          }
         }
         // dC = sum over the batch's rows of dE_u D_u^T; with fewer outputs than threads,
         // g consecutive lanes share an output (each every g-th row), combined by shuffles
-        for (int base = 0; base < g_dc * nC; base += BWD_THREADS) {
+        StepQR dcx((int)threadIdx.x >> g_dc_shift, BWD_THREADS >> g_dc_shift, s.R);  // (r, b) of o
+        for (int base = 0; base < g_dc * nC; base += BWD_THREADS, dcx.next()) {
           const int og = base + (int)threadIdx.x;
           const bool ok = og < g_dc * nC;
-          const int o = ok ? og / g_dc : 0, part = og - (og / g_dc) * g_dc;
-          const int r = o / s.R, b = o - r * s.R;
+          const int o = og >> g_dc_shift, part = og & (g_dc - 1);
+          const int r = dcx.q, b = dcx.r;
           float acc = 0.f;
           if (ok)
             for (int rr = part; rr < nr; rr += g_dc) {
@@ -377,19 +402,21 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
       // shuffles within the wave (the loop runs whole block strides so every lane takes
       // part in the shuffles)
       float* g1 = dG1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
-      for (int base = 0; base < 4 * s.d1 * s.R; base += BWD_THREADS) {
+      StepQR dax((int)threadIdx.x >> 2, BWD_THREADS >> 2, s.R);  // (j1, a) of o
+      for (int base = 0; base < 4 * s.d1 * s.R; base += BWD_THREADS, dax.next()) {
         const int o4 = base + (int)threadIdx.x;
         const bool ok = o4 < 4 * s.d1 * s.R;
-        const int o = ok ? o4 >> 2 : 0, part = o4 & 3;
-        const int j1 = o / s.R, a = o - j1 * s.R;
+        const int o = o4 >> 2, part = o4 & 3;
+        const int j1 = ok ? dax.q : 0, a = ok ? dax.r : 0;
         const int nterm = d2R > part ? (d2R - part + 3) >> 2 : 0;
         float v = ok ? dot_strided(dCs + j1 * d2R + part, 4, Bm + a * bp + part, 4, nterm) : 0.f;
         v += __shfl_xor(v, 1, 64);
         v += __shfl_xor(v, 2, 64);
         if (ok && part == 0) unsafeAtomicAdd(&g1[o], v);
       }
-      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) {
-        const int a = o / d2R, cc = o - a * d2R;
+      StepQR dbx(threadIdx.x, BWD_THREADS, d2R);  // (a, column)
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS, dbx.next()) {
+        const int a = dbx.q, cc = dbx.r;
         float acc = 0.f;
         for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(As[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
         if (db_lds)
