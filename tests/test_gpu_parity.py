@@ -324,6 +324,17 @@ def test_backward_small(lib, orc, k):
     check_backward(lib, orc, case, name=f"tiny{k}")
 
 
+@pytest.mark.parametrize("T,n", [
+    (2, (6, 5, 252)),   # MFMA backward at its limit: the dG3 half plus scratch fill all 160 KB of LDS
+    (2, (6, 5, 253)),   # one past it: the generic kernels
+    (64, (2, 2, 9)),    # MFMA backward at its table limit (64 tables, 128 owners)
+])
+def test_backward_shape_limits(lib, orc, T, n):
+    case = ttgen.tiny(3100 + n[2] + T, T, n, (4, 4, 8), 32, B=24, max_len=10, zipf=1.1)
+    check_backward(lib, orc, case, name=f"limits T={T} n3={n[2]}")
+    check_forward(lib, orc, case, name=f"limits T={T} n3={n[2]}")
+
+
 def test_backward_config5_small_batch(lib, orc):
     check_backward(lib, orc, ttgen.make(5, bags=64), name="config5 B=64")
 
