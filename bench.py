@@ -142,7 +142,20 @@ KERNEL_SYMBOL = {"fwd_fused": "k_fwd_r32", "bwd_fused": "k_bwd_r32", "pool": "k_
                  "ingest": "k_ingest"}
 
 
-def write_traffic(pmc_dir, copy_mib=1024, kernel="bwd_fused"):
+def run_key(args):
+    """What a counter measurement holds for: the workload and the flags that change the kernels' work."""
+    import ttgen
+
+    name = ttgen.CONFIGS[args.config]["workload"]
+    if args.row_factors or args.cores != 3:
+        L = len(args.row_factors.split(",")) if args.row_factors else args.cores
+        name += f"_{L}cores"
+        if args.row_factors:
+            name += f"[{args.row_factors}|{args.dim_factors}]"
+    return {"workload": name, "reuse": args.reuse, "sched": args.sched, "fused_sgd": not args.unfused_sgd}
+
+
+def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused"):
     """HBM bytes per launch of `kernel` from rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch).
 
     Each counter is scaled by the factor that makes it read the true size on the
@@ -166,7 +179,7 @@ def write_traffic(pmc_dir, copy_mib=1024, kernel="bwd_fused"):
             elif "elementwise" in name:
                 vals[c]["copy"].append(float(r["Counter_Value"]))
     true_kib = copy_mib * 1024.0
-    out = {"kernel": kernel, "symbol": sym, "source": source_digest(kernel), "copy_mib": copy_mib}
+    out = {"kernel": kernel, "symbol": sym, "source": source_digest(kernel), "run": key, "copy_mib": copy_mib}
     total = 0.0
     for c, v in vals.items():
         if not v["k"] or not v["copy"]:
@@ -282,14 +295,14 @@ def main():
                     help="also run one plain elementwise copy of this many MiB (counter calibration runs)")
     ap.add_argument("--write-traffic", metavar="DIR", default=None,
                     help="CPU only: turn the FETCH_SIZE / WRITE_SIZE counter CSVs under DIR (one rocprofv3 --pmc "
-                         "pass each, of a run with --copy-mib) into profiles/traffic.json, then exit")
+                         "pass each, of a run with --copy-mib and the same workload flags) into "
+                         "profiles/traffic.json, then exit")
     args = ap.parse_args()
     if args.write_traffic:
-        write_traffic(args.write_traffic)
+        write_traffic(args.write_traffic, run_key(args))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(the sharding design is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -448,6 +461,11 @@ def main():
     phases_ms = {k: round(float(np.median(v)), 4) for k, v in phases.items()}
 
     work, unit, bound = algorithmic_work(dominant, case, counts)
+    # the fused kernels run on the matrix cores only for the shapes the MFMA kernels serve
+    on_mfma = dominant in ("fwd_fused", "bwd_fused") and P.N.tt_emb_kernel_uses_mfma(
+        emb.handle, P.N.KERNELS[dominant], M)
+    if bound == "mfma" and not on_mfma:
+        bound = "alu"
     if unit == "flop" and bound == "alu":
         achieved = work / (dom_ms * 1e-3) / 1e12
         roof = dict(bound=bound, achieved=round(achieved, 3), peak=PEAK_FP32_VALU / 1e12, unit="TFLOP/s",
@@ -464,7 +482,9 @@ def main():
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
     if os.path.exists(tpath):
         tr = json.load(open(tpath))
-        if tr.get("kernel") == dominant and tr.get("source") == source_digest(dominant):
+        if (tr.get("kernel") == dominant and tr.get("source") == source_digest(dominant)
+                and tr.get("run") == run_key(args) and tr.get("symbol") == KERNEL_SYMBOL[dominant]
+                and on_mfma):
             roof["traffic"] = tr.get("bytes_per_launch")
     roof["kernel"] = dominant
     roof["kernel_ms"] = round(dom_ms, 4)

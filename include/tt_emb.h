@@ -289,6 +289,17 @@ typedef enum {
  * stay owned by the caller. */
 tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* ev_end);
 
+/* Whether `kernel` (TT_EMB_K_FWD_FUSED or TT_EMB_K_BWD_FUSED) runs on the
+ * matrix cores for this handle: *uses_mfma = 1 for the MFMA kernels (forward
+ * for the view d = (4,4,8) with R = 32 or 64, backward for d = (4,4,8) with
+ * R = 32 and n3 <= 252), 0 for the generic vector-ALU kernels.  The forward
+ * decides per call from its index count, given here as num_indices
+ * (0 <= num_indices <= desc.max_indices); the backward decides from
+ * desc.max_indices.  Every other kernel id reports 0.  Host only.
+ * TT_EMB_EINVAL for a NULL handle or flag, an unknown kernel id or
+ * num_indices out of range. */
+tt_emb_status tt_emb_kernel_uses_mfma(tt_emb_handle h, int kernel, int64_t num_indices, int* uses_mfma);
+
 /* Static text for a status code. */
 const char* tt_emb_status_string(tt_emb_status s);
 

@@ -70,6 +70,7 @@ _SIG = {
     "tt_emb_debug_grouping": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
     "tt_emb_status_string": ([C.c_int], C.c_char_p),
     "tt_emb_profile": ([_P, C.c_int, _P, _P], C.c_int),
+    "tt_emb_kernel_uses_mfma": ([_P, C.c_int, C.c_int64, C.POINTER(C.c_int)], C.c_int),
     "tt_emb_set_reuse": ([_P, C.c_int], C.c_int),
     "tt_emb_set_schedule": ([_P, C.c_int], C.c_int),
     "tt_emb_create_n": ([C.POINTER(tt_emb_desc_n), C.POINTER(_P)], C.c_int),
@@ -184,3 +185,9 @@ def tt_emb_set_schedule(h, mode: int) -> None:
 
 def tt_emb_profile(h, kernel: int, ev_begin, ev_end) -> None:
     check("tt_emb_profile", lib.tt_emb_profile(h, int(kernel), ev_begin, ev_end))
+
+
+def tt_emb_kernel_uses_mfma(h, kernel: int, num_indices: int) -> bool:
+    flag = C.c_int(-1)
+    check("tt_emb_kernel_uses_mfma", lib.tt_emb_kernel_uses_mfma(h, int(kernel), int(num_indices), C.byref(flag)))
+    return bool(flag.value)

@@ -159,8 +159,9 @@ int64_t chain_level_floats(const Shape& s);
 hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.
 bool bwd_r32_supported(const Shape& s, int64_t max_indices);
-// Whether the MFMA forward serves this shape.
+// Whether the MFMA forward serves this shape (R = 32, R = 64).
 bool fwd_r32_supported(const Shape& s, int64_t max_indices);
+bool fwd_r64_supported(const Shape& s, int64_t max_indices);
 
 // Small generic kernels shared across units (defined in group.hip).
 hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);

@@ -279,6 +279,16 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
   return TT_EMB_OK;
 }
 
+tt_emb_status tt_emb_kernel_uses_mfma(tt_emb_handle h, int kernel, int64_t num_indices, int* uses_mfma) {
+  if (!h || !uses_mfma || kernel < TT_EMB_K_NONE || kernel > TT_EMB_K_SPLIT) return TT_EMB_EINVAL;
+  if (num_indices < 0 || num_indices > h->desc.max_indices) return TT_EMB_EINVAL;
+  bool m = false;
+  if (kernel == TT_EMB_K_FWD_FUSED) m = fwd_r32_supported(h->s, num_indices) || fwd_r64_supported(h->s, num_indices);
+  if (kernel == TT_EMB_K_BWD_FUSED) m = bwd_r32_supported(h->s, h->desc.max_indices);
+  *uses_mfma = m ? 1 : 0;
+  return TT_EMB_OK;
+}
+
 tt_emb_status tt_emb_destroy(tt_emb_handle h) {
   delete h;
   return TT_EMB_OK;

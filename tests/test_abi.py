@@ -118,6 +118,30 @@ def test_reuse_levels_and_workspace(N):
 
 
 
+@pytest.mark.parametrize("n,d,R,M,num,fwd,bwd", [
+    ((200, 200, 250), (4, 4, 8), 32, 1 << 20, 1 << 20, 1, 1),   # both MFMA kernels
+    ((400, 500, 500), (4, 4, 8), 64, 1 << 20, 1 << 20, 1, 0),   # MFMA forward, generic backward
+    ((100, 100, 100), (4, 4, 4), 16, 1 << 20, 1 << 20, 0, 0),   # generic both ways
+    ((6, 5, 252), (4, 4, 8), 32, 1000, 1000, 1, 1),             # the backward's LDS accumulator fills
+    ((6, 5, 253), (4, 4, 8), 32, 1000, 1000, 1, 0),             # one row past it
+    ((10, 10, 10), (4, 4, 8), 32, 1 << 24, 1 << 24, 0, 0),      # E offsets would pass 2^31
+    ((10, 10, 10), (4, 4, 8), 32, 1 << 24, 1000, 1, 0),         # small call: the forward decides per call
+])
+def test_kernel_uses_mfma(N, n, d, R, M, num, fwd, bwd):
+    h = N.tt_emb_create(_desc(N, T=2, n=n, d=d, R=R, M=M, B=10))
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], num) == bool(fwd)
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["bwd_fused"], num) == bool(bwd)
+    assert not N.tt_emb_kernel_uses_mfma(h, N.KERNELS["pool"], num)
+    flag = C.c_int()
+    E = N.TT_EMB_EINVAL
+    assert N.lib.tt_emb_kernel_uses_mfma(h, 8, 0, C.byref(flag)) == E
+    assert N.lib.tt_emb_kernel_uses_mfma(h, 2, M + 1, C.byref(flag)) == E
+    assert N.lib.tt_emb_kernel_uses_mfma(h, 2, -1, C.byref(flag)) == E
+    assert N.lib.tt_emb_kernel_uses_mfma(h, 2, 0, None) == E
+    assert N.lib.tt_emb_kernel_uses_mfma(None, 2, 0, C.byref(flag)) == E
+    N.tt_emb_destroy(h)
+
+
 def _desc_n(N, L=4, T=2, n=(3, 4, 5, 2), d=(2, 2, 2, 1), R=4, M=100, B=10, rows=None):
     x = N.tt_emb_desc_n()
     x.num_tables = T
@@ -147,6 +171,19 @@ def test_create_n_shapes_and_workspace(N):
     assert N.tt_emb_workspace_size(h5) > N.tt_emb_workspace_size(h8)
     for h in (h3, h3n, h4, h2, h8, h5):
         N.tt_emb_destroy(h)
+
+
+def test_kernel_uses_mfma_on_the_three_core_view(N):
+    # four cores d = (2, 2, 4, 8) view as d = (4, 4, 8): the MFMA kernels serve them
+    h = N.tt_emb_create_n(_desc_n(N, L=4, n=(10, 20, 10, 30), d=(2, 2, 4, 8), R=32, M=1000))
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], 1000)
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["bwd_fused"], 1000)
+    assert not N.tt_emb_kernel_uses_mfma(h, N.KERNELS["merge"], 1000)
+    N.tt_emb_destroy(h)
+    # two cores d = (16, 8) view as d = (16, 1, 8) around an identity core: generic kernels
+    h = N.tt_emb_create_n(_desc_n(N, L=2, n=(100, 100), d=(16, 8), R=32, M=1000))
+    assert not N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], 1000)
+    N.tt_emb_destroy(h)
 
 
 @pytest.mark.parametrize("kw,code", [
