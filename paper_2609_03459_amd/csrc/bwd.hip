@@ -112,15 +112,17 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restri
 // D = 128: a lane owns two columns (one 8-byte load per occurrence), the bag
 // index of each occurrence is read into a scalar register so every dV row is a
 // uniform base, and 16 rows are in flight before they are summed in order.
+// Chunks go in sorted order, an eighth of them per XCD, so each XCD reads the
+// grad_out rows and bag ids of about one table, and more of them hit its L2.
 __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                   const uint32_t* __restrict__ sorted_pos,
                                                   const int32_t* __restrict__ bag_of,
                                                   const int32_t* __restrict__ ctr, float* __restrict__ dE,
                                                   float* __restrict__ part) {
   const int nvalid = ctr[C_NVALID];
-  const int c = blockIdx.x * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = (int)xcd_block(blockIdx.x, gridDim.x) * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
-  if (i0 >= nvalid) return;
+  if (i0 >= nvalid) return;  // also the blocks past the chunk count that round the grid to 8
   const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
   const SegEnds ends = seg_ends(sorted_uid, i0, i1, nvalid);
@@ -464,14 +466,15 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
   prof_begin(prof, K_SEG_SUM, st);
-  if (s.D == 128)
-    hipLaunchKernelGGL(k_seg_dE128, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
-                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
+  if (s.D == 128) {
+    hipLaunchKernelGGL(k_seg_dE128, dim3(xcd_grid((nseg + SEG_WAVES - 1) / SEG_WAVES)), dim3(64 * SEG_WAVES), 0, st,
+                       dV, (const int32_t*)w.sorted_uid, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
                        (const int32_t*)w.ctr, dE, w.seg_part);
-  else
+  } else {
     hipLaunchKernelGGL(k_seg_dE, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
                        (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
                        (const int32_t*)w.ctr, s.D, dE, w.seg_part);
+  }
   prof_end(prof, K_SEG_SUM, st);
   hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);

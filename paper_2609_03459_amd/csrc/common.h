@@ -170,6 +170,17 @@ hipError_t scan_u32_exclusive(const uint32_t* in, uint32_t* out, int64_t n, uint
                               hipStream_t st);
 int persistent_grid();
 
+// The dispatcher deals workgroups to the eight XCDs in turn (XCD = block id mod 8),
+// and each XCD has its own L2.  A launch of xcd_grid(n) blocks that takes its work
+// item from xcd_block gives every XCD one contiguous eighth of the items, so data
+// that neighbouring items share (rows of one table) is cached in one L2.  Items
+// past n land on the last blocks and must be skipped by the kernel.
+constexpr unsigned NUM_XCD = 8;
+inline unsigned xcd_grid(unsigned n) { return (n + NUM_XCD - 1) / NUM_XCD * NUM_XCD; }
+__device__ __forceinline__ unsigned xcd_block(unsigned b, unsigned grid) {
+  return (b % NUM_XCD) * (grid / NUM_XCD) + b / NUM_XCD;
+}
+
 // ---------------------------------------------------------------------------
 // Device helpers.
 // ---------------------------------------------------------------------------
