@@ -1,7 +1,8 @@
 // Backward pass of the TT-embedding gather (FlowTT Section 3.2, Eq. 1) and SGD.
 //   dE segment sums : dE_u = sum of grad_out rows over the occurrences of u,
-//                     walked in sorted order in fixed chunks; rows that cross a
-//                     chunk boundary are finished from per-chunk partials
+//                     walked in sorted order in fixed chunks; a short row that
+//                     crosses a chunk end is summed whole by its first chunk,
+//                     a long one is finished from per-chunk partials
 //                     (deterministic, no atomics)
 //   per group       : C recomputed, dD_u = C^T dE_u and dC_u = dE_u D_u^T per row,
 //                     sum dC over the group first, then dA = (sum dC) B^T and
@@ -18,25 +19,46 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
 // ---------------------------------------------------------------------------
 // dE segment sums over the sorted occurrences
 // ---------------------------------------------------------------------------
-// Where chunk c's sum for row cur goes.  A row's occurrences are contiguous, so
-// only the chunk's first row can have begun before it (head partial) and only its
-// last row can go on after it (tail partial); k_seg_fix finishes those rows.
+// What chunk c = [i0, i1) of the sorted occurrences sums.  A row's occurrences
+// are contiguous, so only the chunk's first row can have begun before it and only
+// its last row can go on after it.  A row of at most SEG_CHUNK occurrences that
+// crosses the chunk end is summed whole by the chunk of its first occurrence,
+// which reads on past its end (less than one chunk), and skipped by the next
+// chunk.  A longer row is split: each chunk sums its part into a partial (head:
+// the row began in an earlier chunk; tail: it goes on after this one), and
+// k_seg_fix adds the parts.
 struct SegEnds {
-  int u_first, u_last;
-  bool head_open, tail_open;
+  int ib, ie;            // occurrences summed here: [ib, ie), empty when ib >= ie
+  int u_head, u_tail;    // the rows whose sums go to the head / tail partial, else -1
 };
-__device__ __forceinline__ SegEnds seg_ends(const int32_t* __restrict__ sorted_uid, int i0, int i1, int nvalid) {
+__device__ __forceinline__ SegEnds seg_ends(const int32_t* __restrict__ sorted_uid,
+                                            const int32_t* __restrict__ occ_start, int i0, int i1, int nvalid) {
   SegEnds e;
-  e.u_first = sorted_uid[i0];
-  e.u_last = sorted_uid[i1 - 1];
-  e.head_open = i0 > 0 && sorted_uid[i0 - 1] == e.u_first;
-  e.tail_open = i1 < nvalid && sorted_uid[i1] == e.u_last;
+  e.ib = i0;
+  e.ie = i1;
+  e.u_head = e.u_tail = -1;
+  const int uf = sorted_uid[i0];
+  if (i0 > 0 && sorted_uid[i0 - 1] == uf) {
+    const int end = occ_start[uf + 1];
+    if (end - occ_start[uf] <= SEG_CHUNK)
+      e.ib = end;  // summed by the previous chunk
+    else
+      e.u_head = uf;
+  }
+  const int ul = sorted_uid[i1 - 1];
+  if (i1 < nvalid && sorted_uid[i1] == ul) {
+    const int end = occ_start[ul + 1];
+    if (end - occ_start[ul] <= SEG_CHUNK)
+      e.ie = end;  // read on to the row's end
+    else if (ul != e.u_head)
+      e.u_tail = ul;
+  }
   return e;
 }
 __device__ __forceinline__ float* seg_dst(const SegEnds& e, int cur, int c, int D, float* __restrict__ dE,
                                           float* __restrict__ part) {
-  if (e.head_open && cur == e.u_first) return part + ((int64_t)c * 2 + 0) * D;
-  if (e.tail_open && cur == e.u_last) return part + ((int64_t)c * 2 + 1) * D;
+  if (cur == e.u_head) return part + ((int64_t)c * 2 + 0) * D;
+  if (cur == e.u_tail) return part + ((int64_t)c * 2 + 1) * D;
   return dE + (int64_t)cur * D;
 }
 __device__ __forceinline__ void seg_flush(const SegEnds& e, int cur, int c, int D, int j0, const float* acc,
@@ -59,26 +81,28 @@ constexpr int SEG_WAVES = 4;
 __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                const uint32_t* __restrict__ sorted_pos,
                                                const int32_t* __restrict__ bag_of,
+                                               const int32_t* __restrict__ occ_start,
                                                const int32_t* __restrict__ ctr, int D, float* __restrict__ dE,
                                                float* __restrict__ part) {
   const int nvalid = ctr[C_NVALID];
   const int c = blockIdx.x * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
   if (i0 >= nvalid) return;
-  const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
-  const SegEnds ends = seg_ends(sorted_uid, i0, i1, nvalid);
+  const SegEnds ends = seg_ends(sorted_uid, occ_start, i0, i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid, nvalid);
+  const int ib = ends.ib, ie = ends.ie;
+  if (ib >= ie) return;
   for (int j0 = 0; j0 < D; j0 += 256) {
     bool colok[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) colok[q] = j0 + q * 64 + lane < D;
-    int cur = sorted_uid[i0];
+    int cur = sorted_uid[ib];
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int base = i0; base < i1; base += 64) {
+    for (int base = ib; base < ie; base += 64) {
       const int i = base + lane;
-      const int my_u = i < i1 ? sorted_uid[i] : -1;
-      const int my_b = i < i1 ? bag_of[sorted_pos[i]] : 0;
-      const int cnt = i1 - base < 64 ? i1 - base : 64;
+      const int my_u = i < ie ? sorted_uid[i] : -1;
+      const int my_b = i < ie ? bag_of[sorted_pos[i]] : 0;
+      const int cnt = ie - base < 64 ? ie - base : 64;
       for (int k0 = 0; k0 < cnt; k0 += 8) {
         float v[8][4];
         int uk[8];
@@ -117,25 +141,27 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restri
 __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
                                                   const uint32_t* __restrict__ sorted_pos,
                                                   const int32_t* __restrict__ bag_of,
+                                                  const int32_t* __restrict__ occ_start,
                                                   const int32_t* __restrict__ ctr, float* __restrict__ dE,
                                                   float* __restrict__ part) {
   const int nvalid = ctr[C_NVALID];
   const int c = (int)xcd_block(blockIdx.x, gridDim.x) * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
   if (i0 >= nvalid) return;  // also the blocks past the chunk count that round the grid to 8
-  const int i1 = i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid;
   const int lane = lane_id();
-  const SegEnds ends = seg_ends(sorted_uid, i0, i1, nvalid);
+  const SegEnds ends = seg_ends(sorted_uid, occ_start, i0, i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid, nvalid);
+  const int ib = ends.ib, ie = ends.ie;
+  if (ib >= ie) return;
   auto flush = [&](int u, float2 acc) {
     reinterpret_cast<float2*>(seg_dst(ends, u, c, 128, dE, part))[lane] = acc;
   };
-  int cur = ends.u_first;
+  int cur = sorted_uid[ib];
   float2 acc = make_float2(0.f, 0.f);
-  for (int base = i0; base < i1; base += 64) {
+  for (int base = ib; base < ie; base += 64) {
     const int i = base + lane;
-    const int my_u = i < i1 ? sorted_uid[i] : -1;
-    const int my_b = i < i1 ? bag_of[sorted_pos[i]] : 0;
-    const int cnt = i1 - base < 64 ? i1 - base : 64;
+    const int my_u = i < ie ? sorted_uid[i] : -1;
+    const int my_b = i < ie ? bag_of[sorted_pos[i]] : 0;
+    const int cnt = ie - base < 64 ? ie - base : 64;
     for (int k0 = 0; k0 < cnt; k0 += 16) {
       float2 v[16];
 #pragma unroll
@@ -162,54 +188,113 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __res
   flush(cur, acc);
 }
 
-// Rows whose occurrences span several chunks: chunk c0 + 1, where c0 holds the
+// Rows of more than SEG_CHUNK occurrences: chunk c0 + 1, where c0 holds the
 // row's first occurrence, finishes the row from c0's tail partial and the head
-// partials of every following chunk.  Four waves split the chunk range; each
-// sums its part with 8 independent accumulators; the parts are combined in a
-// fixed order.
-__global__ void __launch_bounds__(256) k_seg_fix(const int32_t* __restrict__ sorted_uid,
-                                                 const int32_t* __restrict__ occ_start,
-                                                 const int32_t* __restrict__ ctr, int D,
-                                                 const float* __restrict__ part, float* __restrict__ dE) {
-  __shared__ float red[4][256];
-  const int nvalid = ctr[C_NVALID];
-  const int c = blockIdx.x;
-  if (c == 0 || c * SEG_CHUNK >= nvalid) return;
+// partials of every following chunk, in chunk order.  A block screens 64 chunks
+// with one lane each (few of them start inside such a row).  Rows of at most
+// FIX_SMALL head partials are fixed one per wave, all at once; longer rows one
+// after the other by the whole block: its waves split the chunk range, each
+// sums its part with four independent accumulators per column, and the parts
+// are combined in a fixed order.
+constexpr int FIX_SCREEN = 64;  // chunks screened per block
+constexpr int FIX_WAVES = 16;
+constexpr int FIX_SMALL = 16;
+__device__ __forceinline__ int fix_row(const int32_t* __restrict__ sorted_uid, const int32_t* __restrict__ occ_start,
+                                       int c, int* c0, int* c1) {
   const int u = sorted_uid[c * SEG_CHUNK];
   const int lo = occ_start[u], hi = occ_start[u + 1];
-  const int c0 = lo / SEG_CHUNK, c1 = (hi - 1) / SEG_CHUNK;
-  if (c0 != c - 1) return;
+  *c0 = lo / SEG_CHUNK;
+  *c1 = (hi - 1) / SEG_CHUNK;
+  return u;
+}
+__global__ void __launch_bounds__(64 * FIX_WAVES) k_seg_fix(const int32_t* __restrict__ sorted_uid,
+                                                            const int32_t* __restrict__ occ_start,
+                                                            const int32_t* __restrict__ ctr, int D,
+                                                            const float* __restrict__ part, float* __restrict__ dE) {
+  __shared__ float red[FIX_WAVES][256];
+  __shared__ uint64_t flagged[2];  // rows with few / many head partials
+  const int nvalid = ctr[C_NVALID];
   const int w = threadIdx.x >> 6, lane = lane_id();
-  const int n = c1 - c0;  // head partials of chunks c0+1 .. c1
-  const int k_lo = c0 + 1 + (int)(((int64_t)n * w) / 4), k_hi = c0 + 1 + (int)(((int64_t)n * (w + 1)) / 4);
-  for (int j0 = 0; j0 < D; j0 += 256) {
-    for (int jj = 0; jj < 4; ++jj) {
-      const int j = j0 + jj * 64 + lane;
-      float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      if (j < D) {
-        int k = k_lo;
-        for (; k + 8 <= k_hi; k += 8)
-#pragma unroll
-          for (int kk = 0; kk < 8; ++kk) a[kk] += part[((int64_t)(k + kk) * 2 + 0) * D + j];
-        for (; k < k_hi; ++k) a[0] += part[((int64_t)k * 2 + 0) * D + j];
-      }
-      red[w][jj * 64 + lane] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  if (w == 0) {
+    const int c = blockIdx.x * FIX_SCREEN + lane;
+    bool fix = false, big = false;
+    if (c > 0 && (int64_t)c * SEG_CHUNK < nvalid) {
+      const int u = sorted_uid[c * SEG_CHUNK];
+      const int lo = occ_start[u], hi = occ_start[u + 1];
+      fix = lo / SEG_CHUNK == c - 1 && hi - lo > SEG_CHUNK;
+      big = (hi - 1) / SEG_CHUNK - lo / SEG_CHUNK > FIX_SMALL;
     }
-    __syncthreads();
-    if (w == 0) {
-      for (int jj = 0; jj < 4; ++jj) {
-        const int j = j0 + jj * 64 + lane;
-        if (j < D) {
-          float acc = part[((int64_t)c0 * 2 + 1) * D + j];
-          acc += red[0][jj * 64 + lane];
-          acc += red[1][jj * 64 + lane];
-          acc += red[2][jj * 64 + lane];
-          acc += red[3][jj * 64 + lane];
-          dE[(int64_t)u * D + j] = acc;
+    const uint64_t m_small = __ballot(fix && !big), m_big = __ballot(fix && big);
+    if (lane == 0) {
+      flagged[0] = m_small;
+      flagged[1] = m_big;
+    }
+  }
+  __syncthreads();
+  // short rows: the v-th flagged chunk goes to wave v mod FIX_WAVES
+  {
+    uint64_t m = flagged[0];
+    for (int v = 0; m; ++v, m &= m - 1) {
+      if (v % FIX_WAVES != w) continue;
+      int c0, c1;
+      const int u = fix_row(sorted_uid, occ_start, blockIdx.x * FIX_SCREEN + __builtin_ctzll(m), &c0, &c1);
+      for (int j = lane; j < D; j += 64) {
+        float a[4] = {part[((int64_t)c0 * 2 + 1) * D + j], 0.f, 0.f, 0.f};
+        int k = c0 + 1;
+        for (; k + 4 <= c1 + 1; k += 4)
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk) a[kk] += part[((int64_t)(k + kk) * 2 + 0) * D + j];
+        for (; k <= c1; ++k) a[0] += part[((int64_t)k * 2 + 0) * D + j];
+        dE[(int64_t)u * D + j] = (a[0] + a[1]) + (a[2] + a[3]);
+      }
+    }
+  }
+  // long rows: the whole block on each
+  uint64_t m = flagged[1];
+  while (m) {
+    const int c = blockIdx.x * FIX_SCREEN + __builtin_ctzll(m);
+    m &= m - 1;
+    int c0, c1;
+    const int u = fix_row(sorted_uid, occ_start, c, &c0, &c1);
+    const int n = c1 - c0;  // head partials of chunks c0+1 .. c1
+    const int k_lo = c0 + 1 + (int)(((int64_t)n * w) / FIX_WAVES);
+    const int k_hi = c0 + 1 + (int)(((int64_t)n * (w + 1)) / FIX_WAVES);
+    for (int j0 = 0; j0 < D; j0 += 256) {
+      bool ok[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ok[q] = j0 + q * 64 + lane < D;
+      float a[4][4] = {};  // [column group][accumulator]
+      int k = k_lo;
+      for (; k + 4 <= k_hi; k += 4)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const float* pr = part + ((int64_t)(k + kk) * 2 + 0) * D + j0 + lane;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (ok[q]) a[q][kk] += pr[q * 64];
+        }
+      for (; k < k_hi; ++k) {
+        const float* pr = part + ((int64_t)k * 2 + 0) * D + j0 + lane;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (ok[q]) a[q][0] += pr[q * 64];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[w][q * 64 + lane] = (a[q][0] + a[q][1]) + (a[q][2] + a[q][3]);
+      __syncthreads();
+      if (w == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = j0 + q * 64 + lane;
+          if (j < D) {
+            float acc = part[((int64_t)c0 * 2 + 1) * D + j];
+            for (int v = 0; v < FIX_WAVES; ++v) acc += red[v][q * 64 + lane];
+            dE[(int64_t)u * D + j] = acc;
+          }
         }
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
@@ -469,14 +554,14 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   if (s.D == 128) {
     hipLaunchKernelGGL(k_seg_dE128, dim3(xcd_grid((nseg + SEG_WAVES - 1) / SEG_WAVES)), dim3(64 * SEG_WAVES), 0, st,
                        dV, (const int32_t*)w.sorted_uid, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
-                       (const int32_t*)w.ctr, dE, w.seg_part);
+                       (const int32_t*)w.occ_start, (const int32_t*)w.ctr, dE, w.seg_part);
   } else {
     hipLaunchKernelGGL(k_seg_dE, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
-                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
+                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
                        (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   }
   prof_end(prof, K_SEG_SUM, st);
-  hipLaunchKernelGGL(k_seg_fix, dim3(nseg), dim3(256), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
+  hipLaunchKernelGGL(k_seg_fix, dim3((nseg + FIX_SCREEN - 1) / FIX_SCREEN), dim3(64 * FIX_WAVES), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, lr, update, prof, st);
   const int grid = persistent_grid() * 2;

@@ -438,7 +438,11 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   __shared__ int32_t lu[SCAN_TILE + SCAN_TILE / 32];        // row id of each element (-1: invalid)
   __shared__ int32_t lg[SCAN_TILE + SCAN_TILE / 32];        // (group id << 1) | group starts here; -1: invalid
   __shared__ uint64_t smem[SCAN_THREADS / 64];
-  const int base = blockIdx.x * SCAN_TILE;
+  // tiles in sorted order, an eighth per XCD: a table's inverse-map entries (a
+  // contiguous range of positions) are scattered within one XCD's L2
+  const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
+  if (tile >= (n + SCAN_TILE - 1) / SCAN_TILE) return;
+  const int base = tile * SCAN_TILE;
 #pragma unroll 4
   for (int j = 0; j < SCAN_ITEMS; ++j) {
     const int e = j * SCAN_THREADS + (int)threadIdx.x;
@@ -462,7 +466,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   }
   uint64_t tot;
   const uint64_t c = (uint64_t)__popc(hb) | ((uint64_t)__popc(pb) << 32);
-  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + tsum[blockIdx.x];
+  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + tsum[tile];
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int i = base + e0 + k;
@@ -681,7 +685,7 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
     hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, s.dedup,
                        w.tsum64, w.ctr);
     hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
-    hipLaunchKernelGGL(k_group_down, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
+    hipLaunchKernelGGL(k_group_down, dim3(xcd_grid(gt)), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
                        s.dedup, (const uint64_t*)w.tsum64, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
                        w.pg_start, w.pg_key, w.ctr);
   }

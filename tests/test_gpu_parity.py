@@ -335,6 +335,34 @@ def test_backward_shape_limits(lib, orc, T, n):
     check_forward(lib, orc, case, name=f"limits T={T} n3={n[2]}")
 
 
+def _row_runs_case(seed, d, R):
+    """Two tables whose sorted occurrences come in runs of chosen lengths, so that
+    the ends of the 256-occurrence dE chunks fall before, inside and just past rows
+    of 255, 256, 257, 511-513 and 1000 occurrences (the second table starts at
+    another offset modulo 256)."""
+    mult = [255, 256, 257, 1, 2, 511, 512, 513, 3, 1000, 256, 255, 1, 257, 7]
+    T, n, B = 2, (6, 5, 40), 64
+    case = ttgen.tiny(seed, T, n, d, R, B=B, max_len=1)
+    rng = np.random.default_rng(seed)
+    N = n[0] * n[1] * n[2]
+    idx, lens = [], []
+    for t in range(T):
+        rows = np.sort(rng.choice(N, len(mult), replace=False))
+        occ = np.repeat(rows, mult)
+        rng.shuffle(occ)  # bag order: each row's occurrences spread over the bags
+        cuts = np.sort(rng.integers(0, occ.size + 1, B - 1))
+        lens.append(np.diff(np.concatenate([[0], cuts, [occ.size]])))
+        idx.append(occ)
+    case["idx"] = np.concatenate(idx).astype(np.int64)
+    case["offsets"] = np.concatenate([[0], np.cumsum(np.concatenate(lens))]).astype(np.int64)
+    return case
+
+
+@pytest.mark.parametrize("d,R", [((4, 4, 8), 32), ((2, 2, 2), 4)])
+def test_backward_rows_across_dE_chunk_ends(lib, orc, d, R):
+    check_backward(lib, orc, _row_runs_case(3300 + R, d, R), name=f"row runs d={d} R={R}")
+
+
 def test_backward_config5_small_batch(lib, orc):
     check_backward(lib, orc, ttgen.make(5, bags=64), name="config5 B=64")
 
