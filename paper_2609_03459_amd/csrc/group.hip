@@ -88,9 +88,18 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
       for (int k = threadIdx.x; k < nwin; k += SORT_THREADS) win[k] = offsets[bfirst + k];
     __syncthreads();
   }
-  int err = 0;
+  // every index of the thread's items is loaded before any is used, so the loads
+  // are in flight together
+  int64_t gv[SORT_ITEMS];
+#pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
-    int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
+    const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
+    gv[j] = o < o1 ? idx[o] : 0;
+  }
+  int err = 0;
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
     if (o >= o1) break;
     int64_t b;
     if (!offsets) {
@@ -109,7 +118,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
       b = upper_bound_global(offsets, 0, NB + 1, o) - 1;
     }
     b = b < 0 ? 0 : (b > NB - 1 ? NB - 1 : b);
-    const int64_t g = idx[o];
+    const int64_t g = gv[j];
     const uint32_t t = (uint32_t)b / (uint32_t)B;
     uint32_t key;
     if (g >= 0 && g < N) {
