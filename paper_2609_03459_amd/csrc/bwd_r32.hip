@@ -514,14 +514,24 @@ __device__ __forceinline__ void reduce_g3(int q, int xb, ShapeArgs s, const floa
   const int acc_n = s.n3 * 128;
   const int e = xb * RED_THREADS + threadIdx.x;
   if (e >= acc_n) return;
-  float acc = 0.f;
-  for (int w = q; w < nwg; w += nq) acc += g3part[(int64_t)w * acc_n + e];
+  // four independent sums, so that four loads are in flight
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int w = q;
+  for (; w + 3 * nq < nwg; w += 4 * nq) {
+    a0 += g3part[(int64_t)w * acc_n + e];
+    a1 += g3part[(int64_t)(w + nq) * acc_n + e];
+    a2 += g3part[(int64_t)(w + 2 * nq) * acc_n + e];
+    a3 += g3part[(int64_t)(w + 3 * nq) * acc_n + e];
+  }
+  for (; w < nwg; w += nq) a0 += g3part[(int64_t)w * acc_n + e];
+  const float acc = (a0 + a1) + (a2 + a3);
   const int i3 = e >> 7, j3 = (e >> 4) & 7, bp = g3_unslot(j3, e & 15);
   put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3, acc, lr, update);
 }
 
-// The three reductions in one launch, so they overlap: blocks [0, T n1) reduce dG1
-// (the longest, first), the next 2 T n2 blocks dG2, the rest dG3.
+// The three reductions in one launch, so they overlap: the first blocks reduce dG3
+// (few blocks, each a chain of one load per owner workgroup), the next T n1 dG1,
+// the rest (2 T n2) dG2.
 __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                               const uint32_t* __restrict__ dense_base,
                                                               const float* __restrict__ dApart, int nsl_cap,
@@ -531,15 +541,14 @@ __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const
                                                               float* __restrict__ dG1, float* __restrict__ dG2,
                                                               float* __restrict__ dG3, float lr, bool update) {
   const int b = blockIdx.x;
-  const int n1b = s.T * s.n1, n2b = 2 * s.T * s.n2;
-  if (b < n1b) {
-    reduce_g1(b, s, dense_cnt, dense_base, dApart, nsl_cap, dG1, lr, update);
-  } else if (b < n1b + n2b) {
-    reduce_g2(b - n1b, run_base, dBpart, nch_cap, dG2, lr, update);
+  const int per_q = (s.n3 * 128 + RED_THREADS - 1) / RED_THREADS;
+  const int n3b = 2 * s.T * per_q, n1b = s.T * s.n1;
+  if (b < n3b) {
+    reduce_g3(b / per_q, b % per_q, s, g3part, nwg, dG3, lr, update);
+  } else if (b < n3b + n1b) {
+    reduce_g1(b - n3b, s, dense_cnt, dense_base, dApart, nsl_cap, dG1, lr, update);
   } else {
-    const int per_q = (s.n3 * 128 + RED_THREADS - 1) / RED_THREADS;
-    const int r = b - n1b - n2b;
-    reduce_g3(r / per_q, r % per_q, s, g3part, nwg, dG3, lr, update);
+    reduce_g2(b - n3b - n1b, run_base, dBpart, nch_cap, dG2, lr, update);
   }
 }
 
