@@ -352,10 +352,11 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* __restrict__ tsum,
   if (total_out && threadIdx.x == 0) *total_out = (int32_t)running;
 }
 
-// each thread scans SCAN_ITEMS consecutive elements
+// each thread scans SCAN_ITEMS consecutive elements; tile offsets from tsum, or
+// with tsum NULL a single tile that also writes the total to total_out
 template <typename T, bool INCLUSIVE>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(const T* __restrict__ in, T* __restrict__ out, int64_t n,
-                                                            const T* __restrict__ tsum) {
+                                                            const T* __restrict__ tsum, int32_t* total_out) {
   __shared__ T smem[SCAN_THREADS / 64];
   const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + (int64_t)threadIdx.x * SCAN_ITEMS;
   T v[SCAN_ITEMS];
@@ -367,7 +368,8 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(const T* __restrict_
     s += v[k];
   }
   T tot;
-  T acc = block_excl_scan<T, SCAN_THREADS>(s, smem, &tot) + tsum[blockIdx.x];
+  T acc = block_excl_scan<T, SCAN_THREADS>(s, smem, &tot) + (tsum ? tsum[blockIdx.x] : (T)0);
+  if (!tsum && total_out && threadIdx.x == 0) *total_out = (int32_t)tot;
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     int64_t i = base + k;
@@ -381,10 +383,15 @@ template <typename T, bool INCLUSIVE>
 static hipError_t scan_generic(const T* in, T* out, int64_t n, T* tsum, int32_t* total_out, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   int ntiles = (int)((n + SCAN_TILE - 1) / SCAN_TILE);
+  if (ntiles == 1) {  // one launch
+    hipLaunchKernelGGL((k_scan_down<T, INCLUSIVE>), dim3(1), dim3(SCAN_THREADS), 0, st, in, out, n, (const T*)nullptr,
+                       total_out);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_scan_reduce<T>, dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, n, tsum);
   hipLaunchKernelGGL(k_scan_top<T>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, ntiles, total_out);
   hipLaunchKernelGGL((k_scan_down<T, INCLUSIVE>), dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, out, n,
-                     (const T*)tsum);
+                     (const T*)tsum, (int32_t*)nullptr);
   return hipGetLastError();
 }
 
