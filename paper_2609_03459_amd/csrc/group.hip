@@ -319,6 +319,107 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
   }
 }
 
+// A sort of at most one tile: every pass in one workgroup, the keys kept in
+// registers and LDS between passes.  Each pass ranks exactly as k_radix_scatter
+// does (wave ballots, per-wave digit counts, tile-local digit starts) and places
+// the tile in LDS in digit order, which for a single tile is the sorted order of
+// that pass.  Reads keys/vals and writes kout/vout (which may be the same arrays).
+template <int BITS>
+__global__ void __launch_bounds__(SORT_THREADS) k_sort_tile(const uint32_t* __restrict__ kin,
+                                                            const uint32_t* __restrict__ vin, uint32_t* kout,
+                                                            uint32_t* vout, int n, int npasses, int dbits) {
+  constexpr int NB = 1 << BITS;
+  __shared__ uint32_t wh[4][NB];  // per-wave digit counts, then the wave's base per digit
+  __shared__ uint32_t sk[SORT_TILE], sv[SORT_TILE];
+  __shared__ uint32_t scan_tmp[SORT_THREADS / 64];
+  const int w = threadIdx.x >> 6;
+  const int lane = lane_id();
+  const int base = w * (SORT_ITEMS * 64);
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  uint32_t key[SORT_ITEMS], val[SORT_ITEMS], rk[SORT_ITEMS];
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    const int i = base + j * 64 + lane;
+    const bool ok = i < n;
+    key[j] = ok ? kin[i] : 0u;
+    val[j] = ok ? vin[i] : 0u;
+  }
+  for (int p = 0; p < npasses; ++p) {
+    const int shift = p * dbits;
+    for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&wh[0][0])[k] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j) {
+      const int i = base + j * 64 + lane;
+      const bool ok = i < n;
+      const uint32_t dg = (key[j] >> shift) & (NB - 1);
+      uint64_t peers = __ballot(ok);
+#pragma unroll
+      for (int b = 0; b < BITS; ++b) {
+        const uint64_t m = __ballot((dg >> b) & 1);
+        peers &= ((dg >> b) & 1) ? m : ~m;
+      }
+      const uint32_t before = __popcll(peers & lt);
+      const uint32_t cnt = __popcll(peers);
+      const uint32_t prev = ok ? wh[w][dg] : 0u;
+      rk[j] = prev + before;
+      if (ok && before == 0) wh[w][dg] = prev + cnt;
+    }
+    __syncthreads();
+    constexpr int DPT = (NB + SORT_THREADS - 1) / SORT_THREADS;  // digits per thread
+    uint32_t tot[DPT], my = 0;
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int d = threadIdx.x * DPT + q;
+      tot[q] = d < NB ? wh[0][d] + wh[1][d] + wh[2][d] + wh[3][d] : 0u;
+      my += tot[q];
+    }
+    uint32_t all;
+    uint32_t run = block_excl_scan<uint32_t, SORT_THREADS>(my, scan_tmp, &all);
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      const int d = threadIdx.x * DPT + q;
+      if (d < NB) {
+        const uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
+        wh[0][d] = run;
+        wh[1][d] = run + c0;
+        wh[2][d] = run + c0 + c1;
+        wh[3][d] = run + c0 + c1 + c2;
+      }
+      run += tot[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j) {
+      const int i = base + j * 64 + lane;
+      if (i < n) {
+        const uint32_t pos = wh[w][(key[j] >> shift) & (NB - 1)] + rk[j];
+        sk[pos] = key[j];
+        sv[pos] = val[j];
+      }
+    }
+    __syncthreads();
+    // element i of the pass's output is the next pass's input element i
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j) {
+      const int i = base + j * 64 + lane;
+      if (i < n) {
+        key[j] = sk[i];
+        val[j] = sv[i];
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    const int i = base + j * 64 + lane;
+    if (i < n) {
+      kout[i] = key[j];
+      vout[i] = val[j];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // generic scans (tile reduce -> single-block scan of tile sums -> tile scan)
 // ---------------------------------------------------------------------------
@@ -482,7 +583,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   }
   uint64_t tot;
   const uint64_t c = (uint64_t)__popc(hb) | ((uint64_t)__popc(pb) << 32);
-  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + tsum[tile];
+  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + (tsum ? tsum[tile] : 0ull);
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int i = base + e0 + k;
@@ -518,6 +619,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
     const uint32_t knext = e + 1 < SCAN_TILE ? lk[pad32(e + 2)] : (i + 1 < n ? sk[i + 1] : kinv);
     if (i == n - 1 || knext >= kinv) {
       // the last valid occurrence: totals and end sentinels
+      ctr[C_NVALID] = i + 1;
       ctr[C_U] = uid + 1;
       ctr[C_P] = pg + 1;
       occ_start[uid + 1] = i + 1;
@@ -682,28 +784,45 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
                      B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr);
   prof_end(prof, K_INGEST, st);
   int cur = 0;
-  for (int p = 0; p < npasses; ++p) {
-    const int shift = p * dbits;
-    uint32_t* tot = w.rtotals + p * radix;
+  if (ntiles == 1) {
+    // one tile: all passes in one launch, the result where the last pass would leave it
+    cur = npasses & 1;
     switch (bits) {
-      case 8: e = radix_pass<8>(w, cur, n, shift, ntiles, tot, st); break;
-      case 9: e = radix_pass<9>(w, cur, n, shift, ntiles, tot, st); break;
-      case 10: e = radix_pass<10>(w, cur, n, shift, ntiles, tot, st); break;
-      default: e = radix_pass<11>(w, cur, n, shift, ntiles, tot, st); break;
+      case 8: hipLaunchKernelGGL(k_sort_tile<8>, dim3(1), dim3(SORT_THREADS), 0, st, w.keys[0], w.vals[0],
+                                 w.keys[cur], w.vals[cur], n, npasses, dbits); break;
+      case 9: hipLaunchKernelGGL(k_sort_tile<9>, dim3(1), dim3(SORT_THREADS), 0, st, w.keys[0], w.vals[0],
+                                 w.keys[cur], w.vals[cur], n, npasses, dbits); break;
+      case 10: hipLaunchKernelGGL(k_sort_tile<10>, dim3(1), dim3(SORT_THREADS), 0, st, w.keys[0], w.vals[0],
+                                  w.keys[cur], w.vals[cur], n, npasses, dbits); break;
+      default: hipLaunchKernelGGL(k_sort_tile<11>, dim3(1), dim3(SORT_THREADS), 0, st, w.keys[0], w.vals[0],
+                                  w.keys[cur], w.vals[cur], n, npasses, dbits); break;
     }
-    if (e != hipSuccess) return e;
-    cur ^= 1;
+  } else {
+    for (int p = 0; p < npasses; ++p) {
+      const int shift = p * dbits;
+      uint32_t* tot = w.rtotals + p * radix;
+      switch (bits) {
+        case 8: e = radix_pass<8>(w, cur, n, shift, ntiles, tot, st); break;
+        case 9: e = radix_pass<9>(w, cur, n, shift, ntiles, tot, st); break;
+        case 10: e = radix_pass<10>(w, cur, n, shift, ntiles, tot, st); break;
+        default: e = radix_pass<11>(w, cur, n, shift, ntiles, tot, st); break;
+      }
+      if (e != hipSuccess) return e;
+      cur ^= 1;
+    }
   }
   const uint32_t* sk = w.keys[cur];
   const uint32_t* sp = w.vals[cur];
   {
     const int gt = (n + SCAN_TILE - 1) / SCAN_TILE;
-    hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, s.dedup,
-                       w.tsum64, w.ctr);
-    hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
+    if (gt > 1) {  // a single tile starts at row 0 and group 0: no tile offsets needed
+      hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, s.dedup,
+                         w.tsum64, w.ctr);
+      hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
+    }
     hipLaunchKernelGGL(k_group_down, dim3(xcd_grid(gt)), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
-                       s.dedup, (const uint64_t*)w.tsum64, w.inv, w.sorted_uid, w.uniq_key, w.uniq_i3, w.occ_start,
-                       w.pg_start, w.pg_key, w.ctr);
+                       s.dedup, gt > 1 ? (const uint64_t*)w.tsum64 : nullptr, w.inv, w.sorted_uid, w.uniq_key,
+                       w.uniq_i3, w.occ_start, w.pg_start, w.pg_key, w.ctr);
   }
   hipLaunchKernelGGL(k_dense_set, dim3(grid_for(M, 256, 2048)), dim3(256), 0, st, (const int32_t*)w.pg_start,
                      (const uint32_t*)w.pg_key, (const int32_t*)w.ctr, s.n1, s.n2, s.slice_rows, w.dense_cnt,

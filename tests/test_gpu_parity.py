@@ -115,11 +115,7 @@ WIDE_KEYS = [
 ]
 
 
-@pytest.mark.parametrize("k", range(len(WIDE_KEYS)))
-def test_grouping_and_forward_wide_keys(lib, orc, k):
-    c = WIDE_KEYS[k]
-    case = ttgen.tiny(2500 + k, c["T"], c["n"], (1, 2, 2), 2, B=300, max_len=6, zipf=1.1)
-    _say(f"[group wide] T={c['T']} n={c['n']} M={case['idx'].size}")
+def _check_grouping(lib, orc, case):
     emb = _make(lib, case)
     _, idx, off = _dev(case)
     emb.group(idx, off, num_bags=case["B"])
@@ -130,10 +126,30 @@ def test_grouping_and_forward_wide_keys(lib, orc, k):
     assert got["U"] == ref["U"] and got["P"] == ref["P"] and got["nvalid"] == ref["nvalid"]
     assert np.array_equal(got["uniq_keys"], ref["uniq_t"] * npad + ref["uniq_g"])
     assert np.array_equal(got["inv"], ref["inv"])
+    assert np.array_equal(got["occ_start"], ref["occ_start"])
     assert np.array_equal(got["occ_pos"], ref["occ_pos"])
     assert np.array_equal(got["pg_start"], ref["pg_start"])
     assert np.array_equal(got["pg_keys"], ref["pg_t"] * (n[0] * n[1]) + ref["pg_q"])
-    check_forward(lib, orc, case, name=f"wide{k}")
+
+
+# 300 bags (about 1,000 keys) are sorted in one launch, 3,000 bags in radix passes over tiles
+@pytest.mark.parametrize("bags", [300, 3000])
+@pytest.mark.parametrize("k", range(len(WIDE_KEYS)))
+def test_grouping_and_forward_wide_keys(lib, orc, k, bags):
+    c = WIDE_KEYS[k]
+    case = ttgen.tiny(2500 + k, c["T"], c["n"], (1, 2, 2), 2, B=bags, max_len=6, zipf=1.1)
+    _say(f"[group wide] T={c['T']} n={c['n']} M={case['idx'].size}")
+    _check_grouping(lib, orc, case)
+    check_forward(lib, orc, case, name=f"wide{k} B={bags}")
+
+
+# a sort tile holds 4,096 keys: up to one tile is sorted in a single launch
+@pytest.mark.parametrize("m", [4095, 4096, 4097, 8193])
+def test_grouping_at_sort_tile_sizes(lib, orc, m):
+    case = ttgen.tiny(2600 + m, 1, (30, 20, 40), (2, 2, 2), 4, B=m, single=True, zipf=1.1)
+    _say(f"[group tile] M={m}")
+    _check_grouping(lib, orc, case)
+    check_forward(lib, orc, case, name=f"M={m}")
 
 
 def test_many_short_bags(lib, orc):
