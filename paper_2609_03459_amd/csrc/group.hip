@@ -54,12 +54,15 @@ __device__ __forceinline__ int64_t upper_bound_global(const int64_t* a, int64_t 
 }
 
 // tile_bag[k] = the bag whose occurrence range holds occurrence k * SORT_TILE
-// (entries stay 0 where invalid offsets leave a tile start uncovered)
+// (entries stay 0 where invalid offsets leave a tile start uncovered); also
+// flags offsets that are not a CSR partition of [0, M) in the error word
 __global__ void k_tile_bags(const int64_t* __restrict__ offsets, int64_t NB, int64_t M,
-                            int32_t* __restrict__ tile_bag) {
+                            int32_t* __restrict__ tile_bag, int32_t* __restrict__ ctr) {
   const int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
   if (b >= NB) return;
   int64_t lo = offsets[b], hi = offsets[b + 1];
+  if (lo < 0 || hi < lo || hi > M || (b == 0 && lo != 0) || (b == NB - 1 && hi != M))
+    atomicOr(&ctr[C_ERR], ERR_OFFSETS);
   lo = lo < 0 ? 0 : (lo > M ? M : lo);
   hi = hi < lo ? lo : (hi > M ? M : hi);
   for (int64_t k = (lo + SORT_TILE - 1) / SORT_TILE; k * SORT_TILE < hi; ++k) tile_bag[k] = (int32_t)b;
@@ -722,15 +725,20 @@ __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uin
   }
 }
 
+// Clears what a grouping accumulates into: the counters and the error word, the
+// radix digit totals, the dense prefix counts and the tile-to-bag map.
 __global__ void k_group_init(int32_t* ctr, int32_t* occ_start, int32_t* pg_start, uint32_t* rtotals,
-                             int nrtotals) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < C_TOTAL) ctr[i] = 0;  // counters and the error word start each grouping at zero
-  if (i < nrtotals) rtotals[i] = 0;
-  if (i == 0) {
+                             int nrtotals, uint32_t* dense_cnt, int64_t ndense, int32_t* tile_bag, int ntile_bag) {
+  const int64_t i0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if (i0 < C_TOTAL) ctr[i0] = 0;
+  if (i0 < nrtotals) rtotals[i0] = 0;
+  if (i0 == 0) {
     occ_start[0] = 0;
     pg_start[0] = 0;
   }
+  for (int64_t i = i0; i < ndense; i += stride) dense_cnt[i] = 0u;
+  for (int64_t i = i0; i < ntile_bag; i += stride) tile_bag[i] = 0;
 }
 
 static int grid_for(int64_t n, int per_block, int cap) {
@@ -760,26 +768,28 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   const int bits = dbits < 8 ? 8 : dbits;
   const int radix = 1 << bits;
   const int nrt = npasses * radix;
-  {
-    int total = C_TOTAL > nrt ? C_TOTAL : nrt;
-    hipLaunchKernelGGL(k_group_init, dim3((total + 255) / 256), dim3(256), 0, st, w.ctr, w.occ_start, w.pg_start,
-                       w.rtotals, nrt);
-  }
-  hipError_t e = fill_u32(w.dense_cnt, s.ndense, 0u, st);
-  if (e != hipSuccess) return e;
   const int64_t NB = (int64_t)s.T * B;
-  if (offsets && NB > 0)
-    hipLaunchKernelGGL(k_check_offsets, dim3(grid_for(NB, 256, 1024)), dim3(256), 0, st, offsets, NB, M, w.ctr);
-  if (M <= 0) return hipGetLastError();
-  const int n = (int)M;
+  const int n = M > 0 ? (int)M : 0;
   const int ntiles = (n + SORT_TILE - 1) / SORT_TILE;
-  prof_begin(prof, K_INGEST, st);
-  if (offsets && NB > 0) {
-    e = fill_u32(reinterpret_cast<uint32_t*>(w.tile_bag), ntiles + 1, 0u, st);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_tile_bags, dim3((unsigned)((NB + 255) / 256)), dim3(256), 0, st, offsets, NB, M,
-                       w.tile_bag);
+  const bool bags = offsets && NB > 0;
+  {
+    const int ntb = bags && n > 0 ? ntiles + 1 : 0;
+    int64_t total = C_TOTAL > nrt ? C_TOTAL : nrt;
+    if (s.ndense > total) total = s.ndense;
+    if (ntb > total) total = ntb;
+    hipLaunchKernelGGL(k_group_init, dim3(grid_for(total, 256, 1024)), dim3(256), 0, st, w.ctr, w.occ_start,
+                       w.pg_start, w.rtotals, nrt, w.dense_cnt, (int64_t)s.ndense, w.tile_bag, ntb);
   }
+  hipError_t e;
+  if (M <= 0) {
+    if (bags)
+      hipLaunchKernelGGL(k_check_offsets, dim3(grid_for(NB, 256, 1024)), dim3(256), 0, st, offsets, NB, M, w.ctr);
+    return hipGetLastError();
+  }
+  prof_begin(prof, K_INGEST, st);
+  if (bags)
+    hipLaunchKernelGGL(k_tile_bags, dim3((unsigned)((NB + 255) / 256)), dim3(256), 0, st, offsets, NB, M,
+                       w.tile_bag, w.ctr);
   hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, (const int32_t*)w.tile_bag,
                      B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr);
   prof_end(prof, K_INGEST, st);

@@ -302,6 +302,37 @@ def test_invalid_indices_flagged_and_skipped(lib, orc):
     assert_close("forward with invalid", V, ref, mag)
 
 
+@pytest.mark.parametrize("kind", ["decreasing", "last_short", "first_nonzero"])
+def test_malformed_offsets_flagged(lib, orc, kind):
+    # offsets that are not a CSR partition of [0, M): every range is clamped into
+    # [0, M] on the device, the error word reports it, and a later grouping with
+    # good offsets clears it and gives the oracle's result
+    case = ttgen.tiny(11, 2, (4, 5, 6), (2, 2, 2), 3, B=30, max_len=6, empty_bags=False)
+    bad = dict(case)
+    off = case["offsets"].copy()
+    if kind == "decreasing":
+        off[7] = off[9] + 2
+    elif kind == "last_short":
+        off[-1] -= 1
+    else:
+        off[0] = 1
+    bad["offsets"] = off
+    _say(f"[fwd] malformed offsets {kind}")
+    emb = _make(lib, case)
+    G, idx, good = _dev(case)
+    _, _, wrong = _dev(bad)
+    emb.forward(*G, idx, wrong, num_bags=case["B"])
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 4  # TT_EMB_ERANGE
+    out = emb.forward(*G, idx, good, num_bags=case["B"])  # same handle and workspace
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    V = out.cpu().numpy().reshape(case["T"] * case["B"], -1)
+    ref, _ = orc.forward(case)
+    mag, _ = orc.forward(abs_case(case))
+    assert_close("forward after malformed offsets", V, ref, mag)
+
+
 # ---------------------------------------------------------------------------
 # backward and SGD
 # ---------------------------------------------------------------------------
