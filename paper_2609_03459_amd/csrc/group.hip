@@ -725,6 +725,45 @@ __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uin
   }
 }
 
+// All three steps above in one workgroup when nruns + 1 <= SCAN_TILE: chunk
+// counts per run, their exclusive scan into run_nch (the total at run_nch[nruns]
+// and in ctr[C_NCHUNKS]) and the chunk list.  A thread owns SCAN_ITEMS
+// consecutive runs.
+__global__ void __launch_bounds__(SCAN_THREADS) k_runs_one_block(const uint32_t* __restrict__ dense_base,
+                                                                 int32_t* __restrict__ ctr, int nruns, int n1,
+                                                                 uint32_t* __restrict__ run_nch,
+                                                                 int4* __restrict__ chunks) {
+  __shared__ uint32_t smem[SCAN_THREADS / 64];
+  const uint32_t nsl = (uint32_t)ctr[C_NSLICES];
+  const int r0 = (int)threadIdx.x * SCAN_ITEMS;
+  uint32_t b[SCAN_ITEMS + 1], cnt[SCAN_ITEMS], sum = 0;
+#pragma unroll
+  for (int k = 0; k <= SCAN_ITEMS; ++k) {
+    const int r = r0 + k;
+    b[k] = r < nruns ? dense_base[(int64_t)r * n1] : nsl;
+  }
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    cnt[k] = r0 + k < nruns ? (b[k + 1] - b[k] + CHUNK_SLICES - 1) / CHUNK_SLICES : 0u;
+    sum += cnt[k];
+  }
+  uint32_t tot;
+  uint32_t acc = block_excl_scan<uint32_t, SCAN_THREADS>(sum, smem, &tot);
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    const int r = r0 + k;
+    if (r <= nruns) run_nch[r] = acc;
+    if (r < nruns)
+      for (uint32_t j = 0; j < cnt[k]; ++j) {
+        const uint32_t f = b[k] + j * CHUNK_SLICES;
+        const uint32_t n = b[k + 1] - f < (uint32_t)CHUNK_SLICES ? b[k + 1] - f : (uint32_t)CHUNK_SLICES;
+        chunks[acc + j] = make_int4((int)f, (int)n, r, 0);
+      }
+    acc += cnt[k];
+  }
+  if (threadIdx.x == 0) ctr[C_NCHUNKS] = (int32_t)tot;
+}
+
 // Clears what a grouping accumulates into: the counters and the error word, the
 // radix digit totals, the dense prefix counts and the tile-to-bag map.
 __global__ void k_group_init(int32_t* ctr, int32_t* occ_start, int32_t* pg_start, uint32_t* rtotals,
@@ -850,6 +889,11 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
                        s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, s.slice_rows,
                        w.slices, w.slice_i1);
   const int nruns = s.T * s.n2;
+  if (nruns + 1 <= SCAN_TILE) {
+    hipLaunchKernelGGL(k_runs_one_block, dim3(1), dim3(SCAN_THREADS), 0, st, (const uint32_t*)w.dense_base, w.ctr,
+                       nruns, s.n1, w.run_nch, w.chunks);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
                      (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
   // exclusive scan in place; the tile sums buffer of the dense scan is free again

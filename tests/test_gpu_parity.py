@@ -143,6 +143,17 @@ def test_grouping_and_forward_wide_keys(lib, orc, k, bags):
     check_forward(lib, orc, case, name=f"wide{k} B={bags}")
 
 
+# the chunk list of up to 4,095 (table, i2) runs is built by one workgroup, of more
+# runs by three launches
+@pytest.mark.parametrize("n", [(3, 2047, 4), (3, 2048, 4)])
+def test_grouping_many_runs(lib, orc, n):
+    case = ttgen.tiny(2700 + n[1], 2, n, (2, 2, 2), 4, B=400, max_len=8, zipf=1.05)
+    _say(f"[group runs] T=2 n={n} M={case['idx'].size}")
+    _check_grouping(lib, orc, case)
+    check_forward(lib, orc, case, name=f"runs n2={n[1]}")
+    check_backward(lib, orc, case, name=f"runs n2={n[1]}")
+
+
 # a sort tile holds 4,096 keys: up to one tile is sorted in a single launch
 @pytest.mark.parametrize("m", [4095, 4096, 4097, 8193])
 def test_grouping_at_sort_tile_sizes(lib, orc, m):
