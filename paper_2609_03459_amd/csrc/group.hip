@@ -725,14 +725,14 @@ __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uin
   }
 }
 
-// All three steps above in one workgroup when nruns + 1 <= SCAN_TILE: chunk
-// counts per run, their exclusive scan into run_nch (the total at run_nch[nruns]
-// and in ctr[C_NCHUNKS]) and the chunk list.  A thread owns SCAN_ITEMS
-// consecutive runs.
+// k_run_counts and the scan of its counts in one workgroup when nruns + 1 <=
+// SCAN_TILE: chunk counts per run, exclusive scan into run_nch (the total at
+// run_nch[nruns] and in ctr[C_NCHUNKS]).  A thread owns SCAN_ITEMS consecutive
+// runs.  (The chunk list stays a launch of its own: a run can hold thousands of
+// chunks at the no-dedup level.)
 __global__ void __launch_bounds__(SCAN_THREADS) k_runs_one_block(const uint32_t* __restrict__ dense_base,
                                                                  int32_t* __restrict__ ctr, int nruns, int n1,
-                                                                 uint32_t* __restrict__ run_nch,
-                                                                 int4* __restrict__ chunks) {
+                                                                 uint32_t* __restrict__ run_nch) {
   __shared__ uint32_t smem[SCAN_THREADS / 64];
   const uint32_t nsl = (uint32_t)ctr[C_NSLICES];
   const int r0 = (int)threadIdx.x * SCAN_ITEMS;
@@ -753,12 +753,6 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_runs_one_block(const uint32_t*
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int r = r0 + k;
     if (r <= nruns) run_nch[r] = acc;
-    if (r < nruns)
-      for (uint32_t j = 0; j < cnt[k]; ++j) {
-        const uint32_t f = b[k] + j * CHUNK_SLICES;
-        const uint32_t n = b[k + 1] - f < (uint32_t)CHUNK_SLICES ? b[k + 1] - f : (uint32_t)CHUNK_SLICES;
-        chunks[acc + j] = make_int4((int)f, (int)n, r, 0);
-      }
     acc += cnt[k];
   }
   if (threadIdx.x == 0) ctr[C_NCHUNKS] = (int32_t)tot;
@@ -891,14 +885,14 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   const int nruns = s.T * s.n2;
   if (nruns + 1 <= SCAN_TILE) {
     hipLaunchKernelGGL(k_runs_one_block, dim3(1), dim3(SCAN_THREADS), 0, st, (const uint32_t*)w.dense_base, w.ctr,
-                       nruns, s.n1, w.run_nch, w.chunks);
-    return hipGetLastError();
+                       nruns, s.n1, w.run_nch);
+  } else {
+    hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
+                       (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
+    // exclusive scan in place; the tile sums buffer of the dense scan is free again
+    e = scan_generic<uint32_t, false>(w.run_nch, w.run_nch, nruns + 1, w.tsum32, w.ctr + C_NCHUNKS, st);
+    if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
-                     (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
-  // exclusive scan in place; the tile sums buffer of the dense scan is free again
-  e = scan_generic<uint32_t, false>(w.run_nch, w.run_nch, nruns + 1, w.tsum32, w.ctr + C_NCHUNKS, st);
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_make_chunks, dim3((nruns + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
                      (const uint32_t*)w.run_nch, (const int32_t*)w.ctr, nruns, s.n1, w.chunks);
   return hipGetLastError();
