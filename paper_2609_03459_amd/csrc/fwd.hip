@@ -144,7 +144,7 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
 // The next row pair's G3 operands are in flight while a pair is computed.
 // ---------------------------------------------------------------------------
 constexpr int F32_WAVES = 4;
-constexpr int F32_WG_PER_CU = 2;  // two workgroups (8 waves, 64 KB LDS) per CU
+constexpr int F32_WG_PER_CU = 3;  // three workgroups (12 waves, 96 KB LDS) per CU
 constexpr int F32_SCR = 2048;     // per-wave LDS floats: [slice 4][j1 4][j2 4][b 32]
 
 // XOR swizzle of the b index: both the stage-1 writes and the stage-2 operand
