@@ -198,6 +198,20 @@ def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused"):
     print(json.dumps(out))
 
 
+def measured_traffic(kernel, key, on_mfma, path=None):
+    """HBM bytes per launch from profiles/traffic.json, or None unless those counters
+    were taken on this kernel as it is now (source digest), on this run (workload,
+    reuse, schedule, update mode) and on the MFMA kernel the file names."""
+    path = path or os.path.join(ROOT, "profiles", "traffic.json")
+    if not on_mfma or not os.path.exists(path):
+        return None
+    tr = json.load(open(path))
+    if (tr.get("kernel") == kernel and tr.get("source") == source_digest(kernel) and tr.get("run") == key
+            and tr.get("symbol") == KERNEL_SYMBOL.get(kernel)):
+        return tr.get("bytes_per_launch")
+    return None
+
+
 def cpu_baseline(case, target_s):
     """The oracle (plain fp64 C, one thread) on a bounded sample of the same workload:
     a seeded subset of bags of every table, forward then backward.  Returns the
@@ -478,14 +492,7 @@ def main():
         achieved = work / (dom_ms * 1e-3) / 1e9
         roof = dict(bound=bound, achieved=round(achieved, 1), peak=PEAK_HBM / 1e9, unit="GB/s",
                     frac=round(achieved / (PEAK_HBM / 1e9), 4))
-    roof["traffic"] = None
-    tpath = os.path.join(ROOT, "profiles", "traffic.json")
-    if os.path.exists(tpath):
-        tr = json.load(open(tpath))
-        if (tr.get("kernel") == dominant and tr.get("source") == source_digest(dominant)
-                and tr.get("run") == run_key(args) and tr.get("symbol") == KERNEL_SYMBOL[dominant]
-                and on_mfma):
-            roof["traffic"] = tr.get("bytes_per_launch")
+    roof["traffic"] = measured_traffic(dominant, run_key(args), on_mfma)
     roof["kernel"] = dominant
     roof["kernel_ms"] = round(dom_ms, 4)
 
