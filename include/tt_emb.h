@@ -292,7 +292,8 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
 /* Whether `kernel` (TT_EMB_K_FWD_FUSED or TT_EMB_K_BWD_FUSED) runs on the
  * matrix cores for this handle: *uses_mfma = 1 for the MFMA kernels (forward
  * for the view d = (4,4,8) with R = 32 or 64, backward for d = (4,4,8) with
- * R = 32 and n3 <= 252), 0 for the generic vector-ALU kernels.  The forward
+ * R = 32, n3 <= 252 and at most 64 tables; both only while their 32-bit
+ * offsets into E and the cores fit), 0 for the generic vector-ALU kernels.  The forward
  * decides per call from its index count, given here as num_indices
  * (0 <= num_indices <= desc.max_indices); the backward decides from
  * desc.max_indices.  Every other kernel id reports 0.  Host only.
