@@ -1,14 +1,18 @@
 #!/usr/bin/env python3
-"""TT-embedding training-step benchmark on one MI355X.
+"""TT-embedding benchmark on one MI355X.
 
-One step is the whole hot path over one batch: prefix-based index grouping,
-fused forward (C = A.B per prefix group, E = C.D per unique row), sum pooling,
-backward (dE segment sums, per-group dD/dC/dA/dB, core-gradient reduction)
-and the in-place SGD update.  Default workload: 8 TT tables of 1e7 rows
-(200 x 200 x 250), D = 128 = 4 x 4 x 8, rank 32, 32,768 bags per table with
-Poisson(20) lengths clipped to [1, 64], Zipf(1.1) row popularity over a seeded
-permutation, upstream gradient N(0, 1), lr 0.01.  Inputs are synthetic and
-already resident in HBM when the timed region starts.
+Default: the training step of the 8-table workload.  One step is the whole
+hot path over one batch: prefix-based index grouping, fused forward
+(C = A.B per prefix group, E = C.D per unique row), sum pooling, backward
+(dE segment sums, per-group dD/dC/dA/dB, core-gradient reduction) and the
+in-place SGD update.  Workload: 8 TT tables of 1e7 rows (200 x 200 x 250),
+D = 128 = 4 x 4 x 8, rank 32, 32,768 bags per table with Poisson(20) lengths
+clipped to [1, 64], Zipf(1.1) row popularity over a seeded permutation,
+upstream gradient N(0, 1), lr 0.01.
+
+`--config 1..4` runs the forward-only workloads (one step = grouping, fused
+forward and pooling); `--mode` overrides the step kind.  Inputs are synthetic
+and already resident in HBM when the timed region starts.
 
 Prints one JSON line (see the keys at the end of main()).
 """
@@ -142,20 +146,91 @@ KERNEL_SYMBOL = {"fwd_fused": "k_fwd_r32", "bwd_fused": "k_bwd_r32", "pool": "k_
                  "ingest": "k_ingest"}
 
 
+def kernel_symbol(kernel, R=32):
+    """Symbol of the MFMA kernel that serves `kernel` at rank R (the forward has one
+    for R = 32 and one for R = 64)."""
+    if kernel == "fwd_fused" and R == 64:
+        return "k_fwd_r64"
+    return KERNEL_SYMBOL[kernel]
+
+
+def step_work(case, counts, mode):
+    """Algorithmic flops F and HBM bytes Q of one whole step (all tables), from the
+    workload and its grouping (U unique rows, P prefix groups over all tables).
+      forward: F = P 2 d1 d2 R^2 + U 2 D R + M D (stage 1, stage 2, pooling adds)
+               Q = 8 M (indices) + 8 (T B + 1) (offsets) + 4 T B D (output) + 4 |cores| (read once)
+      train  : adds F += M D (dE aggregation) + U 4 D R (dD, dC) + P 6 d1 d2 R^2 (C again, dA, dB)
+                        + 2 |cores| (the update)
+                    Q += 4 T B D (upstream gradient) + 4 |cores| (gradients) + 12 |cores| (update:
+                        read core and gradient, write core)"""
+    T, B, R = case["T"], case["B"], case["R"]
+    (n1, n2, n3), (d1, d2, d3) = view_dims(case["n"], case["d"])
+    D = d1 * d2 * d3
+    U, P = counts["U"], counts["P"]
+    M = int(case["idx"].size)
+    if "cores" in case:
+        ncore = sum(int(G.size) for G in case["cores"])
+    else:
+        ncore = int(case["G1"].size + case["G2"].size + case["G3"].size)
+    F = P * 2.0 * d1 * d2 * R * R + U * 2.0 * D * R + M * D
+    Q = 8.0 * M + 8.0 * (T * B + 1) + 4.0 * T * B * D + 4.0 * ncore
+    if mode == "train":
+        F += M * D + U * 4.0 * D * R + P * 6.0 * d1 * d2 * R * R + 2.0 * ncore
+        Q += 4.0 * T * B * D + 4.0 * ncore + 12.0 * ncore
+    return F, Q
+
+
+def whole_call(case, counts, mode, ms):
+    """The step's roofline time max(F / peak FP32, Q / peak HBM) and its fraction of the
+    measured step time."""
+    F, Q = step_work(case, counts, mode)
+    tf, tq = F / PEAK_FP32_MFMA, Q / PEAK_HBM
+    t = max(tf, tq)
+    return {"flop": F, "bytes": Q, "bound": "fp32" if tf >= tq else "hbm", "roof_ms": round(t * 1e3, 5),
+            "frac": round(t / (ms * 1e-3), 4)}
+
+
+def cpu_model():
+    """Model name of the host CPU (first entry of /proc/cpuinfo) and its logical CPU count."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return name, os.cpu_count() or 0
+
+
 def run_key(args):
     """What a counter measurement holds for: the workload and the flags that change the kernels' work."""
     import ttgen
 
     name = ttgen.CONFIGS[args.config]["workload"]
+    if getattr(args, "bags", None):
+        name += f"_bags{args.bags}"
     if args.row_factors or args.cores != 3:
         L = len(args.row_factors.split(",")) if args.row_factors else args.cores
         name += f"_{L}cores"
         if args.row_factors:
             name += f"[{args.row_factors}|{args.dim_factors}]"
-    return {"workload": name, "reuse": args.reuse, "sched": args.sched, "fused_sgd": not args.unfused_sgd}
+    key = {"workload": name, "reuse": args.reuse, "sched": args.sched, "fused_sgd": not args.unfused_sgd}
+    mode = step_mode(args)
+    if mode != "train":
+        key["mode"] = mode
+    return key
 
 
-def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused"):
+def step_mode(args):
+    """The step the run times: the training step for the training workload (config 5),
+    the forward for the forward-only workloads, unless --mode says otherwise."""
+    m = getattr(args, "mode", None)
+    return m if m else ("train" if args.config == 5 else "forward")
+
+
+def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused", R=32):
     """HBM bytes per launch of `kernel` from rocprofv3 FETCH_SIZE and WRITE_SIZE (KiB per dispatch).
 
     Each counter is scaled by the factor that makes it read the true size on the
@@ -166,7 +241,7 @@ def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused"):
 
     import numpy as np
 
-    sym = KERNEL_SYMBOL[kernel]
+    sym = kernel_symbol(kernel, R)
     vals = {"FETCH_SIZE": {"k": [], "copy": []}, "WRITE_SIZE": {"k": [], "copy": []}}
     for f in sorted(glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)):
         for r in csv.DictReader(open(f)):
@@ -192,31 +267,41 @@ def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused"):
         total += raw * scale * 1024.0
     out["bytes_per_launch"] = round(total)
     path = os.path.join(ROOT, "profiles", "traffic.json")
+    entries = traffic_entries(path)
+    entries = [e for e in entries if not (e.get("kernel") == kernel and e.get("run") == key)] + [out]
     with open(path, "w") as f:
-        json.dump(out, f, indent=1)
+        json.dump({"entries": entries}, f, indent=1)
         f.write("\n")
     print(json.dumps(out))
 
 
-def measured_traffic(kernel, key, on_mfma, path=None):
-    """HBM bytes per launch from profiles/traffic.json, or None unless those counters
-    were taken on this kernel as it is now (source digest), on this run (workload,
-    reuse, schedule, update mode) and on the MFMA kernel the file names."""
-    path = path or os.path.join(ROOT, "profiles", "traffic.json")
-    if not on_mfma or not os.path.exists(path):
-        return None
+def traffic_entries(path):
+    """Stored counter measurements: one entry per (kernel, run)."""
+    if not os.path.exists(path):
+        return []
     tr = json.load(open(path))
-    if (tr.get("kernel") == kernel and tr.get("source") == source_digest(kernel) and tr.get("run") == key
-            and tr.get("symbol") == KERNEL_SYMBOL.get(kernel)):
-        return tr.get("bytes_per_launch")
+    return tr.get("entries", [tr] if "kernel" in tr else [])
+
+
+def measured_traffic(kernel, key, on_mfma, path=None, R=32):
+    """HBM bytes per launch from profiles/traffic.json, or None unless counters were
+    taken on this kernel as it is now (source digest), on this run (workload, reuse,
+    schedule, update mode, step) and on the MFMA kernel the entry names."""
+    path = path or os.path.join(ROOT, "profiles", "traffic.json")
+    if not on_mfma:
+        return None
+    for tr in traffic_entries(path):
+        if (tr.get("kernel") == kernel and tr.get("source") == source_digest(kernel) and tr.get("run") == key
+                and tr.get("symbol") == kernel_symbol(kernel, R)):
+            return tr.get("bytes_per_launch")
     return None
 
 
-def cpu_baseline(case, target_s):
+def cpu_baseline(case, target_s, mode="train"):
     """The oracle (plain fp64 C, one thread) on a bounded sample of the same workload:
-    a seeded subset of bags of every table, forward then backward.  Returns the
-    one-thread figure and the same sample with the tables (independent) run on a
-    thread pool, one single-table oracle call per table."""
+    a seeded subset of bags of every table, forward then (training step) backward.
+    Returns the one-thread figure and the same sample with the tables (independent)
+    run on a thread pool, one single-table oracle call per table."""
     import numpy as np
 
     import oracle
@@ -235,26 +320,34 @@ def cpu_baseline(case, target_s):
                 lo, hi = (off[gb], off[gb + 1]) if off is not None else (gb, gb + 1)
                 idx_parts.append(case["idx"][lo:hi])
                 lens.append(hi - lo)
-            dv.append(case["dV"][t, bags])
+            if "dV" in case:
+                dv.append(case["dV"][t, bags])
         o = np.zeros(T * nb + 1, np.int64)
         o[1:] = np.cumsum(lens)
-        return dict(case, B=nb, idx=np.concatenate(idx_parts), offsets=o, dV=np.stack(dv))
+        out = dict(case, B=nb, idx=np.concatenate(idx_parts), offsets=o)
+        if dv:
+            out["dV"] = np.stack(dv)
+        return out
 
     def run(c):
         t0 = time.perf_counter()
         if "cores" in c:
             oracle.forward_n(c)
-            oracle.backward_n(c)
+            if mode == "train":
+                oracle.backward_n(c)
         else:
             oracle.forward(c)
-            oracle.backward(c)
+            if mode == "train":
+                oracle.backward(c)
         return time.perf_counter() - t0
 
     def table(c, t):  # table t of a sample as a one-table case
         nb = c["B"]
         o = c["offsets"]
         lo, hi = o[t * nb], o[(t + 1) * nb]
-        one = dict(c, T=1, idx=c["idx"][lo:hi], offsets=o[t * nb:(t + 1) * nb + 1] - lo, dV=c["dV"][t:t + 1])
+        one = dict(c, T=1, idx=c["idx"][lo:hi], offsets=o[t * nb:(t + 1) * nb + 1] - lo)
+        if "dV" in c:
+            one["dV"] = c["dV"][t:t + 1]
         if "cores" in c:
             one["cores"] = [G[t:t + 1] for G in c["cores"]]
         else:
@@ -268,9 +361,11 @@ def cpu_baseline(case, target_s):
     s = sub(nb)
     dt = run(s)
     lookups = int(s["idx"].size)
+    what = "forward + backward" if mode == "train" else "forward"
+    model, ncpu = cpu_model()
     one = dict(value=lookups / dt, unit="lookups/s", cores=1, kind="oracle",
-               sample=f"{nb} seeded bags per table x {T} tables ({lookups} lookups), forward + backward, "
-                      f"fp64 C oracle, 1 thread, {dt:.1f} s")
+               sample=f"{nb} seeded bags per table x {T} tables ({lookups} lookups), {what}, "
+                      f"fp64 C oracle, 1 thread, {dt:.1f} s", cpu_model=model, host_cpus=ncpu)
     from concurrent.futures import ThreadPoolExecutor
     nthr = max(1, min(T, os.cpu_count() or 1, 16))
     parts = [table(s, t) for t in range(T)]
@@ -280,7 +375,7 @@ def cpu_baseline(case, target_s):
     dtm = time.perf_counter() - t0
     many = dict(value=lookups / dtm, unit="lookups/s", cores=nthr, kind="oracle",
                 sample=f"the same sample, {T} tables on {nthr} threads (one single-table oracle call each), "
-                       f"{dtm:.1f} s")
+                       f"{dtm:.1f} s", cpu_model=model, host_cpus=ncpu)
     return one, many
 
 
@@ -289,7 +384,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=5, help="workload recipe (5 = training step)")
+    ap.add_argument("--config", type=int, default=5,
+                    help="workload recipe (5 = training step; 1-4 = the forward-only workloads)")
+    ap.add_argument("--mode", choices=["train", "forward"], default=None,
+                    help="step to time: training step (default for config 5) or forward = grouping, fused "
+                         "forward and pooling (default for configs 1-4)")
+    ap.add_argument("--bags", type=int, default=None, help="bags per table (default: the workload's 32,768)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--reuse", choices=["prefix", "unique", "none"], default="prefix",
                     help="reuse level (ablation of Section 4.5): prefix groups (default), exact dedup only, none")
@@ -311,9 +411,15 @@ def main():
                     help="CPU only: turn the FETCH_SIZE / WRITE_SIZE counter CSVs under DIR (one rocprofv3 --pmc "
                          "pass each, of a run with --copy-mib and the same workload flags) into "
                          "profiles/traffic.json, then exit")
+    ap.add_argument("--traffic-kernel", default=None, choices=sorted(KERNEL_SYMBOL),
+                    help="with --write-traffic: the kernel the counters are for (default: the step's fused kernel)")
     args = ap.parse_args()
+    mode = step_mode(args)
     if args.write_traffic:
-        write_traffic(args.write_traffic, run_key(args))
+        import ttgen
+
+        kern = args.traffic_kernel or ("bwd_fused" if mode == "train" else "fwd_fused")
+        write_traffic(args.write_traffic, run_key(args), kernel=kern, R=ttgen.CONFIGS[args.config]["R"])
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the library has no multi-GPU path", file=sys.stderr)
@@ -325,7 +431,7 @@ def main():
     import paper_2609_03459_amd as P
     import ttgen
 
-    case = ttgen.make(args.config, with_grad=True)
+    case = ttgen.make(args.config, bags=args.bags, with_grad=mode == "train")
     if args.row_factors or args.cores != 3:
         if args.row_factors:
             nL = tuple(int(x) for x in args.row_factors.split(","))
@@ -355,10 +461,11 @@ def main():
         G = [torch.from_numpy(case[k]).to(dev) for k in ("G1", "G2", "G3")]
     idx = torch.from_numpy(case["idx"]).to(dev)
     off = None if case["offsets"] is None else torch.from_numpy(case["offsets"]).to(dev)
-    dV = torch.from_numpy(case["dV"]).to(dev)
+    dV = torch.from_numpy(case["dV"]).to(dev) if mode == "train" else None
     out = torch.empty((T, B, D), dtype=torch.float32, device=dev)
-    grads = tuple(torch.empty(s, dtype=torch.float32, device=dev) for s in emb.core_shapes())
-    lr = case["lr"]
+    grads = tuple(torch.empty(s, dtype=torch.float32, device=dev) for s in emb.core_shapes()) if (
+        mode == "train" and ("cores" in case or args.unfused_sgd)) else None
+    lr = case.get("lr", 0.01)
     stream = torch.cuda.current_stream().cuda_stream
     ev = HipEvents()
 
@@ -394,8 +501,9 @@ def main():
 
     def step():
         fwd(False)
-        bwd()
-        sgd()
+        if mode == "train":
+            bwd()
+            sgd()
 
     if args.copy_mib:
         # reads and writes exactly copy_mib MiB each: the calibration of the byte counters
@@ -406,7 +514,8 @@ def main():
         del x, y
 
     # warmup; the first steps also time each candidate kernel once
-    kernels = [k for k in P.N.KERNELS if L >= 4 or k not in ("merge", "split")]
+    kernels = [k for k in P.N.KERNELS if (L >= 4 or k not in ("merge", "split")) and
+               (mode == "train" or k not in ("seg_sum", "bwd_fused", "split"))]
     kernel_ms = {}
     e0, e1 = ev.create(), ev.create()
     for w in range(max(args.warmup, len(kernels))):
@@ -458,6 +567,8 @@ def main():
 
     # phase split (grouping / forward / backward / sgd), as in the paper's breakdown
     phases = {"group": [], "forward": [], "backward": [], "sgd": []}
+    if mode != "train":
+        phases = {"group": [], "forward": []}
     pe = [ev.create() for _ in range(5)]
     for _ in range(3):
         ev.record(pe[0], stream)
@@ -465,10 +576,11 @@ def main():
         ev.record(pe[1], stream)
         fwd(True)
         ev.record(pe[2], stream)
-        bwd()
-        ev.record(pe[3], stream)
-        sgd()
-        ev.record(pe[4], stream)
+        if mode == "train":
+            bwd()
+            ev.record(pe[3], stream)
+            sgd()
+            ev.record(pe[4], stream)
         torch.cuda.synchronize()
         for j, name in enumerate(phases):
             phases[name].append(ev.elapsed_ms(pe[j], pe[j + 1]))
@@ -492,8 +604,9 @@ def main():
         achieved = work / (dom_ms * 1e-3) / 1e9
         roof = dict(bound=bound, achieved=round(achieved, 1), peak=PEAK_HBM / 1e9, unit="GB/s",
                     frac=round(achieved / (PEAK_HBM / 1e9), 4))
-    roof["traffic"] = measured_traffic(dominant, run_key(args), on_mfma)
+    roof["traffic"] = measured_traffic(dominant, run_key(args), on_mfma, R=R)
     roof["kernel"] = dominant
+    roof["symbol"] = kernel_symbol(dominant, R) if on_mfma else None
     roof["kernel_ms"] = round(dom_ms, 4)
 
     lookups = M
@@ -513,11 +626,13 @@ def main():
         "config": {"workload": case["workload"], "tables": T, "rows_per_table": case["N"], "cores": L,
                    "row_factors": list(n),
                    "dim_factors": list(d), "rank": R, "batch_per_table": B, "lookups": lookups,
-                   "step": "group+forward+pool+backward+sgd" + (
-                       " (sgd fused into the backward's reductions)" if L == 3 and not args.unfused_sgd else ""),
+                   "step": ("group+forward+pool+backward+sgd" + (
+                       " (sgd fused into the backward's reductions)" if L == 3 and not args.unfused_sgd else ""))
+                   if mode == "train" else "group+forward+pool",
                    "parallelism": "single-gpu",
                    "reuse": args.reuse, "sched": args.sched},
         "roofline": roof,
+        "whole_call": whole_call(case, counts, mode, ms_per_step),
         "step_ms_median": round(step_med, 4),
         "copy_gbps_measured": round(copy_gbps, 1),
         "phases_ms": phases_ms,
@@ -525,7 +640,7 @@ def main():
         "grouping": {"unique_rows": counts["U"], "prefix_groups": counts["P"], "slices": counts["nslices"]},
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"], res["cpu_baseline_threads"] = cpu_baseline(case, args.cpu_seconds)
+        res["cpu_baseline"], res["cpu_baseline_threads"] = cpu_baseline(case, args.cpu_seconds, mode)
     print(json.dumps(res), flush=True)
 
 

@@ -125,10 +125,20 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
 typedef enum { TT_EMB_SCHED_STEAL = 0, TT_EMB_SCHED_STATIC = 1, TT_EMB_SCHED_STEAL_CKPT = 2 } tt_emb_sched;
 tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode);
 
-/* Bytes of device workspace needed for calls up to desc.max_indices and
- * desc.max_bags at the handle's reuse level.  The same workspace carries the
- * index grouping from a forward call to the following backward call. */
-tt_emb_status tt_emb_workspace_size(tt_emb_handle h, size_t* bytes);
+/* Bytes of device workspace for a call with num_indices indices and num_bags
+ * bags per table (0 <= num_indices <= desc.max_indices, 0 <= num_bags <=
+ * desc.max_bags), at the handle's reuse level; pass the desc maxima for a
+ * workspace that serves every call.  The same workspace carries the index
+ * grouping from a forward call to the following backward call of the same
+ * sizes.  This is the size a backward call (tt_emb_backward,
+ * tt_emb_backward_sgd, tt_emb_backward_n) requires; tt_emb_group and the
+ * forward calls accept less, since the regions only the backward uses (dE
+ * partials and gradient partials) come last in the layout.  Everything
+ * bounded by the batch scales with num_indices (about 40 bytes plus 4*D bytes
+ * of rows per index, and up to (num_indices/32 + prefix groups) work slices);
+ * the dense per-prefix arrays take 12 bytes per (table, i1, i2) slot.  Host
+ * only.  TT_EMB_EINVAL for a NULL handle or pointer or sizes out of range. */
+tt_emb_status tt_emb_workspace_size(tt_emb_handle h, int64_t num_indices, int64_t num_bags, size_t* bytes);
 
 /* Prefix-based index grouping alone (Section 3.3, Fig. 4): sort the indices
  * of each table, keep exact uniques, take their mixed-radix digits and
@@ -154,8 +164,13 @@ tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, 
  * no index touches are zero).  Per unique row, dE is the sum of grad_out
  * over its occurrences; per row dD = C^T dE and dC = dE D^T; per prefix
  * group the dC are summed first and dA = (sum dC) B^T, dB = A^T (sum dC).
- * Per-core gradients are reduced by segments, not by per-row global atomics.
- * reuse_grouping as for tt_emb_forward. */
+ * On the MFMA shape (see tt_emb_kernel_uses_mfma) the gradients of G1 and G2
+ * are fixed-order segment sums of per-slice and per-chunk partials, and dG3 is
+ * summed in on-chip memory per (table, rank half) and then over workgroups in
+ * a fixed order (its on-chip adds land in arrival order, so dG3 is
+ * reproducible to rounding, not bit for bit); the generic kernels of other
+ * shapes add their partial products into the gradients with global float
+ * atomics.  reuse_grouping as for tt_emb_forward. */
 tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
                               const int64_t* indices, int64_t num_indices, const int64_t* offsets,
                               int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
@@ -204,9 +219,10 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
  * and the three-core operator runs on it and cores L-2, L-1:
  * C = (merged slice) . S_{L-2} once per prefix group of the first L-1 digits,
  * E = C . S_{L-1} per unique row.  The backward carries the merged core's
- * gradient back through the chain one level at a time, with plain sums (no
- * atomics), into cores 0..L-3.  For L = 2 the middle core of the three-core
- * operator is the identity.  Grouping,
+ * gradient back through the chain one level at a time into cores 0..L-3; each
+ * level's blocks add their chunk sums into those gradients with global float
+ * atomics.  For L = 2 the middle core of the three-core operator is the
+ * identity.  Grouping,
  * reuse levels, schedules, errors and tt_emb_debug_grouping work as above on
  * the three-factor view (n_0...n_{L-3}, n_{L-2}, n_{L-1}) for L >= 4 and
  * (n_0, 1, n_1) for L = 2: its digits and prefix keys are those of the view.
@@ -293,10 +309,10 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
  * matrix cores for this handle: *uses_mfma = 1 for the MFMA kernels (forward
  * for the view d = (4,4,8) with R = 32 or 64, backward for d = (4,4,8) with
  * R = 32, n3 <= 252 and at most 64 tables; both only while their 32-bit
- * offsets into E and the cores fit), 0 for the generic vector-ALU kernels.  The forward
- * decides per call from its index count, given here as num_indices
- * (0 <= num_indices <= desc.max_indices); the backward decides from
- * desc.max_indices.  Every other kernel id reports 0.  Host only.
+ * offsets into E and the cores fit), 0 for the generic vector-ALU kernels.
+ * Both decide per call from its index count, given here as num_indices
+ * (0 <= num_indices <= desc.max_indices).  Every other kernel id reports 0.
+ * Host only.
  * TT_EMB_EINVAL for a NULL handle or flag, an unknown kernel id or
  * num_indices out of range. */
 tt_emb_status tt_emb_kernel_uses_mfma(tt_emb_handle h, int kernel, int64_t num_indices, int* uses_mfma);

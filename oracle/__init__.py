@@ -60,7 +60,7 @@ def _load():
         lib.orc_backward.restype = C.c_int64
         lib.orc_forward_n.argtypes = [C.POINTER(_ShapeN), P, P, C.c_int64, P, P]
         lib.orc_forward_n.restype = C.c_int64
-        lib.orc_backward_n.argtypes = [C.POINTER(_ShapeN), P, P, C.c_int64, P, P, P]
+        lib.orc_backward_n.argtypes = [C.POINTER(_ShapeN), P, P, C.c_int64, P, P, P, P]
         lib.orc_backward_n.restype = C.c_int64
         lib.orc_sgd.argtypes = [P, P, C.c_int64, C.c_double, P]
         lib.orc_sgd.restype = None
@@ -215,15 +215,24 @@ def forward_n(case):
     return V, int(inv)
 
 
-def backward_n(case, dV=None):
+def backward_n(case, dV=None, want=None):
     """Core gradients with L cores of L = sum <dV, V>: the chain rule through the chain
-    of slices, per occurrence (for L = 3 exactly Eq. 1).  Returns ([dG_k], invalid)."""
+    of slices, per occurrence (for L = 3 exactly Eq. 1).  `want` = optional list of L
+    per-slice boolean masks [T*n_k] (or None entries): only the wanted slices are then
+    guaranteed exact.  Returns ([dG_k], invalid)."""
     s = _shape_n(case)
     cores = [_f32(G) for G in case["cores"]]
     dV = _f32(case["dV"] if dV is None else dV)
     idx = _i64(case["idx"])
     off = _i64(case["offsets"])
     dG = [np.zeros(G.shape, dtype=np.float64) for G in cores]
+    wp = None
+    if want is not None:
+        masks = [None if w is None else np.ascontiguousarray(w, dtype=np.uint8) for w in want]
+        if len(masks) != s.L:
+            raise ValueError("one mask (or None) per core")
+        wp = (C.c_void_p * s.L)(*[None if m is None else m.ctypes.data for m in masks])
     inv = _load().orc_backward_n(C.byref(s), C.cast(_ptr_array(cores), C.c_void_p), _ptr(idx), idx.size, _ptr(off),
-                                 _ptr(dV), C.cast(_ptr_array(dG), C.c_void_p))
+                                 _ptr(dV), C.cast(_ptr_array(dG), C.c_void_p),
+                                 None if wp is None else C.cast(wp, C.c_void_p))
     return dG, int(inv)

@@ -355,9 +355,13 @@ int64_t orc_forward_n(const shape_n_t* s, const float* const* G, const int64_t* 
  *   for k = L-1 .. 1:  dS_k += X_{k-1}^T dX_k     (dX_k viewed as m_{k-1} x d_k r_{k+1})
  *                      dX_{k-1} = dX_k S_k^T      (m_{k-1} x r_k)
  *   dS_0 += dX_0.
- * For L = 3: dG3 += C^T dE, dC = dE D^T, dG2 += A^T dC, dG1 += dC B^T (Eq. 1). */
+ * For L = 3: dG3 += C^T dE, dC = dE D^T, dG2 += A^T dC, dG1 += dC B^T (Eq. 1).
+ * Optional want: NULL, or L masks (each NULL or per-slice flags [T*n_k]); when
+ * some mask is given, an occurrence that touches no wanted slice of any core is
+ * skipped, so only the wanted slices' gradients are guaranteed (those stay
+ * exact: every occurrence that adds to them is kept, in the same order). */
 int64_t orc_backward_n(const shape_n_t* s, const float* const* G, const int64_t* idx, int64_t M,
-                       const int64_t* offsets, const float* dV, double* const* dG) {
+                       const int64_t* offsets, const float* dV, double* const* dG, const uint8_t* const* want) {
   int64_t D = dimD_n(s);
   for (int k = 0; k < s->L; ++k) memset(dG[k], 0, sizeof(double) * s->T * s->n[k] * slice_len_n(s, k));
   int64_t* bag = (int64_t*)malloc(sizeof(int64_t) * (M > 0 ? M : 1));
@@ -371,6 +375,8 @@ int64_t orc_backward_n(const shape_n_t* s, const float* const* G, const int64_t*
   double** dX = alloc_chain_n(s);
   int64_t dig[ORC_MAXL];
   int64_t invalid = 0;
+  int masked = 0;  /* as in orc_backward: select only when some mask is given */
+  for (int k = 0; want && k < s->L; ++k) masked |= want[k] != NULL;
   for (int64_t o = 0; o < M; ++o) {
     int64_t g = idx[o];
     if (g < 0 || g >= s->N) {
@@ -379,6 +385,11 @@ int64_t orc_backward_n(const shape_n_t* s, const float* const* G, const int64_t*
     }
     int64_t gb = bag[o], t = gb / s->B;
     mixed_radix_n(s, g, dig);
+    if (masked) {
+      int w = 0;
+      for (int k = 0; k < s->L && !w; ++k) w = want[k] && want[k][t * s->n[k] + dig[k]];
+      if (!w) continue;
+    }
     chain_n(s, G, t, dig, X);
     for (int64_t j = 0; j < D; ++j) dX[s->L - 1][j] = (double)dV[gb * D + j];
     int64_t m = D / s->d[s->L - 1];  /* m_{L-2} */

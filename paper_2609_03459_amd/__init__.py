@@ -68,7 +68,8 @@ class TTEmbedding:
         self.reuse = reuse
         # work distribution (Section 4.4 ablation): "steal" (default), "static" or "steal_ckpt"
         self.set_schedule(sched)
-        self.ws_bytes = N.tt_emb_workspace_size(self.handle)
+        # a workspace that serves every call up to the maxima
+        self.ws_bytes = N.tt_emb_workspace_size(self.handle, int(max_indices), int(max_bags))
         # 256-byte aligned workspace carved from one torch allocation
         raw = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=device)
         shift = (-raw.data_ptr()) % 256
@@ -81,10 +82,14 @@ class TTEmbedding:
         self.sched = sched
 
     def __del__(self):
+        # at interpreter exit the binding's module globals may already be gone
         h = getattr(self, "handle", None)
-        if h:
-            N.tt_emb_destroy(h)
-            self.handle = None
+        self.handle = None
+        if h and N is not None and getattr(N, "lib", None) is not None:
+            try:
+                N.tt_emb_destroy(h)
+            except Exception:
+                pass
 
     # shapes
     def core_shapes(self):

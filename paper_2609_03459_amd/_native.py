@@ -58,7 +58,7 @@ _I64 = C.c_int64
 _SIG = {
     "tt_emb_create": ([C.POINTER(tt_emb_desc), C.POINTER(_P)], C.c_int),
     "tt_emb_destroy": ([_P], C.c_int),
-    "tt_emb_workspace_size": ([_P, C.POINTER(C.c_size_t)], C.c_int),
+    "tt_emb_workspace_size": ([_P, _I64, _I64, C.POINTER(C.c_size_t)], C.c_int),
     "tt_emb_group": ([_P, _P, _I64, _P, _I64, _P, C.c_size_t, _P], C.c_int),
     "tt_emb_forward": ([_P, _P, _P, _P, _P, _I64, _P, _I64, _P, C.c_int, _P, C.c_size_t, _P], C.c_int),
     "tt_emb_backward": ([_P, _P, _P, _P, _P, _I64, _P, _I64, _P, _P, _P, _P, C.c_int, _P, C.c_size_t, _P],
@@ -143,9 +143,9 @@ def tt_emb_destroy(h: int) -> None:
     check("tt_emb_destroy", lib.tt_emb_destroy(h))
 
 
-def tt_emb_workspace_size(h: int) -> int:
+def tt_emb_workspace_size(h: int, num_indices: int, num_bags: int) -> int:
     n = C.c_size_t()
-    check("tt_emb_workspace_size", lib.tt_emb_workspace_size(h, C.byref(n)))
+    check("tt_emb_workspace_size", lib.tt_emb_workspace_size(h, int(num_indices), int(num_bags), C.byref(n)))
     return int(n.value)
 
 

@@ -553,10 +553,12 @@ __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const
 }
 
 bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit float offsets into dE (rows x 128) and G3 must fit
+  // 32-bit float offsets into dE (rows x 128), G1 (slices of 128), G2 (slices of 4,096) and G3 (slices
+  // of 256) must fit
   // LDS: the n3 x 128 accumulator plus 8 x 16 x SCR_PITCH scratch floats fit 160 KB for n3 <= 252
   return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 252 && s.T <= 64 &&
-         max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31);
+         max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) &&
+         (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n2 * 4096 < (int64_t(1) << 31);
 }
 
 // With update set, dG1..dG3 are the cores themselves and receive G -= lr * dG.
@@ -564,7 +566,8 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
                           float* dG1, float* dG2, float* dG3, float lr, bool update, const Prof& prof,
                           hipStream_t st) {
   const int nq = 2 * s.T;
-  int per_q = persistent_grid() / nq;
+  const int cap = persistent_grid() < MAX_BWD_WG ? persistent_grid() : MAX_BWD_WG;
+  int per_q = cap / nq;
   if (per_q < 1) per_q = 1;
   const int grid = nq * per_q;
   if (grid > MAX_BWD_WG || nq * SCHED_STRIDE > C_TOTAL - C_BWD_CTR) return hipErrorInvalidValue;

@@ -66,7 +66,7 @@ constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
 constexpr int SLICE_ROWS = 32;   // unique rows per work slice
 constexpr int CHUNK_SLICES = 32; // slices per chunk of the specialised kernels (one (t, i2) run)
 constexpr int SEG_CHUNK = 256;   // sorted occurrences per dE chunk
-constexpr int MAX_BWD_WG = 1024;
+constexpr int MAX_BWD_WG = 256;  // workgroups of the MFMA backward (one per CU on MI355X)
 
 // Device pointers carved out of the caller's workspace.
 struct Work {
@@ -128,6 +128,8 @@ inline void prof_end(const Prof& p, int k, hipStream_t st) {
 
 // Workspace layout for given capacities (bytes) and carving.
 size_t workspace_bytes(const Shape& s, int64_t M, int64_t B);
+// Bytes of that layout a forward call uses (the regions before the backward-only ones).
+size_t forward_workspace_bytes(const Shape& s, int64_t M, int64_t B);
 void carve(const Shape& s, int64_t M, int64_t B, void* base, Work* w);
 
 // Launchers (each returns hipGetLastError() of its launches).

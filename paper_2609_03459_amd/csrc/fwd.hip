@@ -755,9 +755,10 @@ bool fwd_r64_supported(const Shape& s, int64_t max_indices) {
 }
 
 bool fwd_r32_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit float offsets into E (rows x 128), G1 and G3
+  // 32-bit float offsets into E (rows x 128), G1 (slices of 128), G2 (slices of 4,096) and G3 (slices of 256)
   return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
-         (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31);
+         (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) &&
+         (int64_t)s.T * s.n2 * 4096 < (int64_t(1) << 31);
 }
 
 hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,

@@ -328,8 +328,8 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
 // the tile in LDS in digit order, which for a single tile is the sorted order of
 // that pass.  Reads keys/vals and writes kout/vout (which may be the same arrays).
 template <int BITS>
-__global__ void __launch_bounds__(SORT_THREADS) k_sort_tile(const uint32_t* __restrict__ kin,
-                                                            const uint32_t* __restrict__ vin, uint32_t* kout,
+__global__ void __launch_bounds__(SORT_THREADS) k_sort_tile(const uint32_t* kin,
+                                                            const uint32_t* vin, uint32_t* kout,
                                                             uint32_t* vout, int n, int npasses, int dbits) {
   constexpr int NB = 1 << BITS;
   __shared__ uint32_t wh[4][NB];  // per-wave digit counts, then the wave's base per digit

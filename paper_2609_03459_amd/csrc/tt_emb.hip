@@ -27,10 +27,13 @@ namespace ttemb {
 static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 
-// Walks the workspace regions in a fixed order; with base == nullptr it only
-// measures.
-static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) {
-  (void)B;
+// Walks the workspace regions of a call with M indices and B bags per table in
+// a fixed order; with base == nullptr it only measures.  Regions that only the
+// backward uses come last: *fwd_end receives where they start, so a forward
+// call needs fewer bytes than a training step.  The grouping that a forward
+// leaves for a backward (reuse_grouping) sits at the same offsets in both, since
+// both calls have the same M and B.
+static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, size_t* fwd_end = nullptr) {
   const int64_t m = M > 0 ? M : 1;
   const int64_t sort_tiles = (m + SORT_TILE - 1) / SORT_TILE;
   const int64_t scan_tiles = (m + SCAN_TILE - 1) / SCAN_TILE;
@@ -44,6 +47,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   };
   Work tmp;
   Work* W = w ? w : &tmp;
+  // --- regions of every call: counters, sort, grouping, work list, rows ---
   W->ctr = (int32_t*)take(sizeof(int32_t) * C_TOTAL);
   W->keys[0] = (uint32_t*)take(4 * m);
   W->keys[1] = (uint32_t*)take(4 * m);
@@ -65,11 +69,15 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->dense_cnt = (uint32_t*)take(4 * s.ndense);
   W->dense_base = (uint32_t*)take(4 * s.ndense);
   W->dense_pg = (int32_t*)take(4 * s.ndense);
-  // slices: at most one per valid occurrence and ceil(n3 / SLICE_ROWS) per prefix
-  // (without dedup a prefix can hold any number of rows: bounded by m alone)
+  // Slices: a prefix group of r rows gives ceil(r / slice_rows) < r / slice_rows + 1
+  // of them, so there are fewer than U / slice_rows + P <= m / slice_rows + min(ndense, m);
+  // with dedup a group also has at most n3 rows, and no slice is empty (at most m).
   const int64_t per_prefix = s.dedup ? (s.n3 + s.slice_rows - 1) / s.slice_rows : m;
-  int64_t nsl_max = s.ndense * per_prefix;
+  const int64_t groups_max = s.ndense < m ? s.ndense : m;
+  int64_t nsl_max = m / s.slice_rows + groups_max + 1;
+  if (s.dedup && s.ndense * per_prefix < nsl_max) nsl_max = s.ndense * per_prefix;
   if (nsl_max > m) nsl_max = m;
+  // chunks: ceil(slices of run / CHUNK_SLICES) per non-empty (t, i2) run
   int64_t nch_max = nsl_max / CHUNK_SLICES + (int64_t)s.T * s.n2 + 1;
   if (nch_max > nsl_max) nch_max = nsl_max;
   W->nsl_max = nsl_max;
@@ -79,38 +87,27 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
   W->run_nch = (uint32_t*)take(4 * ((int64_t)s.T * s.n2 + 1));
   W->chunks = (int4*)take(16 * nch_max);
   W->E = (float*)take(4 * (size_t)m * s.D);
-  W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
-  const bool bwd_r32 = bwd_r32_supported(s, m);
-  W->dApart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nsl_max * s.d1 * s.R : 0);
-  W->dBpart = (float*)take(bwd_r32 ? 4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2) : 0);
-  W->g3part = (float*)take(bwd_r32 ? 4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2) : 0);
-  const size_t ncore = (size_t)s.T * ((size_t)s.n1 * s.d1 * s.R + (size_t)s.n2 * s.R * s.d2 * s.R +
-                                      (size_t)s.n3 * s.R * s.d3);
-  W->gscratch = (float*)take(bwd_r32 ? 0 : 4 * ncore);
-  if (bwd_r32) W->gscratch = nullptr;
-  // merged first core (L >= 4) or identity middle core (L = 2), and its gradient
+  // merged first core (L >= 4) or identity middle core (L = 2)
   const size_t nmerged = s.L >= 4 ? (size_t)s.T * s.n1 * s.d1 * s.R : (s.L == 2 ? (size_t)s.T * s.R * s.R : 0);
-  W->g1m = (float*)take(4 * nmerged);
-  W->dg1m = (float*)take(4 * nmerged);
-  if (!nmerged) {
-    W->g1m = nullptr;
-    W->dg1m = nullptr;
-  }
+  W->g1m = nmerged ? (float*)take(4 * nmerged) : nullptr;
   const size_t nlev = (size_t)chain_level_floats(s);
-  W->xlev = (float*)take(4 * nlev);
-  W->dxlev = (float*)take(4 * nlev);
-  if (!nlev) {
-    W->xlev = nullptr;
-    W->dxlev = nullptr;
-  }
+  W->xlev = nlev ? (float*)take(4 * nlev) : nullptr;
+  const bool bwd_r32 = bwd_r32_supported(s, m);
   const bool generic = !bwd_r32 || !fwd_r32_supported(s, m);
   const size_t nC = (size_t)s.d1 * s.d2 * s.R;
-  W->ckpt = (float*)take(generic ? 4 * CKPT_SLOTS * nC : 0);
-  W->ckpt_tag = (int32_t*)take(generic ? 4 * CKPT_SLOTS : 0);
-  if (!generic) {
-    W->ckpt = nullptr;
-    W->ckpt_tag = nullptr;
-  }
+  W->ckpt = generic ? (float*)take(4 * CKPT_SLOTS * nC) : nullptr;
+  W->ckpt_tag = generic ? (int32_t*)take(4 * CKPT_SLOTS) : nullptr;
+  if (fwd_end) *fwd_end = off;
+  // --- regions of the backward only ---
+  W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
+  W->dApart = bwd_r32 ? (float*)take(4 * (size_t)2 * nsl_max * s.d1 * s.R) : nullptr;
+  W->dBpart = bwd_r32 ? (float*)take(4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2)) : nullptr;
+  W->g3part = bwd_r32 ? (float*)take(4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2)) : nullptr;
+  const size_t ncore = (size_t)s.T * ((size_t)s.n1 * s.d1 * s.R + (size_t)s.n2 * s.R * s.d2 * s.R +
+                                      (size_t)s.n3 * s.R * s.d3);
+  W->gscratch = bwd_r32 ? nullptr : (float*)take(4 * ncore);
+  W->dg1m = nmerged ? (float*)take(4 * nmerged) : nullptr;
+  W->dxlev = nlev ? (float*)take(4 * nlev) : nullptr;
   const int par = sort_passes(s.key_bits) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];
@@ -120,6 +117,12 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w) 
 }
 
 size_t workspace_bytes(const Shape& s, int64_t M, int64_t B) { return layout(s, M, B, nullptr, nullptr); }
+
+size_t forward_workspace_bytes(const Shape& s, int64_t M, int64_t B) {
+  size_t fwd = 0;
+  layout(s, M, B, nullptr, nullptr, &fwd);
+  return fwd;
+}
 
 void carve(const Shape& s, int64_t M, int64_t B, void* base, Work* w) { layout(s, M, B, (char*)base, w); }
 
@@ -284,7 +287,7 @@ tt_emb_status tt_emb_kernel_uses_mfma(tt_emb_handle h, int kernel, int64_t num_i
   if (num_indices < 0 || num_indices > h->desc.max_indices) return TT_EMB_EINVAL;
   bool m = false;
   if (kernel == TT_EMB_K_FWD_FUSED) m = fwd_r32_supported(h->s, num_indices) || fwd_r64_supported(h->s, num_indices);
-  if (kernel == TT_EMB_K_BWD_FUSED) m = bwd_r32_supported(h->s, h->desc.max_indices);
+  if (kernel == TT_EMB_K_BWD_FUSED) m = bwd_r32_supported(h->s, num_indices);
   *uses_mfma = m ? 1 : 0;
   return TT_EMB_OK;
 }
@@ -308,21 +311,26 @@ tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode) {
   return TT_EMB_OK;
 }
 
-tt_emb_status tt_emb_workspace_size(tt_emb_handle h, size_t* bytes) {
+tt_emb_status tt_emb_workspace_size(tt_emb_handle h, int64_t num_indices, int64_t num_bags, size_t* bytes) {
   if (!h || !bytes) return TT_EMB_EINVAL;
-  *bytes = workspace_bytes(h->s, h->desc.max_indices, h->desc.max_bags);
+  if (num_indices < 0 || num_bags < 0 || num_indices > h->desc.max_indices || num_bags > h->desc.max_bags)
+    return TT_EMB_EINVAL;
+  *bytes = workspace_bytes(h->s, num_indices, num_bags);
   return TT_EMB_OK;
 }
 
+// Host checks of a call's batch; `training` selects the workspace size of a
+// backward (every region) over that of a grouping or forward call.
 static tt_emb_status check_batch(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets, int64_t B,
-                                 const void* ws, size_t ws_bytes) {
+                                 const void* ws, size_t ws_bytes, bool training) {
   if (!h || !ws) return TT_EMB_EINVAL;
   if (M < 0 || B < 0 || M > h->desc.max_indices || B > h->desc.max_bags) return TT_EMB_EINVAL;
   if (M > 0 && !idx) return TT_EMB_EINVAL;
   if (!offsets && M != (int64_t)h->s.T * B) return TT_EMB_EINVAL;
   if (offsets && B == 0 && M != 0) return TT_EMB_EINVAL;
   if (!al(idx, 8) || !al(offsets, 8) || !al(ws, 256)) return TT_EMB_EINVAL;
-  if (ws_bytes < workspace_bytes(h->s, h->desc.max_indices, h->desc.max_bags)) return TT_EMB_EINVAL;
+  const size_t need = training ? workspace_bytes(h->s, M, B) : forward_workspace_bytes(h->s, M, B);
+  if (ws_bytes < need) return TT_EMB_EINVAL;
   return TT_EMB_OK;
 }
 
@@ -331,7 +339,7 @@ static tt_emb_status hip_status(hipError_t e) { return e == hipSuccess ? TT_EMB_
 static tt_emb_status do_group(tt_emb_handle h, const int64_t* idx, int64_t M, const int64_t* offsets, int64_t B,
                               void* ws, hipStream_t st) {
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, ws, &w);
+  carve(h->s, M, B, ws, &w);
   h->g_valid = false;
   hipError_t e = launch_group(h->s, w, idx, M, offsets, B, h->prof, st);
   if (e != hipSuccess) return TT_EMB_EHIP;
@@ -351,7 +359,7 @@ static bool grouping_matches(tt_emb_handle h, const int64_t* idx, int64_t M, con
 
 tt_emb_status tt_emb_group(tt_emb_handle h, const int64_t* indices, int64_t num_indices, const int64_t* offsets,
                            int64_t num_bags, void* workspace, size_t ws_bytes, void* stream) {
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, false);
   if (st != TT_EMB_OK) return st;
   return do_group(h, indices, num_indices, offsets, num_bags, workspace, (hipStream_t)stream);
 }
@@ -360,7 +368,7 @@ tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, 
                              const int64_t* indices, int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                              float* out, int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
   if (h && h->s.L != 3) return TT_EMB_EINVAL;
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, false);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || (!out && num_bags > 0)) return TT_EMB_EINVAL;
   if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(out, 16)) return TT_EMB_EINVAL;
@@ -372,7 +380,7 @@ tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, 
     if (st != TT_EMB_OK) return st;
   }
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, num_indices, num_bags, workspace, &w);
   return hip_status(launch_forward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, out, h->prof, s));
 }
 
@@ -381,7 +389,7 @@ tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2,
                               int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
                               int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
   if (h && h->s.L != 3) return TT_EMB_EINVAL;
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, true);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || !dG1 || !dG2 || !dG3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
   if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(grad_out, 16) || !al(dG1, 16) || !al(dG2, 16) ||
@@ -395,7 +403,7 @@ tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2,
     if (st != TT_EMB_OK) return st;
   }
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, num_indices, num_bags, workspace, &w);
   return hip_status(
       launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, dG1, dG2, dG3, 0.f, false,
                       h->prof, s));
@@ -406,7 +414,7 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
                                   const float* grad_out, float lr, int reuse_grouping, void* workspace,
                                   size_t ws_bytes, void* stream) {
   if (h && h->s.L != 3) return TT_EMB_EINVAL;
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, true);
   if (st != TT_EMB_OK) return st;
   if (!G1 || !G2 || !G3 || (!grad_out && num_bags > 0)) return TT_EMB_EINVAL;
   if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(grad_out, 16)) return TT_EMB_EINVAL;
@@ -418,7 +426,7 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
     if (st != TT_EMB_OK) return st;
   }
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, num_indices, num_bags, workspace, &w);
   return hip_status(launch_backward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, grad_out, G1, G2, G3, lr,
                                     true, h->prof, s));
 }
@@ -447,14 +455,14 @@ static tt_emb_status group_or_reuse(tt_emb_handle h, const int64_t* idx, int64_t
 tt_emb_status tt_emb_forward_n(tt_emb_handle h, const float* const* cores, const int64_t* indices,
                                int64_t num_indices, const int64_t* offsets, int64_t num_bags, float* out,
                                int reuse_grouping, void* workspace, size_t ws_bytes, void* stream) {
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, false);
   if (st != TT_EMB_OK) return st;
   if (!cores_ok(h, cores) || (!out && num_bags > 0) || !al(out, 16)) return TT_EMB_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   if ((st = group_or_reuse(h, indices, num_indices, offsets, num_bags, workspace, reuse_grouping, s)) != TT_EMB_OK)
     return st;
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, num_indices, num_bags, workspace, &w);
   const int L = h->s.L;
   const float *G1 = cores[0], *G2 = cores[1], *G3 = cores[L - 1];
   hipError_t e = hipSuccess;
@@ -474,7 +482,7 @@ tt_emb_status tt_emb_backward_n(tt_emb_handle h, const float* const* cores, cons
                                 int64_t num_indices, const int64_t* offsets, int64_t num_bags, const float* grad_out,
                                 float* const* grads, int reuse_grouping, void* workspace, size_t ws_bytes,
                                 void* stream) {
-  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes);
+  tt_emb_status st = check_batch(h, indices, num_indices, offsets, num_bags, workspace, ws_bytes, true);
   if (st != TT_EMB_OK) return st;
   if (!cores_ok(h, cores) || !cores_ok(h, (const float* const*)grads) || (!grad_out && num_bags > 0) ||
       !al(grad_out, 16))
@@ -483,7 +491,7 @@ tt_emb_status tt_emb_backward_n(tt_emb_handle h, const float* const* cores, cons
   if ((st = group_or_reuse(h, indices, num_indices, offsets, num_bags, workspace, reuse_grouping, s)) != TT_EMB_OK)
     return st;
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, num_indices, num_bags, workspace, &w);
   const int L = h->s.L;
   const float *G1 = cores[0], *G2 = cores[1], *G3 = cores[L - 1];
   float *dG1 = grads[0], *dG2 = grads[1], *dG3 = grads[L - 1];
@@ -520,7 +528,7 @@ tt_emb_status tt_emb_sgd_n(tt_emb_handle h, float* const* cores, const float* co
 tt_emb_status tt_emb_check_errors(tt_emb_handle h, void* workspace, void* stream) {
   if (!h || !workspace) return TT_EMB_EINVAL;
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, 0, 0, workspace, &w);  // the counters head every layout
   if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return TT_EMB_EHIP;
   int32_t err = 0;
   if (hipMemcpy(&err, w.ctr + C_ERR, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess) return TT_EMB_EHIP;
@@ -539,7 +547,7 @@ tt_emb_status tt_emb_debug_grouping(tt_emb_handle h, void* workspace, int64_t* u
   if (!h->g_valid || h->g_ws != workspace) return TT_EMB_EINVAL;
   hipStream_t st = (hipStream_t)stream;
   Work w;
-  carve(h->s, h->desc.max_indices, h->desc.max_bags, workspace, &w);
+  carve(h->s, h->g_M, h->g_B, workspace, &w);  // the layout of the grouped call
   if (hipStreamSynchronize(st) != hipSuccess) return TT_EMB_EHIP;
   int32_t c[8];
   if (hipMemcpy(c, w.ctr, sizeof(c), hipMemcpyDeviceToHost) != hipSuccess) return TT_EMB_EHIP;

@@ -34,12 +34,37 @@ def test_every_header_symbol_is_exported(N):
 
 def test_create_destroy_and_workspace(N):
     h = N.tt_emb_create(_desc(N))
-    ws = N.tt_emb_workspace_size(h)
+    ws = N.tt_emb_workspace_size(h, 100, 10)
     assert ws > 0 and ws % 256 == 0
     h2 = N.tt_emb_create(_desc(N, M=1000))
-    assert N.tt_emb_workspace_size(h2) > ws
+    assert N.tt_emb_workspace_size(h2, 1000, 10) > ws
+    # sized per call: the same handle needs less for a smaller call, and as much
+    # as a handle made for that size
+    assert N.tt_emb_workspace_size(h2, 100, 10) == ws
+    assert N.tt_emb_workspace_size(h2, 0, 0) < ws
+    n = C.c_size_t()
+    E = N.TT_EMB_EINVAL
+    assert N.lib.tt_emb_workspace_size(h2, 1001, 10, C.byref(n)) == E  # beyond max_indices
+    assert N.lib.tt_emb_workspace_size(h2, 10, 11, C.byref(n)) == E    # beyond max_bags
+    assert N.lib.tt_emb_workspace_size(h2, -1, 10, C.byref(n)) == E
+    assert N.lib.tt_emb_workspace_size(h2, 10, 10, None) == E
+    assert N.lib.tt_emb_workspace_size(None, 10, 10, C.byref(n)) == E
     N.tt_emb_destroy(h)
     N.tt_emb_destroy(h2)
+
+
+def test_workspace_of_the_training_workload(N):
+    # 8 tables of 200 x 200 x 250 rows, d = (4, 4, 8), R = 32, 5,246,700 indices in
+    # 32,768 bags per table: the bound on work slices (indices / 32 + prefix slots)
+    # keeps the workspace near its E rows (2.69 GB) instead of one slice per index
+    M, B = 5246700, 32768
+    h = N.tt_emb_create(_desc(N, T=8, n=(200, 200, 250), d=(4, 4, 8), R=32, M=M, B=B))
+    ws = N.tt_emb_workspace_size(h, M, B)
+    rows = 4 * M * 128
+    assert rows < ws < rows + 1.4e9, ws
+    # and per call: a quarter of the batch needs well under half of it
+    assert N.tt_emb_workspace_size(h, M // 4, B // 4) < ws / 2
+    N.tt_emb_destroy(h)
     assert N.lib.tt_emb_destroy(None) == N.TT_EMB_OK
     assert N.status_string(N.TT_EMB_ERANGE).startswith("index")
 
@@ -58,7 +83,8 @@ def test_create_rejects_bad_shapes(N, kw, code):
 
 def test_calls_reject_bad_arguments_without_launching(N):
     h = N.tt_emb_create(_desc(N, T=2, M=100, B=10))
-    ws_bytes = N.tt_emb_workspace_size(h)
+    ws_bytes = N.tt_emb_workspace_size(h, 100, 10)
+    ws_call = N.tt_emb_workspace_size(h, 20, 10)  # what a training call of 20 indices needs
     fake = 1 << 20  # aligned non-null addresses; nothing may be dereferenced
     off = fake
     E = N.TT_EMB_EINVAL
@@ -66,7 +92,7 @@ def test_calls_reject_bad_arguments_without_launching(N):
     # null handle, null workspace, small workspace
     assert f(None, fake, fake, fake, fake, 20, None, 10, fake, 0, fake, ws_bytes, None) == E
     assert f(h, fake, fake, fake, fake, 20, None, 10, fake, 0, None, ws_bytes, None) == E
-    assert f(h, fake, fake, fake, fake, 20, None, 10, fake, 0, fake, ws_bytes - 1, None) == E
+    assert f(h, fake, fake, fake, fake, 20, None, 10, fake, 0, fake, 256, None) == E
     # NULL offsets require num_indices == T*B
     assert f(h, fake, fake, fake, fake, 19, None, 10, fake, 0, fake, ws_bytes, None) == E
     # beyond capacities
@@ -92,7 +118,9 @@ def test_calls_reject_bad_arguments_without_launching(N):
     assert bs(h, fake, fake, fake + 4, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes, None) == E  # misaligned
     assert bs(h, fake, fake, fake, fake, 20, off, 10, None, lr, 0, fake, ws_bytes, None) == E  # null grad_out
     assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 1, fake, ws_bytes, None) == E  # no grouping yet
-    assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_bytes - 1, None) == E
+    assert bs(h, fake, fake, fake, fake, 20, off, 10, fake, lr, 0, fake, ws_call - 1, None) == E
+    assert b(h, fake, fake, fake, fake, 20, off, 10, fake, fake, fake, fake, 0, fake, ws_call - 1, None) == E
+    assert N.lib.tt_emb_group(h, fake, 20, off, 10, fake, 256, None) == E
     assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
     assert N.lib.tt_emb_set_schedule(h, 3) == E and N.lib.tt_emb_set_schedule(h, -1) == E
     assert N.lib.tt_emb_set_schedule(None, 0) == E
@@ -103,14 +131,14 @@ def test_calls_reject_bad_arguments_without_launching(N):
 
 def test_reuse_levels_and_workspace(N):
     h = N.tt_emb_create(_desc(N, T=2, M=1000, B=100))
-    base = N.tt_emb_workspace_size(h)
+    base = N.tt_emb_workspace_size(h, 1000, 100)
     assert N.lib.tt_emb_set_reuse(h, 3) == N.TT_EMB_EINVAL
     assert N.lib.tt_emb_set_reuse(h, -1) == N.TT_EMB_EINVAL
     assert N.lib.tt_emb_set_reuse(None, 0) == N.TT_EMB_EINVAL
     sizes = {}
     for name, level in N.REUSE.items():
         N.tt_emb_set_reuse(h, level)
-        sizes[name] = N.tt_emb_workspace_size(h)
+        sizes[name] = N.tt_emb_workspace_size(h, 1000, 100)
     assert sizes["prefix"] == base
     # one slice per row (and per occurrence without dedup) needs more room
     assert sizes["unique"] >= base and sizes["none"] >= sizes["unique"]
@@ -125,7 +153,11 @@ def test_reuse_levels_and_workspace(N):
     ((6, 5, 252), (4, 4, 8), 32, 1000, 1000, 1, 1),             # the backward's LDS accumulator fills
     ((6, 5, 253), (4, 4, 8), 32, 1000, 1000, 1, 0),             # one row past it
     ((10, 10, 10), (4, 4, 8), 32, 1 << 24, 1 << 24, 0, 0),      # E offsets would pass 2^31
-    ((10, 10, 10), (4, 4, 8), 32, 1 << 24, 1000, 1, 0),         # small call: the forward decides per call
+    ((10, 10, 10), (4, 4, 8), 32, 1 << 24, 1000, 1, 1),         # small call: both decide per call
+    # 32-bit G2 offsets (T n2 4096 floats) or G1 offsets (T n1 128 floats) would pass 2^31: generic kernels
+    ((1, 300000, 2), (4, 4, 8), 32, 1000, 1000, 0, 0),
+    ((9000000, 1, 2), (4, 4, 8), 32, 1000, 1000, 0, 0),
+    ((1, 70000, 2), (4, 4, 8), 64, 1000, 1000, 0, 0),
 ])
 def test_kernel_uses_mfma(N, n, d, R, M, num, fwd, bwd):
     h = N.tt_emb_create(_desc(N, T=2, n=n, d=d, R=R, M=M, B=10))
@@ -160,15 +192,15 @@ def test_create_n_shapes_and_workspace(N):
     # L = 3 through create_n is the three-core handle
     h3 = N.tt_emb_create(_desc(N))
     h3n = N.tt_emb_create_n(_desc_n(N, L=3, n=(3, 4, 5), d=(2, 2, 2)))
-    assert N.tt_emb_workspace_size(h3) == N.tt_emb_workspace_size(h3n)
+    assert N.tt_emb_workspace_size(h3, 100, 10) == N.tt_emb_workspace_size(h3n, 100, 10)
     # L = 4 and L = 2 need room for the merged / identity core and its gradient
     h4 = N.tt_emb_create_n(_desc_n(N))
     h2 = N.tt_emb_create_n(_desc_n(N, L=2, n=(12, 10), d=(4, 2)))
-    assert N.tt_emb_workspace_size(h4) > 0 and N.tt_emb_workspace_size(h2) > 0
+    assert N.tt_emb_workspace_size(h4, 100, 10) > 0 and N.tt_emb_workspace_size(h2, 100, 10) > 0
     h8 = N.tt_emb_create_n(_desc_n(N, L=8, n=(2,) * 8, d=(1, 2, 1, 2, 1, 2, 1, 2)))
     # wide merged cores are served too (their chain runs level by level in the workspace)
     h5 = N.tt_emb_create_n(_desc_n(N, L=5, n=(2, 2, 2, 2, 2), d=(8, 8, 2, 1, 1), R=64))
-    assert N.tt_emb_workspace_size(h5) > N.tt_emb_workspace_size(h8)
+    assert N.tt_emb_workspace_size(h5, 100, 10) > N.tt_emb_workspace_size(h8, 100, 10)
     for h in (h3, h3n, h4, h2, h8, h5):
         N.tt_emb_destroy(h)
 
@@ -202,7 +234,7 @@ def test_create_n_rejects_bad_shapes(N, kw, code):
 
 def test_calls_n_reject_bad_arguments_without_launching(N):
     h = N.tt_emb_create_n(_desc_n(N, T=2, M=100, B=10))
-    ws_bytes = N.tt_emb_workspace_size(h)
+    ws_bytes = N.tt_emb_workspace_size(h, 100, 10)
     fake = 1 << 20
     off = fake
     E = N.TT_EMB_EINVAL
@@ -214,12 +246,13 @@ def test_calls_n_reject_bad_arguments_without_launching(N):
     assert f(h, short, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
     assert f(h, mis, fake, 20, off, 10, fake, 0, fake, ws_bytes, None) == E
     assert f(h, cores, fake, 20, off, 10, None, 0, fake, ws_bytes, None) == E
-    assert f(h, cores, fake, 20, off, 10, fake, 0, fake, ws_bytes - 1, None) == E
+    assert f(h, cores, fake, 20, off, 10, fake, 0, fake, 256, None) == E
     assert f(h, cores, fake, 20, off, 10, fake, 1, fake, ws_bytes, None) == E  # no grouping yet
     b = N.lib.tt_emb_backward_n
     assert b(h, cores, fake, 20, off, 10, fake, None, 0, fake, ws_bytes, None) == E
     assert b(h, cores, fake, 20, off, 10, fake, short, 0, fake, ws_bytes, None) == E
     assert b(h, cores, fake, 20, off, 10, None, cores, 0, fake, ws_bytes, None) == E
+    assert b(h, cores, fake, 20, off, 10, fake, cores, 0, fake, N.tt_emb_workspace_size(h, 20, 10) - 1, None) == E
     assert N.lib.tt_emb_sgd_n(h, cores, mis, C.c_float(0.1), None) == E
     assert N.lib.tt_emb_sgd_n(None, cores, cores, C.c_float(0.1), None) == E
     # the three-core calls refuse a handle with four cores

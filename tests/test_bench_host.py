@@ -17,7 +17,7 @@ import bench  # noqa: E402
 
 def _args(**kw):
     a = dict(config=5, cores=3, row_factors=None, dim_factors=None, reuse="prefix", sched="steal",
-             unfused_sgd=False)
+             unfused_sgd=False, mode=None, bags=None)
     a.update(kw)
     return argparse.Namespace(**a)
 
@@ -65,3 +65,54 @@ def test_algorithmic_work_of_the_fused_kernels():
     big = dict(case, T=8)
     w, _, _ = bench.algorithmic_work("bwd_fused", big, {"U": 1089937, "P": 309642, "nvalid": 5246700})
     assert abs(w / 1e9 - 48.3) < 0.1
+
+
+def test_run_key_and_step_of_the_forward_only_workloads():
+    # configs 1-4 time the forward (grouping, fused forward, pooling) unless told otherwise
+    assert bench.step_mode(_args(config=4)) == "forward"
+    assert bench.step_mode(_args(config=5)) == "train"
+    assert bench.step_mode(_args(config=4, mode="train")) == "train"
+    k4 = bench.run_key(_args(config=4))
+    assert k4["mode"] == "forward" and "mode" not in bench.run_key(_args())
+    assert bench.run_key(_args(config=4, mode="train")) != k4
+    assert bench.run_key(_args(bags=4096))["workload"].endswith("_bags4096")
+    # the forward's MFMA kernel at rank 64 is its own symbol
+    assert bench.kernel_symbol("fwd_fused", 64) == "k_fwd_r64"
+    assert bench.kernel_symbol("fwd_fused", 32) == "k_fwd_r32"
+    assert bench.kernel_symbol("bwd_fused", 32) == "k_bwd_r32"
+
+
+def _case8():
+    n, d, R, T, B = (200, 200, 250), (4, 4, 8), 32, 8, 32768
+    return {"T": T, "B": B, "R": R, "n": n, "d": d, "idx": np.zeros(5246700, np.int64),
+            "G1": np.zeros((T, n[0], d[0], R), np.float32), "G2": np.zeros((T, n[1], R, d[1], R), np.float32),
+            "G3": np.zeros((T, n[2], R, d[2]), np.float32)}
+
+
+def test_step_work_of_the_training_workload():
+    # the whole call's algorithmic flops and bytes at the training workload's grouping
+    case = _case8()
+    counts = {"U": 1089937, "P": 309642, "nvalid": 5246700}
+    M, NB, D = 5246700, 8 * 32768, 128
+    ncore = 8 * (200 * 4 * 32 + 200 * 32 * 4 * 32 + 250 * 32 * 8)
+    Ff, Qf = bench.step_work(case, counts, "forward")
+    assert Ff == 309642 * 2 * 16 * 32 * 32 + 1089937 * 2 * 128 * 32 + M * D
+    assert Qf == 8 * M + 8 * (NB + 1) + 4 * NB * D + 4 * ncore
+    Ft, Qt = bench.step_work(case, counts, "train")
+    assert Ft - Ff == M * D + 1089937 * 4 * 128 * 32 + 309642 * 6 * 16 * 32 * 32 + 2 * ncore
+    assert Qt - Qf == 4 * NB * D + 16 * ncore
+    # about 19.8 + 49 GFLOP: compute-bound, about 0.44 ms of FP32 peak
+    assert 68e9 < Ft < 70e9
+    w = bench.whole_call(case, counts, "train", 2.0)
+    assert w["bound"] == "fp32" and abs(w["roof_ms"] - Ft / 157.3e12 * 1e3) < 1e-4
+    assert abs(w["frac"] - (Ft / 157.3e12) / 2.0e-3) < 1e-4
+    # a latency-scale forward of 4,096 single lookups is bound by its bytes
+    small = {"T": 1, "B": 4096, "R": 8, "n": (100, 100, 100), "d": (2, 2, 4), "idx": np.zeros(4096, np.int64),
+             "G1": np.zeros((1, 100, 2, 8)), "G2": np.zeros((1, 100, 8, 2, 8)), "G3": np.zeros((1, 100, 8, 4))}
+    ws = bench.whole_call(small, {"U": 4090, "P": 3356, "nvalid": 4096}, "forward", 0.1)
+    assert ws["bound"] == "hbm"
+
+
+def test_cpu_model_is_named():
+    name, n = bench.cpu_model()
+    assert isinstance(name, str) and name and n >= 1

@@ -203,6 +203,68 @@ def test_full_size_four_cores(lib, orc):
         rhs = float((grads[k].double() * dcores[k].double()).sum())
         scale = float((grads[k].double().abs() * dcores[k].double().abs()).sum())
         assert abs(lhs - rhs) <= TOL * scale, (k, lhs, rhs, scale)
+    # and element by element on sampled slices of every core: the most-used slice of
+    # each core in the first and last table, and a random one in the first table
+    want = _sampled_slices_n(case, (0, T - 1), seed=7502)
+    _say(f"[cores full] L=4 gradients on {[int(w.sum()) for w in want]} slices per core")
+    ref = _oracle_backward_n_by_table(orc, case, want)
+    mag = _oracle_backward_n_by_table(orc, _abs_n(case), want)
+    for k in range(4):
+        sel = np.flatnonzero(want[k])
+        g = grads[k].cpu().numpy()
+        assert_close(f"full L=4 dG{k + 1} (sampled slices)", g.reshape(T * n[k], -1)[sel],
+                      ref[k].reshape(T * n[k], -1)[sel], mag[k].reshape(T * n[k], -1)[sel])
+
+
+def _part_case_n(case, t, b0, b1):
+    """Bags [b0, b1) of table t of an L-core case as a one-table case of its own."""
+    B = case["B"]
+    off = case["offsets"]
+    lo, hi = int(off[t * B + b0]), int(off[t * B + b1])
+    return dict(case, T=1, B=b1 - b0, idx=case["idx"][lo:hi], offsets=off[t * B + b0:t * B + b1 + 1] - lo,
+                cores=[G[t:t + 1] for G in case["cores"]], dV=case["dV"][t:t + 1, b0:b1])
+
+
+def _oracle_backward_n_by_table(orc, case, want, splits=4):
+    """orc.backward_n with slice masks on a thread pool: each table with a wanted slice
+    (tables are independent) in `splits` bag ranges, each a case of its own; the
+    ranges' gradients are added in double and stacked over tables."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    T, n, L, B = case["T"], case["n"], len(case["n"]), case["B"]
+    jobs = []
+    for t in range(T):
+        w = [m[t * n[k]:(t + 1) * n[k]] for k, m in enumerate(want)]
+        if any(x.any() for x in w):
+            cuts = [B * j // splits for j in range(splits + 1)]
+            jobs += [(t, cuts[j], cuts[j + 1], w) for j in range(splits) if cuts[j + 1] > cuts[j]]
+
+    def one(job):
+        t, b0, b1, w = job
+        return t, orc.backward_n(_part_case_n(case, t, b0, b1), want=w)[0]
+
+    out = [np.zeros(G.shape) for G in case["cores"]]
+    with ThreadPoolExecutor(8) as ex:
+        for t, g in ex.map(one, jobs):
+            for k in range(L):
+                out[k][t] += g[k][0]
+    return out
+
+
+def _sampled_slices_n(case, tables, seed):
+    T, n, B = case["T"], case["n"], case["B"]
+    bag = np.repeat(np.arange(T * B), np.diff(case["offsets"]))
+    tab = bag // B
+    dig = np.stack(np.unravel_index(case["idx"], n), 1)
+    rng = np.random.default_rng(seed)
+    want = [np.zeros(T * nk, np.uint8) for nk in n]
+    for t in tables:
+        sel = tab == t
+        for k in range(len(n)):
+            want[k][t * n[k] + np.bincount(dig[sel, k], minlength=n[k]).argmax()] = 1
+    for k in range(len(n)):
+        want[k][tables[0] * n[k] + int(rng.integers(0, n[k]))] = 1
+    return want
 
 
 def test_autograd_module_n(lib, orc):

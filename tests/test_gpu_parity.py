@@ -266,8 +266,8 @@ def test_forward_deterministic(lib):
 # ---------------------------------------------------------------------------
 # edge cases
 # ---------------------------------------------------------------------------
-def _edge(kind):
-    case = ttgen.tiny(77, 2, (6, 5, 100), (2, 2, 2), 4, B=40, max_len=8, zipf=1.1)
+def _edge(kind, d=(2, 2, 2), R=4):
+    case = ttgen.tiny(77, 2, (6, 5, 100), d, R, B=40, max_len=8, zipf=1.1)
     idx = case["idx"].copy()
     rng = np.random.default_rng(5)
     n3 = 100
@@ -282,9 +282,107 @@ def _edge(kind):
     return case
 
 
+EDGE_SHAPES = [((2, 2, 2), 4), ((4, 4, 8), 32), ((4, 4, 8), 64)]
+
+
+@pytest.mark.parametrize("dR", EDGE_SHAPES, ids=["generic", "mfma_r32", "mfma_r64"])
 @pytest.mark.parametrize("kind", ["all_equal", "one_prefix", "distinct_prefixes"])
-def test_edge_index_patterns(lib, orc, kind):
-    check_forward(lib, orc, _edge(kind), name=kind)
+def test_edge_index_patterns(lib, orc, kind, dR):
+    # each pattern through the forward, the backward and the fused backward-and-SGD,
+    # on the generic kernels and on the MFMA shapes (R = 32: both fused kernels on
+    # the matrix cores; R = 64: the matrix-core forward)
+    case = _edge(kind, *dR)
+    name = f"{kind} d={dR[0]} R={dR[1]}"
+    check_forward(lib, orc, case, name=name)
+    check_backward(lib, orc, case, name=name)
+    _say(f"[bwd+sgd] {name}")
+    emb = _make(lib, case)
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.backward_sgd(*G, idx, off, dV, 0.01, num_bags=case["B"], reuse_grouping=False)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    _check_sgd(orc, case, G, 0.01, name)
+
+
+def _run_slices(g, n):
+    """Work slices (at most 32 rows each) of every prefix group from a debug grouping, in
+    the fused kernels' (table, i2, i1) order, with each group's first slice within its
+    (table, i2) run: returns (rows, slices, first, run) per group."""
+    n1, n2 = n[0], n[1]
+    keys = np.asarray(g["pg_keys"], np.int64)
+    rows = np.diff(np.asarray(g["pg_start"], np.int64))
+    t, q = keys // (n1 * n2), keys % (n1 * n2)
+    i1, i2 = q // n2, q % n2
+    order = np.lexsort((i1, i2, t))
+    sl = (rows + 31) // 32
+    run = (t * n2 + i2)[order]
+    first = np.zeros(len(order), np.int64)
+    acc, prev = 0, -1
+    for j, p in enumerate(order):
+        if run[j] != prev:
+            acc, prev = 0, run[j]
+        first[j] = acc
+        acc += sl[p]
+    return rows[order], sl[order], first, run
+
+
+def _hot_prefix_case(seed, T, n, B, hot, per_bag=20):
+    """Bags whose indices fall in the listed hot prefixes (i1, i2) with uniform i3 most
+    of the time, else anywhere: long prefix groups of many work slices."""
+    case = ttgen.tiny(seed, T, n, (4, 4, 8), 32, B=B, max_len=per_bag, zipf=1.1, empty_bags=False)
+    rng = np.random.default_rng(seed)
+    idx = case["idx"].copy()
+    pick = rng.random(idx.size) < 0.85
+    h = np.asarray(hot)[rng.integers(0, len(hot), idx.size)]
+    idx[pick] = ((h[pick, 0] * n[1] + h[pick, 1]) * n[2] + rng.integers(0, n[2], int(pick.sum())))
+    case["idx"] = idx.astype(np.int64)
+    return case
+
+
+def test_forward_prefix_group_longer_than_a_chunk(lib, orc):
+    # one (i1, i2) prefix with about 2,000 distinct suffixes: its group is cut into more
+    # work slices than a chunk holds (32 x 32 rows), so the MFMA forward meets the same
+    # group in consecutive chunks and quads
+    n = (3, 2, 2000)
+    case = _hot_prefix_case(7101, 1, n, B=300, hot=[(1, 1), (2, 0)], per_bag=24)
+    emb = _make(lib, case)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["fwd_fused"], case["idx"].size)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    g = emb.debug_grouping(case["idx"].size)
+    rows, sl, first, run = _run_slices(g, n)
+    assert sl.max() > 32, sl.max()
+    check_forward(lib, orc, case, name="group of > 32 slices")
+    check_backward(lib, orc, case, name="group of > 32 slices (generic backward)")
+
+
+def test_backward_prefix_groups_across_chunk_ends(lib, orc):
+    # twelve prefixes of one (table, i2) run, each with nearly all 250 suffixes: groups
+    # of 7-8 work slices, so the run's slices fill several chunks and groups straddle
+    # their ends, on both fused MFMA kernels (forward, backward, fused update)
+    n = (12, 2, 250)
+    hot = [(i1, 0) for i1 in range(12)]
+    case = _hot_prefix_case(7102, 2, n, B=400, hot=hot, per_bag=20)
+    emb = _make(lib, case)
+    M = case["idx"].size
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["fwd_fused"], M)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    g = emb.debug_grouping(M)
+    rows, sl, first, run = _run_slices(g, n)
+    straddle = (first // 32) != ((first + sl - 1) // 32)
+    assert rows.max() > 200 and straddle.sum() >= 2, (rows.max(), straddle.sum())
+    check_forward(lib, orc, case, name="groups across chunk ends")
+    check_backward(lib, orc, case, name="groups across chunk ends")
+    _say("[bwd+sgd] groups across chunk ends")
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.backward_sgd(*G, idx, off, dV, 0.01, num_bags=case["B"], reuse_grouping=False)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    _check_sgd(orc, case, G, 0.01, "groups across chunk ends")
 
 
 def test_edge_empty_and_single_bag(lib, orc):
@@ -425,17 +523,99 @@ def test_backward_config5_small_batch(lib, orc):
     check_backward(lib, orc, ttgen.make(5, bags=64), name="config5 B=64")
 
 
-def test_backward_config5_full_sampled_slices(lib, orc):
-    case = ttgen.make(5)
+def _table_case(case, t):
+    """Table t of a case as a one-table case of its own."""
+    B = case["B"]
+    off = case["offsets"]
+    lo, hi = int(off[t * B]), int(off[(t + 1) * B])
+    one = dict(case, T=1, idx=case["idx"][lo:hi], offsets=off[t * B:(t + 1) * B + 1] - lo)
+    for k in ("G1", "G2", "G3"):
+        one[k] = case[k][t:t + 1]
+    if "dV" in case:
+        one["dV"] = case["dV"][t:t + 1]
+    return one
+
+
+def _oracle_backward_by_table(orc, case, want):
+    """orc.backward with slice masks, each table (independent of the others) as a case
+    of its own on a thread pool; returns the three gradients stacked over tables."""
+    from concurrent.futures import ThreadPoolExecutor
+
     T, n = case["T"], case["n"]
-    rng = np.random.default_rng(17)
-    want = []
+
+    def one(t):
+        w = [m[t * n[k]:(t + 1) * n[k]] for k, m in enumerate(want)]
+        if not any(x.any() for x in w):
+            return None
+        return orc.backward(_table_case(case, t), want=w)[:3]
+
+    with ThreadPoolExecutor(min(T, 8)) as ex:
+        parts = list(ex.map(one, range(T)))
+    out = []
     for k in range(3):
-        m = np.zeros(T * n[k], np.uint8)
-        for t in (0, T - 1):
-            m[t * n[k] + rng.integers(0, n[k])] = 1
-        want.append(m)
-    check_backward(lib, orc, case, name="config5 full", want=want)
+        shape = (1,) + tuple(case[("G1", "G2", "G3")[k]].shape[1:])
+        out.append(np.concatenate([np.zeros(shape) if p is None else p[k] for p in parts]))
+    return out
+
+
+def _hottest_slices(case, extra_tables=(0,), extra=2, seed=17):
+    """Per core, the slice with the most occurrences in every table (the longest fp32
+    sums of the gradient), plus `extra` random slices in the listed tables."""
+    T, n, B = case["T"], case["n"], case["B"]
+    bag = np.repeat(np.arange(T * B), np.diff(case["offsets"]))
+    tab = bag // B
+    dig = np.stack(np.unravel_index(case["idx"], n), 1)
+    rng = np.random.default_rng(seed)
+    want = [np.zeros(T * nk, np.uint8) for nk in n]
+    for t in range(T):
+        sel = tab == t
+        for k in range(3):
+            want[k][t * n[k] + np.bincount(dig[sel, k], minlength=n[k]).argmax()] = 1
+            if t in extra_tables:
+                want[k][t * n[k] + rng.choice(n[k], extra, replace=False)] = 1
+    return want
+
+
+def _sel(a, T, want_k):
+    return a.reshape(T * a.shape[1], -1)[np.flatnonzero(want_k)]
+
+
+def test_backward_config5_full_hottest_slices(lib, orc):
+    # The training workload at full size, in the launch sequence the benchmark
+    # times (forward with grouping, then the backward reusing it): every table's
+    # most-used slice of each core (about 80k occurrences summed into one dG3
+    # slice) plus random slices, element by element against the oracle; then the
+    # fused backward-and-SGD call on the same grouping, the call the benchmark times.
+    case = ttgen.make(5)
+    T, B, lr = case["T"], case["B"], case["lr"]
+    M = int(case["idx"].size)
+    want = _hottest_slices(case, extra_tables=(0, T - 1))
+    _say(f"[bwd] config5 full, hottest + random slices ({sum(int(w.sum()) for w in want)} slices)")
+    emb = _make(lib, case)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.forward(*G, idx, off, num_bags=B)
+    grads = emb.backward(*G, idx, off, dV, num_bags=B, reuse_grouping=True)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    ref = _oracle_backward_by_table(orc, case, want)
+    mag = _oracle_backward_by_table(orc, abs_case(case), want)
+    for k in range(3):
+        g = grads[k].cpu().numpy()
+        assert_close(f"dG{k + 1} config5 full (hottest slices)", _sel(g, T, want[k]), _sel(ref[k], T, want[k]),
+                     _sel(mag[k], T, want[k]))
+    del grads
+    _say("[bwd+sgd] config5 full, same slices")
+    emb.backward_sgd(*G, idx, off, dV, lr, num_bags=B, reuse_grouping=True)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    for k, cname in enumerate(("G1", "G2", "G3")):
+        new = _sel(G[k].cpu().numpy().astype(np.float64), T, want[k])
+        exp = _sel(orc.sgd(case[cname], ref[k], lr), T, want[k])
+        # gradient error scaled by lr plus one fp32 rounding of the updated value
+        bound = TOL * lr * _sel(mag[k], T, want[k]) + 2.0 ** -23 * np.abs(exp)
+        assert np.all(np.abs(new - exp) <= bound + 1e-30), cname
 
 
 def test_sgd_step(lib, orc):

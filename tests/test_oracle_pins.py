@@ -292,3 +292,85 @@ def test_grouping_single_index_bags(orc):
     ref = _numpy_grouping(case)
     for key in ref:
         assert np.array_equal(got[key], ref[key]), key
+
+
+# ---------------------------------------------------------------------------
+# The oracle's subset options, which the full-size GPU checks rely on: a bag
+# list computes exactly those bags of the full forward, and slice masks keep
+# every occurrence that adds to a wanted slice (in the same order), so the
+# wanted slices' gradients are those of the full backward, bit for bit.
+# ---------------------------------------------------------------------------
+def _dup_invalid_case(seed, T=3, n=(4, 3, 5), d=(2, 1, 3), R=3, B=9):
+    case = ttgen.tiny(seed, T, n, d, R, B=B, max_len=6, N=n[0] * n[1] * n[2] - 3)
+    idx = case["idx"].copy()
+    idx[::7] = idx[0]             # repeated rows inside and across bags
+    idx[3::11] = case["N"] + 1    # padding rows: invalid
+    idx[5::13] = -1
+    case["idx"] = idx
+    return case
+
+
+@pytest.mark.parametrize("seed", [61, 62])
+def test_forward_bag_subset_is_the_full_forward_on_those_bags(orc, seed):
+    case = _dup_invalid_case(seed)
+    V, inv_all = orc.forward(case)
+    nb = case["T"] * case["B"]
+    rng = np.random.default_rng(seed)
+    bags = np.concatenate([rng.choice(nb, 7, replace=False), [nb - 1, 0, 3, 3]])  # unsorted, repeated
+    Vs, _ = orc.forward(case, bags=bags)
+    assert np.array_equal(Vs, V[bags])
+    assert inv_all > 0
+
+
+def _masks(rng, T, n, count):
+    out = []
+    for nk in n:
+        m = np.zeros(T * nk, np.uint8)
+        m[rng.choice(T * nk, min(count, T * nk), replace=False)] = 1
+        out.append(m)
+    return out
+
+
+@pytest.mark.parametrize("seed", [71, 72, 73])
+def test_backward_slice_masks_keep_the_wanted_slices_exact(orc, seed):
+    case = _dup_invalid_case(seed)
+    T, n = case["T"], case["n"]
+    full = orc.backward(case)
+    rng = np.random.default_rng(seed)
+    want = _masks(rng, T, n, 2)
+    if seed == 73:
+        want[1] = None  # a core with no mask: only the others select
+    part = orc.backward(case, want=want)
+    assert part[3] == full[3]
+    for k in range(3):
+        if want[k] is None:
+            continue
+        sel = np.flatnonzero(want[k])
+        g = part[k].reshape(T * n[k], -1)[sel]
+        r = full[k].reshape(T * n[k], -1)[sel]
+        assert np.array_equal(g, r), k
+    # occurrences touching no wanted slice were skipped: some unwanted slice differs
+    diffs = [np.any(part[k] != full[k]) for k in range(3)]
+    assert any(diffs)
+
+
+@pytest.mark.parametrize("seed,L", [(81, 4), (82, 5), (83, 2)])
+def test_backward_n_slice_masks_keep_the_wanted_slices_exact(orc, seed, L):
+    n = {2: (6, 5), 4: (3, 2, 4, 3), 5: (2, 3, 2, 2, 3)}[L]
+    d = {2: (2, 3), 4: (2, 1, 2, 2), 5: (1, 2, 1, 2, 2)}[L]
+    case = ttgen.tiny_n(seed, 2, n, d, 3, 11, max_len=6)
+    full, _ = orc.backward_n(case)
+    rng = np.random.default_rng(seed)
+    T = case["T"]
+    want = _masks(rng, T, n, 1)
+    part, _ = orc.backward_n(case, want=want)
+    for k in range(L):
+        sel = np.flatnonzero(want[k])
+        g = part[k].reshape(T * n[k], -1)[sel]
+        r = full[k].reshape(T * n[k], -1)[sel]
+        assert np.array_equal(g, r), k
+    # a list of no masks selects nothing away: the full backward
+    none, _ = orc.backward_n(case, want=[None] * L)
+    assert all(np.array_equal(none[k], full[k]) for k in range(L))
+    with pytest.raises(ValueError):
+        orc.backward_n(case, want=want[:-1])
