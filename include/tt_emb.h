@@ -62,7 +62,8 @@ typedef enum {
   TT_EMB_ENOMEM = 2,      /* host allocation of the handle failed */
   TT_EMB_EHIP = 3,        /* a HIP runtime call or kernel launch failed */
   TT_EMB_ERANGE = 4,      /* device saw an index outside [0, N) or malformed offsets */
-  TT_EMB_EUNSUPPORTED = 5 /* shape beyond this library's limits (see tt_emb_create) */
+  TT_EMB_EUNSUPPORTED = 5, /* shape beyond this library's limits (see tt_emb_create) */
+  TT_EMB_ESCRATCH = 6      /* call larger than the static scratch of tt_emb_forward_noalloc */
 } tt_emb_status;
 
 /* Shape of the tables served by one handle.  Every table of a call has the
@@ -158,6 +159,27 @@ tt_emb_status tt_emb_group(tt_emb_handle h, const int64_t* indices, int64_t num_
 tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
                              const int64_t* indices, int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                              float* out, int reuse_grouping, void* workspace, size_t ws_bytes, void* stream);
+
+/* Forward pass that allocates nothing and takes no workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  It computes what tt_emb_forward
+ * with reuse_grouping = 0 computes, with the same kernels, on a workspace held
+ * in a static device array of TT_EMB_NOALLOC_SCRATCH_BYTES bytes that each GPU
+ * the library runs on keeps until the process ends.  Returns TT_EMB_ESCRATCH,
+ * launching nothing, when the call's forward workspace would exceed it (at
+ * D = 128 about 100,000 indices fit, less with many prefix slots T*n1*n2).
+ * Every call on one GPU shares that GPU's array and leaves its grouping there:
+ * calls that overlap on one GPU (other streams or host threads) race and give
+ * wrong results; calls in stream order do not.  The grouping it makes is not
+ * available to tt_emb_backward (nothing of the caller's workspace is touched).
+ * `stream` must belong to the current device (TT_EMB_EINVAL otherwise); at most
+ * TT_EMB_NOALLOC_MAX_DEVICES devices.  Other arguments and errors as for
+ * tt_emb_forward. */
+#define TT_EMB_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define TT_EMB_NOALLOC_MAX_DEVICES 64
+tt_emb_status tt_emb_forward_noalloc(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                                     const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                                     int64_t num_bags, float* out, void* stream);
 
 /* Backward pass (Section 3.2, Eq. 1) of L = sum <grad_out, out> into dense
  * core gradients dG1, dG2, dG3 (same shapes as the cores, OVERWRITTEN; rows

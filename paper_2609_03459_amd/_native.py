@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libttemb.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "tt_emb.h")
 
-TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED = range(6)
+TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED, TT_EMB_ESCRATCH = range(7)
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TT_EMB_NOALLOC_SCRATCH_BYTES
 REUSE = {"prefix": 0, "unique": 1, "none": 2}
 SCHED = {"steal": 0, "static": 1, "steal_ckpt": 2}
 KERNELS = {"ingest": 1, "fwd_fused": 2, "pool": 3, "seg_sum": 4, "bwd_fused": 5, "merge": 6, "split": 7}
@@ -77,6 +78,7 @@ _SIG = {
     "tt_emb_forward_n": ([_P, _P, _P, _I64, _P, _I64, _P, C.c_int, _P, C.c_size_t, _P], C.c_int),
     "tt_emb_backward_n": ([_P, _P, _P, _I64, _P, _I64, _P, _P, C.c_int, _P, C.c_size_t, _P], C.c_int),
     "tt_emb_sgd_n": ([_P, _P, _P, C.c_float, _P], C.c_int),
+    "tt_emb_forward_noalloc": ([_P, _P, _P, _P, _P, _I64, _P, _I64, _P, _P], C.c_int),
 }
 for _name, (_args, _res) in _SIG.items():
     _f = getattr(lib, _name)
@@ -191,3 +193,7 @@ def tt_emb_kernel_uses_mfma(h, kernel: int, num_indices: int) -> bool:
     flag = C.c_int(-1)
     check("tt_emb_kernel_uses_mfma", lib.tt_emb_kernel_uses_mfma(h, int(kernel), int(num_indices), C.byref(flag)))
     return bool(flag.value)
+
+
+def tt_emb_forward_noalloc(h, g1, g2, g3, idx, m, off, nb, out, stream) -> None:
+    check("tt_emb_forward_noalloc", lib.tt_emb_forward_noalloc(h, g1, g2, g3, idx, m, off, nb, out, stream))

@@ -2,6 +2,7 @@
 // The operator and its conventions are described in include/tt_emb.h.
 #include "../../include/tt_emb.h"
 
+#include <mutex>
 #include <new>
 #include <stdint.h>
 #include <string.h>
@@ -9,6 +10,12 @@
 #include "common.h"
 
 using namespace ttemb;
+
+// Workspace of tt_emb_forward_noalloc: a static array that every GPU the library
+// runs on holds until the process ends.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, once per device
+// (scratch_base below), and only that address is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[TT_EMB_NOALLOC_SCRATCH_BYTES];
 
 struct tt_emb_s {
   Shape s;
@@ -165,6 +172,7 @@ const char* tt_emb_status_string(tt_emb_status s) {
     case TT_EMB_EHIP: return "HIP runtime error";
     case TT_EMB_ERANGE: return "index or offsets out of range";
     case TT_EMB_EUNSUPPORTED: return "shape not supported";
+    case TT_EMB_ESCRATCH: return "call too large for the static scratch of the allocation-free forward";
   }
   return "unknown status";
 }
@@ -381,6 +389,56 @@ tt_emb_status tt_emb_forward(tt_emb_handle h, const float* G1, const float* G2, 
   }
   Work w;
   carve(h->s, num_indices, num_bags, workspace, &w);
+  return hip_status(launch_forward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, out, h->prof, s));
+}
+
+// Device address of `scratch` on the current device, looked up on the first call
+// made there and kept per device (each device holds its own copy of the array).
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[TT_EMB_NOALLOC_MAX_DEVICES];
+
+static tt_emb_status scratch_base(hipStream_t stream, void** base) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return TT_EMB_EHIP;
+  if (dev < 0 || dev >= TT_EMB_NOALLOC_MAX_DEVICES) return TT_EMB_EUNSUPPORTED;
+  if (stream) {  // the stream must belong to the current device, whose copy is looked up
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return TT_EMB_EHIP;
+    if ((int)sdev != dev) return TT_EMB_EINVAL;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TT_EMB_EHIP;
+    g_scratch_dev[dev] = p;
+  }
+  *base = g_scratch_dev[dev];
+  return TT_EMB_OK;
+}
+
+tt_emb_status tt_emb_forward_noalloc(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
+                                     const int64_t* indices, int64_t num_indices, const int64_t* offsets,
+                                     int64_t num_bags, float* out, void* stream) {
+  if (!h || h->s.L != 3) return TT_EMB_EINVAL;
+  if (num_indices < 0 || num_bags < 0 || num_indices > h->desc.max_indices || num_bags > h->desc.max_bags)
+    return TT_EMB_EINVAL;
+  if (forward_workspace_bytes(h->s, num_indices, num_bags) > (size_t)TT_EMB_NOALLOC_SCRATCH_BYTES)
+    return TT_EMB_ESCRATCH;
+  hipStream_t s = (hipStream_t)stream;
+  void* base = nullptr;
+  tt_emb_status st = scratch_base(s, &base);
+  if (st != TT_EMB_OK) return st;
+  // the checks of tt_emb_forward, with the scratch as the workspace
+  st = check_batch(h, indices, num_indices, offsets, num_bags, base, TT_EMB_NOALLOC_SCRATCH_BYTES, false);
+  if (st != TT_EMB_OK) return st;
+  if (!G1 || !G2 || !G3 || (!out && num_bags > 0)) return TT_EMB_EINVAL;
+  if (!al(G1, 16) || !al(G2, 16) || !al(G3, 16) || !al(out, 16)) return TT_EMB_EINVAL;
+  // grouped into the scratch (no grouping of the caller's workspace is touched or
+  // recorded); the grouping's launches clear every counter and table they rely on
+  Work w;
+  carve(h->s, num_indices, num_bags, base, &w);
+  if (launch_group(h->s, w, indices, num_indices, offsets, num_bags, h->prof, s) != hipSuccess)
+    return TT_EMB_EHIP;
   return hip_status(launch_forward(h->s, w, G1, G2, G3, offsets, num_indices, num_bags, out, h->prof, s));
 }
 

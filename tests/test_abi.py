@@ -264,3 +264,22 @@ def test_calls_n_reject_bad_arguments_without_launching(N):
                                      None) == E
     assert N.lib.tt_emb_sgd(h, fake, fake, fake, fake, fake, fake, lr, None) == E
     N.tt_emb_destroy(h)
+
+
+def test_noalloc_forward_host_checks(N):
+    # host-side refusals of the allocation-free forward, before any device call
+    E = N.TT_EMB_EINVAL
+    fake = 1 << 20
+    h = N.tt_emb_create(_desc(N, T=8, n=(200, 200, 250), d=(4, 4, 8), R=32, M=1 << 20, B=32768))
+    f = N.lib.tt_emb_forward_noalloc
+    assert f(None, fake, fake, fake, fake, 20, fake, 10, fake, None) == E
+    assert f(h, fake, fake, fake, fake, (1 << 20) + 1, fake, 10, fake, None) == E  # beyond max_indices
+    assert f(h, fake, fake, fake, fake, 20, fake, 32769, fake, None) == E          # beyond max_bags
+    assert f(h, fake, fake, fake, fake, -1, fake, 10, fake, None) == E
+    # 10^6 indices of 128 floats need far more than the 64 MiB scratch
+    assert f(h, fake, fake, fake, fake, 1 << 20, fake, 32768, fake, None) == N.TT_EMB_ESCRATCH
+    assert "scratch" in N.status_string(N.TT_EMB_ESCRATCH)
+    N.tt_emb_destroy(h)
+    h4 = N.tt_emb_create_n(_desc_n(N))
+    assert f(h4, fake, fake, fake, fake, 20, fake, 10, fake, None) == E  # four cores: not a three-core call
+    N.tt_emb_destroy(h4)
