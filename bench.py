@@ -67,8 +67,9 @@ class HipEvents:
 # Source files that define each benchmarked kernel and its launch (the counters
 # of a kernel stay valid while these files are unchanged).
 KERNEL_SOURCES = {
-    "bwd_fused": ["bwd_r32.hip", "common.h"],
-    "fwd_fused": ["fwd.hip", "common.h"],
+    # the fused kernels' work units (slices, chunks) are cut by the grouping, sized in tt_emb.hip
+    "bwd_fused": ["bwd_r32.hip", "common.h", "group.hip", "tt_emb.hip"],
+    "fwd_fused": ["fwd.hip", "common.h", "group.hip", "tt_emb.hip"],
     "pool": ["fwd.hip", "common.h"],
     "seg_sum": ["bwd.hip", "common.h"],
     "ingest": ["group.hip", "common.h"],

@@ -26,6 +26,7 @@ struct Shape {
   int slice_rows;  // rows per work slice: SLICE_ROWS, or 1 when prefix reuse is off (ablation)
   int dedup;       // 1: exact dedup of rows; 0: every occurrence is its own row (ablation)
   int sched;       // work distribution: SCHED_STEAL, SCHED_STATIC or SCHED_STEAL_CKPT (ablation)
+  int chunk_slices;  // slices per chunk of one (t, i2) run (TTEMB_CHUNK, or TTEMB_R64_CHUNK at R = 64)
   // Number of TT cores and their factors.  The fields above are the three-factor
   // view that the grouping and the fused kernels work on: for L = 3 the cores
   // themselves; for L >= 4 (n1, d1) = products of the factors of cores 0..L-3,
@@ -64,7 +65,16 @@ constexpr int SCAN_THREADS = 256;
 constexpr int SCAN_ITEMS = 16;
 constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
 constexpr int SLICE_ROWS = 32;   // unique rows per work slice
-constexpr int CHUNK_SLICES = 32; // slices per chunk of the specialised kernels (one (t, i2) run)
+constexpr int CHUNK_SLICES = 32; // most slices per chunk (one (t, i2) run); Shape::chunk_slices <= this
+// Slices per chunk at rank 64: the MFMA forward streams B from L2 for every quad
+// (nothing is kept per chunk), so short chunks cost no reloads and give the
+// persistent waves many more work units than there are waves.
+#ifndef TTEMB_R64_CHUNK
+#define TTEMB_R64_CHUNK 4
+#endif
+#ifndef TTEMB_CHUNK
+#define TTEMB_CHUNK 32
+#endif
 constexpr int SEG_CHUNK = 256;   // sorted occurrences per dE chunk
 constexpr int MAX_BWD_WG = 256;  // workgroups of the MFMA backward (one per CU on MI355X)
 

@@ -696,10 +696,10 @@ __global__ void k_make_slices_rows(const uint32_t* __restrict__ dense_base,
   }
 }
 
-// chunks of the specialised kernels: up to CHUNK_SLICES consecutive slices of
+// chunks of the specialised kernels: up to cs (the shape's chunk_slices) consecutive slices of
 // one (t, i2) run; run r covers slices [dense_base[r*n1], dense_base[(r+1)*n1])
 __global__ void k_run_counts(const uint32_t* __restrict__ dense_base, const int32_t* __restrict__ ctr, int nruns,
-                             int n1, uint32_t* __restrict__ run_nch) {
+                             int n1, int cs, uint32_t* __restrict__ run_nch) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r > nruns) return;
   if (r == nruns) {  // the scan turns this slot into the total
@@ -708,19 +708,19 @@ __global__ void k_run_counts(const uint32_t* __restrict__ dense_base, const int3
   }
   const uint32_t b0 = dense_base[(int64_t)r * n1];
   const uint32_t b1 = r + 1 < nruns ? dense_base[(int64_t)(r + 1) * n1] : (uint32_t)ctr[C_NSLICES];
-  run_nch[r] = (b1 - b0 + CHUNK_SLICES - 1) / CHUNK_SLICES;
+  run_nch[r] = (b1 - b0 + cs - 1) / cs;
 }
 
 __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uint32_t* __restrict__ run_base,
-                              const int32_t* __restrict__ ctr, int nruns, int n1, int4* __restrict__ chunks) {
+                              const int32_t* __restrict__ ctr, int nruns, int n1, int cs, int4* __restrict__ chunks) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= nruns) return;
   const uint32_t b0 = dense_base[(int64_t)r * n1];
   const uint32_t b1 = r + 1 < nruns ? dense_base[(int64_t)(r + 1) * n1] : (uint32_t)ctr[C_NSLICES];
   const uint32_t c0 = run_base[r];
-  for (uint32_t k = 0; b0 + k * CHUNK_SLICES < b1; ++k) {
-    const uint32_t f = b0 + k * CHUNK_SLICES;
-    const uint32_t n = b1 - f < (uint32_t)CHUNK_SLICES ? b1 - f : (uint32_t)CHUNK_SLICES;
+  for (uint32_t k = 0; b0 + k * cs < b1; ++k) {
+    const uint32_t f = b0 + k * cs;
+    const uint32_t n = b1 - f < (uint32_t)cs ? b1 - f : (uint32_t)cs;
     chunks[c0 + k] = make_int4((int)f, (int)n, r, 0);
   }
 }
@@ -731,7 +731,7 @@ __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uin
 // runs.  (The chunk list stays a launch of its own: a run can hold thousands of
 // chunks at the no-dedup level.)
 __global__ void __launch_bounds__(SCAN_THREADS) k_runs_one_block(const uint32_t* __restrict__ dense_base,
-                                                                 int32_t* __restrict__ ctr, int nruns, int n1,
+                                                                 int32_t* __restrict__ ctr, int nruns, int n1, int cs,
                                                                  uint32_t* __restrict__ run_nch) {
   __shared__ uint32_t smem[SCAN_THREADS / 64];
   const uint32_t nsl = (uint32_t)ctr[C_NSLICES];
@@ -744,7 +744,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_runs_one_block(const uint32_t*
   }
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
-    cnt[k] = r0 + k < nruns ? (b[k + 1] - b[k] + CHUNK_SLICES - 1) / CHUNK_SLICES : 0u;
+    cnt[k] = r0 + k < nruns ? (b[k + 1] - b[k] + cs - 1) / cs : 0u;
     sum += cnt[k];
   }
   uint32_t tot;
@@ -885,16 +885,16 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   const int nruns = s.T * s.n2;
   if (nruns + 1 <= SCAN_TILE) {
     hipLaunchKernelGGL(k_runs_one_block, dim3(1), dim3(SCAN_THREADS), 0, st, (const uint32_t*)w.dense_base, w.ctr,
-                       nruns, s.n1, w.run_nch);
+                       nruns, s.n1, s.chunk_slices, w.run_nch);
   } else {
     hipLaunchKernelGGL(k_run_counts, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
-                       (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
+                       (const int32_t*)w.ctr, nruns, s.n1, s.chunk_slices, w.run_nch);
     // exclusive scan in place; the tile sums buffer of the dense scan is free again
     e = scan_generic<uint32_t, false>(w.run_nch, w.run_nch, nruns + 1, w.tsum32, w.ctr + C_NCHUNKS, st);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(k_make_chunks, dim3((nruns + 255) / 256), dim3(256), 0, st, (const uint32_t*)w.dense_base,
-                     (const uint32_t*)w.run_nch, (const int32_t*)w.ctr, nruns, s.n1, w.chunks);
+                     (const uint32_t*)w.run_nch, (const int32_t*)w.ctr, nruns, s.n1, s.chunk_slices, w.chunks);
   return hipGetLastError();
 }
 

@@ -84,8 +84,8 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   int64_t nsl_max = m / s.slice_rows + groups_max + 1;
   if (s.dedup && s.ndense * per_prefix < nsl_max) nsl_max = s.ndense * per_prefix;
   if (nsl_max > m) nsl_max = m;
-  // chunks: ceil(slices of run / CHUNK_SLICES) per non-empty (t, i2) run
-  int64_t nch_max = nsl_max / CHUNK_SLICES + (int64_t)s.T * s.n2 + 1;
+  // chunks: ceil(slices of run / chunk_slices) per non-empty (t, i2) run
+  int64_t nch_max = nsl_max / s.chunk_slices + (int64_t)s.T * s.n2 + 1;
   if (nch_max > nsl_max) nch_max = nsl_max;
   W->nsl_max = nsl_max;
   W->nch_max = nch_max;
@@ -213,6 +213,7 @@ static tt_emb_status create_view(const tt_emb_desc* d, int L, const int32_t* nk,
   s.slice_rows = SLICE_ROWS;
   s.dedup = 1;
   s.sched = SCHED_STEAL;
+  s.chunk_slices = s.R == 64 ? TTEMB_R64_CHUNK : TTEMB_CHUNK;
   s.L = L;
   for (int k = 0; k < MAX_CORES; ++k) {
     s.nk[k] = k < L ? nk[k] : 1;
