@@ -394,9 +394,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--reuse", choices=["prefix", "unique", "none"], default="prefix",
                     help="reuse level (ablation of Section 4.5): prefix groups (default), exact dedup only, none")
-    ap.add_argument("--sched", choices=["steal", "static", "steal_ckpt"], default="steal",
+    ap.add_argument("--sched", choices=["steal", "static", "steal_ckpt", "group"], default="steal",
                     help="work distribution (ablation of Section 4.4): stealing (default), static shares, "
-                         "stealing with checkpointed intermediates")
+                         "stealing with checkpointed intermediates, static prefix mapping (whole groups)")
     ap.add_argument("--cores", type=int, choices=sorted(CORE_SPLITS), default=3,
                     help="number of TT cores: the same tables factorised over L cores (L > 3: future work in "
                          "the paper)")

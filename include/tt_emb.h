@@ -116,14 +116,29 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
  *                            resident worker, L2-resident), and a worker that
  *                            meets the same group later reloads it instead of
  *                            recomputing it, whenever the entry still holds
- *                            that group.
+ *                            that group;
+ *   TT_EMB_SCHED_GROUP       static prefix mapping, the baseline of Section
+ *                            4.4: every prefix group is one work unit of its
+ *                            own, never split across workers (a group of more
+ *                            than 64 work slices, i.e. more than 2,048 unique
+ *                            rows, is cut into 64-slice pieces), and each
+ *                            worker takes a fixed contiguous share of the
+ *                            groups.
  * The checkpoint applies to the kernels that keep one C per worker (the
  * generic kernels); the MFMA kernels (forward for d = (4,4,8) with R = 32 or
  * 64, backward for d = (4,4,8) with R = 32) build C for four slices per
  * matrix-core tile and treat STEAL_CKPT as STEAL.  All
- * modes compute the same function.  Host only; may be changed between calls;
- * returns TT_EMB_EINVAL for an unknown mode. */
-typedef enum { TT_EMB_SCHED_STEAL = 0, TT_EMB_SCHED_STATIC = 1, TT_EMB_SCHED_STEAL_CKPT = 2 } tt_emb_sched;
+ * modes compute the same function.  Host only; may be changed between calls,
+ * except that TT_EMB_SCHED_GROUP cuts the work list in the grouping and needs a
+ * larger workspace: set it before tt_emb_workspace_size, and a grouping made
+ * in another mode is not reused across a switch into or out of it.  Returns
+ * TT_EMB_EINVAL for an unknown mode. */
+typedef enum {
+  TT_EMB_SCHED_STEAL = 0,
+  TT_EMB_SCHED_STATIC = 1,
+  TT_EMB_SCHED_STEAL_CKPT = 2,
+  TT_EMB_SCHED_GROUP = 3
+} tt_emb_sched;
 tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode);
 
 /* Bytes of device workspace for a call with num_indices indices and num_bags

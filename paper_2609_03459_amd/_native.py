@@ -17,7 +17,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "tt_emb.h")
 TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED, TT_EMB_ESCRATCH = range(7)
 NOALLOC_SCRATCH_BYTES = 64 << 20  # TT_EMB_NOALLOC_SCRATCH_BYTES
 REUSE = {"prefix": 0, "unique": 1, "none": 2}
-SCHED = {"steal": 0, "static": 1, "steal_ckpt": 2}
+SCHED = {"steal": 0, "static": 1, "steal_ckpt": 2, "group": 3}
 KERNELS = {"ingest": 1, "fwd_fused": 2, "pool": 3, "seg_sum": 4, "bwd_fused": 5, "merge": 6, "split": 7}
 
 

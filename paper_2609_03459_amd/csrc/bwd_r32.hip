@@ -160,12 +160,12 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
 
   int f = 0, ns = 0, run = -1;
   // claim a chunk; load its slice descriptors and the i3 words of its first quad
-  // SCHED_STATIC: this wave's fixed share of the owner's chunks, in order
+  // static modes: this wave's fixed share of the owner's chunks, in order
   const int owid = (blockIdx.x / nq) * BW_WAVES + wave, onw = (gridDim.x / nq) * BW_WAVES;
   int st_next = share_lo(nch, onw, owid);
   const int st_hi = share_lo(nch, onw, owid + 1);
   auto next_chunk = [&]() {
-    const int cc = s.sched == SCHED_STATIC ? (st_next < st_hi ? st_next++ : -1) : claim_queues(qctr, nch, 1, 0, &cursor);
+    const int cc = sched_static(s.sched) ? (st_next < st_hi ? st_next++ : -1) : claim_queues(qctr, nch, 1, 0, &cursor);
     if (cc >= 0) {
       const int4 ch = chunks[c_lo + cc];
       f = __builtin_amdgcn_readfirstlane(ch.x);

@@ -25,7 +25,7 @@ struct Shape {
   int64_t ndense;  // T*n1*n2 prefix slots
   int slice_rows;  // rows per work slice: SLICE_ROWS, or 1 when prefix reuse is off (ablation)
   int dedup;       // 1: exact dedup of rows; 0: every occurrence is its own row (ablation)
-  int sched;       // work distribution: SCHED_STEAL, SCHED_STATIC or SCHED_STEAL_CKPT (ablation)
+  int sched;       // work distribution: SCHED_STEAL, SCHED_STATIC, SCHED_STEAL_CKPT or SCHED_GROUP (ablation)
   int chunk_slices;  // slices per chunk of one (t, i2) run (TTEMB_CHUNK, or TTEMB_R64_CHUNK at R = 64)
   // Number of TT cores and their factors.  The fields above are the three-factor
   // view that the grouping and the fused kernels work on: for L = 3 the cores
@@ -278,7 +278,14 @@ __device__ __forceinline__ int claim_block(int32_t* q, int nchunks, int nq, int 
 }
 
 // Work distribution modes (values of the C-ABI's tt_emb_sched).
-enum : int { SCHED_STEAL = 0, SCHED_STATIC = 1, SCHED_STEAL_CKPT = 2 };
+enum : int { SCHED_STEAL = 0, SCHED_STATIC = 1, SCHED_STEAL_CKPT = 2, SCHED_GROUP = 3 };
+// Static modes: fixed contiguous shares of the chunk list (SCHED_GROUP: chunks are
+// whole prefix groups, see GROUP_CHUNK_MAX).
+__host__ __device__ __forceinline__ bool sched_static(int sched) { return sched == SCHED_STATIC || sched == SCHED_GROUP; }
+// SCHED_GROUP cuts chunks at prefix-group boundaries: one chunk per group, a group
+// of more slices than this (more than 2,048 rows) in pieces of this many, which the
+// fused kernels' per-lane slice descriptors bound.
+constexpr int GROUP_CHUNK_MAX = 64;
 // Checkpoint table of the generic fused kernels: CKPT_SLOTS entries of one C
 // (d1 d2 R floats) each, tagged with the prefix group they hold.
 constexpr int CKPT_SLOTS = 1024;
@@ -289,7 +296,7 @@ constexpr int CKPT_SLOTS = 1024;
 // block takes the same branch.
 __device__ __forceinline__ int claim_block_sched(int sched, int32_t* q, int nchunks, int home, int* cursor,
                                                  int* s_chunk, int* next) {
-  if (sched == SCHED_STATIC) {
+  if (sched_static(sched)) {
     const int hi = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x + 1);
     return *next < hi ? (*next)++ : -1;
   }

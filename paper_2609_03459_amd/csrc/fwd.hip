@@ -53,6 +53,8 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
                                                              const float* __restrict__ G2,
                                                              const float* __restrict__ G3,
                                                              const int4* __restrict__ slices,
+                                                             const int4* __restrict__ chunks,
+                                                             const uint32_t* __restrict__ run_base,
                                                              const int32_t* __restrict__ uniq_i3,
                                                              int32_t* __restrict__ ctr, float* __restrict__ E,
                                                              float* __restrict__ ckpt, int32_t* __restrict__ ckpt_tag,
@@ -67,7 +69,9 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
   float* Bs = As + s.d1 * s.R;  // R * (d2R + 1) when stage_b
   __shared__ int s_chunk, s_flag;
   const int nsl = ctr[C_NSLICES];
-  const int nchunks = (nsl + FWD_CHUNK - 1) / FWD_CHUNK;
+  // work units: FWD_CHUNK consecutive slices, or with SCHED_GROUP the chunk list's whole groups
+  const bool by_group = s.sched == SCHED_GROUP;
+  const int nchunks = by_group ? (int)run_base[s.T * s.n2] : (nsl + FWD_CHUNK - 1) / FWD_CHUNK;
   int victim = 0;
   int next = share_lo(nchunks, (int)gridDim.x, (int)blockIdx.x);
   int cur_pg = -1, cur_run = -1;
@@ -76,8 +80,15 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
     const int c = claim_block_sched(s.sched, ctr + C_FWD_CTR, nchunks, blockIdx.x % SCHED_NQ, &victim, &s_chunk,
                                     &next);
     if (c < 0) break;
-    const int s0 = c * FWD_CHUNK;
-    const int s1 = s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl;
+    int s0, s1;
+    if (by_group) {
+      const int4 ch = chunks[c];
+      s0 = ch.x;
+      s1 = ch.x + ch.y;
+    } else {
+      s0 = c * FWD_CHUNK;
+      s1 = s0 + FWD_CHUNK < nsl ? s0 + FWD_CHUNK : nsl;
+    }
     for (int si = s0; si < s1; ++si) {
       const int4 sl = slices[si];
       const int p = sl.x, rb = sl.y, re = sl.z;
@@ -181,12 +192,12 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   int c_rb = 0, c_nr = 0, c_i1 = 0;
   int f = 0, ns = 0, run = -1, t = 0, qd = 0;
   int c = -1;
-  // SCHED_STATIC: this wave's fixed share of the chunks, in order
+  // static modes: this wave's fixed share of the chunks, in order
   const int wid = blockIdx.x * F32_WAVES + wave, nw = gridDim.x * F32_WAVES;
   int st_next = share_lo(nch, nw, wid);
   const int st_hi = share_lo(nch, nw, wid + 1);
   auto next_chunk = [&]() {
-    if (s.sched == SCHED_STATIC)
+    if (sched_static(s.sched))
       c = st_next < st_hi ? st_next++ : -1;
     else
       c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
@@ -403,7 +414,7 @@ __global__ void __launch_bounds__(64 * F64_WAVES, F64_WG_PER_CU)
   int st_next = share_lo(nch, nw, wid);
   const int st_hi = share_lo(nch, nw, wid + 1);
   auto next_chunk = [&]() {
-    if (s.sched == SCHED_STATIC)
+    if (sched_static(s.sched))
       c = st_next < st_hi ? st_next++ : -1;
     else
       c = claim_queues(ctr + C_FWD_CTR, nch, SCHED_NQ, blockIdx.x % SCHED_NQ, &cursor);
@@ -806,12 +817,12 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
     prof_begin(prof, K_FWD_FUSED, st);
     if (wide)
       hipLaunchKernelGGL(k_fwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
-                         (const int4*)w.slices, (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag,
-                         stage_b);
+                         (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                         (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag, stage_b);
     else
       hipLaunchKernelGGL(k_fwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
-                         (const int4*)w.slices, (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag,
-                         stage_b);
+                         (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
+                         (const int32_t*)w.uniq_i3, w.ctr, w.E, w.ckpt, w.ckpt_tag, stage_b);
     prof_end(prof, K_FWD_FUSED, st);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

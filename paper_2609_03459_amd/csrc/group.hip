@@ -725,6 +725,31 @@ __global__ void k_make_chunks(const uint32_t* __restrict__ dense_base, const uin
   }
 }
 
+// SCHED_GROUP: chunks are whole prefix groups.  Chunks per prefix slot (a group of
+// more than GROUP_CHUNK_MAX slices in pieces), scanned in place into each slot's
+// first chunk; a run's first chunk is then that of its first slot.
+__global__ void k_slot_chunks(const uint32_t* __restrict__ dense_cnt, int64_t ndense, uint32_t* __restrict__ cnt_out) {
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < ndense; x += (int64_t)gridDim.x * blockDim.x)
+    cnt_out[x] = (dense_cnt[x] + GROUP_CHUNK_MAX - 1) / GROUP_CHUNK_MAX;
+}
+__global__ void k_group_run_base(const uint32_t* __restrict__ slot_base, const int32_t* __restrict__ ctr, int nruns,
+                                 int n1, uint32_t* __restrict__ run_base) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < nruns) run_base[r] = slot_base[(int64_t)r * n1];
+  if (r == nruns) run_base[r] = (uint32_t)ctr[C_NCHUNKS];
+}
+__global__ void k_make_group_chunks(const uint32_t* __restrict__ dense_cnt, const uint32_t* __restrict__ dense_base,
+                                    const uint32_t* __restrict__ slot_base, int64_t ndense, int n1,
+                                    int4* __restrict__ chunks) {
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < ndense; x += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t c = dense_cnt[x];
+    for (uint32_t k = 0; k * GROUP_CHUNK_MAX < c; ++k) {
+      const uint32_t n = c - k * GROUP_CHUNK_MAX < (uint32_t)GROUP_CHUNK_MAX ? c - k * GROUP_CHUNK_MAX : GROUP_CHUNK_MAX;
+      chunks[slot_base[x] + k] = make_int4((int)(dense_base[x] + k * GROUP_CHUNK_MAX), (int)n, (int)(x / n1), 0);
+    }
+  }
+}
+
 // k_run_counts and the scan of its counts in one workgroup when nruns + 1 <=
 // SCAN_TILE: chunk counts per run, exclusive scan into run_nch (the total at
 // run_nch[nruns] and in ctr[C_NCHUNKS]).  A thread owns SCAN_ITEMS consecutive
@@ -883,6 +908,20 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
                        s.ndense, (const int32_t*)w.pg_start, (const uint32_t*)w.pg_key, s.n1, s.slice_rows,
                        w.slices, w.slice_i1);
   const int nruns = s.T * s.n2;
+  if (s.sched == SCHED_GROUP) {
+    // slot chunk counts, then their exclusive scan, in dense_pg (free once the slices are made)
+    uint32_t* slot_base = reinterpret_cast<uint32_t*>(w.dense_pg);
+    hipLaunchKernelGGL(k_slot_chunks, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
+                       (const uint32_t*)w.dense_cnt, s.ndense, slot_base);
+    e = scan_generic<uint32_t, false>(slot_base, slot_base, s.ndense, w.tsum32, w.ctr + C_NCHUNKS, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_group_run_base, dim3((nruns + 1 + 255) / 256), dim3(256), 0, st, (const uint32_t*)slot_base,
+                       (const int32_t*)w.ctr, nruns, s.n1, w.run_nch);
+    hipLaunchKernelGGL(k_make_group_chunks, dim3(grid_for(s.ndense, 256, 4096)), dim3(256), 0, st,
+                       (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const uint32_t*)slot_base,
+                       s.ndense, s.n1, w.chunks);
+    return hipGetLastError();
+  }
   if (nruns + 1 <= SCAN_TILE) {
     hipLaunchKernelGGL(k_runs_one_block, dim3(1), dim3(SCAN_THREADS), 0, st, (const uint32_t*)w.dense_base, w.ctr,
                        nruns, s.n1, s.chunk_slices, w.run_nch);

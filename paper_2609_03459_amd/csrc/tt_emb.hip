@@ -84,8 +84,10 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   int64_t nsl_max = m / s.slice_rows + groups_max + 1;
   if (s.dedup && s.ndense * per_prefix < nsl_max) nsl_max = s.ndense * per_prefix;
   if (nsl_max > m) nsl_max = m;
-  // chunks: ceil(slices of run / chunk_slices) per non-empty (t, i2) run
-  int64_t nch_max = nsl_max / s.chunk_slices + (int64_t)s.T * s.n2 + 1;
+  // chunks: ceil(slices of run / chunk_slices) per non-empty (t, i2) run, or with
+  // SCHED_GROUP ceil(slices of group / GROUP_CHUNK_MAX) per prefix group
+  int64_t nch_max = s.sched == SCHED_GROUP ? groups_max + nsl_max / GROUP_CHUNK_MAX + 1
+                                           : nsl_max / s.chunk_slices + (int64_t)s.T * s.n2 + 1;
   if (nch_max > nsl_max) nch_max = nsl_max;
   W->nsl_max = nsl_max;
   W->nch_max = nch_max;
@@ -315,7 +317,9 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level) {
 }
 
 tt_emb_status tt_emb_set_schedule(tt_emb_handle h, int mode) {
-  if (!h || mode < TT_EMB_SCHED_STEAL || mode > TT_EMB_SCHED_STEAL_CKPT) return TT_EMB_EINVAL;
+  if (!h || mode < TT_EMB_SCHED_STEAL || mode > TT_EMB_SCHED_GROUP) return TT_EMB_EINVAL;
+  // the group mode cuts the work list differently: no grouping is reused across it
+  if ((mode == TT_EMB_SCHED_GROUP) != (h->s.sched == SCHED_GROUP)) h->g_valid = false;
   h->s.sched = mode;
   return TT_EMB_OK;
 }

@@ -122,7 +122,7 @@ def test_calls_reject_bad_arguments_without_launching(N):
     assert b(h, fake, fake, fake, fake, 20, off, 10, fake, fake, fake, fake, 0, fake, ws_call - 1, None) == E
     assert N.lib.tt_emb_group(h, fake, 20, off, 10, fake, 256, None) == E
     assert N.lib.tt_emb_group(h, None, 20, off, 10, fake, ws_bytes, None) == E
-    assert N.lib.tt_emb_set_schedule(h, 3) == E and N.lib.tt_emb_set_schedule(h, -1) == E
+    assert N.lib.tt_emb_set_schedule(h, 4) == E and N.lib.tt_emb_set_schedule(h, -1) == E
     assert N.lib.tt_emb_set_schedule(None, 0) == E
     assert N.lib.tt_emb_set_schedule(h, 2) == N.TT_EMB_OK and N.lib.tt_emb_set_schedule(h, 0) == N.TT_EMB_OK
     assert N.lib.tt_emb_debug_grouping(h, fake, None, None, None, None, None, None, None, None, None) == E
@@ -283,3 +283,14 @@ def test_noalloc_forward_host_checks(N):
     h4 = N.tt_emb_create_n(_desc_n(N))
     assert f(h4, fake, fake, fake, fake, 20, fake, 10, fake, None) == E  # four cores: not a three-core call
     N.tt_emb_destroy(h4)
+
+
+def test_group_schedule_sizes_its_own_work_list(N):
+    # the static prefix mapping cuts one chunk per prefix group: more chunk partials
+    h = N.tt_emb_create(_desc(N, T=2, n=(20, 30, 40), d=(4, 4, 8), R=32, M=5000, B=100))
+    base = N.tt_emb_workspace_size(h, 5000, 100)
+    N.tt_emb_set_schedule(h, N.SCHED["group"])
+    assert N.tt_emb_workspace_size(h, 5000, 100) > base
+    N.tt_emb_set_schedule(h, N.SCHED["static"])
+    assert N.tt_emb_workspace_size(h, 5000, 100) == base
+    N.tt_emb_destroy(h)

@@ -733,8 +733,9 @@ def _run_mode(lib, case, **kw):
 @pytest.mark.parametrize("which", ["hot_r64", "mfma"])
 def test_schedules_same_results(lib, orc, which):
     # Section 4.4 ablation modes compute the same function: static shares, stealing,
-    # and stealing with the checkpointed intermediate (hot prefix groups spanning
-    # several chunks on the generic kernels)
+    # stealing with the checkpointed intermediate (hot prefix groups spanning
+    # several chunks on the generic kernels), and the static prefix mapping (each
+    # group one work unit)
     if which == "hot_r64":
         case = ttgen.make(4, bags=256, with_grad=True)
     else:
@@ -744,7 +745,7 @@ def test_schedules_same_results(lib, orc, which):
     mag_v, _ = orc.forward(abs_case(case))
     ref = orc.backward(case)[:3]
     mag = orc.backward(abs_case(case))[:3]
-    for sched in ("steal", "static", "steal_ckpt"):
+    for sched in ("steal", "static", "steal_ckpt", "group"):
         _say(f"[sched] {which} {sched}")
         V, grads, emb = _run_mode(lib, case, sched=sched)
         assert_close(f"forward {which} {sched}", V, ref_v, mag_v)
