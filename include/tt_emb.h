@@ -201,13 +201,17 @@ tt_emb_status tt_emb_forward_noalloc(tt_emb_handle h, const float* G1, const flo
  * no index touches are zero).  Per unique row, dE is the sum of grad_out
  * over its occurrences; per row dD = C^T dE and dC = dE D^T; per prefix
  * group the dC are summed first and dA = (sum dC) B^T, dB = A^T (sum dC).
- * On the MFMA shape (see tt_emb_kernel_uses_mfma) the gradients of G1 and G2
- * are fixed-order segment sums of per-slice and per-chunk partials, and dG3 is
- * summed in on-chip memory per (table, rank half) and then over workgroups in
- * a fixed order (its on-chip adds land in arrival order, so dG3 is
- * reproducible to rounding, not bit for bit); the generic kernels of other
- * shapes add their partial products into the gradients with global float
- * atomics.  reuse_grouping as for tt_emb_forward. */
+ * The per-core gradients are reduced by segments, with no global float
+ * atomics: dG1 is a fixed-order sum of per-slice partials over the slices of
+ * each (table, i1), dG2 of per-chunk partials over the chunks of each
+ * (table, i2).  dG3: on the MFMA shape (see tt_emb_kernel_uses_mfma) it is
+ * summed in on-chip memory per (table, rank half) and workgroup, then over the
+ * workgroups in a fixed order (the on-chip adds land in arrival order, so this
+ * dG3 is reproducible to rounding, not bit for bit); on other shapes every
+ * unique row's dD is a partial, the rows are put in (table, i3) order by a
+ * stable sort, and each dG3 slice is the sum over its rows in that order, so
+ * all three gradients are bit-reproducible there.  reuse_grouping as for
+ * tt_emb_forward. */
 tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
                               const int64_t* indices, int64_t num_indices, const int64_t* offsets,
                               int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
@@ -227,10 +231,8 @@ tt_emb_status tt_emb_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const
  * happens after the whole reduction (the kernels that read the cores have
  * finished; rows no index touches are unchanged).  G1..G3 are read and then
  * updated in place; indices, offsets, grad_out, reuse_grouping, workspace
- * and errors as for tt_emb_backward.  On the shapes the MFMA kernels serve
- * the update is applied inside the final gradient reductions; otherwise the
- * gradients go to a core-sized region of the workspace first (included in
- * tt_emb_workspace_size for those shapes). */
+ * and errors as for tt_emb_backward.  The update is applied inside the final
+ * segment sums of the gradients, as each element's sum is formed. */
 tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* G3, const int64_t* indices,
                                   int64_t num_indices, const int64_t* offsets, int64_t num_bags,
                                   const float* grad_out, float lr, int reuse_grouping, void* workspace,

@@ -305,9 +305,12 @@ __global__ void __launch_bounds__(64 * FIX_WAVES) k_seg_fix(const int32_t* __res
 // so reads across a's take distinct banks) when it fits.  Per slice: A staged; C
 // recomputed (or reloaded from the checkpoint); the slice's rows in batches whose
 // dE rows are staged together: dD per row into dG3, the rows' dC summed; then dA
-// into dG1 and dB = A^T (sum dC) summed over the chunk in LDS (added to dG2 once
-// per chunk) when it fits, else added per slice.  Core gradients meet in global
-// atomics.
+// into the slice's partial and dB = A^T (sum dC) summed over the chunk (in LDS
+// when it fits, else in the chunk's partial in global memory, each element owned
+// by one thread) into the chunk's partial; dD of every row into the row's partial.
+// No two blocks write one partial, and the fixed-order segment sums below turn the
+// partials into dG1 (over the slices of (t, i1)), dG2 (over the chunks of
+// (t, i2)) and dG3 (over the rows of (t, i3)).
 // ---------------------------------------------------------------------------
 constexpr int BWD_LDS_FLOATS = 40448;  // dynamic LDS budget (158 KB of the 160 KB)
 constexpr int BWD_DE_FLOATS = 4096;    // dE rows staged per batch
@@ -378,8 +381,8 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
                                                              const uint32_t* __restrict__ run_base,
                                                              const int32_t* __restrict__ uniq_i3,
                                                              int32_t* __restrict__ ctr, const float* __restrict__ dE,
-                                                             float* __restrict__ dG1, float* __restrict__ dG2,
-                                                             float* __restrict__ dG3, float* __restrict__ ckpt,
+                                                             float* __restrict__ dApart, float* __restrict__ dBpart,
+                                                             float* __restrict__ dDpart, float* __restrict__ ckpt,
                                                              int32_t* __restrict__ ckpt_tag, int stage_b, int db_lds,
                                                              int rows_per_batch) {
   extern __shared__ float lds[];
@@ -415,7 +418,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
     const int run = ch.z;  // t * n2 + i2
     const int t = run / s.n2;
     const float* Bg = G2 + (int64_t)run * nB;
-    float* g2 = dG2 + (int64_t)run * nB;
+    float* g2 = dBpart + (int64_t)c * nB;  // this chunk's dB partial
     __syncthreads();  // the previous chunk is done with Bs and dBs
     if (stage_b) {
       StepQR ix(threadIdx.x, BWD_THREADS, d2R);
@@ -458,8 +461,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
           const int part = tk / RD, e = tk - part * RD;
           const int b = e / s.d3, j3 = e - b * s.d3;
           for (int rr = part; rr < nr; rr += g_dd) {
-            const float acc = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
-            unsafeAtomicAdd(&dG3[((int64_t)(t * s.n3 + uniq_i3[u0 + rr]) * s.R + b) * s.d3 + j3], acc);
+            dDpart[(int64_t)(u0 + rr) * RD + e] = dot_strided(C + b, s.R, dEb + rr * s.D + j3, s.d3, rows12);
           }
         }
         // dC = sum over the batch's rows of dE_u D_u^T; with fewer outputs than threads,
@@ -488,7 +490,7 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
       // dA: four consecutive lanes per output, each over every fourth term, combined by
       // shuffles within the wave (the loop runs whole block strides so every lane takes
       // part in the shuffles)
-      float* g1 = dG1 + ((int64_t)(t * s.n1 + i1) * s.d1) * s.R;
+      float* g1 = dApart + (int64_t)si * s.d1 * s.R;  // this slice's dA partial
       StepQR dax((int)threadIdx.x >> 2, BWD_THREADS >> 2, s.R);  // (j1, a) of o
       for (int base = 0; base < 4 * s.d1 * s.R; base += BWD_THREADS, dax.next()) {
         const int o4 = base + (int)threadIdx.x;
@@ -499,22 +501,174 @@ __global__ void __launch_bounds__(BWD_THREADS) k_bwd_generic(ShapeArgs s, const 
         float v = ok ? dot_strided(dCs + j1 * d2R + part, 4, Bm + a * bp + part, 4, nterm) : 0.f;
         v += __shfl_xor(v, 1, 64);
         v += __shfl_xor(v, 2, 64);
-        if (ok && part == 0) unsafeAtomicAdd(&g1[o], v);
+        if (ok && part == 0) g1[o] = v;
       }
       StepQR dbx(threadIdx.x, BWD_THREADS, d2R);  // (a, column)
       for (int o = threadIdx.x; o < nB; o += BWD_THREADS, dbx.next()) {
         const int a = dbx.q, cc = dbx.r;
         float acc = 0.f;
         for (int j1 = 0; j1 < s.d1; ++j1) acc = fmaf(As[j1 * s.R + a], dCs[j1 * d2R + cc], acc);
+        // each thread owns its elements across the chunk's slices
         if (db_lds)
-          dBs[o] += acc;  // each thread owns its elements across the chunk's slices
+          dBs[o] += acc;
         else
-          unsafeAtomicAdd(&g2[o], acc);
+          g2[o] = si == s0 ? acc : g2[o] + acc;
       }
     }
     if (db_lds)
-      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) unsafeAtomicAdd(&g2[o], dBs[o]);
+      for (int o = threadIdx.x; o < nB; o += BWD_THREADS) g2[o] = dBs[o];
   }
+}
+
+// ---------------------------------------------------------------------------
+// Fixed-order segment sums of the generic backward's partials.  Each writes its
+// sum into the gradient, or with update set subtracts lr times it from the core
+// itself (the fused backward-and-SGD call; the fused kernel has finished reading
+// the cores).  Every element of its core is visited exactly once; untouched
+// slices get zero (or are left as they are by the update).
+// ---------------------------------------------------------------------------
+constexpr int GRED_THREADS = 256;
+
+__device__ __forceinline__ void put_g(float* out, int64_t i, float acc, float lr, bool update) {
+  out[i] = update ? out[i] - lr * acc : acc;
+}
+
+// dG1[t][i1] = sum of the dA partials of the slices of prefixes (i1, i2), i2 ascending
+// (each prefix's slices in order); block (t i1, column block)
+__global__ void __launch_bounds__(GRED_THREADS) k_gred_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
+                                                          const uint32_t* __restrict__ dense_base,
+                                                          const float* __restrict__ dApart, float* __restrict__ dG1,
+                                                          float lr, bool update) {
+  __shared__ uint32_t cnt[GRED_THREADS], base[GRED_THREADS];
+  const int ti1 = blockIdx.x;
+  const int t = ti1 / s.n1, i1 = ti1 - t * s.n1;
+  const int d1R = s.d1 * s.R;
+  const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
+  float a0 = 0.f, a1 = 0.f;  // even and odd slices of the ordered list, added at the end
+  int k = 0;
+  for (int r0 = 0; r0 < s.n2; r0 += GRED_THREADS) {
+    const int i2 = r0 + (int)threadIdx.x;
+    __syncthreads();
+    if (i2 < s.n2) {
+      const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
+      cnt[threadIdx.x] = dense_cnt[slot];
+      base[threadIdx.x] = dense_base[slot];
+    } else {
+      cnt[threadIdx.x] = 0;
+    }
+    __syncthreads();
+    if (e < d1R) {
+      const int nr = s.n2 - r0 < GRED_THREADS ? s.n2 - r0 : GRED_THREADS;
+      for (int q = 0; q < nr; ++q)
+        for (uint32_t j = 0; j < cnt[q]; ++j, ++k) {
+          const float v = dApart[(int64_t)(base[q] + j) * d1R + e];
+          if (k & 1)
+            a1 += v;
+          else
+            a0 += v;
+        }
+    }
+  }
+  if (e < d1R) put_g(dG1, (int64_t)ti1 * d1R + e, a0 + a1, lr, update);
+}
+
+// dG2[t][i2] = sum of the dB partials of the chunks of run (t, i2), in chunk order
+__global__ void __launch_bounds__(GRED_THREADS) k_gred_g2(const uint32_t* __restrict__ run_base,
+                                                          const float* __restrict__ dBpart, int nB,
+                                                          float* __restrict__ dG2, float lr, bool update) {
+  const int r = blockIdx.x;
+  const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
+  if (e >= nB) return;
+  const int c0 = (int)run_base[r], c1 = (int)run_base[r + 1];
+  float a[4] = {0.f, 0.f, 0.f, 0.f};  // chunk c goes to a[(c - c0) & 3]: four loads in flight
+  int c = c0;
+  for (; c + 4 <= c1; c += 4)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] += dBpart[(int64_t)(c + q) * nB + e];
+  for (; c < c1; ++c) a[(c - c0) & 3] += dBpart[(int64_t)c * nB + e];
+  put_g(dG2, (int64_t)r * nB + e, (a[0] + a[1]) + (a[2] + a[3]), lr, update);
+}
+
+// Sort keys t n3 + i3 of the unique rows (positions from U on get `sentinel`, which
+// sorts last), values = row ids
+__global__ void k_g3_keys(ShapeArgs s, const uint32_t* __restrict__ uniq_key, const int32_t* __restrict__ ctr, int n,
+                          uint32_t sentinel, uint32_t* __restrict__ keys, uint32_t* __restrict__ vals) {
+  const int U = ctr[C_U];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+    uint32_t k = sentinel;
+    if (i < U) {
+      const Digits d = decode_key(uniq_key[i], s.Npad, s.n2, s.n3);
+      k = (uint32_t)d.t * (uint32_t)s.n3 + (uint32_t)d.i3;
+    }
+    keys[i] = k;
+    vals[i] = (uint32_t)i;
+  }
+}
+
+// [lo, hi) of every (t, i3) in the sorted rows (bins no row falls in keep lo = hi = 0)
+__global__ void k_g3_bins(const uint32_t* __restrict__ keys, const int32_t* __restrict__ ctr, int32_t* __restrict__ lo,
+                          int32_t* __restrict__ hi) {
+  const int U = ctr[C_U];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < U; i += gridDim.x * blockDim.x) {
+    const uint32_t k = keys[i];
+    if (i == 0 || keys[i - 1] != k) lo[k] = i;
+    if (i == U - 1 || keys[i + 1] != k) hi[k] = i + 1;
+  }
+}
+
+// dG3[t][i3] = sum of the dD partials of the rows of (t, i3), in row order
+__global__ void __launch_bounds__(GRED_THREADS) k_gred_g3(const int32_t* __restrict__ lo,
+                                                          const int32_t* __restrict__ hi,
+                                                          const uint32_t* __restrict__ rows,
+                                                          const float* __restrict__ dDpart, int RD,
+                                                          float* __restrict__ dG3, float lr, bool update) {
+  const int b = blockIdx.x;
+  const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
+  if (e >= RD) return;
+  const int k0 = lo[b], k1 = hi[b];
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  int k = k0;
+  for (; k + 4 <= k1; k += 4)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] += dDpart[(int64_t)rows[k + q] * RD + e];
+  for (; k < k1; ++k) a[(k - k0) & 3] += dDpart[(int64_t)rows[k] * RD + e];
+  put_g(dG3, (int64_t)b * RD + e, (a[0] + a[1]) + (a[2] + a[3]), lr, update);
+}
+
+static int bits_of(uint64_t x) {
+  int b = 0;
+  while (x) {
+    ++b;
+    x >>= 1;
+  }
+  return b;
+}
+
+// The three segment sums of the generic backward (M sorted occurrences bound the rows).
+static hipError_t launch_generic_reduce(const Shape& s, const Work& w, int64_t M, float* dG1, float* dG2, float* dG3,
+                                        float lr, bool update, hipStream_t st) {
+  const int d1R = s.d1 * s.R, nB = s.R * s.d2 * s.R, RD = s.R * s.d3;
+  const int n = (int)M;
+  const uint32_t nbins = (uint32_t)s.T * (uint32_t)s.n3;
+  hipLaunchKernelGGL(k_g3_keys, dim3((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096), dim3(256), 0, st,
+                     shape_args(s), (const uint32_t*)w.uniq_key, (const int32_t*)w.ctr, n, nbins, w.g3keys[0],
+                     w.g3vals[0]);
+  int res = 0;
+  hipError_t e = sort_pairs(w, w.g3keys, w.g3vals, n, bits_of(nbins), &res, st);
+  if (e != hipSuccess) return e;
+  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.g3lo), nbins, 0u, st)) != hipSuccess) return e;
+  if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.g3hi), nbins, 0u, st)) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_g3_bins, dim3((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096), dim3(256), 0, st,
+                     (const uint32_t*)w.g3keys[res], (const int32_t*)w.ctr, w.g3lo, w.g3hi);
+  hipLaunchKernelGGL(k_gred_g3, dim3(nbins, (RD + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
+                     (const int32_t*)w.g3lo, (const int32_t*)w.g3hi, (const uint32_t*)w.g3vals[res],
+                     (const float*)w.dDpart, RD, dG3, lr, update);
+  hipLaunchKernelGGL(k_gred_g1, dim3(s.T * s.n1, (d1R + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
+                     shape_args(s), (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base,
+                     (const float*)w.dApart, dG1, lr, update);
+  hipLaunchKernelGGL(k_gred_g2, dim3(s.T * s.n2, (nB + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
+                     (const uint32_t*)w.run_nch, (const float*)w.dBpart, nB, dG2, lr, update);
+  return hipGetLastError();
 }
 
 hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
@@ -522,32 +676,19 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                            float* dG3, float lr, bool update, const Prof& prof, hipStream_t st) {
   (void)offsets;
   (void)B;
-  const int64_t n1s = (int64_t)s.T * s.n1 * s.d1 * s.R;
-  const int64_t n2s = (int64_t)s.T * s.n2 * s.R * s.d2 * s.R;
-  const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
   hipError_t e;
   const bool fast = bwd_r32_supported(s, w.M);
-  // fused update: the MFMA path applies it in its reductions (dG1..dG3 are the
-  // cores); the generic path sums into the workspace's gradient scratch and then
-  // runs the update
-  float* G1u = dG1;
-  float* G2u = dG2;
-  float* G3u = dG3;
-  if (update) {
-    if (M <= 0) return hipSuccess;  // zero gradients: the update leaves the cores as they are
-    if (!fast) {
-      if (!w.gscratch) return hipErrorInvalidValue;
-      dG1 = w.gscratch;
-      dG2 = dG1 + n1s;
-      dG3 = dG2 + n2s;
-    }
-  }
-  if (!fast || M <= 0) {
+  // With update set, dG1..dG3 are the cores themselves: both paths apply the update
+  // in their final segment sums, after the fused kernel has read the cores.
+  if (M <= 0) {
+    if (update) return hipSuccess;  // zero gradients: the update leaves the cores as they are
+    const int64_t n1s = (int64_t)s.T * s.n1 * s.d1 * s.R;
+    const int64_t n2s = (int64_t)s.T * s.n2 * s.R * s.d2 * s.R;
+    const int64_t n3s = (int64_t)s.T * s.n3 * s.R * s.d3;
     if ((e = fill_f32(dG1, n1s, 0.f, st)) != hipSuccess) return e;
     if ((e = fill_f32(dG2, n2s, 0.f, st)) != hipSuccess) return e;
-    if ((e = fill_f32(dG3, n3s, 0.f, st)) != hipSuccess) return e;
+    return fill_f32(dG3, n3s, 0.f, st);
   }
-  if (M <= 0) return hipSuccess;
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
   prof_begin(prof, K_SEG_SUM, st);
@@ -564,6 +705,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   hipLaunchKernelGGL(k_seg_fix, dim3((nseg + FIX_SCREEN - 1) / FIX_SCREEN), dim3(64 * FIX_WAVES), 0, st, (const int32_t*)w.sorted_uid, (const int32_t*)w.occ_start,
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, lr, update, prof, st);
+  if (!w.dDpart || !w.g3lo) return hipErrorInvalidValue;
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
     return e;
@@ -581,17 +723,16 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   if (wide)
     hipLaunchKernelGGL(k_bwd_generic<1024>, dim3(grid), dim3(1024), lds, st, shape_args(s), G1, G2, G3,
                        (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
-                       pl.stage_b, pl.db_lds, pl.rows);
+                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, w.dApart, w.dBpart, w.dDpart, w.ckpt,
+                       w.ckpt_tag, pl.stage_b, pl.db_lds, pl.rows);
   else
     hipLaunchKernelGGL(k_bwd_generic<256>, dim3(grid), dim3(256), lds, st, shape_args(s), G1, G2, G3,
                        (const int4*)w.slices, (const int4*)w.chunks, (const uint32_t*)w.run_nch,
-                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, dG1, dG2, dG3, w.ckpt, w.ckpt_tag,
-                       pl.stage_b, pl.db_lds, pl.rows);
+                       (const int32_t*)w.uniq_i3, w.ctr, (const float*)dE, w.dApart, w.dBpart, w.dDpart, w.ckpt,
+                       w.ckpt_tag, pl.stage_b, pl.db_lds, pl.rows);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  if (update) return launch_sgd(s, G1u, G2u, G3u, dG1, dG2, dG3, lr, st);
-  return hipSuccess;
+  return launch_generic_reduce(s, w, M, dG1, dG2, dG3, lr, update, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -103,10 +103,17 @@ struct Work {
   int32_t* slice_i1;      // [nsl_max] first digit i1 of each slice's group
   uint32_t* run_nch;      // [T*n2 + 1] chunks per (t, i2) run, then their exclusive scan
   int4* chunks;           // [nch_max] (first slice, slice count, run, 0)
-  float* dApart;          // [2][nsl_max][d1*R] backward: dA of each slice, per rank half
-  float* dBpart;          // [2][nch_max][R*d2*R/2] backward: dB of each chunk, per rank half
+  float* dApart;          // backward: dA of each slice, [2][nsl_max][d1*R] (MFMA: one per rank half) or
+                          // [nsl_max][d1*R] (generic)
+  float* dBpart;          // backward: dB of each chunk, [2][nch_max][R*d2*R/2] (MFMA) or [nch_max][R*d2*R]
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
-  float* gscratch;        // gradients of the fused backward-and-SGD call on the generic path (core-sized), else null
+  // generic backward (shapes the MFMA backward does not serve), else null: partials of
+  // the fixed-order segment sums and the (table, i3) order of the unique rows
+  float* dDpart;          // [M][R*d3] dD of each unique row
+  uint32_t* g3keys[2];    // [M] sort keys t*n3 + i3 of the unique rows (ping-pong)
+  uint32_t* g3vals[2];    // [M] unique row ids (ping-pong)
+  int32_t* g3lo;          // [T*n3] first position of each (t, i3) in the sorted rows
+  int32_t* g3hi;          // [T*n3] one past its last
   float* g1m;             // L >= 4: merged first core [T][n1][d1][R] of the view; L = 2: identity middle core
                           // [T][1][R][1][R]; null for L = 3
   float* dg1m;            // gradient of g1m (same size; for L = 2 computed and discarded)
@@ -174,6 +181,11 @@ bool bwd_r32_supported(const Shape& s, int64_t max_indices);
 // Whether the MFMA forward serves this shape (R = 32, R = 64).
 bool fwd_r32_supported(const Shape& s, int64_t max_indices);
 bool fwd_r64_supported(const Shape& s, int64_t max_indices);
+
+// Stable radix sort of n pairs between keys[0..1] / vals[0..1] (input in index 0); *out
+// = the index holding the result (group.hip).
+hipError_t sort_pairs(const Work& w, uint32_t* const keys[2], uint32_t* const vals[2], int n, int key_bits,
+                      int* out, hipStream_t st);
 
 // Small generic kernels shared across units (defined in group.hip).
 hipError_t fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t st);

@@ -817,6 +817,38 @@ static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntile
   return hipGetLastError();
 }
 
+// Stable LSD radix sort of n (key, value) pairs of key_bits-bit keys between the
+// ping-pong buffers keys[0..1] / vals[0..1] (input in [0]), with the grouping's
+// radix count and total buffers as scratch (the grouping no longer reads them).
+// *out receives the buffer index that holds the result.
+hipError_t sort_pairs(const Work& w, uint32_t* const keys[2], uint32_t* const vals[2], int n, int key_bits,
+                      int* out, hipStream_t st) {
+  const int npasses = sort_passes(key_bits < 1 ? 1 : key_bits);
+  const int dbits = (key_bits + npasses - 1) / npasses;
+  const int bits = dbits < 8 ? 8 : dbits;
+  const int ntiles = (n + SORT_TILE - 1) / SORT_TILE;
+  Work v = w;
+  int cur = 0;
+  for (int p = 0; p < npasses && n > 0; ++p) {
+    v.keys[0] = keys[0];
+    v.keys[1] = keys[1];
+    v.vals[0] = vals[0];
+    v.vals[1] = vals[1];
+    uint32_t* tot = w.rtotals + p * (1 << bits);
+    hipError_t e;
+    switch (bits) {
+      case 8: e = radix_pass<8>(v, cur, n, p * dbits, ntiles, tot, st); break;
+      case 9: e = radix_pass<9>(v, cur, n, p * dbits, ntiles, tot, st); break;
+      case 10: e = radix_pass<10>(v, cur, n, p * dbits, ntiles, tot, st); break;
+      default: e = radix_pass<11>(v, cur, n, p * dbits, ntiles, tot, st); break;
+    }
+    if (e != hipSuccess) return e;
+    cur ^= 1;
+  }
+  *out = cur;
+  return hipGetLastError();
+}
+
 hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64_t M, const int64_t* offsets,
                         int64_t B, const Prof& prof, hipStream_t st) {
   // passes of equal width, at most RADIX_MAX_BITS bits each

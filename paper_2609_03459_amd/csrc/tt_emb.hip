@@ -109,12 +109,18 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   if (fwd_end) *fwd_end = off;
   // --- regions of the backward only ---
   W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
-  W->dApart = bwd_r32 ? (float*)take(4 * (size_t)2 * nsl_max * s.d1 * s.R) : nullptr;
-  W->dBpart = bwd_r32 ? (float*)take(4 * (size_t)2 * nch_max * (s.R * s.d2 * s.R / 2)) : nullptr;
+  // gradient partials: the MFMA backward's rank halves, or the generic backward's
+  // per-slice dA, per-chunk dB and per-row dD with the (t, i3) order of the rows
+  W->dApart = (float*)take(4 * (size_t)(bwd_r32 ? 2 : 1) * nsl_max * s.d1 * s.R);
+  W->dBpart = (float*)take(4 * (size_t)nch_max * s.R * s.d2 * s.R);
   W->g3part = bwd_r32 ? (float*)take(4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2)) : nullptr;
-  const size_t ncore = (size_t)s.T * ((size_t)s.n1 * s.d1 * s.R + (size_t)s.n2 * s.R * s.d2 * s.R +
-                                      (size_t)s.n3 * s.R * s.d3);
-  W->gscratch = bwd_r32 ? nullptr : (float*)take(4 * ncore);
+  W->dDpart = bwd_r32 ? nullptr : (float*)take(4 * (size_t)m * s.R * s.d3);
+  for (int k = 0; k < 2; ++k) {
+    W->g3keys[k] = bwd_r32 ? nullptr : (uint32_t*)take(4 * m);
+    W->g3vals[k] = bwd_r32 ? nullptr : (uint32_t*)take(4 * m);
+  }
+  W->g3lo = bwd_r32 ? nullptr : (int32_t*)take(4 * (size_t)s.T * s.n3);
+  W->g3hi = bwd_r32 ? nullptr : (int32_t*)take(4 * (size_t)s.T * s.n3);
   W->dg1m = nmerged ? (float*)take(4 * nmerged) : nullptr;
   W->dxlev = nlev ? (float*)take(4 * nlev) : nullptr;
   const int par = sort_passes(s.key_bits) & 1;

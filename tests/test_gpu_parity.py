@@ -255,6 +255,22 @@ def test_full_size_sampled_bags(lib, orc, cfg):
     check_forward(lib, orc, case, bags=bags, name=f"config{cfg} full, 96 sampled bags")
 
 
+@pytest.mark.parametrize("k", [1, 5, 7])
+def test_generic_backward_deterministic(lib, k):
+    # the generic backward reduces its partials by fixed-order segment sums: two runs
+    # (fresh handles and workspaces, so the scheduling differs) give the same bits
+    c = dict(TINY[k])
+    case = ttgen.tiny(3500 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    _say(f"[bwd determinism] tiny{k}")
+    runs = []
+    for _ in range(2):
+        emb, G, grads, dV = gpu_train(lib, case)
+        assert not lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], case["idx"].size)
+        runs.append([g.cpu().numpy() for g in grads])
+    for a, b in zip(*runs):
+        assert np.array_equal(a, b)
+
+
 def test_forward_deterministic(lib):
     case = ttgen.make(3, bags=512)
     _say("[fwd] determinism config3 B=512")
