@@ -258,10 +258,9 @@ tt_emb_status tt_emb_backward_sgd(tt_emb_handle h, float* G1, float* G2, float* 
  * and the three-core operator runs on it and cores L-2, L-1:
  * C = (merged slice) . S_{L-2} once per prefix group of the first L-1 digits,
  * E = C . S_{L-1} per unique row.  The backward carries the merged core's
- * gradient back through the chain one level at a time into cores 0..L-3; each
- * level's blocks add their chunk sums into those gradients with global float
- * atomics.  For L = 2 the middle core of the three-core operator is the
- * identity.  Grouping,
+ * gradient back through the chain one level at a time into cores 0..L-3, each
+ * level as per-block partials summed in a fixed order (no atomics).  For L = 2
+ * the middle core of the three-core operator is the identity.  Grouping,
  * reuse levels, schedules, errors and tt_emb_debug_grouping work as above on
  * the three-factor view (n_0...n_{L-3}, n_{L-2}, n_{L-1}) for L >= 4 and
  * (n_0, 1, n_1) for L = 2: its digits and prefix keys are those of the view.

@@ -119,6 +119,7 @@ struct Work {
   float* dg1m;            // gradient of g1m (same size; for L = 2 computed and discarded)
   float* xlev;            // L >= 5: partial products of the merged cores' inner levels, chain_level_floats(s)
   float* dxlev;           // L >= 5: their gradients (same size)
+  float* splitpart;       // L >= 4: partials of one backward level of the merged chain, split_partial_floats(s)
   float* ckpt;            // [CKPT_SLOTS][d1*d2*R] checkpointed C of the generic kernels (null for the MFMA shape)
   int32_t* ckpt_tag;      // [CKPT_SLOTS] prefix group held by each entry, -1 = none
   int64_t nsl_max, nch_max;
@@ -174,6 +175,8 @@ hipError_t launch_identity(const Shape& s, const Work& w, hipStream_t st);
 int64_t core_elems(const Shape& s, int k);
 // Floats of the inner partial-product levels of the merged cores (0 when L < 5).
 int64_t chain_level_floats(const Shape& s);
+// Floats of the largest level's partials in the backward of the merged chain (0 when L < 4).
+int64_t split_partial_floats(const Shape& s);
 // G -= lr * dG on n floats.
 hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.

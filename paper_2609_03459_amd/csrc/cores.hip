@@ -112,15 +112,15 @@ __global__ void __launch_bounds__(LV_THREADS) k_merge_level(LevelArgs a, int pc,
 
 // One backward level k of the merged chain.  Block (t, c, chunk) takes child c of
 // core k and a chunk of pc consecutive parents p; with X = X_{k-1}(t, p) and
-// dX = dX_k(t, p n_k + c) staged in LDS it adds
-//     X^T . dX              into dS_k(t, c)        (summed over the chunk first)
-//     dX . S_k(t, c)^T      into dX_{k-1}(t, p)    (one partial per child)
-// with atomics into zeroed outputs; zero partials are not added.
+// dX = dX_k(t, p n_k + c) staged in LDS it writes
+//     X^T . dX              summed over the chunk: the (t, c, chunk) partial of dS_k(t, c)
+//     dX . S_k(t, c)^T      for each parent: the (t, p, c) partial of dX_{k-1}(t, p)
+// No two blocks write one partial; k_split_sum adds them in a fixed order.
 __global__ void __launch_bounds__(LV_THREADS) k_split_level(LevelArgs a, int pc, int stage_s,
                                                             const float* __restrict__ Xprev,
                                                             const float* __restrict__ dXk,
-                                                            const float* __restrict__ Sk, float* __restrict__ dSk,
-                                                            float* __restrict__ dXprev) {
+                                                            const float* __restrict__ Sk, float* __restrict__ partS,
+                                                            float* __restrict__ partX) {
   extern __shared__ float lds[];
   const int64_t nchunk = (a.P + pc - 1) / pc;
   const int64_t tc = blockIdx.x / nchunk;  // t * n_k + c
@@ -147,16 +147,16 @@ __global__ void __launch_bounds__(LV_THREADS) k_split_level(LevelArgs a, int pc,
     }
   __syncthreads();
   const int rows = np * a.mprev;
-  float* gS = dSk + tc * a.R * a.cols;
+  float* gS = partS + blockIdx.x * (int64_t)a.R * a.cols;  // blockIdx.x = tc * nchunk + chunk
   for (int o = threadIdx.x; o < a.R * a.cols; o += LV_THREADS) {
     const int b = o / a.cols, col = o - b * a.cols;
     float acc = 0.f;
     for (int r = 0; r < rows; ++r) acc = fmaf(Xs[r * a.R + b], dXs[r * a.cols + col], acc);
-    if (acc != 0.f) unsafeAtomicAdd(&gS[o], acc);
+    gS[o] = acc;
   }
-  float* gX = dXprev + (t * a.P + p0) * xl;
   for (int o = threadIdx.x; o < rows * a.R; o += LV_THREADS) {
     const int r = o / a.R, b = o - r * a.R;
+    const int pp = r / a.mprev, rr = r - pp * a.mprev;
     const float* d = dXs + r * a.cols;
     float acc = 0.f;
     if (stage_s) {
@@ -166,8 +166,58 @@ __global__ void __launch_bounds__(LV_THREADS) k_split_level(LevelArgs a, int pc,
       const float* sr = S + b * a.cols;
       for (int col = 0; col < a.cols; ++col) acc = fmaf(d[col], sr[col], acc);
     }
-    if (acc != 0.f) unsafeAtomicAdd(&gX[o], acc);
+    partX[((t * a.P + p0 + pp) * a.nk + ch) * xl + rr * a.R + b] = acc;
   }
+}
+
+// dS_k(t, c) = sum over the parent chunks of their partials (chunk order), and
+// dX_{k-1}(t, p) = sum over the children c of their partials (c ascending): one
+// thread per output element, elements [0, nS) of dS_k then [0, nX) of dX_{k-1}.
+__global__ void __launch_bounds__(LV_THREADS) k_split_sum(LevelArgs a, int64_t nchunk,
+                                                          const float* __restrict__ partS,
+                                                          const float* __restrict__ partX, float* __restrict__ dSk,
+                                                          float* __restrict__ dXprev) {
+  const int64_t RC = (int64_t)a.R * a.cols, xl = (int64_t)a.mprev * a.R;
+  const int64_t nS = (int64_t)a.T * a.nk * RC, nX = (int64_t)a.T * a.P * xl;
+  for (int64_t o = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; o < nS + nX; o += (int64_t)gridDim.x * blockDim.x) {
+    float acc = 0.f;
+    if (o < nS) {
+      const int64_t tc = o / RC, e = o - tc * RC;
+      for (int64_t j = 0; j < nchunk; ++j) acc += partS[(tc * nchunk + j) * RC + e];
+      dSk[o] = acc;
+    } else {
+      const int64_t x = o - nS;
+      const int64_t tp = x / xl, w = x - tp * xl;
+      for (int c = 0; c < a.nk; ++c) acc += partX[(tp * a.nk + c) * xl + w];
+      dXprev[x] = acc;
+    }
+  }
+}
+
+// Parents per block of the split of level k: their X and dX rows within 32 KB of
+// LDS, and whether S_k(t, c) (padded rows) is staged too (16 KB more).
+static void split_plan(const Shape& s, int k, int64_t* pc_out, int* stage_out) {
+  const LevelArgs a = level_args(s, k);
+  const int64_t per = (int64_t)a.mprev * (a.R + a.cols);
+  int64_t pc = 8192 / per;
+  if (pc < 1) pc = 1;
+  if (pc > a.P) pc = a.P;
+  *pc_out = pc;
+  *stage_out = (int64_t)a.R * (a.cols + 1) <= 4096;
+}
+
+int64_t split_partial_floats(const Shape& s) {
+  int64_t most = 0;
+  for (int k = 1; k <= s.L - 3; ++k) {
+    const LevelArgs a = level_args(s, k);
+    int64_t pc;
+    int st;
+    split_plan(s, k, &pc, &st);
+    const int64_t nchunk = (a.P + pc - 1) / pc;
+    const int64_t n = (int64_t)a.T * a.nk * nchunk * a.R * a.cols + (int64_t)a.T * a.P * a.nk * a.mprev * a.R;
+    if (n > most) most = n;
+  }
+  return most;
 }
 
 __global__ void k_identity(float* __restrict__ G, int T, int R) {
@@ -211,32 +261,34 @@ hipError_t launch_merge(const Shape& s, const Work& w, const float* const* cores
 
 hipError_t launch_split(const Shape& s, const Work& w, const float* const* cores, float* const* grads,
                         const Prof& prof, hipStream_t st) {
-  if (s.L < 4 || !w.g1m || !w.dg1m || (s.L >= 5 && (!w.xlev || !w.dxlev))) return hipErrorInvalidValue;
+  if (s.L < 4 || !w.g1m || !w.dg1m || !w.splitpart || (s.L >= 5 && (!w.xlev || !w.dxlev)))
+    return hipErrorInvalidValue;
   hipError_t e;
-  for (int k = 0; k <= s.L - 3; ++k)
-    if ((e = fill_f32(grads[k], core_elems(s, k), 0.f, st)) != hipSuccess) return e;
-  const int64_t nlev = chain_level_floats(s);
-  if (nlev && (e = fill_f32(w.dxlev, nlev, 0.f, st)) != hipSuccess) return e;
   prof_begin(prof, K_SPLIT, st);
   for (int k = s.L - 3; k >= 1; --k) {
     const LevelArgs a = level_args(s, k);
     const float* Xprev = k == 1 ? cores[0] : level_x(s, w, k - 1);
     const float* dXk = k == s.L - 3 ? w.dg1m : w.dxlev + level_offset(s, k);
     float* dXprev = k == 1 ? grads[0] : w.dxlev + level_offset(s, k - 1);
-    // parents per block: their X and dX rows within 32 KB of LDS; S_k(t, c)
-    // (padded rows) staged too when it fits in 16 KB more
+    int64_t pc;
+    int stage_s;
+    split_plan(s, k, &pc, &stage_s);
     const int64_t per = (int64_t)a.mprev * (a.R + a.cols);
-    int64_t pc = 8192 / per;
-    if (pc < 1) pc = 1;
-    if (pc > a.P) pc = a.P;
-    const int stage_s = (int64_t)a.R * (a.cols + 1) <= 4096;
     const size_t lds = sizeof(float) * (size_t)(pc * per + (stage_s ? a.R * (a.cols + 1) : 0));
     if ((e = hipFuncSetAttribute((const void*)k_split_level, hipFuncAttributeMaxDynamicSharedMemorySize,
                                  (int)lds)) != hipSuccess)
       return e;
-    const int64_t blocks = (int64_t)a.T * a.nk * ((a.P + pc - 1) / pc);
+    const int64_t nchunk = (a.P + pc - 1) / pc;
+    const int64_t blocks = (int64_t)a.T * a.nk * nchunk;
+    float* partS = w.splitpart;
+    float* partX = partS + blocks * a.R * a.cols;
     hipLaunchKernelGGL(k_split_level, dim3((unsigned)blocks), dim3(LV_THREADS), lds, st, a, (int)pc, stage_s, Xprev,
-                       dXk, (const float*)cores[k], grads[k], dXprev);
+                       dXk, (const float*)cores[k], partS, partX);
+    const int64_t nout = (int64_t)a.T * a.nk * a.R * a.cols + (int64_t)a.T * a.P * a.mprev * a.R;
+    int64_t sb = (nout + LV_THREADS - 1) / LV_THREADS;
+    if (sb > 8192) sb = 8192;
+    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)sb), dim3(LV_THREADS), 0, st, a, nchunk, (const float*)partS,
+                       (const float*)partX, grads[k], dXprev);
   }
   prof_end(prof, K_SPLIT, st);
   return hipGetLastError();

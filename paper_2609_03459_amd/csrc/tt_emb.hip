@@ -123,6 +123,8 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   W->g3hi = bwd_r32 ? nullptr : (int32_t*)take(4 * (size_t)s.T * s.n3);
   W->dg1m = nmerged ? (float*)take(4 * nmerged) : nullptr;
   W->dxlev = nlev ? (float*)take(4 * nlev) : nullptr;
+  const size_t nsplit = (size_t)split_partial_floats(s);
+  W->splitpart = nsplit ? (float*)take(4 * nsplit) : nullptr;
   const int par = sort_passes(s.key_bits) & 1;
   W->sorted_keys = W->keys[par];
   W->sorted_pos = W->vals[par];

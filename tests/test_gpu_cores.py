@@ -267,6 +267,25 @@ def _sampled_slices_n(case, tables, seed):
     return want
 
 
+@pytest.mark.parametrize("n,d,R", [((3, 4, 5, 6), (2, 1, 2, 2), 5), ((2, 3, 2, 4, 5), (1, 2, 2, 1, 3), 4)])
+def test_gradients_n_deterministic(lib, n, d, R):
+    # every gradient of a generic view is a fixed-order sum (segment sums in the view's
+    # backward, chunk and child partials in the split): two runs give the same bits
+    case = ttgen.tiny_n(7650 + len(n), 2, n, d, R, 40, max_len=6, zipf=1.1)
+    _say(f"[cores determinism] L={len(n)} n={n} d={d} R={R}")
+    runs = []
+    for _ in range(2):
+        emb = _make(lib, case)
+        cores, idx, off = _dev(case)
+        dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+        emb.forward_n(cores, idx, off, num_bags=case["B"])
+        grads = emb.backward_n(cores, idx, off, dV, num_bags=case["B"])
+        torch.cuda.synchronize()
+        runs.append([g.cpu().numpy() for g in grads])
+    for k, (a, b) in enumerate(zip(*runs)):
+        assert np.array_equal(a, b), k
+
+
 def test_autograd_module_n(lib, orc):
     case = ttgen.tiny_n(7600, 2, (5, 4, 20, 30), (2, 2, 4, 8), 32, 60, max_len=12, zipf=1.1)
     _say("[cores autograd] L=4 n=(5,4,20,30) d=(2,2,4,8) R=32")
