@@ -131,8 +131,8 @@ def algorithmic_work(kernel, case, counts):
         return P * 6.0 * d1 * d2 * R * R + U * 4.0 * D * R, "flop", "mfma"
     if kernel == "pool":
         return 4.0 * M + 8.0 * (NB + 1) + 4.0 * NB * D + 4.0 * U * D, "byte", "hbm"
-    if kernel == "seg_sum":
-        return 4.0 * NB * D + 4.0 * U * D + 12.0 * nv + 4.0 * (U + 1), "byte", "hbm"
+    if kernel == "seg_sum":  # dV rows read once, dE rows written, row id and bag per sorted occurrence
+        return 4.0 * NB * D + 4.0 * U * D + 8.0 * nv + 4.0 * (U + 1), "byte", "hbm"
     if kernel == "ingest":
         return 8.0 * M + 8.0 * (NB + 1) + 12.0 * M, "byte", "hbm"
     (n1, _, _), _ = view_dims(case["n"], case["d"])

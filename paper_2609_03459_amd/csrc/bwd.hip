@@ -71,6 +71,15 @@ __device__ __forceinline__ void seg_flush(const SegEnds& e, int cur, int c, int 
   }
 }
 
+// The bag of every sorted occurrence, gathered once through the sorted positions,
+// so that the dE sums read it in order instead of chasing two indices per row.
+__global__ void k_sorted_bag(const uint32_t* __restrict__ sorted_pos, const int32_t* __restrict__ bag_of,
+                             const int32_t* __restrict__ ctr, int32_t* __restrict__ sorted_bag) {
+  const int nvalid = ctr[C_NVALID];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nvalid; i += gridDim.x * blockDim.x)
+    sorted_bag[i] = bag_of[sorted_pos[i]];
+}
+
 // One wave per chunk of SEG_CHUNK sorted occurrences; lanes hold 4 columns
 // each (column blocks of 256); occurrence indices are fetched 64 at a time and
 // the grad_out rows of 8 occurrences are loaded before they are summed.
@@ -79,8 +88,7 @@ __device__ __forceinline__ void seg_flush(const SegEnds& e, int cur, int c, int 
 constexpr int SEG_WAVES = 4;
 
 __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
-                                               const uint32_t* __restrict__ sorted_pos,
-                                               const int32_t* __restrict__ bag_of,
+                                               const int32_t* __restrict__ sorted_bag,
                                                const int32_t* __restrict__ occ_start,
                                                const int32_t* __restrict__ ctr, int D, float* __restrict__ dE,
                                                float* __restrict__ part) {
@@ -101,7 +109,7 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restri
     for (int base = ib; base < ie; base += 64) {
       const int i = base + lane;
       const int my_u = i < ie ? sorted_uid[i] : -1;
-      const int my_b = i < ie ? bag_of[sorted_pos[i]] : 0;
+      const int my_b = i < ie ? sorted_bag[i] : 0;
       const int cnt = ie - base < 64 ? ie - base : 64;
       for (int k0 = 0; k0 < cnt; k0 += 8) {
         float v[8][4];
@@ -139,8 +147,7 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restri
 // Chunks go in sorted order, an eighth of them per XCD, so each XCD reads the
 // grad_out rows and bag ids of about one table, and more of them hit its L2.
 __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
-                                                  const uint32_t* __restrict__ sorted_pos,
-                                                  const int32_t* __restrict__ bag_of,
+                                                  const int32_t* __restrict__ sorted_bag,
                                                   const int32_t* __restrict__ occ_start,
                                                   const int32_t* __restrict__ ctr, float* __restrict__ dE,
                                                   float* __restrict__ part) {
@@ -160,7 +167,7 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __res
   for (int base = ib; base < ie; base += 64) {
     const int i = base + lane;
     const int my_u = i < ie ? sorted_uid[i] : -1;
-    const int my_b = i < ie ? bag_of[sorted_pos[i]] : 0;
+    const int my_b = i < ie ? sorted_bag[i] : 0;
     const int cnt = ie - base < 64 ? ie - base : 64;
     for (int k0 = 0; k0 < cnt; k0 += 16) {
       float2 v[16];
@@ -691,14 +698,17 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   }
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
+  hipLaunchKernelGGL(k_sorted_bag, dim3((M + 255) / 256 < 8192 ? (unsigned)((M + 255) / 256) : 8192u), dim3(256), 0,
+                     st, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.ctr,
+                     w.sorted_bag);
   prof_begin(prof, K_SEG_SUM, st);
   if (s.D == 128) {
     hipLaunchKernelGGL(k_seg_dE128, dim3(xcd_grid((nseg + SEG_WAVES - 1) / SEG_WAVES)), dim3(64 * SEG_WAVES), 0, st,
-                       dV, (const int32_t*)w.sorted_uid, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of,
+                       dV, (const int32_t*)w.sorted_uid, (const int32_t*)w.sorted_bag,
                        (const int32_t*)w.occ_start, (const int32_t*)w.ctr, dE, w.seg_part);
   } else {
     hipLaunchKernelGGL(k_seg_dE, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,
-                       (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.occ_start,
+                       (const int32_t*)w.sorted_bag, (const int32_t*)w.occ_start,
                        (const int32_t*)w.ctr, s.D, dE, w.seg_part);
   }
   prof_end(prof, K_SEG_SUM, st);

@@ -91,6 +91,7 @@ struct Work {
   int32_t* bag_of;        // [M] global bag of each occurrence
   int32_t* inv;           // [M] unique id of each occurrence (-1 invalid)
   int32_t* sorted_uid;    // [M] unique id of each sorted occurrence
+  int32_t* sorted_bag;    // [M] backward: global bag of each sorted occurrence
   uint32_t* uniq_key;     // [M] key of each unique row
   int32_t* uniq_i3;       // [M] last digit i3 of each unique row
   int32_t* occ_start;     // [M+1] first sorted position of each unique row

@@ -109,6 +109,7 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   if (fwd_end) *fwd_end = off;
   // --- regions of the backward only ---
   W->seg_part = (float*)take(4 * (size_t)nseg * 2 * s.D);
+  W->sorted_bag = (int32_t*)take(4 * m);
   // gradient partials: the MFMA backward's rank halves, or the generic backward's
   // per-slice dA, per-chunk dB and per-row dD with the (t, i3) order of the rows
   W->dApart = (float*)take(4 * (size_t)(bwd_r32 ? 2 : 1) * nsl_max * s.d1 * s.R);
