@@ -11,7 +11,8 @@ import os
 import re
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libttemb.so")
+# TT_EMB_LIB names another build of the same library (the sanitizer test's host build)
+LIB_PATH = os.environ.get("TT_EMB_LIB") or os.path.join(HERE, "libttemb.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "tt_emb.h")
 
 TT_EMB_OK, TT_EMB_EINVAL, TT_EMB_ENOMEM, TT_EMB_EHIP, TT_EMB_ERANGE, TT_EMB_EUNSUPPORTED, TT_EMB_ESCRATCH = range(7)
