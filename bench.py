@@ -68,7 +68,7 @@ class HipEvents:
 # of a kernel stay valid while these files are unchanged).
 KERNEL_SOURCES = {
     # the fused kernels' work units (slices, chunks) are cut by the grouping, sized in tt_emb.hip
-    "bwd_fused": ["bwd_r32.hip", "common.h", "group.hip", "tt_emb.hip"],
+    "bwd_fused": ["bwd_r32.hip", "bwd_r64.hip", "common.h", "group.hip", "tt_emb.hip"],
     "fwd_fused": ["fwd.hip", "common.h", "group.hip", "tt_emb.hip"],
     "pool": ["fwd.hip", "common.h"],
     "seg_sum": ["bwd.hip", "common.h"],
@@ -148,10 +148,12 @@ KERNEL_SYMBOL = {"fwd_fused": "k_fwd_r32", "bwd_fused": "k_bwd_r32", "pool": "k_
 
 
 def kernel_symbol(kernel, R=32):
-    """Symbol of the MFMA kernel that serves `kernel` at rank R (the forward has one
-    for R = 32 and one for R = 64)."""
+    """Symbol of the MFMA kernel that serves `kernel` at rank R (the forward and the
+    backward have one for R = 32 and one for R = 64)."""
     if kernel == "fwd_fused" and R == 64:
         return "k_fwd_r64"
+    if kernel == "bwd_fused" and R == 64:
+        return "k_bwd_r64"
     return KERNEL_SYMBOL[kernel]
 
 

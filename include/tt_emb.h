@@ -125,9 +125,9 @@ tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level);
  *                            worker takes a fixed contiguous share of the
  *                            groups.
  * The checkpoint applies to the kernels that keep one C per worker (the
- * generic kernels); the MFMA kernels (forward for d = (4,4,8) with R = 32 or
- * 64, backward for d = (4,4,8) with R = 32) build C for four slices per
- * matrix-core tile and treat STEAL_CKPT as STEAL.  All
+ * generic kernels); the MFMA kernels (forward and backward for d = (4,4,8)
+ * with R = 32 or 64) build C for four slices per matrix-core tile and treat
+ * STEAL_CKPT as STEAL.  All
  * modes compute the same function.  Host only; may be changed between calls,
  * except that TT_EMB_SCHED_GROUP cuts the work list in the grouping and needs a
  * larger workspace: set it before tt_emb_workspace_size, and a grouping made
@@ -204,14 +204,14 @@ tt_emb_status tt_emb_forward_noalloc(tt_emb_handle h, const float* G1, const flo
  * The per-core gradients are reduced by segments, with no global float
  * atomics: dG1 is a fixed-order sum of per-slice partials over the slices of
  * each (table, i1), dG2 of per-chunk partials over the chunks of each
- * (table, i2).  dG3: on the MFMA shape (see tt_emb_kernel_uses_mfma) it is
- * summed in on-chip memory per (table, rank half) and workgroup, then over the
- * workgroups in a fixed order (the on-chip adds land in arrival order, so this
- * dG3 is reproducible to rounding, not bit for bit); on other shapes every
- * unique row's dD is a partial, the rows are put in (table, i3) order by a
- * stable sort, and each dG3 slice is the sum over its rows in that order, so
- * all three gradients are bit-reproducible there.  reuse_grouping as for
- * tt_emb_forward. */
+ * (table, i2).  dG3: on the R = 32 MFMA shape (see tt_emb_kernel_uses_mfma)
+ * it is summed in on-chip memory per (table, rank half) and workgroup, then
+ * over the workgroups in a fixed order (the on-chip adds land in arrival
+ * order, so this dG3 is reproducible to rounding, not bit for bit); on every
+ * other shape, the R = 64 MFMA shape included, every unique row's dD is a
+ * partial, the rows are put in (table, i3) order by a stable sort, and each
+ * dG3 slice is the sum over its rows in that order, so all three gradients
+ * are bit-reproducible there.  reuse_grouping as for tt_emb_forward. */
 tt_emb_status tt_emb_backward(tt_emb_handle h, const float* G1, const float* G2, const float* G3,
                               const int64_t* indices, int64_t num_indices, const int64_t* offsets,
                               int64_t num_bags, const float* grad_out, float* dG1, float* dG2, float* dG3,
@@ -345,9 +345,10 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
 
 /* Whether `kernel` (TT_EMB_K_FWD_FUSED or TT_EMB_K_BWD_FUSED) runs on the
  * matrix cores for this handle: *uses_mfma = 1 for the MFMA kernels (forward
- * for the view d = (4,4,8) with R = 32 or 64, backward for d = (4,4,8) with
- * R = 32, n3 <= 252 and at most 64 tables; both only while their 32-bit
- * offsets into E and the cores fit), 0 for the generic vector-ALU kernels.
+ * for the view d = (4,4,8) with R = 32 or 64; backward for d = (4,4,8) with
+ * R = 32, n3 <= 252 and at most 64 tables, or with R = 64; all only while
+ * their 32-bit offsets into E and the cores fit and, at R = 64, a table's
+ * third core spans under 4 GiB), 0 for the generic vector-ALU kernels.
  * Both decide per call from its index count, given here as num_indices
  * (0 <= num_indices <= desc.max_indices).  Every other kernel id reports 0.
  * Host only.

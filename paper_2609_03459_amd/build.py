@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libttemb.so")
-SOURCES = ["tt_emb.hip", "group.hip", "fwd.hip", "bwd.hip", "bwd_r32.hip", "cores.hip"]
+SOURCES = ["tt_emb.hip", "group.hip", "fwd.hip", "bwd.hip", "bwd_r32.hip", "bwd_r64.hip", "cores.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

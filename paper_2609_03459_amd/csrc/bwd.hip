@@ -12,6 +12,8 @@
 namespace ttemb {
 
 ShapeArgs shape_args(const Shape& s);
+hipError_t launch_bwd_r64(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
+                          const Prof& prof, hipStream_t st);
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           float* dG1, float* dG2, float* dG3, float lr, bool update, const Prof& prof,
                           hipStream_t st);
@@ -716,6 +718,10 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, lr, update, prof, st);
   if (!w.dDpart || !w.g3lo) return hipErrorInvalidValue;
+  if (bwd_r64_supported(s, w.M)) {  // MFMA partials, then the same segment sums
+    if ((e = launch_bwd_r64(s, w, G1, G2, G3, prof, st)) != hipSuccess) return e;
+    return launch_generic_reduce(s, w, M, dG1, dG2, dG3, lr, update, st);
+  }
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
     return e;

@@ -182,6 +182,9 @@ int64_t split_partial_floats(const Shape& s);
 hipError_t launch_sgd1(float* G, const float* dG, int64_t n, float lr, hipStream_t st);
 // Whether the MFMA backward (and its partial-sum workspace) serves this shape.
 bool bwd_r32_supported(const Shape& s, int64_t max_indices);
+// Whether the MFMA backward for R = 64 serves this shape (it writes the generic
+// backward's partials, so needs no workspace of its own).
+bool bwd_r64_supported(const Shape& s, int64_t max_indices);
 // Whether the MFMA forward serves this shape (R = 32, R = 64).
 bool fwd_r32_supported(const Shape& s, int64_t max_indices);
 bool fwd_r64_supported(const Shape& s, int64_t max_indices);
@@ -407,9 +410,6 @@ namespace ttemb {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Orders this wave's LDS writes before its later LDS reads of other lanes'
-// data (a wave's LDS requests complete in order; this keeps the compiler
-// from reordering across the exchange and waits for outstanding writes).
 // one of four wave-uniform values by a per-lane index
 template <typename T>
 __device__ __forceinline__ T sel4(int j, T a, T b, T c, T d) {
@@ -430,6 +430,9 @@ __device__ __forceinline__ float4 buf_f32x4(buf_t r, uint32_t off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+// Orders this wave's LDS writes before its later LDS reads of other lanes'
+// data (a wave's LDS requests complete in order; this keeps the compiler
+// from reordering across the exchange and waits for outstanding writes).
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();

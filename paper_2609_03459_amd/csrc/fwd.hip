@@ -759,10 +759,11 @@ hipError_t launch_pool(const Shape& s, const float* E, const int32_t* inv, const
 }
 
 bool fwd_r64_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit offsets into E (rows x 128), G1, G2 and G3
+  // 32-bit offsets into E (rows x 128), G1, G2 and G3; a table's G3 (n3 x 2,048 bytes) is
+  // one buffer descriptor's 32-bit range
   return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 64 && max_indices * 128 < (int64_t(1) << 31) &&
          (int64_t)s.T * s.n1 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n2 * 16384 < (int64_t(1) << 31) &&
-         (int64_t)s.T * s.n3 * 512 < (int64_t(1) << 31);
+         (int64_t)s.T * s.n3 * 512 < (int64_t(1) << 31) && (int64_t)s.n3 * 2048 < (int64_t(1) << 32);
 }
 
 bool fwd_r32_supported(const Shape& s, int64_t max_indices) {

@@ -307,7 +307,7 @@ tt_emb_status tt_emb_kernel_uses_mfma(tt_emb_handle h, int kernel, int64_t num_i
   if (num_indices < 0 || num_indices > h->desc.max_indices) return TT_EMB_EINVAL;
   bool m = false;
   if (kernel == TT_EMB_K_FWD_FUSED) m = fwd_r32_supported(h->s, num_indices) || fwd_r64_supported(h->s, num_indices);
-  if (kernel == TT_EMB_K_BWD_FUSED) m = bwd_r32_supported(h->s, num_indices);
+  if (kernel == TT_EMB_K_BWD_FUSED) m = bwd_r32_supported(h->s, num_indices) || bwd_r64_supported(h->s, num_indices);
   *uses_mfma = m ? 1 : 0;
   return TT_EMB_OK;
 }

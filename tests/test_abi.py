@@ -148,7 +148,7 @@ def test_reuse_levels_and_workspace(N):
 
 @pytest.mark.parametrize("n,d,R,M,num,fwd,bwd", [
     ((200, 200, 250), (4, 4, 8), 32, 1 << 20, 1 << 20, 1, 1),   # both MFMA kernels
-    ((400, 500, 500), (4, 4, 8), 64, 1 << 20, 1 << 20, 1, 0),   # MFMA forward, generic backward
+    ((400, 500, 500), (4, 4, 8), 64, 1 << 20, 1 << 20, 1, 1),   # both MFMA kernels at R = 64
     ((100, 100, 100), (4, 4, 4), 16, 1 << 20, 1 << 20, 0, 0),   # generic both ways
     ((6, 5, 252), (4, 4, 8), 32, 1000, 1000, 1, 1),             # the backward's LDS accumulator fills
     ((6, 5, 253), (4, 4, 8), 32, 1000, 1000, 1, 0),             # one row past it
@@ -172,6 +172,16 @@ def test_kernel_uses_mfma(N, n, d, R, M, num, fwd, bwd):
     assert N.lib.tt_emb_kernel_uses_mfma(h, 2, 0, None) == E
     assert N.lib.tt_emb_kernel_uses_mfma(None, 2, 0, C.byref(flag)) == E
     N.tt_emb_destroy(h)
+
+
+def test_r64_kernels_keep_one_tables_third_core_in_one_descriptor(N):
+    # at R = 64 a table's third core takes n3 x 2,048 bytes, addressed through one buffer
+    # descriptor of 32-bit extent: from n3 = 2^21 on the generic kernels serve
+    for n3, mfma in ((1 << 21, False), ((1 << 21) - 1, True)):
+        h = N.tt_emb_create(_desc(N, T=1, n=(1, 1, n3), d=(4, 4, 8), R=64, M=1000, B=10))
+        assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], 1000) == mfma
+        assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["bwd_fused"], 1000) == mfma
+        N.tt_emb_destroy(h)
 
 
 def _desc_n(N, L=4, T=2, n=(3, 4, 5, 2), d=(2, 2, 2, 1), R=4, M=100, B=10, rows=None):

@@ -80,6 +80,7 @@ def test_run_key_and_step_of_the_forward_only_workloads():
     assert bench.kernel_symbol("fwd_fused", 64) == "k_fwd_r64"
     assert bench.kernel_symbol("fwd_fused", 32) == "k_fwd_r32"
     assert bench.kernel_symbol("bwd_fused", 32) == "k_bwd_r32"
+    assert bench.kernel_symbol("bwd_fused", 64) == "k_bwd_r64"
 
 
 def _case8():

@@ -255,7 +255,7 @@ def test_full_size_sampled_bags(lib, orc, cfg):
     check_forward(lib, orc, case, bags=bags, name=f"config{cfg} full, 96 sampled bags")
 
 
-@pytest.mark.parametrize("k", [1, 5, 7])
+@pytest.mark.parametrize("k", [1, 7])
 def test_generic_backward_deterministic(lib, k):
     # the generic backward reduces its partials by fixed-order segment sums: two runs
     # (fresh handles and workspaces, so the scheduling differs) give the same bits
@@ -266,6 +266,21 @@ def test_generic_backward_deterministic(lib, k):
     for _ in range(2):
         emb, G, grads, dV = gpu_train(lib, case)
         assert not lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], case["idx"].size)
+        runs.append([g.cpu().numpy() for g in grads])
+    for a, b in zip(*runs):
+        assert np.array_equal(a, b)
+
+
+def test_r64_backward_deterministic(lib):
+    # the R = 64 MFMA backward writes per-slice, per-chunk and per-row partials that the
+    # same fixed-order segment sums reduce: two runs give the same bits
+    c = dict(TINY[5])
+    case = ttgen.tiny(3505, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
+    _say("[bwd determinism] tiny5 R=64")
+    runs = []
+    for _ in range(2):
+        emb, G, grads, dV = gpu_train(lib, case)
+        assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], case["idx"].size)
         runs.append([g.cpu().numpy() for g in grads])
     for a, b in zip(*runs):
         assert np.array_equal(a, b)
@@ -305,8 +320,8 @@ EDGE_SHAPES = [((2, 2, 2), 4), ((4, 4, 8), 32), ((4, 4, 8), 64)]
 @pytest.mark.parametrize("kind", ["all_equal", "one_prefix", "distinct_prefixes"])
 def test_edge_index_patterns(lib, orc, kind, dR):
     # each pattern through the forward, the backward and the fused backward-and-SGD,
-    # on the generic kernels and on the MFMA shapes (R = 32: both fused kernels on
-    # the matrix cores; R = 64: the matrix-core forward)
+    # on the generic kernels and on the MFMA shapes (R = 32 and R = 64: both fused
+    # kernels on the matrix cores)
     case = _edge(kind, *dR)
     name = f"{kind} d={dR[0]} R={dR[1]}"
     check_forward(lib, orc, case, name=name)
@@ -343,10 +358,10 @@ def _run_slices(g, n):
     return rows[order], sl[order], first, run
 
 
-def _hot_prefix_case(seed, T, n, B, hot, per_bag=20):
+def _hot_prefix_case(seed, T, n, B, hot, per_bag=20, d=(4, 4, 8), R=32):
     """Bags whose indices fall in the listed hot prefixes (i1, i2) with uniform i3 most
     of the time, else anywhere: long prefix groups of many work slices."""
-    case = ttgen.tiny(seed, T, n, (4, 4, 8), 32, B=B, max_len=per_bag, zipf=1.1, empty_bags=False)
+    case = ttgen.tiny(seed, T, n, d, R, B=B, max_len=per_bag, zipf=1.1, empty_bags=False)
     rng = np.random.default_rng(seed)
     idx = case["idx"].copy()
     pick = rng.random(idx.size) < 0.85
@@ -399,6 +414,39 @@ def test_backward_prefix_groups_across_chunk_ends(lib, orc):
     torch.cuda.synchronize()
     assert emb.check_errors() == 0
     _check_sgd(orc, case, G, 0.01, "groups across chunk ends")
+
+
+@pytest.mark.parametrize("sched", ["steal", "group"])
+def test_r64_backward_groups_across_quads_and_chunks(lib, orc, sched):
+    # R = 64 cuts a (table, i2) run into chunks of four work slices (one quad); groups
+    # of 7-8 slices straddle quads and chunks.  Under the static prefix mapping a
+    # chunk is a whole group of several quads, whose dB partial the MFMA backward
+    # accumulates quad after quad.  Forward, backward and the fused update.
+    n = (12, 2, 250)
+    hot = [(i1, 0) for i1 in range(12)]
+    case = _hot_prefix_case(7103, 2, n, B=300, hot=hot, per_bag=20, R=64)
+    M = case["idx"].size
+    name = f"R=64 groups across quads, {sched}"
+    V, grads, emb = _run_mode(lib, case, sched=sched)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["fwd_fused"], M)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
+    g = emb.debug_grouping(M)
+    rows, sl, first, run = _run_slices(g, n)
+    assert sl.max() > 4 and ((first // 4) != ((first + sl - 1) // 4)).sum() >= 2
+    ref_v, _ = orc.forward(case)
+    mag_v, _ = orc.forward(abs_case(case))
+    assert_close(f"forward {name}", V, ref_v, mag_v)
+    ref = orc.backward(case)[:3]
+    mag = orc.backward(abs_case(case))[:3]
+    for k in range(3):
+        assert_close(f"dG{k + 1} {name}", grads[k], ref[k], mag[k])
+    _say(f"[bwd+sgd] {name}")
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.backward_sgd(*G, idx, off, dV, 0.01, num_bags=case["B"], reuse_grouping=False)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    _check_sgd(orc, case, G, 0.01, name)
 
 
 def test_edge_empty_and_single_bag(lib, orc):
@@ -746,7 +794,7 @@ def _run_mode(lib, case, **kw):
     return out.cpu().numpy().reshape(-1, D), [g.cpu().numpy() for g in grads], emb
 
 
-@pytest.mark.parametrize("which", ["hot_r64", "mfma"])
+@pytest.mark.parametrize("which", ["hot_r64", "hot_generic", "mfma"])
 def test_schedules_same_results(lib, orc, which):
     # Section 4.4 ablation modes compute the same function: static shares, stealing,
     # stealing with the checkpointed intermediate (hot prefix groups spanning
@@ -754,6 +802,10 @@ def test_schedules_same_results(lib, orc, which):
     # group one work unit)
     if which == "hot_r64":
         case = ttgen.make(4, bags=256, with_grad=True)
+    elif which == "hot_generic":
+        # d = (4, 4, 4), R = 16: generic kernels both ways, groups of about 60 slices
+        case = _hot_prefix_case(7006, 1, (3, 2, 2000), B=300, hot=[(1, 1), (2, 0)], per_bag=24,
+                                d=(4, 4, 4), R=16)
     else:
         c = dict(TINY[4])
         case = ttgen.tiny(7004, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
@@ -767,7 +819,7 @@ def test_schedules_same_results(lib, orc, which):
         assert_close(f"forward {which} {sched}", V, ref_v, mag_v)
         for k in range(3):
             assert_close(f"dG{k + 1} {which} {sched}", grads[k], ref[k], mag[k])
-        if which == "hot_r64" and sched == "steal_ckpt":
+        if which == "hot_generic" and sched == "steal_ckpt":
             # the workload must exercise the checkpoint: some prefix group spans chunks
             g = emb.debug_grouping(int(case["idx"].size))
             assert np.max(np.diff(g["pg_start"])) > 8 * 32

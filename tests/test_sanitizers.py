@@ -70,7 +70,7 @@ def test_library_host_code_under_asan_ubsan(tmp_path):
         pytest.skip("no clang AddressSanitizer runtime in this ROCm")
     lib = str(tmp_path / "libttemb_asan.so")
     csrc = os.path.join(ROOT, "paper_2609_03459_amd", "csrc")
-    srcs = [os.path.join(csrc, f) for f in ("tt_emb.hip", "group.hip", "fwd.hip", "bwd.hip", "bwd_r32.hip",
+    srcs = [os.path.join(csrc, f) for f in ("tt_emb.hip", "group.hip", "fwd.hip", "bwd.hip", "bwd_r32.hip", "bwd_r64.hip",
                                             "cores.hip")]
     # each -fsanitize= applies to the host compilation only (-Xarch_host); the device
     # code is built as usual, since the host objects name its code object
