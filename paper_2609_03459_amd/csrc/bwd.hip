@@ -542,43 +542,60 @@ __device__ __forceinline__ void put_g(float* out, int64_t i, float acc, float lr
   out[i] = update ? out[i] - lr * acc : acc;
 }
 
+// Eight accumulators take consecutive terms of an ordered list in turn (eight loads
+// in flight per thread); their fixed tree sum is the segment's sum.
+__device__ __forceinline__ float sum8(const float (&a)[8]) {
+  return ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+}
+
 // dG1[t][i1] = sum of the dA partials of the slices of prefixes (i1, i2), i2 ascending
-// (each prefix's slices in order); block (t i1, column block)
+// (each prefix's slices in order); block (t i1, column block).  Each round of
+// GRED_THREADS prefixes is scanned into a list of slice ids in LDS (G1_WIN at a
+// time), which every column then walks in list order.
+constexpr int G1_WIN = 2048;
 __global__ void __launch_bounds__(GRED_THREADS) k_gred_g1(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                           const uint32_t* __restrict__ dense_base,
                                                           const float* __restrict__ dApart, float* __restrict__ dG1,
                                                           float lr, bool update) {
-  __shared__ uint32_t cnt[GRED_THREADS], base[GRED_THREADS];
+  __shared__ uint32_t wsum[GRED_THREADS / 64];
+  __shared__ uint32_t list[G1_WIN];
   const int ti1 = blockIdx.x;
   const int t = ti1 / s.n1, i1 = ti1 - t * s.n1;
   const int d1R = s.d1 * s.R;
   const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
-  float a0 = 0.f, a1 = 0.f;  // even and odd slices of the ordered list, added at the end
-  int k = 0;
+  const bool col = e < d1R;
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int r0 = 0; r0 < s.n2; r0 += GRED_THREADS) {
     const int i2 = r0 + (int)threadIdx.x;
-    __syncthreads();
+    uint32_t cnt = 0, base = 0;
     if (i2 < s.n2) {
       const int64_t slot = ((int64_t)t * s.n2 + i2) * s.n1 + i1;
-      cnt[threadIdx.x] = dense_cnt[slot];
-      base[threadIdx.x] = dense_base[slot];
-    } else {
-      cnt[threadIdx.x] = 0;
+      cnt = dense_cnt[slot];
+      base = dense_base[slot];
     }
-    __syncthreads();
-    if (e < d1R) {
-      const int nr = s.n2 - r0 < GRED_THREADS ? s.n2 - r0 : GRED_THREADS;
-      for (int q = 0; q < nr; ++q)
-        for (uint32_t j = 0; j < cnt[q]; ++j, ++k) {
-          const float v = dApart[(int64_t)(base[q] + j) * d1R + e];
-          if (k & 1)
-            a1 += v;
-          else
-            a0 += v;
+    uint32_t total;
+    const uint32_t pos = block_excl_scan<uint32_t, GRED_THREADS>(cnt, wsum, &total);
+    for (uint32_t w0 = 0; w0 < total; w0 += G1_WIN) {
+      const uint32_t k0 = pos > w0 ? pos : w0;
+      const uint32_t k1 = pos + cnt < w0 + G1_WIN ? pos + cnt : w0 + G1_WIN;
+      for (uint32_t k = k0; k < k1; ++k) list[k - w0] = base + (k - pos);
+      __syncthreads();
+      const int wn = (int)(total - w0 < (uint32_t)G1_WIN ? total - w0 : (uint32_t)G1_WIN);
+      if (col) {
+        int j = 0;
+        for (; j + 8 <= wn; j += 8) {
+          float v[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = dApart[(int64_t)list[j + q] * d1R + e];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) a[q] += v[q];
         }
+        for (; j < wn; ++j) a[0] += dApart[(int64_t)list[j] * d1R + e];
+      }
+      __syncthreads();  // the list is refilled
     }
   }
-  if (e < d1R) put_g(dG1, (int64_t)ti1 * d1R + e, a0 + a1, lr, update);
+  if (col) put_g(dG1, (int64_t)ti1 * d1R + e, sum8(a), lr, update);
 }
 
 // dG2[t][i2] = sum of the dB partials of the chunks of run (t, i2), in chunk order
@@ -589,13 +606,17 @@ __global__ void __launch_bounds__(GRED_THREADS) k_gred_g2(const uint32_t* __rest
   const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
   if (e >= nB) return;
   const int c0 = (int)run_base[r], c1 = (int)run_base[r + 1];
-  float a[4] = {0.f, 0.f, 0.f, 0.f};  // chunk c goes to a[(c - c0) & 3]: four loads in flight
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   int c = c0;
-  for (; c + 4 <= c1; c += 4)
+  for (; c + 8 <= c1; c += 8) {
+    float v[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) a[q] += dBpart[(int64_t)(c + q) * nB + e];
-  for (; c < c1; ++c) a[(c - c0) & 3] += dBpart[(int64_t)c * nB + e];
-  put_g(dG2, (int64_t)r * nB + e, (a[0] + a[1]) + (a[2] + a[3]), lr, update);
+    for (int q = 0; q < 8; ++q) v[q] = dBpart[(int64_t)(c + q) * nB + e];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) a[q] += v[q];
+  }
+  for (; c < c1; ++c) a[0] += dBpart[(int64_t)c * nB + e];
+  put_g(dG2, (int64_t)r * nB + e, sum8(a), lr, update);
 }
 
 // Sort keys t n3 + i3 of the unique rows (positions from U on get `sentinel`, which
@@ -635,13 +656,17 @@ __global__ void __launch_bounds__(GRED_THREADS) k_gred_g3(const int32_t* __restr
   const int e = blockIdx.y * GRED_THREADS + threadIdx.x;
   if (e >= RD) return;
   const int k0 = lo[b], k1 = hi[b];
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   int k = k0;
-  for (; k + 4 <= k1; k += 4)
+  for (; k + 8 <= k1; k += 8) {
+    float v[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) a[q] += dDpart[(int64_t)rows[k + q] * RD + e];
-  for (; k < k1; ++k) a[(k - k0) & 3] += dDpart[(int64_t)rows[k] * RD + e];
-  put_g(dG3, (int64_t)b * RD + e, (a[0] + a[1]) + (a[2] + a[3]), lr, update);
+    for (int q = 0; q < 8; ++q) v[q] = dDpart[(int64_t)rows[k + q] * RD + e];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) a[q] += v[q];
+  }
+  for (; k < k1; ++k) a[0] += dDpart[(int64_t)rows[k] * RD + e];
+  put_g(dG3, (int64_t)b * RD + e, sum8(a), lr, update);
 }
 
 static int bits_of(uint64_t x) {
