@@ -682,6 +682,69 @@ def test_backward_config5_full_hottest_slices(lib, orc):
         assert np.all(np.abs(new - exp) <= bound + 1e-30), cname
 
 
+def _oracle_backward_by_slice(orc, case, want):
+    """orc.backward with slice masks, one wanted slice per call on a thread pool (each
+    call visits only the occurrences that touch its slice); returns the three
+    gradients with the wanted slices filled in."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    tasks = [(k, int(i)) for k, m in enumerate(want) for i in np.flatnonzero(m)]
+
+    def one(task):
+        k, i = task
+        w = [np.zeros_like(m) for m in want]
+        w[k][i] = 1
+        return orc.backward(case, want=w)[k]
+
+    with ThreadPoolExecutor(min(len(tasks), 16)) as ex:
+        parts = list(ex.map(one, tasks))
+    out = [np.zeros(case[("G1", "G2", "G3")[k]].shape) for k in range(3)]
+    for (k, i), g in zip(tasks, parts):
+        T = case["T"]
+        out[k].reshape(T * out[k].shape[1], -1)[i] = g.reshape(T * g.shape[1], -1)[i]
+    return out
+
+
+def test_backward_config4_full_hottest_slices(lib, orc):
+    # The hot-prefix workload at full size as a training step on the R = 64 MFMA
+    # backward (forward with grouping, backward reusing it, then the fused update):
+    # the most-used slice of each core (the hottest prefix's G1 and G2 slices and the
+    # most-used G3 slice) plus two random slices per core, against the oracle.
+    case = ttgen.make(4, with_grad=True)
+    T, B, lr = case["T"], case["B"], 0.01
+    M = int(case["idx"].size)
+    want = _hottest_slices(case, extra_tables=(0,))
+    _say(f"[bwd] config4 full, hottest + random slices ({sum(int(w.sum()) for w in want)} slices)")
+    emb = _make(lib, case)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.forward(*G, idx, off, num_bags=B)
+    grads = emb.backward(*G, idx, off, dV, num_bags=B, reuse_grouping=True)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    from concurrent.futures import ThreadPoolExecutor
+
+    with ThreadPoolExecutor(2) as ex:  # the signed and the absolute case side by side
+        ref_f = ex.submit(_oracle_backward_by_slice, orc, case, want)
+        mag_f = ex.submit(_oracle_backward_by_slice, orc, abs_case(case), want)
+        ref, mag = ref_f.result(), mag_f.result()
+    for k in range(3):
+        g = grads[k].cpu().numpy()
+        assert_close(f"dG{k + 1} config4 full (hottest slices)", _sel(g, T, want[k]), _sel(ref[k], T, want[k]),
+                     _sel(mag[k], T, want[k]))
+    del grads
+    _say("[bwd+sgd] config4 full, same slices")
+    emb.backward_sgd(*G, idx, off, dV, lr, num_bags=B, reuse_grouping=True)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    for k, cname in enumerate(("G1", "G2", "G3")):
+        new = _sel(G[k].cpu().numpy().astype(np.float64), T, want[k])
+        exp = _sel(orc.sgd(case[cname], ref[k], lr), T, want[k])
+        bound = TOL * lr * _sel(mag[k], T, want[k]) + 2.0 ** -23 * np.abs(exp)
+        assert np.all(np.abs(new - exp) <= bound + 1e-30), cname
+
+
 def test_sgd_step(lib, orc):
     case = ttgen.make(5, bags=32)
     _say("[sgd] config5 B=32")
