@@ -114,7 +114,9 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   int cur_run = -1;
   float Bop[32];   // stage-1 B operand B_h[a = 4 s + l4][16 nt + l15], (s, nt) -> 4 s + nt
   float BTop[32];  // dA B operand B_h^T[(j2 = l4, b' = s)][a = 16 nt2 + l15], (s, nt2) -> 16 nt2 + s
-  f32x4 dB[8];     // (mt, nt) -> 4 mt + nt
+  f32x4 dB[8];     // (mt, nt) -> 4 mt + nt; zeroed here and after each chunk's partial is stored
+#pragma unroll
+  for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // slice descriptors of the current chunk, lane j holding slice f + j (j < ns;
   // other lanes have no rows): first row, row count, i1
@@ -133,12 +135,20 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     const int b2 = __builtin_amdgcn_readlane(c_rb, qd0 + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd0 + 3);
     const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
     e_np = q3 + ((n3 + 1) >> 1);
-    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
-    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
-    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    // pair P of slice j starts at row base_j + 2 P and has a second row iff
+    // 2 P + 1 < lim_j, with the wave-uniform base_j = b_j - 2 q_j, lim_j = n_j + 2 q_j
+    const bool s1 = lane >= q1, s2 = lane >= q2, s3 = lane >= q3;
+    const int j = (int)s1 + (int)s2 + (int)s3;
+    int base = b0, lim = n0;
+    base = s1 ? b1 - 2 * q1 : base;
+    lim = s1 ? n1 + 2 * q1 : lim;
+    base = s2 ? b2 - 2 * q2 : base;
+    lim = s2 ? n2 + 2 * q2 : lim;
+    base = s3 ? b3 - 2 * q3 : base;
+    lim = s3 ? n3 + 2 * q3 : lim;
     const bool ok = lane < e_np;
-    const bool has1 = ok && pr + 1 < nr;
-    e_ra = ok ? rb + pr : b0;  // lanes past the quad's pairs keep a valid row
+    const bool has1 = ok && 2 * lane + 1 < lim;
+    e_ra = ok ? base + 2 * lane : b0;  // lanes past the quad's pairs keep a valid row
     e_ia = uniq_i3[e_ra];
     e_ib = uniq_i3[has1 ? e_ra + 1 : e_ra];
     e_jh = (j << 16) | (has1 ? 1 << 18 : 0);
@@ -206,9 +216,13 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   };
   // The next quad's operands are loaded before the current quad's dA product, so
   // that product and its stores cover their latency: its row-pair descriptors,
-  // its stage-1 A operand (clamped rows, zeroed at use for missing slices) and
-  // its first two row pairs.  At a chunk end the next chunk is claimed first.
+  // its stage-1 A operand and its first two row pairs.  At a chunk end the next
+  // chunk is claimed first.  In a quad of fewer than four slices the missing
+  // slices' A rows repeat a loaded slice: a product's output row depends on its own
+  // operand row only, and the stack rows of missing slices are neither read by the
+  // row pairs nor summed into dB nor stored as dA, so they need no clearing.
   float Aop[8];
+  float ATq[8];  // dB A operands A_j^T of the quad's four slices, (j, half) -> 2 j + half
   BwPair XA, XB, XC;
   auto prefetch_quad = [&]() {
     d_ra = e_ra;
@@ -223,6 +237,15 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
                       (uint32_t)((lane & 3) * 32 + l4);
 #pragma unroll
     for (int s4 = 0; s4 < 8; ++s4) Aop[s4] = Ag[4 * s4];
+    // loaded with Aop, ahead of every row-pair load of the quad: vector memory
+    // counts complete in issue order, so a wait for an operand loaded later (at a
+    // slice switch) would also wait for the row pairs prefetched before it
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(c_i1, qd + j) * 128u + (uint32_t)(l4 * 32 + l15);
+      ATq[2 * j] = Aj[0];
+      ATq[2 * j + 1] = Aj[16];
+    }
     pair_load(XA, 0);
     pair_load(XB, np > 1 ? 1 : 0);
   };
@@ -247,22 +270,17 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         }
       cur_run = run;
     }
-    if (qd == 0) {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
     const int nqs = ns - qd < 4 ? ns - qd : 4;
     const int sb = f + qd;
     // stage 1: Cstack_h (16 x 64) = Astack (16 x 32) . B_h (32 x 64),
-    // Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
+    // Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4] (rows of missing slices unused)
     {
-      const bool aj_ok = (l15 >> 2) < nqs;
       f32x4 Cs[4];
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4) {
-        const float a = aj_ok ? Aop[s4] : 0.f;
+        const float a = Aop[s4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Bop[4 * s4 + nt], Cs[nt], 0, 0, 0);
       }
@@ -273,14 +291,11 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int r = 0; r < 4; ++r) scr_c[SCR_PITCH * r + 16 * nt] = Cs[nt][r];
       wave_lds_sync();
     }
-    // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4] and the dB A operand rows
-    float CT[4], AT0, AT1;
+    // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4]
+    float CT[4];
     auto slice_begin = [&](int j) {
 #pragma unroll
       for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[4 * SCR_PITCH * j + SCR_PITCH * s4 + lane];  // row 4 j + s4
-      const float* Aj = G1t + (uint32_t)__builtin_amdgcn_readlane(c_i1, qd + j) * 128u + (uint32_t)(l4 * 32 + l15);
-      AT0 = Aj[0];
-      AT1 = Aj[16];
     };
     slice_begin(0);
     f32x4 dC = {0.f, 0.f, 0.f, 0.f};
@@ -308,13 +323,8 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
       pa_o0 = lds_cas_old(pa_u, w.x, add2(w.x, dd[0], dd[1]));
       pa_o1 = lds_cas_old(pa_u + 1, w.y, add2(w.y, dd[2], dd[3]));
     };
-    // slice j done: dB_h += A_j^T . dC_h (M = a, N = (j2, b'), K = j1); dC_h to slot j for dA
+    // slice j done: dC_h to rows 4 j .. 4 j + 3 of the stack, for the quad's dB and dA
     auto slice_end = [&](int j) {
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        dB[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT0, dC[nt], dB[nt], 0, 0, 0);
-        dB[4 + nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(AT1, dC[nt], dB[4 + nt], 0, 0, 0);
-      }
       wave_lds_sync();
 #pragma unroll
       for (int r = 0; r < 4; ++r) scr_d[4 * SCR_PITCH * j + 16 * r] = dC[r];  // row 4 j + l4, column 16 r + l15
@@ -342,6 +352,22 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     }
     slice_end(cj);
     wave_lds_sync();
+    // dB_h += A_j^T . dC_j (M = a, N = (j2, b'), K = j1) for the quad's slices, before
+    // the next quad's operands replace ATq; each lane's B operand dC_j[j1 = l4][16 nt + l15]
+    // is what it wrote to the stack itself
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j < nqs) {
+        float dcj[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) dcj[nt] = scr_d[4 * SCR_PITCH * j + 16 * nt];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          dB[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(ATq[2 * j], dcj[nt], dB[nt], 0, 0, 0);
+          dB[4 + nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(ATq[2 * j + 1], dcj[nt], dB[4 + nt], 0, 0, 0);
+        }
+      }
+    }
     // the next quad: the rest of this chunk, or the first quad of the next chunk
     const int c_done = c;
     const bool chunk_end = qd + 4 >= ns;
@@ -356,14 +382,13 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     // (j2, b') taken as (j2 = l4, b' = s) in step s, so that each lane reads 16
     // contiguous floats of its stack row l15
     {
-      const bool m_ok = (l15 >> 2) < nqs;
       f32x4 dA0 = {0.f, 0.f, 0.f, 0.f}, dA1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const f32x4 v = *reinterpret_cast<const f32x4*>(scr_a + 4 * q);
 #pragma unroll
         for (int c4 = 0; c4 < 4; ++c4) {
-          const float av = m_ok ? v[c4] : 0.f;
+          const float av = v[c4];
           dA0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[4 * q + c4], dA0, 0, 0, 0);
           dA1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[16 + 4 * q + c4], dA1, 0, 0, 0);
         }
@@ -388,6 +413,8 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
   acc_finish();

@@ -430,6 +430,11 @@ __device__ __forceinline__ float4 buf_f32x4(buf_t r, uint32_t off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+// Waits until every vector memory access of this wave has completed (s_waitcnt
+// vmcnt(0), the other counters untouched: expcnt 7, lgkmcnt 15).  The compiler
+// keeps such an explicit wait and counts it when it places its own waits.
+__device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Orders this wave's LDS writes before its later LDS reads of other lanes'
 // data (a wave's LDS requests complete in order; this keeps the compiler
 // from reordering across the exchange and waits for outstanding writes).

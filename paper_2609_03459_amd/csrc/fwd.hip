@@ -147,7 +147,7 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
 // and work through them four slices ("a quad") at a time:
 //   * stage 1: Cstack (16 x 128) = Astack (16 x 32) . B (32 x 128) with
 //     v_mfma_f32_16x16x4f32, rows (slice, j1), columns (j2, b); 64 instructions;
-//   * Cstack goes through a per-wave XOR-swizzled LDS tile into the B operand of
+//   * Cstack goes through a per-wave padded LDS tile into the B operand of
 //     stage 2, C'^T (b x jj) of one slice;
 //   * stage 2 per row pair: E^T (rows x j3, jj) = D^T . C'^T, 8 instructions;
 //     each lane ends up with four consecutive floats of one E row (one 16-byte
@@ -155,14 +155,16 @@ __global__ void __launch_bounds__(FWD_THREADS) k_fwd_generic(ShapeArgs s, const 
 // The next row pair's G3 operands are in flight while a pair is computed.
 // ---------------------------------------------------------------------------
 constexpr int F32_WAVES = 4;
-constexpr int F32_WG_PER_CU = 3;  // three workgroups (12 waves, 96 KB LDS) per CU
-constexpr int F32_SCR = 2048;     // per-wave LDS floats: [slice 4][j1 4][j2 4][b 32]
-
-// XOR swizzle of the b index: both the stage-1 writes and the stage-2 operand
-// reads put at most two lanes on one bank
-__device__ __forceinline__ uint32_t fscr_at(int sl, int j1, int j2, int b) {
-  return (uint32_t)(sl * 512 + j1 * 128 + j2 * 32 + (b ^ ((8 * sl + 4 * j1 + 16 * j2) & 31)));
-}
+constexpr int F32_WG_PER_CU = 3;  // three workgroups (12 waves, 111 KB LDS) per CU (four spill at 128 VGPRs)
+// Per-wave LDS tile of the C stack: row (slice, j1, j2) holds the 32 b values of one
+// (j1, j2), rows F32_ROW floats apart, slices F32_SLICE apart.  The padding puts at
+// most two lanes on a bank for the stage-1 writes (the four slices of a write land
+// 16 banks apart) and for the stage-2 reads (a lane's row pitch of 36 spreads the
+// sixteen rows over distinct bank groups), whether the LDS has 32 or 64 banks, and
+// makes every access a per-lane base plus an immediate offset.
+constexpr int F32_ROW = 36;
+constexpr int F32_SLICE = 16 * F32_ROW + 16;
+constexpr int F32_SCR = 4 * F32_SLICE;
 
 __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     k_fwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
@@ -173,6 +175,10 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* scr = scr_all + wave * F32_SCR;
+  // this lane's stage-1 write base (slice l4, b = l15 (+ 16)) and stage-2 read base
+  // (row jj = (j1, j2) = l15, b = 4 s + l4)
+  float* scr_w = scr + F32_SLICE * (lane >> 4) + (lane & 15);
+  const float* scr_r = scr + F32_ROW * (lane & 15) + (lane >> 4);
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
   const int orow = l4 >> 1;  // E row of the pair this lane's output belongs to
@@ -213,6 +219,10 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       c_rb = sd.y;
       c_nr = lane < ns ? sd.z - sd.y : 0;
       c_i1 = slice_i1[sl];
+      // the descriptors are needed at once; waiting for them here (and for the
+      // older loads) leaves nothing of this path pending where it rejoins the
+      // in-chunk path, whose waits the compiler would otherwise make as strict
+      vm_wait_all();
     }
   };
 
@@ -229,12 +239,20 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     const int b2 = __builtin_amdgcn_readlane(c_rb, qd + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd + 3);
     const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
     e_np = q3 + ((n3 + 1) >> 1);
-    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
-    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
-    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    // pair P of slice j starts at row base_j + 2 P and has a second row iff
+    // 2 P + 1 < lim_j, with the wave-uniform base_j = b_j - 2 q_j, lim_j = n_j + 2 q_j
+    const bool s1 = lane >= q1, s2 = lane >= q2, s3 = lane >= q3;
+    const int j = (int)s1 + (int)s2 + (int)s3;
+    int base = b0, lim = n0;
+    base = s1 ? b1 - 2 * q1 : base;
+    lim = s1 ? n1 + 2 * q1 : lim;
+    base = s2 ? b2 - 2 * q2 : base;
+    lim = s2 ? n2 + 2 * q2 : lim;
+    base = s3 ? b3 - 2 * q3 : base;
+    lim = s3 ? n3 + 2 * q3 : lim;
     const bool ok = lane < e_np;
-    const bool has1 = ok && pr + 1 < nr;
-    const int ra = ok ? rb + pr : b0;  // lanes past the quad's pairs keep a valid row
+    const bool has1 = ok && 2 * lane + 1 < lim;
+    const int ra = ok ? base + 2 * lane : b0;  // lanes past the quad's pairs keep a valid row
     e_ia = uniq_i3[ra];
     e_ib = uniq_i3[has1 ? ra + 1 : ra];
     e_ra = ra | (j << 28) | (has1 ? 1 << 30 : 0);
@@ -272,6 +290,19 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   };
 
   FPair XA, XB;
+  // B of the chunk's run: loaded before the quad's first row pairs, since vector
+  // memory counts complete in issue order (a B loaded after them would make stage 1
+  // wait for the row pairs too)
+  auto load_B = [&]() {
+    if (run != cur_run) {
+      const float* Bg = G2 + (uint32_t)run * 4096u + (uint32_t)(l4 * 128 + l15);
+#pragma unroll
+      for (int s4 = 0; s4 < 8; ++s4)
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt) Bop[8 * s4 + nt] = Bg[s4 * 512 + 16 * nt];
+      cur_run = run;
+    }
+  };
   next_chunk();
   if (c >= 0) {
     build_desc();
@@ -281,18 +312,11 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     d_ib = e_ib;
     np = e_np;
     g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+    load_B();
     pair_load(XA, 0);
     pair_load(XB, np > 1 ? 1 : 0);
   }
   while (c >= 0) {
-    if (run != cur_run) {
-      const float* Bg = G2 + (uint32_t)run * 4096u + (uint32_t)(l4 * 128 + l15);
-#pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4)
-#pragma unroll
-        for (int nt = 0; nt < 8; ++nt) Bop[8 * s4 + nt] = Bg[s4 * 512 + 16 * nt];
-      cur_run = run;
-    }
     // stage 1 (rows of slices beyond the chunk's end come from a repeated slice and are never read)
     {
       f32x4 Cs[8];
@@ -307,7 +331,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
 #pragma unroll
       for (int nt = 0; nt < 8; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) scr[fscr_at(l4, r, nt >> 1, 16 * (nt & 1) + l15)] = Cs[nt][r];
+        for (int r = 0; r < 4; ++r) scr_w[F32_ROW * (4 * r + (nt >> 1)) + 16 * (nt & 1)] = Cs[nt][r];
       wave_lds_sync();
     }
     // the next quad (the rest of this chunk, or a new chunk claimed now): its
@@ -324,7 +348,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     float CT[8];
     auto slice_begin = [&](int j) {
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr[fscr_at(j, l15 >> 2, l15 & 3, 4 * s4 + l4)];
+      for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr_r[F32_SLICE * j + 4 * s4];
     };
     slice_begin(0);
     // E rows of a pair through a descriptor that ends after the pair's real rows, so
@@ -359,6 +383,7 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       d_ib = e_ib;
       np = e_np;
       g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+      load_B();
       pair_load(XA, 0);
       pair_load(XB, np > 1 ? 1 : 0);
     }
@@ -442,12 +467,20 @@ __global__ void __launch_bounds__(64 * F64_WAVES, F64_WG_PER_CU)
     const int b2 = __builtin_amdgcn_readlane(c_rb, qd + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd + 3);
     const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
     e_np = q3 + ((n3 + 1) >> 1);
-    const int j = (lane >= q1) + (lane >= q2) + (lane >= q3);
-    const int pr = 2 * (lane - sel4(j, 0, q1, q2, q3));
-    const int rb = sel4(j, b0, b1, b2, b3), nr = sel4(j, n0, n1, n2, n3);
+    // pair P of slice j starts at row base_j + 2 P and has a second row iff
+    // 2 P + 1 < lim_j, with the wave-uniform base_j = b_j - 2 q_j, lim_j = n_j + 2 q_j
+    const bool s1 = lane >= q1, s2 = lane >= q2, s3 = lane >= q3;
+    const int j = (int)s1 + (int)s2 + (int)s3;
+    int base = b0, lim = n0;
+    base = s1 ? b1 - 2 * q1 : base;
+    lim = s1 ? n1 + 2 * q1 : lim;
+    base = s2 ? b2 - 2 * q2 : base;
+    lim = s2 ? n2 + 2 * q2 : lim;
+    base = s3 ? b3 - 2 * q3 : base;
+    lim = s3 ? n3 + 2 * q3 : lim;
     const bool ok = lane < e_np;
-    const bool has1 = ok && pr + 1 < nr;
-    const int ra = ok ? rb + pr : b0;
+    const bool has1 = ok && 2 * lane + 1 < lim;
+    const int ra = ok ? base + 2 * lane : b0;
     e_ia = uniq_i3[ra];
     e_ib = uniq_i3[has1 ? ra + 1 : ra];
     e_ra = ra | (j << 28) | (has1 ? 1 << 30 : 0);
