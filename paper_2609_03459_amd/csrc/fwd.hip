@@ -303,6 +303,29 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       cur_run = run;
     }
   };
+  // Stage 1 of a quad, Cstack (16 x 128) = Astack (16 x 32) . B (32 x 128) with rows
+  // (slice, j1) and columns (j2, b), in eight groups of eight MFMAs (one contraction
+  // step s4 each), so that the next quad's groups can run between the current quad's
+  // row pairs; the result waits in Cs until the current quad's C^T reads are done.
+  // Rows of slices beyond the chunk's end come from a repeated slice and are never read.
+  f32x4 Cs[8];
+  auto s1_zero = [&]() {
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  auto s1_group = [&](int s4) {
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt)
+      Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[s4], Bop[8 * s4 + nt], Cs[nt], 0, 0, 0);
+  };
+  auto s1_store = [&]() {
+    // lane holds C[slice l4][j1 r][j2 = nt >> 1][b = 16 (nt & 1) + l15]
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) scr_w[F32_ROW * (4 * r + (nt >> 1)) + 16 * (nt & 1)] = Cs[nt][r];
+    wave_lds_sync();
+  };
   next_chunk();
   if (c >= 0) {
     build_desc();
@@ -315,34 +338,24 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     load_B();
     pair_load(XA, 0);
     pair_load(XB, np > 1 ? 1 : 0);
+    s1_zero();
+#pragma unroll
+    for (int s4 = 0; s4 < 8; ++s4) s1_group(s4);
+    s1_store();
   }
   while (c >= 0) {
-    // stage 1 (rows of slices beyond the chunk's end come from a repeated slice and are never read)
-    {
-      f32x4 Cs[8];
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt) Cs[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4)
-#pragma unroll
-        for (int nt = 0; nt < 8; ++nt)
-          Cs[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(Aop[s4], Bop[8 * s4 + nt], Cs[nt], 0, 0, 0);
-      // lane holds C[slice l4][j1 r][j2 = nt >> 1][b = 16 (nt & 1) + l15]
-#pragma unroll
-      for (int nt = 0; nt < 8; ++nt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) scr_w[F32_ROW * (4 * r + (nt >> 1)) + 16 * (nt & 1)] = Cs[nt][r];
-      wave_lds_sync();
-    }
     // the next quad (the rest of this chunk, or a new chunk claimed now): its
-    // descriptors and stage-1 A operand load while this quad's rows are computed
+    // descriptors, stage-1 A operand and (new run) B load while this quad's rows are
+    // computed; this quad's B is no longer needed
     if (qd + 4 >= ns)
       next_chunk();
     else
       qd += 4;
-    if (c >= 0) {
+    const bool nxt = c >= 0;
+    if (nxt) {
       build_desc();
       load_A();
+      load_B();
     }
     // stage-2 B operand of slice j: C'^T[b = 4 s + l4][jj = l15]
     float CT[8];
@@ -369,21 +382,35 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       }
       pair_compute(X);
     };
-    for (int P = 0; P < np; P += 2) {
+    // the first eight row pairs (loads past the last pair are clamped repeats), each
+    // followed by one stage-1 group of the next quad, then the rest
+    if (nxt) s1_zero();
+    int P = 0;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      pair_load(XB, P + 1 < np ? P + 1 : np - 1);
+      if (P < np) step(XA);
+      if (nxt) s1_group(2 * g);
+      pair_load(XA, P + 2 < np ? P + 2 : np - 1);
+      if (P + 1 < np) step(XB);
+      if (nxt) s1_group(2 * g + 1);
+      P += 2;
+    }
+    for (; P < np; P += 2) {
       pair_load(XB, P + 1 < np ? P + 1 : np - 1);
       step(XA);
       pair_load(XA, P + 2 < np ? P + 2 : np - 1);
       if (P + 1 < np) step(XB);
     }
     wave_lds_sync();
-    // the next quad becomes current; its first two row pairs load during its stage 1
-    if (c >= 0) {
+    // the next quad becomes current: its C into the tile, its first two row pairs load
+    if (nxt) {
+      s1_store();
       d_ra = e_ra;
       d_ia = e_ia;
       d_ib = e_ib;
       np = e_np;
       g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
-      load_B();
       pair_load(XA, 0);
       pair_load(XB, np > 1 ? 1 : 0);
     }
