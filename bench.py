@@ -227,10 +227,12 @@ def run_key(args):
 
 
 def step_mode(args):
-    """The step the run times: the training step for the training workload (config 5),
+    """The step the run times: the training step for the training workloads (configs 5 and 6),
     the forward for the forward-only workloads, unless --mode says otherwise."""
+    import ttgen
+
     m = getattr(args, "mode", None)
-    return m if m else ("train" if args.config == 5 else "forward")
+    return m if m else ("train" if ttgen.CONFIGS[args.config]["train"] else "forward")
 
 
 def write_traffic(pmc_dir, key, copy_mib=1024, kernel="bwd_fused", R=32):
@@ -388,7 +390,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=5,
-                    help="workload recipe (5 = training step; 1-4 = the forward-only workloads)")
+                    help="workload recipe (5 = training step; 1-4 = the forward-only workloads; 6 = the "
+                         "training step at the paper's D = 32, R = 32)")
     ap.add_argument("--mode", choices=["train", "forward"], default=None,
                     help="step to time: training step (default for config 5) or forward = grouping, fused "
                          "forward and pooling (default for configs 1-4)")

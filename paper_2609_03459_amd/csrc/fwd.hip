@@ -166,6 +166,9 @@ constexpr int F32_ROW = 36;
 constexpr int F32_SLICE = 16 * F32_ROW + 16;
 constexpr int F32_SCR = 4 * F32_SLICE;
 
+// D3 = 8: d = (4, 4, 8), row groups of two rows; D3 = 2: d = (4, 4, 2) (D = 32), row groups
+// of eight rows, each lane's stage-2 operand from its own row of the group.
+template <int D3>
 __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     k_fwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
               const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
@@ -179,15 +182,20 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   // (row jj = (j1, j2) = l15, b = 4 s + l4)
   float* scr_w = scr + F32_SLICE * (lane >> 4) + (lane & 15);
   const float* scr_r = scr + F32_ROW * (lane & 15) + (lane >> 4);
+  constexpr int GR = 16 / D3;              // rows per stage-2 group ("pair" below)
+  constexpr int DW = 16 * D3;              // floats per E row
+  constexpr uint32_t G3ROW = 128u * D3;    // bytes per G3 row (R d3 floats)
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
-  const int orow = l4 >> 1;  // E row of the pair this lane's output belongs to
-  // stage-2 A operand: lane m = l15 = (row sel, j3), K index b = 4 s + l4
-  const int asel = l15 >> 3;
-  // byte offsets: this lane's stage-2 A word in a G3 row (b = l4, j3 = l15 & 7; + 128 bytes
-  // per K step) and its E store (row orow of the pair, four floats)
-  const uint32_t vo_d = 4u * (uint32_t)(l4 * 8 + (l15 & 7));
-  const uint32_t vo_e = 4u * (uint32_t)(orow * 128 + l15 * 8 + 4 * (l4 & 1));
+  // stage-2 A operand: lane m = l15 = (row asel of the group, j3), K index b = 4 s + l4
+  const int asel = l15 / D3;
+  // byte offsets: this lane's stage-2 A word in a G3 row (b = l4, j3 = l15 % D3; + 16 D3
+  // bytes per K step) and its E store: output row 4 l4 + r of the MFMA is group row
+  // (4 l4 + r) / D3, so for D3 = 8 four consecutive floats of row l4 / 2, for D3 = 2 two
+  // floats of rows 2 l4 and 2 l4 + 1 (the second 128 bytes on)
+  const uint32_t vo_d = 4u * (uint32_t)(l4 * D3 + (l15 % D3));
+  const uint32_t vo_e = D3 == 8 ? 4u * (uint32_t)((l4 >> 1) * 128 + l15 * 8 + 4 * (l4 & 1))
+                                : 4u * (uint32_t)(2 * l4 * DW + l15 * 2);
 
   int cursor = 0;
   int cur_run = -1;
@@ -226,36 +234,61 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     }
   };
 
-  // Row-pair descriptors, lane P holding pair P of a quad (slice j owns
-  // (nr_j + 1) / 2 consecutive pairs): first row | j << 28 | (second row real) << 30,
-  // and i3 of both rows.  Built for the next quad while the current one runs (e_*),
-  // then made current (d_*).
+  // Row-group descriptors, lane P holding group P of a quad (slice j owns
+  // ceil(nr_j / GR) consecutive groups): first row | j << 25 | (real rows - 1) << 27,
+  // and for D3 = 8 the i3 of both rows; for D3 = 2 the position of the group's first row
+  // in the quad's row list (slice 0's rows, then slice 1's, ...: at most 128), whose i3
+  // values lanes L and L + 64 hold in d_i3lo / d_i3hi.  Built for the next quad while the
+  // current one runs (e_*), then made current (d_*).
   int d_ra = 0, d_ia = 0, d_ib = 0, np = 0;
   int e_ra = 0, e_ia = 0, e_ib = 0, e_np = 0;
+  int d_i3lo = 0, d_i3hi = 0, e_i3lo = 0, e_i3hi = 0;
   auto build_desc = [&]() {
     const int n0 = __builtin_amdgcn_readlane(c_nr, qd), n1 = __builtin_amdgcn_readlane(c_nr, qd + 1);
     const int n2 = __builtin_amdgcn_readlane(c_nr, qd + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd + 3);
     const int b0 = __builtin_amdgcn_readlane(c_rb, qd), b1 = __builtin_amdgcn_readlane(c_rb, qd + 1);
     const int b2 = __builtin_amdgcn_readlane(c_rb, qd + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd + 3);
-    const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
-    e_np = q3 + ((n3 + 1) >> 1);
-    // pair P of slice j starts at row base_j + 2 P and has a second row iff
-    // 2 P + 1 < lim_j, with the wave-uniform base_j = b_j - 2 q_j, lim_j = n_j + 2 q_j
+    const int q1 = (n0 + GR - 1) / GR, q2 = q1 + (n1 + GR - 1) / GR, q3 = q2 + (n2 + GR - 1) / GR;
+    e_np = q3 + (n3 + GR - 1) / GR;
+    // group P of slice j starts at row base_j + GR P and holds min(GR, lim_j - GR P) rows,
+    // with the wave-uniform base_j = b_j - GR q_j, lim_j = n_j + GR q_j
     const bool s1 = lane >= q1, s2 = lane >= q2, s3 = lane >= q3;
     const int j = (int)s1 + (int)s2 + (int)s3;
     int base = b0, lim = n0;
-    base = s1 ? b1 - 2 * q1 : base;
-    lim = s1 ? n1 + 2 * q1 : lim;
-    base = s2 ? b2 - 2 * q2 : base;
-    lim = s2 ? n2 + 2 * q2 : lim;
-    base = s3 ? b3 - 2 * q3 : base;
-    lim = s3 ? n3 + 2 * q3 : lim;
+    base = s1 ? b1 - GR * q1 : base;
+    lim = s1 ? n1 + GR * q1 : lim;
+    base = s2 ? b2 - GR * q2 : base;
+    lim = s2 ? n2 + GR * q2 : lim;
+    base = s3 ? b3 - GR * q3 : base;
+    lim = s3 ? n3 + GR * q3 : lim;
     const bool ok = lane < e_np;
-    const bool has1 = ok && 2 * lane + 1 < lim;
-    const int ra = ok ? base + 2 * lane : b0;  // lanes past the quad's pairs keep a valid row
-    e_ia = uniq_i3[ra];
-    e_ib = uniq_i3[has1 ? ra + 1 : ra];
-    e_ra = ra | (j << 28) | (has1 ? 1 << 30 : 0);
+    const int left = lim - GR * lane;
+    const int cnt = ok ? (left < GR ? left : GR) : 1;
+    const int ra = ok ? base + GR * lane : b0;  // lanes past the quad's groups keep a valid row
+    if (D3 == 8) {
+      e_ia = uniq_i3[ra];
+      e_ib = uniq_i3[cnt > 1 ? ra + 1 : ra];
+    } else {
+      // the quad's row list: slice j's rows at positions p_j .. p_j + n_j - 1
+      const int p1 = n0, p2 = p1 + n1, p3 = p2 + n2, ptot = p3 + n3;
+      auto list_row = [&](int x) {  // row at position x (x < ptot), else a valid row
+        const bool t1 = x >= p1, t2 = x >= p2, t3 = x >= p3;
+        int r = b0 + x;
+        r = t1 ? b1 + x - p1 : r;
+        r = t2 ? b2 + x - p2 : r;
+        r = t3 ? b3 + x - p3 : r;
+        return x < ptot ? r : b0;
+      };
+      e_i3lo = uniq_i3[list_row(lane)];
+      e_i3hi = uniq_i3[list_row(lane + 64)];
+      int pj = 0;
+      pj = s1 ? p1 : pj;
+      pj = s2 ? p2 : pj;
+      pj = s3 ? p3 : pj;
+      const int qj = s3 ? q3 : (s2 ? q2 : (s1 ? q1 : 0));
+      e_ia = pj + GR * (lane - qj);
+    }
+    e_ra = ra | (j << 25) | ((cnt - 1) << 27);
   };
   // stage-1 A operand of the quad at qd: Astack[(slice aj, j1 = lane & 3)][a = 4 s + l4]
   // (missing slices repeat the first; their rows are never read)
@@ -273,20 +306,30 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
 
   struct FPair {
     float d[8];
-    int ra;     // first row of the pair (wave-uniform)
-    int j;      // slice within the quad (wave-uniform)
-    bool has1;  // the second row is real (wave-uniform)
+    int ra;   // first row of the group (wave-uniform)
+    int j;    // slice within the quad (wave-uniform)
+    int cnt;  // real rows of the group (wave-uniform)
   };
   buf_t g3buf = make_buf(G3, 0);  // G3[t] of the current quad
   auto pair_load = [&](FPair& X, int P) {
     const int rw = __builtin_amdgcn_readlane(d_ra, P);
-    const int ia = __builtin_amdgcn_readlane(d_ia, P), ib = __builtin_amdgcn_readlane(d_ib, P);
-    X.ra = rw & 0x0FFFFFFF;
-    X.j = (rw >> 28) & 3;
-    X.has1 = (rw >> 30) & 1;
-    const uint32_t o = vo_d + (uint32_t)(asel ? ib : ia) * 1024u;
+    X.ra = rw & 0x01FFFFFF;
+    X.j = (rw >> 25) & 3;
+    X.cnt = ((rw >> 27) & 7) + 1;
+    uint32_t i3;
+    if (D3 == 8) {
+      const int ia = __builtin_amdgcn_readlane(d_ia, P), ib = __builtin_amdgcn_readlane(d_ib, P);
+      i3 = (uint32_t)(asel ? ib : ia);
+    } else {
+      // i3 of this lane's row of the group (rows past the last real one repeat it), read
+      // from the lane of the row list that holds it
+      const int x = __builtin_amdgcn_readlane(d_ia, P) + (asel < X.cnt ? asel : X.cnt - 1);
+      const int lo = __builtin_amdgcn_ds_bpermute(4 * x, d_i3lo), hi = __builtin_amdgcn_ds_bpermute(4 * x, d_i3hi);
+      i3 = (uint32_t)(x < 64 ? lo : hi);
+    }
+    const uint32_t o = vo_d + i3 * G3ROW;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) X.d[k] = buf_f32(g3buf, o, 128u * k);
+    for (int k = 0; k < 8; ++k) X.d[k] = buf_f32(g3buf, o, 16u * D3 * k);
   };
 
   FPair XA, XB;
@@ -333,8 +376,10 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     d_ra = e_ra;
     d_ia = e_ia;
     d_ib = e_ib;
+    d_i3lo = e_i3lo;
+    d_i3hi = e_i3hi;
     np = e_np;
-    g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+    g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * (G3ROW / 4), (uint32_t)s.n3 * G3ROW);
     load_B();
     pair_load(XA, 0);
     pair_load(XB, np > 1 ? 1 : 0);
@@ -364,15 +409,23 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr_r[F32_SLICE * j + 4 * s4];
     };
     slice_begin(0);
-    // E rows of a pair through a descriptor that ends after the pair's real rows, so
-    // the missing second row of a lone last row is not written
+    // E rows of a group through a descriptor that ends after the group's real rows, so
+    // the rows past them (padding of a short group) are not written
     auto pair_compute = [&](const FPair& X) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 0; s4 < 8; ++s4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[s4], CT[s4], acc, 0, 0, 0);
-      // lane holds E[row orow][jj = l15][j3 = 4 (l4 & 1) + r]
-      const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * 128, X.has1 ? 1024u : 512u);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
+      const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * DW, (uint32_t)X.cnt * (4u * DW));
+      if (D3 == 8) {
+        // lane holds E[row l4 / 2][jj = l15][j3 = 4 (l4 & 1) + r]
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
+      } else {
+        // lane holds E[row 2 l4 + (r / 2)][jj = l15][j3 = r % 2]
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(acc[0]), __float_as_uint(acc[1])}, eb, vo_e, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(acc[2]), __float_as_uint(acc[3])}, eb,
+                                              vo_e + 4u * DW, 0, 0);
+      }
     };
     int cj = 0;
     auto step = [&](const FPair& X) {
@@ -409,8 +462,10 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       d_ra = e_ra;
       d_ia = e_ia;
       d_ib = e_ib;
+      d_i3lo = e_i3lo;
+      d_i3hi = e_i3hi;
       np = e_np;
-      g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * 256u, (uint32_t)s.n3 * 1024u);
+      g3buf = make_buf(G3 + (uint32_t)(t * s.n3) * (G3ROW / 4), (uint32_t)s.n3 * G3ROW);
       pair_load(XA, 0);
       pair_load(XB, np > 1 ? 1 : 0);
     }
@@ -827,8 +882,9 @@ bool fwd_r64_supported(const Shape& s, int64_t max_indices) {
 }
 
 bool fwd_r32_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit float offsets into E (rows x 128), G1 (slices of 128), G2 (slices of 4,096) and G3 (slices of 256)
-  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
+  // d = (4, 4, 8) or (4, 4, 2); 32-bit float offsets into E (rows x at most 128), G1 (slices of 128),
+  // G2 (slices of 4,096) and G3 (slices of at most 256) must fit (so do the 25-bit rows of a descriptor)
+  return s.d1 == 4 && s.d2 == 4 && (s.d3 == 8 || s.d3 == 2) && s.R == 32 && max_indices * 128 < (int64_t(1) << 31) &&
          (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) && (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) &&
          (int64_t)s.T * s.n2 * 4096 < (int64_t(1) << 31);
 }
@@ -843,7 +899,8 @@ hipError_t launch_forward(const Shape& s, const Work& w, const float* G1, const 
     if (fwd_r32_supported(s, M)) {
       const int blocks = persistent_grid() * F32_WG_PER_CU;
       prof_begin(prof, K_FWD_FUSED, st);
-      hipLaunchKernelGGL(k_fwd_r32, dim3(blocks), dim3(64 * F32_WAVES), 0, st, shape_args(s), G1, G2, G3,
+      hipLaunchKernelGGL(s.d3 == 8 ? k_fwd_r32<8> : k_fwd_r32<2>, dim3(blocks), dim3(64 * F32_WAVES), 0, st,
+                         shape_args(s), G1, G2, G3,
                          (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
                          (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.E);
       prof_end(prof, K_FWD_FUSED, st);

@@ -73,6 +73,8 @@ TINY = [
     dict(T=1, n=(100, 100, 100), d=(2, 2, 4), R=8, B=1000, single=True),
     dict(T=2, n=(9, 11, 13), d=(3, 5, 7), R=17, B=50, max_len=9),
     dict(T=4, n=(200, 200, 250), d=(4, 4, 4), R=16, B=512, single=True, zipf=1.05),
+    # D = 32 at R = 32 (the paper's operating point): MFMA forward over groups of eight rows
+    dict(T=2, n=(30, 20, 40), d=(4, 4, 2), R=32, B=300, max_len=20, zipf=1.1),
 ]
 
 
@@ -248,7 +250,11 @@ def test_config4_small_batch(lib, orc):
     check_forward(lib, orc, ttgen.make(4, bags=128), name="config4 B=128")
 
 
-@pytest.mark.parametrize("cfg", [3, 4])
+def test_config6_small_batch(lib, orc):
+    check_forward(lib, orc, ttgen.make(6, bags=256), name="config6 B=256")
+
+
+@pytest.mark.parametrize("cfg", [3, 4, 6])
 def test_full_size_sampled_bags(lib, orc, cfg):
     case = ttgen.make(cfg)
     bags = ttgen.sample_bags(cfg, case["T"], case["B"], 96)
@@ -313,10 +319,10 @@ def _edge(kind, d=(2, 2, 2), R=4):
     return case
 
 
-EDGE_SHAPES = [((2, 2, 2), 4), ((4, 4, 8), 32), ((4, 4, 8), 64)]
+EDGE_SHAPES = [((2, 2, 2), 4), ((4, 4, 8), 32), ((4, 4, 8), 64), ((4, 4, 2), 32)]
 
 
-@pytest.mark.parametrize("dR", EDGE_SHAPES, ids=["generic", "mfma_r32", "mfma_r64"])
+@pytest.mark.parametrize("dR", EDGE_SHAPES, ids=["generic", "mfma_r32", "mfma_r64", "mfma_r32_d32"])
 @pytest.mark.parametrize("kind", ["all_equal", "one_prefix", "distinct_prefixes"])
 def test_edge_index_patterns(lib, orc, kind, dR):
     # each pattern through the forward, the backward and the fused backward-and-SGD,
@@ -386,6 +392,22 @@ def test_forward_prefix_group_longer_than_a_chunk(lib, orc):
     assert sl.max() > 32, sl.max()
     check_forward(lib, orc, case, name="group of > 32 slices")
     check_backward(lib, orc, case, name="group of > 32 slices (generic backward)")
+
+
+def test_forward_d32_full_and_partial_row_groups(lib, orc):
+    # D = 32 = (4, 4, 2): the MFMA forward takes eight rows of a slice per product.  Hot
+    # prefixes give slices of 32 rows (four full groups) and the rest slices of one to a
+    # few rows (one partial group), across chunk ends and quads
+    n = (6, 4, 300)
+    case = _hot_prefix_case(7303, 2, n, B=200, hot=[(1, 1), (4, 2), (5, 3)], per_bag=16, d=(4, 4, 2), R=32)
+    emb = _make(lib, case)
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["fwd_fused"], case["idx"].size)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    g = emb.debug_grouping(case["idx"].size)
+    rows, sl, first, run = _run_slices(g, n)
+    assert rows.max() > 64 and (rows % 8 != 0).any() and (rows < 8).any()
+    check_forward(lib, orc, case, name="d=(4,4,2) hot prefixes")
 
 
 def test_backward_prefix_groups_across_chunk_ends(lib, orc):
@@ -537,7 +559,7 @@ def check_backward(lib, orc, case, name="", want=None):
     return emb, G, grads, ref, mag
 
 
-@pytest.mark.parametrize("k", [0, 1, 2, 3, 4, 5, 7])
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4, 5, 7, 9])
 def test_backward_small(lib, orc, k):
     c = dict(TINY[k])
     case = ttgen.tiny(3000 + k, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
