@@ -216,6 +216,10 @@ __device__ __forceinline__ unsigned xcd_block(unsigned b, unsigned grid) {
 // Device helpers.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+// the value of lane L ^ 1 (DPP quad permutation 1, 0, 3, 2)
+__device__ __forceinline__ float swap_neighbour(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
 
 template <typename T>
 __device__ __forceinline__ T wave_incl_scan(T v) {

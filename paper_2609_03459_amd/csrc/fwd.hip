@@ -179,21 +179,25 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* scr = scr_all + wave * F32_SCR;
   // this lane's stage-1 write base (slice l4, b = l15 (+ 16)) and stage-2 read base
-  // (row jj = (j1, j2) = l15, b = 4 s + l4)
+  // (row jj = (j1, j2) = l15, b = 4 s + l4 for D3 = 8, b = 8 l4 + s for D3 = 2)
   float* scr_w = scr + F32_SLICE * (lane >> 4) + (lane & 15);
-  const float* scr_r = scr + F32_ROW * (lane & 15) + (lane >> 4);
+  const float* scr_r = scr + F32_ROW * (lane & 15) + (D3 == 2 ? 8 : 1) * (lane >> 4);
   constexpr int GR = 16 / D3;              // rows per stage-2 group ("pair" below)
   constexpr int DW = 16 * D3;              // floats per E row
   constexpr uint32_t G3ROW = 128u * D3;    // bytes per G3 row (R d3 floats)
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
   // stage-2 A operand: lane m = l15 = (row asel of the group, j3), K index b = 4 s + l4
+  // (D3 = 8) or b = 8 l4 + s (D3 = 2)
   const int asel = l15 / D3;
-  // byte offsets: this lane's stage-2 A word in a G3 row (b = l4, j3 = l15 % D3; + 16 D3
-  // bytes per K step) and its E store: output row 4 l4 + r of the MFMA is group row
-  // (4 l4 + r) / D3, so for D3 = 8 four consecutive floats of row l4 / 2, for D3 = 2 two
-  // floats of rows 2 l4 and 2 l4 + 1 (the second 128 bytes on)
-  const uint32_t vo_d = 4u * (uint32_t)(l4 * D3 + (l15 % D3));
+  const bool odd_lane = (lane & 1) != 0;
+  // byte offsets: this lane's stage-2 A words in a G3 row and its E store.  D3 = 8: the
+  // word b = l4, j3 = l15 % 8, then 16 D3 bytes per K step.  D3 = 2: the lanes of j3 = 0
+  // and 1 of a row share the 64 bytes of b = 8 l4 .. 8 l4 + 7 (both j3), the even lane
+  // loading the first 32, the odd lane the second.  Output row 4 l4 + r of the MFMA is
+  // group row (4 l4 + r) / D3, so for D3 = 8 four consecutive floats of row l4 / 2, for
+  // D3 = 2 two floats of rows 2 l4 and 2 l4 + 1 (the second 128 bytes on)
+  const uint32_t vo_d = D3 == 8 ? 4u * (uint32_t)(l4 * D3 + (l15 % D3)) : 4u * (uint32_t)(16 * l4 + 8 * (l15 & 1));
   const uint32_t vo_e = D3 == 8 ? 4u * (uint32_t)((l4 >> 1) * 128 + l15 * 8 + 4 * (l4 & 1))
                                 : 4u * (uint32_t)(2 * l4 * DW + l15 * 2);
 
@@ -328,8 +332,14 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       i3 = (uint32_t)(x < 64 ? lo : hi);
     }
     const uint32_t o = vo_d + i3 * G3ROW;
+    if (D3 == 8) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) X.d[k] = buf_f32(g3buf, o, 16u * D3 * k);
+      for (int k = 0; k < 8; ++k) X.d[k] = buf_f32(g3buf, o, 16u * D3 * k);
+    } else {
+      const float4 lo = buf_f32x4(g3buf, o), hi = buf_f32x4(g3buf, o + 16u);
+      X.d[0] = lo.x; X.d[1] = lo.y; X.d[2] = lo.z; X.d[3] = lo.w;
+      X.d[4] = hi.x; X.d[5] = hi.y; X.d[6] = hi.z; X.d[7] = hi.w;
+    }
   };
 
   FPair XA, XB;
@@ -406,15 +416,29 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
     float CT[8];
     auto slice_begin = [&](int j) {
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr_r[F32_SLICE * j + 4 * s4];
+      for (int s4 = 0; s4 < 8; ++s4) CT[s4] = scr_r[F32_SLICE * j + (D3 == 2 ? 1 : 4) * s4];
     };
     slice_begin(0);
     // E rows of a group through a descriptor that ends after the group's real rows, so
     // the rows past them (padding of a short group) are not written
     auto pair_compute = [&](const FPair& X) {
+      float Aw[8];
+      if (D3 == 8) {
+#pragma unroll
+        for (int s4 = 0; s4 < 8; ++s4) Aw[s4] = X.d[s4];
+      } else {
+        // the even lane holds (b, j3) for b = 8 l4 + 0..3, the odd lane for b = 8 l4 + 4..7,
+        // both j3 interleaved; each keeps its own j3 and takes the rest from its neighbour
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float from_even = swap_neighbour(X.d[2 * i + 1]), from_odd = swap_neighbour(X.d[2 * i]);
+          Aw[i] = odd_lane ? from_even : X.d[2 * i];
+          Aw[4 + i] = odd_lane ? X.d[2 * i + 1] : from_odd;
+        }
+      }
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s4 = 0; s4 < 8; ++s4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[s4], CT[s4], acc, 0, 0, 0);
+      for (int s4 = 0; s4 < 8; ++s4) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Aw[s4], CT[s4], acc, 0, 0, 0);
       const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * DW, (uint32_t)X.cnt * (4u * DW));
       if (D3 == 8) {
         // lane holds E[row l4 / 2][jj = l15][j3 = 4 (l4 & 1) + r]
