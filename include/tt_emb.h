@@ -345,8 +345,9 @@ tt_emb_status tt_emb_profile(tt_emb_handle h, int kernel, void* ev_begin, void* 
 
 /* Whether `kernel` (TT_EMB_K_FWD_FUSED or TT_EMB_K_BWD_FUSED) runs on the
  * matrix cores for this handle: *uses_mfma = 1 for the MFMA kernels (forward
- * for the view d = (4,4,8) with R = 32 or 64; backward for d = (4,4,8) with
- * R = 32, n3 <= 252 and at most 64 tables, or with R = 64; all only while
+ * for the view d = (4,4,8) with R = 32 or 64 and for d = (4,4,2) with R = 32;
+ * backward for d = (4,4,8) or (4,4,2) with R = 32, n3 <= 252 and at most 64
+ * tables, and for d = (4,4,8) with R = 64; all only while
  * their 32-bit offsets into E and the cores fit and, at R = 64, a table's
  * third core spans under 4 GiB), 0 for the generic vector-ALU kernels.
  * Both decide per call from its index count, given here as num_indices

@@ -1,4 +1,5 @@
-// Backward pass for d = (4, 4, 8), R = 32 (D = 128) on MFMA (FlowTT Section 3.2, Eq. 1).
+// Backward pass for R = 32 and d = (4, 4, 8) (D = 128) or d = (4, 4, 2) (D = 32) on MFMA
+// (FlowTT Section 3.2, Eq. 1).
 //
 // Work is split by table t and by half h of the rank index b of the last
 // core (b = 16 h + b'), so each (t, h) owner does its half of every product
@@ -13,6 +14,8 @@
 // dA_h of a slice go to scratch; three small kernels finish dG1, dG2 and dG3
 // by fixed-order segment sums.  Workgroup blockIdx % (2T) owns (t, h), so
 // with T = 8 every table lives on one XCD (blockIdx % 8).
+// The per-row products take the rows of a slice in groups of 16 / d3 (pairs for
+// d3 = 8, eights for d3 = 2), so that a group's (row, j3) columns fill one MFMA tile.
 #include "common.h"
 
 namespace ttemb {
@@ -28,7 +31,7 @@ constexpr int BW_WAVES = 8;
 constexpr int SCR_PITCH = 68;
 constexpr int BW_SCR = 16 * SCR_PITCH;
 
-// The LDS dG3 accumulator holds, per table row i3, 128 floats ordered
+// The LDS dG3 accumulator holds, per table row i3, 16 d3 floats ordered
 // [j3][16 slots]: rank row b' = 4 g + r of column j3 sits at slot
 // 4 ((g + (j3 >> 1)) & 3) + r.  A dD tile gives lane (j3, g) the four
 // consecutive slots of its column, and the rotation by j3 >> 1 spreads the
@@ -57,8 +60,12 @@ __device__ __forceinline__ uint64_t lds_cas_old(uint64_t* u, uint64_t cmp, uint6
 }
 
 
-// operands of one row pair (rows r0 and r0 + 1 of a slice; a lone last row pairs
-// with a row of zeros, which its buffer loads return past the end of the pair)
+// operands of one row group.  d3 = 8: rows r0 and r0 + 1 of a slice (a lone last
+// row pairs with a row of zeros, which its buffer loads return past the end of the
+// pair), with the layouts below.  d3 = 2: up to eight rows (rows past the last read
+// as zeros), with eb the 16 bytes of dE[row l15 / 2][8 l4 .. 8 l4 + 7] this lane loads
+// (the first half on even lanes, the second on odd), e4 = dE[rows 2 l4, 2 l4 + 1][2 l15
+// .. 2 l15 + 1] and d4 = G3[i3 of those rows][16 h + l15][0 .. 1]
 struct BwPair {
   float eb[4];  // dD B operand: dE[row][(4 s + l4) * 8 + j3], row r0 in lanes 0-7 of each 16, r0 + 1 in 8-15
   float4 e4;    // dC A operand: dE[row l4 >> 1][l15 * 8 + 4 (l4 & 1) + k]
@@ -69,6 +76,7 @@ struct BwPair {
   int j;        // the pair's slice within the quad (wave-uniform)
 };
 
+template <int D3>
 __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     k_bwd_r32(ShapeArgs s, const float* __restrict__ G1, const float* __restrict__ G2, const float* __restrict__ G3,
               const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
@@ -78,37 +86,46 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int acc_n = s.n3 * 128;
+  constexpr int GR = 16 / D3;     // rows per group
+  constexpr int DW = 16 * D3;     // floats per dE row
+  constexpr int AROW = 16 * D3;   // floats per accumulator row (half the rank of a G3 row)
+  const int acc_n = s.n3 * AROW;
+  // d3 = 2: eight more rows after the table's, which the columns of a group's missing
+  // rows (exact zeros) go to, one per row position, so they never meet a live column
+  const int acc_lds = acc_n + (D3 == 2 ? 8 * AROW : 0);
   float* g3acc = lds;  // [n3][j3][16 slots]
-  float* scr = lds + acc_n + wave * BW_SCR;
+  float* scr = lds + acc_lds + wave * BW_SCR;
   const int nq = 2 * s.T;
   const int q = blockIdx.x % nq;
   const int t = q % s.T, h = q / s.T;
   int32_t* qctr = ctr + C_BWD_CTR + q * SCHED_STRIDE;  // the owner's queue: all of table t's chunks
 
-  for (int i = threadIdx.x; i < acc_n; i += blockDim.x) g3acc[i] = 0.f;
+  for (int i = threadIdx.x; i < acc_lds; i += blockDim.x) g3acc[i] = 0.f;
   __syncthreads();
 
   const int c_lo = (int)run_base[t * s.n2], c_hi = (int)run_base[(t + 1) * s.n2];
   const int nch = c_hi - c_lo;
   const int l15 = lane & 15, l4 = lane >> 4;
-  const bool rowsel = (l15 >> 3) != 0;  // dD column of row r0 + 1
-  const bool prow = (l4 >> 1) != 0;     // dC K slots of row r0 + 1
+  const bool rowsel = (l15 >> 3) != 0;  // d3 = 8: dD column of row r0 + 1
+  const bool prow = (l4 >> 1) != 0;     // d3 = 8: dC K slots of row r0 + 1
+  const int asel = l15 / D3;            // group row of this lane's dD column
+  const bool odd_lane = (lane & 1) != 0;
   // per-lane float offsets; every operand is a uniform base plus one of these
-  // byte offsets of this lane's operand words: in a pair's two dE rows (the second
-  // row 512 bytes on) and in a G3[t] row
-  const uint32_t vo_eb = 4u * (uint32_t)(l4 * 8 + (lane & 7) + (rowsel ? 128 : 0));
-  const uint32_t vo_e4 = 4u * (uint32_t)(l15 * 8 + 4 * (l4 & 1) + (prow ? 128 : 0));
-  const uint32_t vo_d4 = 4u * (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1));
-  const uint32_t o_g3 = g3_slot_base(lane & 7, l4);  // this lane's four dD values in an accumulator row
+  // byte offsets of this lane's operand words: in a group's dE rows and in a G3[t] row
+  const uint32_t vo_eb = D3 == 8 ? 4u * (uint32_t)(l4 * 8 + (lane & 7) + (rowsel ? 128 : 0))
+                                 : 4u * (uint32_t)(DW * asel + 8 * l4 + 4 * (lane & 1));
+  const uint32_t vo_e4 = D3 == 8 ? 4u * (uint32_t)(l15 * 8 + 4 * (l4 & 1) + (prow ? 128 : 0))
+                                 : 4u * (uint32_t)(2 * l4 * DW + 2 * l15);
+  const uint32_t vo_d4 = D3 == 8 ? 4u * (uint32_t)((16 * h + l15) * 8 + 4 * (l4 & 1)) : 4u * (uint32_t)((16 * h + l15) * 2);
+  const uint32_t o_g3 = g3_slot_base(l15 % D3, l4);  // this lane's four dD values in an accumulator row
   const float* G1t = G1 + (uint32_t)(t * s.n1) * 128u;
-  const float* G3t = G3 + (uint32_t)(t * s.n3) * 256u;
+  const float* G3t = G3 + (uint32_t)(t * s.n3) * (32u * D3);
   // this lane's scratch bases: C write (row 4 l4 + r, column 16 nt + l15), dC write
   // (row 4 j + l4, column 16 r + l15) and dA operand read (row l15, columns 16 l4 + s)
   float* scr_c = scr + 4 * SCR_PITCH * l4 + l15;
   float* scr_d = scr + SCR_PITCH * l4 + l15;
   const float* scr_a = scr + SCR_PITCH * l15 + 16 * l4;
-  const buf_t g3buf = make_buf(G3t, (uint32_t)s.n3 * 1024u);
+  const buf_t g3buf = make_buf(G3t, (uint32_t)s.n3 * (128u * D3));
 
   int cursor = 0;
   int cur_run = -1;
@@ -122,50 +139,109 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   // other lanes have no rows): first row, row count, i1
   int c_rb = 0, c_nr = 0, c_i1 = 0;
   int qd = 0;  // first slice of the current quad within the chunk
-  // Row-pair descriptors of a quad, lane P holding pair P (P < np; slice j owns
-  // (nr_j + 1) / 2 consecutive pairs): the pair's first row, and packed, i3 of its
-  // two rows (8 bits each, n3 <= 256), its slice j and whether the second row is
-  // real.  Built one quad ahead (e_*) so the i3 loads are in flight meanwhile.
+  // Row-group descriptors of a quad, lane P holding group P (P < np; slice j owns
+  // ceil(nr_j / GR) consecutive groups): the group's first row, and packed, for
+  // d3 = 8 i3 of its two rows (8 bits each, n3 <= 256), its slice j and whether the
+  // second row is real; for d3 = 2 the position of its first row in the quad's row
+  // list (slice 0's rows, then slice 1's, ...: at most 128), its slice j and its row
+  // count - 1, with the list's i3 values in lanes L and L + 64 of d_i3lo / d_i3hi.
+  // Built one quad ahead (e_*) so the i3 loads are in flight meanwhile.
   int d_ra = 0, d_pk = 0, np = 0;
   int e_ra = 0, e_ia = 0, e_ib = 0, e_jh = 0, e_np = 0;
+  int d_i3lo = 0, d_i3hi = 0, e_i3lo = 0, e_i3hi = 0;
   auto build_desc = [&](int qd0) {
     const int n0 = __builtin_amdgcn_readlane(c_nr, qd0), n1 = __builtin_amdgcn_readlane(c_nr, qd0 + 1);
     const int n2 = __builtin_amdgcn_readlane(c_nr, qd0 + 2), n3 = __builtin_amdgcn_readlane(c_nr, qd0 + 3);
     const int b0 = __builtin_amdgcn_readlane(c_rb, qd0), b1 = __builtin_amdgcn_readlane(c_rb, qd0 + 1);
     const int b2 = __builtin_amdgcn_readlane(c_rb, qd0 + 2), b3 = __builtin_amdgcn_readlane(c_rb, qd0 + 3);
-    const int q1 = (n0 + 1) >> 1, q2 = q1 + ((n1 + 1) >> 1), q3 = q2 + ((n2 + 1) >> 1);
-    e_np = q3 + ((n3 + 1) >> 1);
-    // pair P of slice j starts at row base_j + 2 P and has a second row iff
-    // 2 P + 1 < lim_j, with the wave-uniform base_j = b_j - 2 q_j, lim_j = n_j + 2 q_j
+    const int q1 = (n0 + GR - 1) / GR, q2 = q1 + (n1 + GR - 1) / GR, q3 = q2 + (n2 + GR - 1) / GR;
+    e_np = q3 + (n3 + GR - 1) / GR;
+    // group P of slice j starts at row base_j + GR P and holds min(GR, lim_j - GR P)
+    // rows, with the wave-uniform base_j = b_j - GR q_j, lim_j = n_j + GR q_j
     const bool s1 = lane >= q1, s2 = lane >= q2, s3 = lane >= q3;
     const int j = (int)s1 + (int)s2 + (int)s3;
     int base = b0, lim = n0;
-    base = s1 ? b1 - 2 * q1 : base;
-    lim = s1 ? n1 + 2 * q1 : lim;
-    base = s2 ? b2 - 2 * q2 : base;
-    lim = s2 ? n2 + 2 * q2 : lim;
-    base = s3 ? b3 - 2 * q3 : base;
-    lim = s3 ? n3 + 2 * q3 : lim;
+    base = s1 ? b1 - GR * q1 : base;
+    lim = s1 ? n1 + GR * q1 : lim;
+    base = s2 ? b2 - GR * q2 : base;
+    lim = s2 ? n2 + GR * q2 : lim;
+    base = s3 ? b3 - GR * q3 : base;
+    lim = s3 ? n3 + GR * q3 : lim;
     const bool ok = lane < e_np;
-    const bool has1 = ok && 2 * lane + 1 < lim;
-    e_ra = ok ? base + 2 * lane : b0;  // lanes past the quad's pairs keep a valid row
-    e_ia = uniq_i3[e_ra];
-    e_ib = uniq_i3[has1 ? e_ra + 1 : e_ra];
-    e_jh = (j << 16) | (has1 ? 1 << 18 : 0);
+    e_ra = ok ? base + GR * lane : b0;  // lanes past the quad's groups keep a valid row
+    if (D3 == 8) {
+      const bool has1 = ok && 2 * lane + 1 < lim;
+      e_ia = uniq_i3[e_ra];
+      e_ib = uniq_i3[has1 ? e_ra + 1 : e_ra];
+      e_jh = (j << 16) | (has1 ? 1 << 18 : 0);
+    } else {
+      const int left = lim - GR * lane;
+      const int cnt = ok ? (left < GR ? left : GR) : 1;
+      // the quad's row list: slice j's rows at positions p_j .. p_j + n_j - 1
+      const int p1 = n0, p2 = p1 + n1, p3 = p2 + n2, ptot = p3 + n3;
+      auto list_row = [&](int x) {  // row at position x (x < ptot), else a valid row
+        const bool t1 = x >= p1, t2 = x >= p2, t3 = x >= p3;
+        int r = b0 + x;
+        r = t1 ? b1 + x - p1 : r;
+        r = t2 ? b2 + x - p2 : r;
+        r = t3 ? b3 + x - p3 : r;
+        return x < ptot ? r : b0;
+      };
+      e_i3lo = uniq_i3[list_row(lane)];
+      e_i3hi = uniq_i3[list_row(lane + 64)];
+      int pj = 0, qj = 0;
+      pj = s1 ? p1 : pj;
+      qj = s1 ? q1 : qj;
+      pj = s2 ? p2 : pj;
+      qj = s2 ? q2 : qj;
+      pj = s3 ? p3 : pj;
+      qj = s3 ? q3 : qj;
+      e_ia = ok ? pj + GR * (lane - qj) : 0;
+      e_ib = 0;
+      e_jh = (j << 16) | ((cnt - 1) << 19);
+    }
   };
   auto pair_load = [&](BwPair& X, int P) {
     const int ra = __builtin_amdgcn_readlane(d_ra, P), pk = __builtin_amdgcn_readlane(d_pk, P);
-    const int i3a = pk & 255, i3b = (pk >> 8) & 255;
-    const bool has1 = (pk >> 18) & 1;
     X.j = (pk >> 16) & 3;
-    // rows ra and ra + 1 through one descriptor that ends after the rows that exist
-    const buf_t eb = make_buf(dE + (size_t)(uint32_t)ra * 128, has1 ? 1024u : 512u);
+    if (D3 == 8) {
+      const int i3a = pk & 255, i3b = (pk >> 8) & 255;
+      const bool has1 = (pk >> 18) & 1;
+      // rows ra and ra + 1 through one descriptor that ends after the rows that exist
+      const buf_t eb = make_buf(dE + (size_t)(uint32_t)ra * 128, has1 ? 1024u : 512u);
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = buf_f32(eb, vo_eb, 128u * s4);
-    X.e4 = buf_f32x4(eb, vo_e4);
-    X.d4 = buf_f32x4(g3buf, vo_d4 + (uint32_t)(prow ? i3b : i3a) * 1024u);
-    const int i3z = i3a > 0 ? i3a - 1 : (s.n3 > 1 ? 1 : 0);
-    X.i3m = rowsel ? (has1 ? i3b : i3z) : i3a;
+      for (int s4 = 0; s4 < 4; ++s4) X.eb[s4] = buf_f32(eb, vo_eb, 128u * s4);
+      X.e4 = buf_f32x4(eb, vo_e4);
+      X.d4 = buf_f32x4(g3buf, vo_d4 + (uint32_t)(prow ? i3b : i3a) * 1024u);
+      const int i3z = i3a > 0 ? i3a - 1 : (s.n3 > 1 ? 1 : 0);
+      X.i3m = rowsel ? (has1 ? i3b : i3z) : i3a;
+    } else {
+      const int x0 = pk & 255, cnt = ((pk >> 19) & 7) + 1;
+      // the group's rows through one descriptor that ends after its last real row
+      const buf_t eb = make_buf(dE + (size_t)(uint32_t)ra * DW, (uint32_t)cnt * (4u * DW));
+      const float4 v = buf_f32x4(eb, vo_eb);
+      X.eb[0] = v.x;
+      X.eb[1] = v.y;
+      X.eb[2] = v.z;
+      X.eb[3] = v.w;
+      const float2 e0 = buf_f32x2(eb, vo_e4), e1 = buf_f32x2(eb, vo_e4 + 4u * DW);
+      X.e4 = make_float4(e0.x, e0.y, e1.x, e1.y);
+      // i3 of group row k (rows past the last real one repeat it), from the lane of the
+      // row list that holds it (a cross-lane read: every call runs on all lanes)
+      auto i3_at = [&](int k) {
+        const int x = x0 + (k < cnt ? k : cnt - 1);
+        const int lo = __builtin_amdgcn_ds_bpermute(4 * x, d_i3lo), hi = __builtin_amdgcn_ds_bpermute(4 * x, d_i3hi);
+        return x < 64 ? lo : hi;
+      };
+      const int r0 = i3_at(2 * l4), r1 = i3_at(2 * l4 + 1);
+      const float2 g0 = buf_f32x2(g3buf, vo_d4 + (uint32_t)r0 * (128u * D3));
+      const float2 g1 = buf_f32x2(g3buf, vo_d4 + (uint32_t)r1 * (128u * D3));
+      X.d4 = make_float4(g0.x, g0.y, g1.x, g1.y);
+      // read on every lane, outside the select: a lane whose own row is missing can
+      // still hold a list entry that another lane's row needs
+      const int ia = i3_at(asel);
+      X.i3m = asel < cnt ? ia : s.n3 + asel;
+    }
   };
 
   int f = 0, ns = 0, run = -1;
@@ -227,6 +303,8 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   auto prefetch_quad = [&]() {
     d_ra = e_ra;
     d_pk = e_ia | (e_ib << 8) | e_jh;
+    d_i3lo = e_i3lo;
+    d_i3hi = e_i3hi;
     np = e_np;
     if (qd + 4 < ns) build_desc(qd + 4);  // the quad after it, one quad ahead
     const int nq4 = ns - qd < 4 ? ns - qd : 4;
@@ -291,27 +369,49 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
         for (int r = 0; r < 4; ++r) scr_c[SCR_PITCH * r + 16 * nt] = Cs[nt][r];
       wave_lds_sync();
     }
-    // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4]
+    // per slice: dD A operand C_h^T[b' = l15][(j1 j2) = 4 s + l4] (d3 = 8) or
+    // C_h^T[b' = l15][(j1 j2) = 4 l4 + s] (d3 = 2)
     float CT[4];
     auto slice_begin = [&](int j) {
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4) CT[s4] = scr[4 * SCR_PITCH * j + SCR_PITCH * s4 + lane];  // row 4 j + s4
+      for (int s4 = 0; s4 < 4; ++s4) {
+        if (D3 == 8)
+          CT[s4] = scr[4 * SCR_PITCH * j + SCR_PITCH * s4 + lane];  // row 4 j + s4
+        else
+          CT[s4] = scr[4 * SCR_PITCH * j + SCR_PITCH * l4 + 16 * s4 + l15];  // row 4 j + l4
+      }
     };
     slice_begin(0);
     f32x4 dC = {0.f, 0.f, 0.f, 0.f};
     auto pair_compute = [&](const BwPair& X) {
       // this lane's accumulator words, read before the products so the read's
       // latency overlaps them
-      float* ap = g3acc + (uint32_t)X.i3m * 128u + o_g3;
+      float* ap = g3acc + (uint32_t)X.i3m * AROW + o_g3;
       const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(ap);
+      float ebk[4];
+      if (D3 == 8) {
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) ebk[s4] = X.eb[s4];
+      } else {
+        // dE[row][(4 l4 + s) * 2 + j3]: the even lane holds s = 0, 1 of both j3, the odd
+        // lane s = 2, 3; each keeps its own j3 and takes the rest from its neighbour.
+        // The swaps run on every lane before the selects: inside a conditional they
+        // would run under a partial lane mask, where a neighbour's value is not read
+        const float w0 = swap_neighbour(X.eb[0]), w1 = swap_neighbour(X.eb[1]);
+        const float w2 = swap_neighbour(X.eb[2]), w3 = swap_neighbour(X.eb[3]);
+        ebk[0] = odd_lane ? w1 : X.eb[0];
+        ebk[1] = odd_lane ? w3 : X.eb[2];
+        ebk[2] = odd_lane ? X.eb[1] : w0;
+        ebk[3] = odd_lane ? X.eb[3] : w2;
+      }
       f32x4 dd = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], X.eb[s4], dd, 0, 0, 0);
+      for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(CT[s4], ebk[s4], dd, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.x, X.d4.x, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.y, X.d4.y, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.z, X.d4.z, dC, 0, 0, 0);
       dC = __builtin_amdgcn_mfma_f32_16x16x4f32(X.e4.w, X.d4.w, dC, 0, 0, 0);
-      // dd: lane holds dD_h[b' = 4 l4 + r][row][j3 = lane & 7]
+      // dd: lane holds dD_h[b' = 4 l4 + r][group row l15 / d3][j3 = l15 % d3]
       // every lane swaps (the zero row's column adds exact zeros), so the add is
       // straight-line code and the read stays ahead of the products; the previous
       // pair's swaps are checked first, this pair's at the next pair
@@ -419,7 +519,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   }
   acc_finish();
   __syncthreads();
-  float* gdst = g3part + (size_t)blockIdx.x * acc_n;
+  float* gdst = g3part + (size_t)blockIdx.x * acc_n;  // the table's rows only
   for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
 }
 
@@ -534,11 +634,12 @@ __device__ __forceinline__ void reduce_g2(int rh, const uint32_t* __restrict__ r
 
 // dG3[t][i3][16 h + b'][j3] = sum over the workgroups that owned (t, h); block xb of
 // owner q covers accumulator elements [512 xb, 512 xb + 512)
+template <int D3>
 __device__ __forceinline__ void reduce_g3(int q, int xb, ShapeArgs s, const float* __restrict__ g3part, int nwg,
                                           float* __restrict__ dG3, float lr, bool update) {
   const int nq = 2 * s.T;
   const int t = q % s.T, h = q / s.T;
-  const int acc_n = s.n3 * 128;
+  const int acc_n = s.n3 * 16 * D3;
   const int e = xb * RED_THREADS + threadIdx.x;
   if (e >= acc_n) return;
   // four independent sums, so that four loads are in flight
@@ -552,13 +653,14 @@ __device__ __forceinline__ void reduce_g3(int q, int xb, ShapeArgs s, const floa
   }
   for (; w < nwg; w += nq) a0 += g3part[(int64_t)w * acc_n + e];
   const float acc = (a0 + a1) + (a2 + a3);
-  const int i3 = e >> 7, j3 = (e >> 4) & 7, bp = g3_unslot(j3, e & 15);
-  put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * 8 + j3, acc, lr, update);
+  const int i3 = e / (16 * D3), j3 = (e >> 4) % D3, bp = g3_unslot(j3, e & 15);
+  put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * D3 + j3, acc, lr, update);
 }
 
 // The three reductions in one launch, so they overlap: the first blocks reduce dG3
 // (few blocks, each a chain of one load per owner workgroup), the next T n1 dG1,
 // the rest (2 T n2) dG2.
+template <int D3>
 __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const uint32_t* __restrict__ dense_cnt,
                                                               const uint32_t* __restrict__ dense_base,
                                                               const float* __restrict__ dApart, int nsl_cap,
@@ -568,10 +670,10 @@ __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const
                                                               float* __restrict__ dG1, float* __restrict__ dG2,
                                                               float* __restrict__ dG3, float lr, bool update) {
   const int b = blockIdx.x;
-  const int per_q = (s.n3 * 128 + RED_THREADS - 1) / RED_THREADS;
+  const int per_q = (s.n3 * 16 * D3 + RED_THREADS - 1) / RED_THREADS;
   const int n3b = 2 * s.T * per_q, n1b = s.T * s.n1;
   if (b < n3b) {
-    reduce_g3(b / per_q, b % per_q, s, g3part, nwg, dG3, lr, update);
+    reduce_g3<D3>(b / per_q, b % per_q, s, g3part, nwg, dG3, lr, update);
   } else if (b < n3b + n1b) {
     reduce_g1(b - n3b, s, dense_cnt, dense_base, dApart, nsl_cap, dG1, lr, update);
   } else {
@@ -580,10 +682,11 @@ __global__ void __launch_bounds__(RED_THREADS) k_reduce_grads(ShapeArgs s, const
 }
 
 bool bwd_r32_supported(const Shape& s, int64_t max_indices) {
-  // 32-bit float offsets into dE (rows x 128), G1 (slices of 128), G2 (slices of 4,096) and G3 (slices
-  // of 256) must fit
+  // d = (4, 4, 8) or (4, 4, 2); 32-bit float offsets into dE (rows x at most 128), G1 (slices of 128),
+  // G2 (slices of 4,096) and G3 (slices of at most 256) must fit
   // LDS: the n3 x 128 accumulator plus 8 x 16 x SCR_PITCH scratch floats fit 160 KB for n3 <= 252
-  return s.d1 == 4 && s.d2 == 4 && s.d3 == 8 && s.R == 32 && s.n3 <= 252 && s.T <= 64 &&
+  // (d3 = 8); i3 travels in 8 bits (d3 = 8) and the row list of d3 = 2 keeps the same bound
+  return s.d1 == 4 && s.d2 == 4 && (s.d3 == 8 || s.d3 == 2) && s.R == 32 && s.n3 <= 252 && s.T <= 64 &&
          max_indices * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n3 * 256 < (int64_t(1) << 31) &&
          (int64_t)s.T * s.n1 * 128 < (int64_t(1) << 31) && (int64_t)s.T * s.n2 * 4096 < (int64_t(1) << 31);
 }
@@ -600,17 +703,19 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   if (grid > MAX_BWD_WG || nq * SCHED_STRIDE > C_TOTAL - C_BWD_CTR) return hipErrorInvalidValue;
   hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), nq * SCHED_STRIDE, 0u, st);
   if (e != hipSuccess) return e;
-  const size_t lds = sizeof(float) * ((size_t)s.n3 * 128 + BW_WAVES * BW_SCR);
-  e = hipFuncSetAttribute((const void*)k_bwd_r32, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  const bool d8 = s.d3 == 8;
+  const size_t lds = sizeof(float) * ((size_t)(s.n3 + (d8 ? 0 : 8)) * 16 * s.d3 + BW_WAVES * BW_SCR);
+  const void* kfn = d8 ? (const void*)k_bwd_r32<8> : (const void*)k_bwd_r32<2>;
+  e = hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   prof_begin(prof, K_BWD_FUSED, st);
-  hipLaunchKernelGGL(k_bwd_r32, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
+  hipLaunchKernelGGL(d8 ? k_bwd_r32<8> : k_bwd_r32<2>, dim3(grid), dim3(64 * BW_WAVES), lds, st, shape_args(s), G1, G2, G3,
                      (const float*)w.E, (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
                      (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.g3part,
                      (int)w.nsl_max, (int)w.nch_max);
   prof_end(prof, K_BWD_FUSED, st);
-  const int red_blocks = s.T * s.n1 + 2 * s.T * s.n2 + nq * ((s.n3 * 128 + RED_THREADS - 1) / RED_THREADS);
-  hipLaunchKernelGGL(k_reduce_grads, dim3(red_blocks), dim3(RED_THREADS), 0, st, shape_args(s),
+  const int red_blocks = s.T * s.n1 + 2 * s.T * s.n2 + nq * ((s.n3 * 16 * s.d3 + RED_THREADS - 1) / RED_THREADS);
+  hipLaunchKernelGGL(d8 ? k_reduce_grads<8> : k_reduce_grads<2>, dim3(red_blocks), dim3(RED_THREADS), 0, st, shape_args(s),
                      (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base, (const float*)w.dApart,
                      (int)w.nsl_max, (const uint32_t*)w.run_nch, (const float*)w.dBpart, (int)w.nch_max,
                      (const float*)w.g3part, grid, dG1, dG2, dG3, lr, update);

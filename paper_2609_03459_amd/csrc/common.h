@@ -430,6 +430,9 @@ __device__ __forceinline__ buf_t make_buf(const void* base, uint32_t num_bytes) 
 __device__ __forceinline__ float buf_f32(buf_t r, uint32_t off, uint32_t soff = 0) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, soff, 0));
 }
+__device__ __forceinline__ float2 buf_f32x2(buf_t r, uint32_t off) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
 __device__ __forceinline__ float4 buf_f32x4(buf_t r, uint32_t off) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }

@@ -429,6 +429,8 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       } else {
         // the even lane holds (b, j3) for b = 8 l4 + 0..3, the odd lane for b = 8 l4 + 4..7,
         // both j3 interleaved; each keeps its own j3 and takes the rest from its neighbour
+        // (the swaps run on every lane, outside the selects, so that no lane mask hides a
+        // neighbour's value)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float from_even = swap_neighbour(X.d[2 * i + 1]), from_odd = swap_neighbour(X.d[2 * i]);

@@ -410,6 +410,31 @@ def test_forward_d32_full_and_partial_row_groups(lib, orc):
     check_forward(lib, orc, case, name="d=(4,4,2) hot prefixes")
 
 
+def test_backward_d32_full_and_partial_row_groups(lib, orc):
+    # D = 32 = (4, 4, 2) on the MFMA backward, which takes eight rows of a slice per
+    # product: slices of 32 rows (four full groups) and of one to a few rows (a partial
+    # group, whose missing rows add zeros elsewhere), across chunk ends and quads; the
+    # gradients and the fused update against the oracle
+    n = (6, 4, 250)
+    case = _hot_prefix_case(7304, 2, n, B=200, hot=[(1, 1), (4, 2), (5, 3)], per_bag=16, d=(4, 4, 2), R=32)
+    emb = _make(lib, case)
+    M = case["idx"].size
+    assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
+    _, idx, off = _dev(case)
+    emb.group(idx, off, num_bags=case["B"])
+    g = emb.debug_grouping(M)
+    rows, sl, first, run = _run_slices(g, n)
+    assert rows.max() > 64 and (rows % 8 != 0).any() and (rows < 8).any()
+    check_backward(lib, orc, case, name="d=(4,4,2) hot prefixes")
+    _say("[bwd+sgd] d=(4,4,2) hot prefixes")
+    G, idx, off = _dev(case)
+    dV = torch.from_numpy(np.ascontiguousarray(case["dV"])).cuda()
+    emb.backward_sgd(*G, idx, off, dV, 0.01, num_bags=case["B"], reuse_grouping=False)
+    torch.cuda.synchronize()
+    assert emb.check_errors() == 0
+    _check_sgd(orc, case, G, 0.01, "d=(4,4,2) hot prefixes")
+
+
 def test_backward_prefix_groups_across_chunk_ends(lib, orc):
     # twelve prefixes of one (table, i2) run, each with nearly all 250 suffixes: groups
     # of 7-8 work slices, so the run's slices fill several chunks and groups straddle
@@ -566,15 +591,20 @@ def test_backward_small(lib, orc, k):
     check_backward(lib, orc, case, name=f"tiny{k}")
 
 
-@pytest.mark.parametrize("T,n", [
-    (2, (6, 5, 252)),   # MFMA backward at its limit: the dG3 half plus scratch fill all 160 KB of LDS
-    (2, (6, 5, 253)),   # one past it: the generic kernels
-    (64, (2, 2, 9)),    # MFMA backward at its table limit (64 tables, 128 owners)
+@pytest.mark.parametrize("T,n,d,mfma", [
+    (2, (6, 5, 252), (4, 4, 8), True),   # MFMA backward at its limit: the dG3 half plus scratch fill all 160 KB of LDS
+    (2, (6, 5, 253), (4, 4, 8), False),  # one past it: the generic kernels
+    (64, (2, 2, 9), (4, 4, 8), True),    # MFMA backward at its table limit (64 tables, 128 owners)
+    (2, (6, 5, 252), (4, 4, 2), True),   # D = 32: the same n3 limit (i3 in 8-bit fields)
+    (2, (6, 5, 253), (4, 4, 2), False),
+    (64, (2, 2, 9), (4, 4, 2), True),
 ])
-def test_backward_shape_limits(lib, orc, T, n):
-    case = ttgen.tiny(3100 + n[2] + T, T, n, (4, 4, 8), 32, B=24, max_len=10, zipf=1.1)
-    check_backward(lib, orc, case, name=f"limits T={T} n3={n[2]}")
-    check_forward(lib, orc, case, name=f"limits T={T} n3={n[2]}")
+def test_backward_shape_limits(lib, orc, T, n, d, mfma):
+    case = ttgen.tiny(3100 + n[2] + T + d[2], T, n, d, 32, B=24, max_len=10, zipf=1.1)
+    emb = _make(lib, case)
+    assert bool(lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], case["idx"].size)) == mfma
+    check_backward(lib, orc, case, name=f"limits T={T} n3={n[2]} d={d}")
+    check_forward(lib, orc, case, name=f"limits T={T} n3={n[2]} d={d}")
 
 
 def _row_runs_case(seed, d, R):
@@ -605,8 +635,9 @@ def test_backward_rows_across_dE_chunk_ends(lib, orc, d, R):
     check_backward(lib, orc, _row_runs_case(3300 + R, d, R), name=f"row runs d={d} R={R}")
 
 
-def test_backward_config5_small_batch(lib, orc):
-    check_backward(lib, orc, ttgen.make(5, bags=64), name="config5 B=64")
+@pytest.mark.parametrize("cfg", [5, 6])
+def test_backward_small_batch(lib, orc, cfg):
+    check_backward(lib, orc, ttgen.make(cfg, bags=64), name=f"config{cfg} B=64")
 
 
 def _table_case(case, t):
@@ -666,17 +697,19 @@ def _sel(a, T, want_k):
     return a.reshape(T * a.shape[1], -1)[np.flatnonzero(want_k)]
 
 
-def test_backward_config5_full_hottest_slices(lib, orc):
-    # The training workload at full size, in the launch sequence the benchmark
-    # times (forward with grouping, then the backward reusing it): every table's
-    # most-used slice of each core (about 80k occurrences summed into one dG3
-    # slice) plus random slices, element by element against the oracle; then the
-    # fused backward-and-SGD call on the same grouping, the call the benchmark times.
-    case = ttgen.make(5)
+@pytest.mark.parametrize("cfg", [5, 6])
+def test_backward_full_hottest_slices(lib, orc, cfg):
+    # The training workloads at full size (D = 128 and D = 32, both on the R = 32 MFMA
+    # backward), in the launch sequence the benchmark times (forward with grouping,
+    # then the backward reusing it): every table's most-used slice of each core (tens
+    # of thousands of occurrences summed into one dG3 slice) plus random slices,
+    # element by element against the oracle; then the fused backward-and-SGD call on
+    # the same grouping, the call the benchmark times.
+    case = ttgen.make(cfg)
     T, B, lr = case["T"], case["B"], case["lr"]
     M = int(case["idx"].size)
     want = _hottest_slices(case, extra_tables=(0, T - 1))
-    _say(f"[bwd] config5 full, hottest + random slices ({sum(int(w.sum()) for w in want)} slices)")
+    _say(f"[bwd] config{cfg} full, hottest + random slices ({sum(int(w.sum()) for w in want)} slices)")
     emb = _make(lib, case)
     assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
     G, idx, off = _dev(case)
@@ -689,10 +722,10 @@ def test_backward_config5_full_hottest_slices(lib, orc):
     mag = _oracle_backward_by_table(orc, abs_case(case), want)
     for k in range(3):
         g = grads[k].cpu().numpy()
-        assert_close(f"dG{k + 1} config5 full (hottest slices)", _sel(g, T, want[k]), _sel(ref[k], T, want[k]),
+        assert_close(f"dG{k + 1} config{cfg} full (hottest slices)", _sel(g, T, want[k]), _sel(ref[k], T, want[k]),
                      _sel(mag[k], T, want[k]))
     del grads
-    _say("[bwd+sgd] config5 full, same slices")
+    _say(f"[bwd+sgd] config{cfg} full, same slices")
     emb.backward_sgd(*G, idx, off, dV, lr, num_bags=B, reuse_grouping=True)
     torch.cuda.synchronize()
     assert emb.check_errors() == 0
