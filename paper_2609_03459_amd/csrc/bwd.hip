@@ -143,26 +143,31 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE(const float* __restri
   }
 }
 
-// D = 128: a lane owns two columns (one 8-byte load per occurrence), the bag
-// index of each occurrence is read into a scalar register so every dV row is a
-// uniform base, and 16 rows are in flight before they are summed in order.
-// Chunks go in sorted order, an eighth of them per XCD, so each XCD reads the
-// grad_out rows and bag ids of about one table, and more of them hit its L2.
-__global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
-                                                  const int32_t* __restrict__ sorted_bag,
-                                                  const int32_t* __restrict__ occ_start,
-                                                  const int32_t* __restrict__ ctr, float* __restrict__ dE,
-                                                  float* __restrict__ part) {
+// D = 128 and D = 32: a lane owns two columns (one 8-byte load per occurrence;
+// for D = 32 sixteen lanes cover a row and the other lanes repeat their loads),
+// the bag index of each occurrence is read into a scalar register so every dV row
+// is a uniform base, and 16 (D = 128) or 32 (D = 32) rows are in flight before
+// they are summed in order.  Chunks go in sorted order, an eighth of them per XCD,
+// so each XCD reads the grad_out rows and bag ids of about one table, and more of
+// them hit its L2.
+template <int D>
+__device__ __forceinline__ void seg_rows(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+                                         const int32_t* __restrict__ sorted_bag, const int32_t* __restrict__ occ_start,
+                                         const int32_t* __restrict__ ctr, float* __restrict__ dE,
+                                         float* __restrict__ part) {
+  constexpr int LN = D / 2;               // lanes that own columns
+  constexpr int KB = D == 128 ? 16 : 32;  // rows in flight
   const int nvalid = ctr[C_NVALID];
   const int c = (int)xcd_block(blockIdx.x, gridDim.x) * SEG_WAVES + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int i0 = c * SEG_CHUNK;
   if (i0 >= nvalid) return;  // also the blocks past the chunk count that round the grid to 8
   const int lane = lane_id();
+  const int col = lane % LN;
   const SegEnds ends = seg_ends(sorted_uid, occ_start, i0, i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid, nvalid);
   const int ib = ends.ib, ie = ends.ie;
   if (ib >= ie) return;
   auto flush = [&](int u, float2 acc) {
-    reinterpret_cast<float2*>(seg_dst(ends, u, c, 128, dE, part))[lane] = acc;
+    if (lane < LN) reinterpret_cast<float2*>(seg_dst(ends, u, c, D, dE, part))[lane] = acc;
   };
   int cur = sorted_uid[ib];
   float2 acc = make_float2(0.f, 0.f);
@@ -171,16 +176,16 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __res
     const int my_u = i < ie ? sorted_uid[i] : -1;
     const int my_b = i < ie ? sorted_bag[i] : 0;
     const int cnt = ie - base < 64 ? ie - base : 64;
-    for (int k0 = 0; k0 < cnt; k0 += 16) {
-      float2 v[16];
+    for (int k0 = 0; k0 < cnt; k0 += KB) {
+      float2 v[KB];
 #pragma unroll
-      for (int kk = 0; kk < 16; ++kk) {
+      for (int kk = 0; kk < KB; ++kk) {
         const int k = k0 + kk < cnt ? k0 + kk : k0;  // clamped: every load is unconditional
         const int b = __builtin_amdgcn_readlane(my_b, k);
-        v[kk] = reinterpret_cast<const float2*>(dV + (size_t)b * 128)[lane];
+        v[kk] = reinterpret_cast<const float2*>(dV + (size_t)b * D)[col];
       }
 #pragma unroll
-      for (int kk = 0; kk < 16; ++kk) {
+      for (int kk = 0; kk < KB; ++kk) {
         if (k0 + kk < cnt) {
           const int u = __builtin_amdgcn_readlane(my_u, k0 + kk);
           if (u != cur) {
@@ -195,6 +200,20 @@ __global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __res
     }
   }
   flush(cur, acc);
+}
+__global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE128(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+                                                  const int32_t* __restrict__ sorted_bag,
+                                                  const int32_t* __restrict__ occ_start,
+                                                  const int32_t* __restrict__ ctr, float* __restrict__ dE,
+                                                  float* __restrict__ part) {
+  seg_rows<128>(dV, sorted_uid, sorted_bag, occ_start, ctr, dE, part);
+}
+__global__ void __launch_bounds__(64 * SEG_WAVES) k_seg_dE32(const float* __restrict__ dV, const int32_t* __restrict__ sorted_uid,
+                                                 const int32_t* __restrict__ sorted_bag,
+                                                 const int32_t* __restrict__ occ_start,
+                                                 const int32_t* __restrict__ ctr, float* __restrict__ dE,
+                                                 float* __restrict__ part) {
+  seg_rows<32>(dV, sorted_uid, sorted_bag, occ_start, ctr, dE, part);
 }
 
 // Rows of more than SEG_CHUNK occurrences: chunk c0 + 1, where c0 holds the
@@ -729,9 +748,9 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      st, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.ctr,
                      w.sorted_bag);
   prof_begin(prof, K_SEG_SUM, st);
-  if (s.D == 128) {
-    hipLaunchKernelGGL(k_seg_dE128, dim3(xcd_grid((nseg + SEG_WAVES - 1) / SEG_WAVES)), dim3(64 * SEG_WAVES), 0, st,
-                       dV, (const int32_t*)w.sorted_uid, (const int32_t*)w.sorted_bag,
+  if (s.D == 128 || s.D == 32) {
+    hipLaunchKernelGGL(s.D == 128 ? k_seg_dE128 : k_seg_dE32, dim3(xcd_grid((nseg + SEG_WAVES - 1) / SEG_WAVES)),
+                       dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid, (const int32_t*)w.sorted_bag,
                        (const int32_t*)w.occ_start, (const int32_t*)w.ctr, dE, w.seg_part);
   } else {
     hipLaunchKernelGGL(k_seg_dE, dim3((nseg + SEG_WAVES - 1) / SEG_WAVES), dim3(64 * SEG_WAVES), 0, st, dV, (const int32_t*)w.sorted_uid,

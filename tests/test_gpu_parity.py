@@ -630,7 +630,7 @@ def _row_runs_case(seed, d, R):
     return case
 
 
-@pytest.mark.parametrize("d,R", [((4, 4, 8), 32), ((2, 2, 2), 4)])
+@pytest.mark.parametrize("d,R", [((4, 4, 8), 32), ((4, 4, 2), 32), ((2, 2, 2), 4)])
 def test_backward_rows_across_dE_chunk_ends(lib, orc, d, R):
     check_backward(lib, orc, _row_runs_case(3300 + R, d, R), name=f"row runs d={d} R={R}")
 
