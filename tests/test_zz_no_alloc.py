@@ -44,7 +44,7 @@ def _noalloc(lib, emb, case):
     return out.cpu().numpy().reshape(T * B, D), ref.cpu().numpy().reshape(T * B, D)
 
 
-@pytest.mark.parametrize("cfg,bags", [(3, (400, 96)), (2, (20000, 3000))])
+@pytest.mark.parametrize("cfg,bags", [(3, (400, 96)), (6, (400, 96)), (2, (20000, 3000))])
 def test_noalloc_forward_two_calls(lib, orc, cfg, bags):
     first = ttgen.make(cfg, bags=bags[0], with_grad=False)
     second = ttgen.make(cfg, seed=ttgen.BASE_SEED + 1, bags=bags[1], with_grad=False)
