@@ -89,10 +89,14 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   constexpr int GR = 16 / D3;     // rows per group
   constexpr int DW = 16 * D3;     // floats per dE row
   constexpr int AROW = 16 * D3;   // floats per accumulator row (half the rank of a G3 row)
+  // LDS pitch of an accumulator row: at d3 = 2 rows of 32 floats would put every row on one
+  // of two bank offsets, so the eight random rows of a group would meet on the same banks;
+  // 36 floats spread them over sixteen
+  constexpr int APITCH = D3 == 2 ? 36 : AROW;
   const int acc_n = s.n3 * AROW;
   // d3 = 2: eight more rows after the table's, which the columns of a group's missing
   // rows (exact zeros) go to, one per row position, so they never meet a live column
-  const int acc_lds = acc_n + (D3 == 2 ? 8 * AROW : 0);
+  const int acc_lds = (s.n3 + (D3 == 2 ? 8 : 0)) * APITCH;
   float* g3acc = lds;  // [n3][j3][16 slots]
   float* scr = lds + acc_lds + wave * BW_SCR;
   const int nq = 2 * s.T;
@@ -386,7 +390,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
     auto pair_compute = [&](const BwPair& X) {
       // this lane's accumulator words, read before the products so the read's
       // latency overlaps them
-      float* ap = g3acc + (uint32_t)X.i3m * AROW + o_g3;
+      float* ap = g3acc + (uint32_t)X.i3m * APITCH + o_g3;
       const ulonglong2 w = *reinterpret_cast<const ulonglong2*>(ap);
       float ebk[4];
       if (D3 == 8) {
@@ -520,7 +524,7 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
   acc_finish();
   __syncthreads();
   float* gdst = g3part + (size_t)blockIdx.x * acc_n;  // the table's rows only
-  for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[i];
+  for (int i = threadIdx.x; i < acc_n; i += blockDim.x) gdst[i] = g3acc[(i / AROW) * APITCH + i % AROW];
 }
 
 // Each reduction writes its sum into `out` (the gradient), or with lr given,
@@ -704,7 +708,7 @@ hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const 
   hipError_t e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), nq * SCHED_STRIDE, 0u, st);
   if (e != hipSuccess) return e;
   const bool d8 = s.d3 == 8;
-  const size_t lds = sizeof(float) * ((size_t)(s.n3 + (d8 ? 0 : 8)) * 16 * s.d3 + BW_WAVES * BW_SCR);
+  const size_t lds = sizeof(float) * (d8 ? (size_t)s.n3 * 128 : (size_t)(s.n3 + 8) * 36) + sizeof(float) * BW_WAVES * BW_SCR;
   const void* kfn = d8 ? (const void*)k_bwd_r32<8> : (const void*)k_bwd_r32<2>;
   e = hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
