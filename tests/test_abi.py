@@ -158,6 +158,13 @@ def test_reuse_levels_and_workspace(N):
     ((1, 300000, 2), (4, 4, 8), 32, 1000, 1000, 0, 0),
     ((9000000, 1, 2), (4, 4, 8), 32, 1000, 1000, 0, 0),
     ((1, 70000, 2), (4, 4, 8), 64, 1000, 1000, 0, 0),
+    # D = 32 = (4, 4, 2) at R = 32: both MFMA kernels, the backward within the same n3 bound
+    ((200, 200, 250), (4, 4, 2), 32, 1 << 20, 1 << 20, 1, 1),
+    ((6, 5, 252), (4, 4, 2), 32, 1000, 1000, 1, 1),
+    ((6, 5, 253), (4, 4, 2), 32, 1000, 1000, 1, 0),
+    ((10, 10, 10), (4, 4, 2), 32, 1 << 24, 1 << 24, 0, 0),
+    ((10, 10, 10), (4, 4, 2), 64, 1000, 1000, 0, 0),            # D = 32 at R = 64: generic
+    ((10, 10, 10), (4, 4, 1), 32, 1000, 1000, 0, 0),            # d3 = 1: generic
 ])
 def test_kernel_uses_mfma(N, n, d, R, M, num, fwd, bwd):
     h = N.tt_emb_create(_desc(N, T=2, n=n, d=d, R=R, M=M, B=10))
@@ -221,6 +228,11 @@ def test_kernel_uses_mfma_on_the_three_core_view(N):
     assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], 1000)
     assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["bwd_fused"], 1000)
     assert not N.tt_emb_kernel_uses_mfma(h, N.KERNELS["merge"], 1000)
+    N.tt_emb_destroy(h)
+    # four cores d = (2, 2, 4, 2) view as d = (4, 4, 2), D = 32: the MFMA kernels too
+    h = N.tt_emb_create_n(_desc_n(N, L=4, n=(10, 20, 10, 30), d=(2, 2, 4, 2), R=32, M=1000))
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["fwd_fused"], 1000)
+    assert N.tt_emb_kernel_uses_mfma(h, N.KERNELS["bwd_fused"], 1000)
     N.tt_emb_destroy(h)
     # two cores d = (16, 8) view as d = (16, 1, 8) around an identity core: generic kernels
     h = N.tt_emb_create_n(_desc_n(N, L=2, n=(100, 100), d=(16, 8), R=32, M=1000))

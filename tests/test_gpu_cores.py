@@ -83,6 +83,7 @@ CASES = [
     dict(T=2, n=(2, 2, 2, 3, 4), d=(4, 4, 2, 1, 1), R=16, B=40, max_len=6),  # wide merged core: d1' = 32
     dict(T=2, n=(5, 4, 3, 2, 2), d=(1, 2, 1, 2, 2), R=2, B=40, max_len=6),  # 20 parents: several per-level chunks
     dict(T=1, n=(2, 2, 2, 2, 2), d=(4, 4, 2, 1, 1), R=64, B=20, max_len=4),  # R = 64: split chunks of 2 parents
+    dict(T=2, n=(5, 4, 20, 30), d=(2, 2, 4, 2), R=32, B=200, max_len=16, zipf=1.1),  # MFMA view (4, 4, 2): D = 32
 ]
 
 

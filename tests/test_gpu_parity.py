@@ -179,7 +179,7 @@ def test_many_short_bags(lib, orc):
 
 
 @pytest.mark.parametrize("reuse", ["unique", "none"])
-@pytest.mark.parametrize("k", [4, 5, 7])
+@pytest.mark.parametrize("k", [4, 5, 7, 9])
 def test_reuse_levels_same_results(lib, orc, reuse, k):
     # Section 4.5 ablation levels compute the same function: forward and backward
     # against the oracle with exact dedup only, and with no dedup at all
@@ -912,7 +912,7 @@ def _run_mode(lib, case, **kw):
     return out.cpu().numpy().reshape(-1, D), [g.cpu().numpy() for g in grads], emb
 
 
-@pytest.mark.parametrize("which", ["hot_r64", "hot_generic", "mfma"])
+@pytest.mark.parametrize("which", ["hot_r64", "hot_generic", "mfma", "mfma_d32"])
 def test_schedules_same_results(lib, orc, which):
     # Section 4.4 ablation modes compute the same function: static shares, stealing,
     # stealing with the checkpointed intermediate (hot prefix groups spanning
@@ -924,6 +924,11 @@ def test_schedules_same_results(lib, orc, which):
         # d = (4, 4, 4), R = 16: generic kernels both ways, groups of about 60 slices
         case = _hot_prefix_case(7006, 1, (3, 2, 2000), B=300, hot=[(1, 1), (2, 0)], per_bag=24,
                                 d=(4, 4, 4), R=16)
+    elif which == "mfma_d32":
+        # D = 32 = (4, 4, 2), R = 32: twelve prefixes of one (table, i2) run with nearly all
+        # suffixes, groups of 7-8 slices across chunk ends (whole groups under "group")
+        case = _hot_prefix_case(7008, 2, (12, 2, 250), B=400, hot=[(i1, 0) for i1 in range(12)], per_bag=20,
+                                d=(4, 4, 2), R=32)
     else:
         c = dict(TINY[4])
         case = ttgen.tiny(7004, c.pop("T"), c.pop("n"), c.pop("d"), c.pop("R"), **c)
