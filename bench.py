@@ -117,8 +117,12 @@ def chain_flops(n, d, R):
     return f
 
 
-def algorithmic_work(kernel, case, counts):
-    """(amount, unit, bound) per launch of `kernel` from the workload and its grouping."""
+def algorithmic_work(kernel, case, counts, on_mfma=False):
+    """(amount, unit, bound) per launch of `kernel` from the workload and its grouping.
+
+    The fused backward's per-group work is C recomputed, dA and dB (6 d1 d2 R^2), except
+    on the R = 64 matrix-core path, where dB is formed by the dG2 reduction from the
+    per-slice dC partials and the fused kernel does C and dA (4 d1 d2 R^2)."""
     T, B, R = case["T"], case["B"], case["R"]
     _, (d1, d2, d3) = view_dims(case["n"], case["d"])
     D = d1 * d2 * d3
@@ -128,7 +132,8 @@ def algorithmic_work(kernel, case, counts):
     if kernel == "fwd_fused":
         return P * 2.0 * d1 * d2 * R * R + U * 2.0 * D * R, "flop", "mfma"
     if kernel == "bwd_fused":
-        return P * 6.0 * d1 * d2 * R * R + U * 4.0 * D * R, "flop", "mfma"
+        g = 4.0 if (R == 64 and on_mfma) else 6.0
+        return P * g * d1 * d2 * R * R + U * 4.0 * D * R, "flop", "mfma"
     if kernel == "pool":
         return 4.0 * M + 8.0 * (NB + 1) + 4.0 * NB * D + 4.0 * U * D, "byte", "hbm"
     if kernel == "seg_sum":  # dV rows read once, dE rows written, row id and bag per sorted occurrence
@@ -592,10 +597,10 @@ def main():
             phases[name].append(ev.elapsed_ms(pe[j], pe[j + 1]))
     phases_ms = {k: round(float(np.median(v)), 4) for k, v in phases.items()}
 
-    work, unit, bound = algorithmic_work(dominant, case, counts)
     # the fused kernels run on the matrix cores only for the shapes the MFMA kernels serve
     on_mfma = dominant in ("fwd_fused", "bwd_fused") and P.N.tt_emb_kernel_uses_mfma(
         emb.handle, P.N.KERNELS[dominant], M)
+    work, unit, bound = algorithmic_work(dominant, case, counts, on_mfma=bool(on_mfma))
     if bound == "mfma" and not on_mfma:
         bound = "alu"
     if unit == "flop" and bound == "alu":

@@ -14,6 +14,8 @@ namespace ttemb {
 ShapeArgs shape_args(const Shape& s);
 hipError_t launch_bwd_r64(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           const Prof& prof, hipStream_t st);
+hipError_t launch_dg2_r64(const Shape& s, const Work& w, const float* G1, float* dG2, float lr, bool update,
+                          hipStream_t st);
 hipError_t launch_bwd_r32(const Shape& s, const Work& w, const float* G1, const float* G2, const float* G3,
                           float* dG1, float* dG2, float* dG3, float lr, bool update, const Prof& prof,
                           hipStream_t st);
@@ -698,8 +700,12 @@ static int bits_of(uint64_t x) {
 }
 
 // The three segment sums of the generic backward (M sorted occurrences bound the rows).
-static hipError_t launch_generic_reduce(const Shape& s, const Work& w, int64_t M, float* dG1, float* dG2, float* dG3,
-                                        float lr, bool update, hipStream_t st) {
+// The segment sums of the generic and R = 64 paths.  After the R = 64 MFMA backward
+// (dg2_from_dc), dG2 comes from the per-slice dC partials by a product with G1, which
+// runs before the dG1 sums: with `update` those overwrite G1.
+static hipError_t launch_generic_reduce(const Shape& s, const Work& w, int64_t M, const float* G1, float* dG1,
+                                        float* dG2, float* dG3, float lr, bool update, bool dg2_from_dc,
+                                        hipStream_t st) {
   const int d1R = s.d1 * s.R, nB = s.R * s.d2 * s.R, RD = s.R * s.d3;
   const int n = (int)M;
   const uint32_t nbins = (uint32_t)s.T * (uint32_t)s.n3;
@@ -716,11 +722,13 @@ static hipError_t launch_generic_reduce(const Shape& s, const Work& w, int64_t M
   hipLaunchKernelGGL(k_gred_g3, dim3(nbins, (RD + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
                      (const int32_t*)w.g3lo, (const int32_t*)w.g3hi, (const uint32_t*)w.g3vals[res],
                      (const float*)w.dDpart, RD, dG3, lr, update);
+  if (dg2_from_dc && (e = launch_dg2_r64(s, w, G1, dG2, lr, update, st)) != hipSuccess) return e;
   hipLaunchKernelGGL(k_gred_g1, dim3(s.T * s.n1, (d1R + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
                      shape_args(s), (const uint32_t*)w.dense_cnt, (const uint32_t*)w.dense_base,
                      (const float*)w.dApart, dG1, lr, update);
-  hipLaunchKernelGGL(k_gred_g2, dim3(s.T * s.n2, (nB + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0, st,
-                     (const uint32_t*)w.run_nch, (const float*)w.dBpart, nB, dG2, lr, update);
+  if (!dg2_from_dc)
+    hipLaunchKernelGGL(k_gred_g2, dim3(s.T * s.n2, (nB + GRED_THREADS - 1) / GRED_THREADS), dim3(GRED_THREADS), 0,
+                       st, (const uint32_t*)w.run_nch, (const float*)w.dBpart, nB, dG2, lr, update);
   return hipGetLastError();
 }
 
@@ -762,9 +770,10 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                      (const int32_t*)w.ctr, s.D, (const float*)w.seg_part, dE);
   if (fast) return launch_bwd_r32(s, w, G1, G2, G3, dG1, dG2, dG3, lr, update, prof, st);
   if (!w.dDpart || !w.g3lo) return hipErrorInvalidValue;
-  if (bwd_r64_supported(s, w.M)) {  // MFMA partials, then the same segment sums
+  if (bwd_r64_supported(s, w.M)) {  // MFMA partials, then the same segment sums (dG2 by a product)
+    if (!w.dCpart) return hipErrorInvalidValue;
     if ((e = launch_bwd_r64(s, w, G1, G2, G3, prof, st)) != hipSuccess) return e;
-    return launch_generic_reduce(s, w, M, dG1, dG2, dG3, lr, update, st);
+    return launch_generic_reduce(s, w, M, G1, dG1, dG2, dG3, lr, update, true, st);
   }
   const int grid = persistent_grid() * 2;
   if ((e = fill_u32(reinterpret_cast<uint32_t*>(w.ctr + C_BWD_CTR), SCHED_NQ * SCHED_STRIDE, 0u, st)) != hipSuccess)
@@ -792,7 +801,7 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
                        w.ckpt_tag, pl.stage_b, pl.db_lds, pl.rows);
   prof_end(prof, K_BWD_FUSED, st);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  return launch_generic_reduce(s, w, M, dG1, dG2, dG3, lr, update, st);
+  return launch_generic_reduce(s, w, M, G1, dG1, dG2, dG3, lr, update, false, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -10,11 +10,14 @@
 //            dD^T (16 x 64) = dE^T . C_j   -> the two rows' dD partials, each row's
 //                                            512 floats [b][j3] stored contiguously
 //            dC_j += dE . D^T              (16 x 64, summed over the slice's rows);
-//   slice end: dC_j replaces C_j in the tile (same rows);
-//   quad end:  dA (16 x 64) = dCstack (16 x 256) . B^T  -> per-slice dA partials
-//              dB (64 x 256) = Astack^T . dCstack      -> the chunk's dB partial.
-// The fixed-order segment sums of the generic path turn the partials into dG1,
-// dG2 and dG3 (or apply the fused update).
+//   slice end: dC_j replaces C_j in the tile (same rows) and goes to the slice's
+//              dC partial (d1 x d2 R);
+//   quad end:  dA (16 x 64) = dCstack (16 x 256) . B^T  -> per-slice dA partials.
+// dB of a (t, i2) run, the sum over its slices of A_s^T dC_s, is formed afterwards
+// from the dC partials by k_dg2_r64, one matrix-core product per run with the
+// contraction over (slice, j1): a 4 KB partial per slice instead of a 64 KB dB
+// partial per chunk.  The fixed-order segment sums of the generic path turn the
+// dA and dD partials into dG1 and dG3 (or apply the fused update).
 #include "common.h"
 
 namespace ttemb {
@@ -32,7 +35,7 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
               const float* __restrict__ dE, const int4* __restrict__ slices, const int32_t* __restrict__ slice_i1,
               const int4* __restrict__ chunks, const uint32_t* __restrict__ run_base,
               const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ dApart,
-              float* __restrict__ dBpart, float* __restrict__ dDpart) {
+              float* __restrict__ dCpart, float* __restrict__ dDpart) {
   __shared__ float scr_all[B64_WAVES * B64_SCR];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -75,7 +78,6 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
     const int c_rb = sd.y, c_nr = lane < ns ? sd.z - sd.y : 0, c_i1 = slice_i1[sl];
     const buf_t bbuf = make_buf(G2 + (size_t)run * 16384, 65536u);
     const buf_t g3buf = make_buf(G3 + (size_t)t * s.n3 * 512, (uint32_t)s.n3 * 2048u);
-    float* dBc = dBpart + (size_t)c * 16384;
     for (int qd = 0; qd < ns; qd += 4) {
       const int nqs = ns - qd < 4 ? ns - qd : 4;
       // ---- stage 1: C of the quad's slices (missing slices repeat the first) ----
@@ -159,12 +161,17 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
             dC[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(e4.w, d4[nt].w, dC[nt], 0, 0, 0);
           }
         }
-        // lane holds dC[jj = 4 l4 + r][b = 16 nt + l15]: rows of slice j, in place of C_j
+        // lane holds dC[jj = 4 l4 + r][b = 16 nt + l15]: rows of slice j, in place of C_j,
+        // and the slice's partial [j1][(j2, b)] = [jj][b]
         wave_lds_sync();
+        float* dcs = dCpart + (size_t)(f + qd + j) * 1024 + 4 * l4 * 64 + l15;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) scr[j * B64_SLICE + (4 * l4 + r) * B64_PITCH + 16 * nt + l15] = dC[nt][r];
+          for (int r = 0; r < 4; ++r) {
+            scr[j * B64_SLICE + (4 * l4 + r) * B64_PITCH + 16 * nt + l15] = dC[nt][r];
+            dcs[r * 64 + 16 * nt] = dC[nt][r];
+          }
       }
       wave_lds_sync();
       // ---- dA (16 x 64) = dCstack (16 x 256) . B^T, contraction (j2, b = 16 l4 + q) ----
@@ -210,41 +217,6 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
             for (int r = 0; r < 4; ++r) dst[r * 64 + 16 * nt] = acc[nt][r];
         }
       }
-      // ---- dB (64 x 256) += Astack^T . dCstack, contraction (slice s, j1 = l4) ----
-      {
-        float at[16];  // A^T[a = 16 mt + l15][(slice s, j1 l4)], (mt, s) -> 4 mt + s; zero for missing slices
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-          const int i1 = __builtin_amdgcn_readlane(c_i1, qd + s4);
-          const float* Ar = G1 + ((size_t)t * s.n1 + i1) * 256 + l4 * 64 + l15;
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) at[4 * mt + s4] = s4 < nqs ? Ar[16 * mt] : 0.f;
-        }
-#pragma unroll 4
-        for (int nt = 0; nt < 16; ++nt) {
-          float bv[4];
-#pragma unroll
-          for (int s4 = 0; s4 < 4; ++s4)
-            bv[s4] = scr[s4 * B64_SLICE + (l4 * 4 + (nt >> 2)) * B64_PITCH + 16 * (nt & 3) + l15];
-          f32x4 acc[4];
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt) {
-            acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s4 = 0; s4 < 4; ++s4)
-              acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(at[4 * mt + s4], bv[s4], acc[mt], 0, 0, 0);
-          }
-          // lane holds dB[a = 16 mt + 4 l4 + r][(j2, b) = 16 nt + l15]; a chunk of several quads
-          // adds its later quads to the partial (only this wave writes it)
-#pragma unroll
-          for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              float* p = dBc + (16 * mt + 4 * l4 + r) * 256 + 16 * nt + l15;
-              *p = qd == 0 ? acc[mt][r] : *p + acc[mt][r];
-            }
-        }
-      }
       wave_lds_sync();
     }
   }
@@ -267,8 +239,110 @@ hipError_t launch_bwd_r64(const Shape& s, const Work& w, const float* G1, const 
   prof_begin(prof, K_BWD_FUSED, st);
   hipLaunchKernelGGL(k_bwd_r64, dim3(blocks), dim3(64 * B64_WAVES), 0, st, shape_args(s), G1, G2, G3,
                      (const float*)w.E, (const int4*)w.slices, (const int32_t*)w.slice_i1, (const int4*)w.chunks,
-                     (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dBpart, w.dDpart);
+                     (const uint32_t*)w.run_nch, (const int32_t*)w.uniq_i3, w.ctr, w.dApart, w.dCpart, w.dDpart);
   prof_end(prof, K_BWD_FUSED, st);
+  return hipGetLastError();
+}
+
+// dG2[t][i2] (R x d2 R) = sum over the slices s of run (t, i2), in slice order, of
+// A_s^T . dC_s, with A_s = G1[t][i1 of s] (d1 x R) and dC_s the slice's dC partial
+// (d1 x d2 R): a matrix-core product whose contraction index is (slice, j1), one MFMA
+// step per slice.  One workgroup per run: wave w takes the columns of j2 = w % 4 (64 of
+// them, sixteen 16 x 16 tiles with the 64 rows a) over the quarter w / 4 of the run's
+// slices, and the quarters are added in order ((q0 + q1) + q2) + q3 through LDS, so
+// the result is the same bits run to run.  The slices of a run are contiguous (the
+// (t, i2, i1) slot order): from the slot base of (t, i2, 0) to that of the next run.
+// With `update`, dG2 is G2 itself and receives G2 - lr sum; G1 must not have been
+// updated yet (the dG1 reduction runs after this kernel).
+constexpr int DG2_WAVES = 16;
+__global__ void __launch_bounds__(64 * DG2_WAVES) k_dg2_r64(ShapeArgs s, const float* __restrict__ G1,
+                                                            const uint32_t* __restrict__ dense_base,
+                                                            const int32_t* __restrict__ slice_i1,
+                                                            const int32_t* __restrict__ ctr,
+                                                            const float* __restrict__ dCpart, float* __restrict__ dG2,
+                                                            float lr, bool update) {
+  extern __shared__ float red[];  // one quarter's sums: [j2][tile, r][lane]
+  const int run = blockIdx.x;
+  const int t = run / s.n2;
+  const int lane = lane_id(), w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l15 = lane & 15, l4 = lane >> 4;
+  const int cg = w & 3, ks = w >> 2;
+  const int64_t slot0 = (int64_t)run * s.n1;
+  const int lo = (int)dense_base[slot0];
+  const int hi = run + 1 < s.T * s.n2 ? (int)dense_base[slot0 + s.n1] : ctr[C_NSLICES];
+  const int n = hi - lo;
+  const int k0 = lo + (int)(((int64_t)n * ks) / 4), k1 = lo + (int)(((int64_t)n * (ks + 1)) / 4);
+  f32x4 acc[16];  // tile (mt, nt) -> 4 mt + nt: rows a = 16 mt + .., columns b = 16 nt + .. of j2 = cg
+#pragma unroll
+  for (int k = 0; k < 16; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float* G1t = G1 + (size_t)t * s.n1 * 256;
+  // operands of slice sl: A^T[a = 16 mt + l15][j1 = l4] and dC[j1 = l4][(cg, b = 16 nt + l15)]
+  auto load = [&](int sl, float* a, float* b) {
+    const float* Ar = G1t + (size_t)slice_i1[sl] * 256 + l4 * 64 + l15;
+    const float* Cr = dCpart + (size_t)sl * 1024 + l4 * 256 + cg * 64 + l15;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) a[m] = Ar[16 * m];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) b[q] = Cr[16 * q];
+  };
+  if (k0 < k1) {
+    float a0[4], b0[4];
+    load(k0, a0, b0);
+    for (int sl = k0; sl < k1; ++sl) {
+      float a1[4], b1[4];
+      load(sl + 1 < k1 ? sl + 1 : sl, a1, b1);  // the next slice's operands while this one runs
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          acc[4 * m + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[m], b0[q], acc[4 * m + q], 0, 0, 0);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        a0[k] = a1[k];
+        b0[k] = b1[k];
+      }
+    }
+  }
+  float* rq = red + cg * 4096 + lane;
+  for (int q = 1; q < 4; ++q) {
+    if (ks == q) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rq[(4 * k + r) * 64] = acc[k][r];
+    }
+    __syncthreads();
+    if (ks == 0) {
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[k][r] += rq[(4 * k + r) * 64];
+    }
+    __syncthreads();
+  }
+  if (ks == 0) {
+    // lane holds dG2[a = 16 mt + 4 l4 + r][j2 = cg][b = 16 nt + l15]
+    float* out = dG2 + (size_t)run * 16384 + cg * 64 + l15;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float* p = out + (16 * m + 4 * l4 + r) * 256 + 16 * q;
+          *p = update ? *p - lr * acc[4 * m + q][r] : acc[4 * m + q][r];
+        }
+  }
+}
+
+hipError_t launch_dg2_r64(const Shape& s, const Work& w, const float* G1, float* dG2, float lr, bool update,
+                          hipStream_t st) {
+  const int lds = (int)sizeof(float) * 4 * 4096;
+  hipError_t e = hipFuncSetAttribute((const void*)k_dg2_r64, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_dg2_r64, dim3(s.T * s.n2), dim3(64 * DG2_WAVES), lds, st, shape_args(s), G1,
+                     (const uint32_t*)w.dense_base, (const int32_t*)w.slice_i1, (const int32_t*)w.ctr,
+                     (const float*)w.dCpart, dG2, lr, update);
   return hipGetLastError();
 }
 

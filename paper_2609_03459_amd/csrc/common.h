@@ -106,7 +106,9 @@ struct Work {
   int4* chunks;           // [nch_max] (first slice, slice count, run, 0)
   float* dApart;          // backward: dA of each slice, [2][nsl_max][d1*R] (MFMA: one per rank half) or
                           // [nsl_max][d1*R] (generic)
-  float* dBpart;          // backward: dB of each chunk, [2][nch_max][R*d2*R/2] (MFMA) or [nch_max][R*d2*R]
+  float* dBpart;          // backward: dB of each chunk, [2][nch_max][R*d2*R/2] (R = 32 MFMA) or [nch_max][R*d2*R]
+                          // (generic); null on the R = 64 MFMA path, which keeps dCpart instead
+  float* dCpart;          // R = 64 MFMA backward: dC sum of each slice, [nsl_max][d1][d2*R]
   float* g3part;          // [MAX_BWD_WG][n3*R*d3/2] backward: dG3 half of each workgroup
   // generic backward (shapes the MFMA backward does not serve), else null: partials of
   // the fixed-order segment sums and the (table, i3) order of the unique rows

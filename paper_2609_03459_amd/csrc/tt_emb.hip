@@ -113,7 +113,10 @@ static size_t layout(const Shape& s, int64_t M, int64_t B, char* base, Work* w, 
   // gradient partials: the MFMA backward's rank halves, or the generic backward's
   // per-slice dA, per-chunk dB and per-row dD with the (t, i3) order of the rows
   W->dApart = (float*)take(4 * (size_t)(bwd_r32 ? 2 : 1) * nsl_max * s.d1 * s.R);
-  W->dBpart = (float*)take(4 * (size_t)nch_max * s.R * s.d2 * s.R);
+  // the R = 64 MFMA backward keeps each slice's dC sum instead of a dB per chunk
+  const bool bwd_r64 = !bwd_r32 && bwd_r64_supported(s, m);
+  W->dBpart = bwd_r64 ? nullptr : (float*)take(4 * (size_t)nch_max * s.R * s.d2 * s.R);
+  W->dCpart = bwd_r64 ? (float*)take(4 * (size_t)nsl_max * s.d1 * s.d2 * s.R) : nullptr;
   W->g3part = bwd_r32 ? (float*)take(4 * (size_t)MAX_BWD_WG * (s.n3 * s.R * s.d3 / 2)) : nullptr;
   W->dDpart = bwd_r32 ? nullptr : (float*)take(4 * (size_t)m * s.R * s.d3);
   for (int k = 0; k < 2; ++k) {

@@ -65,6 +65,11 @@ def test_algorithmic_work_of_the_fused_kernels():
     big = dict(case, T=8)
     w, _, _ = bench.algorithmic_work("bwd_fused", big, {"U": 1089937, "P": 309642, "nvalid": 5246700})
     assert abs(w / 1e9 - 48.3) < 0.1
+    # at R = 64 on the matrix cores dB leaves the fused kernel (formed by the dG2 reduction)
+    r64 = dict(case, R=64)
+    assert bench.algorithmic_work("bwd_fused", r64, counts)[0] == 6 * 16 * 64 * 64 + 4 * 128 * 64
+    assert bench.algorithmic_work("bwd_fused", r64, counts, on_mfma=True)[0] == 4 * 16 * 64 * 64 + 4 * 128 * 64
+    assert bench.algorithmic_work("bwd_fused", case, counts, on_mfma=True)[0] == bwd
 
 
 def test_run_key_and_step_of_the_forward_only_workloads():
