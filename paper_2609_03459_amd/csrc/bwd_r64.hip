@@ -247,97 +247,84 @@ hipError_t launch_bwd_r64(const Shape& s, const Work& w, const float* G1, const 
 // dG2[t][i2] (R x d2 R) = sum over the slices s of run (t, i2), in slice order, of
 // A_s^T . dC_s, with A_s = G1[t][i1 of s] (d1 x R) and dC_s the slice's dC partial
 // (d1 x d2 R): a matrix-core product whose contraction index is (slice, j1), one MFMA
-// step per slice.  One workgroup per run: wave w takes the columns of j2 = w % 4 (64 of
-// them, sixteen 16 x 16 tiles with the 64 rows a) over the quarter w / 4 of the run's
-// slices, and the quarters are added in order ((q0 + q1) + q2) + q3 through LDS, so
-// the result is the same bits run to run.  The slices of a run are contiguous (the
-// (t, i2, i1) slot order): from the slot base of (t, i2, 0) to that of the next run.
-// With `update`, dG2 is G2 itself and receives G2 - lr sum; G1 must not have been
-// updated yet (the dG1 reduction runs after this kernel).
+// step per slice.  One workgroup per run: wave w takes 32 of the 256 columns (j2, b),
+// cg = w % 8, as eight 16 x 16 tiles with the 64 rows a, over the half w / 8 of the run's
+// slices, and the halves are added in order through LDS, so the result is the same bits
+// run to run.  Few accumulators keep a wave near 64 VGPRs, so two workgroups share a
+// CU at eight waves per SIMD, and the waves' operand loads overlap each other's products.
+// The slices of a run are contiguous (the (t, i2, i1) slot order): from the slot base of
+// (t, i2, 0) to that of the next run.  With `update`, dG2 is G2 itself and receives
+// G2 - lr sum; G1 must not have been updated yet (the dG1 reduction runs after this).
 constexpr int DG2_WAVES = 16;
-__global__ void __launch_bounds__(64 * DG2_WAVES) k_dg2_r64(ShapeArgs s, const float* __restrict__ G1,
-                                                            const uint32_t* __restrict__ dense_base,
-                                                            const int32_t* __restrict__ slice_i1,
-                                                            const int32_t* __restrict__ ctr,
-                                                            const float* __restrict__ dCpart, float* __restrict__ dG2,
-                                                            float lr, bool update) {
-  extern __shared__ float red[];  // one quarter's sums: [j2][tile, r][lane]
+__global__ void __launch_bounds__(64 * DG2_WAVES, 8) k_dg2_r64(ShapeArgs s, const float* __restrict__ G1,
+                                                               const uint32_t* __restrict__ dense_base,
+                                                               const int32_t* __restrict__ slice_i1,
+                                                               const int32_t* __restrict__ ctr,
+                                                               const float* __restrict__ dCpart,
+                                                               float* __restrict__ dG2, float lr, bool update) {
+  extern __shared__ float red[];  // the second half's sums: [cg][tile, r][lane]
   const int run = blockIdx.x;
   const int t = run / s.n2;
   const int lane = lane_id(), w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l15 = lane & 15, l4 = lane >> 4;
-  const int cg = w & 3, ks = w >> 2;
+  const int cg = w & 7, ks = w >> 3;
   const int64_t slot0 = (int64_t)run * s.n1;
   const int lo = (int)dense_base[slot0];
   const int hi = run + 1 < s.T * s.n2 ? (int)dense_base[slot0 + s.n1] : ctr[C_NSLICES];
   const int n = hi - lo;
-  const int k0 = lo + (int)(((int64_t)n * ks) / 4), k1 = lo + (int)(((int64_t)n * (ks + 1)) / 4);
-  f32x4 acc[16];  // tile (mt, nt) -> 4 mt + nt: rows a = 16 mt + .., columns b = 16 nt + .. of j2 = cg
+  const int k0 = lo + (int)(((int64_t)n * ks) / 2), k1 = lo + (int)(((int64_t)n * (ks + 1)) / 2);
+  f32x4 acc[8];  // tile (mt, nt) -> 2 mt + nt: rows a = 16 mt + .., columns 32 cg + 16 nt + ..
 #pragma unroll
-  for (int k = 0; k < 16; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < 8; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
   const float* G1t = G1 + (size_t)t * s.n1 * 256;
-  // operands of slice sl: A^T[a = 16 mt + l15][j1 = l4] and dC[j1 = l4][(cg, b = 16 nt + l15)]
-  auto load = [&](int sl, float* a, float* b) {
-    const float* Ar = G1t + (size_t)slice_i1[sl] * 256 + l4 * 64 + l15;
-    const float* Cr = dCpart + (size_t)sl * 1024 + l4 * 256 + cg * 64 + l15;
+  // the half's slices 64 at a time, their i1 in the lanes (one load); per slice the
+  // operands A^T[a = 16 mt + l15][j1 = l4] and dC[j1 = l4][32 cg + 16 nt + l15]
+  for (int base = k0; base < k1; base += 64) {
+    const int cnt = k1 - base < 64 ? k1 - base : 64;
+    const int my_i1 = slice_i1[base + (lane < cnt ? lane : 0)];
+    for (int k = 0; k < cnt; ++k) {
+      const int sl = base + k;
+      const float* Ar = G1t + (size_t)__builtin_amdgcn_readlane(my_i1, k) * 256 + l4 * 64 + l15;
+      const float* Cr = dCpart + (size_t)sl * 1024 + l4 * 256 + cg * 32 + l15;
+      float a[4], b[2];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) a[m] = Ar[16 * m];
+      for (int m = 0; m < 4; ++m) a[m] = Ar[16 * m];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) b[q] = Cr[16 * q];
-  };
-  if (k0 < k1) {
-    float a0[4], b0[4];
-    load(k0, a0, b0);
-    for (int sl = k0; sl < k1; ++sl) {
-      float a1[4], b1[4];
-      load(sl + 1 < k1 ? sl + 1 : sl, a1, b1);  // the next slice's operands while this one runs
+      for (int q = 0; q < 2; ++q) b[q] = Cr[16 * q];
 #pragma unroll
       for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          acc[4 * m + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[m], b0[q], acc[4 * m + q], 0, 0, 0);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        a0[k] = a1[k];
-        b0[k] = b1[k];
-      }
+        for (int q = 0; q < 2; ++q)
+          acc[2 * m + q] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[m], b[q], acc[2 * m + q], 0, 0, 0);
     }
   }
-  float* rq = red + cg * 4096 + lane;
-  for (int q = 1; q < 4; ++q) {
-    if (ks == q) {
+  float* rq = red + cg * 2048 + lane;
+  if (ks == 1) {
 #pragma unroll
-      for (int k = 0; k < 16; ++k)
+    for (int k = 0; k < 8; ++k)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) rq[(4 * k + r) * 64] = acc[k][r];
-    }
-    __syncthreads();
-    if (ks == 0) {
-#pragma unroll
-      for (int k = 0; k < 16; ++k)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[k][r] += rq[(4 * k + r) * 64];
-    }
-    __syncthreads();
+      for (int r = 0; r < 4; ++r) rq[(4 * k + r) * 64] = acc[k][r];
   }
+  __syncthreads();
   if (ks == 0) {
-    // lane holds dG2[a = 16 mt + 4 l4 + r][j2 = cg][b = 16 nt + l15]
-    float* out = dG2 + (size_t)run * 16384 + cg * 64 + l15;
+    // lane holds dG2[a = 16 mt + 4 l4 + r][(j2, b) = 32 cg + 16 nt + l15]
+    float* out = dG2 + (size_t)run * 16384 + cg * 32 + l15;
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
+          const float v = acc[2 * m + q][r] + rq[(4 * (2 * m + q) + r) * 64];
           float* p = out + (16 * m + 4 * l4 + r) * 256 + 16 * q;
-          *p = update ? *p - lr * acc[4 * m + q][r] : acc[4 * m + q][r];
+          *p = update ? *p - lr * v : v;
         }
   }
 }
 
 hipError_t launch_dg2_r64(const Shape& s, const Work& w, const float* G1, float* dG2, float lr, bool update,
                           hipStream_t st) {
-  const int lds = (int)sizeof(float) * 4 * 4096;
+  const int lds = (int)sizeof(float) * 8 * 2048;
   hipError_t e = hipFuncSetAttribute((const void*)k_dg2_r64, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_dg2_r64, dim3(s.T * s.n2), dim3(64 * DG2_WAVES), lds, st, shape_args(s), G1,
