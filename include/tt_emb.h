@@ -204,7 +204,10 @@ tt_emb_status tt_emb_forward_noalloc(tt_emb_handle h, const float* G1, const flo
  * The per-core gradients are reduced by segments, with no global float
  * atomics: dG1 is a fixed-order sum of per-slice partials over the slices of
  * each (table, i1), dG2 of per-chunk partials over the chunks of each
- * (table, i2).  dG3: on the R = 32 MFMA shape (see tt_emb_kernel_uses_mfma)
+ * (table, i2), except on the R = 64 MFMA shape, where each slice's sum dC is
+ * kept and dG2 of (table, i2) is the product of the stacked A^T and sum dC of
+ * its slices, contracted in slice order.  dG3: on the R = 32 MFMA shape (see
+ * tt_emb_kernel_uses_mfma)
  * it is summed in on-chip memory per (table, rank half) and workgroup, then
  * over the workgroups in a fixed order (the on-chip adds land in arrival
  * order, so this dG3 is reproducible to rounding, not bit for bit); on every
@@ -331,7 +334,7 @@ typedef enum {
   TT_EMB_K_FWD_FUSED = 2, /* forward: C = A.B per prefix group, E = C.D per unique row */
   TT_EMB_K_POOL = 3,      /* forward: sum pooling of E rows into the bags */
   TT_EMB_K_SEG_SUM = 4,   /* backward: dE per unique row, summed over its occurrences */
-  TT_EMB_K_BWD_FUSED = 5, /* backward: per prefix group dD, dC, sum dC, dA, dB */
+  TT_EMB_K_BWD_FUSED = 5, /* backward: per prefix group dD, dC, sum dC, dA, dB (dB after it at R = 64) */
   TT_EMB_K_MERGE = 6,     /* L >= 4: merged first core from cores 0..L-3 */
   TT_EMB_K_SPLIT = 7      /* L >= 4 backward: gradients of cores 0..L-3 from the merged core's */
 } tt_emb_kernel;
