@@ -167,6 +167,14 @@ hipError_t launch_debug_digits(const Shape& s, const Work& w, int32_t* out, int 
 
 static bool al(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+// Rows per work slice at the prefix reuse level: 16 on the R = 64 matrix-core shape,
+// whose work units are one quad of slices, so that a hot prefix's quads hold at most 32
+// row pairs instead of 64 (the heaviest quads otherwise end the launch alone); else
+// SLICE_ROWS.
+static int prefix_slice_rows(const Shape& s) {
+  return s.R == 64 && s.d1 == 4 && s.d2 == 4 && s.d3 == 8 ? 16 : SLICE_ROWS;
+}
+
 static int bit_length(uint64_t x) {
   int b = 0;
   while (x) {
@@ -224,7 +232,7 @@ static tt_emb_status create_view(const tt_emb_desc* d, int L, const int32_t* nk,
   s.key_bits = bit_length(s.kinv);
   s.n12 = s.n1 * s.n2;
   s.ndense = (int64_t)T * s.n1 * s.n2;
-  s.slice_rows = SLICE_ROWS;
+  s.slice_rows = prefix_slice_rows(s);
   s.dedup = 1;
   s.sched = SCHED_STEAL;
   s.chunk_slices = s.R == 64 ? TTEMB_R64_CHUNK : TTEMB_CHUNK;
@@ -322,7 +330,7 @@ tt_emb_status tt_emb_destroy(tt_emb_handle h) {
 
 tt_emb_status tt_emb_set_reuse(tt_emb_handle h, int level) {
   if (!h || level < TT_EMB_REUSE_PREFIX || level > TT_EMB_REUSE_NONE) return TT_EMB_EINVAL;
-  h->s.slice_rows = level == TT_EMB_REUSE_PREFIX ? SLICE_ROWS : 1;
+  h->s.slice_rows = level == TT_EMB_REUSE_PREFIX ? prefix_slice_rows(h->s) : 1;
   h->s.dedup = level == TT_EMB_REUSE_NONE ? 0 : 1;
   h->g_valid = false;  // a grouping made at another level must not be reused
   return TT_EMB_OK;

@@ -342,17 +342,18 @@ def test_edge_index_patterns(lib, orc, kind, dR):
     _check_sgd(orc, case, G, 0.01, name)
 
 
-def _run_slices(g, n):
-    """Work slices (at most 32 rows each) of every prefix group from a debug grouping, in
-    the fused kernels' (table, i2, i1) order, with each group's first slice within its
-    (table, i2) run: returns (rows, slices, first, run) per group."""
+def _run_slices(g, n, slice_rows=32):
+    """Work slices (at most slice_rows rows each: 32, or 16 on the R = 64 matrix-core shape)
+    of every prefix group from a debug grouping, in the fused kernels' (table, i2, i1)
+    order, with each group's first slice within its (table, i2) run: returns (rows,
+    slices, first, run) per group."""
     n1, n2 = n[0], n[1]
     keys = np.asarray(g["pg_keys"], np.int64)
     rows = np.diff(np.asarray(g["pg_start"], np.int64))
     t, q = keys // (n1 * n2), keys % (n1 * n2)
     i1, i2 = q // n2, q % n2
     order = np.lexsort((i1, i2, t))
-    sl = (rows + 31) // 32
+    sl = (rows + slice_rows - 1) // slice_rows
     run = (t * n2 + i2)[order]
     first = np.zeros(len(order), np.int64)
     acc, prev = 0, -1
@@ -465,10 +466,10 @@ def test_backward_prefix_groups_across_chunk_ends(lib, orc):
 
 @pytest.mark.parametrize("sched", ["steal", "group"])
 def test_r64_backward_groups_across_quads_and_chunks(lib, orc, sched):
-    # R = 64 cuts a (table, i2) run into chunks of four work slices (one quad); groups
-    # of 7-8 slices straddle quads and chunks.  Under the static prefix mapping a
-    # chunk is a whole group of several quads, whose dB partial the MFMA backward
-    # accumulates quad after quad.  Forward, backward and the fused update.
+    # R = 64 cuts a (table, i2) run into chunks of four work slices (one quad) of at most
+    # 16 rows; groups of 13-16 slices straddle quads and chunks.  Under the static prefix
+    # mapping a chunk is a whole group of several quads.  Forward, backward (per-slice dC
+    # sums, dG2 formed per run) and the fused update.
     n = (12, 2, 250)
     hot = [(i1, 0) for i1 in range(12)]
     case = _hot_prefix_case(7103, 2, n, B=300, hot=hot, per_bag=20, R=64)
@@ -478,7 +479,7 @@ def test_r64_backward_groups_across_quads_and_chunks(lib, orc, sched):
     assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["fwd_fused"], M)
     assert lib.N.tt_emb_kernel_uses_mfma(emb.handle, lib.N.KERNELS["bwd_fused"], M)
     g = emb.debug_grouping(M)
-    rows, sl, first, run = _run_slices(g, n)
+    rows, sl, first, run = _run_slices(g, n, slice_rows=16)
     assert sl.max() > 4 and ((first // 4) != ((first + sl - 1) // 4)).sum() >= 2
     ref_v, _ = orc.forward(case)
     mag_v, _ = orc.forward(abs_case(case))
