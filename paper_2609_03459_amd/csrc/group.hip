@@ -162,15 +162,30 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __r
   for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&h[0][0])[k] = 0;
   __syncthreads();
   const int base = blockIdx.x * SORT_TILE;
-  uint32_t k[SORT_ITEMS];
+  if (base + SORT_TILE <= n) {
+    // a full tile: the order of the counts does not matter, so 16-byte loads
+    const uint4* k4 = reinterpret_cast<const uint4*>(keys + base) + threadIdx.x;
+    uint4 v[SORT_ITEMS / 4];
 #pragma unroll
-  for (int j = 0; j < SORT_ITEMS; ++j) {
-    const int i = base + j * SORT_THREADS + threadIdx.x;
-    k[j] = i < n ? keys[i] : 0u;
+    for (int j = 0; j < SORT_ITEMS / 4; ++j) v[j] = k4[j * SORT_THREADS];
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS / 4; ++j) {
+      atomicAdd(&h[w][(v[j].x >> shift) & (NB - 1)], 1u);
+      atomicAdd(&h[w][(v[j].y >> shift) & (NB - 1)], 1u);
+      atomicAdd(&h[w][(v[j].z >> shift) & (NB - 1)], 1u);
+      atomicAdd(&h[w][(v[j].w >> shift) & (NB - 1)], 1u);
+    }
+  } else {
+    uint32_t k[SORT_ITEMS];
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j) {
+      const int i = base + j * SORT_THREADS + threadIdx.x;
+      k[j] = i < n ? keys[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j)
+      if (base + j * SORT_THREADS + (int)threadIdx.x < n) atomicAdd(&h[w][(k[j] >> shift) & (NB - 1)], 1u);
   }
-#pragma unroll
-  for (int j = 0; j < SORT_ITEMS; ++j)
-    if (base + j * SORT_THREADS + (int)threadIdx.x < n) atomicAdd(&h[w][(k[j] >> shift) & (NB - 1)], 1u);
   __syncthreads();
   for (int d = threadIdx.x; d < NB; d += SORT_THREADS)
     counts[d * ntiles + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
@@ -221,8 +236,8 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
                                                                 const uint32_t* __restrict__ totals) {
   constexpr int NB = 1 << BITS;
   __shared__ uint32_t wh[4][NB];  // per-wave digit counts, then the wave's local base per digit
-  __shared__ uint32_t lbase[NB];  // tile-local start of each digit
-  __shared__ uint32_t dbase[NB];  // global start of each digit
+  __shared__ uint32_t dpos[NB];   // output position of the tile's first key of each digit, less
+                                  // that key's position in the tile's digit order
   __shared__ uint32_t sk[SORT_TILE], sv[SORT_TILE];
   __shared__ uint32_t scan_tmp[SORT_THREADS / 64];
   const int w = threadIdx.x >> 6;
@@ -240,6 +255,16 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
     const bool ok = i < n;
     key[j] = ok ? kin[i] : 0u;
     val[j] = ok ? vin[i] : 0u;
+  }
+  // this tile's offset within each digit and the pass's digit totals, loaded with the
+  // keys so that the write-out below needs no global read
+  constexpr int DPT = (NB + SORT_THREADS - 1) / SORT_THREADS;  // digits per thread
+  uint32_t toff[DPT], gt[DPT];
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) {
+    const int d = threadIdx.x * DPT + q;
+    toff[q] = d < NB ? offs[d * ntiles + blockIdx.x] : 0u;
+    gt[q] = d < NB ? totals[d] : 0u;
   }
 #pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
@@ -260,7 +285,6 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
   }
   __syncthreads();
   // tile-local digit starts (exclusive scan over digits of the per-digit totals)
-  constexpr int DPT = (NB + SORT_THREADS - 1) / SORT_THREADS;  // digits per thread
   uint32_t tot[DPT], my = 0;
 #pragma unroll
   for (int q = 0; q < DPT; ++q) {
@@ -270,29 +294,17 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
   }
   uint32_t all;
   uint32_t run = block_excl_scan<uint32_t, SORT_THREADS>(my, scan_tmp, &all);
-  {
-    // digit bases: exclusive scan of the digit totals of the whole pass
-    uint32_t gt[DPT], gmy = 0;
+  // digit bases: exclusive scan of the digit totals of the whole pass
+  uint32_t gmy = 0;
 #pragma unroll
-    for (int q = 0; q < DPT; ++q) {
-      const int d = threadIdx.x * DPT + q;
-      gt[q] = d < NB ? totals[d] : 0u;
-      gmy += gt[q];
-    }
-    uint32_t gall;
-    uint32_t grun = block_excl_scan<uint32_t, SORT_THREADS>(gmy, scan_tmp, &gall);
-#pragma unroll
-    for (int q = 0; q < DPT; ++q) {
-      const int d = threadIdx.x * DPT + q;
-      if (d < NB) dbase[d] = grun;
-      grun += gt[q];
-    }
-  }
+  for (int q = 0; q < DPT; ++q) gmy += gt[q];
+  uint32_t gall;
+  uint32_t grun = block_excl_scan<uint32_t, SORT_THREADS>(gmy, scan_tmp, &gall);
 #pragma unroll
   for (int q = 0; q < DPT; ++q) {
     const int d = threadIdx.x * DPT + q;
     if (d < NB) {
-      lbase[d] = run;
+      dpos[d] = grun + toff[q] - run;
       const uint32_t c0 = wh[0][d], c1 = wh[1][d], c2 = wh[2][d];
       wh[0][d] = run;
       wh[1][d] = run + c0;
@@ -300,6 +312,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
       wh[3][d] = run + c0 + c1 + c2;
     }
     run += tot[q];
+    grun += gt[q];
   }
   __syncthreads();
 #pragma unroll
@@ -315,8 +328,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
   __syncthreads();
   for (int p = threadIdx.x; p < nt; p += SORT_THREADS) {
     const uint32_t k = sk[p];
-    const uint32_t dg = (k >> shift) & (NB - 1);
-    const uint32_t pos = dbase[dg] + offs[dg * ntiles + blockIdx.x] + ((uint32_t)p - lbase[dg]);
+    const uint32_t pos = dpos[(k >> shift) & (NB - 1)] + (uint32_t)p;
     kout[pos] = k;
     vout[pos] = sv[p];
   }
