@@ -77,11 +77,24 @@ __device__ __forceinline__ void seg_flush(const SegEnds& e, int cur, int c, int 
 
 // The bag of every sorted occurrence, gathered once through the sorted positions,
 // so that the dE sums read it in order instead of chasing two indices per row.
-__global__ void k_sorted_bag(const uint32_t* __restrict__ sorted_pos, const int32_t* __restrict__ bag_of,
-                             const int32_t* __restrict__ ctr, int32_t* __restrict__ sorted_bag) {
+// Blocks take contiguous runs of SB_ITEMS x 256 sorted occurrences, an eighth of
+// them per XCD: the sorted order is table by table, so an XCD reads the bag ids of
+// about one table, a range its L2 holds.
+constexpr int SB_ITEMS = 4;
+__global__ void __launch_bounds__(256) k_sorted_bag(const uint32_t* __restrict__ sorted_pos,
+                                                    const int32_t* __restrict__ bag_of,
+                                                    const int32_t* __restrict__ ctr, int32_t* __restrict__ sorted_bag) {
   const int nvalid = ctr[C_NVALID];
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nvalid; i += gridDim.x * blockDim.x)
-    sorted_bag[i] = bag_of[sorted_pos[i]];
+  const int i0 = (int)xcd_block(blockIdx.x, gridDim.x) * (SB_ITEMS * 256) + (int)threadIdx.x;
+  uint32_t p[SB_ITEMS];
+#pragma unroll
+  for (int k = 0; k < SB_ITEMS; ++k) p[k] = i0 + 256 * k < nvalid ? sorted_pos[i0 + 256 * k] : 0u;
+  int32_t b[SB_ITEMS];
+#pragma unroll
+  for (int k = 0; k < SB_ITEMS; ++k) b[k] = i0 + 256 * k < nvalid ? bag_of[p[k]] : 0;
+#pragma unroll
+  for (int k = 0; k < SB_ITEMS; ++k)
+    if (i0 + 256 * k < nvalid) sorted_bag[i0 + 256 * k] = b[k];
 }
 
 // One wave per chunk of SEG_CHUNK sorted occurrences; lanes hold 4 columns
@@ -752,8 +765,8 @@ hipError_t launch_backward(const Shape& s, const Work& w, const float* G1, const
   }
   float* dE = w.E;
   const int nseg = (int)((M + SEG_CHUNK - 1) / SEG_CHUNK);
-  hipLaunchKernelGGL(k_sorted_bag, dim3((M + 255) / 256 < 8192 ? (unsigned)((M + 255) / 256) : 8192u), dim3(256), 0,
-                     st, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.ctr,
+  hipLaunchKernelGGL(k_sorted_bag, dim3(xcd_grid((unsigned)((M + SB_ITEMS * 256 - 1) / (SB_ITEMS * 256)))), dim3(256),
+                     0, st, (const uint32_t*)w.sorted_pos, (const int32_t*)w.bag_of, (const int32_t*)w.ctr,
                      w.sorted_bag);
   prof_begin(prof, K_SEG_SUM, st);
   if (s.D == 128 || s.D == 32) {

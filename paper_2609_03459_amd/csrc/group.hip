@@ -78,6 +78,14 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
   const int64_t NB = (int64_t)T * B;
   const int64_t o0 = (int64_t)blockIdx.x * SORT_TILE;
   const int64_t o1 = (o0 + SORT_TILE < M ? o0 + SORT_TILE : M);
+  // every index of the thread's items is loaded before any is used, and before the
+  // bag window, so the loads are in flight together
+  int64_t gv[SORT_ITEMS];
+#pragma unroll
+  for (int j = 0; j < SORT_ITEMS; ++j) {
+    const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
+    gv[j] = o < o1 ? idx[o] : 0;
+  }
   int64_t bfirst = 0, nwin = 0;
   if (offsets) {
     // bags of this tile: from the bag holding o0 to the one holding the next tile's first occurrence
@@ -90,14 +98,6 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     if (nwin <= INGEST_WIN)
       for (int k = threadIdx.x; k < nwin; k += SORT_THREADS) win[k] = offsets[bfirst + k];
     __syncthreads();
-  }
-  // every index of the thread's items is loaded before any is used, so the loads
-  // are in flight together
-  int64_t gv[SORT_ITEMS];
-#pragma unroll
-  for (int j = 0; j < SORT_ITEMS; ++j) {
-    const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
-    gv[j] = o < o1 ? idx[o] : 0;
   }
   int err = 0;
 #pragma unroll
@@ -575,6 +575,14 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
   if (tile >= (n + SCAN_TILE - 1) / SCAN_TILE) return;
   const int base = tile * SCAN_TILE;
+  // the positions of the thread's striped elements, loaded with the keys so that the
+  // inverse-map stores below wait on no load
+  uint32_t pos[SCAN_ITEMS];
+#pragma unroll
+  for (int j = 0; j < SCAN_ITEMS; ++j) {
+    const int e = j * SCAN_THREADS + (int)threadIdx.x;
+    pos[j] = base + e < n ? sp[base + e] : 0u;
+  }
 #pragma unroll 4
   for (int j = 0; j < SCAN_ITEMS; ++j) {
     const int e = j * SCAN_THREADS + (int)threadIdx.x;
@@ -610,13 +618,13 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   }
   __syncthreads();
   // all global writes in striped order (consecutive lanes, consecutive elements)
-#pragma unroll 4
+#pragma unroll
   for (int j = 0; j < SCAN_ITEMS; ++j) {
     const int e = j * SCAN_THREADS + (int)threadIdx.x;
     const int i = base + e;
     if (i >= n) continue;
     const int32_t uid = lu[pad32(e)];
-    inv[sp[i]] = uid;
+    inv[pos[j]] = uid;
     if (uid < 0) continue;
     sorted_uid[i] = uid;
     const uint32_t key = lk[pad32(e + 1)], kp = lk[pad32(e)];
