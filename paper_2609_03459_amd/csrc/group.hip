@@ -158,10 +158,15 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __r
                                                              uint32_t* __restrict__ counts, int ntiles) {
   constexpr int NB = 1 << BITS;
   __shared__ uint32_t h[4][NB];  // one histogram per wave
+  // tiles in order, an eighth per XCD: the counts of 32 neighbouring tiles share a
+  // cache line, written from one L2, and the scatter reads its tiles' keys again
+  // on the same XCD
+  const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
   const int w = threadIdx.x >> 6;
   for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&h[0][0])[k] = 0;
   __syncthreads();
-  const int base = blockIdx.x * SORT_TILE;
+  const int base = tile * SORT_TILE;
   if (base + SORT_TILE <= n) {
     // a full tile: the order of the counts does not matter, so 16-byte loads
     const uint4* k4 = reinterpret_cast<const uint4*>(keys + base) + threadIdx.x;
@@ -188,7 +193,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_hist(const uint32_t* __r
   }
   __syncthreads();
   for (int d = threadIdx.x; d < NB; d += SORT_THREADS)
-    counts[d * ntiles + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
+    counts[d * ntiles + tile] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
 }
 
 // one block per digit: exclusive offsets of every tile within that digit, and
@@ -240,11 +245,14 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
                                   // that key's position in the tile's digit order
   __shared__ uint32_t sk[SORT_TILE], sv[SORT_TILE];
   __shared__ uint32_t scan_tmp[SORT_THREADS / 64];
+  // tiles in order, an eighth per XCD (as in the histogram of the same pass)
+  const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
   const int w = threadIdx.x >> 6;
   const int lane = lane_id();
   for (int k = threadIdx.x; k < 4 * NB; k += SORT_THREADS) (&wh[0][0])[k] = 0;
   __syncthreads();
-  const int tile0 = blockIdx.x * SORT_TILE;
+  const int tile0 = tile * SORT_TILE;
   const int base = tile0 + w * (SORT_ITEMS * 64);
   const int nt = n - tile0 < SORT_TILE ? n - tile0 : SORT_TILE;  // keys in this tile
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -263,7 +271,7 @@ __global__ void __launch_bounds__(SORT_THREADS) k_radix_scatter(const uint32_t* 
 #pragma unroll
   for (int q = 0; q < DPT; ++q) {
     const int d = threadIdx.x * DPT + q;
-    toff[q] = d < NB ? offs[d * ntiles + blockIdx.x] : 0u;
+    toff[q] = d < NB ? offs[d * ntiles + tile] : 0u;
     gt[q] = d < NB ? totals[d] : 0u;
   }
 #pragma unroll
@@ -527,21 +535,41 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_reduce(const uint32_t* _
                                                                uint32_t n3, int dedup, uint64_t* __restrict__ tsum,
                                                                int32_t* __restrict__ ctr) {
   __shared__ uint64_t smem[SCAN_THREADS / 64];
-  const int base = blockIdx.x * SCAN_TILE;
-  uint64_t c = 0;
-#pragma unroll 4
-  for (int j = 0; j < SCAN_ITEMS; ++j) {
-    const int i = base + j * SCAN_THREADS + (int)threadIdx.x;
-    if (i < n) {
-      const uint32_t k = sk[i];
-      if (k < kinv) {
-        const uint32_t kp = i > 0 ? sk[i - 1] : 0u;
-        const bool head = i == 0 || kp != k || !dedup;
-        const bool pgh = head && (i == 0 || kp / n3 != k / n3);
-        c += (uint64_t)head | ((uint64_t)pgh << 32);
-        if (i == n - 1 || sk[i + 1] >= kinv) ctr[C_NVALID] = i + 1;
-      }
+  // each thread counts SCAN_ITEMS consecutive keys (16-byte loads), so a key's
+  // predecessor is in a register, and each key's prefix is divided out once
+  const int e0 = blockIdx.x * SCAN_TILE + (int)threadIdx.x * SCAN_ITEMS;
+  uint32_t k[SCAN_ITEMS];
+  if (e0 + SCAN_ITEMS <= n) {
+    const uint4* k4 = reinterpret_cast<const uint4*>(sk + e0);
+#pragma unroll
+    for (int q = 0; q < SCAN_ITEMS / 4; ++q) {
+      const uint4 v = k4[q];
+      k[4 * q] = v.x;
+      k[4 * q + 1] = v.y;
+      k[4 * q + 2] = v.z;
+      k[4 * q + 3] = v.w;
     }
+  } else {
+#pragma unroll
+    for (int q = 0; q < SCAN_ITEMS; ++q) k[q] = e0 + q < n ? sk[e0 + q] : kinv;
+  }
+  const uint32_t kprev = e0 > 0 && e0 <= n ? sk[e0 - 1] : 0u;
+  const uint32_t knext = e0 + SCAN_ITEMS < n ? sk[e0 + SCAN_ITEMS] : kinv;
+  uint64_t c = 0;
+  uint32_t pprev = kprev / n3;
+#pragma unroll
+  for (int q = 0; q < SCAN_ITEMS; ++q) {
+    const int i = e0 + q;
+    const uint32_t key = k[q], kp = q ? k[q - 1] : kprev;
+    const uint32_t pk = key / n3;
+    if (i < n && key < kinv) {
+      const bool head = i == 0 || kp != key || !dedup;
+      const bool pgh = head && (i == 0 || pprev != pk);
+      c += (uint64_t)head | ((uint64_t)pgh << 32);
+      const uint32_t kn = q + 1 < SCAN_ITEMS ? k[q + 1] : knext;
+      if (i == n - 1 || kn >= kinv) ctr[C_NVALID] = i + 1;
+    }
+    pprev = pk;
   }
   uint64_t tot;
   block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot);
@@ -828,10 +856,10 @@ static int grid_for(int64_t n, int per_block, int cap) {
 
 template <int BITS>
 static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntiles, uint32_t* tot, hipStream_t st) {
-  hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift, w.rcounts,
-                     ntiles);
+  hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift,
+                     w.rcounts, ntiles);
   hipLaunchKernelGGL(k_radix_scan, dim3(1 << BITS), dim3(256), 0, st, w.rcounts, ntiles, tot);
-  hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(ntiles), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
+  hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
                      w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles,
                      (const uint32_t*)tot);
   return hipGetLastError();
