@@ -302,6 +302,48 @@ __global__ void __launch_bounds__(64 * FIX_WAVES) k_seg_fix(const int32_t* __res
     const int n = c1 - c0;  // head partials of chunks c0+1 .. c1
     const int k_lo = c0 + 1 + (int)(((int64_t)n * w) / FIX_WAVES);
     const int k_hi = c0 + 1 + (int)(((int64_t)n * (w + 1)) / FIX_WAVES);
+    if ((D & 1) == 0 && D <= 128) {
+      // a lane owns a column pair, so one load takes a whole partial row, and eight
+      // partials are in flight per wave
+      const int jc = 2 * lane;
+      const bool ok = jc < D;
+      float2 a[8];
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk) a[kk] = make_float2(0.f, 0.f);
+      int k = k_lo;
+      for (; k + 8 <= k_hi; k += 8) {
+        float2 v[8];
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk)
+          v[kk] = ok ? *reinterpret_cast<const float2*>(part + ((int64_t)(k + kk) * 2 + 0) * D + jc) : make_float2(0.f, 0.f);
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+          a[kk].x += v[kk].x;
+          a[kk].y += v[kk].y;
+        }
+      }
+      for (; k < k_hi; ++k) {
+        const float2 v = ok ? *reinterpret_cast<const float2*>(part + ((int64_t)k * 2 + 0) * D + jc) : make_float2(0.f, 0.f);
+        a[0].x += v.x;
+        a[0].y += v.y;
+      }
+      red[w][jc & 255] = ((a[0].x + a[1].x) + (a[2].x + a[3].x)) + ((a[4].x + a[5].x) + (a[6].x + a[7].x));
+      red[w][(jc + 1) & 255] = ((a[0].y + a[1].y) + (a[2].y + a[3].y)) + ((a[4].y + a[5].y) + (a[6].y + a[7].y));
+      __syncthreads();
+      if (w == 0) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int j = 64 * q + lane;
+          if (j < D) {
+            float acc = part[((int64_t)c0 * 2 + 1) * D + j];
+            for (int v = 0; v < FIX_WAVES; ++v) acc += red[v][j];
+            dE[(int64_t)u * D + j] = acc;
+          }
+        }
+      }
+      __syncthreads();
+      continue;
+    }
     for (int j0 = 0; j0 < D; j0 += 256) {
       bool ok[4];
 #pragma unroll

@@ -73,8 +73,10 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
                                                          const int32_t* __restrict__ tile_bag, int64_t B, int T,
                                                          int64_t N, uint32_t Npad, uint32_t kinv,
                                                          uint32_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                                         int32_t* __restrict__ bag_of, int32_t* __restrict__ ctr) {
+                                                         int32_t* __restrict__ bag_of, int32_t* __restrict__ ctr,
+                                                         uint32_t* __restrict__ counts0, int nb0, int ntiles) {
   __shared__ int64_t win[INGEST_WIN];
+  __shared__ uint32_t h0[1 << RADIX_MAX_BITS];  // digit counts of the first sort pass (bits 0 .. log2 nb0)
   const int64_t NB = (int64_t)T * B;
   const int64_t o0 = (int64_t)blockIdx.x * SORT_TILE;
   const int64_t o1 = (o0 + SORT_TILE < M ? o0 + SORT_TILE : M);
@@ -86,6 +88,8 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
     gv[j] = o < o1 ? idx[o] : 0;
   }
+  if (counts0)
+    for (int d = threadIdx.x; d < nb0; d += SORT_THREADS) h0[d] = 0u;
   int64_t bfirst = 0, nwin = 0;
   if (offsets) {
     // bags of this tile: from the bag holding o0 to the one holding the next tile's first occurrence
@@ -97,8 +101,8 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     nwin = l - f + 2;  // offsets[bfirst .. l + 1]
     if (nwin <= INGEST_WIN)
       for (int k = threadIdx.x; k < nwin; k += SORT_THREADS) win[k] = offsets[bfirst + k];
-    __syncthreads();
   }
+  __syncthreads();  // the bag window and the cleared digit counts
   int err = 0;
 #pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
@@ -133,8 +137,13 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     keys[o] = key;
     vals[o] = (uint32_t)o;
     bag_of[o] = (int32_t)b;
+    if (counts0) atomicAdd(&h0[key & (uint32_t)(nb0 - 1)], 1u);
   }
   if (err) atomicOr(&ctr[C_ERR], ERR_INDEX);
+  if (counts0) {  // this tile's counts of the first pass, laid out as the histogram kernel's
+    __syncthreads();
+    for (int d = threadIdx.x; d < nb0; d += SORT_THREADS) counts0[d * ntiles + blockIdx.x] = h0[d];
+  }
 }
 
 __global__ void k_check_offsets(const int64_t* __restrict__ offsets, int64_t NB, int64_t M, int32_t* ctr) {
@@ -854,10 +863,14 @@ static int grid_for(int64_t n, int per_block, int cap) {
   return (int)g;
 }
 
+// counted: the tile counts of this pass are already in rcounts (the first pass of
+// the grouping's sort, counted by the ingest kernel)
 template <int BITS>
-static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntiles, uint32_t* tot, hipStream_t st) {
-  hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift,
-                     w.rcounts, ntiles);
+static hipError_t radix_pass(const Work& w, int cur, int n, int shift, int ntiles, uint32_t* tot, hipStream_t st,
+                             bool counted = false) {
+  if (!counted)
+    hipLaunchKernelGGL(k_radix_hist<BITS>, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, w.keys[cur], n, shift,
+                       w.rcounts, ntiles);
   hipLaunchKernelGGL(k_radix_scan, dim3(1 << BITS), dim3(256), 0, st, w.rcounts, ntiles, tot);
   hipLaunchKernelGGL(k_radix_scatter<BITS>, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, w.keys[cur], w.vals[cur],
                      w.keys[cur ^ 1], w.vals[cur ^ 1], n, shift, (const uint32_t*)w.rcounts, ntiles,
@@ -928,8 +941,11 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
   if (bags)
     hipLaunchKernelGGL(k_tile_bags, dim3((unsigned)((NB + 255) / 256)), dim3(256), 0, st, offsets, NB, M,
                        w.tile_bag, w.ctr);
+  // with more than one tile, ingest also counts the digits of the first sort pass
+  const bool count0 = ntiles > 1 && npasses > 0;
   hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, (const int32_t*)w.tile_bag,
-                     B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr);
+                     B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr, count0 ? w.rcounts : nullptr,
+                     radix, ntiles);
   prof_end(prof, K_INGEST, st);
   int cur = 0;
   if (ntiles == 1) {
@@ -950,10 +966,10 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
       const int shift = p * dbits;
       uint32_t* tot = w.rtotals + p * radix;
       switch (bits) {
-        case 8: e = radix_pass<8>(w, cur, n, shift, ntiles, tot, st); break;
-        case 9: e = radix_pass<9>(w, cur, n, shift, ntiles, tot, st); break;
-        case 10: e = radix_pass<10>(w, cur, n, shift, ntiles, tot, st); break;
-        default: e = radix_pass<11>(w, cur, n, shift, ntiles, tot, st); break;
+        case 8: e = radix_pass<8>(w, cur, n, shift, ntiles, tot, st, p == 0); break;
+        case 9: e = radix_pass<9>(w, cur, n, shift, ntiles, tot, st, p == 0); break;
+        case 10: e = radix_pass<10>(w, cur, n, shift, ntiles, tot, st, p == 0); break;
+        default: e = radix_pass<11>(w, cur, n, shift, ntiles, tot, st, p == 0); break;
       }
       if (e != hipSuccess) return e;
       cur ^= 1;
