@@ -580,6 +580,20 @@ __device__ __forceinline__ void reduce_g1(int ti1, ShapeArgs s, const uint32_t* 
       __syncthreads();
       const int wn = (int)(total - w0 < (uint32_t)G1_LIST ? total - w0 : (uint32_t)G1_LIST);
       int j = g;
+      for (; j + 56 < wn; j += 64) {  // sixteen loads in flight; the same accumulators in the same order
+        float2 v[16];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const size_t l = (size_t)list[j + 8 * q] * 64;
+          v[2 * q] = P0[l];
+          v[2 * q + 1] = P1[l];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          add(a[2 * (q & 3)], v[2 * q]);
+          add(a[2 * (q & 3) + 1], v[2 * q + 1]);
+        }
+      }
       for (; j + 24 < wn; j += 32) {
         const size_t l0 = (size_t)list[j] * 64, l1 = (size_t)list[j + 8] * 64;
         const size_t l2 = (size_t)list[j + 16] * 64, l3 = (size_t)list[j + 24] * 64;
@@ -621,10 +635,23 @@ __device__ __forceinline__ void reduce_g2(int rh, const uint32_t* __restrict__ r
                                           float lr, bool update) {
   const int run = rh >> 1, h = rh & 1;
   const int c0 = (int)run_base[run], c1 = (int)run_base[run + 1];
-  // thread k owns elements k + 512 m (m < 4): four independent loads per chunk
+  // thread k owns elements k + 512 m (m < 4); four chunks' loads are in flight
+  // together and added in chunk order
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int c = c0; c < c1; ++c) {
-    const float* src = dBpart + ((size_t)h * nch_cap + c) * 2048 + threadIdx.x;
+  const float* src = dBpart + ((size_t)h * nch_cap + c0) * 2048 + threadIdx.x;
+  int c = c0;
+  for (; c + 4 <= c1; c += 4, src += 4 * 2048) {
+    float v[4][4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) v[k][m] = src[k * 2048 + RED_THREADS * m];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) acc[m] += v[k][m];
+  }
+  for (; c < c1; ++c, src += 2048) {
 #pragma unroll
     for (int m = 0; m < 4; ++m) acc[m] += src[RED_THREADS * m];
   }
