@@ -608,7 +608,9 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   __shared__ int32_t lg[SCAN_TILE + SCAN_TILE / 32];        // (group id << 1) | group starts here; -1: invalid
   __shared__ uint64_t smem[SCAN_THREADS / 64];
   // tiles in sorted order, an eighth per XCD: a table's inverse-map entries (a
-  // contiguous range of positions) are scattered within one XCD's L2
+  // contiguous range of positions) are scattered within one XCD's L2, and the
+  // kernel's sequential reads and writes are non-temporal so that they do not push
+  // those lines out
   const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
   if (tile >= (n + SCAN_TILE - 1) / SCAN_TILE) return;
   const int base = tile * SCAN_TILE;
@@ -618,12 +620,12 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
 #pragma unroll
   for (int j = 0; j < SCAN_ITEMS; ++j) {
     const int e = j * SCAN_THREADS + (int)threadIdx.x;
-    pos[j] = base + e < n ? sp[base + e] : 0u;
+    pos[j] = base + e < n ? __builtin_nontemporal_load(sp + base + e) : 0u;
   }
 #pragma unroll 4
   for (int j = 0; j < SCAN_ITEMS; ++j) {
     const int e = j * SCAN_THREADS + (int)threadIdx.x;
-    lk[pad32(e + 1)] = base + e < n ? sk[base + e] : kinv;
+    lk[pad32(e + 1)] = base + e < n ? __builtin_nontemporal_load(sk + base + e) : kinv;
   }
   if (threadIdx.x == 0) lk[0] = base > 0 ? sk[base - 1] : 0u;
   __syncthreads();
@@ -663,12 +665,12 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
     const int32_t uid = lu[pad32(e)];
     inv[pos[j]] = uid;
     if (uid < 0) continue;
-    sorted_uid[i] = uid;
+    __builtin_nontemporal_store(uid, sorted_uid + i);
     const uint32_t key = lk[pad32(e + 1)], kp = lk[pad32(e)];
     if (i == 0 || kp != key || !dedup) {
-      uniq_key[uid] = key;
-      uniq_i3[uid] = (int)((key % Npad) % n3);
-      occ_start[uid] = i;
+      __builtin_nontemporal_store(key, uniq_key + uid);
+      __builtin_nontemporal_store((int)((key % Npad) % n3), uniq_i3 + uid);
+      __builtin_nontemporal_store(i, occ_start + uid);
     }
     const int32_t gv = lg[pad32(e)];
     const int32_t pg = gv >> 1;
