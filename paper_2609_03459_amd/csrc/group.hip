@@ -78,7 +78,11 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
   __shared__ int64_t win[INGEST_WIN];
   __shared__ uint32_t h0[1 << RADIX_MAX_BITS];  // digit counts of the first sort pass (bits 0 .. log2 nb0)
   const int64_t NB = (int64_t)T * B;
-  const int64_t o0 = (int64_t)blockIdx.x * SORT_TILE;
+  // tiles in order, an eighth per XCD, as the sort's first pass takes them: that pass
+  // reads a tile's keys and positions on the XCD that wrote them
+  const int tile = (int)xcd_block(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
+  const int64_t o0 = (int64_t)tile * SORT_TILE;
   const int64_t o1 = (o0 + SORT_TILE < M ? o0 + SORT_TILE : M);
   // every index of the thread's items is loaded before any is used, and before the
   // bag window, so the loads are in flight together
@@ -86,15 +90,15 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
 #pragma unroll
   for (int j = 0; j < SORT_ITEMS; ++j) {
     const int64_t o = o0 + (int64_t)j * SORT_THREADS + threadIdx.x;
-    gv[j] = o < o1 ? idx[o] : 0;
+    gv[j] = o < o1 ? __builtin_nontemporal_load(idx + o) : 0;
   }
   if (counts0)
     for (int d = threadIdx.x; d < nb0; d += SORT_THREADS) h0[d] = 0u;
   int64_t bfirst = 0, nwin = 0;
   if (offsets) {
     // bags of this tile: from the bag holding o0 to the one holding the next tile's first occurrence
-    int64_t f = tile_bag[blockIdx.x];
-    int64_t l = o1 < M ? (int64_t)tile_bag[blockIdx.x + 1] : NB - 1;
+    int64_t f = tile_bag[tile];
+    int64_t l = o1 < M ? (int64_t)tile_bag[tile + 1] : NB - 1;
     f = f < 0 ? 0 : (f > NB - 1 ? NB - 1 : f);
     l = l < f ? f : (l > NB - 1 ? NB - 1 : l);
     bfirst = f;
@@ -136,13 +140,13 @@ __global__ void __launch_bounds__(SORT_THREADS) k_ingest(const int64_t* __restri
     }
     keys[o] = key;
     vals[o] = (uint32_t)o;
-    bag_of[o] = (int32_t)b;
+    __builtin_nontemporal_store((int32_t)b, bag_of + o);
     if (counts0) atomicAdd(&h0[key & (uint32_t)(nb0 - 1)], 1u);
   }
   if (err) atomicOr(&ctr[C_ERR], ERR_INDEX);
   if (counts0) {  // this tile's counts of the first pass, laid out as the histogram kernel's
     __syncthreads();
-    for (int d = threadIdx.x; d < nb0; d += SORT_THREADS) counts0[d * ntiles + blockIdx.x] = h0[d];
+    for (int d = threadIdx.x; d < nb0; d += SORT_THREADS) counts0[d * ntiles + tile] = h0[d];
   }
 }
 
@@ -945,7 +949,7 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
                        w.tile_bag, w.ctr);
   // with more than one tile, ingest also counts the digits of the first sort pass
   const bool count0 = ntiles > 1 && npasses > 0;
-  hipLaunchKernelGGL(k_ingest, dim3(ntiles), dim3(SORT_THREADS), 0, st, idx, M, offsets, (const int32_t*)w.tile_bag,
+  hipLaunchKernelGGL(k_ingest, dim3(xcd_grid(ntiles)), dim3(SORT_THREADS), 0, st, idx, M, offsets, (const int32_t*)w.tile_bag,
                      B, s.T, s.N, s.Npad, s.kinv, w.keys[0], w.vals[0], w.bag_of, w.ctr, count0 ? w.rcounts : nullptr,
                      radix, ntiles);
   prof_end(prof, K_INGEST, st);
