@@ -42,6 +42,9 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
   float* scr = scr_all + wave * B64_SCR;
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
+  // per-row dD partials (2 KB per unique row) beyond the last-level cache: stored
+  // non-temporally
+  const bool dd_nt = (uint64_t)(uint32_t)ctr[C_U] * 2048u > STREAM_BYTES;
   // byte offsets of this lane's operand words:
   //   stage 1 B[a = 16 l4 + k][16 nt + l15] in G2[t][i2] (+ 1,024 bytes per k, + 64 per nt)
   const uint32_t vo_b = 4u * (uint32_t)(l4 * 4096 + l15);
@@ -154,7 +157,10 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
 #pragma unroll
             for (int s4 = 0; s4 < 4; ++s4) dd = __builtin_amdgcn_mfma_f32_16x16x4f32(e_b[s4], CB[4 * nt + s4], dd, 0, 0, 0);
             // lane holds dD[row l4 >> 1][b = 16 nt + l15][j3 = 4 (l4 & 1) + r]
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, dd), db, vo_dd + 512u * nt, 0, 0);
+            if (dd_nt)
+              __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, dd), db, vo_dd + 512u * nt, 0, CPOL_NT);
+            else
+              __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, dd), db, vo_dd + 512u * nt, 0, 0);
             dC[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(e4.x, d4[nt].x, dC[nt], 0, 0, 0);
             dC[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(e4.y, d4[nt].y, dC[nt], 0, 0, 0);
             dC[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(e4.z, d4[nt].z, dC[nt], 0, 0, 0);
@@ -164,13 +170,14 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
         // lane holds dC[jj = 4 l4 + r][b = 16 nt + l15]: rows of slice j, in place of C_j,
         // and the slice's partial [j1][(j2, b)] = [jj][b]
         wave_lds_sync();
+        // the slice's partial, read once by the dG2 product: stored non-temporally
         float* dcs = dCpart + (size_t)(f + qd + j) * 1024 + 4 * l4 * 64 + l15;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             scr[j * B64_SLICE + (4 * l4 + r) * B64_PITCH + 16 * nt + l15] = dC[nt][r];
-            dcs[r * 64 + 16 * nt] = dC[nt][r];
+            __builtin_nontemporal_store(dC[nt][r], dcs + r * 64 + 16 * nt);
           }
       }
       wave_lds_sync();

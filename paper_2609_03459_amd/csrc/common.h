@@ -268,6 +268,14 @@ namespace ttemb {
 // claims before it exits.  The forward uses one queue per XCD (workgroup
 // blockIdx % 8 runs on XCD blockIdx % 8); the specialised backward gives every
 // (table, rank half) owner one queue, since its LDS accumulator is its own.
+// An array that one kernel writes and a later kernel gathers (embedding rows, the
+// backward's partials) is stored non-temporally when it is larger than the chip's
+// 256 MB last-level cache (MALL): it cannot stay there for its reader, and ordinary
+// stores would push out lines the writer itself still reads.  Smaller arrays are
+// stored normally, so that their reader finds them in that cache.
+constexpr uint64_t STREAM_BYTES = 256ull << 20;
+constexpr int CPOL_NT = 2;  // buffer-store cache policy: non-temporal
+
 constexpr int SCHED_NQ = 8;       // queues of the forward scheduler: one per XCD
 constexpr int SCHED_STRIDE = 32;  // ints between queue counters (128 bytes)
 

@@ -185,6 +185,8 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
   constexpr int GR = 16 / D3;              // rows per stage-2 group ("pair" below)
   constexpr int DW = 16 * D3;              // floats per E row
   constexpr uint32_t G3ROW = 128u * D3;    // bytes per G3 row (R d3 floats)
+  // E rows of all unique rows beyond the last-level cache: stored non-temporally
+  const bool e_nt = (uint64_t)(uint32_t)ctr[C_U] * (4u * DW) > STREAM_BYTES;
   const int nch = (int)run_base[s.T * s.n2];
   const int l15 = lane & 15, l4 = lane >> 4;
   // stage-2 A operand: lane m = l15 = (row asel of the group, j3), K index b = 4 s + l4
@@ -444,13 +446,22 @@ __global__ void __launch_bounds__(64 * F32_WAVES, F32_WG_PER_CU)
       const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * DW, (uint32_t)X.cnt * (4u * DW));
       if (D3 == 8) {
         // lane holds E[row l4 / 2][jj = l15][j3 = 4 (l4 & 1) + r]
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
+        if (e_nt)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, CPOL_NT);
+        else
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
       } else {
         // lane holds E[row 2 l4 + (r / 2)][jj = l15][j3 = r % 2]
         typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(acc[0]), __float_as_uint(acc[1])}, eb, vo_e, 0, 0);
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(acc[2]), __float_as_uint(acc[3])}, eb,
-                                              vo_e + 4u * DW, 0, 0);
+        const u32x2 e01 = u32x2{__float_as_uint(acc[0]), __float_as_uint(acc[1])};
+        const u32x2 e23 = u32x2{__float_as_uint(acc[2]), __float_as_uint(acc[3])};
+        if (e_nt) {
+          __builtin_amdgcn_raw_buffer_store_b64(e01, eb, vo_e, 0, CPOL_NT);
+          __builtin_amdgcn_raw_buffer_store_b64(e23, eb, vo_e + 4u * DW, 0, CPOL_NT);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b64(e01, eb, vo_e, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(e23, eb, vo_e + 4u * DW, 0, 0);
+        }
       }
     };
     int cj = 0;
@@ -523,6 +534,8 @@ __global__ void __launch_bounds__(64 * F64_WAVES, F64_WG_PER_CU)
               const int32_t* __restrict__ uniq_i3, int32_t* __restrict__ ctr, float* __restrict__ E) {
   __shared__ float scr_all[F64_WAVES * F64_SCR];
   const int lane = lane_id();
+  // E rows of all unique rows beyond the last-level cache: stored non-temporally
+  const bool e_nt = (uint64_t)(uint32_t)ctr[C_U] * 512u > STREAM_BYTES;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   float* scr = scr_all + wave * F64_SCR;
   const int nch = (int)run_base[s.T * s.n2];
@@ -702,7 +715,10 @@ __global__ void __launch_bounds__(64 * F64_WAVES, F64_WG_PER_CU)
 #pragma unroll
       for (int k = 0; k < 16; ++k) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(X.d[k], CT[k], acc, 0, 0, 0);
       const buf_t eb = make_buf(E + (size_t)(uint32_t)X.ra * 128, X.has1 ? 1024u : 512u);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
+      if (e_nt)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, CPOL_NT);
+      else
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), eb, vo_e, 0, 0);
     };
     int cj = 0;
     auto step = [&](const FPair& X) {
