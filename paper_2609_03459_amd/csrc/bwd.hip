@@ -181,8 +181,18 @@ __device__ __forceinline__ void seg_rows(const float* __restrict__ dV, const int
   const SegEnds ends = seg_ends(sorted_uid, occ_start, i0, i0 + SEG_CHUNK < nvalid ? i0 + SEG_CHUNK : nvalid, nvalid);
   const int ib = ends.ib, ie = ends.ie;
   if (ib >= ie) return;
+  // dE of all unique rows beyond the last-level cache: stored non-temporally.  The row
+  // goes through a descriptor of its 4 D bytes (lanes past LN fall outside it), so the
+  // two cache policies stay two distinct stores
+  const bool de_nt = (uint64_t)(uint32_t)ctr[C_U] * (4u * D) > STREAM_BYTES;
   auto flush = [&](int u, float2 acc) {
-    if (lane < LN) reinterpret_cast<float2*>(seg_dst(ends, u, c, D, dE, part))[lane] = acc;
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const buf_t row = make_buf(seg_dst(ends, u, c, D, dE, part), 4u * D);
+    const u32x2 v = u32x2{__float_as_uint(acc.x), __float_as_uint(acc.y)};
+    if (de_nt)
+      __builtin_amdgcn_raw_buffer_store_b64(v, row, 8u * (uint32_t)lane, 0, CPOL_NT);
+    else
+      __builtin_amdgcn_raw_buffer_store_b64(v, row, 8u * (uint32_t)lane, 0, 0);
   };
   int cur = sorted_uid[ib];
   float2 acc = make_float2(0.f, 0.f);

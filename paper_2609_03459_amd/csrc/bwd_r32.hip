@@ -497,26 +497,29 @@ __global__ void __launch_bounds__(64 * BW_WAVES, 1)
           dA1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, BTop[16 + 4 * q + c4], dA1, 0, 0, 0);
         }
       }
-      // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]
+      // lane holds dA_h[slice l4][j1 r][a = 16 nt2 + l15]; the partial is read once, by the
+      // dG1 sum: stored non-temporally
       if (l4 < nqs) {
         float* dst = dApart + ((size_t)h * nsl_cap + (sb + l4)) * 128 + l15;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          dst[r * 32] = dA0[r];
-          dst[r * 32 + 16] = dA1[r];
+          __builtin_nontemporal_store(dA0[r], dst + r * 32);
+          __builtin_nontemporal_store(dA1[r], dst + r * 32 + 16);
         }
       }
     }
     wave_lds_sync();
     if (chunk_end) {
-      // dB_h partial of the finished chunk, lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)]
+      // dB_h partial of the finished chunk, lane holds dB_h[a = 16 mt + 4 l4 + r][(j2 = nt, b' = l15)];
+      // read once, by the dG2 sum: stored non-temporally
       float* dst = dBpart + ((size_t)h * nch_cap + (c_lo + c_done)) * 2048;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15] = dB[4 * mt + nt][r];
+          for (int r = 0; r < 4; ++r)
+            __builtin_nontemporal_store(dB[4 * mt + nt][r], dst + (16 * mt + 4 * l4 + r) * 64 + 16 * nt + l15);
 #pragma unroll
       for (int k = 0; k < 8; ++k) dB[k] = f32x4{0.f, 0.f, 0.f, 0.f};
     }

@@ -215,13 +215,14 @@ __global__ void __launch_bounds__(64 * B64_WAVES, B64_WG_PER_CU)
             for (int k = 0; k < 16; ++k) acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[k], bv[k], acc[nt], 0, 0, 0);
           }
         }
-        // lane holds dA[slice l4][j1 r][a = 16 nt + l15]
+        // lane holds dA[slice l4][j1 r][a = 16 nt + l15]; read once, by the dG1 sum: stored
+        // non-temporally
         if (l4 < nqs) {
           float* dst = dApart + (size_t)(f + qd + l4) * 256 + l15;
 #pragma unroll
           for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dst[r * 64 + 16 * nt] = acc[nt][r];
+            for (int r = 0; r < 4; ++r) __builtin_nontemporal_store(acc[nt][r], dst + r * 64 + 16 * nt);
         }
       }
       wave_lds_sync();
