@@ -672,11 +672,11 @@ __global__ void __launch_bounds__(GRED_THREADS) k_gred_g1(ShapeArgs s, const uin
         for (; j + 8 <= wn; j += 8) {
           float v[8];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] = dApart[(int64_t)list[j + q] * d1R + e];
+          for (int q = 0; q < 8; ++q) v[q] = ntl(dApart + (int64_t)list[j + q] * d1R + e);
 #pragma unroll
           for (int q = 0; q < 8; ++q) a[q] += v[q];
         }
-        for (; j < wn; ++j) a[0] += dApart[(int64_t)list[j] * d1R + e];
+        for (; j < wn; ++j) a[0] += ntl(dApart + (int64_t)list[j] * d1R + e);
       }
       __syncthreads();  // the list is refilled
     }
@@ -747,11 +747,11 @@ __global__ void __launch_bounds__(GRED_THREADS) k_gred_g3(const int32_t* __restr
   for (; k + 8 <= k1; k += 8) {
     float v[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = dDpart[(int64_t)rows[k + q] * RD + e];
+    for (int q = 0; q < 8; ++q) v[q] = ntl(dDpart + (int64_t)rows[k + q] * RD + e);
 #pragma unroll
     for (int q = 0; q < 8; ++q) a[q] += v[q];
   }
-  for (; k < k1; ++k) a[0] += dDpart[(int64_t)rows[k] * RD + e];
+  for (; k < k1; ++k) a[0] += ntl(dDpart + (int64_t)rows[k] * RD + e);
   put_g(dG3, (int64_t)b * RD + e, sum8(a), lr, update);
 }
 

@@ -588,8 +588,8 @@ __device__ __forceinline__ void reduce_g1(int ti1, ShapeArgs s, const uint32_t* 
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           const size_t l = (size_t)list[j + 8 * q] * 64;
-          v[2 * q] = P0[l];
-          v[2 * q + 1] = P1[l];
+          v[2 * q] = ntl2(P0 + l);
+          v[2 * q + 1] = ntl2(P1 + l);
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -600,19 +600,19 @@ __device__ __forceinline__ void reduce_g1(int ti1, ShapeArgs s, const uint32_t* 
       for (; j + 24 < wn; j += 32) {
         const size_t l0 = (size_t)list[j] * 64, l1 = (size_t)list[j + 8] * 64;
         const size_t l2 = (size_t)list[j + 16] * 64, l3 = (size_t)list[j + 24] * 64;
-        add(a[0], P0[l0]);
-        add(a[1], P1[l0]);
-        add(a[2], P0[l1]);
-        add(a[3], P1[l1]);
-        add(a[4], P0[l2]);
-        add(a[5], P1[l2]);
-        add(a[6], P0[l3]);
-        add(a[7], P1[l3]);
+        add(a[0], ntl2(P0 + l0));
+        add(a[1], ntl2(P1 + l0));
+        add(a[2], ntl2(P0 + l1));
+        add(a[3], ntl2(P1 + l1));
+        add(a[4], ntl2(P0 + l2));
+        add(a[5], ntl2(P1 + l2));
+        add(a[6], ntl2(P0 + l3));
+        add(a[7], ntl2(P1 + l3));
       }
       for (; j < wn; j += 8) {
         const size_t l0 = (size_t)list[j] * 64;
-        add(a[0], P0[l0]);
-        add(a[1], P1[l0]);
+        add(a[0], ntl2(P0 + l0));
+        add(a[1], ntl2(P1 + l0));
       }
       __syncthreads();
     }
@@ -648,7 +648,7 @@ __device__ __forceinline__ void reduce_g2(int rh, const uint32_t* __restrict__ r
 #pragma unroll
     for (int k = 0; k < 4; ++k)
 #pragma unroll
-      for (int m = 0; m < 4; ++m) v[k][m] = src[k * 2048 + RED_THREADS * m];
+      for (int m = 0; m < 4; ++m) v[k][m] = ntl(src + k * 2048 + RED_THREADS * m);
 #pragma unroll
     for (int k = 0; k < 4; ++k)
 #pragma unroll
@@ -656,7 +656,7 @@ __device__ __forceinline__ void reduce_g2(int rh, const uint32_t* __restrict__ r
   }
   for (; c < c1; ++c, src += 2048) {
 #pragma unroll
-    for (int m = 0; m < 4; ++m) acc[m] += src[RED_THREADS * m];
+    for (int m = 0; m < 4; ++m) acc[m] += ntl(src + RED_THREADS * m);
   }
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
@@ -680,12 +680,12 @@ __device__ __forceinline__ void reduce_g3(int q, int xb, ShapeArgs s, const floa
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
   int w = q;
   for (; w + 3 * nq < nwg; w += 4 * nq) {
-    a0 += g3part[(int64_t)w * acc_n + e];
-    a1 += g3part[(int64_t)(w + nq) * acc_n + e];
-    a2 += g3part[(int64_t)(w + 2 * nq) * acc_n + e];
-    a3 += g3part[(int64_t)(w + 3 * nq) * acc_n + e];
+    a0 += ntl(g3part + (int64_t)w * acc_n + e);
+    a1 += ntl(g3part + (int64_t)(w + nq) * acc_n + e);
+    a2 += ntl(g3part + (int64_t)(w + 2 * nq) * acc_n + e);
+    a3 += ntl(g3part + (int64_t)(w + 3 * nq) * acc_n + e);
   }
-  for (; w < nwg; w += nq) a0 += g3part[(int64_t)w * acc_n + e];
+  for (; w < nwg; w += nq) a0 += ntl(g3part + (int64_t)w * acc_n + e);
   const float acc = (a0 + a1) + (a2 + a3);
   const int i3 = e / (16 * D3), j3 = (e >> 4) % D3, bp = g3_unslot(j3, e & 15);
   put_grad(dG3, (((int64_t)t * s.n3 + i3) * 32 + 16 * h + bp) * D3 + j3, acc, lr, update);

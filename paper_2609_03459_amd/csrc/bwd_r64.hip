@@ -298,7 +298,7 @@ __global__ void __launch_bounds__(64 * DG2_WAVES, 8) k_dg2_r64(ShapeArgs s, cons
 #pragma unroll
       for (int m = 0; m < 4; ++m) a[m] = Ar[16 * m];
 #pragma unroll
-      for (int q = 0; q < 2; ++q) b[q] = Cr[16 * q];
+      for (int q = 0; q < 2; ++q) b[q] = ntl(Cr + 16 * q);
 #pragma unroll
       for (int m = 0; m < 4; ++m)
 #pragma unroll

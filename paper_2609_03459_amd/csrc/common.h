@@ -275,6 +275,13 @@ namespace ttemb {
 // stored normally, so that their reader finds them in that cache.
 constexpr uint64_t STREAM_BYTES = 256ull << 20;
 constexpr int CPOL_NT = 2;  // buffer-store cache policy: non-temporal
+// Non-temporal loads, for partial results that a reduction reads exactly once
+__device__ __forceinline__ float ntl(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ float2 ntl2(const float2* p) {
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const f32x2v v = __builtin_nontemporal_load(reinterpret_cast<const f32x2v*>(p));
+  return make_float2(v.x, v.y);
+}
 
 constexpr int SCHED_NQ = 8;       // queues of the forward scheduler: one per XCD
 constexpr int SCHED_STRIDE = 32;  // ints between queue counters (128 bytes)
