@@ -474,23 +474,21 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_reduce(const T* __restric
   if (threadIdx.x == 0) tsum[blockIdx.x] = tot;
 }
 
+// The sum of v[0 .. count - 1] over the block (every thread gets it): a down-sweep
+// block forms its tile's offset from the raw tile totals itself, so no launch scans
+// the totals in between (integer sums: the order does not change them).
 template <typename T>
-__global__ void __launch_bounds__(SCAN_THREADS) k_scan_top(T* __restrict__ tsum, int ntiles, int32_t* total_out) {
-  __shared__ T smem[SCAN_THREADS / 64];
-  T running = 0;
-  for (int start = 0; start < ntiles; start += SCAN_THREADS) {
-    int i = start + threadIdx.x;
-    T v = i < ntiles ? tsum[i] : (T)0;
-    T tot;
-    T ex = block_excl_scan<T, SCAN_THREADS>(v, smem, &tot);
-    if (i < ntiles) tsum[i] = running + ex;
-    running += tot;
-  }
-  if (total_out && threadIdx.x == 0) *total_out = (int32_t)running;
+__device__ __forceinline__ T block_sum_first(const T* __restrict__ v, int count, T* smem) {
+  T s = 0;
+  for (int i = threadIdx.x; i < count; i += SCAN_THREADS) s += v[i];
+  T tot;
+  block_excl_scan<T, SCAN_THREADS>(s, smem, &tot);
+  return tot;
 }
 
-// each thread scans SCAN_ITEMS consecutive elements; tile offsets from tsum, or
-// with tsum NULL a single tile that also writes the total to total_out
+// each thread scans SCAN_ITEMS consecutive elements; the tile's offset is the sum of
+// the tile totals in tsum before it (tsum NULL: a single tile); the last tile writes
+// the total to total_out
 template <typename T, bool INCLUSIVE>
 __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(const T* __restrict__ in, T* __restrict__ out, int64_t n,
                                                             const T* __restrict__ tsum, int32_t* total_out) {
@@ -504,9 +502,10 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_scan_down(const T* __restrict_
     v[k] = i < n ? in[i] : (T)0;
     s += v[k];
   }
+  const T before = tsum ? block_sum_first<T>(tsum, (int)blockIdx.x, smem) : (T)0;
   T tot;
-  T acc = block_excl_scan<T, SCAN_THREADS>(s, smem, &tot) + (tsum ? tsum[blockIdx.x] : (T)0);
-  if (!tsum && total_out && threadIdx.x == 0) *total_out = (int32_t)tot;
+  T acc = block_excl_scan<T, SCAN_THREADS>(s, smem, &tot) + before;
+  if (total_out && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *total_out = (int32_t)(before + tot);
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     int64_t i = base + k;
@@ -526,9 +525,8 @@ static hipError_t scan_generic(const T* in, T* out, int64_t n, T* tsum, int32_t*
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_scan_reduce<T>, dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, n, tsum);
-  hipLaunchKernelGGL(k_scan_top<T>, dim3(1), dim3(SCAN_THREADS), 0, st, tsum, ntiles, total_out);
   hipLaunchKernelGGL((k_scan_down<T, INCLUSIVE>), dim3(ntiles), dim3(SCAN_THREADS), 0, st, in, out, n,
-                     (const T*)tsum, (int32_t*)nullptr);
+                     (const T*)tsum, total_out);
   return hipGetLastError();
 }
 
@@ -649,7 +647,8 @@ __global__ void __launch_bounds__(SCAN_THREADS) k_group_down(const uint32_t* __r
   }
   uint64_t tot;
   const uint64_t c = (uint64_t)__popc(hb) | ((uint64_t)__popc(pb) << 32);
-  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + (tsum ? tsum[tile] : 0ull);
+  const uint64_t before = tsum ? block_sum_first<uint64_t>(tsum, tile, smem) : 0ull;
+  uint64_t acc = block_excl_scan<uint64_t, SCAN_THREADS>(c, smem, &tot) + before;
 #pragma unroll
   for (int k = 0; k < SCAN_ITEMS; ++k) {
     const int i = base + e0 + k;
@@ -988,7 +987,6 @@ hipError_t launch_group(const Shape& s, const Work& w, const int64_t* idx, int64
     if (gt > 1) {  // a single tile starts at row 0 and group 0: no tile offsets needed
       hipLaunchKernelGGL(k_group_reduce, dim3(gt), dim3(SCAN_THREADS), 0, st, sk, n, s.kinv, (uint32_t)s.n3, s.dedup,
                          w.tsum64, w.ctr);
-      hipLaunchKernelGGL(k_scan_top<uint64_t>, dim3(1), dim3(SCAN_THREADS), 0, st, w.tsum64, gt, nullptr);
     }
     hipLaunchKernelGGL(k_group_down, dim3(xcd_grid(gt)), dim3(SCAN_THREADS), 0, st, sk, sp, n, s.kinv, (uint32_t)s.n3, s.Npad,
                        s.dedup, gt > 1 ? (const uint64_t*)w.tsum64 : nullptr, w.inv, w.sorted_uid, w.uniq_key,
