@@ -258,6 +258,22 @@ __device__ __forceinline__ T block_excl_scan(T v, T* smem, T* total) {
 
 namespace ttemb {
 
+// Cache policy of arrays that one kernel writes and a later kernel reads.  Partial
+// results that a reduction reads exactly once are loaded non-temporally there, and
+// the backward's dA, dB and dC partials are also stored non-temporally.  Embedding rows,
+// dE and the per-row dD partials are stored non-temporally when the array is larger
+// than the chip's 256 MB last-level cache (MALL): it cannot stay there for its reader,
+// and ordinary stores would push out lines the writer itself still reads; smaller
+// ones are stored normally, so that their reader finds them in that cache.
+constexpr uint64_t STREAM_BYTES = 256ull << 20;
+constexpr int CPOL_NT = 2;  // buffer-store cache policy: non-temporal
+__device__ __forceinline__ float ntl(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ float2 ntl2(const float2* p) {
+  typedef float f32x2v __attribute__((ext_vector_type(2)));
+  const f32x2v v = __builtin_nontemporal_load(reinterpret_cast<const f32x2v*>(p));
+  return make_float2(v.x, v.y);
+}
+
 // Persistent-thread scheduler with chunked work stealing (FlowTT Section 3.4).
 // The chunk list is cut into nq contiguous queues; queue v holds chunks
 // [share_lo(v), share_lo(v + 1)) and has one claim counter on a 128-byte line
@@ -268,21 +284,6 @@ namespace ttemb {
 // claims before it exits.  The forward uses one queue per XCD (workgroup
 // blockIdx % 8 runs on XCD blockIdx % 8); the specialised backward gives every
 // (table, rank half) owner one queue, since its LDS accumulator is its own.
-// An array that one kernel writes and a later kernel gathers (embedding rows, the
-// backward's partials) is stored non-temporally when it is larger than the chip's
-// 256 MB last-level cache (MALL): it cannot stay there for its reader, and ordinary
-// stores would push out lines the writer itself still reads.  Smaller arrays are
-// stored normally, so that their reader finds them in that cache.
-constexpr uint64_t STREAM_BYTES = 256ull << 20;
-constexpr int CPOL_NT = 2;  // buffer-store cache policy: non-temporal
-// Non-temporal loads, for partial results that a reduction reads exactly once
-__device__ __forceinline__ float ntl(const float* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ float2 ntl2(const float2* p) {
-  typedef float f32x2v __attribute__((ext_vector_type(2)));
-  const f32x2v v = __builtin_nontemporal_load(reinterpret_cast<const f32x2v*>(p));
-  return make_float2(v.x, v.y);
-}
-
 constexpr int SCHED_NQ = 8;       // queues of the forward scheduler: one per XCD
 constexpr int SCHED_STRIDE = 32;  // ints between queue counters (128 bytes)
 
